@@ -1,0 +1,518 @@
+/*
+ * rgnn_oracle.c -- plain, slow, fp64 CPU reference of the RGCN, RGAT and HGT
+ * layers and of the RGAT backward pass.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header or helper with the GPU library.
+ *
+ * Every function evaluates the defining equations edge by edge, in fp64, from
+ * the same float32 inputs the GPU path reads:
+ *   - no compact materialization, no linear-operator reordering, no fusion;
+ *   - per-edge terms (h_u W_r, h_v W_r, HGT keys/values) are recomputed for
+ *     every edge; node-level linears that the definitions state per node
+ *     (RGCN self-loop, HGT query and output linears) are computed per node;
+ *   - each destination is handled in passes: logits, softmax, aggregation.
+ *
+ * Conventions (row vectors, y = x W, as in the paper's RGCN equation and its
+ * typed-linear formula Y[i,0,j] = sum_k X[i,0,k] W[T[i],k,j]):
+ *   h      [N, d_in]              node features
+ *   W      [R, d_in, d_out]       one weight per relation
+ *   W0     [d_in, d_out]          virtual self-loop weight (may be NULL)
+ *   w_src, w_dst [R, d_out]       RGAT attention vectors
+ *   outputs are fp64, row-major.
+ *
+ * OpenMP parallelises over destinations only; each destination's sums are
+ * taken in edge-id order, so results do not depend on the thread count.
+ *
+ * Return value: 0 on success, -1 on invalid arguments, -3 on allocation failure.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* In-edges of every destination, listed in increasing edge id. */
+typedef struct {
+    int64_t *ptr;   /* [N+1] */
+    int64_t *eid;   /* [E]   */
+} in_lists;
+
+static int build_in_lists(int64_t N, int64_t E, const int32_t *dst, in_lists *a)
+{
+    a->ptr = (int64_t *)calloc((size_t)N + 1, sizeof(int64_t));
+    a->eid = (int64_t *)malloc((size_t)(E > 0 ? E : 1) * sizeof(int64_t));
+    if (!a->ptr || !a->eid) return -3;
+    for (int64_t e = 0; e < E; ++e) a->ptr[dst[e] + 1]++;
+    for (int64_t v = 0; v < N; ++v) a->ptr[v + 1] += a->ptr[v];
+    int64_t *fill = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    if (!fill) return -3;
+    memcpy(fill, a->ptr, (size_t)N * sizeof(int64_t));
+    for (int64_t e = 0; e < E; ++e) a->eid[fill[dst[e]]++] = e;
+    free(fill);
+    return 0;
+}
+
+static void free_in_lists(in_lists *a) { free(a->ptr); free(a->eid); }
+
+static int check_coo(int64_t N, int64_t E, int32_t R, const int32_t *src,
+                     const int32_t *dst, const int32_t *rel)
+{
+    if (N < 0 || E < 0 || R <= 0) return -1;
+    for (int64_t e = 0; e < E; ++e) {
+        if (src[e] < 0 || src[e] >= N || dst[e] < 0 || dst[e] >= N) return -1;
+        if (rel[e] < 0 || rel[e] >= R) return -1;
+    }
+    return 0;
+}
+
+/* y[0:n] = x[0:k] M, M row-major [k, ldm] starting at column c0 (fp32 M). */
+static void vecmat(const double *x, const float *M, int k, int ldm, int c0, int n, double *y)
+{
+    for (int j = 0; j < n; ++j) y[j] = 0.0;
+    for (int i = 0; i < k; ++i) {
+        const double xi = x[i];
+        const float *row = M + (size_t)i * ldm + c0;
+        for (int j = 0; j < n; ++j) y[j] += xi * (double)row[j];
+    }
+}
+
+static void load_row(const float *h, int64_t n, int d, double *x)
+{
+    const float *p = h + (size_t)n * d;
+    for (int i = 0; i < d; ++i) x[i] = (double)p[i];
+}
+
+/* Rows to produce: sel[0:nsel], or every node when sel is NULL. */
+static inline int64_t sel_node(const int32_t *sel, int64_t i) { return sel ? sel[i] : i; }
+
+/* ------------------------------------------------------------------------ */
+/* RGCN (the paper's RGCN equation):
+ *   out_v = act( h_v W0 + sum_r sum_{u in N_v^r} h_u W_r / c_{v,r} )
+ * with c_{v,r} the number of in-edges of v with relation r (duplicates counted)
+ * and the self-loop term present only when W0 is given.  act = ReLU if relu. */
+int oracle_rgcn_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
+                        const int32_t *src, const int32_t *dst, const int32_t *rel,
+                        const float *h, const float *W, const float *W0, int32_t relu,
+                        int64_t nsel, const int32_t *sel, double *out)
+{
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0) return -1;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    const int64_t nrows = sel ? nsel : N;
+    int err = 0;
+#pragma omp parallel reduction(| : err)
+    {
+        int64_t *cnt = (int64_t *)malloc((size_t)R * sizeof(int64_t));
+        double *x = (double *)malloc((size_t)d_in * sizeof(double));
+        double *m = (double *)malloc((size_t)d_out * sizeof(double));
+        if (!cnt || !x || !m) err = 1;
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t i = 0; i < nrows; ++i) {
+            if (err) continue;
+            const int64_t v = sel_node(sel, i);
+            double *o = out + (size_t)i * d_out;
+            for (int j = 0; j < d_out; ++j) o[j] = 0.0;
+            if (W0) {
+                load_row(h, v, d_in, x);
+                vecmat(x, W0, d_in, d_out, 0, d_out, m);
+                for (int j = 0; j < d_out; ++j) o[j] += m[j];
+            }
+            for (int r = 0; r < R; ++r) cnt[r] = 0;
+            for (int64_t p = a.ptr[v]; p < a.ptr[v + 1]; ++p) cnt[rel[a.eid[p]]]++;
+            for (int64_t p = a.ptr[v]; p < a.ptr[v + 1]; ++p) {
+                const int64_t e = a.eid[p];
+                const int r = rel[e];
+                load_row(h, src[e], d_in, x);
+                vecmat(x, W + (size_t)r * d_in * d_out, d_in, d_out, 0, d_out, m);
+                const double inv_c = 1.0 / (double)cnt[r];
+                for (int j = 0; j < d_out; ++j) o[j] += m[j] * inv_c;
+            }
+            if (relu)
+                for (int j = 0; j < d_out; ++j) o[j] = o[j] > 0.0 ? o[j] : 0.0;
+        }
+        free(cnt); free(x); free(m);
+    }
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* RGAT (the paper's RGAT listing and the RGAT/HGT figure caption).  For every
+ * in-edge e = (u -> v, r) and head k (columns [k*dh, (k+1)*dh) of d_out):
+ *   m_e   = h_u W_r                        (edge message)
+ *   t_e   = h_v W_r
+ *   y_e,k = sum_{j in k} m_e[j] w_src[r][j] + t_e[j] w_dst[r][j]
+ *   z_e,k = leakyrelu(y_e,k)  (slope `neg_slope` for y <= 0)
+ *   alpha = exp(z_e,k) / sum_{e' in group(e)} exp(z_e',k)
+ *   out_v[j in k] = sum_e alpha_e,k m_e[j]   (0 when v has no in-edges)
+ * group(e) = all in-edges of v (scope 0) or those of v with relation r (scope 1).
+ * Both the numerator and denominator are taken relative to the group maximum,
+ * which leaves alpha unchanged.
+ * Optional outputs, for scope 0 only: stat_max[v,k] = max z, stat_sum[v,k] =
+ * sum exp(z - max); alpha_out[e,k] for every in-edge of a produced row. */
+int oracle_rgat_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
+                        int32_t heads, const int32_t *src, const int32_t *dst,
+                        const int32_t *rel, const float *h, const float *W,
+                        const float *w_src, const float *w_dst, double neg_slope,
+                        int32_t scope, int64_t nsel, const int32_t *sel, double *out,
+                        double *stat_max, double *stat_sum, double *alpha_out)
+{
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0 || heads <= 0 ||
+        d_out % heads || (scope != 0 && scope != 1))
+        return -1;
+    const int H = heads, dh = d_out / heads;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    const int64_t nrows = sel ? nsel : N;
+    int err = 0;
+#pragma omp parallel reduction(| : err)
+    {
+        double *x = (double *)malloc((size_t)d_in * sizeof(double));
+        double *xv = (double *)malloc((size_t)d_in * sizeof(double));
+        double *t = (double *)malloc((size_t)d_out * sizeof(double));
+        double *mx = (double *)malloc((size_t)R * H * sizeof(double));
+        double *sm = (double *)malloc((size_t)R * H * sizeof(double));
+        double *msg = NULL, *z = NULL;
+        int64_t cap = 0;
+        if (!x || !xv || !t || !mx || !sm) err = 1;
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t i = 0; i < nrows; ++i) {
+            if (err) continue;
+            const int64_t v = sel_node(sel, i);
+            const int64_t p0 = a.ptr[v], deg = a.ptr[v + 1] - p0;
+            double *o = out + (size_t)i * d_out;
+            for (int j = 0; j < d_out; ++j) o[j] = 0.0;
+            if (deg > cap) {
+                free(msg); free(z);
+                cap = deg;
+                msg = (double *)malloc((size_t)cap * d_out * sizeof(double));
+                z = (double *)malloc((size_t)cap * H * sizeof(double));
+                if (!msg || !z) { err = 1; cap = 0; continue; }
+            }
+            load_row(h, v, d_in, xv);
+            /* pass 1: messages and logits of every in-edge */
+            for (int64_t q = 0; q < deg; ++q) {
+                const int64_t e = a.eid[p0 + q];
+                const int r = rel[e];
+                const float *Wr = W + (size_t)r * d_in * d_out;
+                load_row(h, src[e], d_in, x);
+                vecmat(x, Wr, d_in, d_out, 0, d_out, msg + q * d_out);
+                vecmat(xv, Wr, d_in, d_out, 0, d_out, t);
+                for (int k = 0; k < H; ++k) {
+                    double y = 0.0;
+                    for (int j = k * dh; j < (k + 1) * dh; ++j)
+                        y += msg[q * d_out + j] * (double)w_src[(size_t)r * d_out + j] +
+                             t[j] * (double)w_dst[(size_t)r * d_out + j];
+                    z[q * H + k] = y > 0.0 ? y : neg_slope * y;
+                }
+            }
+            /* pass 2: softmax maximum and denominator per group and head */
+            const int G = scope == 0 ? 1 : R;
+            for (int q = 0; q < G * H; ++q) { mx[q] = -INFINITY; sm[q] = 0.0; }
+            for (int64_t q = 0; q < deg; ++q) {
+                const int gi = scope == 0 ? 0 : rel[a.eid[p0 + q]];
+                for (int k = 0; k < H; ++k)
+                    if (z[q * H + k] > mx[gi * H + k]) mx[gi * H + k] = z[q * H + k];
+            }
+            for (int64_t q = 0; q < deg; ++q) {
+                const int gi = scope == 0 ? 0 : rel[a.eid[p0 + q]];
+                for (int k = 0; k < H; ++k) sm[gi * H + k] += exp(z[q * H + k] - mx[gi * H + k]);
+            }
+            /* pass 3: attention-weighted sum of the messages */
+            for (int64_t q = 0; q < deg; ++q) {
+                const int64_t e = a.eid[p0 + q];
+                const int gi = scope == 0 ? 0 : rel[e];
+                for (int k = 0; k < H; ++k) {
+                    const double al = exp(z[q * H + k] - mx[gi * H + k]) / sm[gi * H + k];
+                    if (alpha_out) alpha_out[(size_t)e * H + k] = al;
+                    for (int j = k * dh; j < (k + 1) * dh; ++j) o[j] += al * msg[q * d_out + j];
+                }
+            }
+            if (scope == 0) {
+                for (int k = 0; k < H; ++k) {
+                    if (stat_max) stat_max[(size_t)i * H + k] = deg ? mx[k] : 0.0;
+                    if (stat_sum) stat_sum[(size_t)i * H + k] = deg ? sm[k] : 0.0;
+                }
+            }
+        }
+        free(x); free(xv); free(t); free(mx); free(sm); free(msg); free(z);
+    }
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* HGT (the layer the paper's RGAT/HGT figure shows; equations of the HGT
+ * paper it cites).  Heads split d into H blocks of dk = d / H.
+ *   K_n = h_n Wk[tau(n)],  Q_n = h_n Wq[tau(n)],  V_n = h_n Wv[tau(n)]
+ *   for every in-edge e = (s -> t, r) and head i:
+ *     a_e,i   = (K_s,i Watt[r][i]) . Q_t,i * mu[r] * att_scale
+ *     msg_e,i = V_s,i Wmsg[r][i]
+ *     alpha_e,i = softmax of a_.,i over all in-edges of t
+ *   agg_t = concat_i sum_e alpha_e,i msg_e,i      (0 without in-edges)
+ *   out_t = agg_t Wa[tau(t)] (if a_linear, else agg_t) + h_t (if residual)
+ * K and V are recomputed for every edge from h_s (they depend only on the
+ * source node; recomputation gives the same fp64 values). */
+int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
+                       int32_t heads, const int32_t *src, const int32_t *dst,
+                       const int32_t *rel, const int32_t *ntype, const float *h,
+                       const float *Wk, const float *Wq, const float *Wv, const float *Wa,
+                       const float *Watt, const float *Wmsg, const float *mu,
+                       double att_scale, int32_t residual, int32_t a_linear,
+                       int64_t nsel, const int32_t *sel, double *out)
+{
+    if (check_coo(N, E, R, src, dst, rel) || T <= 0 || d <= 0 || heads <= 0 || d % heads)
+        return -1;
+    for (int64_t n = 0; n < N; ++n)
+        if (ntype[n] < 0 || ntype[n] >= T) return -1;
+    const int H = heads, dk = d / heads;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    const int64_t nrows = sel ? nsel : N;
+    int err = 0;
+#pragma omp parallel reduction(| : err)
+    {
+        double *x = (double *)malloc((size_t)d * sizeof(double));
+        double *q = (double *)malloc((size_t)d * sizeof(double));
+        double *kk = (double *)malloc((size_t)d * sizeof(double));
+        double *vv = (double *)malloc((size_t)d * sizeof(double));
+        double *kw = (double *)malloc((size_t)dk * sizeof(double));
+        double *agg = (double *)malloc((size_t)d * sizeof(double));
+        double *mx = (double *)malloc((size_t)H * sizeof(double));
+        double *sm = (double *)malloc((size_t)H * sizeof(double));
+        double *msg = NULL, *att = NULL;
+        int64_t cap = 0;
+        if (!x || !q || !kk || !vv || !kw || !agg || !mx || !sm) err = 1;
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t i = 0; i < nrows; ++i) {
+            if (err) continue;
+            const int64_t t = sel_node(sel, i);
+            const int64_t p0 = a.ptr[t], deg = a.ptr[t + 1] - p0;
+            if (deg > cap) {
+                free(msg); free(att);
+                cap = deg;
+                msg = (double *)malloc((size_t)cap * d * sizeof(double));
+                att = (double *)malloc((size_t)cap * H * sizeof(double));
+                if (!msg || !att) { err = 1; cap = 0; continue; }
+            }
+            load_row(h, t, d, x);
+            vecmat(x, Wq + (size_t)ntype[t] * d * d, d, d, 0, d, q);
+            for (int64_t p = 0; p < deg; ++p) {
+                const int64_t e = a.eid[p0 + p];
+                const int64_t s = src[e];
+                const int r = rel[e];
+                load_row(h, s, d, x);
+                vecmat(x, Wk + (size_t)ntype[s] * d * d, d, d, 0, d, kk);
+                vecmat(x, Wv + (size_t)ntype[s] * d * d, d, d, 0, d, vv);
+                for (int hh = 0; hh < H; ++hh) {
+                    const float *Wat = Watt + ((size_t)r * H + hh) * dk * dk;
+                    const float *Wms = Wmsg + ((size_t)r * H + hh) * dk * dk;
+                    vecmat(kk + hh * dk, Wat, dk, dk, 0, dk, kw);
+                    double dot = 0.0;
+                    for (int j = 0; j < dk; ++j) dot += kw[j] * q[hh * dk + j];
+                    att[p * H + hh] = dot * (double)mu[r] * att_scale;
+                    vecmat(vv + hh * dk, Wms, dk, dk, 0, dk, msg + p * d + hh * dk);
+                }
+            }
+            for (int hh = 0; hh < H; ++hh) { mx[hh] = -INFINITY; sm[hh] = 0.0; }
+            for (int64_t p = 0; p < deg; ++p)
+                for (int hh = 0; hh < H; ++hh)
+                    if (att[p * H + hh] > mx[hh]) mx[hh] = att[p * H + hh];
+            for (int64_t p = 0; p < deg; ++p)
+                for (int hh = 0; hh < H; ++hh) sm[hh] += exp(att[p * H + hh] - mx[hh]);
+            for (int j = 0; j < d; ++j) agg[j] = 0.0;
+            for (int64_t p = 0; p < deg; ++p)
+                for (int hh = 0; hh < H; ++hh) {
+                    const double al = exp(att[p * H + hh] - mx[hh]) / sm[hh];
+                    for (int j = hh * dk; j < (hh + 1) * dk; ++j) agg[j] += al * msg[p * d + j];
+                }
+            double *o = out + (size_t)i * d;
+            if (a_linear) vecmat(agg, Wa + (size_t)ntype[t] * d * d, d, d, 0, d, o);
+            else for (int j = 0; j < d; ++j) o[j] = agg[j];
+            if (residual)
+                for (int j = 0; j < d; ++j) o[j] += (double)h[(size_t)t * d + j];
+        }
+        free(x); free(q); free(kk); free(vv); free(kw); free(agg); free(mx); free(sm);
+        free(msg); free(att);
+    }
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* RGAT backward for the loss L = sum(out * G) (G = grad_out), softmax over all
+ * in-edges of the destination (scope 0).  With the forward's notation and
+ * Y_e,k = dL/dy_e,k:
+ *   dalpha_e,k = sum_{j in k} G_v[j] m_e[j]
+ *   s_v,k      = sum_{e in in(v)} alpha_e,k dalpha_e,k
+ *   Y_e,k      = alpha_e,k (dalpha_e,k - s_v,k) * (1 if y_e,k > 0 else slope)
+ *   dm_e[j]    = alpha_e,k G_v[j] + Y_e,k w_src[r][j]     (message and atts paths)
+ *   dt_e[j]    = Y_e,k w_dst[r][j]                          (attt path)
+ *   dW_r      += h_u^T dm_e + h_v^T dt_e
+ *   dh_u      += dm_e W_r^T ;   dh_v += dt_e W_r^T
+ *   dw_src[r] += Y_e,k m_e ;    dw_dst[r] += Y_e,k t_e
+ * node_mask (nullable): compute dh only for nodes with node_mask[n] != 0
+ * rel_mask  (nullable): compute dW, dw_src, dw_dst only for those relations.
+ * Entries outside the masks are left at zero.  Only destinations that feed a
+ * requested entry are visited. */
+int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
+                         int32_t heads, const int32_t *src, const int32_t *dst,
+                         const int32_t *rel, const float *h, const float *W,
+                         const float *w_src, const float *w_dst, double neg_slope,
+                         const float *G, const uint8_t *node_mask, const uint8_t *rel_mask,
+                         double *dh, double *dW, double *dw_src, double *dw_dst)
+{
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_in > 512 || d_out <= 0 ||
+        heads <= 0 || d_out % heads)
+        return -1;
+    const int H = heads, dh_ = d_out / heads;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    /* destinations whose in-edges contribute to a requested entry */
+    uint8_t *need = (uint8_t *)calloc((size_t)(N > 0 ? N : 1), 1);
+    if (!need) { free_in_lists(&a); return -3; }
+    for (int64_t e = 0; e < E; ++e) {
+        const int want_rel = rel_mask ? rel_mask[rel[e]] != 0 : 1;
+        const int want_node = node_mask ? (node_mask[src[e]] || node_mask[dst[e]]) : 1;
+        if (want_rel || want_node) need[dst[e]] = 1;
+    }
+    memset(dh, 0, (size_t)N * d_in * sizeof(double));
+    memset(dW, 0, (size_t)R * d_in * d_out * sizeof(double));
+    memset(dw_src, 0, (size_t)R * d_out * sizeof(double));
+    memset(dw_dst, 0, (size_t)R * d_out * sizeof(double));
+    int err = 0;
+    /* Destinations are processed one at a time in increasing id; the work of a
+     * destination is split over threads by output entry, so every sum is
+     * accumulated in a fixed order. */
+    double *msg = NULL, *t = NULL, *al = NULL, *Y = NULL, *dm = NULL, *dtv = NULL;
+    int64_t cap = 0;
+    double *xv = (double *)malloc((size_t)d_in * sizeof(double));
+    double *x = (double *)malloc((size_t)d_in * sizeof(double));
+    double *mx = (double *)malloc((size_t)H * sizeof(double));
+    double *sm = (double *)malloc((size_t)H * sizeof(double));
+    double *sv = (double *)malloc((size_t)H * sizeof(double));
+    if (!xv || !x || !mx || !sm || !sv) err = 1;
+    for (int64_t v = 0; v < N && !err; ++v) {
+        if (!need[v]) continue;
+        const int64_t p0 = a.ptr[v], deg = a.ptr[v + 1] - p0;
+        if (deg == 0) continue;
+        if (deg > cap) {
+            free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
+            cap = deg;
+            msg = (double *)malloc((size_t)cap * d_out * sizeof(double));
+            t = (double *)malloc((size_t)cap * d_out * sizeof(double));
+            al = (double *)malloc((size_t)cap * H * sizeof(double));
+            Y = (double *)malloc((size_t)cap * H * sizeof(double));
+            dm = (double *)malloc((size_t)cap * d_out * sizeof(double));
+            dtv = (double *)malloc((size_t)cap * d_out * sizeof(double));
+            if (!msg || !t || !al || !Y || !dm || !dtv) { err = 1; break; }
+        }
+        load_row(h, v, d_in, xv);
+        /* forward recomputation: messages, t_e, logits, softmax */
+#pragma omp parallel for schedule(static) if (deg >= 64)
+        for (int64_t q = 0; q < deg; ++q) {
+            double xl[512];
+            const int64_t e = a.eid[p0 + q];
+            const int r = rel[e];
+            const float *Wr = W + (size_t)r * d_in * d_out;
+            for (int i = 0; i < d_in; ++i) xl[i] = (double)h[(size_t)src[e] * d_in + i];
+            vecmat(xl, Wr, d_in, d_out, 0, d_out, msg + q * d_out);
+            vecmat(xv, Wr, d_in, d_out, 0, d_out, t + q * d_out);
+            for (int k = 0; k < H; ++k) {
+                double y = 0.0;
+                for (int j = k * dh_; j < (k + 1) * dh_; ++j)
+                    y += msg[q * d_out + j] * (double)w_src[(size_t)r * d_out + j] +
+                         t[q * d_out + j] * (double)w_dst[(size_t)r * d_out + j];
+                Y[q * H + k] = y;          /* pre-activation, reused below */
+                al[q * H + k] = y > 0.0 ? y : neg_slope * y;
+            }
+        }
+        for (int k = 0; k < H; ++k) { mx[k] = -INFINITY; sm[k] = 0.0; sv[k] = 0.0; }
+        for (int64_t q = 0; q < deg; ++q)
+            for (int k = 0; k < H; ++k) if (al[q * H + k] > mx[k]) mx[k] = al[q * H + k];
+        for (int64_t q = 0; q < deg; ++q)
+            for (int k = 0; k < H; ++k) sm[k] += exp(al[q * H + k] - mx[k]);
+        for (int64_t q = 0; q < deg; ++q)
+            for (int k = 0; k < H; ++k) al[q * H + k] = exp(al[q * H + k] - mx[k]) / sm[k];
+        /* dalpha and s_v */
+        const float *Gv = G + (size_t)v * d_out;
+        for (int64_t q = 0; q < deg; ++q)
+            for (int k = 0; k < H; ++k) {
+                double da = 0.0;
+                for (int j = k * dh_; j < (k + 1) * dh_; ++j) da += (double)Gv[j] * msg[q * d_out + j];
+                sv[k] += al[q * H + k] * da;
+                dm[q * d_out + k * dh_] = da;   /* stash dalpha in the first slot */
+            }
+        for (int64_t q = 0; q < deg; ++q) {
+            const int64_t e = a.eid[p0 + q];
+            const int r = rel[e];
+            for (int k = 0; k < H; ++k) {
+                const double y = Y[q * H + k];
+                const double da = dm[q * d_out + k * dh_];
+                const double dz = al[q * H + k] * (da - sv[k]);
+                Y[q * H + k] = dz * (y > 0.0 ? 1.0 : neg_slope);
+            }
+            for (int j = 0; j < d_out; ++j) {
+                const int k = j / dh_;
+                dm[q * d_out + j] = al[q * H + k] * (double)Gv[j] + Y[q * H + k] * (double)w_src[(size_t)r * d_out + j];
+                dtv[q * d_out + j] = Y[q * H + k] * (double)w_dst[(size_t)r * d_out + j];
+            }
+        }
+        /* scatter in edge-id order; parallel over output entries */
+        for (int64_t q = 0; q < deg; ++q) {
+            const int64_t e = a.eid[p0 + q];
+            const int r = rel[e];
+            const int64_t u = src[e];
+            const float *Wr = W + (size_t)r * d_in * d_out;
+            if (!rel_mask || rel_mask[r]) {
+#pragma omp parallel for schedule(static) if (d_in * d_out >= 1 << 16)
+                for (int i = 0; i < d_in; ++i) {
+                    const double hu = (double)h[(size_t)u * d_in + i], hv = xv[i];
+                    double *row = dW + ((size_t)r * d_in + i) * d_out;
+                    for (int j = 0; j < d_out; ++j) row[j] += hu * dm[q * d_out + j] + hv * dtv[q * d_out + j];
+                }
+                for (int j = 0; j < d_out; ++j) {
+                    const int k = j / dh_;
+                    dw_src[(size_t)r * d_out + j] += Y[q * H + k] * msg[q * d_out + j];
+                    dw_dst[(size_t)r * d_out + j] += Y[q * H + k] * t[q * d_out + j];
+                }
+            }
+            if (!node_mask || node_mask[u]) {
+                for (int i = 0; i < d_in; ++i) {
+                    double s = 0.0;
+                    for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * dm[q * d_out + j];
+                    dh[(size_t)u * d_in + i] += s;
+                }
+            }
+            if (!node_mask || node_mask[v]) {
+                for (int i = 0; i < d_in; ++i) {
+                    double s = 0.0;
+                    for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * dtv[q * d_out + j];
+                    dh[(size_t)v * d_in + i] += s;
+                }
+            }
+        }
+    }
+    (void)x;
+    free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
+    free(xv); free(x); free(mx); free(sm); free(sv); free(need);
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

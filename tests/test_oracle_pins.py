@@ -1,0 +1,472 @@
+"""Pins of the fp64 oracle against formulations that do not share its loops.
+
+Each layer is checked against a dense formulation (one adjacency matrix per
+relation, multiplicities as weights) written with numpy / torch tensor algebra,
+against the homogeneous special cases the paper names (GCN for one relation,
+GAT for one relation with attention, scaled dot-product attention for HGT on a
+complete graph), against closed forms, invariants of the edge softmax, and --
+for the RGAT backward pass -- against torch.autograd and central finite
+differences.  A dropped term, a wrong sign or index, or a transposed operand in
+the oracle fails at least one of these.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import tiny_graph, tiny_tensors
+
+KINDS = ["random", "hub", "dups", "isolated", "empty"]
+
+
+def dense_adj(g):
+    A = np.zeros((g["R"], g["N"], g["N"]))
+    np.add.at(A, (g["rel"], g["dst"], g["src"]), 1.0)
+    return A
+
+
+def leaky(x, s):
+    return np.where(x > 0, x, s * x)
+
+
+# ---------------------------------------------------------------- RGCN
+def rgcn_dense(g, h, W, W0, relu):
+    A = dense_adj(g)
+    c = A.sum(axis=2, keepdims=True)
+    An = np.divide(A, c, out=np.zeros_like(A), where=c > 0)
+    out = np.einsum("rvu,ui,rij->vj", An, h.astype(np.float64), W.astype(np.float64))
+    if W0 is not None:
+        out += h.astype(np.float64) @ W0.astype(np.float64)
+    return np.maximum(out, 0) if relu else out
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("self_loop,relu", [(True, False), (False, False), (True, True)])
+def test_rgcn_dense_brute_force(kind, self_loop, relu):
+    g = tiny_graph(11, N=23, E=90, R=4, T=2, kind=kind)
+    t = tiny_tensors(11, g, 8, 6)
+    W0 = t["W0"] if self_loop else None
+    ref = rgcn_dense(g, t["h"], t["W"], W0, relu)
+    got = oracle.rgcn_forward(g, t["h"], t["W"], W0, relu=relu)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_rgcn_reduces_to_gcn():
+    """One relation, one node type, no self-loop: h' = A* h W with A* the
+    in-degree-normalised adjacency (the paper's GCN layer), evaluated with
+    scipy's sparse product."""
+    import scipy.sparse as sp
+    g = tiny_graph(5, N=24, E=80, R=1, T=1)
+    t = tiny_tensors(5, g, 7, 5)
+    A = sp.coo_matrix((np.ones(g["E"]), (g["dst"], g["src"])), shape=(g["N"], g["N"])).tocsr()
+    deg = np.asarray(A.sum(axis=1)).ravel()
+    Dinv = sp.diags(np.divide(1.0, deg, out=np.zeros_like(deg), where=deg > 0))
+    ref = (Dinv @ A) @ (t["h"].astype(np.float64) @ t["W"][0].astype(np.float64))
+    got = oracle.rgcn_forward(g, t["h"], t["W"])
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_rgcn_identity_weights_closed_form():
+    """W_r = I, no self-loop: out_v = sum_r mean_{u in N_v^r} h_u."""
+    g = tiny_graph(3, N=15, E=60, R=3, kind="dups")
+    h = tiny_tensors(3, g, 4, 4)["h"]
+    W = np.stack([np.eye(4, dtype=np.float32)] * 3)
+    ref = np.zeros((15, 4))
+    for v in range(15):
+        for r in range(3):
+            us = [g["src"][e] for e in range(g["E"]) if g["dst"][e] == v and g["rel"][e] == r]
+            if us:
+                ref[v] += np.mean(h[us].astype(np.float64), axis=0)
+    np.testing.assert_allclose(oracle.rgcn_forward(g, h, W), ref, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- RGAT
+def rgat_dense(g, h, W, ws, wt, H, slope, scope, return_alpha=False):
+    R, N = g["R"], g["N"]
+    d_out = W.shape[2]
+    dh = d_out // H
+    A = dense_adj(g)
+    M = np.einsum("ui,rij->ruj", h.astype(np.float64), W.astype(np.float64)).reshape(R, N, H, dh)
+    wsh = ws.astype(np.float64).reshape(R, H, dh)
+    wth = wt.astype(np.float64).reshape(R, H, dh)
+    S = np.einsum("ruhc,rhc->ruh", M, wsh)                 # source term per (r, u, head)
+    Tt = np.einsum("rvhc,rhc->rvh", M, wth)                # destination term per (r, v, head)
+    Z = leaky(S[:, None, :, :] + Tt[:, :, None, :], slope)  # [R, v, u, H]
+    mask = (A > 0)[..., None]
+    Zm = np.where(mask, Z, -np.inf)
+    if scope == 0:
+        mx = Zm.max(axis=(0, 2), keepdims=True)
+    else:
+        mx = Zm.max(axis=2, keepdims=True)
+    mx = np.where(np.isfinite(mx), mx, 0.0)
+    ex = np.where(mask, np.exp(np.where(mask, Z, 0.0) - mx), 0.0) * A[..., None]
+    den = ex.sum(axis=(0, 2), keepdims=True) if scope == 0 else ex.sum(axis=2, keepdims=True)
+    al = np.divide(ex, den, out=np.zeros_like(ex), where=den > 0)
+    out = np.einsum("rvuh,ruhc->vhc", al, M).reshape(N, d_out)
+    return (out, al) if return_alpha else out
+
+
+def rgat_reordered(g, h, W, ws, wt, H, slope):
+    """Linear operator reordering: atts = h_u (W_r w_src), attt = h_v (W_r w_dst),
+    and out_v = sum_r (sum_u alpha h_u) W_r -- evaluated independently."""
+    R, N = g["R"], g["N"]
+    d_in, d_out = W.shape[1], W.shape[2]
+    dh = d_out // H
+    h64, W64 = h.astype(np.float64), W.astype(np.float64)
+    Wh = W64.reshape(R, d_in, H, dh)
+    wsp = np.einsum("rihc,rhc->rhi", Wh, ws.astype(np.float64).reshape(R, H, dh))  # W_r w_src
+    wtp = np.einsum("rihc,rhc->rhi", Wh, wt.astype(np.float64).reshape(R, H, dh))
+    out = np.zeros((N, H, dh))
+    for v in range(N):
+        es = [e for e in range(g["E"]) if g["dst"][e] == v]
+        if not es:
+            continue
+        z = np.array([leaky(h64[g["src"][e]] @ wsp[g["rel"][e]].T + h64[v] @ wtp[g["rel"][e]].T,
+                            slope) for e in es])                    # [deg, H]
+        a = np.exp(z - z.max(axis=0)); a /= a.sum(axis=0)
+        for r in range(R):
+            sel = [i for i, e in enumerate(es) if g["rel"][e] == r]
+            if not sel:
+                continue
+            agg = np.einsum("eh,ei->hi", a[sel], h64[[g["src"][es[i]] for i in sel]])
+            out[v] += np.einsum("hi,ihc->hc", agg, Wh[r])
+    return out.reshape(N, d_out)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("H,scope", [(1, 0), (2, 0), (1, 1), (2, 1)])
+def test_rgat_dense_brute_force(kind, H, scope):
+    g = tiny_graph(21, N=19, E=85, R=3, T=2, kind=kind)
+    t = tiny_tensors(21, g, 6, 8, heads=H, att_var=1.0)
+    ref = rgat_dense(g, t["h"], t["W"], t["w_src"], t["w_dst"], H, 0.2, scope)
+    got = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=H,
+                              neg_slope=0.2, scope=scope)
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("H", [1, 2])
+def test_rgat_reordering_identity(H):
+    g = tiny_graph(4, N=14, E=60, R=3, kind="dups")
+    t = tiny_tensors(4, g, 5, 8, heads=H, att_var=1.0)
+    ref = rgat_reordered(g, t["h"], t["W"], t["w_src"], t["w_dst"], H, 0.2)
+    got = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=H)
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+def test_rgat_reduces_to_gat():
+    """One relation, one head, no duplicate edges: single-head GAT, with the
+    masked softmax taken by torch.softmax in fp64."""
+    rng = np.random.default_rng(9)
+    N = 17
+    mask = rng.random((N, N)) < 0.3                      # mask[v, u]: edge u -> v
+    dst, src = np.nonzero(mask)
+    g = dict(N=N, E=len(src), R=1, T=1, src=src.astype(np.int32), dst=dst.astype(np.int32),
+             rel=np.zeros(len(src), np.int32), ntype=np.zeros(N, np.int32))
+    t = tiny_tensors(9, g, 6, 6, att_var=1.0)
+    Wm = torch.tensor(t["W"][0], dtype=torch.float64)
+    Hm = torch.tensor(t["h"], dtype=torch.float64) @ Wm
+    a_s = torch.tensor(t["w_src"][0], dtype=torch.float64)
+    a_t = torch.tensor(t["w_dst"][0], dtype=torch.float64)
+    logit = torch.nn.functional.leaky_relu((Hm @ a_t)[:, None] + (Hm @ a_s)[None, :], 0.2)
+    logit = logit.masked_fill(~torch.tensor(mask), float("-inf"))
+    alpha = torch.softmax(logit, dim=1).nan_to_num(0.0)
+    ref = (alpha @ Hm).numpy()
+    got = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"])
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+def test_rgat_zero_attention_is_mean():
+    """w_src = w_dst = 0: every logit is 0, alpha = 1/deg, out_v = mean of h_u W_r."""
+    g = tiny_graph(8, N=12, E=50, R=3, kind="dups")
+    t = tiny_tensors(8, g, 5, 5)
+    z = np.zeros_like(t["w_src"])
+    got = oracle.rgat_forward(g, t["h"], t["W"], z, z)
+    ref = np.zeros((12, 5))
+    for v in range(12):
+        es = [e for e in range(g["E"]) if g["dst"][e] == v]
+        if es:
+            ref[v] = np.mean([t["h"][g["src"][e]].astype(np.float64) @ t["W"][g["rel"][e]]
+                              for e in es], axis=0)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("scope", [0, 1])
+def test_rgat_softmax_sums_to_one(scope):
+    g = tiny_graph(13, N=20, E=120, R=4, kind="hub")
+    t = tiny_tensors(13, g, 6, 8, heads=2, att_var=1.0)
+    _, alpha = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=2,
+                                   scope=scope, want_alpha=True)
+    key = g["dst"] if scope == 0 else g["dst"].astype(np.int64) * g["R"] + g["rel"]
+    for k in np.unique(key):
+        np.testing.assert_allclose(alpha[key == k].sum(axis=0), 1.0, atol=1e-12)
+
+
+def test_rgat_destination_term_shift_invariance():
+    """With slope 1 (no nonlinearity) the destination term is a constant per
+    softmax group; softmax is invariant to it, so w_dst must not matter:
+    per-(dst, rel) groups for any R, per-dst groups for R = 1."""
+    for R, scope in [(4, 1), (1, 0)]:
+        g = tiny_graph(17, N=18, E=90, R=R, kind="random")
+        t = tiny_tensors(17, g, 6, 6, att_var=1.0)
+        a = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], neg_slope=1.0,
+                                scope=scope)
+        b = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], 3.0 * t["w_dst"] + 1.0,
+                                neg_slope=1.0, scope=scope)
+        np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-13)
+    # ... and with slope 0.2 it does matter (the check above is not vacuous)
+    c = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], neg_slope=0.2)
+    d = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], 3.0 * t["w_dst"] + 1.0, neg_slope=0.2)
+    assert np.abs(c - d).max() > 1e-3
+
+
+def test_rgat_stats_match_definition():
+    g = tiny_graph(2, N=16, E=70, R=3, kind="isolated")
+    t = tiny_tensors(2, g, 6, 6, att_var=1.0)
+    _, mx, sm = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], want_stats=True)
+    ref, al = rgat_dense(g, t["h"], t["W"], t["w_src"], t["w_dst"], 1, 0.2, 0, return_alpha=True)
+    for v in range(16):
+        es = [e for e in range(g["E"]) if g["dst"][e] == v]
+        if not es:
+            assert mx[v, 0] == 0 and sm[v, 0] == 0
+            continue
+        z = [leaky(t["h"][g["src"][e]].astype(np.float64) @ t["W"][g["rel"][e]] @ t["w_src"][g["rel"][e]]
+                   + t["h"][v].astype(np.float64) @ t["W"][g["rel"][e]] @ t["w_dst"][g["rel"][e]], 0.2)
+             for e in es]
+        assert abs(mx[v, 0] - max(z)) < 1e-12
+        assert abs(sm[v, 0] - sum(np.exp(np.array(z) - max(z)))) < 1e-12
+
+
+@pytest.mark.parametrize("layer", ["rgcn", "rgat", "hgt"])
+def test_permutation_equivariance(layer):
+    """Relabelling nodes permutes the output rows; shuffling the COO order changes nothing."""
+    g = tiny_graph(31, N=21, E=100, R=3, T=2, kind="hub")
+    t = tiny_tensors(31, g, 8, 8, heads=2, att_var=1.0)
+    rng = np.random.default_rng(0)
+    pi = rng.permutation(g["N"]).astype(np.int32)        # old id -> new id
+    inv = np.argsort(pi)
+    eperm = rng.permutation(g["E"])
+    g2 = dict(g, src=pi[g["src"]][eperm], dst=pi[g["dst"]][eperm], rel=g["rel"][eperm],
+              ntype=g["ntype"][inv])
+    t2 = dict(t, h=t["h"][inv])
+
+    def run(gg, tt):
+        if layer == "rgcn":
+            return oracle.rgcn_forward(gg, tt["h"], tt["W"], tt["W0"])
+        if layer == "rgat":
+            return oracle.rgat_forward(gg, tt["h"], tt["W"], tt["w_src"], tt["w_dst"], heads=2)
+        return oracle.hgt_forward(gg, tt["h"], tt["Wk"], tt["Wq"], tt["Wv"], tt["Wa"], tt["Watt"],
+                                  tt["Wmsg"], tt["mu"], heads=2)
+    np.testing.assert_allclose(run(g2, t2)[pi], run(g, t), rtol=1e-11, atol=1e-13)
+
+
+def test_sel_rows_match_full():
+    g = tiny_graph(6, N=30, E=150, R=3, T=2, kind="hub")
+    t = tiny_tensors(6, g, 8, 8, heads=2, att_var=1.0)
+    sel = np.array([0, 29, 3, 3, 17], np.int32)
+    full = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=2)
+    part = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=2, sel=sel)
+    np.testing.assert_array_equal(part, full[sel])
+
+
+# ---------------------------------------------------------------- HGT
+def hgt_dense(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, H, scale, residual=True, a_linear=True):
+    N, R = g["N"], g["R"]
+    d = h.shape[1]
+    dk = d // H
+    h64 = h.astype(np.float64)
+    nt = g["ntype"]
+    K = np.einsum("ni,nij->nj", h64, Wk.astype(np.float64)[nt]).reshape(N, H, dk)
+    Q = np.einsum("ni,nij->nj", h64, Wq.astype(np.float64)[nt]).reshape(N, H, dk)
+    V = np.einsum("ni,nij->nj", h64, Wv.astype(np.float64)[nt]).reshape(N, H, dk)
+    KW = np.einsum("shc,rhcj->rshj", K, Watt.astype(np.float64))
+    att = np.einsum("rshj,thj->rtsh", KW, Q) * (mu.astype(np.float64)[:, None, None, None] * scale)
+    msg = np.einsum("shc,rhcj->rshj", V, Wmsg.astype(np.float64))
+    A = dense_adj(g)
+    mask = (A > 0)[..., None]
+    am = np.where(mask, att, -np.inf)
+    mx = am.max(axis=(0, 2), keepdims=True)
+    mx = np.where(np.isfinite(mx), mx, 0.0)
+    ex = np.where(mask, np.exp(np.where(mask, att, 0.0) - mx), 0.0) * A[..., None]
+    den = ex.sum(axis=(0, 2), keepdims=True)
+    al = np.divide(ex, den, out=np.zeros_like(ex), where=den > 0)
+    agg = np.einsum("rtsh,rshj->thj", al, msg).reshape(N, d)
+    out = np.einsum("ni,nij->nj", agg, Wa.astype(np.float64)[nt]) if a_linear else agg
+    return out + h64 if residual else out
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("H", [1, 2, 4])
+def test_hgt_dense_brute_force(kind, H):
+    g = tiny_graph(41, N=17, E=80, R=3, T=3, kind=kind)
+    t = tiny_tensors(41, g, 8, 8, heads=H)
+    scale = 1.0 / np.sqrt(8 // H)
+    ref = hgt_dense(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                    t["mu"], H, scale)
+    got = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"],
+                             t["Wmsg"], t["mu"], heads=H)
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+def test_hgt_flags():
+    g = tiny_graph(42, N=15, E=60, R=2, T=2)
+    t = tiny_tensors(42, g, 8, 8, heads=2)
+    args = (t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"], t["mu"])
+    for res, lin in [(False, True), (True, False), (False, False)]:
+        ref = hgt_dense(g, *args, 2, 0.5, residual=res, a_linear=lin)
+        got = oracle.hgt_forward(g, *args, heads=2, att_scale=0.5, residual=res, a_linear=lin)
+        np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("H", [1, 4])
+def test_hgt_complete_graph_is_scaled_dot_product_attention(H):
+    """One node type, one relation, W_att = W_msg = I, mu = 1, complete graph
+    (every ordered pair incl. self): agg = softmax(Q K^T * scale) V per head,
+    computed by torch's scaled_dot_product_attention in fp64."""
+    N, d = 13, 8
+    dk = d // H
+    g = tiny_graph(44, N=N, E=0, R=1, T=1, kind="complete")
+    t = tiny_tensors(44, g, d, d, heads=H)
+    eye = np.broadcast_to(np.eye(dk, dtype=np.float32), (1, H, dk, dk)).copy()
+    one = np.ones(1, np.float32)
+    scale = 1.0 / np.sqrt(dk)
+    got = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], eye, eye, one,
+                             heads=H, att_scale=scale, residual=False, a_linear=False)
+    h = torch.tensor(t["h"], dtype=torch.float64)
+    q = (h @ torch.tensor(t["Wq"][0], dtype=torch.float64)).reshape(N, H, dk).transpose(0, 1)
+    k = (h @ torch.tensor(t["Wk"][0], dtype=torch.float64)).reshape(N, H, dk).transpose(0, 1)
+    v = (h @ torch.tensor(t["Wv"][0], dtype=torch.float64)).reshape(N, H, dk).transpose(0, 1)
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=scale)
+    ref = ref.transpose(0, 1).reshape(N, d).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+def test_hgt_zero_attention_weight_is_mean():
+    """W_att = 0: every score is 0, agg_t = mean over in-edges of V_s W_msg,r."""
+    g = tiny_graph(45, N=12, E=40, R=2, T=2, kind="dups")
+    t = tiny_tensors(45, g, 8, 8, heads=2)
+    zero = np.zeros_like(t["Watt"])
+    got = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], zero, t["Wmsg"],
+                             t["mu"], heads=2, residual=False, a_linear=False)
+    ref = np.zeros((12, 8))
+    for v in range(12):
+        es = [e for e in range(g["E"]) if g["dst"][e] == v]
+        rows = []
+        for e in es:
+            s, r = g["src"][e], g["rel"][e]
+            V = (t["h"][s].astype(np.float64) @ t["Wv"][g["ntype"][s]]).reshape(2, 4)
+            rows.append(np.concatenate([V[i] @ t["Wmsg"][r, i] for i in range(2)]))
+        if rows:
+            ref[v] = np.mean(rows, axis=0)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- RGAT backward
+def rgat_torch_dense(g, h, W, ws, wt, H, slope):
+    R, N = g["R"], g["N"]
+    d_out = W.shape[2]
+    dh = d_out // H
+    A = torch.tensor(dense_adj(g))
+    M = torch.einsum("ui,rij->ruj", h, W).reshape(R, N, H, dh)
+    S = torch.einsum("ruhc,rhc->ruh", M, ws.reshape(R, H, dh))
+    Tt = torch.einsum("rvhc,rhc->rvh", M, wt.reshape(R, H, dh))
+    Z = torch.nn.functional.leaky_relu(S[:, None] + Tt[:, :, None], slope)
+    mask = (A > 0)[..., None].expand_as(Z)
+    mx = torch.where(mask, Z, torch.tensor(-torch.inf, dtype=Z.dtype)).amax(dim=(0, 2), keepdim=True)
+    mx = torch.where(torch.isfinite(mx), mx, torch.zeros_like(mx)).detach()
+    Zc = torch.where(mask, Z, mx.expand_as(Z))
+    ex = torch.exp(Zc - mx) * A[..., None]
+    den = ex.sum(dim=(0, 2), keepdim=True)
+    den = torch.where(den > 0, den, torch.ones_like(den))
+    al = ex / den
+    return torch.einsum("rvuh,ruhc->vhc", al, M).reshape(N, d_out)
+
+
+@pytest.mark.parametrize("kind,H", [("random", 1), ("hub", 1), ("dups", 2), ("isolated", 2)])
+def test_rgat_backward_vs_autograd(kind, H):
+    g = tiny_graph(51, N=14, E=70, R=3, kind=kind)
+    t = tiny_tensors(51, g, 6, 8, heads=H, att_var=1.0)
+    ts = {k: torch.tensor(t[k], dtype=torch.float64, requires_grad=True)
+          for k in ("h", "W", "w_src", "w_dst")}
+    out = rgat_torch_dense(g, ts["h"], ts["W"], ts["w_src"], ts["w_dst"], H, 0.2)
+    (out * torch.tensor(t["grad_out"], dtype=torch.float64)).sum().backward()
+    dh, dW, dws, dwd = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"],
+                                            t["grad_out"], heads=H)
+    for got, k in [(dh, "h"), (dW, "W"), (dws, "w_src"), (dwd, "w_dst")]:
+        np.testing.assert_allclose(got, ts[k].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+
+
+def test_rgat_backward_finite_differences():
+    """Central differences of L = sum(out * G) for every parameter entry."""
+    g = tiny_graph(52, N=6, E=16, R=2, kind="dups")
+    t = tiny_tensors(52, g, 3, 4, heads=2, att_var=1.0)
+    G = t["grad_out"]
+
+    def loss(tt):
+        out = oracle.rgat_forward(g, tt["h"], tt["W"], tt["w_src"], tt["w_dst"], heads=2)
+        return float((out * G).sum())
+    grads = dict(zip(("h", "W", "w_src", "w_dst"),
+                     oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], G, heads=2)))
+    for k in grads:
+        base = t[k]
+        fd = np.zeros(base.shape)
+        for idx in np.ndindex(base.shape):
+            step = 1e-2 * max(1e-2, abs(float(base[idx])))
+            plus, minus = base.copy(), base.copy()
+            plus[idx] = np.float32(base[idx] + step)
+            minus[idx] = np.float32(base[idx] - step)
+            denom = float(plus[idx]) - float(minus[idx])
+            fd[idx] = (loss(dict(t, **{k: plus})) - loss(dict(t, **{k: minus}))) / denom
+        np.testing.assert_allclose(grads[k], fd, rtol=2e-3, atol=2e-4, err_msg=k)
+
+
+def test_rgat_backward_masks():
+    g = tiny_graph(53, N=20, E=100, R=4, kind="hub")
+    t = tiny_tensors(53, g, 6, 6, att_var=1.0)
+    full = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    nm = np.zeros(20, np.uint8); nm[[0, 5, 19]] = 1
+    rm = np.zeros(4, np.uint8); rm[2] = 1
+    part = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                node_mask=nm, rel_mask=rm)
+    np.testing.assert_allclose(part[0][nm == 1], full[0][nm == 1], rtol=1e-12, atol=1e-14)
+    for a, b in zip(part[1:], full[1:]):
+        np.testing.assert_allclose(a[2], b[2], rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- integer preprocessing
+@pytest.mark.parametrize("kind", KINDS + ["complete"])
+def test_graph_index_against_python_sets(kind):
+    g = tiny_graph(61, N=13, E=70, R=4, T=3, kind=kind)
+    ix = oracle.graph_index(g)
+    E, N, R, T = g["E"], g["N"], g["R"], g["T"]
+    src, dst, rel, nt = (list(map(int, g[k])) for k in ("src", "dst", "rel", "ntype"))
+    order = sorted(range(E), key=lambda e: (dst[e], rel[e], src[e], e))
+    assert list(ix["in_eid"]) == order
+    assert list(ix["in_src"]) == [src[e] for e in order]
+    assert list(ix["in_rel"]) == [rel[e] for e in order]
+    assert list(ix["dst_rowptr"]) == [sum(1 for e in range(E) if dst[e] < v) for v in range(N + 1)]
+    segs = sorted({(dst[e], rel[e]) for e in range(E)})
+    assert ix["U_dst"] == len(segs)
+    assert list(ix["seg_rel"]) == [r for _, r in segs]
+    assert list(ix["seg_ptr"]) == [sum(1 for e in range(E) if (dst[e], rel[e]) < s) for s in segs] + [E]
+    assert list(ix["dst_segptr"]) == [sum(1 for s in segs if s[0] < v) for v in range(N + 1)]
+    pairs = sorted({(rel[e], src[e]) for e in range(E)})
+    assert ix["U_src"] == len(pairs)
+    assert list(ix["uniq_src"]) == [s for _, s in pairs]
+    assert list(ix["uniq_rel_ptr"]) == [sum(1 for p in pairs if p[0] < r) for r in range(R + 1)]
+    pos = {p: i for i, p in enumerate(pairs)}
+    assert list(ix["edge2uniq"]) == [pos[(rel[e], src[e])] for e in order]
+    assert list(ix["ntype_perm"]) == sorted(range(N), key=lambda n: (nt[n], n))
+    assert list(ix["ntype_ptr"]) == [sum(1 for n in range(N) if nt[n] < t) for t in range(T + 1)]
+
+
+def test_compaction_counts_seven_to_five():
+    """Compact materialization keeps one row per unique (source, relation) pair:
+    a graph with 7 edges and 5 distinct pairs needs 5 rows instead of 7 (the
+    count the paper's compaction figure gives; the figure's graph itself is
+    not recoverable, so only the count is checked)."""
+    src = np.array([0, 0, 1, 1, 2, 2, 3], np.int32)
+    rel = np.array([0, 0, 0, 1, 1, 1, 0], np.int32)
+    dst = np.array([1, 2, 0, 3, 0, 3, 2], np.int32)
+    g = dict(N=4, E=7, R=2, T=1, src=src, dst=dst, rel=rel, ntype=np.zeros(4, np.int32))
+    ix = oracle.graph_index(g)
+    assert ix["U_src"] == 5 and g["E"] == 7
