@@ -1,0 +1,547 @@
+// api.cpp -- C ABI entry points of librgnn: argument checks, plan selection by
+// modelled HBM bytes, workspace carving and the kernel sequence of each layer.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "rgnn_internal.h"
+
+namespace rgnn {
+
+size_t hgt_lds_bytes(int R, int heads);
+rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
+                               const float *w_src, const float *w_dst, int d_in, int d_out,
+                               float slope, const float *saved, const float *G, float *dh,
+                               float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
+                               hipStream_t s, size_t *need);
+
+namespace {
+thread_local std::string g_err;
+}
+
+rgnn_status fail(rgnn_status st, const std::string &msg)
+{
+    g_err = msg;
+    return st;
+}
+
+rgnn_status hip_fail(hipError_t e, const char *what)
+{
+    g_err = std::string(what) + ": " + hipGetErrorString(e);
+    return RGNN_EDEVICE;
+}
+
+// ------------------------------------------------------------------ profiling
+namespace {
+struct ProfRec {
+    std::string name;
+    hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+}  // namespace
+
+LaunchScope::LaunchScope(const char *n, hipStream_t s) : name(n), stream(s), slot(-1)
+{
+    if (!g_prof_on) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    ProfRec r{n, nullptr, nullptr};
+    if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return;
+    if (hipEventRecord(r.a, s) != hipSuccess) return;
+    g_prof.push_back(r);
+    slot = (int)g_prof.size() - 1;
+}
+
+LaunchScope::~LaunchScope()
+{
+    if (slot < 0) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (slot < (int)g_prof.size()) (void)hipEventRecord(g_prof[slot].b, stream);
+}
+
+// ------------------------------------------------------------------ helpers
+namespace {
+
+inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
+
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base((char *)b) {}
+    template <class T>
+    T *take(size_t n)
+    {
+        T *p = base ? (T *)(base + off) : nullptr;
+        off += pad256(n * sizeof(T));
+        return p;
+    }
+};
+
+rgnn_status check_graph(const rgnn_graph *g)
+{
+    if (!g) return fail(RGNN_EINVAL, "graph is NULL");
+    if (g->device < 0) return fail(RGNN_EINVAL, "graph was created host-only");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != g->device)
+        return fail(RGNN_EINVAL, "graph lives on device " + std::to_string(g->device) +
+                                     " but the current device is " + std::to_string(dev));
+    return RGNN_OK;
+}
+
+bool dim_ok(int d) { return d == 64 || d == 128; }
+
+// ---- modelled HBM bytes of the two plans (gathered rows counted per edge) ----
+void plan_bytes(const rgnn_graph *g, int layer, int d_in, int d_out, int H, double *tf, double *af)
+{
+    const double E = (double)g->E, N = (double)g->N, U = (double)g->U_src, V = (double)g->V;
+    const double bi = 4.0 * d_in, bo = 4.0 * d_out;
+    if (layer == RGNN_LAYER_RGCN) {
+        *tf = U * (bi + bo) + E * (4 + bo) + V * 12 + N * bo;
+        *af = E * (4 + bi) + V * (bi + 12) + V * (bi + bo) + V * bo + N * bo;
+    } else {
+        *tf = U * (bi + bo + 4 * H) + E * (4 + bo + 4 * H) + V * 12 + N * (bi + bo + 8 * H);
+        *af = E * (4 + bi) + V * (bi + 20) + N * (bi + 8) + V * 8 + N * 8 + V * (bi + bo + 8) +
+              V * bo + N * bo;
+    }
+}
+
+int resolve_plan(const rgnn_graph *g, int layer, int d_in, int d_out, int H, int plan)
+{
+    if (plan != RGNN_PLAN_AUTO) return plan;
+    if (layer == RGNN_LAYER_RGAT && H != 1) return RGNN_PLAN_TRANSFORM_FIRST;
+    double tf, af;
+    plan_bytes(g, layer, d_in, d_out, H, &tf, &af);
+    return af < tf ? RGNN_PLAN_AGGREGATE_FIRST : RGNN_PLAN_TRANSFORM_FIRST;
+}
+
+// ---- workspace layouts ----
+struct RgcnWs { float *M, *partial, *S, *T; };
+size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *base, RgcnWs *w)
+{
+    Carver c(base);
+    RgcnWs x{};
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+        x.M = c.take<float>((size_t)g->U_src * d_out);
+        x.partial = c.take<float>((size_t)g->n_slots * (2 + d_out));
+    } else {
+        x.S = c.take<float>((size_t)g->V * d_in);
+        x.T = c.take<float>((size_t)g->V * d_out);
+    }
+    if (w) *w = x;
+    return c.off;
+}
+
+struct RgatWs { float *M, *atts, *wsp, *wtp, *partial, *S, *vstat, *T, *saved; };
+size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, void *base,
+                   RgatWs *w)
+{
+    Carver c(base);
+    RgatWs x{};
+    x.wsp = c.take<float>((size_t)g->R * H * d_in);
+    x.wtp = c.take<float>((size_t)g->R * H * d_in);
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+        x.M = c.take<float>((size_t)g->U_src * d_out);
+        x.atts = c.take<float>((size_t)g->U_src * H);
+        x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
+    } else {
+        x.S = c.take<float>((size_t)g->V * d_in);
+        x.vstat = c.take<float>((size_t)g->V * 2);
+        x.T = c.take<float>((size_t)g->V * d_out);
+        x.saved = c.take<float>((size_t)g->N * 2);
+    }
+    if (w) *w = x;
+    return c.off;
+}
+
+struct HgtWs { float *KV, *Q, *agg, *partial; };
+size_t hgt_layout(const rgnn_graph *g, int d, int H, void *base, HgtWs *w)
+{
+    Carver c(base);
+    HgtWs x{};
+    x.KV = c.take<float>((size_t)g->N * 2 * d);
+    x.Q = c.take<float>((size_t)g->N * d);
+    x.agg = c.take<float>((size_t)g->N * d);
+    x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d));
+    if (w) *w = x;
+    return c.off;
+}
+
+size_t segment_gemm_layout(int64_t M, int32_t T, void *base, Tile **tiles, int64_t *ntiles)
+{
+    // upper bound on the tile count: every type may add one partial tile
+    const int64_t n = (M + kGemmTileRows - 1) / kGemmTileRows + T;
+    Carver c(base);
+    Tile *t = c.take<Tile>((size_t)std::max<int64_t>(n, 1));
+    if (tiles) *tiles = t;
+    if (ntiles) *ntiles = n;
+    return c.off;
+}
+
+}  // namespace
+}  // namespace rgnn
+
+using namespace rgnn;
+
+extern "C" const char *rgnn_last_error(void) { return g_err.c_str(); }
+extern "C" const char *rgnn_version(void) { return "librgnn 0.1 (gfx950, fp32)"; }
+
+extern "C" rgnn_status rgnn_profile_enable(int32_t on)
+{
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on = on != 0;
+    return RGNN_OK;
+}
+
+extern "C" rgnn_status rgnn_profile_reset(void)
+{
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    for (auto &r : g_prof) {
+        (void)hipEventSynchronize(r.b);
+        (void)hipEventDestroy(r.a);
+        (void)hipEventDestroy(r.b);
+    }
+    g_prof.clear();
+    return RGNN_OK;
+}
+
+namespace {
+struct ProfAgg { std::string name; int64_t n; double ms; };
+std::vector<ProfAgg> prof_aggregate(rgnn_status *st)
+{
+    std::vector<ProfAgg> out;
+    *st = RGNN_OK;
+    for (auto &r : g_prof) {
+        hipError_t e = hipEventSynchronize(r.b);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+        if (e != hipSuccess) { *st = hip_fail(e, "profiling event"); return out; }
+        auto it = std::find_if(out.begin(), out.end(), [&](const ProfAgg &p) { return p.name == r.name; });
+        if (it == out.end()) out.push_back(ProfAgg{r.name, 1, ms});
+        else { it->n++; it->ms += ms; }
+    }
+    return out;
+}
+}  // namespace
+
+extern "C" rgnn_status rgnn_profile_count(int32_t *count)
+{
+    if (!count) return fail(RGNN_EINVAL, "count is NULL");
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    rgnn_status st;
+    auto agg = prof_aggregate(&st);
+    *count = (int32_t)agg.size();
+    return st;
+}
+
+extern "C" rgnn_status rgnn_profile_read(int32_t i, char *name, size_t name_bytes,
+                                         int64_t *launches, double *total_ms)
+{
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    rgnn_status st;
+    auto agg = prof_aggregate(&st);
+    if (st != RGNN_OK) return st;
+    if (i < 0 || i >= (int)agg.size()) return fail(RGNN_EINVAL, "profile index out of range");
+    if (name && name_bytes) {
+        std::snprintf(name, name_bytes, "%s", agg[i].name.c_str());
+    }
+    if (launches) *launches = agg[i].n;
+    if (total_ms) *total_ms = agg[i].ms;
+    return RGNN_OK;
+}
+
+// ------------------------------------------------------------------ planning
+extern "C" rgnn_status rgnn_select_plan(const rgnn_graph_t *g, int32_t layer, int32_t d_in,
+                                        int32_t d_out, int32_t heads, int32_t *plan,
+                                        double *bytes_tf, double *bytes_af)
+{
+    if (!g) return fail(RGNN_EINVAL, "graph is NULL");
+    if (layer != RGNN_LAYER_RGCN && layer != RGNN_LAYER_RGAT)
+        return fail(RGNN_EINVAL, "plans exist for RGCN and RGAT only");
+    if (heads <= 0) return fail(RGNN_EINVAL, "heads must be positive");
+    double tf, af;
+    plan_bytes(g, layer, d_in, d_out, heads, &tf, &af);
+    if (bytes_tf) *bytes_tf = tf;
+    if (bytes_af) *bytes_af = af;
+    if (plan) *plan = resolve_plan(g, layer, d_in, d_out, heads, RGNN_PLAN_AUTO);
+    return RGNN_OK;
+}
+
+extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer, int32_t d_in,
+                                           int32_t d_out, int32_t heads, int32_t plan,
+                                           size_t *bytes)
+{
+    if (!g || !bytes) return fail(RGNN_EINVAL, "NULL argument");
+    if (heads <= 0) return fail(RGNN_EINVAL, "heads must be positive");
+    if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
+    switch (layer) {
+    case RGNN_LAYER_RGCN:
+        *bytes = rgcn_layout(g, d_in, d_out, resolve_plan(g, layer, d_in, d_out, 1, plan), nullptr, nullptr);
+        return RGNN_OK;
+    case RGNN_LAYER_RGAT:
+        *bytes = rgat_layout(g, d_in, d_out, heads, resolve_plan(g, layer, d_in, d_out, heads, plan),
+                             nullptr, nullptr);
+        return RGNN_OK;
+    case RGNN_LAYER_HGT:
+        *bytes = hgt_layout(g, d_out, heads, nullptr, nullptr);
+        return RGNN_OK;
+    case RGNN_LAYER_RGAT_BACKWARD: {
+        size_t need = 0;
+        rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, nullptr,
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
+        *bytes = need;
+        return RGNN_OK;
+    }
+    default:
+        return fail(RGNN_EINVAL, "unknown layer");
+    }
+}
+
+// ------------------------------------------------------------------ RGCN
+extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W,
+                                    const float *W0, int32_t d_in, int32_t d_out, int32_t flags,
+                                    int32_t plan, float *out, void *ws, size_t ws_bytes,
+                                    void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !W || !out) return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (!dim_ok(d_in) || !dim_ok(d_out)) return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128");
+    if (flags & ~RGNN_FLAG_RELU) return fail(RGNN_EINVAL, "unknown RGCN flag");
+    if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
+    plan = resolve_plan(g, RGNN_LAYER_RGCN, d_in, d_out, 1, plan);
+    const size_t need = rgcn_layout(g, d_in, d_out, plan, nullptr, nullptr);
+    if (need && (!ws || ws_bytes < need))
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    RgcnWs w;
+    rgcn_layout(g, d_in, d_out, plan, ws, &w);
+    hipStream_t s = (hipStream_t)stream;
+    const int relu = (flags & RGNN_FLAG_RELU) ? 1 : 0;
+    const int relu_in_traversal = relu && !W0;
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+        // compact materialization: one message row per unique (src, rel) pair
+        GemmArgs ga;
+        ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
+        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
+        ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
+        ga.Y = w.M; ga.ldy = d_out;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        TravArgs ta;
+        ta.g = g; ta.M = w.M; ta.d = d_out; ta.out = out; ta.partial = w.partial;
+        ta.relu = relu_in_traversal;
+        if ((st = launch_rgcn_traverse_tf(ta, s)) != RGNN_OK) return st;
+        if ((st = launch_merge_partials(ta, 0, s)) != RGNN_OK) return st;
+    } else {
+        TravArgs ta;
+        ta.g = g; ta.h = h; ta.d = d_in; ta.S = w.S;
+        if ((st = launch_rgcn_traverse_af(ta, s)) != RGNN_OK) return st;
+        GemmArgs ga;
+        ga.X = w.S; ga.ldx = d_in; ga.gather = g->dev.vseg_byrel;
+        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
+        ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
+        ga.Y = w.T; ga.ldy = d_out; ga.scatter = g->dev.vseg_byrel;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_reduce(g, w.T, d_out, out, 0, relu_in_traversal, s)) != RGNN_OK) return st;
+    }
+    if (W0) {   // virtual self-loop h_v W0, accumulated into out (then the activation)
+        GemmArgs ga;
+        ga.X = h; ga.ldx = d_in; ga.W[0] = W0; ga.K = d_in; ga.Nc = d_out;
+        ga.tiles = g->dev.tiles_all; ga.ntiles = g->n_tiles_all;
+        ga.Y = out; ga.ldy = d_out;
+        ga.ep.accumulate = 1; ga.ep.relu = relu;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    }
+    return RGNN_OK;
+}
+
+// ------------------------------------------------------------------ RGAT
+extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
+                                    const float *w_src, const float *w_dst, int32_t d_in,
+                                    int32_t d_out, int32_t heads, float neg_slope,
+                                    int32_t softmax_scope, int32_t plan, float *out, float *saved,
+                                    void *ws, size_t ws_bytes, void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !W || !w_src || !w_dst || !out) return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (!dim_ok(d_in) || !dim_ok(d_out)) return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128");
+    if (heads <= 0 || d_out % heads) return fail(RGNN_EINVAL, "heads must divide d_out");
+    if ((d_out / heads) % 16) return fail(RGNN_EUNSUPPORTED, "d_out / heads must be a multiple of 16");
+    if (softmax_scope == RGNN_SOFTMAX_PER_DST_REL)
+        return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) is not implemented");
+    if (softmax_scope != RGNN_SOFTMAX_PER_DST) return fail(RGNN_EINVAL, "unknown softmax scope");
+    if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
+    if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
+    plan = resolve_plan(g, RGNN_LAYER_RGAT, d_in, d_out, heads, plan);
+    if (plan == RGNN_PLAN_AGGREGATE_FIRST && (heads != 1 || d_in != d_out))
+        return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs heads == 1 and d_in == d_out");
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST && d_in != d_out)
+        return fail(RGNN_EUNSUPPORTED, "RGAT needs d_in == d_out");
+    const size_t need = rgat_layout(g, d_in, d_out, heads, plan, nullptr, nullptr);
+    if (!ws || ws_bytes < need)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    RgatWs w;
+    rgat_layout(g, d_in, d_out, heads, plan, ws, &w);
+    hipStream_t s = (hipStream_t)stream;
+    // linear operator reordering: W_r w_dst[r] (and W_r w_src[r]) once per relation
+    if ((st = launch_reorder_vec(W, w_dst, g->R, d_in, d_out, heads, w.wtp, s)) != RGNN_OK) return st;
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+        GemmArgs ga;
+        ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
+        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
+        ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
+        ga.Y = w.M; ga.ldy = d_out;
+        ga.ep.dot_vec = w_src; ga.ep.dot_out = w.atts; ga.ep.dot_heads = heads;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        TravArgs ta;
+        ta.g = g; ta.h = h; ta.M = w.M; ta.atts = w.atts; ta.wtp = w.wtp;
+        ta.slope = neg_slope; ta.heads = heads; ta.d = d_out;
+        ta.out = out; ta.saved = saved; ta.partial = w.partial;
+        if ((st = launch_rgat_traverse_tf(ta, s)) != RGNN_OK) return st;
+        if ((st = launch_merge_partials(ta, 1, s)) != RGNN_OK) return st;
+    } else {
+        if ((st = launch_reorder_vec(W, w_src, g->R, d_in, d_out, 1, w.wsp, s)) != RGNN_OK) return st;
+        float *stats = saved ? saved : w.saved;
+        TravArgs ta;
+        ta.g = g; ta.h = h; ta.wsp = w.wsp; ta.wtp = w.wtp; ta.slope = neg_slope;
+        ta.heads = 1; ta.d = d_in; ta.S = w.S; ta.vstat = w.vstat; ta.saved = stats;
+        if ((st = launch_rgat_traverse_af(ta, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_stats(ta, s)) != RGNN_OK) return st;
+        GemmArgs ga;
+        ga.X = w.S; ga.ldx = d_in; ga.gather = g->dev.vseg_byrel;
+        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
+        ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
+        ga.Y = w.T; ga.ldy = d_out; ga.scatter = g->dev.vseg_byrel;
+        ga.ep.scale_mode = 1; ga.ep.seg_stat = w.vstat; ga.ep.row_dst = g->dev.vseg_dst;
+        ga.ep.dst_stat = stats;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_reduce(g, w.T, d_out, out, 0, 0, s)) != RGNN_OK) return st;
+    }
+    return RGNN_OK;
+}
+
+// ------------------------------------------------------------------ HGT
+extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk,
+                                   const float *Wq, const float *Wv, const float *Wa,
+                                   const float *Watt, const float *Wmsg, const float *mu,
+                                   int32_t d, int32_t heads, float att_scale, int32_t flags,
+                                   float *out, void *ws, size_t ws_bytes, void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !Wk || !Wq || !Wv || !Watt || !Wmsg || !mu || !out)
+        return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if ((flags & RGNN_FLAG_A_LINEAR) && !Wa) return fail(RGNN_EINVAL, "Wa is NULL");
+    if (flags & ~(RGNN_FLAG_RESIDUAL | RGNN_FLAG_A_LINEAR)) return fail(RGNN_EINVAL, "unknown HGT flag");
+    if (d != 64) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 64");
+    if (heads != 1 && heads != 2 && heads != 4) return fail(RGNN_EUNSUPPORTED, "HGT heads must be 1, 2 or 4");
+    if (!std::isfinite(att_scale)) return fail(RGNN_EINVAL, "att_scale must be finite");
+    const size_t need = hgt_layout(g, d, heads, nullptr, nullptr);
+    if (!ws || ws_bytes < need)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    HgtWs w;
+    hgt_layout(g, d, heads, ws, &w);
+    hipStream_t s = (hipStream_t)stream;
+    // K | V | Q of every node in one node-typed GEMM (segment MM over node types)
+    GemmArgs ga;
+    ga.X = h; ga.ldx = d; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
+    ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
+    ga.K = d; ga.Nc = 3 * d;
+    ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
+    ga.Y = w.KV; ga.ldy = 2 * d;
+    ga.ep.Y2 = w.Q; ga.ep.ldy2 = d; ga.ep.split = 2 * d;
+    if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    HgtArgs ha;
+    ha.g = g; ha.KV = w.KV; ha.Q = w.Q; ha.Watt = Watt; ha.Wmsg = Wmsg; ha.mu = mu;
+    ha.scale = att_scale; ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
+    if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
+    if ((st = launch_hgt_merge(ha, s)) != RGNN_OK) return st;
+    if (flags & RGNN_FLAG_A_LINEAR) {
+        GemmArgs gb;
+        gb.X = w.agg; gb.ldx = d; gb.gather = g->dev.ntype_perm; gb.scatter = g->dev.ntype_perm;
+        gb.W[0] = Wa; gb.K = d; gb.Nc = d;
+        gb.tiles = g->dev.tiles_nodes; gb.ntiles = g->n_tiles_nodes;
+        gb.Y = out; gb.ldy = d;
+        if (flags & RGNN_FLAG_RESIDUAL) { gb.ep.residual = h; gb.ep.ld_res = d; }
+        return launch_typed_gemm(gb, s);
+    }
+    if (flags & RGNN_FLAG_RESIDUAL) return launch_add(out, w.agg, h, g->N * d, s);
+    hipError_t e = hipMemcpyAsync(out, w.agg, (size_t)g->N * d * sizeof(float),
+                                  hipMemcpyDeviceToDevice, s);
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "hipMemcpyAsync");
+}
+
+// ------------------------------------------------------------------ RGAT backward
+extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, const float *W,
+                                     const float *w_src, const float *w_dst, int32_t d_in,
+                                     int32_t d_out, int32_t heads, float neg_slope,
+                                     const float *saved, const float *grad_out, float *grad_h,
+                                     float *grad_W, float *grad_w_src, float *grad_w_dst,
+                                     void *ws, size_t ws_bytes, void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !W || !w_src || !w_dst || !saved || !grad_out || !grad_h || !grad_W ||
+        !grad_w_src || !grad_w_dst)
+        return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (heads != 1) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports heads == 1");
+    if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d = 64");
+    if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
+    return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
+                              grad_h, grad_W, grad_w_src, grad_w_dst, ws, ws_bytes,
+                              (hipStream_t)stream, nullptr);
+}
+
+// ------------------------------------------------------------------ segment MM
+extern "C" rgnn_status rgnn_segment_gemm_workspace_size(int64_t M, int32_t num_types, size_t *bytes)
+{
+    if (!bytes || M < 0 || num_types <= 0) return fail(RGNN_EINVAL, "bad argument");
+    *bytes = segment_gemm_layout(M, num_types, nullptr, nullptr, nullptr);
+    return RGNN_OK;
+}
+
+extern "C" rgnn_status rgnn_segment_gemm(const float *X, int64_t ldx, const int32_t *gather,
+                                         const int64_t *type_ptr, int32_t num_types,
+                                         const float *W, int32_t K, int32_t Nc, float *Y,
+                                         int64_t ldy, const int32_t *scatter, void *ws,
+                                         size_t ws_bytes, void *stream)
+{
+    if (!X || !W || !Y || !type_ptr) return fail(RGNN_EINVAL, "NULL pointer");
+    if (num_types <= 0) return fail(RGNN_EINVAL, "num_types must be positive");
+    if (!((K == 64 || K == 128) && (Nc == 64 || Nc == 128)))
+        return fail(RGNN_EUNSUPPORTED, "K and Nc must be 64 or 128");
+    if (ldx < K || ldy < Nc) return fail(RGNN_EINVAL, "leading dimension too small");
+    if (type_ptr[0] != 0) return fail(RGNN_EINVAL, "type_ptr[0] must be 0");
+    for (int t = 0; t < num_types; ++t)
+        if (type_ptr[t + 1] < type_ptr[t]) return fail(RGNN_EINVAL, "type_ptr is not monotone");
+    const int64_t M = type_ptr[num_types];
+    if (M >= (int64_t(1) << 31) - 1) return fail(RGNN_ERANGE, "too many rows");
+    const size_t need = segment_gemm_layout(M, num_types, nullptr, nullptr, nullptr);
+    if (!ws || ws_bytes < need)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    std::vector<int32_t> tp(num_types + 1);
+    for (int t = 0; t <= num_types; ++t) tp[t] = (int32_t)type_ptr[t];
+    std::vector<Tile> tiles;
+    build_tiles(tp, kGemmTileRows, tiles);
+    Tile *dt = nullptr;
+    segment_gemm_layout(M, num_types, ws, &dt, nullptr);
+    hipStream_t s = (hipStream_t)stream;
+    if (tiles.empty()) return RGNN_OK;
+    // The tile table is enqueued on the stream; the host vector must outlive the
+    // copy, so this call waits for it (a few KB).
+    hipError_t e = hipMemcpyAsync(dt, tiles.data(), tiles.size() * sizeof(Tile),
+                                  hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "tile table upload");
+    GemmArgs ga;
+    ga.X = X; ga.ldx = ldx; ga.gather = gather; ga.W[0] = W; ga.K = K; ga.Nc = Nc;
+    ga.tiles = dt; ga.ntiles = (int64_t)tiles.size();
+    ga.Y = Y; ga.ldy = ldy; ga.scatter = scatter;
+    return launch_typed_gemm(ga, s);
+}

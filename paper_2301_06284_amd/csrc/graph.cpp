@@ -1,0 +1,420 @@
+// graph.cpp -- host-side graph preprocessing (the COO -> CSR conversion and the
+// index construction the paper emits as preprocessing code, Section "Code
+// Generation"), device upload, info and export.
+//
+// Every order is fully specified so the arrays are reproducible bit for bit:
+//   in-edges      sorted by (dst, rel, src, original edge id)
+//   segments      maximal runs of equal (dst, rel) in that order
+//   compact map   unique (rel, src) pairs in ascending (rel, src) order
+//                 (Section "Compact Tensor Materialization": one row per pair)
+//   node types    node ids stable-sorted by type (segment MM over node types)
+// All sorts are stable LSD counting sorts, O(E + N + R) each.
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "rgnn_internal.h"
+
+namespace rgnn {
+
+namespace {
+
+// Stable counting sort of `perm` by key[perm[i]] in [0, K).
+void counting_sort(std::vector<int32_t> &perm, const int32_t *key, int64_t K,
+                   std::vector<int32_t> &tmp, std::vector<int64_t> &cnt)
+{
+    cnt.assign((size_t)K + 1, 0);
+    for (int32_t e : perm) cnt[(size_t)key[e] + 1]++;
+    for (int64_t k = 0; k < K; ++k) cnt[k + 1] += cnt[k];
+    tmp.resize(perm.size());
+    for (int32_t e : perm) tmp[(size_t)cnt[key[e]]++] = e;
+    perm.swap(tmp);
+}
+
+}  // namespace
+
+void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vector<Tile> &out)
+{
+    out.clear();
+    const int ntypes = (int)type_ptr.size() - 1;
+    for (int t = 0; t < ntypes; ++t)
+        for (int32_t r0 = type_ptr[t]; r0 < type_ptr[t + 1]; r0 += tile_rows)
+            out.push_back(Tile{t, r0, std::min<int32_t>(tile_rows, type_ptr[t + 1] - r0), 0});
+}
+
+rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
+                             const int32_t *dst, const int32_t *rel, const int32_t *ntype,
+                             rgnn_graph *g)
+{
+    HostIndex &x = g->host;
+    g->N = N; g->E = E; g->R = R; g->T = T;
+    const int C = g->chunk;
+    try {
+        // ---- in-edges by (dst, rel, src, eid): LSD passes src, rel, dst ----
+        std::vector<int32_t> perm((size_t)E), tmp;
+        std::vector<int64_t> cnt;
+        for (int64_t e = 0; e < E; ++e) perm[e] = (int32_t)e;
+        counting_sort(perm, src, N, tmp, cnt);
+        counting_sort(perm, rel, R, tmp, cnt);
+        counting_sort(perm, dst, N, tmp, cnt);
+        x.in_eid = perm;
+        x.in_src.resize(E); x.in_rel.resize(E);
+        for (int64_t i = 0; i < E; ++i) {
+            x.in_src[i] = src[perm[i]];
+            x.in_rel[i] = rel[perm[i]];
+        }
+        x.rowptr.assign((size_t)N + 1, 0);
+        for (int64_t e = 0; e < E; ++e) x.rowptr[(size_t)dst[e] + 1]++;
+        g->max_in_deg = 0; g->n_empty = 0;
+        for (int64_t v = 0; v < N; ++v) {
+            const int32_t deg = x.rowptr[v + 1];
+            g->max_in_deg = std::max<int64_t>(g->max_in_deg, deg);
+            g->n_empty += deg == 0;
+            x.rowptr[v + 1] += x.rowptr[v];
+        }
+        // ---- (dst, rel) segments ----
+        x.seg_ptr.clear(); x.seg_rel.clear();
+        x.dst_segptr.assign((size_t)N + 1, 0);
+        for (int64_t v = 0; v < N; ++v) {
+            for (int32_t i = x.rowptr[v]; i < x.rowptr[v + 1]; ++i) {
+                if (i == x.rowptr[v] || x.in_rel[i] != x.in_rel[i - 1]) {
+                    x.seg_ptr.push_back(i);
+                    x.seg_rel.push_back(x.in_rel[i]);
+                }
+            }
+            x.dst_segptr[v + 1] = (int32_t)x.seg_ptr.size();
+        }
+        g->U_dst = (int64_t)x.seg_ptr.size();
+        x.seg_ptr.push_back((int32_t)E);
+        // ---- compact (rel, src) map: LSD passes src, rel over edge ids ----
+        for (int64_t e = 0; e < E; ++e) perm[e] = (int32_t)e;
+        counting_sort(perm, src, N, tmp, cnt);
+        counting_sort(perm, rel, R, tmp, cnt);
+        std::vector<int32_t> pair_of((size_t)E);
+        x.uniq_src.clear();
+        x.uniq_rel_ptr.assign((size_t)R + 1, 0);
+        for (int64_t i = 0; i < E; ++i) {
+            const int32_t e = perm[i];
+            if (i == 0 || rel[e] != rel[perm[i - 1]] || src[e] != src[perm[i - 1]]) {
+                x.uniq_src.push_back(src[e]);
+                x.uniq_rel_ptr[(size_t)rel[e] + 1]++;
+            }
+            pair_of[e] = (int32_t)x.uniq_src.size() - 1;
+        }
+        for (int32_t r = 0; r < R; ++r) x.uniq_rel_ptr[r + 1] += x.uniq_rel_ptr[r];
+        g->U_src = (int64_t)x.uniq_src.size();
+        x.e2u.resize(E);
+        for (int64_t i = 0; i < E; ++i) x.e2u[i] = pair_of[x.in_eid[i]];
+        // ---- node-type segments ----
+        std::vector<int32_t> zeros;
+        if (!ntype) { zeros.assign((size_t)N, 0); ntype = zeros.data(); }
+        std::vector<int32_t> nperm((size_t)N);
+        for (int64_t n = 0; n < N; ++n) nperm[n] = (int32_t)n;
+        counting_sort(nperm, ntype, T, tmp, cnt);
+        x.ntype_perm = nperm;
+        x.ntype_ptr.assign((size_t)T + 1, 0);
+        for (int64_t n = 0; n < N; ++n) x.ntype_ptr[(size_t)ntype[n] + 1]++;
+        for (int32_t t = 0; t < T; ++t) x.ntype_ptr[t + 1] += x.ntype_ptr[t];
+
+        // ---- virtual segments: segments cut into pieces of at most C edges ----
+        x.vseg_ptr.clear(); x.vseg_rel.clear(); x.vseg_dst.clear(); x.vseg_cnt.clear();
+        x.dst_vsegptr.assign((size_t)N + 1, 0);
+        for (int64_t v = 0; v < N; ++v) {
+            for (int32_t s = x.dst_segptr[v]; s < x.dst_segptr[v + 1]; ++s) {
+                const int32_t b = x.seg_ptr[s], e = x.seg_ptr[s + 1];
+                for (int32_t p = b; p < e; p += C) {
+                    x.vseg_ptr.push_back(p);
+                    x.vseg_rel.push_back(x.seg_rel[s]);
+                    x.vseg_dst.push_back((int32_t)v);
+                    x.vseg_cnt.push_back(e - b);
+                }
+            }
+            x.dst_vsegptr[v + 1] = (int32_t)x.vseg_ptr.size();
+        }
+        g->V = (int64_t)x.vseg_ptr.size();
+        x.vseg_ptr.push_back((int32_t)E);
+        // vsegs grouped by relation (stable: (rel, dst) order) for the typed GEMMs
+        std::vector<int32_t> vperm((size_t)g->V);
+        for (int64_t i = 0; i < g->V; ++i) vperm[i] = (int32_t)i;
+        counting_sort(vperm, x.vseg_rel.data(), R, tmp, cnt);
+        x.vseg_byrel = vperm;
+        x.rel_vsegptr.assign((size_t)R + 1, 0);
+        for (int64_t i = 0; i < g->V; ++i) x.rel_vsegptr[(size_t)x.vseg_rel[i] + 1]++;
+        for (int32_t r = 0; r < R; ++r) x.rel_vsegptr[r + 1] += x.rel_vsegptr[r];
+        x.vsegdst_byrel.resize((size_t)g->V);
+        for (int64_t i = 0; i < g->V; ++i) x.vsegdst_byrel[i] = x.vseg_dst[x.vseg_byrel[i]];
+
+        // ---- traversal work items ----
+        x.items.clear(); x.item_slot.clear(); x.split_dst.clear();
+        x.split_slotptr.assign(1, 0);
+        int32_t slots = 0;
+        int64_t v = 0;
+        auto deg = [&](int64_t u) { return x.rowptr[u + 1] - x.rowptr[u]; };
+        while (v < N) {
+            if (deg(v) > C) {
+                int32_t s = x.dst_vsegptr[v];
+                const int32_t se = x.dst_vsegptr[v + 1];
+                while (s < se) {
+                    const int32_t s0 = s;
+                    int32_t tot = 0;
+                    while (s < se && (s == s0 || tot + (x.vseg_ptr[s + 1] - x.vseg_ptr[s]) <= C)) {
+                        tot += x.vseg_ptr[s + 1] - x.vseg_ptr[s];
+                        ++s;
+                    }
+                    x.items.push_back(Item{(int32_t)v, (int32_t)v + 1, s0, s});
+                    x.item_slot.push_back(slots++);
+                }
+                x.split_dst.push_back((int32_t)v);
+                x.split_slotptr.push_back(slots);
+                ++v;
+            } else {
+                const int64_t v0 = v;
+                int64_t tot = 0;
+                while (v < N && deg(v) <= C && tot + deg(v) <= C && v - v0 < kMaxDstPerItem) {
+                    tot += deg(v);
+                    ++v;
+                }
+                x.items.push_back(Item{(int32_t)v0, (int32_t)v, x.dst_vsegptr[v0], x.dst_vsegptr[v]});
+                x.item_slot.push_back(-1);
+            }
+        }
+        g->n_items = (int64_t)x.items.size();
+        g->n_split = (int64_t)x.split_dst.size();
+        g->n_slots = slots;
+
+        // ---- GEMM tile tables ----
+        build_tiles(x.uniq_rel_ptr, kGemmTileRows, x.tiles_pairs);
+        build_tiles(x.rel_vsegptr, kGemmTileRows, x.tiles_vsegs);
+        build_tiles(x.ntype_ptr, kGemmTileRows, x.tiles_nodes);
+        std::vector<int32_t> all{0, (int32_t)N};
+        build_tiles(all, kGemmTileRows, x.tiles_all);
+        g->n_tiles_pairs = (int64_t)x.tiles_pairs.size();
+        g->n_tiles_vsegs = (int64_t)x.tiles_vsegs.size();
+        g->n_tiles_nodes = (int64_t)x.tiles_nodes.size();
+        g->n_tiles_all = (int64_t)x.tiles_all.size();
+        build_tiles(x.rel_vsegptr, bwd_outer_rows(), x.tiles_outer);
+        g->n_tiles_outer = (int64_t)x.tiles_outer.size();
+        x.rel_chunkptr.assign((size_t)R + 1, 0);
+        for (const Tile &t : x.tiles_outer) x.rel_chunkptr[(size_t)t.type + 1]++;
+        for (int32_t r = 0; r < R; ++r) x.rel_chunkptr[r + 1] += x.rel_chunkptr[r];
+    } catch (const std::bad_alloc &) {
+        return fail(RGNN_ENOMEM, "host allocation failed while building the graph index");
+    }
+    return RGNN_OK;
+}
+
+namespace {
+
+template <class T>
+size_t padded(size_t n) { return (n * sizeof(T) + 255) & ~size_t(255); }
+
+rgnn_status upload(rgnn_graph *g, hipStream_t s)
+{
+    HostIndex &x = g->host;
+    DeviceIndex &d = g->dev;
+    struct Part { void **dst; const void *src; size_t bytes; };
+    std::vector<Part> parts;
+    auto add32 = [&](int32_t **p, const std::vector<int32_t> &v) {
+        parts.push_back(Part{(void **)p, v.data(), v.size() * sizeof(int32_t)});
+    };
+    add32(&d.rowptr, x.rowptr); add32(&d.in_src, x.in_src); add32(&d.in_rel, x.in_rel);
+    add32(&d.in_eid, x.in_eid); add32(&d.seg_ptr, x.seg_ptr); add32(&d.seg_rel, x.seg_rel);
+    add32(&d.dst_segptr, x.dst_segptr); add32(&d.uniq_src, x.uniq_src);
+    add32(&d.uniq_rel_ptr, x.uniq_rel_ptr); add32(&d.e2u, x.e2u);
+    add32(&d.ntype_perm, x.ntype_perm); add32(&d.ntype_ptr, x.ntype_ptr);
+    add32(&d.vseg_ptr, x.vseg_ptr); add32(&d.vseg_rel, x.vseg_rel); add32(&d.vseg_dst, x.vseg_dst);
+    add32(&d.vseg_cnt, x.vseg_cnt); add32(&d.dst_vsegptr, x.dst_vsegptr);
+    add32(&d.vseg_byrel, x.vseg_byrel); add32(&d.rel_vsegptr, x.rel_vsegptr);
+    add32(&d.vsegdst_byrel, x.vsegdst_byrel); add32(&d.rel_chunkptr, x.rel_chunkptr);
+    add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
+    add32(&d.split_slotptr, x.split_slotptr);
+    parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
+    parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_nodes, x.tiles_nodes.data(), x.tiles_nodes.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
+    size_t total = 0;
+    for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
+    total = std::max<size_t>(total, 256);
+    hipError_t e = hipMalloc(&d.base, total);
+    if (e != hipSuccess) {
+        d.base = nullptr;
+        return e == hipErrorOutOfMemory ? fail(RGNN_ENOMEM, "hipMalloc of the graph index failed")
+                                        : hip_fail(e, "hipMalloc");
+    }
+    d.bytes = total;
+    size_t off = 0;
+    for (auto &p : parts) {
+        *p.dst = (char *)d.base + off;
+        if (p.bytes) {
+            e = hipMemcpyAsync(*p.dst, p.src, p.bytes, hipMemcpyHostToDevice, s);
+            if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (graph upload)");
+        }
+        off += (p.bytes + 255) & ~size_t(255);
+    }
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize (graph upload)");
+    return RGNN_OK;
+}
+
+rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
+                          const int32_t *dst, const int32_t *rel, const int32_t *ntype,
+                          int32_t flags, void *stream, rgnn_graph_t **out)
+{
+    if (!out) return fail(RGNN_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (N < 0 || E < 0) return fail(RGNN_EINVAL, "negative node or edge count");
+    if (N >= (int64_t(1) << 31) - 1 || E >= (int64_t(1) << 31) - 1)
+        return fail(RGNN_ERANGE, "node and edge counts must be below 2^31 - 1");
+    if (R <= 0 || T <= 0) return fail(RGNN_EINVAL, "num_rels and num_ntypes must be positive");
+    if (E > 0 && (!src || !dst || !rel)) return fail(RGNN_EINVAL, "NULL edge array");
+    if (flags & ~RGNN_GRAPH_HOST_ONLY) return fail(RGNN_EINVAL, "unknown graph flag");
+    for (int64_t e = 0; e < E; ++e) {
+        if (src[e] < 0 || src[e] >= N || dst[e] < 0 || dst[e] >= N)
+            return fail(RGNN_ERANGE, "edge " + std::to_string(e) + ": node id out of range");
+        if (rel[e] < 0 || rel[e] >= R)
+            return fail(RGNN_ERANGE, "edge " + std::to_string(e) + ": relation out of range");
+    }
+    if (ntype)
+        for (int64_t n = 0; n < N; ++n)
+            if (ntype[n] < 0 || ntype[n] >= T)
+                return fail(RGNN_ERANGE, "node " + std::to_string(n) + ": node type out of range");
+    rgnn_graph *g = new (std::nothrow) rgnn_graph();
+    if (!g) return fail(RGNN_ENOMEM, "host allocation failed");
+    rgnn_status st = build_host_index(N, T, R, E, src, dst, rel, ntype, g);
+    if (st != RGNN_OK) { delete g; return st; }
+    if (!(flags & RGNN_GRAPH_HOST_ONLY)) {
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) { delete g; return hip_fail(e, "hipGetDevice"); }
+        g->device = dev;
+        st = upload(g, (hipStream_t)stream);
+        if (st != RGNN_OK) {
+            if (g->dev.base) (void)hipFree(g->dev.base);
+            delete g;
+            return st;
+        }
+        // The device copy is authoritative; drop the large host arrays.
+        HostIndex empty;
+        g->host.in_src.swap(empty.in_src); g->host.in_rel.swap(empty.in_rel);
+        g->host.in_eid.swap(empty.in_eid); g->host.e2u.swap(empty.e2u);
+    }
+    *out = g;
+    return RGNN_OK;
+}
+
+}  // namespace
+}  // namespace rgnn
+
+using namespace rgnn;
+
+extern "C" rgnn_status rgnn_graph_create_coo(int64_t num_nodes, int32_t num_ntypes,
+                                             int32_t num_rels, int64_t num_edges,
+                                             const int32_t *src, const int32_t *dst,
+                                             const int32_t *rel, const int32_t *ntype,
+                                             int32_t flags, void *stream, rgnn_graph_t **out)
+{
+    return create_common(num_nodes, num_ntypes, num_rels, num_edges, src, dst, rel, ntype, flags,
+                         stream, out);
+}
+
+extern "C" rgnn_status rgnn_graph_create_csr(int64_t num_nodes, int32_t num_ntypes,
+                                             int32_t num_rels, const int64_t *dst_rowptr,
+                                             const int32_t *col_src, const int32_t *rel,
+                                             const int32_t *ntype, int32_t flags, void *stream,
+                                             rgnn_graph_t **out)
+{
+    if (!out) return fail(RGNN_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (num_nodes < 0) return fail(RGNN_EINVAL, "negative node count");
+    if (!dst_rowptr) return fail(RGNN_EINVAL, "dst_rowptr is NULL");
+    if (dst_rowptr[0] != 0) return fail(RGNN_EINVAL, "dst_rowptr[0] must be 0");
+    for (int64_t v = 0; v < num_nodes; ++v)
+        if (dst_rowptr[v + 1] < dst_rowptr[v])
+            return fail(RGNN_EINVAL, "dst_rowptr is not monotone at " + std::to_string(v));
+    const int64_t E = dst_rowptr[num_nodes];
+    if (E >= (int64_t(1) << 31) - 1) return fail(RGNN_ERANGE, "edge count must be below 2^31 - 1");
+    std::vector<int32_t> dst;
+    try {
+        dst.resize((size_t)E);
+    } catch (const std::bad_alloc &) {
+        return fail(RGNN_ENOMEM, "host allocation failed");
+    }
+    for (int64_t v = 0; v < num_nodes; ++v)
+        for (int64_t i = dst_rowptr[v]; i < dst_rowptr[v + 1]; ++i) dst[i] = (int32_t)v;
+    return create_common(num_nodes, num_ntypes, num_rels, E, col_src, dst.data(), rel, ntype,
+                         flags, stream, out);
+}
+
+extern "C" rgnn_status rgnn_graph_destroy(rgnn_graph_t *g)
+{
+    if (!g) return RGNN_OK;
+    if (g->dev.base) {
+        int cur = 0;
+        (void)hipGetDevice(&cur);
+        if (cur != g->device) (void)hipSetDevice(g->device);
+        hipError_t e = hipFree(g->dev.base);
+        if (cur != g->device) (void)hipSetDevice(cur);
+        g->dev.base = nullptr;
+        if (e != hipSuccess) { delete g; return hip_fail(e, "hipFree"); }
+    }
+    delete g;
+    return RGNN_OK;
+}
+
+extern "C" rgnn_status rgnn_graph_info(const rgnn_graph_t *g, rgnn_graph_info_t *info)
+{
+    if (!g || !info) return fail(RGNN_EINVAL, "NULL argument");
+    info->num_nodes = g->N;
+    info->num_edges = g->E;
+    info->num_rels = g->R;
+    info->num_ntypes = g->T;
+    info->num_src_pairs = g->U_src;
+    info->num_dst_segments = g->U_dst;
+    info->max_in_degree = g->max_in_deg;
+    info->num_empty_dst = g->n_empty;
+    info->num_vsegs = g->V;
+    info->num_items = g->n_items;
+    info->num_split_dst = g->n_split;
+    info->chunk_edges = g->chunk;
+    info->device = g->device;
+    return RGNN_OK;
+}
+
+extern "C" rgnn_status rgnn_graph_export(const rgnn_graph_t *g, int32_t kind, void *dst,
+                                         size_t bytes)
+{
+    if (!g || !dst) return fail(RGNN_EINVAL, "NULL argument");
+    const HostIndex &x = g->host;
+    const DeviceIndex &d = g->dev;
+    const std::vector<int32_t> *hv = nullptr;
+    const int32_t *dp = nullptr;
+    size_t n = 0;
+    switch (kind) {
+    case RGNN_IDX_DST_ROWPTR: hv = &x.rowptr; dp = d.rowptr; n = (size_t)g->N + 1; break;
+    case RGNN_IDX_IN_SRC: hv = &x.in_src; dp = d.in_src; n = (size_t)g->E; break;
+    case RGNN_IDX_IN_REL: hv = &x.in_rel; dp = d.in_rel; n = (size_t)g->E; break;
+    case RGNN_IDX_IN_EID: hv = &x.in_eid; dp = d.in_eid; n = (size_t)g->E; break;
+    case RGNN_IDX_SEG_PTR: hv = &x.seg_ptr; dp = d.seg_ptr; n = (size_t)g->U_dst + 1; break;
+    case RGNN_IDX_SEG_REL: hv = &x.seg_rel; dp = d.seg_rel; n = (size_t)g->U_dst; break;
+    case RGNN_IDX_DST_SEGPTR: hv = &x.dst_segptr; dp = d.dst_segptr; n = (size_t)g->N + 1; break;
+    case RGNN_IDX_UNIQ_SRC: hv = &x.uniq_src; dp = d.uniq_src; n = (size_t)g->U_src; break;
+    case RGNN_IDX_UNIQ_REL_PTR: hv = &x.uniq_rel_ptr; dp = d.uniq_rel_ptr; n = (size_t)g->R + 1; break;
+    case RGNN_IDX_EDGE2UNIQ: hv = &x.e2u; dp = d.e2u; n = (size_t)g->E; break;
+    case RGNN_IDX_NTYPE_PERM: hv = &x.ntype_perm; dp = d.ntype_perm; n = (size_t)g->N; break;
+    case RGNN_IDX_NTYPE_PTR: hv = &x.ntype_ptr; dp = d.ntype_ptr; n = (size_t)g->T + 1; break;
+    default: return fail(RGNN_EINVAL, "unknown index kind " + std::to_string(kind));
+    }
+    if (bytes < n * sizeof(int32_t))
+        return fail(RGNN_EINVAL, "export buffer too small: need " +
+                                     std::to_string(n * sizeof(int32_t)) + " bytes");
+    if (n == 0) return RGNN_OK;
+    if (g->device < 0) {
+        std::memcpy(dst, hv->data(), n * sizeof(int32_t));
+        return RGNN_OK;
+    }
+    hipError_t e = hipMemcpy(dst, dp, n * sizeof(int32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (export)");
+    return RGNN_OK;
+}

@@ -1,0 +1,226 @@
+// rgnn_internal.h -- shared definitions of librgnn (host + device code).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "rgnn.h"
+
+namespace rgnn {
+
+// Maximum in-edges one traversal work item handles.  Destinations with more
+// in-edges are split into several items whose partial softmax states are merged.
+constexpr int kChunkEdges = 64;
+// Maximum destinations bundled into one work item.
+constexpr int kMaxDstPerItem = 32;
+// Rows of one typed-GEMM tile (a tile never mixes weight types).
+constexpr int kGemmTileRows = 128;
+
+struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
+    int32_t type, row0, rows, pad;
+};
+
+struct Item {          // one traversal work item
+    int32_t dst0, dst1;   // destinations [dst0, dst1)
+    int32_t vs0, vs1;     // virtual segments [vs0, vs1) (subset of the destinations' ones)
+};
+
+// Host copy of every index array (kept for host-only graphs and while building).
+struct HostIndex {
+    std::vector<int32_t> rowptr, in_src, in_rel, in_eid;
+    std::vector<int32_t> seg_ptr, seg_rel, dst_segptr;
+    std::vector<int32_t> uniq_src, uniq_rel_ptr, e2u;
+    std::vector<int32_t> ntype_perm, ntype_ptr;
+    // scheduling
+    std::vector<int32_t> vseg_ptr, vseg_rel, vseg_dst, vseg_cnt, dst_vsegptr;
+    std::vector<int32_t> vseg_byrel, rel_vsegptr, vsegdst_byrel;
+    std::vector<Item> items;
+    std::vector<int32_t> item_slot, split_dst, split_slotptr;
+    std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
+    std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
+};
+
+// Device copies (one allocation, carved).
+struct DeviceIndex {
+    void *base = nullptr;
+    size_t bytes = 0;
+    int32_t *rowptr = nullptr, *in_src = nullptr, *in_rel = nullptr, *in_eid = nullptr;
+    int32_t *seg_ptr = nullptr, *seg_rel = nullptr, *dst_segptr = nullptr;
+    int32_t *uniq_src = nullptr, *uniq_rel_ptr = nullptr, *e2u = nullptr;
+    int32_t *ntype_perm = nullptr, *ntype_ptr = nullptr;
+    int32_t *vseg_ptr = nullptr, *vseg_rel = nullptr, *vseg_dst = nullptr, *vseg_cnt = nullptr;
+    int32_t *dst_vsegptr = nullptr, *vseg_byrel = nullptr, *rel_vsegptr = nullptr;
+    int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr;
+    Item *items = nullptr;
+    int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
+    Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
+         *tiles_all = nullptr, *tiles_outer = nullptr;
+};
+
+}  // namespace rgnn
+
+struct rgnn_graph {
+    int64_t N = 0, E = 0;
+    int32_t R = 0, T = 0;
+    int64_t U_src = 0, U_dst = 0, V = 0;
+    int64_t n_items = 0, n_split = 0, n_slots = 0;
+    int64_t max_in_deg = 0, n_empty = 0;
+    int32_t chunk = rgnn::kChunkEdges;
+    int32_t device = -1;
+    int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
+    int64_t n_tiles_outer = 0;
+    rgnn::HostIndex host;
+    rgnn::DeviceIndex dev;
+};
+
+namespace rgnn {
+
+// ---- error reporting (api.cpp) ----
+rgnn_status fail(rgnn_status st, const std::string &msg);
+rgnn_status hip_fail(hipError_t e, const char *what);
+
+// ---- graph building (graph.cpp) ----
+rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
+                             const int32_t *dst, const int32_t *rel, const int32_t *ntype,
+                             rgnn_graph *g);
+void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vector<Tile> &out);
+int bwd_outer_rows();
+rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s);
+
+// ---- profiling (api.cpp) ----
+struct LaunchScope {   // records a hipEvent pair around one kernel launch when profiling
+    LaunchScope(const char *name, hipStream_t s);
+    ~LaunchScope();
+    const char *name;
+    hipStream_t stream;
+    int slot;
+};
+
+// ---- kernel launchers (device .hip files) ----
+struct GemmEpilogue {
+    // Optional per-row scale of the A rows (Section "Operator-Specific Schedule":
+    // a per-row scalar applied to the tiles of matrix A).  scale_mode:
+    //   0 none; 1 row scale = exp(seg_max[r] - dst_max[dst]) / dst_sum[dst]
+    int scale_mode = 0;
+    const float *seg_stat = nullptr;   // [rows, 2] (max, sum) per GEMM row (by scatter id)
+    const int32_t *row_dst = nullptr;  // destination of each GEMM row (by scatter id)
+    const float *dst_stat = nullptr;   // [N, 2] (max, sum)
+    // Optional row dot products of the output with a per-type vector, written to
+    // dot_out[scatter_row * heads + head] (heads split the output columns).
+    const float *dot_vec = nullptr;    // [types, Nc]
+    float *dot_out = nullptr;
+    int dot_heads = 1;
+    // Optional residual: Y[row] += res[row] (same row index as the output).
+    const float *residual = nullptr;
+    int64_t ld_res = 0;
+    int accumulate = 0;                // Y[row] += result instead of =
+    int relu = 0;                      // apply max(0, .) after everything
+    // Second output for columns >= split (split == Nc: unused).
+    float *Y2 = nullptr;
+    int64_t ldy2 = 0;
+    int split = 0;
+};
+
+struct GemmArgs {
+    const float *X = nullptr;   int64_t ldx = 0;
+    const int32_t *gather = nullptr;     // row -> X row (NULL: identity)
+    const float *W[3] = {nullptr, nullptr, nullptr};   // column parts, each [types, K, Np]
+    int nparts = 1;
+    int trans_b = 0;                     // B = W[type]^T (W stored [types, Nc, K])
+    int K = 0, Nc = 0;
+    const Tile *tiles = nullptr;   int64_t ntiles = 0;
+    float *Y = nullptr;   int64_t ldy = 0;
+    const int32_t *scatter = nullptr;    // row -> Y row (NULL: identity)
+    GemmEpilogue ep;
+};
+rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s);
+
+// Reordered attention vectors: out[r, k, :] = W_r[:, k-cols] v[r, k-cols]
+rgnn_status launch_reorder_vec(const float *W, const float *v, int R, int d_in, int d_out,
+                               int heads, float *out, hipStream_t s);
+
+struct TravArgs {
+    const rgnn_graph *g = nullptr;
+    const float *h = nullptr;            // node features [N, d_in]
+    const float *M = nullptr;            // compact messages [U_src, d_out] (transform-first)
+    const float *atts = nullptr;         // [U_src, heads] (transform-first RGAT)
+    const float *wsp = nullptr;          // [R, heads, d_in] reordered w_src (aggregate-first)
+    const float *wtp = nullptr;          // [R, heads, d_in] reordered w_dst
+    float slope = 0.2f;
+    int heads = 1;
+    int d = 64;
+    float *out = nullptr;                // [N, d]
+    float *saved = nullptr;              // [N, heads, 2] or NULL
+    float *partial = nullptr;            // [slots, 2*heads + d]
+    float *S = nullptr;                  // aggregate-first: [V, d] per-vseg sums
+    float *vstat = nullptr;              // aggregate-first: [V, 2] per-vseg (max, sum)
+    int relu = 0;
+};
+rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s);
+rgnn_status launch_rgcn_traverse_af(const TravArgs &a, hipStream_t s);
+rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s);
+rgnn_status launch_rgat_traverse_af(const TravArgs &a, hipStream_t s);
+rgnn_status launch_merge_partials(const TravArgs &a, int softmax, hipStream_t s);
+rgnn_status launch_vseg_stats(const TravArgs &a, hipStream_t s);
+rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
+                               int accumulate, int relu, hipStream_t s);
+rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);
+rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
+
+struct HgtArgs {
+    const rgnn_graph *g = nullptr;
+    const float *KV = nullptr;     // [N, 2d]: K then V per node
+    const float *Q = nullptr;      // [N, d]
+    const float *Watt = nullptr, *Wmsg = nullptr, *mu = nullptr;
+    float scale = 0.25f;
+    int heads = 4;
+    int d = 64;
+    float *agg = nullptr;          // [N, d]
+    float *partial = nullptr;      // [slots, 2*heads + d]
+};
+rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
+rgnn_status launch_hgt_merge(const HgtArgs &a, hipStream_t s);
+
+struct BwdArgs {
+    const rgnn_graph *g = nullptr;
+    const float *h = nullptr, *W = nullptr, *w_src = nullptr, *w_dst = nullptr;
+    const float *wsp = nullptr, *wtp = nullptr;   // reordered [R, d_in]
+    const float *saved = nullptr;                 // [N, 2]
+    const float *G = nullptr;                     // grad_out [N, d_out]
+    const float *dS = nullptr;                    // [V, d_in]  G_v W_r^T per vseg
+    float slope = 0.2f;
+    int d = 64;
+    float *Sa = nullptr;          // [V, d_in]  sum alpha h_u per vseg
+    float *ssum = nullptr;        // [slots] partial s_v for split destinations
+    float *sv = nullptr;          // [N] s_v
+    float *dh = nullptr;          // [N, d_in] (atomics; zeroed before)
+    float *acc_ws = nullptr;      // [copies, R, d_in] privatized dws' accumulators
+    float *acc_wt = nullptr;      // [copies, R, d_in] privatized dwt' accumulators
+    int copies = 1;
+    int phase = 0;
+};
+rgnn_status launch_rgat_bwd_traverse(const BwdArgs &a, hipStream_t s);
+rgnn_status launch_rgat_bwd_merge_s(const BwdArgs &a, hipStream_t s);
+
+struct OuterArgs {
+    const rgnn_graph *g = nullptr;
+    const float *A = nullptr;      // [V, d_in]   rows by vseg id
+    const float *B = nullptr;      // [N, d_out]  rows by destination of the vseg
+    int d_in = 64, d_out = 64;
+    float *partial = nullptr;      // [nchunks, d_in, d_out]
+    const int32_t *chunk_rel = nullptr;   // (device) relation of each K-chunk
+    const int32_t *chunk_row0 = nullptr;  // (device) first vseg-by-rel row of each chunk
+    const int32_t *chunk_rows = nullptr;
+    int64_t nchunks = 0;
+};
+rgnn_status launch_outer_gemm(const OuterArgs &a, hipStream_t s);
+rgnn_status launch_bwd_finalize(const rgnn_graph *g, const float *partial, const int32_t *rel_chunkptr,
+                                const float *acc_ws, const float *acc_wt, int copies,
+                                const float *W, const float *w_src, const float *w_dst,
+                                int d_in, int d_out, float *dW, float *dws, float *dwt,
+                                hipStream_t s);
+
+}  // namespace rgnn

@@ -1,0 +1,103 @@
+"""Shared helpers of the GPU parity tests: run a layer through the C ABI with
+torch-allocated outputs and workspace, and the row-normalised error measure.
+
+Tolerance (fp32 GPU vs fp64 oracle): for every output row v,
+    max_j |gpu[v, j] - ref[v, j]| / ||ref[v]||_2  <=  1e-4,
+and rows whose reference is exactly zero (destinations without in-edges)
+must be exactly zero on the GPU as well.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TOL = 1e-4
+
+
+def row_err(got, ref) -> float:
+    got = np.asarray(got, np.float64).reshape(len(ref), -1)
+    ref = np.asarray(ref, np.float64).reshape(len(ref), -1)
+    nrm = np.linalg.norm(ref, axis=1)
+    zero = nrm == 0
+    if zero.any() and np.abs(got[zero]).max(initial=0.0) != 0.0:
+        return float("inf")
+    if not (~zero).any():
+        return 0.0
+    return float((np.abs(got - ref)[~zero].max(axis=1) / nrm[~zero]).max())
+
+
+def sample_rows(g, n_random=400, seed=0):
+    """Destinations to check at full size: the largest in-degrees (hubs split
+    over many work items), some without in-edges, and a random sample."""
+    deg = np.bincount(g["dst"], minlength=g["N"])
+    rng = np.random.default_rng(seed)
+    top = np.argsort(-deg, kind="stable")[:6]
+    empty = np.flatnonzero(deg == 0)[:40]
+    rnd = rng.choice(g["N"], size=min(n_random, g["N"]), replace=False)
+    return np.unique(np.concatenate([top, empty, rnd])).astype(np.int32)
+
+
+class Runner:
+    """Runs the library's layers on one device with torch-owned buffers."""
+
+    def __init__(self, g, t, device="cuda:0"):
+        import torch
+        from paper_2301_06284_amd import rgnn
+        self.torch, self.rgnn = torch, rgnn
+        self.dev = torch.device(device)
+        self.g = g
+        self.G = rgnn.Graph.from_dict(g)
+        self.T = {k: torch.from_numpy(np.ascontiguousarray(v)).to(self.dev) for k, v in t.items()}
+
+    def ws(self, layer, d_in, d_out, heads=1, plan=0):
+        n = self.rgnn.workspace_size(self.G, layer, d_in, d_out, heads, plan)
+        return self.torch.empty(max(n, 256), dtype=self.torch.uint8, device=self.dev)
+
+    def rgcn(self, W0=True, relu=False, plan=0):
+        T, torch = self.T, self.torch
+        d_in, d_out = T["W"].shape[1], T["W"].shape[2]
+        out = torch.full((self.g["N"], d_out), float("nan"), device=self.dev)
+        self.rgnn.rgcn_forward(self.G, T["h"], T["W"], T["W0"] if W0 else None, out,
+                               self.ws(0, d_in, d_out, 1, plan), d_in, d_out,
+                               self.rgnn.FLAG_RELU if relu else 0, plan)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
+    def rgat(self, heads=1, plan=0, slope=0.2, want_saved=False):
+        T, torch = self.T, self.torch
+        d_in, d_out = T["W"].shape[1], T["W"].shape[2]
+        out = torch.full((self.g["N"], d_out), float("nan"), device=self.dev)
+        saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev)
+        self.rgnn.rgat_forward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved,
+                               self.ws(1, d_in, d_out, heads, plan), d_in, d_out, heads, slope,
+                               0, plan)
+        torch.cuda.synchronize()
+        if want_saved:
+            return out.cpu().numpy(), saved
+        return out.cpu().numpy()
+
+    def hgt(self, heads, scale, flags=None):
+        T, torch, rgnn = self.T, self.torch, self.rgnn
+        d = T["h"].shape[1]
+        flags = rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR if flags is None else flags
+        out = torch.full((self.g["N"], d), float("nan"), device=self.dev)
+        rgnn.hgt_forward(self.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
+                         T["mu"], out, self.ws(2, d, d, heads), d, heads, scale, flags)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
+    def rgat_backward(self, slope=0.2):
+        T, torch, rgnn = self.T, self.torch, self.rgnn
+        d = T["W"].shape[1]
+        R = T["W"].shape[0]
+        _, saved = self.rgat(heads=1, slope=slope, want_saved=True)
+        gh = torch.full((self.g["N"], d), float("nan"), device=self.dev)
+        gW = torch.full((R, d, d), float("nan"), device=self.dev)
+        gs = torch.full((R, d), float("nan"), device=self.dev)
+        gt = torch.full((R, d), float("nan"), device=self.dev)
+        rgnn.rgat_backward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], saved, T["grad_out"],
+                           gh, gW, gs, gt, self.ws(3, d, d), d, d, 1, slope)
+        torch.cuda.synchronize()
+        return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
+
+    def close(self):
+        self.G.close()

@@ -1,0 +1,129 @@
+"""CPU checks of the C ABI library: it loads, exports every symbol the header
+declares, builds graph indexes on the host bit-exactly (host-only graphs need
+no GPU), and turns bad inputs into the documented status codes."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _rgnn():
+    from paper_2301_06284_amd import rgnn
+    return rgnn
+
+
+def test_header_symbols_exported():
+    rgnn = _rgnn()
+    hdr = open(os.path.join(ROOT, "include", "rgnn.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    declared = set(re.findall(r"\b(rgnn_\w+|rgcn_forward|rgat_forward|hgt_forward|rgat_backward)\s*\(", hdr))
+    assert declared, "no declarations found"
+    lib = ctypes.CDLL(rgnn.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(lib, name), f"{name} declared in rgnn.h but not exported"
+    assert declared <= set(rgnn.EXPORTED) | {"rgnn_graph_t"}
+
+
+@pytest.mark.parametrize("kind", ["random", "hub", "dups", "isolated", "empty", "complete"])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_host_graph_index_bit_exact(kind, seed):
+    rgnn = _rgnn()
+    g = workloads.tiny_graph(seed, N=90, E=700, R=5, T=3, kind=kind)
+    G = rgnn.Graph.from_dict(g, host_only=True)
+    ix = oracle.graph_index(g)
+    for k in rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(G.export(k), ix[k], err_msg=k)
+    inf = G.info()
+    assert inf["num_src_pairs"] == ix["U_src"] and inf["num_dst_segments"] == ix["U_dst"]
+    G.close()
+
+
+def test_host_graph_index_workload1():
+    rgnn = _rgnn()
+    g = workloads.make_graph(1)
+    G = rgnn.Graph.from_dict(g, host_only=True)
+    ix = oracle.graph_index(g)
+    for k in rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(G.export(k), ix[k], err_msg=k)
+
+
+def test_csr_equals_coo():
+    rgnn = _rgnn()
+    g = workloads.tiny_graph(4, N=50, E=400, R=4, T=2, kind="hub")
+    order = np.argsort(g["dst"], kind="stable")
+    rowptr = np.zeros(g["N"] + 1, np.int64)
+    np.cumsum(np.bincount(g["dst"], minlength=g["N"]), out=rowptr[1:])
+    Gc = rgnn.Graph.from_csr(g["N"], g["T"], g["R"], rowptr, g["src"][order], g["rel"][order],
+                             g["ntype"], host_only=True)
+    g2 = dict(g, src=g["src"][order], dst=g["dst"][order], rel=g["rel"][order])
+    ix = oracle.graph_index(g2)
+    for k in rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(Gc.export(k), ix[k], err_msg=k)
+
+
+def test_error_codes():
+    rgnn = _rgnn()
+    g = workloads.tiny_graph(1, N=10, E=30, R=3, T=2)
+    bad = dict(g, src=g["src"].copy()); bad["src"][3] = 10
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.Graph.from_dict(bad, host_only=True)
+    assert e.value.status == rgnn.ERANGE
+    bad = dict(g, rel=g["rel"].copy()); bad["rel"][0] = -1
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.Graph.from_dict(bad, host_only=True)
+    assert e.value.status == rgnn.ERANGE
+    bad = dict(g, ntype=g["ntype"].copy()); bad["ntype"][2] = 2
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.Graph.from_dict(bad, host_only=True)
+    assert e.value.status == rgnn.ERANGE
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.Graph.from_coo(10, 0, 3, g["src"], g["dst"], g["rel"], host_only=True)
+    assert e.value.status == rgnn.EINVAL
+    rowptr = np.array([0, 2, 1, 3], np.int64)
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.Graph.from_csr(3, 1, 1, rowptr, np.zeros(3, np.int32), np.zeros(3, np.int32), host_only=True)
+    assert e.value.status == rgnn.EINVAL
+    # a host-only graph cannot run layers
+    G = rgnn.Graph.from_dict(g, host_only=True)
+    lib = rgnn.lib()
+    st = lib.rgcn_forward(G.handle, None, None, None, 64, 64, 0, 0, None, None, 0, None)
+    assert st == rgnn.EINVAL and b"host-only" in lib.rgnn_last_error()
+    # export buffer too small
+    buf = np.zeros(2, np.int32)
+    st = lib.rgnn_graph_export(G.handle, 1, buf.ctypes.data_as(ctypes.c_void_p), buf.nbytes)
+    assert st == rgnn.EINVAL
+
+
+def test_workspace_and_plan_model():
+    rgnn = _rgnn()
+    g = workloads.make_graph(1)
+    G = rgnn.Graph.from_dict(g, host_only=True)
+    for layer, heads in [(rgnn.LAYER_RGCN, 1), (rgnn.LAYER_RGAT, 1), (rgnn.LAYER_RGAT, 4),
+                         (rgnn.LAYER_HGT, 4), (rgnn.LAYER_RGAT_BACKWARD, 1)]:
+        for plan in (1, 2):
+            assert rgnn.workspace_size(G, layer, 64, 64, heads, plan) > 0
+    plan, tf, af = rgnn.select_plan(G, rgnn.LAYER_RGAT, 64, 64, 1)
+    assert plan == (2 if af < tf else 1) and tf > 0 and af > 0
+    # multi-head RGAT always resolves to transform-first
+    assert rgnn.select_plan(G, rgnn.LAYER_RGAT, 64, 64, 4)[0] == 1
+
+
+def test_product_does_not_import_oracle():
+    """The GPU package never reaches the oracle (no CPU fallback)."""
+    import ast
+    pkg = os.path.join(ROOT, "paper_2301_06284_amd")
+    for fn in os.listdir(pkg):
+        if fn.endswith(".py"):
+            tree = ast.parse(open(os.path.join(pkg, fn)).read())
+            for node in ast.walk(tree):
+                if isinstance(node, ast.Import):
+                    assert all(not a.name.startswith("oracle") for a in node.names), fn
+                if isinstance(node, ast.ImportFrom):
+                    assert not (node.module or "").startswith("oracle"), fn

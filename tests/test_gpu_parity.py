@@ -1,0 +1,187 @@
+"""GPU parity on small graphs: every layer and plan through the C ABI against
+the fp64 oracle, element by element, on graphs that still span many work
+items, split hub destinations, empty destinations, duplicate edges and
+ragged GEMM tiles.  Index arrays are compared bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from helpers import TOL, Runner, row_err
+
+pytestmark = pytest.mark.gpu
+
+KINDS = ["random", "hub", "dups", "isolated", "empty"]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2301_06284_amd import rgnn  # noqa: F401  (fails loudly if not built)
+    torch.cuda.set_device(0)
+
+
+def graph(kind, seed=5, N=300, E=4000, R=6, T=3):
+    return workloads.tiny_graph(seed, N=N, E=E, R=R, T=T, kind=kind)
+
+
+@pytest.mark.parametrize("kind", KINDS + ["complete"])
+def test_device_graph_index_bit_exact(kind):
+    from paper_2301_06284_amd import rgnn
+    g = graph(kind, N=120 if kind == "complete" else 300)
+    print(f"graph index {kind}", flush=True)
+    G = rgnn.Graph.from_dict(g)
+    ix = oracle.graph_index(g)
+    for k in rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(G.export(k), ix[k], err_msg=k)
+    G.close()
+
+
+@pytest.mark.parametrize("K,Nc", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_segment_gemm(K, Nc):
+    import torch
+    from paper_2301_06284_amd import rgnn
+    rng = np.random.default_rng(K + Nc)
+    type_ptr = np.array([0, 5, 5, 200, 201, 777, 1000], np.int64)   # empty and 1-row types
+    M, T = int(type_ptr[-1]), len(type_ptr) - 1
+    X = rng.standard_normal((1500, K)).astype(np.float32)
+    W = rng.standard_normal((T, K, Nc)).astype(np.float32)
+    gather = rng.integers(0, 1500, M).astype(np.int32)
+    scatter = rng.permutation(1200)[:M].astype(np.int32)
+    print(f"segment_gemm {K}x{Nc}", flush=True)
+    dev = torch.device("cuda:0")
+    Xd, Wd = torch.from_numpy(X).to(dev), torch.from_numpy(W).to(dev)
+    gd, sd = torch.from_numpy(gather).to(dev), torch.from_numpy(scatter).to(dev)
+    Y = torch.zeros(1200, Nc, device=dev)
+    ws = torch.empty(rgnn.segment_gemm_workspace_size(M, T), dtype=torch.uint8, device=dev)
+    rgnn.segment_gemm(Xd, gd, type_ptr, Wd, Y, sd, ws, K, Nc)
+    torch.cuda.synchronize()
+    ref = np.zeros((1200, Nc))
+    for t in range(T):
+        rows = np.arange(type_ptr[t], type_ptr[t + 1])
+        ref[scatter[rows]] = X[gather[rows]].astype(np.float64) @ W[t].astype(np.float64)
+    assert row_err(Y.cpu().numpy(), ref) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("plan", [1, 2])
+@pytest.mark.parametrize("W0,relu", [(True, False), (False, False), (True, True), (False, True)])
+def test_rgcn_small(kind, plan, W0, relu):
+    g = graph(kind)
+    t = workloads.tiny_tensors(1, g, 64, 64)
+    print(f"rgcn {kind} plan={plan} W0={W0} relu={relu}", flush=True)
+    run = Runner(g, t)
+    got = run.rgcn(W0=W0, relu=relu, plan=plan)
+    ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"] if W0 else None, relu=relu)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("d_in,d_out", [(128, 128), (64, 128), (128, 64)])
+@pytest.mark.parametrize("plan", [1, 2])
+def test_rgcn_dims(d_in, d_out, plan):
+    g = graph("hub", seed=9)
+    t = workloads.tiny_tensors(9, g, d_in, d_out)
+    print(f"rgcn dims {d_in}->{d_out} plan={plan}", flush=True)
+    run = Runner(g, t)
+    got = run.rgcn(plan=plan)
+    ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 2), (1, 4)])
+def test_rgat_small(kind, plan, heads):
+    g = graph(kind)
+    t = workloads.tiny_tensors(2, g, 64, 64, heads=heads, att_var=1.0)
+    print(f"rgat {kind} plan={plan} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got, saved = run.rgat(heads=heads, plan=plan, want_saved=True)
+    ref, mx, sm = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads,
+                                      want_stats=True)
+    run.close()
+    assert row_err(got, ref) <= TOL
+    sv = saved.cpu().numpy()
+    np.testing.assert_allclose(sv[..., 0], mx, rtol=1e-4, atol=1e-4)
+    np.testing.assert_allclose(sv[..., 1], sm, rtol=1e-4, atol=1e-5)
+
+
+@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 8)])
+def test_rgat_d128(plan, heads):
+    g = graph("hub", seed=4)
+    t = workloads.tiny_tensors(4, g, 128, 128, heads=heads, att_var=1.0)
+    print(f"rgat d128 plan={plan} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.rgat(heads=heads, plan=plan)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("heads", [1, 2, 4])
+def test_hgt_small(kind, heads):
+    g = graph(kind, T=4, R=7)
+    t = workloads.tiny_tensors(3, g, 64, 64, heads=heads)
+    scale = 1.0 / np.sqrt(64 // heads)
+    print(f"hgt {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt(heads, scale)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=heads, att_scale=scale)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("flags", [0, 2, 4])
+def test_hgt_flags(flags):
+    g = graph("hub", T=2, R=3)
+    t = workloads.tiny_tensors(6, g, 64, 64, heads=4)
+    print(f"hgt flags={flags}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt(4, 0.3, flags=flags)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=4, att_scale=0.3, residual=bool(flags & 2),
+                             a_linear=bool(flags & 4))
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_rgat_backward_small(kind):
+    g = graph(kind, E=3000)
+    t = workloads.tiny_tensors(8, g, 64, 64, att_var=1.0)
+    print(f"rgat backward {kind}", flush=True)
+    run = Runner(g, t)
+    gh, gW, gs, gt = run.rgat_backward()
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    assert row_err(gh, dh) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    assert row_err(gs, dws) <= TOL
+    assert row_err(gt, dwt) <= TOL
+
+
+def test_forward_bitwise_deterministic():
+    g = graph("hub", seed=12)
+    t = workloads.tiny_tensors(12, g, 64, 64, heads=4, att_var=1.0)
+    print("determinism", flush=True)
+    run = Runner(g, t)
+    for fn in (lambda: run.rgcn(plan=1), lambda: run.rgcn(plan=2), lambda: run.rgat(plan=1),
+               lambda: run.rgat(plan=2), lambda: run.hgt(4, 0.25)):
+        a, b = fn(), fn()
+        assert np.array_equal(a, b)
+    run.close()
+
+
+def test_plans_agree():
+    g = graph("dups", seed=13)
+    t = workloads.tiny_tensors(13, g, 64, 64, att_var=1.0)
+    print("plans agree", flush=True)
+    run = Runner(g, t)
+    for fn in (run.rgcn, run.rgat):
+        a, b = fn(plan=1), fn(plan=2)
+        assert row_err(a, b.astype(np.float64)) <= 1e-5
+    run.close()
