@@ -89,55 +89,109 @@ static void load_row(const float *h, int64_t n, int d, double *x)
 /* Rows to produce: sel[0:nsel], or every node when sel is NULL. */
 static inline int64_t sel_node(const int32_t *sel, int64_t i) { return sel ? sel[i] : i; }
 
+/* Per-destination scratch: per-edge messages and logits of one row. */
+typedef struct {
+    double *msg, *aux, *z;
+    int64_t cap;
+    int64_t *cnt;
+} row_scratch;
+
+static int scratch_reserve(row_scratch *s, int64_t deg, int d, int H)
+{
+    if (deg <= s->cap) return 0;
+    free(s->msg); free(s->aux); free(s->z);
+    s->cap = deg;
+    s->msg = (double *)malloc((size_t)deg * d * sizeof(double));
+    s->aux = (double *)malloc((size_t)deg * d * sizeof(double));
+    s->z = (double *)malloc((size_t)deg * H * sizeof(double));
+    if (!s->msg || !s->aux || !s->z) { s->cap = 0; return -3; }
+    return 0;
+}
+
+static void scratch_free(row_scratch *s) { free(s->msg); free(s->aux); free(s->z); free(s->cnt); }
+
+/* Destinations with more in-edges than this are handled one at a time with
+ * the per-edge pass spread over threads; all others one per thread.  The
+ * arithmetic and the order of every sum are the same either way. */
+#define BIG_ROW 4096
+
 /* ------------------------------------------------------------------------ */
 /* RGCN (the paper's RGCN equation):
  *   out_v = act( h_v W0 + sum_r sum_{u in N_v^r} h_u W_r / c_{v,r} )
  * with c_{v,r} the number of in-edges of v with relation r (duplicates counted)
  * and the self-loop term present only when W0 is given.  act = ReLU if relu. */
+typedef struct {
+    int64_t N, E; int32_t R, d_in, d_out;
+    const int32_t *src, *rel; const float *h, *W, *W0; int32_t relu;
+    const int32_t *sel; double *out; in_lists a;
+} rgcn_ctx;
+
+static int rgcn_row(const rgcn_ctx *c, int64_t i, int inner, row_scratch *sc)
+{
+    const int64_t v = sel_node(c->sel, i);
+    const int64_t p0 = c->a.ptr[v], deg = c->a.ptr[v + 1] - p0;
+    const int d_in = c->d_in, d_out = c->d_out;
+    if (scratch_reserve(sc, deg, d_out, 1)) return -3;
+    double *o = c->out + (size_t)i * d_out;
+    for (int j = 0; j < d_out; ++j) o[j] = 0.0;
+    if (c->W0) {
+        double x[512], m[512];
+        load_row(c->h, v, d_in, x);
+        vecmat(x, c->W0, d_in, d_out, 0, d_out, m);
+        for (int j = 0; j < d_out; ++j) o[j] += m[j];
+    }
+    for (int r = 0; r < c->R; ++r) sc->cnt[r] = 0;
+    for (int64_t p = p0; p < p0 + deg; ++p) sc->cnt[c->rel[c->a.eid[p]]]++;
+#pragma omp parallel for schedule(static) if (inner)
+    for (int64_t q = 0; q < deg; ++q) {
+        double x[512];
+        const int64_t e = c->a.eid[p0 + q];
+        load_row(c->h, c->src[e], d_in, x);
+        vecmat(x, c->W + (size_t)c->rel[e] * d_in * d_out, d_in, d_out, 0, d_out,
+               sc->msg + q * d_out);
+    }
+    for (int64_t q = 0; q < deg; ++q) {
+        const double inv_c = 1.0 / (double)sc->cnt[c->rel[c->a.eid[p0 + q]]];
+        for (int j = 0; j < d_out; ++j) o[j] += sc->msg[q * d_out + j] * inv_c;
+    }
+    if (c->relu)
+        for (int j = 0; j < d_out; ++j) o[j] = o[j] > 0.0 ? o[j] : 0.0;
+    return 0;
+}
+
 int oracle_rgcn_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
                         const int32_t *src, const int32_t *dst, const int32_t *rel,
                         const float *h, const float *W, const float *W0, int32_t relu,
                         int64_t nsel, const int32_t *sel, double *out)
 {
-    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0) return -1;
-    in_lists a;
-    int rc = build_in_lists(N, E, dst, &a);
-    if (rc) { free_in_lists(&a); return rc; }
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0 || d_in > 512 ||
+        d_out > 512)
+        return -1;
+    rgcn_ctx c = {N, E, R, d_in, d_out, src, rel, h, W, W0, relu, sel, out, {0, 0}};
+    int rc = build_in_lists(N, E, dst, &c.a);
+    if (rc) { free_in_lists(&c.a); return rc; }
     const int64_t nrows = sel ? nsel : N;
     int err = 0;
 #pragma omp parallel reduction(| : err)
     {
-        int64_t *cnt = (int64_t *)malloc((size_t)R * sizeof(int64_t));
-        double *x = (double *)malloc((size_t)d_in * sizeof(double));
-        double *m = (double *)malloc((size_t)d_out * sizeof(double));
-        if (!cnt || !x || !m) err = 1;
+        row_scratch sc = {0, 0, 0, 0, (int64_t *)malloc((size_t)R * sizeof(int64_t))};
+        if (!sc.cnt) err = 1;
 #pragma omp for schedule(dynamic, 16)
         for (int64_t i = 0; i < nrows; ++i) {
-            if (err) continue;
             const int64_t v = sel_node(sel, i);
-            double *o = out + (size_t)i * d_out;
-            for (int j = 0; j < d_out; ++j) o[j] = 0.0;
-            if (W0) {
-                load_row(h, v, d_in, x);
-                vecmat(x, W0, d_in, d_out, 0, d_out, m);
-                for (int j = 0; j < d_out; ++j) o[j] += m[j];
-            }
-            for (int r = 0; r < R; ++r) cnt[r] = 0;
-            for (int64_t p = a.ptr[v]; p < a.ptr[v + 1]; ++p) cnt[rel[a.eid[p]]]++;
-            for (int64_t p = a.ptr[v]; p < a.ptr[v + 1]; ++p) {
-                const int64_t e = a.eid[p];
-                const int r = rel[e];
-                load_row(h, src[e], d_in, x);
-                vecmat(x, W + (size_t)r * d_in * d_out, d_in, d_out, 0, d_out, m);
-                const double inv_c = 1.0 / (double)cnt[r];
-                for (int j = 0; j < d_out; ++j) o[j] += m[j] * inv_c;
-            }
-            if (relu)
-                for (int j = 0; j < d_out; ++j) o[j] = o[j] > 0.0 ? o[j] : 0.0;
+            if (err || c.a.ptr[v + 1] - c.a.ptr[v] > BIG_ROW) continue;
+            if (rgcn_row(&c, i, 0, &sc)) err = 1;
         }
-        free(cnt); free(x); free(m);
+        scratch_free(&sc);
     }
-    free_in_lists(&a);
+    row_scratch sc = {0, 0, 0, 0, (int64_t *)malloc((size_t)R * sizeof(int64_t))};
+    if (!sc.cnt) err = 1;
+    for (int64_t i = 0; i < nrows && !err; ++i) {
+        const int64_t v = sel_node(sel, i);
+        if (c.a.ptr[v + 1] - c.a.ptr[v] > BIG_ROW && rgcn_row(&c, i, 1, &sc)) err = 1;
+    }
+    scratch_free(&sc);
+    free_in_lists(&c.a);
     return err ? -3 : 0;
 }
 
@@ -155,6 +209,72 @@ int oracle_rgcn_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d
  * which leaves alpha unchanged.
  * Optional outputs, for scope 0 only: stat_max[v,k] = max z, stat_sum[v,k] =
  * sum exp(z - max); alpha_out[e,k] for every in-edge of a produced row. */
+typedef struct {
+    int64_t N, E; int32_t R, d_in, d_out, H, scope;
+    const int32_t *src, *rel; const float *h, *W, *w_src, *w_dst; double slope;
+    const int32_t *sel; double *out, *stat_max, *stat_sum, *alpha_out; in_lists a;
+} rgat_ctx;
+
+static int rgat_row(const rgat_ctx *c, int64_t i, int inner, row_scratch *sc, double *mx,
+                    double *sm)
+{
+    const int64_t v = sel_node(c->sel, i);
+    const int64_t p0 = c->a.ptr[v], deg = c->a.ptr[v + 1] - p0;
+    const int d_in = c->d_in, d_out = c->d_out, H = c->H, dh = d_out / H;
+    if (scratch_reserve(sc, deg, d_out, H)) return -3;
+    double *o = c->out + (size_t)i * d_out;
+    for (int j = 0; j < d_out; ++j) o[j] = 0.0;
+    /* pass 1: messages and logits of every in-edge */
+#pragma omp parallel for schedule(static) if (inner)
+    for (int64_t q = 0; q < deg; ++q) {
+        double x[512], xv[512];
+        double *msg = sc->msg + q * d_out, *t = sc->aux + q * d_out;
+        const int64_t e = c->a.eid[p0 + q];
+        const int r = c->rel[e];
+        const float *Wr = c->W + (size_t)r * d_in * d_out;
+        load_row(c->h, c->src[e], d_in, x);
+        load_row(c->h, v, d_in, xv);
+        vecmat(x, Wr, d_in, d_out, 0, d_out, msg);
+        vecmat(xv, Wr, d_in, d_out, 0, d_out, t);
+        for (int k = 0; k < H; ++k) {
+            double y = 0.0;
+            for (int j = k * dh; j < (k + 1) * dh; ++j)
+                y += msg[j] * (double)c->w_src[(size_t)r * d_out + j] +
+                     t[j] * (double)c->w_dst[(size_t)r * d_out + j];
+            sc->z[q * H + k] = y > 0.0 ? y : c->slope * y;
+        }
+    }
+    /* pass 2: softmax maximum and denominator per group and head */
+    const int G = c->scope == 0 ? 1 : c->R;
+    for (int q = 0; q < G * H; ++q) { mx[q] = -INFINITY; sm[q] = 0.0; }
+    for (int64_t q = 0; q < deg; ++q) {
+        const int gi = c->scope == 0 ? 0 : c->rel[c->a.eid[p0 + q]];
+        for (int k = 0; k < H; ++k)
+            if (sc->z[q * H + k] > mx[gi * H + k]) mx[gi * H + k] = sc->z[q * H + k];
+    }
+    for (int64_t q = 0; q < deg; ++q) {
+        const int gi = c->scope == 0 ? 0 : c->rel[c->a.eid[p0 + q]];
+        for (int k = 0; k < H; ++k) sm[gi * H + k] += exp(sc->z[q * H + k] - mx[gi * H + k]);
+    }
+    /* pass 3: attention-weighted sum of the messages */
+    for (int64_t q = 0; q < deg; ++q) {
+        const int64_t e = c->a.eid[p0 + q];
+        const int gi = c->scope == 0 ? 0 : c->rel[e];
+        for (int k = 0; k < H; ++k) {
+            const double al = exp(sc->z[q * H + k] - mx[gi * H + k]) / sm[gi * H + k];
+            if (c->alpha_out) c->alpha_out[(size_t)e * H + k] = al;
+            for (int j = k * dh; j < (k + 1) * dh; ++j) o[j] += al * sc->msg[q * d_out + j];
+        }
+    }
+    if (c->scope == 0) {
+        for (int k = 0; k < H; ++k) {
+            if (c->stat_max) c->stat_max[(size_t)i * H + k] = deg ? mx[k] : 0.0;
+            if (c->stat_sum) c->stat_sum[(size_t)i * H + k] = deg ? sm[k] : 0.0;
+        }
+    }
+    return 0;
+}
+
 int oracle_rgat_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
                         int32_t heads, const int32_t *src, const int32_t *dst,
                         const int32_t *rel, const float *h, const float *W,
@@ -162,88 +282,38 @@ int oracle_rgat_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d
                         int32_t scope, int64_t nsel, const int32_t *sel, double *out,
                         double *stat_max, double *stat_sum, double *alpha_out)
 {
-    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0 || heads <= 0 ||
-        d_out % heads || (scope != 0 && scope != 1))
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_out <= 0 || d_in > 512 ||
+        d_out > 512 || heads <= 0 || d_out % heads || (scope != 0 && scope != 1))
         return -1;
-    const int H = heads, dh = d_out / heads;
-    in_lists a;
-    int rc = build_in_lists(N, E, dst, &a);
-    if (rc) { free_in_lists(&a); return rc; }
+    rgat_ctx c = {N, E, R, d_in, d_out, heads, scope, src, rel, h, W, w_src, w_dst, neg_slope,
+                  sel, out, stat_max, stat_sum, alpha_out, {0, 0}};
+    int rc = build_in_lists(N, E, dst, &c.a);
+    if (rc) { free_in_lists(&c.a); return rc; }
     const int64_t nrows = sel ? nsel : N;
+    const size_t gh = (size_t)R * heads * sizeof(double);
     int err = 0;
 #pragma omp parallel reduction(| : err)
     {
-        double *x = (double *)malloc((size_t)d_in * sizeof(double));
-        double *xv = (double *)malloc((size_t)d_in * sizeof(double));
-        double *t = (double *)malloc((size_t)d_out * sizeof(double));
-        double *mx = (double *)malloc((size_t)R * H * sizeof(double));
-        double *sm = (double *)malloc((size_t)R * H * sizeof(double));
-        double *msg = NULL, *z = NULL;
-        int64_t cap = 0;
-        if (!x || !xv || !t || !mx || !sm) err = 1;
+        row_scratch sc = {0, 0, 0, 0, 0};
+        double *mx = (double *)malloc(gh), *sm = (double *)malloc(gh);
+        if (!mx || !sm) err = 1;
 #pragma omp for schedule(dynamic, 16)
         for (int64_t i = 0; i < nrows; ++i) {
-            if (err) continue;
             const int64_t v = sel_node(sel, i);
-            const int64_t p0 = a.ptr[v], deg = a.ptr[v + 1] - p0;
-            double *o = out + (size_t)i * d_out;
-            for (int j = 0; j < d_out; ++j) o[j] = 0.0;
-            if (deg > cap) {
-                free(msg); free(z);
-                cap = deg;
-                msg = (double *)malloc((size_t)cap * d_out * sizeof(double));
-                z = (double *)malloc((size_t)cap * H * sizeof(double));
-                if (!msg || !z) { err = 1; cap = 0; continue; }
-            }
-            load_row(h, v, d_in, xv);
-            /* pass 1: messages and logits of every in-edge */
-            for (int64_t q = 0; q < deg; ++q) {
-                const int64_t e = a.eid[p0 + q];
-                const int r = rel[e];
-                const float *Wr = W + (size_t)r * d_in * d_out;
-                load_row(h, src[e], d_in, x);
-                vecmat(x, Wr, d_in, d_out, 0, d_out, msg + q * d_out);
-                vecmat(xv, Wr, d_in, d_out, 0, d_out, t);
-                for (int k = 0; k < H; ++k) {
-                    double y = 0.0;
-                    for (int j = k * dh; j < (k + 1) * dh; ++j)
-                        y += msg[q * d_out + j] * (double)w_src[(size_t)r * d_out + j] +
-                             t[j] * (double)w_dst[(size_t)r * d_out + j];
-                    z[q * H + k] = y > 0.0 ? y : neg_slope * y;
-                }
-            }
-            /* pass 2: softmax maximum and denominator per group and head */
-            const int G = scope == 0 ? 1 : R;
-            for (int q = 0; q < G * H; ++q) { mx[q] = -INFINITY; sm[q] = 0.0; }
-            for (int64_t q = 0; q < deg; ++q) {
-                const int gi = scope == 0 ? 0 : rel[a.eid[p0 + q]];
-                for (int k = 0; k < H; ++k)
-                    if (z[q * H + k] > mx[gi * H + k]) mx[gi * H + k] = z[q * H + k];
-            }
-            for (int64_t q = 0; q < deg; ++q) {
-                const int gi = scope == 0 ? 0 : rel[a.eid[p0 + q]];
-                for (int k = 0; k < H; ++k) sm[gi * H + k] += exp(z[q * H + k] - mx[gi * H + k]);
-            }
-            /* pass 3: attention-weighted sum of the messages */
-            for (int64_t q = 0; q < deg; ++q) {
-                const int64_t e = a.eid[p0 + q];
-                const int gi = scope == 0 ? 0 : rel[e];
-                for (int k = 0; k < H; ++k) {
-                    const double al = exp(z[q * H + k] - mx[gi * H + k]) / sm[gi * H + k];
-                    if (alpha_out) alpha_out[(size_t)e * H + k] = al;
-                    for (int j = k * dh; j < (k + 1) * dh; ++j) o[j] += al * msg[q * d_out + j];
-                }
-            }
-            if (scope == 0) {
-                for (int k = 0; k < H; ++k) {
-                    if (stat_max) stat_max[(size_t)i * H + k] = deg ? mx[k] : 0.0;
-                    if (stat_sum) stat_sum[(size_t)i * H + k] = deg ? sm[k] : 0.0;
-                }
-            }
+            if (err || c.a.ptr[v + 1] - c.a.ptr[v] > BIG_ROW) continue;
+            if (rgat_row(&c, i, 0, &sc, mx, sm)) err = 1;
         }
-        free(x); free(xv); free(t); free(mx); free(sm); free(msg); free(z);
+        scratch_free(&sc); free(mx); free(sm);
     }
-    free_in_lists(&a);
+    row_scratch sc = {0, 0, 0, 0, 0};
+    double *mx = (double *)malloc(gh), *sm = (double *)malloc(gh);
+    if (!mx || !sm) err = 1;
+    for (int64_t i = 0; i < nrows && !err; ++i) {
+        const int64_t v = sel_node(sel, i);
+        if (c.a.ptr[v + 1] - c.a.ptr[v] > BIG_ROW && rgat_row(&c, i, 1, &sc, mx, sm)) err = 1;
+    }
+    scratch_free(&sc); free(mx); free(sm);
+    free_in_lists(&c.a);
     return err ? -3 : 0;
 }
 
@@ -259,6 +329,65 @@ int oracle_rgat_forward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d
  *   out_t = agg_t Wa[tau(t)] (if a_linear, else agg_t) + h_t (if residual)
  * K and V are recomputed for every edge from h_s (they depend only on the
  * source node; recomputation gives the same fp64 values). */
+typedef struct {
+    int64_t N, E; int32_t R, T, d, H;
+    const int32_t *src, *rel, *ntype; const float *h, *Wk, *Wq, *Wv, *Wa, *Watt, *Wmsg, *mu;
+    double scale; int32_t residual, a_linear;
+    const int32_t *sel; double *out; in_lists a;
+} hgt_ctx;
+
+static int hgt_row(const hgt_ctx *c, int64_t i, int inner, row_scratch *sc, double *mx,
+                   double *sm)
+{
+    const int64_t t = sel_node(c->sel, i);
+    const int64_t p0 = c->a.ptr[t], deg = c->a.ptr[t + 1] - p0;
+    const int d = c->d, H = c->H, dk = d / H;
+    if (scratch_reserve(sc, deg, d, H)) return -3;
+    double q[512], agg[512];
+    {
+        double x[512];
+        load_row(c->h, t, d, x);
+        vecmat(x, c->Wq + (size_t)c->ntype[t] * d * d, d, d, 0, d, q);
+    }
+#pragma omp parallel for schedule(static) if (inner)
+    for (int64_t p = 0; p < deg; ++p) {
+        double x[512], kk[512], vv[512], kw[512];
+        const int64_t e = c->a.eid[p0 + p];
+        const int64_t s = c->src[e];
+        const int r = c->rel[e];
+        load_row(c->h, s, d, x);
+        vecmat(x, c->Wk + (size_t)c->ntype[s] * d * d, d, d, 0, d, kk);
+        vecmat(x, c->Wv + (size_t)c->ntype[s] * d * d, d, d, 0, d, vv);
+        for (int hh = 0; hh < H; ++hh) {
+            const float *Wat = c->Watt + ((size_t)r * H + hh) * dk * dk;
+            const float *Wms = c->Wmsg + ((size_t)r * H + hh) * dk * dk;
+            vecmat(kk + hh * dk, Wat, dk, dk, 0, dk, kw);
+            double dot = 0.0;
+            for (int j = 0; j < dk; ++j) dot += kw[j] * q[hh * dk + j];
+            sc->z[p * H + hh] = dot * (double)c->mu[r] * c->scale;
+            vecmat(vv + hh * dk, Wms, dk, dk, 0, dk, sc->msg + p * d + hh * dk);
+        }
+    }
+    for (int hh = 0; hh < H; ++hh) { mx[hh] = -INFINITY; sm[hh] = 0.0; }
+    for (int64_t p = 0; p < deg; ++p)
+        for (int hh = 0; hh < H; ++hh)
+            if (sc->z[p * H + hh] > mx[hh]) mx[hh] = sc->z[p * H + hh];
+    for (int64_t p = 0; p < deg; ++p)
+        for (int hh = 0; hh < H; ++hh) sm[hh] += exp(sc->z[p * H + hh] - mx[hh]);
+    for (int j = 0; j < d; ++j) agg[j] = 0.0;
+    for (int64_t p = 0; p < deg; ++p)
+        for (int hh = 0; hh < H; ++hh) {
+            const double al = exp(sc->z[p * H + hh] - mx[hh]) / sm[hh];
+            for (int j = hh * dk; j < (hh + 1) * dk; ++j) agg[j] += al * sc->msg[p * d + j];
+        }
+    double *o = c->out + (size_t)i * d;
+    if (c->a_linear) vecmat(agg, c->Wa + (size_t)c->ntype[t] * d * d, d, d, 0, d, o);
+    else for (int j = 0; j < d; ++j) o[j] = agg[j];
+    if (c->residual)
+        for (int j = 0; j < d; ++j) o[j] += (double)c->h[(size_t)t * d + j];
+    return 0;
+}
+
 int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
                        int32_t heads, const int32_t *src, const int32_t *dst,
                        const int32_t *rel, const int32_t *ntype, const float *h,
@@ -267,82 +396,40 @@ int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
                        double att_scale, int32_t residual, int32_t a_linear,
                        int64_t nsel, const int32_t *sel, double *out)
 {
-    if (check_coo(N, E, R, src, dst, rel) || T <= 0 || d <= 0 || heads <= 0 || d % heads)
+    if (check_coo(N, E, R, src, dst, rel) || T <= 0 || d <= 0 || d > 512 || heads <= 0 ||
+        d % heads)
         return -1;
     for (int64_t n = 0; n < N; ++n)
         if (ntype[n] < 0 || ntype[n] >= T) return -1;
-    const int H = heads, dk = d / heads;
-    in_lists a;
-    int rc = build_in_lists(N, E, dst, &a);
-    if (rc) { free_in_lists(&a); return rc; }
+    hgt_ctx c = {N, E, R, T, d, heads, src, rel, ntype, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu,
+                 att_scale, residual, a_linear, sel, out, {0, 0}};
+    int rc = build_in_lists(N, E, dst, &c.a);
+    if (rc) { free_in_lists(&c.a); return rc; }
     const int64_t nrows = sel ? nsel : N;
+    const size_t hb = (size_t)heads * sizeof(double);
     int err = 0;
 #pragma omp parallel reduction(| : err)
     {
-        double *x = (double *)malloc((size_t)d * sizeof(double));
-        double *q = (double *)malloc((size_t)d * sizeof(double));
-        double *kk = (double *)malloc((size_t)d * sizeof(double));
-        double *vv = (double *)malloc((size_t)d * sizeof(double));
-        double *kw = (double *)malloc((size_t)dk * sizeof(double));
-        double *agg = (double *)malloc((size_t)d * sizeof(double));
-        double *mx = (double *)malloc((size_t)H * sizeof(double));
-        double *sm = (double *)malloc((size_t)H * sizeof(double));
-        double *msg = NULL, *att = NULL;
-        int64_t cap = 0;
-        if (!x || !q || !kk || !vv || !kw || !agg || !mx || !sm) err = 1;
+        row_scratch sc = {0, 0, 0, 0, 0};
+        double *mx = (double *)malloc(hb), *sm = (double *)malloc(hb);
+        if (!mx || !sm) err = 1;
 #pragma omp for schedule(dynamic, 16)
         for (int64_t i = 0; i < nrows; ++i) {
-            if (err) continue;
             const int64_t t = sel_node(sel, i);
-            const int64_t p0 = a.ptr[t], deg = a.ptr[t + 1] - p0;
-            if (deg > cap) {
-                free(msg); free(att);
-                cap = deg;
-                msg = (double *)malloc((size_t)cap * d * sizeof(double));
-                att = (double *)malloc((size_t)cap * H * sizeof(double));
-                if (!msg || !att) { err = 1; cap = 0; continue; }
-            }
-            load_row(h, t, d, x);
-            vecmat(x, Wq + (size_t)ntype[t] * d * d, d, d, 0, d, q);
-            for (int64_t p = 0; p < deg; ++p) {
-                const int64_t e = a.eid[p0 + p];
-                const int64_t s = src[e];
-                const int r = rel[e];
-                load_row(h, s, d, x);
-                vecmat(x, Wk + (size_t)ntype[s] * d * d, d, d, 0, d, kk);
-                vecmat(x, Wv + (size_t)ntype[s] * d * d, d, d, 0, d, vv);
-                for (int hh = 0; hh < H; ++hh) {
-                    const float *Wat = Watt + ((size_t)r * H + hh) * dk * dk;
-                    const float *Wms = Wmsg + ((size_t)r * H + hh) * dk * dk;
-                    vecmat(kk + hh * dk, Wat, dk, dk, 0, dk, kw);
-                    double dot = 0.0;
-                    for (int j = 0; j < dk; ++j) dot += kw[j] * q[hh * dk + j];
-                    att[p * H + hh] = dot * (double)mu[r] * att_scale;
-                    vecmat(vv + hh * dk, Wms, dk, dk, 0, dk, msg + p * d + hh * dk);
-                }
-            }
-            for (int hh = 0; hh < H; ++hh) { mx[hh] = -INFINITY; sm[hh] = 0.0; }
-            for (int64_t p = 0; p < deg; ++p)
-                for (int hh = 0; hh < H; ++hh)
-                    if (att[p * H + hh] > mx[hh]) mx[hh] = att[p * H + hh];
-            for (int64_t p = 0; p < deg; ++p)
-                for (int hh = 0; hh < H; ++hh) sm[hh] += exp(att[p * H + hh] - mx[hh]);
-            for (int j = 0; j < d; ++j) agg[j] = 0.0;
-            for (int64_t p = 0; p < deg; ++p)
-                for (int hh = 0; hh < H; ++hh) {
-                    const double al = exp(att[p * H + hh] - mx[hh]) / sm[hh];
-                    for (int j = hh * dk; j < (hh + 1) * dk; ++j) agg[j] += al * msg[p * d + j];
-                }
-            double *o = out + (size_t)i * d;
-            if (a_linear) vecmat(agg, Wa + (size_t)ntype[t] * d * d, d, d, 0, d, o);
-            else for (int j = 0; j < d; ++j) o[j] = agg[j];
-            if (residual)
-                for (int j = 0; j < d; ++j) o[j] += (double)h[(size_t)t * d + j];
+            if (err || c.a.ptr[t + 1] - c.a.ptr[t] > BIG_ROW) continue;
+            if (hgt_row(&c, i, 0, &sc, mx, sm)) err = 1;
         }
-        free(x); free(q); free(kk); free(vv); free(kw); free(agg); free(mx); free(sm);
-        free(msg); free(att);
+        scratch_free(&sc); free(mx); free(sm);
     }
-    free_in_lists(&a);
+    row_scratch sc = {0, 0, 0, 0, 0};
+    double *mx = (double *)malloc(hb), *sm = (double *)malloc(hb);
+    if (!mx || !sm) err = 1;
+    for (int64_t i = 0; i < nrows && !err; ++i) {
+        const int64_t t = sel_node(sel, i);
+        if (c.a.ptr[t + 1] - c.a.ptr[t] > BIG_ROW && hgt_row(&c, i, 1, &sc, mx, sm)) err = 1;
+    }
+    scratch_free(&sc); free(mx); free(sm);
+    free_in_lists(&c.a);
     return err ? -3 : 0;
 }
 

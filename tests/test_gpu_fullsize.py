@@ -1,0 +1,146 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times.  The whole output is computed on the GPU; the fp64 oracle
+recomputes sampled destinations one by one (the largest hubs, destinations
+without in-edges and a random sample).  Properties that hold at any size are
+checked on every row: empty destinations give exact zeros, softmax
+denominators are >= 1, outputs are finite.
+
+Workloads (seeded, see workloads/synth.py):
+  1  RGCN   2 000 nodes / 20 000 edges / 8 relations, d = 64
+  2  RGAT   880 000 nodes / 5.7 M edges / 96 relations, d = 64
+  3  HGT    1.9 M nodes / 21 M edges / 7 relations, d = 64 = 4 x 16
+  4  RGCN, RGAT at d = 128 on 2.5 M nodes / 16 M edges / 535 relations
+  5  RGAT backward on workload 2's graph
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from helpers import TOL, Runner, row_err, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+_cache = {}
+
+
+def load(k):
+    if k not in _cache:
+        _cache.clear()
+        g = workloads.make_graph(k)
+        layer = workloads.CONFIGS[k]["layers"][0]
+        t = workloads.make_tensors(k, g, layer)
+        _cache[k] = (g, t, Runner(g, t))
+    return _cache[k]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available()
+    torch.cuda.set_device(0)
+    yield
+    _cache.clear()
+
+
+def check_properties(g, out, saved=None):
+    deg = np.bincount(g["dst"], minlength=g["N"])
+    assert np.isfinite(out).all()
+    if saved is not None:
+        s = saved.cpu().numpy().reshape(g["N"], -1, 2)
+        assert (s[deg == 0] == 0).all()
+        assert (s[deg > 0][..., 1] >= 1 - 1e-5).all()
+        assert np.isfinite(s).all()
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_workload1_rgcn_all_rows(plan):
+    g, t, run = load(1)
+    print(f"workload 1 rgcn plan={plan}", flush=True)
+    got = run.rgcn(W0=True, plan=plan)
+    ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])
+    assert row_err(got, ref) <= TOL
+
+
+def test_workload1_graph_index_bit_exact():
+    g, t, run = load(1)
+    ix = oracle.graph_index(g)
+    for k in run.rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(run.G.export(k), ix[k], err_msg=k)
+
+
+def test_workload2_graph_index_bit_exact():
+    g, t, run = load(2)
+    print("workload 2 index", flush=True)
+    ix = oracle.graph_index(g)
+    for k in run.rgnn.INDEX_KINDS:
+        np.testing.assert_array_equal(run.G.export(k), ix[k], err_msg=k)
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_workload2_rgat(plan):
+    g, t, run = load(2)
+    print(f"workload 2 rgat plan={plan}", flush=True)
+    got, saved = run.rgat(plan=plan, want_saved=True)
+    check_properties(g, got, saved)
+    sel = sample_rows(g, 300, seed=plan)
+    ref, mx, sm = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], sel=sel,
+                                      want_stats=True)
+    assert row_err(got[sel], ref) <= TOL
+    s = saved.cpu().numpy()[sel, 0]
+    np.testing.assert_allclose(s[:, 0], mx[:, 0], rtol=1e-4, atol=1e-4)
+    np.testing.assert_allclose(s[:, 1], sm[:, 0], rtol=1e-4)
+
+
+def test_workload3_hgt():
+    g, t, run = load(3)
+    print("workload 3 hgt", flush=True)
+    got = run.hgt(4, 0.25)
+    assert np.isfinite(got).all()
+    sel = sample_rows(g, 300)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=4, att_scale=0.25, sel=sel)
+    assert row_err(got[sel], ref) <= TOL
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_workload4_rgcn(plan):
+    g, t, run = load(4)
+    print(f"workload 4 rgcn plan={plan}", flush=True)
+    got = run.rgcn(W0=True, plan=plan)
+    assert np.isfinite(got).all()
+    sel = sample_rows(g, 200, seed=plan)
+    ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"], sel=sel)
+    assert row_err(got[sel], ref) <= TOL
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_workload4_rgat(plan):
+    g, t, run = load(4)
+    print(f"workload 4 rgat plan={plan}", flush=True)
+    got, saved = run.rgat(plan=plan, want_saved=True)
+    check_properties(g, got, saved)
+    sel = sample_rows(g, 150, seed=10 + plan)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], sel=sel)
+    assert row_err(got[sel], ref) <= TOL
+
+
+def test_workload5_rgat_backward():
+    g, t, run = load(5)
+    print("workload 5 rgat backward", flush=True)
+    gh, gW, gs, gt = run.rgat_backward()
+    for a in (gh, gW, gs, gt):
+        assert np.isfinite(a).all()
+    rng = np.random.default_rng(5)
+    relcount = np.bincount(g["rel"], minlength=g["R"])
+    rels = np.r_[np.argsort(relcount)[:3], [20]]
+    nodes = rng.choice(g["N"], 60, replace=False)
+    nm = np.zeros(g["N"], np.uint8); nm[nodes] = 1
+    rm = np.zeros(g["R"], np.uint8); rm[rels] = 1
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"],
+                                            t["grad_out"], node_mask=nm, rel_mask=rm)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh[nodes], dh[nodes], structural_zero=isolated[nodes]) <= TOL
+    assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64)) <= TOL
+    assert row_err(gs[rels], dws[rels]) <= TOL
+    assert row_err(gt[rels], dwt[rels]) <= TOL
