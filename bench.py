@@ -68,6 +68,10 @@ class Ctx:
         self.torch.cuda.empty_cache()
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def time_steps(torch, fn, steps, warmup):
     for _ in range(warmup):
         fn()
@@ -182,6 +186,7 @@ def main():
     layers = {}
 
     # ------------------------------------------------ headline: RGAT forward, workload 2
+    log("workload 2: generating and building the graph")
     c = Ctx(2)
     d, H = 64, 1
     inf = c.info
@@ -190,6 +195,7 @@ def main():
     saved = torch.empty(inf["num_nodes"], H, 2, device=c.dev)
     plans = {}
     for p in (rgnn.PLAN_TRANSFORM_FIRST, rgnn.PLAN_AGGREGATE_FIRST):
+        log(f"workload 2: RGAT forward plan {p}")
         ws = c.ws(rgnn.LAYER_RGAT, d, d, H, p)
         fn = (lambda ws=ws, p=p: rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"],
                                                    c.T["w_dst"], out, saved, ws, d, d, H, 0.2,
@@ -208,6 +214,7 @@ def main():
     layers["rgat_fwd_am_like_880k_" + names[other]] = {
         "edges_per_s": E / (plans[other][0] * 1e-3), "ms": plans[other][0],
         "kernels_ms": {k: round(v[1], 4) for k, v in plans[other][1].items()}}
+    log("cpu baseline")
     cpu = None if args.no_cpu else cpu_baseline(c, args.cpu_seconds)
     line_kernels = {k: {"launches_per_step": n, "mean_ms": round(m, 4)} for k, (n, m) in kern.items()}
     c.close()
@@ -215,6 +222,7 @@ def main():
 
     if args.only == "all":
         # ------------------------------------------------ RGAT backward (workload 5 = graph 2)
+        log("workload 5: RGAT backward")
         c = Ctx(5)
         out = torch.empty(inf["num_nodes"], d, device=c.dev)
         saved = torch.empty(inf["num_nodes"], 1, 2, device=c.dev)
@@ -235,6 +243,7 @@ def main():
         del out, saved, wsf, gh, gW, gs, gt, wsb
 
         # ------------------------------------------------ HGT forward, workload 3
+        log("workload 3: HGT forward")
         c = Ctx(3)
         d3 = 64
         out = torch.empty(c.info["num_nodes"], d3, device=c.dev)
@@ -249,6 +258,7 @@ def main():
         del out, ws
 
         # ------------------------------------------------ RGCN and RGAT at d = 128, workload 4
+        log("workload 4: RGCN and RGAT at d = 128")
         c = Ctx(4)
         d4 = 128
         out = torch.empty(c.info["num_nodes"], d4, device=c.dev)
@@ -272,6 +282,7 @@ def main():
         del out
 
         # ------------------------------------------------ RGCN, workload 1 (small, launch-bound)
+        log("workload 1: RGCN")
         c = Ctx(1)
         out = torch.empty(c.info["num_nodes"], 64, device=c.dev)
         ws = c.ws(rgnn.LAYER_RGCN, 64, 64)

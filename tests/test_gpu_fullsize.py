@@ -140,7 +140,7 @@ def test_workload5_rgat_backward():
     dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"],
                                             t["grad_out"], node_mask=nm, rel_mask=rm)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
-    assert row_err(gh[nodes], dh[nodes], structural_zero=isolated[nodes]) <= TOL
+    assert row_err(gh[nodes], dh[nodes], structural_zero=isolated[nodes], cancel_floor=1e-6) <= TOL
     assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64)) <= TOL
     assert row_err(gs[rels], dws[rels]) <= TOL
     assert row_err(gt[rels], dwt[rels]) <= TOL

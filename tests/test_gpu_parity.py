@@ -159,7 +159,7 @@ def test_rgat_backward_small(kind):
     run.close()
     dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
-    assert row_err(gh, dh, structural_zero=isolated) <= TOL
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
     assert row_err(gs, dws) <= TOL
     assert row_err(gt, dwt) <= TOL
