@@ -138,7 +138,7 @@ size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *bas
     return c.off;
 }
 
-struct RgatWs { float *M, *atts, *wsp, *wtp, *partial, *S, *vstat, *T, *saved; };
+struct RgatWs { float *M, *atts, *wsp, *wtp, *vatt, *partial, *S, *vstat, *vscale, *T, *saved; };
 size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, void *base,
                    RgatWs *w)
 {
@@ -146,6 +146,7 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     RgatWs x{};
     x.wsp = c.take<float>((size_t)g->R * H * d_in);
     x.wtp = c.take<float>((size_t)g->R * H * d_in);
+    x.vatt = c.take<float>((size_t)g->V * H);
     if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
         x.M = c.take<float>((size_t)g->U_src * d_out);
         x.atts = c.take<float>((size_t)g->U_src * H);
@@ -153,6 +154,7 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     } else {
         x.S = c.take<float>((size_t)g->V * d_in);
         x.vstat = c.take<float>((size_t)g->V * 2);
+        x.vscale = c.take<float>((size_t)g->V);
         x.T = c.take<float>((size_t)g->V * d_out);
         x.saved = c.take<float>((size_t)g->N * 2);
     }
@@ -336,7 +338,8 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
         ta.g = g; ta.M = w.M; ta.d = d_out; ta.out = out; ta.partial = w.partial;
         ta.relu = relu_in_traversal;
         if ((st = launch_rgcn_traverse_tf(ta, s)) != RGNN_OK) return st;
-        if ((st = launch_merge_partials(ta, 0, s)) != RGNN_OK) return st;
+        if ((st = launch_merge_partials(g, d_out, 1, 0, w.partial, out, nullptr, ta.relu, s)) != RGNN_OK)
+            return st;
     } else {
         TravArgs ta;
         ta.g = g; ta.h = h; ta.d = d_in; ta.S = w.S;
@@ -389,8 +392,14 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     RgatWs w;
     rgat_layout(g, d_in, d_out, heads, plan, ws, &w);
     hipStream_t s = (hipStream_t)stream;
-    // linear operator reordering: W_r w_dst[r] (and W_r w_src[r]) once per relation
+    // linear operator reordering: W_r w_dst[r] (and W_r w_src[r]) once per relation,
+    // then the destination term h_v . (W_r w_dst[r]) once per (dst, rel) segment
     if ((st = launch_reorder_vec(W, w_dst, g->R, d_in, d_out, heads, w.wtp, s)) != RGNN_OK) return st;
+    {
+        TravArgs ta;
+        ta.g = g; ta.h = h; ta.wtp = w.wtp; ta.heads = heads; ta.d = d_in; ta.vatt = w.vatt;
+        if ((st = launch_seg_attn(ta, s)) != RGNN_OK) return st;
+    }
     if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
         GemmArgs ga;
         ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
@@ -400,17 +409,19 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         ga.ep.dot_vec = w_src; ga.ep.dot_out = w.atts; ga.ep.dot_heads = heads;
         if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         TravArgs ta;
-        ta.g = g; ta.h = h; ta.M = w.M; ta.atts = w.atts; ta.wtp = w.wtp;
+        ta.g = g; ta.h = h; ta.M = w.M; ta.atts = w.atts; ta.wtp = w.wtp; ta.vatt = w.vatt;
         ta.slope = neg_slope; ta.heads = heads; ta.d = d_out;
         ta.out = out; ta.saved = saved; ta.partial = w.partial;
         if ((st = launch_rgat_traverse_tf(ta, s)) != RGNN_OK) return st;
-        if ((st = launch_merge_partials(ta, 1, s)) != RGNN_OK) return st;
+        if ((st = launch_merge_partials(g, d_out, heads, 1, w.partial, out, saved, 0, s)) != RGNN_OK)
+            return st;
     } else {
         if ((st = launch_reorder_vec(W, w_src, g->R, d_in, d_out, 1, w.wsp, s)) != RGNN_OK) return st;
         float *stats = saved ? saved : w.saved;
         TravArgs ta;
-        ta.g = g; ta.h = h; ta.wsp = w.wsp; ta.wtp = w.wtp; ta.slope = neg_slope;
+        ta.g = g; ta.h = h; ta.wsp = w.wsp; ta.wtp = w.wtp; ta.vatt = w.vatt; ta.slope = neg_slope;
         ta.heads = 1; ta.d = d_in; ta.S = w.S; ta.vstat = w.vstat; ta.saved = stats;
+        ta.vscale = w.vscale;
         if ((st = launch_rgat_traverse_af(ta, s)) != RGNN_OK) return st;
         if ((st = launch_vseg_stats(ta, s)) != RGNN_OK) return st;
         GemmArgs ga;
@@ -418,8 +429,7 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
         ga.Y = w.T; ga.ldy = d_out; ga.scatter = g->dev.vseg_byrel;
-        ga.ep.scale_mode = 1; ga.ep.seg_stat = w.vstat; ga.ep.row_dst = g->dev.vseg_dst;
-        ga.ep.dst_stat = stats;
+        ga.ep.row_scale = w.vscale;
         if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         if ((st = launch_vseg_reduce(g, w.T, d_out, out, 0, 0, s)) != RGNN_OK) return st;
     }
@@ -461,7 +471,8 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     ha.g = g; ha.KV = w.KV; ha.Q = w.Q; ha.Watt = Watt; ha.Wmsg = Wmsg; ha.mu = mu;
     ha.scale = att_scale; ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
     if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
-    if ((st = launch_hgt_merge(ha, s)) != RGNN_OK) return st;
+    if ((st = launch_merge_partials(g, d, heads, 1, w.partial, w.agg, nullptr, 0, s)) != RGNN_OK)
+        return st;
     if (flags & RGNN_FLAG_A_LINEAR) {
         GemmArgs gb;
         gb.X = w.agg; gb.ldx = d; gb.gather = g->dev.ntype_perm; gb.scatter = g->dev.ntype_perm;

@@ -162,9 +162,30 @@ __global__ __launch_bounds__(256) void merge_s_kernel(int64_t n_split, const int
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n_split) return;
+    if (split_slotptr[i + 1] - split_slotptr[i] > kBigRange) return;
     float s = 0.f;
     for (int sl = split_slotptr[i]; sl < split_slotptr[i + 1]; ++sl) s += ssum[sl];
     sv[split_dst[i]] = s;
+}
+
+// One workgroup per split destination with many partials; thread sums are
+// added in thread order.
+__global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_split,
+                                                          const int32_t *split_dst,
+                                                          const int32_t *split_slotptr,
+                                                          const float *ssum, float *sv)
+{
+    __shared__ float part[256];
+    const int i = big_split[blockIdx.x];
+    float s = 0.f;
+    for (int sl = split_slotptr[i] + (int)threadIdx.x; sl < split_slotptr[i + 1]; sl += 256) s += ssum[sl];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float t = 0.f;
+        for (int j = 0; j < 256; ++j) t += part[j];
+        sv[split_dst[i]] = t;
+    }
 }
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -222,7 +243,7 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
                                                            float *dW, float *dws, float *dwt)
 {
     __shared__ float pws[D], pwt[D];
-    const int r = blockIdx.x, tid = threadIdx.x;
+    const int r = blockIdx.x, tid = threadIdx.x;   // blockIdx.y: which 256 entries of dW_r
     if (tid < D) {
         float a = 0.f, b = 0.f;
         for (int c = 0; c < copies; ++c) {
@@ -233,14 +254,15 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
     }
     __syncthreads();
     const int c0 = rel_chunkptr[r], c1 = rel_chunkptr[r + 1];
-    for (int idx = tid; idx < D * D; idx += 256) {
+    {
+        const int idx = blockIdx.y * 256 + tid;
         const int i = idx / D, j = idx % D;
         float s = 0.f;
         for (int c = c0; c < c1; ++c) s += partial[(size_t)c * D * D + idx];
         s += pws[i] * w_src[(size_t)r * D + j] + pwt[i] * w_dst[(size_t)r * D + j];
         dW[(size_t)r * D * D + idx] = s;
     }
-    if (tid < D) {
+    if (blockIdx.y == 0 && tid < D) {
         float a = 0.f, b = 0.f;
         for (int i = 0; i < D; ++i) {
             const float wij = W[((size_t)r * D + i) * D + tid];
@@ -344,6 +366,12 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                                    s, g->n_split, g->dev.split_dst, g->dev.split_slotptr, w.ssum, w.sv);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s launch");
+            if (g->n_big_split) {
+                LaunchScope ls("rgat_bwd_merge_s_big", s);
+                hipLaunchKernelGGL(merge_s_big_kernel, dim3((unsigned)g->n_big_split), dim3(256), 0, s,
+                                   g->dev.big_split, g->dev.split_dst, g->dev.split_slotptr, w.ssum, w.sv);
+            }
+            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
             {
                 LaunchScope ls("rgat_bwd_traverse", s);
                 hipLaunchKernelGGL((rgat_bwd_kernel<1>), dim3(grid.x, 1), dim3(256), 0, s, k);
@@ -359,7 +387,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");
     {
         LaunchScope ls("rgat_bwd_finalize", s);
-        hipLaunchKernelGGL(bwd_finalize_kernel, dim3((unsigned)g->R), dim3(256), 0, s, w.partial,
+        hipLaunchKernelGGL(bwd_finalize_kernel, dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
                            g->dev.rel_chunkptr, w.acc_ws, w.acc_wt, kCopies, g->R, W, w_src, w_dst,
                            dW, dws, dwt);
     }

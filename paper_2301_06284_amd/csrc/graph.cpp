@@ -181,6 +181,14 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         g->n_items = (int64_t)x.items.size();
         g->n_split = (int64_t)x.split_dst.size();
         g->n_slots = slots;
+        x.big_split.clear();
+        for (int64_t i = 0; i < g->n_split; ++i)
+            if (x.split_slotptr[i + 1] - x.split_slotptr[i] > kBigRange) x.big_split.push_back((int32_t)i);
+        x.big_vdst.clear();
+        for (int64_t u = 0; u < N; ++u)
+            if (x.dst_vsegptr[u + 1] - x.dst_vsegptr[u] > kBigRange) x.big_vdst.push_back((int32_t)u);
+        g->n_big_split = (int64_t)x.big_split.size();
+        g->n_big_vdst = (int64_t)x.big_vdst.size();
 
         // ---- GEMM tile tables ----
         build_tiles(x.uniq_rel_ptr, kGemmTileRows, x.tiles_pairs);
@@ -228,6 +236,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.vsegdst_byrel, x.vsegdst_byrel); add32(&d.rel_chunkptr, x.rel_chunkptr);
     add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
     add32(&d.split_slotptr, x.split_slotptr);
+    add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});

@@ -167,31 +167,6 @@ __global__ __launch_bounds__(512) void hgt_kernel(HK k)
     }
 }
 
-template <int H>
-__global__ __launch_bounds__(256) void hgt_merge_kernel(int64_t n_split, const int32_t *split_dst,
-                                                        const int32_t *split_slotptr,
-                                                        const float *partial, float *agg)
-{
-    constexpr int LH = D / H / 4, GPB = 256 / G, REC = 2 * H + D;
-    const int gl = threadIdx.x % G;
-    const int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
-    if (i >= n_split) return;
-    const int v = split_dst[i];
-    const int b = split_slotptr[i], e = split_slotptr[i + 1];
-    const int head = gl / LH;
-    float M = -INFINITY;
-    for (int sl = b; sl < e; ++sl) M = fmaxf(M, partial[(size_t)sl * REC + head * 2]);
-    float Z = 0.f;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sl = b; sl < e; ++sl) {
-        const float *pr = partial + (size_t)sl * REC;
-        const float c = __expf(pr[head * 2] - M);
-        Z += pr[head * 2 + 1] * c;
-        acc = lin4(acc, 1.f, ld4(pr + 2 * H + gl * 4), c);
-    }
-    st4(agg + (size_t)v * D + gl * 4, scale4(acc, Z > 0.f ? 1.f / Z : 0.f));
-}
-
 }  // namespace
 
 size_t hgt_lds_bytes(int R, int heads)
@@ -224,23 +199,6 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
 #undef HGT
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt traversal launch");
-}
-
-rgnn_status launch_hgt_merge(const HgtArgs &a, hipStream_t s)
-{
-    const rgnn_graph *g = a.g;
-    if (g->n_split == 0) return RGNN_OK;
-    LaunchScope ls("hgt_merge", s);
-    const unsigned nb = (unsigned)((g->n_split + 15) / 16);
-#define HM(H) hipLaunchKernelGGL((hgt_merge_kernel<H>), dim3(nb), dim3(256), 0, s, g->n_split, \
-                                 g->dev.split_dst, g->dev.split_slotptr, a.partial, a.agg)
-    if (a.heads == 1) HM(1);
-    else if (a.heads == 2) HM(2);
-    else if (a.heads == 4) HM(4);
-    else return fail(RGNN_EUNSUPPORTED, "HGT merge supports heads in {1, 2, 4}");
-#undef HM
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt merge launch");
 }
 
 }  // namespace rgnn

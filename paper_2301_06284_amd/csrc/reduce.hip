@@ -1,0 +1,410 @@
+// reduce.hip -- per-destination reductions and small helpers of the layers:
+// merging the partial softmax states of destinations split over several work
+// items, per-destination softmax statistics and sums over (dst, rel) segment
+// rows for the aggregate-first plan, the reordered attention vectors
+// W_r w[r] (linear operator reordering), fill / ReLU / add.
+// Every reduction runs in a fixed order, so results are reproducible bit for bit.
+#include "rgnn_internal.h"
+
+namespace rgnn {
+
+namespace {
+
+__device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+__device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
+__device__ __forceinline__ float4 scale4(float4 a, float s) { return make_float4(a.x * s, a.y * s, a.z * s, a.w * s); }
+__device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
+{
+    return make_float4(a.x * s + b.x * t, a.y * s + b.y * t, a.z * s + b.z * t, a.w * s + b.w * t);
+}
+__device__ __forceinline__ float4 relu4(float4 a)
+{
+    return make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
+}
+
+// Destinations with more than kBigRange segments are left to the block kernel.
+// Also writes, per segment, the scale exp(m_seg - M_v) / Z_v that finishes the
+// softmax when the typed GEMM applies W_r to the segment's sum.
+__global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *dst_vsegptr,
+                                                         const float *vstat, float *saved,
+                                                         float *vscale)
+{
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (v >= N) return;
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    if (e - b > kBigRange) return;
+    float M = -INFINITY;
+    for (int i = b; i < e; ++i) M = fmaxf(M, vstat[(size_t)i * 2]);
+    float Z = 0.f;
+    for (int i = b; i < e; ++i) Z += vstat[(size_t)i * 2 + 1] * __expf(vstat[(size_t)i * 2] - M);
+    saved[v * 2] = b < e ? M : 0.f;
+    saved[v * 2 + 1] = Z;
+    for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)i * 2] - M) / Z;
+}
+
+// One workgroup per destination with many segments: strided per-thread
+// partial (max, sum), combined in thread order through LDS.
+__global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_vdst,
+                                                             const int32_t *dst_vsegptr,
+                                                             const float *vstat, float *saved,
+                                                             float *vscale)
+{
+    __shared__ float sm[256], ss[256];
+    __shared__ float fin[2];
+    const int v = big_vdst[blockIdx.x];
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    float m = -INFINITY, s = 0.f;
+    for (int i = b + (int)threadIdx.x; i < e; i += 256) {
+        const float mi = vstat[(size_t)i * 2], si = vstat[(size_t)i * 2 + 1];
+        const float mn = fmaxf(m, mi);
+        s = s * __expf(m - mn) + si * __expf(mi - mn);
+        m = mn;
+    }
+    sm[threadIdx.x] = m;
+    ss[threadIdx.x] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float M = -INFINITY;
+        for (int t = 0; t < 256; ++t) M = fmaxf(M, sm[t]);
+        float Z = 0.f;
+        for (int t = 0; t < 256; ++t)
+            if (ss[t] > 0.f) Z += ss[t] * __expf(sm[t] - M);
+        saved[(size_t)v * 2] = M;
+        saved[(size_t)v * 2 + 1] = Z;
+        fin[0] = M;
+        fin[1] = Z;
+    }
+    __syncthreads();
+    const float M = fin[0], Zi = 1.f / fin[1];
+    for (int i = b + (int)threadIdx.x; i < e; i += 256) vscale[i] = __expf(vstat[(size_t)i * 2] - M) * Zi;
+}
+
+// out_v (+)= sum of the transformed segment rows of v (then optional ReLU).
+template <int D>
+__global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
+                                                          const float *T, float *out,
+                                                          int accumulate, int relu)
+{
+    constexpr int G = D / 4, GPB = 256 / G;
+    const int gl = threadIdx.x % G;
+    const int64_t v = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
+    if (v >= N) return;
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    if (e - b > kBigRange) return;
+    float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = b; i < e; ++i) acc = add4(acc, ld4(T + (size_t)i * D + gl * 4));
+    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
+}
+
+// One 1024-thread workgroup per destination with many segments: every group
+// of D/4 lanes sums a strided subset of the rows, the group sums are then
+// added in group order.
+template <int D>
+__global__ __launch_bounds__(1024) void vseg_reduce_big_kernel(const int32_t *big_vdst,
+                                                               const int32_t *dst_vsegptr,
+                                                               const float *T, float *out,
+                                                               int accumulate, int relu)
+{
+    constexpr int G = D / 4, NG = 1024 / G;
+    __shared__ float4 part[NG * G];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    const int v = big_vdst[blockIdx.x];
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = b + gi; i < e; i += NG) acc = add4(acc, ld4(T + (size_t)i * D + gl * 4));
+    part[gi * G + gl] = acc;
+    __syncthreads();
+    if (gi == 0) {
+        float4 tot = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < NG; ++j) tot = add4(tot, part[j * G + gl]);
+        st4(out + (size_t)v * D + gl * 4, relu ? relu4(tot) : tot);
+    }
+}
+
+// ---------------------------------------------------------------- merges
+// Combine the partials of destinations split over several items, in slot
+// order.  softmax: partial = (m, s) per head then acc[D]; else acc only.
+template <int D, int H, bool SOFTMAX>
+__global__ __launch_bounds__(256) void merge_kernel(int64_t n_split, const int32_t *split_dst,
+                                                    const int32_t *split_slotptr,
+                                                    const float *partial, float *out,
+                                                    float *saved, int relu)
+{
+    constexpr int G = D / 4, GPB = 256 / G, LH = D / H / 4;
+    constexpr int REC = SOFTMAX ? 2 * H + D : 2 + D;
+    constexpr int OFF = SOFTMAX ? 2 * H : 2;
+    const int gl = threadIdx.x % G;
+    const int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
+    if (i >= n_split) return;
+    const int v = split_dst[i];
+    const int b = split_slotptr[i], e = split_slotptr[i + 1];
+    if (e - b > kBigRange) return;
+    const int head = gl / LH;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (SOFTMAX) {
+        float M = -INFINITY;
+        for (int sl = b; sl < e; ++sl) M = fmaxf(M, partial[(size_t)sl * REC + head * 2]);
+        float Z = 0.f;
+        for (int sl = b; sl < e; ++sl) {
+            const float *pr = partial + (size_t)sl * REC;
+            const float c = __expf(pr[head * 2] - M);
+            Z += pr[head * 2 + 1] * c;
+            acc = lin4(acc, 1.f, ld4(pr + OFF + gl * 4), c);
+        }
+        acc = scale4(acc, Z > 0.f ? 1.f / Z : 0.f);
+        if (saved && gl % LH == 0) {
+            saved[((size_t)v * H + head) * 2] = M;
+            saved[((size_t)v * H + head) * 2 + 1] = Z;
+        }
+    } else {
+        for (int sl = b; sl < e; ++sl) acc = add4(acc, ld4(partial + (size_t)sl * REC + OFF + gl * 4));
+    }
+    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
+}
+
+// One 1024-thread workgroup per destination split over many items: each
+// group of D/4 lanes merges a strided subset of the partials, then group 0
+// merges the group states in group order.
+template <int D, int H, bool SOFTMAX>
+__global__ __launch_bounds__(1024) void merge_big_kernel(const int32_t *big_split,
+                                                         const int32_t *split_dst,
+                                                         const int32_t *split_slotptr,
+                                                         const float *partial, float *out,
+                                                         float *saved, int relu)
+{
+    constexpr int G = D / 4, NG = 1024 / G, LH = D / H / 4;
+    constexpr int REC = SOFTMAX ? 2 * H + D : 2 + D;
+    constexpr int OFF = SOFTMAX ? 2 * H : 2;
+    __shared__ float4 pacc[NG * G];
+    __shared__ float pm[NG * H], ps[NG * H];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    const int i = big_split[blockIdx.x];
+    const int v = split_dst[i];
+    const int b = split_slotptr[i], e = split_slotptr[i + 1];
+    const int head = gl / LH;
+    float m = -INFINITY, s = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sl = b + gi; sl < e; sl += NG) {
+        const float *pr = partial + (size_t)sl * REC;
+        const float4 a = ld4(pr + OFF + gl * 4);
+        if (SOFTMAX) {
+            const float mi = pr[head * 2], si = pr[head * 2 + 1];
+            const float mn = fmaxf(m, mi);
+            const float c1 = __expf(m - mn), c2 = __expf(mi - mn);
+            s = s * c1 + si * c2;
+            acc = lin4(acc, c1, a, c2);
+            m = mn;
+        } else {
+            acc = add4(acc, a);
+        }
+    }
+    pacc[gi * G + gl] = acc;
+    if (gl % LH == 0) { pm[gi * H + head] = m; ps[gi * H + head] = s; }
+    __syncthreads();
+    if (gi != 0) return;
+    float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (SOFTMAX) {
+        float M = -INFINITY;
+        for (int j = 0; j < NG; ++j) M = fmaxf(M, pm[j * H + head]);
+        float Z = 0.f;
+        for (int j = 0; j < NG; ++j) {
+            if (!(ps[j * H + head] > 0.f)) continue;
+            const float c = __expf(pm[j * H + head] - M);
+            Z += ps[j * H + head] * c;
+            tot = lin4(tot, 1.f, pacc[j * G + gl], c);
+        }
+        tot = scale4(tot, Z > 0.f ? 1.f / Z : 0.f);
+        if (saved && gl % LH == 0) {
+            saved[((size_t)v * H + head) * 2] = M;
+            saved[((size_t)v * H + head) * 2 + 1] = Z;
+        }
+    } else {
+        for (int j = 0; j < NG; ++j) tot = add4(tot, pacc[j * G + gl]);
+    }
+    st4(out + (size_t)v * D + gl * 4, relu ? relu4(tot) : tot);
+}
+
+__global__ void fill_kernel(float *p, int64_t n, float v)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__global__ void relu_kernel(float *p, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = fmaxf(p[i], 0.f);
+}
+
+__global__ void add_kernel(float *out, const float *a, const float *b, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) out[i] = a[i] + b[i];
+}
+
+// Reordered attention vectors: out[r, k, i] = sum_{j in head k} W[r, i, j] v[r, j].
+__global__ __launch_bounds__(256) void reorder_vec_kernel(const float *W, const float *v, int R,
+                                                          int d_in, int d_out, int heads,
+                                                          float *out)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (r, k, i)
+    if (idx >= (int64_t)R * heads * d_in) return;
+    const int i = (int)(idx % d_in);
+    const int k = (int)((idx / d_in) % heads);
+    const int r = (int)(idx / ((int64_t)d_in * heads));
+    const int dh = d_out / heads;
+    const float *Wr = W + ((size_t)r * d_in + i) * d_out + k * dh;
+    const float *vr = v + (size_t)r * d_out + k * dh;
+    float s = 0.f;
+    for (int j = 0; j < dh; ++j) s += Wr[j] * vr[j];
+    out[idx] = s;
+}
+
+inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
+
+hipError_t last() { return hipGetLastError(); }
+
+}  // namespace
+
+rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
+                                  const float *partial, float *out, float *saved, int relu,
+                                  hipStream_t s)
+{
+    if (g->n_split == 0) return RGNN_OK;
+    const int32_t *sd = g->dev.split_dst, *sp = g->dev.split_slotptr, *bs = g->dev.big_split;
+    const unsigned nb = blocks_for(g->n_split, 256 / (d / 4));
+    const unsigned nbig = (unsigned)g->n_big_split;
+    {
+        LaunchScope ls("merge_partials", s);
+#define MERGE(D, H, SM) hipLaunchKernelGGL((merge_kernel<D, H, SM>), dim3(nb), dim3(256), 0, s, \
+                                           g->n_split, sd, sp, partial, out, saved, relu)
+        if (!softmax) {
+            if (d == 64) MERGE(64, 1, false);
+            else if (d == 128) MERGE(128, 1, false);
+            else return fail(RGNN_EUNSUPPORTED, "merge: d must be 64 or 128");
+        } else if (d == 64 && heads == 1) MERGE(64, 1, true);
+        else if (d == 64 && heads == 2) MERGE(64, 2, true);
+        else if (d == 64 && heads == 4) MERGE(64, 4, true);
+        else if (d == 128 && heads == 1) MERGE(128, 1, true);
+        else if (d == 128 && heads == 2) MERGE(128, 2, true);
+        else if (d == 128 && heads == 4) MERGE(128, 4, true);
+        else if (d == 128 && heads == 8) MERGE(128, 8, true);
+        else return fail(RGNN_EUNSUPPORTED, "merge: unsupported (d, heads)");
+#undef MERGE
+    }
+    hipError_t e = last();
+    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    if (nbig == 0) return RGNN_OK;
+    {
+        LaunchScope ls("merge_partials_big", s);
+#define MERGEB(D, H, SM) hipLaunchKernelGGL((merge_big_kernel<D, H, SM>), dim3(nbig), dim3(1024), 0, \
+                                            s, bs, sd, sp, partial, out, saved, relu)
+        if (!softmax) {
+            if (d == 64) MERGEB(64, 1, false);
+            else MERGEB(128, 1, false);
+        } else if (d == 64 && heads == 1) MERGEB(64, 1, true);
+        else if (d == 64 && heads == 2) MERGEB(64, 2, true);
+        else if (d == 64 && heads == 4) MERGEB(64, 4, true);
+        else if (d == 128 && heads == 1) MERGEB(128, 1, true);
+        else if (d == 128 && heads == 2) MERGEB(128, 2, true);
+        else if (d == 128 && heads == 4) MERGEB(128, 4, true);
+        else MERGEB(128, 8, true);
+#undef MERGEB
+    }
+    e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "merge_big launch");
+}
+
+rgnn_status launch_vseg_stats(const TravArgs &a, hipStream_t s)
+{
+    const rgnn_graph *g = a.g;
+    if (g->N == 0) return RGNN_OK;
+    {
+        LaunchScope ls("vseg_stats", s);
+        hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(g->N, 256)), dim3(256), 0, s, g->N,
+                           g->dev.dst_vsegptr, a.vstat, a.saved, a.vscale);
+    }
+    hipError_t e = last();
+    if (e != hipSuccess) return hip_fail(e, "vseg_stats launch");
+    if (g->n_big_vdst == 0) return RGNN_OK;
+    {
+        LaunchScope ls("vseg_stats_big", s);
+        hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)g->n_big_vdst), dim3(256), 0, s,
+                           g->dev.big_vdst, g->dev.dst_vsegptr, a.vstat, a.saved, a.vscale);
+    }
+    e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_stats_big launch");
+}
+
+rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
+                               int accumulate, int relu, hipStream_t s)
+{
+    if (g->N == 0) return RGNN_OK;
+    if (d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 64 or 128");
+    {
+        LaunchScope ls("vseg_reduce", s);
+        const unsigned nb = blocks_for(g->N, 256 / (d / 4));
+        if (d == 64)
+            hipLaunchKernelGGL((vseg_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, T, out, accumulate, relu);
+        else
+            hipLaunchKernelGGL((vseg_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, T, out, accumulate, relu);
+    }
+    hipError_t e = last();
+    if (e != hipSuccess) return hip_fail(e, "vseg_reduce launch");
+    if (g->n_big_vdst == 0) return RGNN_OK;
+    {
+        LaunchScope ls("vseg_reduce_big", s);
+        const unsigned nb = (unsigned)g->n_big_vdst;
+        if (d == 64)
+            hipLaunchKernelGGL((vseg_reduce_big_kernel<64>), dim3(nb), dim3(1024), 0, s,
+                               g->dev.big_vdst, g->dev.dst_vsegptr, T, out, accumulate, relu);
+        else
+            hipLaunchKernelGGL((vseg_reduce_big_kernel<128>), dim3(nb), dim3(1024), 0, s,
+                               g->dev.big_vdst, g->dev.dst_vsegptr, T, out, accumulate, relu);
+    }
+    e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce_big launch");
+}
+
+rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s)
+{
+    if (n == 0) return RGNN_OK;
+    LaunchScope ls("fill", s);
+    hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, p, n, v);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "fill launch");
+}
+
+rgnn_status launch_relu(float *p, int64_t n, hipStream_t s)
+{
+    if (n == 0) return RGNN_OK;
+    LaunchScope ls("relu", s);
+    hipLaunchKernelGGL(relu_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, p, n);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "relu launch");
+}
+
+rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s)
+{
+    if (n == 0) return RGNN_OK;
+    LaunchScope ls("add", s);
+    hipLaunchKernelGGL(add_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, out, a, b, n);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "add launch");
+}
+
+rgnn_status launch_reorder_vec(const float *W, const float *v, int R, int d_in, int d_out,
+                               int heads, float *out, hipStream_t s)
+{
+    const int64_t n = (int64_t)R * heads * d_in;
+    LaunchScope ls("reorder_vec", s);
+    hipLaunchKernelGGL(reorder_vec_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, W, v, R,
+                       d_in, d_out, heads, out);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "reorder_vec launch");
+}
+
+}  // namespace rgnn

@@ -17,7 +17,10 @@ constexpr int kChunkEdges = 64;
 // Maximum destinations bundled into one work item.
 constexpr int kMaxDstPerItem = 32;
 // Rows of one typed-GEMM tile (a tile never mixes weight types).
-constexpr int kGemmTileRows = 128;
+constexpr int kGemmTileRows = 512;
+// Reductions over more records than this (partials of a split destination,
+// segments of one destination) get a whole workgroup instead of one group.
+constexpr int kBigRange = 32;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
@@ -39,6 +42,8 @@ struct HostIndex {
     std::vector<int32_t> vseg_byrel, rel_vsegptr, vsegdst_byrel;
     std::vector<Item> items;
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
+    std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
+    std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
 };
@@ -56,6 +61,7 @@ struct DeviceIndex {
     int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr;
     Item *items = nullptr;
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
+    int32_t *big_split = nullptr, *big_vdst = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
 };
@@ -72,6 +78,7 @@ struct rgnn_graph {
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0;
+    int64_t n_big_split = 0, n_big_vdst = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
@@ -102,12 +109,8 @@ struct LaunchScope {   // records a hipEvent pair around one kernel launch when 
 // ---- kernel launchers (device .hip files) ----
 struct GemmEpilogue {
     // Optional per-row scale of the A rows (Section "Operator-Specific Schedule":
-    // a per-row scalar applied to the tiles of matrix A).  scale_mode:
-    //   0 none; 1 row scale = exp(seg_max[r] - dst_max[dst]) / dst_sum[dst]
-    int scale_mode = 0;
-    const float *seg_stat = nullptr;   // [rows, 2] (max, sum) per GEMM row (by scatter id)
-    const int32_t *row_dst = nullptr;  // destination of each GEMM row (by scatter id)
-    const float *dst_stat = nullptr;   // [N, 2] (max, sum)
+    // a per-row scalar applied to the tiles of matrix A), indexed by scatter id.
+    const float *row_scale = nullptr;
     // Optional row dot products of the output with a per-type vector, written to
     // dot_out[scatter_row * heads + head] (heads split the output columns).
     const float *dot_vec = nullptr;    // [types, Nc]
@@ -157,13 +160,21 @@ struct TravArgs {
     float *partial = nullptr;            // [slots, 2*heads + d]
     float *S = nullptr;                  // aggregate-first: [V, d] per-vseg sums
     float *vstat = nullptr;              // aggregate-first: [V, 2] per-vseg (max, sum)
+    float *vatt = nullptr;               // [V, heads] destination attention term per vseg
+    float *vscale = nullptr;             // aggregate-first: [V] softmax scale per vseg
     int relu = 0;
 };
+// vatt[vs, k] = h_v . wtp[r, k] for every virtual segment (v, r).
+rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgcn_traverse_af(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgat_traverse_af(const TravArgs &a, hipStream_t s);
-rgnn_status launch_merge_partials(const TravArgs &a, int softmax, hipStream_t s);
+// Finish destinations split over several work items: combine their partials
+// (softmax: (max, sum) per head then the D-vector; else the D-vector only).
+rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
+                                  const float *partial, float *out, float *saved, int relu,
+                                  hipStream_t s);
 rgnn_status launch_vseg_stats(const TravArgs &a, hipStream_t s);
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
                                int accumulate, int relu, hipStream_t s);
@@ -182,7 +193,6 @@ struct HgtArgs {
     float *partial = nullptr;      // [slots, 2*heads + d]
 };
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
-rgnn_status launch_hgt_merge(const HgtArgs &a, hipStream_t s);
 
 struct BwdArgs {
     const rgnn_graph *g = nullptr;
