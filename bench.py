@@ -40,6 +40,8 @@ def parse():
     p.add_argument("--only", choices=["headline", "all"], default="all",
                    help="headline: time only the RGAT workload of the headline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline leg")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="also run a 1 GiB device copy (reference for HBM byte counters)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target wall time of the CPU-baseline sample")
     return p.parse_args()
@@ -147,6 +149,23 @@ def roofline_of(kernels, model):
     return name, ms, gbs, tfl, m
 
 
+def counter_traffic(tag, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a copy of known size), or None
+    when there is none or the kernel's source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{tag}_hbm_counters.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))["kernels"].get(kernel)
+    if not rec or not rec.get("source"):
+        return None
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != rec["source_sha256_16"]:
+        return None
+    return rec["bytes_per_launch"]
+
+
 def cpu_baseline(ctx, target_s):
     import oracle
     g, t = ctx.g, ctx.t
@@ -194,7 +213,8 @@ def main():
     out = torch.empty(inf["num_nodes"], d, device=c.dev)
     saved = torch.empty(inf["num_nodes"], H, 2, device=c.dev)
     plans = {}
-    for p in (rgnn.PLAN_TRANSFORM_FIRST, rgnn.PLAN_AGGREGATE_FIRST):
+    other = rgnn.PLAN_AGGREGATE_FIRST if plan == rgnn.PLAN_TRANSFORM_FIRST else rgnn.PLAN_TRANSFORM_FIRST
+    for p in ((plan,) if args.only == "headline" else (plan, other)):
         log(f"workload 2: RGAT forward plan {p}")
         ws = c.ws(rgnn.LAYER_RGAT, d, d, H, p)
         fn = (lambda ws=ws, p=p: rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"],
@@ -205,15 +225,25 @@ def main():
         plans[p] = (ms, kern, fn)
         del ws
     ms, kern, fn = plans[plan]
-    other = rgnn.PLAN_AGGREGATE_FIRST if plan == rgnn.PLAN_TRANSFORM_FIRST else rgnn.PLAN_TRANSFORM_FIRST
     model = rgat_tf_model(inf, d, H) if plan == rgnn.PLAN_TRANSFORM_FIRST else rgat_af_model(inf, d)
     kname, kms, kgbs, ktfl, km = roofline_of(kern, model)
     E = inf["num_edges"]
     value = E / (ms * 1e-3)
     names = {1: "transform_first", 2: "aggregate_first"}
-    layers["rgat_fwd_am_like_880k_" + names[other]] = {
-        "edges_per_s": E / (plans[other][0] * 1e-3), "ms": plans[other][0],
-        "kernels_ms": {k: round(v[1], 4) for k, v in plans[other][1].items()}}
+    if other in plans:
+        layers["rgat_fwd_am_like_880k_" + names[other]] = {
+            "edges_per_s": E / (plans[other][0] * 1e-3), "ms": plans[other][0],
+            "kernels_ms": {k: round(v[1], 4) for k, v in plans[other][1].items()}}
+    if args.calibrate_copy:
+        # a plain device copy of known size, for scaling the FETCH_SIZE /
+        # WRITE_SIZE counters of a profiling run (1 GiB read + 1 GiB written)
+        log("copy calibration")
+        src = torch.ones(1 << 28, device=c.dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     log("cpu baseline")
     cpu = None if args.no_cpu else cpu_baseline(c, args.cpu_seconds)
     line_kernels = {k: {"launches_per_step": n, "mean_ms": round(m, 4)} for k, (n, m) in kern.items()}
@@ -320,7 +350,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": kgbs / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": counter_traffic("rgat_am_like_880k", kname),
             "mean_ms": kms,
             "algorithmic_bytes": km["bytes"],
             "algorithmic_tflops": ktfl,
