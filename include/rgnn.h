@@ -110,7 +110,10 @@ typedef enum {
     RGNN_IDX_UNIQ_REL_PTR = 8,  /* [R+1]     pair offsets per relation             */
     RGNN_IDX_EDGE2UNIQ = 9,     /* [E]       pair index of each sorted in-edge     */
     RGNN_IDX_NTYPE_PERM = 10,   /* [N]       node ids, stable-sorted by node type  */
-    RGNN_IDX_NTYPE_PTR = 11     /* [T+1]     offsets of the node-type segments     */
+    RGNN_IDX_NTYPE_PTR = 11,    /* [T+1]     offsets of the node-type segments     */
+    RGNN_IDX_OUT_PTR = 12,      /* [N+1]     out-edge offsets per source node      */
+    RGNN_IDX_OUT_POS = 13       /* [E]       sorted in-edge position of each out-edge,
+                                             out-edges in (src, rel, position) order */
 } rgnn_index_kind;
 
 /* ------------------------------------------------------------------ graph */

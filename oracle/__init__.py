@@ -186,6 +186,8 @@ def graph_index(g) -> dict:
         edge2uniq [E], the pair index of each edge in the sorted in-edge order
     * node-type segments: ntype_perm [N] (node ids, stable by type),
         ntype_ptr [T+1]
+    * out-edges: out_ptr [N+1] (out-edge offsets per source) and out_pos [E],
+        the sorted in-edge positions ordered by (src, rel, position)
     All arrays are int64 here; only their values are compared.
     """
     N, E, R, T = g["N"], g["E"], g["R"], g["T"]
@@ -216,7 +218,11 @@ def graph_index(g) -> dict:
     ntype_perm = np.argsort(ntype, kind="stable").astype(np.int64)
     ntype_ptr = np.zeros(T + 1, np.int64)
     np.cumsum(np.bincount(ntype, minlength=T), out=ntype_ptr[1:])
-    return dict(dst_rowptr=dst_rowptr, in_src=in_src, in_rel=in_rel, in_eid=order,
+    position = np.arange(E, dtype=np.int64)
+    out_pos = np.lexsort((position, in_rel, in_src))
+    out_ptr = np.zeros(N + 1, np.int64)
+    np.cumsum(np.bincount(src, minlength=N), out=out_ptr[1:])
+    return dict(out_ptr=out_ptr, out_pos=out_pos,dst_rowptr=dst_rowptr, in_src=in_src, in_rel=in_rel, in_eid=order,
                 seg_ptr=seg_ptr, seg_rel=seg_rel, dst_segptr=dst_segptr,
                 uniq_src=uniq_src, uniq_rel_ptr=uniq_rel_ptr, edge2uniq=edge2uniq,
                 ntype_perm=ntype_perm, ntype_ptr=ntype_ptr,

@@ -12,13 +12,6 @@
 
 namespace rgnn {
 
-size_t hgt_lds_bytes(int R, int heads);
-rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
-                               const float *w_src, const float *w_dst, int d_in, int d_out,
-                               float slope, const float *saved, const float *G, float *dh,
-                               float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
-                               hipStream_t s, size_t *need);
-
 namespace {
 thread_local std::string g_err;
 }

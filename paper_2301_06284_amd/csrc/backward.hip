@@ -8,16 +8,30 @@
 //   dalpha_e = G_v . (h_u W_r) = h_u . dS_{v,r},   dS_{v,r} = G_v W_r^T
 //   s_v      = sum_e alpha_e dalpha_e
 //   Y_e      = alpha_e (dalpha_e - s_v) leaky'(y_e)
-//   dh_u    += alpha_e dS_{v,r} + Y_e ws'_r       (atomic scatter)
-//   dh_v    += Y_e wt'_r
+//   dh_u    += alpha_e dS_{v,r} + Y_e ws'_r       (u as a source)
+//   dh_v    += Y_e wt'_r                          (v as a destination)
 //   dW_r     = sum_seg (sum_e alpha_e h_u)^T G_v  +  dws'_r^T w_src[r] + dwt'_r^T w_dst[r]
 //              with dws'_r = sum_e Y_e h_u,  dwt'_r = sum_e Y_e h_v
 //   dw_src[r] = dws'_r W_r,   dw_dst[r] = dwt'_r W_r
-// Kernel sequence: dS by the typed GEMM (B = W_r^T) over (dst, rel) segments;
-// a traversal that recomputes the attention and scatters dh with float atomics
-// after summing within each lane's segment (the paper's partial aggregation
-// before atomics); an outer-product MFMA GEMM for dW over K-chunks of
-// segments with a deterministic combine; and a per-relation finalize.
+//
+// Kernel sequence:
+//   1. dS by the typed GEMM (B = W_r^T) over the (dst, rel) segments, and the
+//      destination attention terms h_v . wt'_r per segment.
+//   2. A destination-major traversal over the forward's work items.  Pass 1
+//      streams the source rows with the next batch in flight and recomputes
+//      alpha, dalpha per edge (kept in LDS), s_v per destination and
+//      Sa = sum alpha h_u per segment; pass 2 forms Y per edge and its sum per
+//      segment.  Pieces of split destinations finish pass 2 in a second launch
+//      once their s_v partials are merged.
+//   3. dh_v's destination term, sum over v's segments of ysum * wt'_r.
+//   4. A source-major traversal over the out-edges (sorted by source, then
+//      relation) that gathers dS rows and adds alpha dS + Y ws'_r into dh_u:
+//      the scatter of the paper's backward becomes a gather, so there are no
+//      per-edge atomics, only one add per source row.  dws' is accumulated per
+//      (source, relation) run in LDS and written once per workgroup.
+//   5. An outer-product MFMA GEMM for dW over K-chunks of segments of one
+//      relation (also summing ysum * h_v per chunk for dwt'), then a
+//      deterministic combine and a per-relation finalize.
 #include "rgnn_internal.h"
 
 namespace rgnn {
@@ -25,13 +39,17 @@ namespace rgnn {
 namespace {
 
 constexpr int D = 64, G = 16;
-constexpr int kUnroll = 4;
-constexpr int kCopies = 64;       // privatized copies of the per-relation accumulators
-constexpr int kOuterRows = 2048;  // segments per outer-product K-chunk
+constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
+constexpr int kU = 4;              // rows per prefetch batch in the traversals
+constexpr int kAccBlocks = 768;    // workgroups of the source-major traversal (one dws' slot each)
+constexpr int kLdsAccRels = 128;   // relations whose dws' accumulators fit in LDS
+constexpr int kOuterRows = 2048;   // segments per outer-product K-chunk
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 __device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
+__device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 {
     return make_float4(a.x * s + b.x * t, a.y * s + b.y * t, a.z * s + b.z * t, a.w * s + b.w * t);
@@ -49,110 +67,173 @@ __device__ __forceinline__ float gsum(float x)
     return x;
 }
 
+// ---------------------------------------------------------------- destination-major traversal
 struct BK {
     int64_t n_items;
     const Item *items;
     const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *in_src;
-    const float *h, *wsp, *wtp, *saved, *dS, *sv_in;
+    const float *h, *wsp, *saved, *dS, *vatt, *sv_in;
     float slope;
-    float *Sa, *ssum, *dh, *acc_ws, *acc_wt;
-    int copies, R;
+    float *Sa;       // [V, D]  sum alpha h_u per segment
+    float *ssum;     // [slots] s_v partial of each piece of a split destination
+    float *ay;       // [E, 2]  per sorted in-edge: (alpha, Y); pieces hold (signed alpha, dalpha) in between
+    float *ysum;     // [V]     sum of Y per segment
 };
 
-// PHASE 0: every item; whole destinations run both passes, pieces of split
-//          destinations run the first pass and leave their part of s_v.
-// PHASE 1: pieces of split destinations only, second pass with the merged s_v.
+struct BStage {
+    int eidx[kE];        // source of each edge
+    int evs[kE];         // item-local segment of each edge
+    int vptr[kE + 1];    // item-local first edge of each segment
+    int vrel[kE];
+    int vdj[kE];         // item-local destination of each segment
+    float vatt[kE];      // h_v . wt'_r of each segment
+    float ea[kE];        // alpha of each edge, sign bit set where the logit is <= 0
+    float eda[kE];       // dalpha of each edge
+    int dptr[kDst + 1];  // item-local first edge of each destination
+    float dM[kDst], dZi[kDst], dsv[kDst];   // per destination: M_v, 1/Z_v, s_v
+};
+
+// PHASE 0: every item.  Whole destinations run both passes; pieces of split
+//          destinations run pass 1, leave their part of s_v in ssum and park
+//          (signed alpha, dalpha) in ay.
+// PHASE 1: pieces of split destinations only: pass 2 with the merged s_v.
 template <int PHASE>
-__global__ __launch_bounds__(256) void rgat_bwd_kernel(BK k)
+__global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
 {
     constexpr int GPB = 256 / G;
-    const int gl = threadIdx.x % G;
-    const int64_t item = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
-    if (item >= k.n_items) return;
-    const int slot = k.item_slot[item];
-    if (PHASE == 1 && slot < 0) return;
-    const Item it = k.items[item];
-    const int copy = blockIdx.x % k.copies;
-    for (int v = it.dst0; v < it.dst1; ++v) {
-        const int sb = max(it.vs0, k.dst_vsegptr[v]);
-        const int se = min(it.vs1, k.dst_vsegptr[v + 1]);
-        if (sb >= se) continue;
-        const float4 hv = ld4(k.h + (size_t)v * D + gl * 4);
-        const float Mv = k.saved[(size_t)v * 2];
-        const float Zinv = 1.f / k.saved[(size_t)v * 2 + 1];
-        float sacc = 0.f;
-        if (PHASE == 0) {
-            for (int vs = sb; vs < se; ++vs) {
-                const int r = k.vseg_rel[vs];
-                const float attt = gsum<G>(dot4(hv, ld4(k.wtp + (size_t)r * D + gl * 4)));
-                const float4 ws = ld4(k.wsp + (size_t)r * D + gl * 4);
-                const float4 ds = ld4(k.dS + (size_t)vs * D + gl * 4);
-                float4 sa = make_float4(0.f, 0.f, 0.f, 0.f);
-                const int e0 = k.vseg_ptr[vs], e1 = k.vseg_ptr[vs + 1];
-                for (int e = e0; e < e1; e += kUnroll) {
-                    int u_[kUnroll];
-                    float4 row[kUnroll];
+    __shared__ BStage stage[GPB];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    BStage &st = stage[gi];
+    const int64_t item = (int64_t)blockIdx.x * GPB + gi;
+    bool valid = item < k.n_items;
+    int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
+    if (valid) {
+        const Item x = k.items[item];
+        slot = k.item_slot[item];
+        dst0 = x.dst0; nd = x.dst1 - x.dst0; vs0 = x.vs0; nv = x.vs1 - x.vs0;
+        e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
+        if (PHASE == 1 && slot < 0) valid = false;
+    }
+    if (valid) {
+        for (int j = gl; j < nv; j += G) {
+            const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
+            st.vptr[j] = a;
+            st.vrel[j] = k.vseg_rel[vs0 + j];
+            st.vatt[j] = k.vatt[vs0 + j];
+            for (int e = a; e < b; ++e) st.evs[e] = j;
+        }
+        if (gl == 0) st.vptr[nv] = ne;
+        auto dvs = [&](int jj) {   // item-local first segment of destination jj
+            const int vs = k.dst_vsegptr[dst0 + jj];
+            return (vs < vs0 ? vs0 : (vs > vs0 + nv ? vs0 + nv : vs)) - vs0;
+        };
+        for (int j = gl; j < nd; j += G) {
+            const int a = dvs(j), b = dvs(j + 1);
+            st.dptr[j] = k.vseg_ptr[vs0 + a] - e0;
+            for (int jv = a; jv < b; ++jv) st.vdj[jv] = j;
+            const int64_t v = dst0 + j;
+            const float Z = k.saved[v * 2 + 1];
+            st.dM[j] = k.saved[v * 2];
+            st.dZi[j] = Z > 0.f ? 1.f / Z : 0.f;
+            if (PHASE == 1) st.dsv[j] = k.sv_in[v];
+        }
+        if (gl == 0) st.dptr[nd] = ne;
+        for (int e = gl; e < ne; e += G) {
+            if (PHASE == 0) {
+                st.eidx[e] = k.in_src[e0 + e];
+            } else {
+                const float2 p = reinterpret_cast<const float2 *>(k.ay)[e0 + e];
+                st.ea[e] = p.x;
+                st.eda[e] = p.y;
+            }
+        }
+    }
+    __syncthreads();
+
+    // pass 1: alpha, dalpha per edge; s_v per destination; Sa per segment
+    if (PHASE == 0 && valid && ne > 0) {
+        int j = 0, jv = 0;
+        while (st.dptr[j + 1] == st.dptr[j]) ++j;   // first destination with edges
+        float s = 0.f;
+        float4 sa = zero4();
+        // ping-pong batches of (source row, ws'_r row, dS row) per edge
+        float4 Ah[kU], Aw[kU], Ad[kU], Bh[kU], Bw[kU], Bd[kU];
+        auto load = [&](float4 (&Xh)[kU], float4 (&Xw)[kU], float4 (&Xd)[kU], int base) {
 #pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) u_[u] = k.in_src[min(e + u, e1 - 1)];
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u < ne ? base + u : ne - 1;
+                const int jj = st.evs[e];
+                Xh[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
+                Xw[u] = ld4(k.wsp + (size_t)st.vrel[jj] * D + gl * 4);
+                Xd[u] = ld4(k.dS + (size_t)(vs0 + jj) * D + gl * 4);
+            }
+        };
+        auto consume = [&](const float4 (&Xh)[kU], const float4 (&Xw)[kU], const float4 (&Xd)[kU],
+                           int base) {
 #pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) row[u] = ld4(k.h + (size_t)u_[u] * D + gl * 4);
-#pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) {
-                        const float y = gsum<G>(dot4(row[u], ws)) + attt;
-                        const float da = gsum<G>(dot4(row[u], ds));
-                        if (e + u < e1) {
-                            const float z = y > 0.f ? y : k.slope * y;
-                            const float al = __expf(z - Mv) * Zinv;
-                            sacc += al * da;
-                            sa = lin4(sa, 1.f, row[u], al);
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u;
+                const float ys = gsum<G>(dot4(Xh[u], Xw[u]));
+                const float da = gsum<G>(dot4(Xh[u], Xd[u]));
+                if (e < ne) {
+                    const float y = ys + st.vatt[jv];
+                    const float z = y > 0.f ? y : k.slope * y;
+                    const float al = __expf(z - st.dM[j]) * st.dZi[j];
+                    s += al * da;
+                    sa = lin4(sa, 1.f, Xh[u], al);
+                    if (gl == 0) {
+                        st.ea[e] = y > 0.f ? al : -al;
+                        st.eda[e] = da;
+                    }
+                    if (e + 1 == st.vptr[jv + 1]) {
+                        st4(k.Sa + (size_t)(vs0 + jv) * D + gl * 4, sa);
+                        sa = zero4();
+                        ++jv;
+                        if (e + 1 == st.dptr[j + 1]) {
+                            if (gl == 0) {
+                                if (slot < 0) st.dsv[j] = s;
+                                else k.ssum[slot] = s;
+                            }
+                            s = 0.f;
+                            ++j;
+                            while (j < nd && st.dptr[j + 1] == st.dptr[j]) ++j;
                         }
                     }
                 }
-                st4(k.Sa + (size_t)vs * D + gl * 4, sa);
             }
-            if (slot >= 0) {
-                if (gl == 0) k.ssum[slot] = sacc;
-                continue;
-            }
+        };
+        load(Ah, Aw, Ad, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int eb = 0; eb < ne; eb += 2 * kU) {
+            load(Bh, Bw, Bd, eb + kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(Ah, Aw, Ad, eb);
+            load(Ah, Aw, Ad, eb + 2 * kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(Bh, Bw, Bd, eb + kU);
         }
-        const float sv = PHASE == 0 ? sacc : k.sv_in[v];
-        float4 dhv = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int vs = sb; vs < se; ++vs) {
-            const int r = k.vseg_rel[vs];
-            const float4 wt = ld4(k.wtp + (size_t)r * D + gl * 4);
-            const float attt = gsum<G>(dot4(hv, wt));
-            const float4 ws = ld4(k.wsp + (size_t)r * D + gl * 4);
-            const float4 ds = ld4(k.dS + (size_t)vs * D + gl * 4);
-            float4 P = make_float4(0.f, 0.f, 0.f, 0.f);
-            float ysum = 0.f;
-            const int e0 = k.vseg_ptr[vs], e1 = k.vseg_ptr[vs + 1];
-            for (int e = e0; e < e1; e += kUnroll) {
-                int u_[kUnroll];
-                float4 row[kUnroll];
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) u_[u] = k.in_src[min(e + u, e1 - 1)];
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) row[u] = ld4(k.h + (size_t)u_[u] * D + gl * 4);
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const float y = gsum<G>(dot4(row[u], ws)) + attt;
-                    const float da = gsum<G>(dot4(row[u], ds));
-                    if (e + u < e1) {
-                        const float z = y > 0.f ? y : k.slope * y;
-                        const float al = __expf(z - Mv) * Zinv;
-                        const float Y = al * (da - sv) * (y > 0.f ? 1.f : k.slope);
-                        atomic_add4(k.dh + (size_t)u_[u] * D + gl * 4, lin4(ds, al, ws, Y));
-                        P = lin4(P, 1.f, row[u], Y);
-                        ysum += Y;
-                    }
-                }
+    }
+    __syncthreads();
+
+    if (PHASE == 0 && valid && slot >= 0) {
+        for (int e = gl; e < ne; e += G)
+            reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(st.ea[e], st.eda[e]);
+        return;
+    }
+    // pass 2: Y per edge and its sum per segment (segment-parallel over lanes)
+    if (valid) {
+        for (int jv = gl; jv < nv; jv += G) {
+            const float sv = st.dsv[st.vdj[jv]];
+            float ys = 0.f;
+            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) {
+                const float a = st.ea[e];
+                const float al = fabsf(a);
+                const float Y = al * (st.eda[e] - sv) * (signbit(a) ? k.slope : 1.f);
+                ys += Y;
+                reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
             }
-            atomic_add4(k.acc_ws + ((size_t)copy * k.R + r) * D + gl * 4, P);
-            atomic_add4(k.acc_wt + ((size_t)copy * k.R + r) * D + gl * 4,
-                        make_float4(hv.x * ysum, hv.y * ysum, hv.z * ysum, hv.w * ysum));
-            dhv = lin4(dhv, 1.f, wt, ysum);
+            k.ysum[vs0 + jv] = ys;
         }
-        atomic_add4(k.dh + (size_t)v * D + gl * 4, dhv);
     }
 }
 
@@ -188,32 +269,206 @@ __global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_spl
     }
 }
 
+// ---------------------------------------------------------------- dh_v destination term
+struct DK {
+    int64_t N;
+    const int32_t *dst_vsegptr, *vseg_rel;
+    const float *ysum, *wtp;
+    float *dh;
+};
+
+// dh_v = sum over v's segments of ysum * wt'_r; one 16-lane group per node
+// (every node, so this also initialises dh).  Nodes with more than kBigRange
+// segments are left to the workgroup kernel below.
+__global__ __launch_bounds__(256) void bwd_dst_term_kernel(DK k)
+{
+    const int gl = threadIdx.x % G;
+    const int64_t v = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;
+    if (v >= k.N) return;
+    const int a = k.dst_vsegptr[v], b = k.dst_vsegptr[v + 1];
+    if (b - a > kBigRange) return;
+    float4 acc = zero4();
+    for (int vs = a; vs < b; ++vs)
+        acc = lin4(acc, 1.f, ld4(k.wtp + (size_t)k.vseg_rel[vs] * D + gl * 4), k.ysum[vs]);
+    st4(k.dh + (size_t)v * D + gl * 4, acc);
+}
+
+__global__ __launch_bounds__(1024) void bwd_dst_term_big_kernel(DK k, const int32_t *big_vdst)
+{
+    constexpr int NG = 1024 / G;
+    __shared__ float4 part[NG][G];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    const int v = big_vdst[blockIdx.x];
+    const int a = k.dst_vsegptr[v], b = k.dst_vsegptr[v + 1];
+    float4 acc = zero4();
+    for (int vs = a + gi; vs < b; vs += NG)
+        acc = lin4(acc, 1.f, ld4(k.wtp + (size_t)k.vseg_rel[vs] * D + gl * 4), k.ysum[vs]);
+    part[gi][gl] = acc;
+    __syncthreads();
+    if (gi == 0) {
+        float4 t = zero4();
+        for (int i = 0; i < NG; ++i) t = add4(t, part[i][gl]);
+        st4(k.dh + (size_t)v * D + gl * 4, t);
+    }
+}
+
+// ---------------------------------------------------------------- source-major traversal
+struct SK {
+    int64_t n_items;
+    const Item *items;           // {node0, node1, q0, q1}: nodes and their out-edge range
+    const int32_t *out_ptr, *out_pos, *out_vseg, *vseg_rel;
+    const float *h, *wsp, *dS, *ay;
+    float *dh;
+    float *accP;                 // [gridDim.x, R, D] dws' partial of each workgroup
+    int R;
+};
+
+struct SStage {
+    int evs[kE];         // segment (dS row) of each out-edge
+    int erel[kE];
+    int enode[kE];       // item-local source of each out-edge
+    float ea[kE], ey[kE];
+    int optr[kDst + 1];  // item-local first out-edge of each source
+};
+
+// Grid-stride over the out-edge work items; the dws' accumulators of a
+// workgroup live in LDS (LDSACC) or in its own global slot.
+template <bool LDSACC>
+__global__ __launch_bounds__(256) void bwd_src_kernel(SK k)
+{
+    constexpr int GPB = 256 / G;
+    __shared__ SStage stage[GPB];
+    extern __shared__ float lds_acc[];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    SStage &st = stage[gi];
+    float *slot_acc = k.accP + (size_t)blockIdx.x * k.R * D;
+    float *acc_p = LDSACC ? lds_acc : slot_acc;
+    if (LDSACC)
+        for (int i = threadIdx.x; i < k.R * D; i += 256) lds_acc[i] = 0.f;
+    __syncthreads();
+    for (int64_t base = (int64_t)blockIdx.x * GPB; base < k.n_items; base += (int64_t)gridDim.x * GPB) {
+        const int64_t item = base + gi;
+        const bool valid = item < k.n_items;
+        int n0 = 0, nn = 0, q0 = 0, nq = 0;
+        if (valid) {
+            const Item x = k.items[item];
+            n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
+            for (int e = gl; e < nq; e += G) {
+                const int vs = k.out_vseg[q0 + e];
+                st.evs[e] = vs;
+                st.erel[e] = k.vseg_rel[vs];
+                const float2 p = reinterpret_cast<const float2 *>(k.ay)[k.out_pos[q0 + e]];
+                st.ea[e] = p.x;
+                st.ey[e] = p.y;
+            }
+            auto opos = [&](int jj) {
+                const int q = k.out_ptr[n0 + jj];
+                return (q < q0 ? q0 : (q > q0 + nq ? q0 + nq : q)) - q0;
+            };
+            for (int j = gl; j < nn; j += G) {
+                const int a = opos(j), b = opos(j + 1);
+                st.optr[j] = a;
+                for (int e = a; e < b; ++e) st.enode[e] = j;
+            }
+            if (gl == 0) st.optr[nn] = nq;
+        }
+        __syncthreads();
+        if (valid && nq > 0) {
+            int j = 0;
+            while (st.optr[j + 1] == st.optr[j]) ++j;   // first source with out-edges
+            float4 acc = zero4();
+            float ysrc = 0.f;
+            // ping-pong batches of (dS row, ws'_r row, source row) per out-edge
+            float4 Ad[kU], Aw[kU], Ah[kU], Bd[kU], Bw[kU], Bh[kU];
+            auto load = [&](float4 (&Xd)[kU], float4 (&Xw)[kU], float4 (&Xh)[kU], int b0) {
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const int e = b0 + u < nq ? b0 + u : nq - 1;
+                    Xd[u] = ld4(k.dS + (size_t)st.evs[e] * D + gl * 4);
+                    Xw[u] = ld4(k.wsp + (size_t)st.erel[e] * D + gl * 4);
+                    Xh[u] = ld4(k.h + (size_t)(n0 + st.enode[e]) * D + gl * 4);
+                }
+            };
+            auto consume = [&](const float4 (&Xd)[kU], const float4 (&Xw)[kU], const float4 (&Xh)[kU],
+                               int b0) {
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const int e = b0 + u;
+                    if (e < nq) {
+                        const float Y = st.ey[e];
+                        acc = lin4(acc, 1.f, Xd[u], st.ea[e]);
+                        acc = lin4(acc, 1.f, Xw[u], Y);
+                        ysrc += Y;
+                        const bool node_end = e + 1 == st.optr[j + 1];
+                        // the last out-edge of the item always ends its source
+                        if (node_end || st.erel[e + 1] != st.erel[e]) {
+                            float *p = acc_p + (size_t)st.erel[e] * D + gl * 4;
+                            atomicAdd(p + 0, ysrc * Xh[u].x);
+                            atomicAdd(p + 1, ysrc * Xh[u].y);
+                            atomicAdd(p + 2, ysrc * Xh[u].z);
+                            atomicAdd(p + 3, ysrc * Xh[u].w);
+                            ysrc = 0.f;
+                        }
+                        if (node_end) {
+                            atomic_add4(k.dh + (size_t)(n0 + j) * D + gl * 4, acc);
+                            acc = zero4();
+                            ++j;
+                            while (j < nn && st.optr[j + 1] == st.optr[j]) ++j;
+                        }
+                    }
+                }
+            };
+            load(Ad, Aw, Ah, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            for (int eb = 0; eb < nq; eb += 2 * kU) {
+                load(Bd, Bw, Bh, eb + kU);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(Ad, Aw, Ah, eb);
+                load(Ad, Aw, Ah, eb + 2 * kU);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(Bd, Bw, Bh, eb + kU);
+            }
+        }
+        __syncthreads();
+    }
+    if (LDSACC)
+        for (int i = threadIdx.x; i < k.R * D; i += 256) slot_acc[i] = lds_acc[i];
+}
+
+// ---------------------------------------------------------------- dW
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// partial[c] = sum over the chunk's segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out)
+// partial[c] = sum over the chunk's segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out);
+// yvec[c]   = sum over the chunk's segments of ysum[seg] * h[dst(seg)].
 __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vseg_byrel,
                                                          const int32_t *vseg_dst, const float *Sa,
-                                                         const float *Gm, float *partial)
+                                                         const float *Gm, const float *h,
+                                                         const float *ysum, float *partial,
+                                                         float *yvec)
 {
     constexpr int KB = 64, P = 68;
     __shared__ float As[KB * P];
     __shared__ float Bs[KB * P];
+    __shared__ float4 yred[256];
     const Tile t = chunks[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int li = lane & 15, q = lane >> 4;
     floatx4 acc[4];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float4 yacc = zero4();   // columns (tid & 15) * 4 .. + 3
     for (int k0 = 0; k0 < t.rows; k0 += KB) {
         __syncthreads();
         // 64 rows x 64 floats of each operand: 16 float4 per row, 1024 float4 per operand
         for (int idx = tid; idx < KB * 16; idx += 256) {
             const int rr = idx >> 4, c4 = (idx & 15) * 4;
-            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+            float4 a = zero4(), b = a;
             if (k0 + rr < t.rows) {
                 const int vs = vseg_byrel[t.row0 + k0 + rr];
+                const int v = vseg_dst[vs];
                 a = ld4(Sa + (size_t)vs * D + c4);
-                b = ld4(Gm + (size_t)vseg_dst[vs] * D + c4);
+                b = ld4(Gm + (size_t)v * D + c4);
+                yacc = lin4(yacc, 1.f, ld4(h + (size_t)v * D + c4), ysum[vs]);
             }
             *reinterpret_cast<float4 *>(&As[rr * P + c4]) = a;
             *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = b;
@@ -232,25 +487,48 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) out[(size_t)(w * 16 + q * 4 + v) * D + cb * 16 + li] = acc[cb][v];
+    yred[tid] = yacc;
+    __syncthreads();
+    if (tid < 16) {
+        float4 s = zero4();
+        for (int i = tid; i < 256; i += 16) s = add4(s, yred[i]);
+        st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
+    }
 }
 
-// Per relation r (one block): combine chunk partials in order, add the rank-1
-// attention terms, and finish dw_src, dw_dst.
+// Per relation r: pws = sum of the workgroup dws' slots, pwt = sum of the
+// relation's chunk ysum*h vectors, both in a fixed order.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float *accP, int nslots, int R,
+                                                         const float *yvec, const int32_t *rel_chunkptr,
+                                                         float *pws, float *pwt)
+{
+    __shared__ float red[2][4][D];
+    const int r = blockIdx.x, i = threadIdx.x % D, c = threadIdx.x / D;
+    float a = 0.f, b = 0.f;
+    for (int sl = c; sl < nslots; sl += 4) a += accP[((size_t)sl * R + r) * D + i];
+    for (int ch = rel_chunkptr[r] + c; ch < rel_chunkptr[r + 1]; ch += 4) b += yvec[(size_t)ch * D + i];
+    red[0][c][i] = a;
+    red[1][c][i] = b;
+    __syncthreads();
+    if (c == 0) {
+        pws[(size_t)r * D + i] = (red[0][0][i] + red[0][1][i]) + (red[0][2][i] + red[0][3][i]);
+        pwt[(size_t)r * D + i] = (red[1][0][i] + red[1][1][i]) + (red[1][2][i] + red[1][3][i]);
+    }
+}
+
+// Per relation r (blockIdx.x) and 256 entries of dW_r (blockIdx.y): combine
+// chunk partials in order, add the rank-1 attention terms; dw_src, dw_dst.
 __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial, const int32_t *rel_chunkptr,
-                                                           const float *acc_ws, const float *acc_wt,
-                                                           int copies, int R, const float *W,
-                                                           const float *w_src, const float *w_dst,
-                                                           float *dW, float *dws, float *dwt)
+                                                           const float *pws_all, const float *pwt_all,
+                                                           const float *W, const float *w_src,
+                                                           const float *w_dst, float *dW, float *dws,
+                                                           float *dwt)
 {
     __shared__ float pws[D], pwt[D];
-    const int r = blockIdx.x, tid = threadIdx.x;   // blockIdx.y: which 256 entries of dW_r
+    const int r = blockIdx.x, tid = threadIdx.x;
     if (tid < D) {
-        float a = 0.f, b = 0.f;
-        for (int c = 0; c < copies; ++c) {
-            a += acc_ws[((size_t)c * R + r) * D + tid];
-            b += acc_wt[((size_t)c * R + r) * D + tid];
-        }
-        pws[tid] = a; pwt[tid] = b;
+        pws[tid] = pws_all[(size_t)r * D + tid];
+        pwt[tid] = pwt_all[(size_t)r * D + tid];
     }
     __syncthreads();
     const int c0 = rel_chunkptr[r], c1 = rel_chunkptr[r + 1];
@@ -282,7 +560,9 @@ __global__ void zero_kernel(float *p, int64_t n)
 
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
-struct BwdWs { float *wsp, *wtp, *dS, *Sa, *ssum, *sv, *acc_ws, *acc_wt, *partial; };
+struct BwdWs {
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *ay, *ysum, *accP, *pws, *pwt, *partial, *yvec;
+};
 
 size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
 {
@@ -293,16 +573,22 @@ size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
         off += pad256(n * sizeof(float));
         return p;
     };
+    const size_t nchunks = (size_t)std::max<int64_t>(g->n_tiles_outer, 1);
     BwdWs x;
     x.wsp = take((size_t)g->R * D);
     x.wtp = take((size_t)g->R * D);
+    x.vatt = take((size_t)std::max<int64_t>(g->V, 1));
     x.dS = take((size_t)g->V * D);
     x.Sa = take((size_t)g->V * D);
     x.ssum = take((size_t)std::max<int64_t>(g->n_slots, 1));
     x.sv = take((size_t)std::max<int64_t>(g->N, 1));
-    x.acc_ws = take((size_t)kCopies * g->R * D);
-    x.acc_wt = take((size_t)kCopies * g->R * D);
-    x.partial = take((size_t)std::max<int64_t>(g->n_tiles_outer, 1) * D * D);
+    x.ay = take((size_t)g->E * 2);
+    x.ysum = take((size_t)std::max<int64_t>(g->V, 1));
+    x.accP = take((size_t)kAccBlocks * g->R * D);
+    x.pws = take((size_t)g->R * D);
+    x.pwt = take((size_t)g->R * D);
+    x.partial = take(nchunks * D * D);
+    x.yvec = take(nchunks * D);
     if (w) *w = x;
     return off;
 }
@@ -336,6 +622,11 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     hipError_t e;
     if ((st = launch_reorder_vec(W, w_src, g->R, D, D, 1, w.wsp, s)) != RGNN_OK) return st;
     if ((st = launch_reorder_vec(W, w_dst, g->R, D, D, 1, w.wtp, s)) != RGNN_OK) return st;
+    {   // h_v . wt'_r per segment
+        TravArgs ta;
+        ta.g = g; ta.h = h; ta.wtp = w.wtp; ta.heads = 1; ta.d = D; ta.vatt = w.vatt;
+        if ((st = launch_seg_attn(ta, s)) != RGNN_OK) return st;
+    }
     // dS_{v,r} = G_v W_r^T for every (dst, rel) segment
     GemmArgs ga;
     ga.X = Gm; ga.ldx = D; ga.gather = g->dev.vsegdst_byrel;
@@ -343,20 +634,18 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
     ga.Y = w.dS; ga.ldy = D; ga.scatter = g->dev.vseg_byrel;
     if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
-    if ((e = zero(dh, g->N * D, s)) != hipSuccess) return hip_fail(e, "zero launch");
-    if ((e = zero(w.acc_ws, (int64_t)kCopies * g->R * D, s)) != hipSuccess) return hip_fail(e, "zero launch");
-    if ((e = zero(w.acc_wt, (int64_t)kCopies * g->R * D, s)) != hipSuccess) return hip_fail(e, "zero launch");
+
     BK k{};
     k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr; k.vseg_rel = g->dev.vseg_rel;
-    k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.wtp = w.wtp; k.saved = saved;
-    k.dS = w.dS; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.dh = dh;
-    k.acc_ws = w.acc_ws; k.acc_wt = w.acc_wt; k.copies = kCopies; k.R = g->R;
+    k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
+    k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
+    k.ysum = w.ysum;
     if (g->n_items) {
         const dim3 grid((unsigned)((g->n_items + 15) / 16));
         {
             LaunchScope ls("rgat_bwd_traverse", s);
-            hipLaunchKernelGGL((rgat_bwd_kernel<0>), dim3(grid.x, 1), dim3(256), 0, s, k);
+            hipLaunchKernelGGL((bwd_traverse_kernel<0>), grid, dim3(256), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
@@ -373,23 +662,61 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
             {
-                LaunchScope ls("rgat_bwd_traverse", s);
-                hipLaunchKernelGGL((rgat_bwd_kernel<1>), dim3(grid.x, 1), dim3(256), 0, s, k);
+                LaunchScope ls("rgat_bwd_traverse_split", s);
+                hipLaunchKernelGGL((bwd_traverse_kernel<1>), grid, dim3(256), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         }
     }
+    if (g->N) {   // dh = destination terms (every row written)
+        DK dk{g->N, g->dev.dst_vsegptr, g->dev.vseg_rel, w.ysum, w.wtp, dh};
+        {
+            LaunchScope ls("rgat_bwd_dst_term", s);
+            hipLaunchKernelGGL(bwd_dst_term_kernel, dim3((unsigned)((g->N + 15) / 16)), dim3(256), 0, s, dk);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "dst_term launch");
+        if (g->n_big_vdst) {
+            LaunchScope ls("rgat_bwd_dst_term_big", s);
+            hipLaunchKernelGGL(bwd_dst_term_big_kernel, dim3((unsigned)g->n_big_vdst), dim3(1024), 0, s, dk,
+                               g->dev.big_vdst);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "dst_term_big launch");
+    }
+    // dh += source terms; dws' per workgroup slot
+    const int nslots = (int)std::min<int64_t>(kAccBlocks, std::max<int64_t>((g->n_oitems + 15) / 16, 1));
+    const bool lds_acc = g->R <= kLdsAccRels;
+    if (!lds_acc && (e = zero(w.accP, (int64_t)nslots * g->R * D, s)) != hipSuccess)
+        return hip_fail(e, "zero launch");
+    {
+        SK sk{};
+        sk.n_items = g->n_oitems; sk.items = g->dev.oitems; sk.out_ptr = g->dev.out_ptr;
+        sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.vseg_rel = g->dev.vseg_rel;
+        sk.h = h; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.accP = w.accP; sk.R = g->R;
+        LaunchScope ls("rgat_bwd_src", s);
+        if (lds_acc)
+            hipLaunchKernelGGL((bwd_src_kernel<true>), dim3((unsigned)nslots), dim3(256),
+                               (size_t)g->R * D * sizeof(float), s, sk);
+        else
+            hipLaunchKernelGGL((bwd_src_kernel<false>), dim3((unsigned)nslots), dim3(256), 0, s, sk);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_src launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
         hipLaunchKernelGGL(outer_gemm_kernel, dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
-                           g->dev.tiles_outer, g->dev.vseg_byrel, g->dev.vseg_dst, w.Sa, Gm, w.partial);
+                           g->dev.tiles_outer, g->dev.vseg_byrel, g->dev.vseg_dst, w.Sa, Gm, h, w.ysum,
+                           w.partial, w.yvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");
     {
+        LaunchScope ls("rgat_bwd_reduce", s);
+        hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g->R), dim3(256), 0, s, w.accP, nslots, g->R,
+                           w.yvec, g->dev.rel_chunkptr, w.pws, w.pwt);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_reduce launch");
+    {
         LaunchScope ls("rgat_bwd_finalize", s);
         hipLaunchKernelGGL(bwd_finalize_kernel, dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
-                           g->dev.rel_chunkptr, w.acc_ws, w.acc_wt, kCopies, g->R, W, w_src, w_dst,
-                           dW, dws, dwt);
+                           g->dev.rel_chunkptr, w.pws, w.pwt, W, w_src, w_dst, dW, dws, dwt);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "finalize launch");
     return RGNN_OK;

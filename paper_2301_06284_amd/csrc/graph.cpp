@@ -8,6 +8,7 @@
 //   compact map   unique (rel, src) pairs in ascending (rel, src) order
 //                 (Section "Compact Tensor Materialization": one row per pair)
 //   node types    node ids stable-sorted by type (segment MM over node types)
+//   out-edges     sorted in-edge positions ordered by (src, rel, position)
 // All sorts are stable LSD counting sorts, O(E + N + R) each.
 #include <algorithm>
 #include <cstring>
@@ -190,6 +191,44 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         g->n_big_split = (int64_t)x.big_split.size();
         g->n_big_vdst = (int64_t)x.big_vdst.size();
 
+        // ---- out-edges: in-edge positions by (src, rel, position) ----
+        {
+            std::vector<int32_t> pos((size_t)E);
+            for (int64_t i = 0; i < E; ++i) pos[i] = (int32_t)i;
+            counting_sort(pos, x.in_rel.data(), R, tmp, cnt);
+            counting_sort(pos, x.in_src.data(), N, tmp, cnt);
+            x.out_pos = pos;
+            x.out_ptr.assign((size_t)N + 1, 0);
+            for (int64_t i = 0; i < E; ++i) x.out_ptr[(size_t)x.in_src[i] + 1]++;
+            for (int64_t u = 0; u < N; ++u) x.out_ptr[u + 1] += x.out_ptr[u];
+            std::vector<int32_t> pos_vseg((size_t)E);
+            for (int64_t vs = 0; vs < g->V; ++vs)
+                for (int32_t i = x.vseg_ptr[vs]; i < x.vseg_ptr[vs + 1]; ++i) pos_vseg[i] = (int32_t)vs;
+            x.out_vseg.resize((size_t)E);
+            for (int64_t q = 0; q < E; ++q) x.out_vseg[q] = pos_vseg[x.out_pos[q]];
+            // work items over out-edges: bundles of small sources, pieces of large ones
+            x.oitems.clear();
+            auto odeg = [&](int64_t u) { return x.out_ptr[u + 1] - x.out_ptr[u]; };
+            int64_t u = 0;
+            while (u < N) {
+                if (odeg(u) > C) {
+                    for (int32_t q = x.out_ptr[u]; q < x.out_ptr[u + 1]; q += C)
+                        x.oitems.push_back(Item{(int32_t)u, (int32_t)u + 1, q,
+                                                std::min<int32_t>(q + C, x.out_ptr[u + 1])});
+                    ++u;
+                } else {
+                    const int64_t u0 = u;
+                    int64_t tot = 0;
+                    while (u < N && odeg(u) <= C && tot + odeg(u) <= C && u - u0 < kMaxDstPerItem) {
+                        tot += odeg(u);
+                        ++u;
+                    }
+                    x.oitems.push_back(Item{(int32_t)u0, (int32_t)u, x.out_ptr[u0], x.out_ptr[u]});
+                }
+            }
+            g->n_oitems = (int64_t)x.oitems.size();
+        }
+
         // ---- GEMM tile tables ----
         build_tiles(x.uniq_rel_ptr, kGemmTileRows, x.tiles_pairs);
         build_tiles(x.rel_vsegptr, kGemmTileRows, x.tiles_vsegs);
@@ -243,6 +282,8 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_nodes, x.tiles_nodes.data(), x.tiles_nodes.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
+    add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
+    parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
     total = std::max<size_t>(total, 256);
@@ -308,6 +349,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         HostIndex empty;
         g->host.in_src.swap(empty.in_src); g->host.in_rel.swap(empty.in_rel);
         g->host.in_eid.swap(empty.in_eid); g->host.e2u.swap(empty.e2u);
+        g->host.out_pos.swap(empty.out_pos); g->host.out_vseg.swap(empty.out_vseg);
     }
     *out = g;
     return RGNN_OK;
@@ -413,6 +455,8 @@ extern "C" rgnn_status rgnn_graph_export(const rgnn_graph_t *g, int32_t kind, vo
     case RGNN_IDX_EDGE2UNIQ: hv = &x.e2u; dp = d.e2u; n = (size_t)g->E; break;
     case RGNN_IDX_NTYPE_PERM: hv = &x.ntype_perm; dp = d.ntype_perm; n = (size_t)g->N; break;
     case RGNN_IDX_NTYPE_PTR: hv = &x.ntype_ptr; dp = d.ntype_ptr; n = (size_t)g->T + 1; break;
+    case RGNN_IDX_OUT_PTR: hv = &x.out_ptr; dp = d.out_ptr; n = (size_t)g->N + 1; break;
+    case RGNN_IDX_OUT_POS: hv = &x.out_pos; dp = d.out_pos; n = (size_t)g->E; break;
     default: return fail(RGNN_EINVAL, "unknown index kind " + std::to_string(kind));
     }
     if (bytes < n * sizeof(int32_t))

@@ -8,10 +8,16 @@
 //   sum_e alpha_e,i (V_s,i Wmsg[r,i])  =  (sum_e alpha_e,i V_s,i) Wmsg[r,i]
 // so Watt is applied once per (destination, relation) segment to the query,
 // and Wmsg once per segment to the attention-weighted value sum, instead of
-// once per edge.  The per-relation matrices are staged in LDS when they fit.
+// once per edge.  The per-relation matrices are staged in LDS, shared by a
+// 1024-thread workgroup, when they fit.
 //
-// Lane layout: a group of 16 lanes owns one work item; lane l holds features
-// 4l..4l+3, so head i is lanes [i*LH, (i+1)*LH) with LH = d_k / 4 lanes.
+// Work items are those of the RGAT traversal (at most kChunkEdges edges: a
+// bundle of small destinations or a piece of a large one), one per group of
+// 16 lanes; lane l holds features 4l..4l+3, so head i is lanes
+// [i*LH, (i+1)*LH) with LH = d_k / 4.  Each item first stages its edge
+// sources and segment / destination boundaries in LDS, then streams the
+// K|V rows of its edges, with their destinations' query rows, kU at a time
+// with the next kU in flight.
 #include "rgnn_internal.h"
 
 namespace rgnn {
@@ -27,6 +33,7 @@ __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
     return make_float4(a.x * s + b.x * t, a.y * s + b.y * t, a.z * s + b.z * t, a.w * s + b.w * t);
 }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 
 template <int W>
 __device__ __forceinline__ float gsum(float x)
@@ -37,7 +44,18 @@ __device__ __forceinline__ float gsum(float x)
 }
 
 constexpr int D = 64, G = 16;
-constexpr int kUnroll = 4;
+constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
+constexpr int kU = 2;                    // gathered K|V rows per batch
+constexpr int kBlock = 1024, GPB = kBlock / G;
+
+struct HStage {
+    int eidx[kE];          // source node of each edge
+    int edst[kE];          // destination node of each edge
+    int vptr[kE + 1];      // item-local edge offset of each virtual segment
+    int vrel[kE];
+    float vmu[kE];         // mu[rel] * att_scale of each virtual segment
+    int dptr[kDst + 1];    // item-local edge offset of each destination
+};
 
 struct HK {
     int64_t n_items;
@@ -49,26 +67,23 @@ struct HK {
     float *agg, *partial;
 };
 
-// y[4 values of this lane] = x_head (1 x dk) . Mat (dk x dk), Mat row-major in
-// memory `Mt` (LDS or global), where x_head is distributed over the head's LH
-// lanes (4 values each).  Column block of this lane: 4 * (gl % LH).
+// y[4 values of this lane] = x_head (1 x dk) . Mat (dk x dk), Mat row-major,
+// with x_head distributed over the head's LH lanes (4 values each).
 template <int LH>
 __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
 {
     constexpr int DK = LH * 4;
     const int base = (gl / LH) * LH;     // first lane of this head within the group
     const int c0 = 4 * (gl % LH);
-    float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 y = zero4();
 #pragma unroll
     for (int jj = 0; jj < LH; ++jj) {
         const float x0 = __shfl(x.x, base + jj, G), x1 = __shfl(x.y, base + jj, G);
         const float x2 = __shfl(x.z, base + jj, G), x3 = __shfl(x.w, base + jj, G);
-        const float4 r0 = ld4(Mt + (4 * jj + 0) * DK + c0);
-        const float4 r1 = ld4(Mt + (4 * jj + 1) * DK + c0);
-        const float4 r2 = ld4(Mt + (4 * jj + 2) * DK + c0);
-        const float4 r3 = ld4(Mt + (4 * jj + 3) * DK + c0);
-        y = lin4(y, 1.f, r0, x0); y = lin4(y, 1.f, r1, x1);
-        y = lin4(y, 1.f, r2, x2); y = lin4(y, 1.f, r3, x3);
+        y = lin4(y, 1.f, ld4(Mt + (4 * jj + 0) * DK + c0), x0);
+        y = lin4(y, 1.f, ld4(Mt + (4 * jj + 1) * DK + c0), x1);
+        y = lin4(y, 1.f, ld4(Mt + (4 * jj + 2) * DK + c0), x2);
+        y = lin4(y, 1.f, ld4(Mt + (4 * jj + 3) * DK + c0), x3);
     }
     return y;
 }
@@ -80,7 +95,7 @@ __device__ __forceinline__ float4 head_matvec_t(float4 x, const float *Mt, int g
     constexpr int DK = LH * 4;
     const int base = (gl / LH) * LH;
     const int c0 = 4 * (gl % LH);
-    float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 y = zero4();
 #pragma unroll
     for (int jj = 0; jj < LH; ++jj) {
         const float4 xj = make_float4(__shfl(x.x, base + jj, G), __shfl(x.y, base + jj, G),
@@ -93,87 +108,144 @@ __device__ __forceinline__ float4 head_matvec_t(float4 x, const float *Mt, int g
     return y;
 }
 
-template <int H, bool LDS>
-__global__ __launch_bounds__(512) void hgt_kernel(HK k)
+template <int H, bool LDSW>
+__global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
 {
-    constexpr int DK = D / H, LH = DK / 4, GPB = 512 / G;
+    constexpr int DK = D / H, LH = DK / 4;
     constexpr int MAT = H * DK * DK;            // floats per relation per matrix
-    extern __shared__ float smem[];
+    extern __shared__ float4 smem4[];
+    float *smem = reinterpret_cast<float *>(smem4);
+    const int nW = LDSW ? 2 * k.R * MAT : 0;
+    HStage *stages = reinterpret_cast<HStage *>(smem + nW);
     const float *Watt = k.Watt, *Wmsg = k.Wmsg;
-    if (LDS) {
-        const int n = k.R * MAT;
-        for (int i = threadIdx.x; i < n; i += 512) {
-            smem[i] = k.Watt[i];
-            smem[n + i] = k.Wmsg[i];
+    if (LDSW) {
+        const int n4 = k.R * MAT / 4;
+        for (int i = threadIdx.x; i < n4; i += kBlock) {
+            smem4[i] = reinterpret_cast<const float4 *>(k.Watt)[i];
+            smem4[n4 + i] = reinterpret_cast<const float4 *>(k.Wmsg)[i];
         }
-        __syncthreads();
         Watt = smem;
-        Wmsg = smem + n;
+        Wmsg = smem + k.R * MAT;
     }
-    const int gl = threadIdx.x % G;
-    const int64_t item = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
-    if (item >= k.n_items) return;
-    const Item it = k.items[item];
-    const int slot = k.item_slot[item];
-    const int head = gl / LH;
-    for (int v = it.dst0; v < it.dst1; ++v) {
-        const int sb = max(it.vs0, k.dst_vsegptr[v]);
-        const int se = min(it.vs1, k.dst_vsegptr[v + 1]);
-        float m = -INFINITY, s = 0.f;
-        float4 agg = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (sb < se) {
-            const float4 q = ld4(k.Q + (size_t)v * D + gl * 4);
-            for (int vs = sb; vs < se; ++vs) {
-                const int r = k.vseg_rel[vs];
-                const float *Wa = Watt + (size_t)r * MAT + (size_t)head * DK * DK;
-                const float *Wm = Wmsg + (size_t)r * MAT + (size_t)head * DK * DK;
-                // query moved through W_att (reordering), with prior and scale folded in
-                const float4 qp = scale4(head_matvec_t<LH>(q, Wa, gl), k.mu[r] * k.scale);
-                float4 vacc = make_float4(0.f, 0.f, 0.f, 0.f);
-                const int e0 = k.vseg_ptr[vs], e1 = k.vseg_ptr[vs + 1];
-                for (int e = e0; e < e1; e += kUnroll) {
-                    int src[kUnroll];
-                    float4 kr[kUnroll], vr[kUnroll];
-#pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) src[u] = k.in_src[min(e + u, e1 - 1)];
-#pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) {
-                        kr[u] = ld4(k.KV + (size_t)src[u] * (2 * D) + gl * 4);
-                        vr[u] = ld4(k.KV + (size_t)src[u] * (2 * D) + D + gl * 4);
-                    }
-#pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) {
-                        const float a = gsum<LH>(dot4(kr[u], qp));
-                        if (e + u < e1) {
-                            const float mn = fmaxf(m, a);
-                            const float c1 = __expf(m - mn), c2 = __expf(a - mn);
-                            s = s * c1 + c2;
-                            vacc = lin4(vacc, c1, vr[u], c2);
-                            agg = scale4(agg, c1);
-                            m = mn;
-                        }
-                    }
-                }
-                agg = add4(agg, head_vecmat<LH>(vacc, Wm, gl));
-            }
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    HStage &st = stages[gi];
+    const int64_t item = (int64_t)blockIdx.x * GPB + gi;
+    const bool valid = item < k.n_items;
+    int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
+    if (valid) {
+        const Item x = k.items[item];
+        dst0 = x.dst0; nd = x.dst1 - x.dst0; vs0 = x.vs0; nv = x.vs1 - x.vs0;
+        e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
+        slot = k.item_slot[item];
+        for (int j = gl; j < nv; j += G) {
+            st.vptr[j] = k.vseg_ptr[vs0 + j] - e0;
+            const int r = k.vseg_rel[vs0 + j];
+            st.vrel[j] = r;
+            st.vmu[j] = k.mu[r] * k.scale;
         }
+        if (gl == 0) st.vptr[nv] = ne;
+        auto dst_edge = [&](int jj) {
+            int vs = k.dst_vsegptr[dst0 + jj];
+            vs = vs < vs0 ? vs0 : (vs > vs0 + nv ? vs0 + nv : vs);
+            return k.vseg_ptr[vs] - e0;
+        };
+        for (int j = gl; j < nd; j += G) {
+            const int ea = dst_edge(j), eb = dst_edge(j + 1);
+            st.dptr[j] = ea;
+            for (int e = ea; e < eb; ++e) st.edst[e] = dst0 + j;
+        }
+        if (gl == 0) st.dptr[nd] = ne;
+        for (int e = gl; e < ne; e += G) st.eidx[e] = k.in_src[e0 + e];
+    }
+    __syncthreads();
+    if (!valid) return;
+
+    const int head = gl / LH;
+    float m = -INFINITY, s = 0.f;
+    float4 agg = zero4(), vacc = zero4(), qp = zero4();
+    auto flush = [&](int jj) {
         if (slot < 0) {
-            st4(k.agg + (size_t)v * D + gl * 4, scale4(agg, s > 0.f ? 1.f / s : 0.f));
+            st4(k.agg + (size_t)(dst0 + jj) * D + gl * 4, scale4(agg, s > 0.f ? 1.f / s : 0.f));
         } else {
             float *pr = k.partial + (size_t)slot * (2 * H + D);
             if (gl % LH == 0) { pr[head * 2] = m; pr[head * 2 + 1] = s; }
             st4(pr + 2 * H + gl * 4, agg);
         }
+        m = -INFINITY; s = 0.f; agg = zero4();
+    };
+    auto start_vseg = [&](int jv, float4 q) {
+        const size_t off = (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK;
+        qp = scale4(head_matvec_t<LH>(q, Watt + off, gl), st.vmu[jv]);
+        vacc = zero4();
+    };
+    int j = 0, jv = 0;
+    while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush(j); ++j; }
+    if (ne > 0) {
+        // Ping-pong batches: batch A is consumed while batch B is in flight.
+        // Each edge brings its K|V row and its destination's query row (the
+        // latter a cache hit after the destination's first edge); a segment is
+        // started from the query row of its first edge.
+        float4 Ak[kU], Av[kU], Aq[kU], Bk[kU], Bv[kU], Bq[kU];
+        auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], float4 (&Xq)[kU], int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u < ne ? base + u : ne - 1;
+                const size_t row = (size_t)st.eidx[e] * (2 * D);
+                Xk[u] = ld4(k.KV + row + gl * 4);
+                Xv[u] = ld4(k.KV + row + D + gl * 4);
+                Xq[u] = ld4(k.Q + (size_t)st.edst[e] * D + gl * 4);
+            }
+        };
+        auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
+                           int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u;
+                if (e < ne) {
+                    if (e == st.vptr[jv]) start_vseg(jv, Xq[u]);
+                    const float a = gsum<LH>(dot4(Xk[u], qp));
+                    const float mn = fmaxf(m, a);
+                    const float c1 = __expf(m - mn), c2 = __expf(a - mn);
+                    s = s * c1 + c2;
+                    vacc = lin4(vacc, c1, Xv[u], c2);
+                    agg = scale4(agg, c1);
+                    m = mn;
+                    if (e + 1 == st.vptr[jv + 1]) {
+                        const size_t off = (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK;
+                        agg = add4(agg, head_vecmat<LH>(vacc, Wmsg + off, gl));
+                        ++jv;
+                        if (e + 1 == st.dptr[j + 1]) {
+                            flush(j);
+                            ++j;
+                            while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush(j); ++j; }
+                        }
+                    }
+                }
+            }
+        };
+        load(Ak, Av, Aq, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int eb = 0; eb < ne; eb += 2 * kU) {
+            load(Bk, Bv, Bq, eb + kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(Ak, Av, Aq, eb);
+            load(Ak, Av, Aq, eb + 2 * kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(Bk, Bv, Bq, eb + kU);
+        }
     }
+    while (j < nd) { flush(j); ++j; }
 }
 
-}  // namespace
+size_t stage_bytes() { return (size_t)GPB * sizeof(HStage); }
 
-size_t hgt_lds_bytes(int R, int heads)
+size_t weight_bytes(int R, int heads)
 {
     const int dk = D / heads;
     return (size_t)2 * R * heads * dk * dk * sizeof(float);
 }
+
+}  // namespace
 
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
 {
@@ -186,18 +258,33 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     k.vseg_rel = g->dev.vseg_rel; k.in_src = g->dev.in_src;
     k.KV = a.KV; k.Q = a.Q; k.Watt = a.Watt; k.Wmsg = a.Wmsg; k.mu = a.mu;
     k.scale = a.scale; k.R = g->R; k.agg = a.agg; k.partial = a.partial;
-    const size_t lds = hgt_lds_bytes(g->R, a.heads);
-    const bool use_lds = lds <= 64 * 1024;
-    const unsigned nb = (unsigned)((g->n_items + 31) / 32);
+    const size_t wb = weight_bytes(g->R, a.heads);
+    const bool use_lds = wb + stage_bytes() <= 160 * 1024;
+    const size_t lds = stage_bytes() + (use_lds ? wb : 0);
+    const unsigned nb = (unsigned)((g->n_items + GPB - 1) / GPB);
     LaunchScope ls("hgt_traverse", s);
-#define HGT(H) do { if (use_lds) hipLaunchKernelGGL((hgt_kernel<H, true>), dim3(nb), dim3(512), lds, s, k); \
-                    else hipLaunchKernelGGL((hgt_kernel<H, false>), dim3(nb), dim3(512), 0, s, k); } while (0)
+    hipError_t e = hipSuccess;
+#define HGT(H)                                                                                  \
+    do {                                                                                        \
+        if (use_lds) {                                                                          \
+            e = hipFuncSetAttribute((const void *)hgt_kernel<H, true>,                          \
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
+            if (e == hipSuccess)                                                                \
+                hipLaunchKernelGGL((hgt_kernel<H, true>), dim3(nb), dim3(kBlock), lds, s, k);   \
+        } else {                                                                                \
+            e = hipFuncSetAttribute((const void *)hgt_kernel<H, false>,                         \
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
+            if (e == hipSuccess)                                                                \
+                hipLaunchKernelGGL((hgt_kernel<H, false>), dim3(nb), dim3(kBlock), lds, s, k);  \
+        }                                                                                       \
+    } while (0)
     if (a.heads == 1) HGT(1);
     else if (a.heads == 2) HGT(2);
     else if (a.heads == 4) HGT(4);
     else return fail(RGNN_EUNSUPPORTED, "HGT traversal supports heads in {1, 2, 4}");
 #undef HGT
-    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute (HGT LDS)");
+    e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt traversal launch");
 }
 

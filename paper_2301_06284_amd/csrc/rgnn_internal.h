@@ -46,6 +46,9 @@ struct HostIndex {
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
+    // out-edges (source-major view of the sorted in-edges), for the backward pass
+    std::vector<int32_t> out_ptr, out_pos, out_vseg;
+    std::vector<Item> oitems;            // {node0, node1, q0, q1} over out-edge offsets
 };
 
 // Device copies (one allocation, carved).
@@ -64,6 +67,8 @@ struct DeviceIndex {
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
+    int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr;
+    Item *oitems = nullptr;
 };
 
 }  // namespace rgnn
@@ -79,6 +84,7 @@ struct rgnn_graph {
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0;
+    int64_t n_oitems = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
@@ -194,43 +200,12 @@ struct HgtArgs {
 };
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
 
-struct BwdArgs {
-    const rgnn_graph *g = nullptr;
-    const float *h = nullptr, *W = nullptr, *w_src = nullptr, *w_dst = nullptr;
-    const float *wsp = nullptr, *wtp = nullptr;   // reordered [R, d_in]
-    const float *saved = nullptr;                 // [N, 2]
-    const float *G = nullptr;                     // grad_out [N, d_out]
-    const float *dS = nullptr;                    // [V, d_in]  G_v W_r^T per vseg
-    float slope = 0.2f;
-    int d = 64;
-    float *Sa = nullptr;          // [V, d_in]  sum alpha h_u per vseg
-    float *ssum = nullptr;        // [slots] partial s_v for split destinations
-    float *sv = nullptr;          // [N] s_v
-    float *dh = nullptr;          // [N, d_in] (atomics; zeroed before)
-    float *acc_ws = nullptr;      // [copies, R, d_in] privatized dws' accumulators
-    float *acc_wt = nullptr;      // [copies, R, d_in] privatized dwt' accumulators
-    int copies = 1;
-    int phase = 0;
-};
-rgnn_status launch_rgat_bwd_traverse(const BwdArgs &a, hipStream_t s);
-rgnn_status launch_rgat_bwd_merge_s(const BwdArgs &a, hipStream_t s);
-
-struct OuterArgs {
-    const rgnn_graph *g = nullptr;
-    const float *A = nullptr;      // [V, d_in]   rows by vseg id
-    const float *B = nullptr;      // [N, d_out]  rows by destination of the vseg
-    int d_in = 64, d_out = 64;
-    float *partial = nullptr;      // [nchunks, d_in, d_out]
-    const int32_t *chunk_rel = nullptr;   // (device) relation of each K-chunk
-    const int32_t *chunk_row0 = nullptr;  // (device) first vseg-by-rel row of each chunk
-    const int32_t *chunk_rows = nullptr;
-    int64_t nchunks = 0;
-};
-rgnn_status launch_outer_gemm(const OuterArgs &a, hipStream_t s);
-rgnn_status launch_bwd_finalize(const rgnn_graph *g, const float *partial, const int32_t *rel_chunkptr,
-                                const float *acc_ws, const float *acc_wt, int copies,
-                                const float *W, const float *w_src, const float *w_dst,
-                                int d_in, int d_out, float *dW, float *dws, float *dwt,
-                                hipStream_t s);
+// RGAT backward (backward.hip).  With need != NULL only stores the workspace
+// bytes the call needs.
+rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
+                               const float *w_src, const float *w_dst, int d_in, int d_out,
+                               float slope, const float *saved, const float *Gm, float *dh,
+                               float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
+                               hipStream_t s, size_t *need);
 
 }  // namespace rgnn

@@ -214,30 +214,37 @@ __device__ __forceinline__ void aggregate_item(const TK &k, const ItemHdr &it, c
         acc = zero4();
     };
     if (it.ne > 0) {
-        float4 cur[kU], nxt[kU];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int e = u < it.ne ? u : it.ne - 1;
-            cur[u] = ld4(rows + (size_t)st.eidx[e] * D + gl * 4);
-        }
-        for (int e0 = 0; e0 < it.ne; e0 += kU) {
-            // unconditional prefetch (clamped to the last edge): with a
-            // conditional one the compiler drains every load before the FMAs
+        // Two row buffers in ping-pong: while one batch is consumed the other
+        // is in flight.  Loads are unconditional (clamped to the last edge)
+        // and no register copies rotate the buffers, so the compiler's waits
+        // never drain the batch still in flight.
+        float4 A[kU], B[kU];
+        auto load = [&](float4 (&X)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
-                const int e = e0 + kU + u < it.ne ? e0 + kU + u : it.ne - 1;
-                nxt[u] = ld4(rows + (size_t)st.eidx[e] * D + gl * 4);
+                const int e = base + u < it.ne ? base + u : it.ne - 1;
+                X[u] = ld4(rows + (size_t)st.eidx[e] * D + gl * 4);
             }
+        };
+        auto consume = [&](const float4 (&X)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
-                const int e = e0 + u;
+                const int e = base + u;
                 if (e < it.ne) {
                     while (e >= st.dptr[j + 1]) { flush(j); ++j; }
-                    acc = lin4(acc, 1.f, cur[u], st.ew[e * H + head]);
+                    acc = lin4(acc, 1.f, X[u], st.ew[e * H + head]);
                 }
             }
-#pragma unroll
-            for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
+        };
+        load(A, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
+            load(B, e0 + kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(A, e0);
+            load(A, e0 + 2 * kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(B, e0 + kU);
         }
     }
     for (; j < it.nd; ++j) flush(j);
@@ -339,21 +346,20 @@ __global__ __launch_bounds__(256) void rgcn_af_kernel(TK k)
     if (!it.valid || it.ne == 0) return;
     int j = 0;
     float4 acc = zero4();
-    float4 cur[kU], nxt[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-        cur[u] = ld4(k.h + (size_t)st.eidx[u < it.ne ? u : it.ne - 1] * D + gl * 4);
-    for (int e0 = 0; e0 < it.ne; e0 += kU) {
+    float4 A[kU], B[kU];   // ping-pong row buffers, as in aggregate_item
+    auto load = [&](float4 (&X)[kU], int base) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const int e = e0 + kU + u < it.ne ? e0 + kU + u : it.ne - 1;
-            nxt[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
+            const int e = base + u < it.ne ? base + u : it.ne - 1;
+            X[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
         }
+    };
+    auto consume = [&](const float4 (&X)[kU], int base) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const int e = e0 + u;
+            const int e = base + u;
             if (e < it.ne) {
-                acc = lin4(acc, 1.f, cur[u], 1.f);
+                acc = lin4(acc, 1.f, X[u], 1.f);
                 if (e + 1 == st.vptr[j + 1]) {
                     st4(k.S + (size_t)(it.vs0 + j) * D + gl * 4, scale4(acc, st.vw[j]));
                     acc = zero4();
@@ -361,8 +367,16 @@ __global__ __launch_bounds__(256) void rgcn_af_kernel(TK k)
                 }
             }
         }
-#pragma unroll
-        for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
+    };
+    load(A, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
+        load(B, e0 + kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(A, e0);
+        load(A, e0 + 2 * kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(B, e0 + kU);
     }
 }
 
@@ -386,30 +400,27 @@ __global__ __launch_bounds__(256) void rgat_af_kernel(TK k)
     int j = 0;
     float m = -INFINITY, s = 0.f;
     float4 acc = zero4();
-    float4 cur[kU], curw[kU], nxt[kU], nxtw[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-        const int e = u < it.ne ? u : it.ne - 1;
-        cur[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
-        curw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
-    }
-    for (int e0 = 0; e0 < it.ne; e0 += kU) {
+    // ping-pong buffers of gathered rows and their relations' w_src vectors
+    float4 A[kU], Aw[kU], B[kU], Bw[kU];
+    auto load = [&](float4 (&X)[kU], float4 (&Xw)[kU], int base) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const int e = e0 + kU + u < it.ne ? e0 + kU + u : it.ne - 1;
-            nxt[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
-            nxtw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
+            const int e = base + u < it.ne ? base + u : it.ne - 1;
+            X[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
+            Xw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
         }
+    };
+    auto consume = [&](const float4 (&X)[kU], const float4 (&Xw)[kU], int base) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const int e = e0 + u;
-            const float atts = gsum<G>(dot4(cur[u], curw[u]));
+            const int e = base + u;
+            const float atts = gsum<G>(dot4(X[u], Xw[u]));
             if (e < it.ne) {
                 const float z = leaky(atts + st.vw[j], k.slope);
                 const float mn = fmaxf(m, z);
                 const float c1 = __expf(m - mn), c2 = __expf(z - mn);
                 s = s * c1 + c2;
-                acc = lin4(acc, c1, cur[u], c2);
+                acc = lin4(acc, c1, X[u], c2);
                 m = mn;
                 if (e + 1 == st.vptr[j + 1]) {
                     const size_t vs = (size_t)it.vs0 + j;
@@ -420,8 +431,16 @@ __global__ __launch_bounds__(256) void rgat_af_kernel(TK k)
                 }
             }
         }
-#pragma unroll
-        for (int u = 0; u < kU; ++u) { cur[u] = nxt[u]; curw[u] = nxtw[u]; }
+    };
+    load(A, Aw, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
+        load(B, Bw, e0 + kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(A, Aw, e0);
+        load(A, Aw, e0 + 2 * kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(B, Bw, e0 + kU);
     }
 }
 

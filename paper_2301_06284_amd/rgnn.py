@@ -25,7 +25,7 @@ GRAPH_HOST_ONLY = 1
 INDEX_KINDS = {
     "dst_rowptr": 0, "in_src": 1, "in_rel": 2, "in_eid": 3, "seg_ptr": 4, "seg_rel": 5,
     "dst_segptr": 6, "uniq_src": 7, "uniq_rel_ptr": 8, "edge2uniq": 9, "ntype_perm": 10,
-    "ntype_ptr": 11,
+    "ntype_ptr": 11, "out_ptr": 12, "out_pos": 13,
 }
 
 EXPORTED = [
@@ -181,7 +181,8 @@ class Graph:
              "edge2uniq": inf["num_edges"], "seg_ptr": inf["num_dst_segments"] + 1,
              "seg_rel": inf["num_dst_segments"], "uniq_src": inf["num_src_pairs"],
              "uniq_rel_ptr": inf["num_rels"] + 1, "ntype_perm": inf["num_nodes"],
-             "ntype_ptr": inf["num_ntypes"] + 1}[kind]
+             "ntype_ptr": inf["num_ntypes"] + 1, "out_ptr": inf["num_nodes"] + 1,
+             "out_pos": inf["num_edges"]}[kind]
         out = np.empty(max(n, 1), np.int32)
         _check(_lib.rgnn_graph_export(self.handle, INDEX_KINDS[kind], _np_ptr(out), out.nbytes))
         return out[:n]

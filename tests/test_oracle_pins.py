@@ -457,6 +457,10 @@ def test_graph_index_against_python_sets(kind):
     assert list(ix["edge2uniq"]) == [pos[(rel[e], src[e])] for e in order]
     assert list(ix["ntype_perm"]) == sorted(range(N), key=lambda n: (nt[n], n))
     assert list(ix["ntype_ptr"]) == [sum(1 for n in range(N) if nt[n] < t) for t in range(T + 1)]
+    # out-edges: every sorted in-edge position listed under its source, by (rel, position)
+    out = sorted(range(E), key=lambda p: (src[order[p]], rel[order[p]], p))
+    assert list(ix["out_pos"]) == out
+    assert list(ix["out_ptr"]) == [sum(1 for e in range(E) if src[e] < u) for u in range(N + 1)]
 
 
 def test_compaction_counts_seven_to_five():
