@@ -23,15 +23,20 @@
 //      Sa = sum alpha h_u per segment; pass 2 forms Y per edge and its sum per
 //      segment.  Pieces of split destinations finish pass 2 in a second launch
 //      once their s_v partials are merged.
-//   3. dh_v's destination term, sum over v's segments of ysum * wt'_r.
-//   4. A source-major traversal over the out-edges (sorted by source, then
-//      relation) that gathers dS rows and adds alpha dS + Y ws'_r into dh_u:
-//      the scatter of the paper's backward becomes a gather, so there are no
-//      per-edge atomics, only one add per source row.  dws' is accumulated per
-//      (source, relation) run in LDS and written once per workgroup.
-//   5. An outer-product MFMA GEMM for dW over K-chunks of segments of one
-//      relation (also summing ysum * h_v per chunk for dwt'), then a
-//      deterministic combine and a per-relation finalize.
+//      A third pass writes dh_v's destination term, the sum over v's
+//      segments of ysum * wt'_r.  dS, Sa and ysum rows are kept in the
+//      by-relation segment order, so the GEMMs over them read and write
+//      contiguous rows.
+//   3. A source-major traversal over the out-edges (sorted by source, then
+//      relation) that gathers dS rows and forms dh_u = (destination term) +
+//      sum alpha dS + Y ws'_r with one store per source row: the scatter of
+//      the paper's backward becomes a gather, with no per-edge atomics.  It
+//      also sums Y per (source, relation) pair, the compact rows of the
+//      forward.
+//   4. dws'_r = sum over r's compact pairs of ysum_pair * h_src, by chunks of
+//      pairs; an outer-product MFMA GEMM for dW over K-chunks of segments of
+//      one relation (also summing ysum * h_v per chunk for dwt'); then a
+//      deterministic combine of the chunks and a per-relation finalize.
 #include "rgnn_internal.h"
 
 namespace rgnn {
@@ -41,8 +46,6 @@ namespace {
 constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 constexpr int kU = 4;              // rows per prefetch batch in the traversals
-constexpr int kAccBlocks = 768;    // workgroups of the source-major traversal (one dws' slot each)
-constexpr int kLdsAccRels = 128;   // relations whose dws' accumulators fit in LDS
 constexpr int kOuterRows = 2048;   // segments per outer-product K-chunk
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
@@ -71,13 +74,14 @@ __device__ __forceinline__ float gsum(float x)
 struct BK {
     int64_t n_items;
     const Item *items;
-    const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *in_src;
-    const float *h, *wsp, *saved, *dS, *vatt, *sv_in;
+    const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_pos, *in_src;
+    const float *h, *wsp, *wtp, *saved, *dS, *vatt, *sv_in;
     float slope;
-    float *Sa;       // [V, D]  sum alpha h_u per segment
+    float *Sa;       // [V, D]  sum alpha h_u per segment (by-relation order)
     float *ssum;     // [slots] s_v partial of each piece of a split destination
     float *ay;       // [E, 2]  per sorted in-edge: (alpha, Y); pieces hold (signed alpha, dalpha) in between
-    float *ysum;     // [V]     sum of Y per segment
+    float *ysum;     // [V]     sum of Y per segment (by-relation order)
+    float *dh;       // [N, D]  destination terms written here
 };
 
 struct BStage {
@@ -85,18 +89,20 @@ struct BStage {
     int evs[kE];         // item-local segment of each edge
     int vptr[kE + 1];    // item-local first edge of each segment
     int vrel[kE];
+    int vpos[kE];        // by-relation position of each segment (row of dS, Sa, ysum)
     int vdj[kE];         // item-local destination of each segment
-    float vatt[kE];      // h_v . wt'_r of each segment
+    float vatt[kE];      // h_v . wt'_r of each segment, then its sum of Y
     float ea[kE];        // alpha of each edge, sign bit set where the logit is <= 0
     float eda[kE];       // dalpha of each edge
     int dptr[kDst + 1];  // item-local first edge of each destination
     float dM[kDst], dZi[kDst], dsv[kDst];   // per destination: M_v, 1/Z_v, s_v
 };
 
-// PHASE 0: every item.  Whole destinations run both passes; pieces of split
+// PHASE 0: every item.  Whole destinations run all passes; pieces of split
 //          destinations run pass 1, leave their part of s_v in ssum and park
 //          (signed alpha, dalpha) in ay.
-// PHASE 1: pieces of split destinations only: pass 2 with the merged s_v.
+// PHASE 1: pieces of split destinations only: pass 2 with the merged s_v (their
+//          destination term is summed by split_dst_term_kernel).
 template <int PHASE>
 __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
 {
@@ -119,6 +125,7 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
             const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
             st.vptr[j] = a;
             st.vrel[j] = k.vseg_rel[vs0 + j];
+            st.vpos[j] = k.vseg_pos[vs0 + j];
             st.vatt[j] = k.vatt[vs0 + j];
             for (int e = a; e < b; ++e) st.evs[e] = j;
         }
@@ -165,7 +172,7 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
                 const int jj = st.evs[e];
                 Xh[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
                 Xw[u] = ld4(k.wsp + (size_t)st.vrel[jj] * D + gl * 4);
-                Xd[u] = ld4(k.dS + (size_t)(vs0 + jj) * D + gl * 4);
+                Xd[u] = ld4(k.dS + (size_t)st.vpos[jj] * D + gl * 4);
             }
         };
         auto consume = [&](const float4 (&Xh)[kU], const float4 (&Xw)[kU], const float4 (&Xd)[kU],
@@ -186,7 +193,7 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
                         st.eda[e] = da;
                     }
                     if (e + 1 == st.vptr[jv + 1]) {
-                        st4(k.Sa + (size_t)(vs0 + jv) * D + gl * 4, sa);
+                        st4(k.Sa + (size_t)st.vpos[jv] * D + gl * 4, sa);
                         sa = zero4();
                         ++jv;
                         if (e + 1 == st.dptr[j + 1]) {
@@ -215,13 +222,13 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
     }
     __syncthreads();
 
+    const bool fin = valid && (PHASE == 1 || slot < 0);   // this launch finishes the item
     if (PHASE == 0 && valid && slot >= 0) {
         for (int e = gl; e < ne; e += G)
             reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(st.ea[e], st.eda[e]);
-        return;
     }
     // pass 2: Y per edge and its sum per segment (segment-parallel over lanes)
-    if (valid) {
+    if (fin) {
         for (int jv = gl; jv < nv; jv += G) {
             const float sv = st.dsv[st.vdj[jv]];
             float ys = 0.f;
@@ -232,8 +239,54 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
                 ys += Y;
                 reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
             }
-            k.ysum[vs0 + jv] = ys;
+            k.ysum[st.vpos[jv]] = ys;
+            st.vatt[jv] = ys;
         }
+    }
+    __syncthreads();
+    // pass 3: destination term dh_v = sum over v's segments of ysum * wt'_r,
+    // streaming the wt' rows of the item's segments in ping-pong batches
+    if (PHASE == 0 && fin) {
+        float4 acc = zero4();
+        int j = 0;
+        auto flush_to = [&](int jn) {   // finish destinations [j, jn)
+            while (j < jn) {
+                st4(k.dh + (size_t)(dst0 + j) * D + gl * 4, acc);
+                acc = zero4();
+                ++j;
+            }
+        };
+        float4 Aw[kU], Bw[kU];
+        auto load = [&](float4 (&Xw)[kU], int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int jv = base + u < nv ? base + u : (nv > 0 ? nv - 1 : 0);
+                Xw[u] = ld4(k.wtp + (size_t)st.vrel[jv] * D + gl * 4);
+            }
+        };
+        auto consume = [&](const float4 (&Xw)[kU], int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int jv = base + u;
+                if (jv < nv) {
+                    flush_to(st.vdj[jv]);
+                    acc = lin4(acc, 1.f, Xw[u], st.vatt[jv]);
+                }
+            }
+        };
+        if (nv > 0) {
+            load(Aw, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            for (int b = 0; b < nv; b += 2 * kU) {
+                load(Bw, b + kU);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(Aw, b);
+                load(Aw, b + 2 * kU);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(Bw, b + kU);
+            }
+        }
+        flush_to(nd);
     }
 }
 
@@ -269,46 +322,26 @@ __global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_spl
     }
 }
 
-// ---------------------------------------------------------------- dh_v destination term
-struct DK {
-    int64_t N;
-    const int32_t *dst_vsegptr, *vseg_rel;
-    const float *ysum, *wtp;
-    float *dh;
-};
-
-// dh_v = sum over v's segments of ysum * wt'_r; one 16-lane group per node
-// (every node, so this also initialises dh).  Nodes with more than kBigRange
-// segments are left to the workgroup kernel below.
-__global__ __launch_bounds__(256) void bwd_dst_term_kernel(DK k)
+// Destination term of a split destination (its segments span several work
+// items): one workgroup per destination, segments strided over 16-lane groups
+// and combined in group order.
+__global__ __launch_bounds__(256) void split_dst_term_kernel(const int32_t *split_dst, const int32_t *dst_vsegptr,
+                                                             const int32_t *vseg_rel, const int32_t *vseg_pos,
+                                                             const float *ysum, const float *wtp, float *dh)
 {
-    const int gl = threadIdx.x % G;
-    const int64_t v = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;
-    if (v >= k.N) return;
-    const int a = k.dst_vsegptr[v], b = k.dst_vsegptr[v + 1];
-    if (b - a > kBigRange) return;
-    float4 acc = zero4();
-    for (int vs = a; vs < b; ++vs)
-        acc = lin4(acc, 1.f, ld4(k.wtp + (size_t)k.vseg_rel[vs] * D + gl * 4), k.ysum[vs]);
-    st4(k.dh + (size_t)v * D + gl * 4, acc);
-}
-
-__global__ __launch_bounds__(1024) void bwd_dst_term_big_kernel(DK k, const int32_t *big_vdst)
-{
-    constexpr int NG = 1024 / G;
+    constexpr int NG = 256 / G;
     __shared__ float4 part[NG][G];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int v = big_vdst[blockIdx.x];
-    const int a = k.dst_vsegptr[v], b = k.dst_vsegptr[v + 1];
+    const int v = split_dst[blockIdx.x];
     float4 acc = zero4();
-    for (int vs = a + gi; vs < b; vs += NG)
-        acc = lin4(acc, 1.f, ld4(k.wtp + (size_t)k.vseg_rel[vs] * D + gl * 4), k.ysum[vs]);
+    for (int vs = dst_vsegptr[v] + gi; vs < dst_vsegptr[v + 1]; vs += NG)
+        acc = lin4(acc, 1.f, ld4(wtp + (size_t)vseg_rel[vs] * D + gl * 4), ysum[vseg_pos[vs]]);
     part[gi][gl] = acc;
     __syncthreads();
     if (gi == 0) {
         float4 t = zero4();
         for (int i = 0; i < NG; ++i) t = add4(t, part[i][gl]);
-        st4(k.dh + (size_t)v * D + gl * 4, t);
+        st4(dh + (size_t)v * D + gl * 4, t);
     }
 }
 
@@ -316,132 +349,151 @@ __global__ __launch_bounds__(1024) void bwd_dst_term_big_kernel(DK k, const int3
 struct SK {
     int64_t n_items;
     const Item *items;           // {node0, node1, q0, q1}: nodes and their out-edge range
-    const int32_t *out_ptr, *out_pos, *out_vseg, *vseg_rel;
-    const float *h, *wsp, *dS, *ay;
-    float *dh;
-    float *accP;                 // [gridDim.x, R, D] dws' partial of each workgroup
-    int R;
+    const int32_t *out_ptr, *out_pos, *out_vseg, *out_rel, *e2u;
+    const float *wsp, *dS, *ay;
+    float *dh;                   // holds the destination terms on entry
+    float *ypair;                // [U_src] sum of Y per compact (src, rel) pair, zeroed before
 };
 
 struct SStage {
-    int evs[kE];         // segment (dS row) of each out-edge
+    int evs[kE];         // dS row (by-relation segment position) of each out-edge
     int erel[kE];
+    int epair[kE];       // compact (src, rel) pair of each out-edge
     int enode[kE];       // item-local source of each out-edge
     float ea[kE], ey[kE];
     int optr[kDst + 1];  // item-local first out-edge of each source
 };
 
-// Grid-stride over the out-edge work items; the dws' accumulators of a
-// workgroup live in LDS (LDSACC) or in its own global slot.
-template <bool LDSACC>
 __global__ __launch_bounds__(256) void bwd_src_kernel(SK k)
 {
     constexpr int GPB = 256 / G;
     __shared__ SStage stage[GPB];
-    extern __shared__ float lds_acc[];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     SStage &st = stage[gi];
-    float *slot_acc = k.accP + (size_t)blockIdx.x * k.R * D;
-    float *acc_p = LDSACC ? lds_acc : slot_acc;
-    if (LDSACC)
-        for (int i = threadIdx.x; i < k.R * D; i += 256) lds_acc[i] = 0.f;
-    __syncthreads();
-    for (int64_t base = (int64_t)blockIdx.x * GPB; base < k.n_items; base += (int64_t)gridDim.x * GPB) {
-        const int64_t item = base + gi;
-        const bool valid = item < k.n_items;
-        int n0 = 0, nn = 0, q0 = 0, nq = 0;
-        if (valid) {
-            const Item x = k.items[item];
-            n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
-            for (int e = gl; e < nq; e += G) {
-                const int vs = k.out_vseg[q0 + e];
-                st.evs[e] = vs;
-                st.erel[e] = k.vseg_rel[vs];
-                const float2 p = reinterpret_cast<const float2 *>(k.ay)[k.out_pos[q0 + e]];
-                st.ea[e] = p.x;
-                st.ey[e] = p.y;
-            }
-            auto opos = [&](int jj) {
-                const int q = k.out_ptr[n0 + jj];
-                return (q < q0 ? q0 : (q > q0 + nq ? q0 + nq : q)) - q0;
-            };
-            for (int j = gl; j < nn; j += G) {
-                const int a = opos(j), b = opos(j + 1);
-                st.optr[j] = a;
-                for (int e = a; e < b; ++e) st.enode[e] = j;
-            }
-            if (gl == 0) st.optr[nn] = nq;
+    const int64_t item = (int64_t)blockIdx.x * GPB + gi;
+    const bool valid = item < k.n_items;
+    int n0 = 0, nn = 0, q0 = 0, nq = 0;
+    bool split = false;   // a piece of a source whose out-edges span several items
+    if (valid) {
+        const Item x = k.items[item];
+        n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
+        split = nn == 1 && k.out_ptr[n0 + 1] - k.out_ptr[n0] > nq;
+        for (int e = gl; e < nq; e += G) {
+            const int p = k.out_pos[q0 + e];
+            st.evs[e] = k.out_vseg[q0 + e];
+            st.erel[e] = k.out_rel[q0 + e];
+            st.epair[e] = k.e2u[p];
+            const float2 a = reinterpret_cast<const float2 *>(k.ay)[p];
+            st.ea[e] = a.x;
+            st.ey[e] = a.y;
         }
-        __syncthreads();
-        if (valid && nq > 0) {
-            int j = 0;
-            while (st.optr[j + 1] == st.optr[j]) ++j;   // first source with out-edges
-            float4 acc = zero4();
-            float ysrc = 0.f;
-            // ping-pong batches of (dS row, ws'_r row, source row) per out-edge
-            float4 Ad[kU], Aw[kU], Ah[kU], Bd[kU], Bw[kU], Bh[kU];
-            auto load = [&](float4 (&Xd)[kU], float4 (&Xw)[kU], float4 (&Xh)[kU], int b0) {
-#pragma unroll
-                for (int u = 0; u < kU; ++u) {
-                    const int e = b0 + u < nq ? b0 + u : nq - 1;
-                    Xd[u] = ld4(k.dS + (size_t)st.evs[e] * D + gl * 4);
-                    Xw[u] = ld4(k.wsp + (size_t)st.erel[e] * D + gl * 4);
-                    Xh[u] = ld4(k.h + (size_t)(n0 + st.enode[e]) * D + gl * 4);
-                }
-            };
-            auto consume = [&](const float4 (&Xd)[kU], const float4 (&Xw)[kU], const float4 (&Xh)[kU],
-                               int b0) {
-#pragma unroll
-                for (int u = 0; u < kU; ++u) {
-                    const int e = b0 + u;
-                    if (e < nq) {
-                        const float Y = st.ey[e];
-                        acc = lin4(acc, 1.f, Xd[u], st.ea[e]);
-                        acc = lin4(acc, 1.f, Xw[u], Y);
-                        ysrc += Y;
-                        const bool node_end = e + 1 == st.optr[j + 1];
-                        // the last out-edge of the item always ends its source
-                        if (node_end || st.erel[e + 1] != st.erel[e]) {
-                            float *p = acc_p + (size_t)st.erel[e] * D + gl * 4;
-                            atomicAdd(p + 0, ysrc * Xh[u].x);
-                            atomicAdd(p + 1, ysrc * Xh[u].y);
-                            atomicAdd(p + 2, ysrc * Xh[u].z);
-                            atomicAdd(p + 3, ysrc * Xh[u].w);
-                            ysrc = 0.f;
-                        }
-                        if (node_end) {
-                            atomic_add4(k.dh + (size_t)(n0 + j) * D + gl * 4, acc);
-                            acc = zero4();
-                            ++j;
-                            while (j < nn && st.optr[j + 1] == st.optr[j]) ++j;
-                        }
-                    }
-                }
-            };
-            load(Ad, Aw, Ah, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            for (int eb = 0; eb < nq; eb += 2 * kU) {
-                load(Bd, Bw, Bh, eb + kU);
-                __builtin_amdgcn_sched_barrier(0);
-                consume(Ad, Aw, Ah, eb);
-                load(Ad, Aw, Ah, eb + 2 * kU);
-                __builtin_amdgcn_sched_barrier(0);
-                consume(Bd, Bw, Bh, eb + kU);
-            }
+        auto opos = [&](int jj) {
+            const int q = k.out_ptr[n0 + jj];
+            return (q < q0 ? q0 : (q > q0 + nq ? q0 + nq : q)) - q0;
+        };
+        for (int j = gl; j < nn; j += G) {
+            const int a = opos(j), b = opos(j + 1);
+            st.optr[j] = a;
+            for (int e = a; e < b; ++e) st.enode[e] = j;
         }
-        __syncthreads();
+        if (gl == 0) st.optr[nn] = nq;
     }
-    if (LDSACC)
-        for (int i = threadIdx.x; i < k.R * D; i += 256) slot_acc[i] = lds_acc[i];
+    __syncthreads();
+    if (!valid || nq == 0) return;
+    int j = 0;
+    while (st.optr[j + 1] == st.optr[j]) ++j;   // first source with out-edges
+    float4 acc = zero4();
+    float ysrc = 0.f;
+    // ping-pong batches of (dS row, ws'_r row, the source's dh row) per out-edge
+    float4 Ad[kU], Aw[kU], Ah[kU], Bd[kU], Bw[kU], Bh[kU];
+    auto load = [&](float4 (&Xd)[kU], float4 (&Xw)[kU], float4 (&Xh)[kU], int b0) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int e = b0 + u < nq ? b0 + u : nq - 1;
+            Xd[u] = ld4(k.dS + (size_t)st.evs[e] * D + gl * 4);
+            Xw[u] = ld4(k.wsp + (size_t)st.erel[e] * D + gl * 4);
+            Xh[u] = ld4(k.dh + (size_t)(n0 + st.enode[e]) * D + gl * 4);
+        }
+    };
+    auto consume = [&](const float4 (&Xd)[kU], const float4 (&Xw)[kU], const float4 (&Xh)[kU], int b0) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int e = b0 + u;
+            if (e < nq) {
+                const float Y = st.ey[e];
+                acc = lin4(acc, 1.f, Xd[u], st.ea[e]);
+                acc = lin4(acc, 1.f, Xw[u], Y);
+                ysrc += Y;
+                const bool node_end = e + 1 == st.optr[j + 1];
+                // the last out-edge of the item always ends its source
+                if (node_end || st.erel[e + 1] != st.erel[e]) {
+                    if (gl == 0) atomicAdd(k.ypair + st.epair[e], ysrc);
+                    ysrc = 0.f;
+                }
+                if (node_end) {
+                    float *p = k.dh + (size_t)(n0 + j) * D + gl * 4;
+                    if (split) atomic_add4(p, acc);
+                    else st4(p, add4(acc, Xh[u]));
+                    acc = zero4();
+                    ++j;
+                    while (j < nn && st.optr[j + 1] == st.optr[j]) ++j;
+                }
+            }
+        }
+    };
+    load(Ad, Aw, Ah, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int eb = 0; eb < nq; eb += 2 * kU) {
+        load(Bd, Bw, Bh, eb + kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(Ad, Aw, Ah, eb);
+        load(Ad, Aw, Ah, eb + 2 * kU);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(Bd, Bw, Bh, eb + kU);
+    }
+}
+
+// pvec[t] = sum over the compact pairs of tile t (one relation) of
+// ypair[pair] * h[src(pair)]; lanes of 16-lane groups over features, groups
+// over pairs, combined in group order.
+__global__ __launch_bounds__(256) void pair_gemv_kernel(const Tile *tiles, const int32_t *uniq_src,
+                                                        const float *ypair, const float *h, float *pvec)
+{
+    constexpr int NG = 256 / G;
+    __shared__ float4 part[NG][G];
+    const Tile t = tiles[blockIdx.x];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    float4 a0 = zero4(), a1 = zero4();
+    int i = gi;
+    for (; i + NG < t.rows; i += 2 * NG) {
+        const int p0 = t.row0 + i, p1 = p0 + NG;
+        const float y0 = ypair[p0], y1 = ypair[p1];
+        const float4 h0 = ld4(h + (size_t)uniq_src[p0] * D + gl * 4);
+        const float4 h1 = ld4(h + (size_t)uniq_src[p1] * D + gl * 4);
+        a0 = lin4(a0, 1.f, h0, y0);
+        a1 = lin4(a1, 1.f, h1, y1);
+    }
+    if (i < t.rows) {
+        const int p0 = t.row0 + i;
+        a0 = lin4(a0, 1.f, ld4(h + (size_t)uniq_src[p0] * D + gl * 4), ypair[p0]);
+    }
+    part[gi][gl] = add4(a0, a1);
+    __syncthreads();
+    if (gi == 0) {
+        float4 s = zero4();
+        for (int g = 0; g < NG; ++g) s = add4(s, part[g][gl]);
+        st4(pvec + (size_t)blockIdx.x * D + gl * 4, s);
+    }
 }
 
 // ---------------------------------------------------------------- dW
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// partial[c] = sum over the chunk's segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out);
-// yvec[c]   = sum over the chunk's segments of ysum[seg] * h[dst(seg)].
-__global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vseg_byrel,
-                                                         const int32_t *vseg_dst, const float *Sa,
+// Chunk c covers rows [row0, row0 + rows) of the by-relation segment order:
+// partial[c] = sum over its segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out);
+// yvec[c]   = sum over its segments of ysum[seg] * h[dst(seg)].
+__global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
+                                                         const float *Sa,
                                                          const float *Gm, const float *h,
                                                          const float *ysum, float *partial,
                                                          float *yvec)
@@ -464,11 +516,11 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
             const int rr = idx >> 4, c4 = (idx & 15) * 4;
             float4 a = zero4(), b = a;
             if (k0 + rr < t.rows) {
-                const int vs = vseg_byrel[t.row0 + k0 + rr];
-                const int v = vseg_dst[vs];
-                a = ld4(Sa + (size_t)vs * D + c4);
+                const int row = t.row0 + k0 + rr;
+                const int v = vsegdst_byrel[row];
+                a = ld4(Sa + (size_t)row * D + c4);
                 b = ld4(Gm + (size_t)v * D + c4);
-                yacc = lin4(yacc, 1.f, ld4(h + (size_t)v * D + c4), ysum[vs]);
+                yacc = lin4(yacc, 1.f, ld4(h + (size_t)v * D + c4), ysum[row]);
             }
             *reinterpret_cast<float4 *>(&As[rr * P + c4]) = a;
             *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = b;
@@ -496,23 +548,26 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     }
 }
 
-// Per relation r: pws = sum of the workgroup dws' slots, pwt = sum of the
-// relation's chunk ysum*h vectors, both in a fixed order.
-__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float *accP, int nslots, int R,
-                                                         const float *yvec, const int32_t *rel_chunkptr,
-                                                         float *pws, float *pwt)
+// Per relation r: pws = sum of r's pair-tile vectors, pwt = sum of r's
+// segment-chunk vectors, both in a fixed order.
+__global__ __launch_bounds__(1024) void bwd_reduce_kernel(const float *pvec, const int32_t *rel_pairtileptr,
+                                                          const float *yvec, const int32_t *rel_chunkptr,
+                                                          float *pws, float *pwt)
 {
-    __shared__ float red[2][4][D];
+    constexpr int NC = 1024 / D;
+    __shared__ float red[2][NC][D];
     const int r = blockIdx.x, i = threadIdx.x % D, c = threadIdx.x / D;
     float a = 0.f, b = 0.f;
-    for (int sl = c; sl < nslots; sl += 4) a += accP[((size_t)sl * R + r) * D + i];
-    for (int ch = rel_chunkptr[r] + c; ch < rel_chunkptr[r + 1]; ch += 4) b += yvec[(size_t)ch * D + i];
+    for (int t = rel_pairtileptr[r] + c; t < rel_pairtileptr[r + 1]; t += NC) a += pvec[(size_t)t * D + i];
+    for (int ch = rel_chunkptr[r] + c; ch < rel_chunkptr[r + 1]; ch += NC) b += yvec[(size_t)ch * D + i];
     red[0][c][i] = a;
     red[1][c][i] = b;
     __syncthreads();
     if (c == 0) {
-        pws[(size_t)r * D + i] = (red[0][0][i] + red[0][1][i]) + (red[0][2][i] + red[0][3][i]);
-        pwt[(size_t)r * D + i] = (red[1][0][i] + red[1][1][i]) + (red[1][2][i] + red[1][3][i]);
+        float x = 0.f, y = 0.f;
+        for (int cc = 0; cc < NC; ++cc) { x += red[0][cc][i]; y += red[1][cc][i]; }
+        pws[(size_t)r * D + i] = x;
+        pwt[(size_t)r * D + i] = y;
     }
 }
 
@@ -561,7 +616,7 @@ __global__ void zero_kernel(float *p, int64_t n)
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct BwdWs {
-    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *ay, *ysum, *accP, *pws, *pwt, *partial, *yvec;
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
 };
 
 size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
@@ -584,7 +639,8 @@ size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
     x.sv = take((size_t)std::max<int64_t>(g->N, 1));
     x.ay = take((size_t)g->E * 2);
     x.ysum = take((size_t)std::max<int64_t>(g->V, 1));
-    x.accP = take((size_t)kAccBlocks * g->R * D);
+    x.ypair = take((size_t)std::max<int64_t>(g->U_src, 1));
+    x.pvec = take((size_t)std::max<int64_t>(g->n_tiles_pairs, 1) * D);
     x.pws = take((size_t)g->R * D);
     x.pwt = take((size_t)g->R * D);
     x.partial = take(nchunks * D * D);
@@ -632,12 +688,13 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     ga.X = Gm; ga.ldx = D; ga.gather = g->dev.vsegdst_byrel;
     ga.W[0] = W; ga.trans_b = 1; ga.K = D; ga.Nc = D;
     ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
-    ga.Y = w.dS; ga.ldy = D; ga.scatter = g->dev.vseg_byrel;
+    ga.Y = w.dS; ga.ldy = D; ga.scatter = nullptr;   // dS rows in by-relation order
     if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
 
     BK k{};
     k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr; k.vseg_rel = g->dev.vseg_rel;
+    k.vseg_pos = g->dev.vseg_pos; k.wtp = w.wtp; k.dh = dh;
     k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
     k.ysum = w.ysum;
@@ -666,51 +723,43 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                 hipLaunchKernelGGL((bwd_traverse_kernel<1>), grid, dim3(256), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
+            {
+                LaunchScope ls("rgat_bwd_split_dst_term", s);
+                hipLaunchKernelGGL(split_dst_term_kernel, dim3((unsigned)g->n_split), dim3(256), 0, s,
+                                   g->dev.split_dst, g->dev.dst_vsegptr, g->dev.vseg_rel, g->dev.vseg_pos,
+                                   w.ysum, w.wtp, dh);
+            }
+            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
         }
     }
-    if (g->N) {   // dh = destination terms (every row written)
-        DK dk{g->N, g->dev.dst_vsegptr, g->dev.vseg_rel, w.ysum, w.wtp, dh};
-        {
-            LaunchScope ls("rgat_bwd_dst_term", s);
-            hipLaunchKernelGGL(bwd_dst_term_kernel, dim3((unsigned)((g->N + 15) / 16)), dim3(256), 0, s, dk);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "dst_term launch");
-        if (g->n_big_vdst) {
-            LaunchScope ls("rgat_bwd_dst_term_big", s);
-            hipLaunchKernelGGL(bwd_dst_term_big_kernel, dim3((unsigned)g->n_big_vdst), dim3(1024), 0, s, dk,
-                               g->dev.big_vdst);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "dst_term_big launch");
-    }
-    // dh += source terms; dws' per workgroup slot
-    const int nslots = (int)std::min<int64_t>(kAccBlocks, std::max<int64_t>((g->n_oitems + 15) / 16, 1));
-    const bool lds_acc = g->R <= kLdsAccRels;
-    if (!lds_acc && (e = zero(w.accP, (int64_t)nslots * g->R * D, s)) != hipSuccess)
-        return hip_fail(e, "zero launch");
-    {
+    // dh += source terms (dh holds the destination terms); Y sums per compact pair
+    if ((e = zero(w.ypair, g->U_src, s)) != hipSuccess) return hip_fail(e, "zero launch");
+    if (g->n_oitems) {
         SK sk{};
         sk.n_items = g->n_oitems; sk.items = g->dev.oitems; sk.out_ptr = g->dev.out_ptr;
-        sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.vseg_rel = g->dev.vseg_rel;
-        sk.h = h; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.accP = w.accP; sk.R = g->R;
+        sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.out_rel = g->dev.out_rel;
+        sk.e2u = g->dev.e2u; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.ypair = w.ypair;
         LaunchScope ls("rgat_bwd_src", s);
-        if (lds_acc)
-            hipLaunchKernelGGL((bwd_src_kernel<true>), dim3((unsigned)nslots), dim3(256),
-                               (size_t)g->R * D * sizeof(float), s, sk);
-        else
-            hipLaunchKernelGGL((bwd_src_kernel<false>), dim3((unsigned)nslots), dim3(256), 0, s, sk);
+        hipLaunchKernelGGL(bwd_src_kernel, dim3((unsigned)((g->n_oitems + 15) / 16)), dim3(256), 0, s, sk);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_src launch");
+    if (g->n_tiles_pairs) {   // dws' per pair tile
+        LaunchScope ls("rgat_bwd_pair_gemv", s);
+        hipLaunchKernelGGL(pair_gemv_kernel, dim3((unsigned)g->n_tiles_pairs), dim3(256), 0, s,
+                           g->dev.tiles_pairs, g->dev.uniq_src, w.ypair, h, w.pvec);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "pair_gemv launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
         hipLaunchKernelGGL(outer_gemm_kernel, dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
-                           g->dev.tiles_outer, g->dev.vseg_byrel, g->dev.vseg_dst, w.Sa, Gm, h, w.ysum,
+                           g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, Gm, h, w.ysum,
                            w.partial, w.yvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");
     {
         LaunchScope ls("rgat_bwd_reduce", s);
-        hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g->R), dim3(256), 0, s, w.accP, nslots, g->R,
-                           w.yvec, g->dev.rel_chunkptr, w.pws, w.pwt);
+        hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g->R), dim3(1024), 0, s, w.pvec,
+                           g->dev.rel_pairtileptr, w.yvec, g->dev.rel_chunkptr, w.pws, w.pwt);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_reduce launch");
     {

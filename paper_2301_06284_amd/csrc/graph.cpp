@@ -204,8 +204,15 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             std::vector<int32_t> pos_vseg((size_t)E);
             for (int64_t vs = 0; vs < g->V; ++vs)
                 for (int32_t i = x.vseg_ptr[vs]; i < x.vseg_ptr[vs + 1]; ++i) pos_vseg[i] = (int32_t)vs;
+            // out_vseg holds the by-relation position of the in-edge's vseg
+            x.vseg_pos.resize((size_t)g->V);
+            for (int64_t i = 0; i < g->V; ++i) x.vseg_pos[x.vseg_byrel[i]] = (int32_t)i;
             x.out_vseg.resize((size_t)E);
-            for (int64_t q = 0; q < E; ++q) x.out_vseg[q] = pos_vseg[x.out_pos[q]];
+            x.out_rel.resize((size_t)E);
+            for (int64_t q = 0; q < E; ++q) {
+                x.out_vseg[q] = x.vseg_pos[pos_vseg[x.out_pos[q]]];
+                x.out_rel[q] = x.in_rel[x.out_pos[q]];
+            }
             // work items over out-edges: bundles of small sources, pieces of large ones
             x.oitems.clear();
             auto odeg = [&](int64_t u) { return x.out_ptr[u + 1] - x.out_ptr[u]; };
@@ -244,6 +251,9 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.rel_chunkptr.assign((size_t)R + 1, 0);
         for (const Tile &t : x.tiles_outer) x.rel_chunkptr[(size_t)t.type + 1]++;
         for (int32_t r = 0; r < R; ++r) x.rel_chunkptr[r + 1] += x.rel_chunkptr[r];
+        x.rel_pairtileptr.assign((size_t)R + 1, 0);
+        for (const Tile &t : x.tiles_pairs) x.rel_pairtileptr[(size_t)t.type + 1]++;
+        for (int32_t r = 0; r < R; ++r) x.rel_pairtileptr[r + 1] += x.rel_pairtileptr[r];
     } catch (const std::bad_alloc &) {
         return fail(RGNN_ENOMEM, "host allocation failed while building the graph index");
     }
@@ -273,6 +283,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.vseg_cnt, x.vseg_cnt); add32(&d.dst_vsegptr, x.dst_vsegptr);
     add32(&d.vseg_byrel, x.vseg_byrel); add32(&d.rel_vsegptr, x.rel_vsegptr);
     add32(&d.vsegdst_byrel, x.vsegdst_byrel); add32(&d.rel_chunkptr, x.rel_chunkptr);
+    add32(&d.rel_pairtileptr, x.rel_pairtileptr);
     add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
     add32(&d.split_slotptr, x.split_slotptr);
     add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
@@ -283,6 +294,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
+    add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
@@ -350,6 +362,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         g->host.in_src.swap(empty.in_src); g->host.in_rel.swap(empty.in_rel);
         g->host.in_eid.swap(empty.in_eid); g->host.e2u.swap(empty.e2u);
         g->host.out_pos.swap(empty.out_pos); g->host.out_vseg.swap(empty.out_vseg);
+        g->host.out_rel.swap(empty.out_rel);
     }
     *out = g;
     return RGNN_OK;

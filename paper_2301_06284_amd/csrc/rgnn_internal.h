@@ -46,8 +46,10 @@ struct HostIndex {
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
+    std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
     // out-edges (source-major view of the sorted in-edges), for the backward pass
-    std::vector<int32_t> out_ptr, out_pos, out_vseg;
+    std::vector<int32_t> out_ptr, out_pos, out_vseg, out_rel;
+    std::vector<int32_t> vseg_pos;       // position of each vseg in the by-relation order
     std::vector<Item> oitems;            // {node0, node1, q0, q1} over out-edge offsets
 };
 
@@ -61,13 +63,14 @@ struct DeviceIndex {
     int32_t *ntype_perm = nullptr, *ntype_ptr = nullptr;
     int32_t *vseg_ptr = nullptr, *vseg_rel = nullptr, *vseg_dst = nullptr, *vseg_cnt = nullptr;
     int32_t *dst_vsegptr = nullptr, *vseg_byrel = nullptr, *rel_vsegptr = nullptr;
-    int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr;
+    int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr, *rel_pairtileptr = nullptr;
     Item *items = nullptr;
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
-    int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr;
+    int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr, *out_rel = nullptr;
+    int32_t *vseg_pos = nullptr;
     Item *oitems = nullptr;
 };
 
