@@ -38,6 +38,7 @@
 //      one relation (also summing ysum * h_v per chunk for dwt'); then a
 //      deterministic combine of the chunks and a per-relation finalize.
 #include "rgnn_internal.h"
+#include "wave_ops.h"
 
 namespace rgnn {
 
@@ -60,14 +61,6 @@ __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 __device__ __forceinline__ void atomic_add4(float *p, float4 v)
 {
     atomicAdd(p + 0, v.x); atomicAdd(p + 1, v.y); atomicAdd(p + 2, v.z); atomicAdd(p + 3, v.w);
-}
-
-template <int W>
-__device__ __forceinline__ float gsum(float x)
-{
-#pragma unroll
-    for (int off = W / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, W);
-    return x;
 }
 
 // ---------------------------------------------------------------- destination-major traversal

@@ -31,6 +31,7 @@
 // D[4*(l/16)+v][l%16], v = 0..3.  The k-slot q = l/16 of step (c, t) is mapped
 // to the actual reduction index kk = 16c + 4q + t, identically for A and B.
 #include "rgnn_internal.h"
+#include "wave_ops.h"
 
 namespace rgnn {
 
@@ -194,10 +195,7 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
 #pragma unroll
                     for (int cb = 0; cb < NCB; ++cb)
                         if (cb / cbh == hh) part += val[cb] * dv[cb];
-                    part += __shfl_xor(part, 8, 16);
-                    part += __shfl_xor(part, 4, 16);
-                    part += __shfl_xor(part, 2, 16);
-                    part += __shfl_xor(part, 1, 16);
+                    part = gsum<16>(part);
                     if (valid && li == 0) a.dot_out[yr * a.dot_heads + hh] = part;
                 }
             }

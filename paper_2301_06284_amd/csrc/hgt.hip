@@ -19,6 +19,7 @@
 // K|V rows of its edges, with their destinations' query rows, kU at a time
 // with the next kU in flight.
 #include "rgnn_internal.h"
+#include "wave_ops.h"
 
 namespace rgnn {
 
@@ -34,14 +35,6 @@ __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-
-template <int W>
-__device__ __forceinline__ float gsum(float x)
-{
-#pragma unroll
-    for (int off = W / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, W);
-    return x;
-}
 
 constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
@@ -67,6 +60,16 @@ struct HK {
     float *agg, *partial;
 };
 
+// Value of lane jj of this lane's head (LH aligned lanes).  A DPP quad
+// broadcast would serve LH = 4 without the LDS crossbar, but it lets the LDS
+// matrix rows of several steps be hoisted ahead of their FMAs and the 1024-lane
+// launch bound then spills; ds_bpermute keeps one step live at a time.
+template <int LH>
+__device__ __forceinline__ float head_bcast(float v, int jj, int base)
+{
+    return __shfl(v, base + jj, G);
+}
+
 // y[4 values of this lane] = x_head (1 x dk) . Mat (dk x dk), Mat row-major,
 // with x_head distributed over the head's LH lanes (4 values each).
 template <int LH>
@@ -78,12 +81,13 @@ __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
     float4 y = zero4();
 #pragma unroll
     for (int jj = 0; jj < LH; ++jj) {
-        const float x0 = __shfl(x.x, base + jj, G), x1 = __shfl(x.y, base + jj, G);
-        const float x2 = __shfl(x.z, base + jj, G), x3 = __shfl(x.w, base + jj, G);
+        const float x0 = head_bcast<LH>(x.x, jj, base), x1 = head_bcast<LH>(x.y, jj, base);
+        const float x2 = head_bcast<LH>(x.z, jj, base), x3 = head_bcast<LH>(x.w, jj, base);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 0) * DK + c0), x0);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 1) * DK + c0), x1);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 2) * DK + c0), x2);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 3) * DK + c0), x3);
+        __builtin_amdgcn_sched_barrier(0);   // bound the live LDS rows to one step
     }
     return y;
 }
@@ -98,12 +102,13 @@ __device__ __forceinline__ float4 head_matvec_t(float4 x, const float *Mt, int g
     float4 y = zero4();
 #pragma unroll
     for (int jj = 0; jj < LH; ++jj) {
-        const float4 xj = make_float4(__shfl(x.x, base + jj, G), __shfl(x.y, base + jj, G),
-                                      __shfl(x.z, base + jj, G), __shfl(x.w, base + jj, G));
+        const float4 xj = make_float4(head_bcast<LH>(x.x, jj, base), head_bcast<LH>(x.y, jj, base),
+                                      head_bcast<LH>(x.z, jj, base), head_bcast<LH>(x.w, jj, base));
         y.x += dot4(ld4(Mt + (c0 + 0) * DK + 4 * jj), xj);
         y.y += dot4(ld4(Mt + (c0 + 1) * DK + 4 * jj), xj);
         y.z += dot4(ld4(Mt + (c0 + 2) * DK + 4 * jj), xj);
         y.w += dot4(ld4(Mt + (c0 + 3) * DK + 4 * jj), xj);
+        __builtin_amdgcn_sched_barrier(0);
     }
     return y;
 }

@@ -24,6 +24,7 @@
 //      destination boundaries.
 // Forward traversals use no atomics: results are bitwise reproducible.
 #include "rgnn_internal.h"
+#include "wave_ops.h"
 
 namespace rgnn {
 
@@ -42,21 +43,6 @@ __device__ __forceinline__ float4 relu4(float4 a)
     return make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
 }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-
-template <int W>
-__device__ __forceinline__ float gsum(float x)
-{
-#pragma unroll
-    for (int off = W / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, W);
-    return x;
-}
-template <int W>
-__device__ __forceinline__ float gmax(float x)
-{
-#pragma unroll
-    for (int off = W / 2; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, W));
-    return x;
-}
 
 __device__ __forceinline__ float leaky(float y, float slope) { return y > 0.f ? y : slope * y; }
 
