@@ -10,8 +10,9 @@
 //     so that each lane fetches four k-values of one column with ds_read_b128;
 //   * each wave computes 16-row blocks with v_mfma_f32_16x16x4f32: the A rows
 //     are gathered straight from global memory (each lane reads 64 contiguous
-//     bytes of its row per load); the next block's rows are prefetched while
-//     the current block runs on the MFMA units;
+//     bytes of its row per load); the rows of the next block (two ahead for
+//     64 x 64 weights) are prefetched while the current block runs on the
+//     MFMA units;
 //   * the epilogue fuses what the paper's fusion rule allows into the GEMM --
 //     a per-row scalar (attention normalisation), a per-row dot product with a
 //     per-type vector (the reordered attention term), residual add,
@@ -23,13 +24,16 @@
 // order, so waiting for any load also waits for every older one.  All loads
 // are unconditional (out-of-tile rows are clamped to a valid row) and issued
 // in the order they are consumed: epilogue operands of block i, then the rows
-// of block i+1, so the MFMAs and the epilogue of block i never wait for the
-// prefetch of block i+1.
+// of block i+PF, so the MFMAs and the epilogue of block i never wait for the
+// prefetches of the blocks after it.
 //
 // MFMA operand layout used (v_mfma_f32_16x16x4f32, one block): lane l supplies
 // A[l%16][l/16] and B[l/16][l%16]; the 4 accumulator VGPRs of lane l hold
-// D[4*(l/16)+v][l%16], v = 0..3.  The k-slot q = l/16 of step (c, t) is mapped
-// to the actual reduction index kk = 16c + 4q + t, identically for A and B.
+// D[4*(l/16)+v][l%16], v = 0..3.  The kernel computes the transposed block
+// D = W^T X^T (A = W^T from LDS, B = the gathered rows), so lane l holds row
+// l%16 and four consecutive columns 4*(l/16) .. +3: one float4 store per
+// column block.  The k-slot q = l/16 of step (c, t) is mapped to the actual
+// reduction index kk = 16c + 4q + t, identically for A and B.
 #include "rgnn_internal.h"
 #include "wave_ops.h"
 
@@ -57,19 +61,21 @@ struct GemmK {
     float *Y; int64_t ldy;
     const int32_t *scatter;
     const float *row_scale;
-    const float *dot_vec; float *dot_out; int dot_heads;
+    const float *dot_vec; float *dot_out;
     const float *residual; int64_t ld_res;
     float *Y2; int64_t ldy2; int split;
 };
 
-template <int K, int NC, int EP>
+template <int K, int NC, int EP, int DH>
 __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
 {
     constexpr int KP = K + 4;           // padded LDS row (conflict-free b128 reads)
     constexpr int NCB = NC / 16;        // 16-column blocks
     constexpr int KC = K / 16;          // 16-wide k chunks (4 MFMA steps each)
     constexpr int MB = kGemmTileRows / 64;
+    constexpr int CBH = NCB / DH;       // column blocks per dot-product head
     __shared__ float Wt[NC * KP];
+    __shared__ float dvs[(EP & EP_DOT) ? NC : 1];
 
     const Tile tile = a.tiles[blockIdx.x];
     const int tid = threadIdx.x;
@@ -95,67 +101,70 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
                 Wt[(n4 + 3) * KP + k] = w.w;
             }
         }
-    }
-    float dv[NCB];
-    if (EP & EP_DOT) {
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) dv[cb] = a.dot_vec[(size_t)tile.type * NC + cb * 16 + li];
+        if (EP & EP_DOT)
+            for (int n = tid; n < NC; n += 256) dvs[n] = a.dot_vec[(size_t)tile.type * NC + n];
     }
     __syncthreads();
 
-    // Row blocks of this wave: rb = wave + 4 i, i < MB.
+    // Row blocks of this wave: rb = wave + 4 i, i < MB.  Lane (li, q) owns row
+    // 16 rb + li of the block and, per column block cb, columns 16 cb + 4q .. +3.
     const int nrb = (tile.rows + 15) >> 4;
     const int32_t *any_idx = reinterpret_cast<const int32_t *>(a.tiles + blockIdx.x);
-    int xr[MB];
+    int xr[MB], yr[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int r = (wave + 4 * i) * 16 + li;
         const int grow = tile.row0 + (r < tile.rows ? r : 0);
-        const int ld = *(a.gather ? a.gather + grow : any_idx);
-        xr[i] = a.gather ? ld : grow;
+        const int lg = *(a.gather ? a.gather + grow : any_idx);
+        const int ls = *(a.scatter ? a.scatter + grow : any_idx);
+        xr[i] = a.gather ? lg : grow;
+        yr[i] = a.scatter ? ls : grow;
     }
-    float4 acur[KC], anext[KC];
-    int64_t ycur[4], ynext[4];
-    auto load_block = [&](int i, float4 (&dst)[KC], int64_t (&ys)[4]) {
+    // Row blocks are prefetched PF blocks ahead (two for 64 x 64 weights, one
+    // for wider ones whose accumulators and B fragments already fill the VGPR
+    // budget); the loop is fully unrolled, so each block's registers are live
+    // only from its load to its MFMAs.
+    constexpr int PF = K * NC <= 64 * 64 ? 2 : 1;
+    float4 ab[MB][KC];
+    auto load_block = [&](int i) {
         const float *p = a.X + (int64_t)xr[i] * a.ldx + q * 4;
 #pragma unroll
-        for (int c = 0; c < KC; ++c) dst[c] = *reinterpret_cast<const float4 *>(p + c * 16);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = (wave + 4 * i) * 16 + q * 4 + v;
-            const int grow = tile.row0 + (r < tile.rows ? r : 0);
-            const int ld = *(a.scatter ? a.scatter + grow : any_idx);
-            ys[v] = a.scatter ? ld : grow;
-        }
+        for (int c = 0; c < KC; ++c) ab[i][c] = *reinterpret_cast<const float4 *>(p + c * 16);
     };
-    load_block(0, acur, ycur);
+#pragma unroll
+    for (int i = 0; i < PF && i < MB; ++i) load_block(i);
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int rb = wave + 4 * i;
         if (rb >= nrb) break;
+        const int64_t y = yr[i];
+        const bool valid = rb * 16 + li < tile.rows;
         // (a) epilogue operands of this block
-        float sc[4];
-        float ex[4][NCB];
-        if (EP & EP_SCALE) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) sc[v] = a.row_scale[ycur[v]];
-        }
+        float sc = 1.f;
+        float4 ex[NCB];
+        if (EP & EP_SCALE) sc = a.row_scale[y];
         if (EP & (EP_RESID | EP_ACC)) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const int col = cb * 16 + li;
-                    float x = 0.f;
-                    if (EP & EP_RESID) x += a.residual[ycur[v] * a.ld_res + col];
-                    if (EP & EP_ACC) x += a.Y[ycur[v] * a.ldy + col];
-                    ex[v][cb] = x;
+            for (int cb = 0; cb < NCB; ++cb) {
+                float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (EP & EP_RESID) {
+                    const float4 t = *reinterpret_cast<const float4 *>(a.residual + y * a.ld_res + cb * 16 + q * 4);
+                    x = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
                 }
+                if (EP & EP_ACC) {
+                    const float4 t = *reinterpret_cast<const float4 *>(a.Y + y * a.ldy + cb * 16 + q * 4);
+                    x = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
+                }
+                ex[cb] = x;
+            }
         }
-        // (b) rows and scatter indices of the next block
-        if (i + 1 < MB) load_block(i + 1, anext, ynext);
-        // (c) MFMAs; B fragments are re-read from LDS for every row block
-        // (keeping the whole weight tile in VGPRs would cap occupancy)
+        // (b) rows of block i + PF
+        if (i + PF < MB) load_block(i + PF);
+        // (c) MFMAs, with W^T as the A operand and the gathered rows as B, so
+        // that the accumulator of lane (li, q) holds row li, columns 4q..4q+3
+        // of each column block.  The W fragments are re-read from LDS for every
+        // row block (keeping the whole weight tile in VGPRs would cap occupancy).
+        const float4 (&acur)[KC] = ab[i];
         floatx4 acc[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -168,70 +177,77 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
                 b[cb] = *reinterpret_cast<const float4 *>(&Wt[(cb * 16 + li) * KP + c * 16 + q * 4]);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(acur[c].x, b[cb].x, acc[cb], 0, 0, 0);
+                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].x, acur[c].x, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(acur[c].y, b[cb].y, acc[cb], 0, 0, 0);
+                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].y, acur[c].y, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(acur[c].z, b[cb].z, acc[cb], 0, 0, 0);
+                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].z, acur[c].z, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(acur[c].w, b[cb].w, acc[cb], 0, 0, 0);
+                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].w, acur[c].w, acc[cb], 0, 0, 0);
         }
-        // (d) epilogue: rows 16*rb + 4q + v, columns 16*cb + li
+        // (d) epilogue
+        float4 o[NCB];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = rb * 16 + q * 4 + v;
-            const bool valid = r < tile.rows;
-            const int64_t yr = ycur[v];
-            float val[NCB];
+        for (int cb = 0; cb < NCB; ++cb) {
+            o[cb] = make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
+            if (EP & EP_SCALE) o[cb] = make_float4(o[cb].x * sc, o[cb].y * sc, o[cb].z * sc, o[cb].w * sc);
+        }
+        if (EP & EP_DOT) {
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) val[cb] = (EP & EP_SCALE) ? acc[cb][v] * sc[v] : acc[cb][v];
-            if (EP & EP_DOT) {
-                const int cbh = NCB / a.dot_heads;     // column blocks per head
-                for (int hh = 0; hh < a.dot_heads; ++hh) {
-                    float part = 0.f;
+            for (int hh = 0; hh < DH; ++hh) {
+                float part = 0.f;
 #pragma unroll
-                    for (int cb = 0; cb < NCB; ++cb)
-                        if (cb / cbh == hh) part += val[cb] * dv[cb];
-                    part = gsum<16>(part);
-                    if (valid && li == 0) a.dot_out[yr * a.dot_heads + hh] = part;
+                for (int cb = hh * CBH; cb < (hh + 1) * CBH; ++cb) {
+                    const float4 d = *reinterpret_cast<const float4 *>(&dvs[cb * 16 + q * 4]);
+                    part += o[cb].x * d.x + o[cb].y * d.y + o[cb].z * d.z + o[cb].w * d.w;
                 }
-            }
-            if (!valid) continue;
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int col = cb * 16 + li;
-                float o = val[cb];
-                if (EP & (EP_RESID | EP_ACC)) o += ex[v][cb];
-                if (EP & EP_RELU) o = fmaxf(o, 0.f);
-                if ((EP & EP_SPLIT) && col >= a.split) a.Y2[yr * a.ldy2 + (col - a.split)] = o;
-                else a.Y[yr * a.ldy + col] = o;
+                part += __shfl_xor(part, 16);
+                part += __shfl_xor(part, 32);
+                if (valid && q == 0) a.dot_out[y * DH + hh] = part;
             }
         }
+        if (!valid) continue;
 #pragma unroll
-        for (int c = 0; c < KC; ++c) acur[c] = anext[c];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) ycur[v] = ynext[v];
+        for (int cb = 0; cb < NCB; ++cb) {
+            float4 v = o[cb];
+            if (EP & (EP_RESID | EP_ACC)) v = make_float4(v.x + ex[cb].x, v.y + ex[cb].y, v.z + ex[cb].z, v.w + ex[cb].w);
+            if (EP & EP_RELU) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
+            const int col = cb * 16 + q * 4;
+            if ((EP & EP_SPLIT) && cb * 16 >= a.split)
+                *reinterpret_cast<float4 *>(a.Y2 + y * a.ldy2 + (col - a.split)) = v;
+            else
+                *reinterpret_cast<float4 *>(a.Y + y * a.ldy + col) = v;
+        }
     }
 }
 
-template <int K, int NC, int EP>
+template <int K, int NC, int EP, int DH = 1>
 void launch_k(const GemmK &k, int64_t ntiles, hipStream_t s)
 {
-    hipLaunchKernelGGL((typed_gemm_kernel<K, NC, EP>), dim3((unsigned)ntiles), dim3(256), 0, s, k);
+    hipLaunchKernelGGL((typed_gemm_kernel<K, NC, EP, DH>), dim3((unsigned)ntiles), dim3(256), 0, s, k);
 }
 
 // Epilogues instantiated per shape: square shapes serve every layer; the
 // rectangular ones serve RGCN with d_in != d_out and the segment-MM entry
 // point; 64 x 192 is the fused K|V|Q projection of HGT.
 template <int K, int NC>
-bool dispatch_square(int ep, const GemmK &k, int64_t n, hipStream_t s)
+bool dispatch_square(int ep, int heads, const GemmK &k, int64_t n, hipStream_t s)
 {
     switch (ep) {
     case 0: launch_k<K, NC, 0>(k, n, s); return true;
-    case EP_DOT: launch_k<K, NC, EP_DOT>(k, n, s); return true;
+    case EP_DOT:
+        switch (heads) {
+        case 1: launch_k<K, NC, EP_DOT, 1>(k, n, s); return true;
+        case 2: launch_k<K, NC, EP_DOT, 2>(k, n, s); return true;
+        case 4: launch_k<K, NC, EP_DOT, 4>(k, n, s); return true;
+        case 8:
+            if constexpr (NC >= 128) { launch_k<K, NC, EP_DOT, 8>(k, n, s); return true; }
+            return false;
+        default: return false;
+        }
     case EP_SCALE: launch_k<K, NC, EP_SCALE>(k, n, s); return true;
     case EP_ACC: launch_k<K, NC, EP_ACC>(k, n, s); return true;
     case EP_ACC | EP_RELU: launch_k<K, NC, EP_ACC | EP_RELU>(k, n, s); return true;
@@ -262,7 +278,7 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
     k.nparts = a.nparts; k.trans_b = a.trans_b;
     k.tiles = a.tiles; k.Y = a.Y; k.ldy = a.ldy; k.scatter = a.scatter;
     k.row_scale = a.ep.row_scale;
-    k.dot_vec = a.ep.dot_vec; k.dot_out = a.ep.dot_out; k.dot_heads = a.ep.dot_heads;
+    k.dot_vec = a.ep.dot_vec; k.dot_out = a.ep.dot_out;
     k.residual = a.ep.residual; k.ld_res = a.ep.ld_res;
     k.Y2 = a.ep.Y2; k.ldy2 = a.ep.ldy2; k.split = a.ep.split;
     if (a.trans_b && a.nparts != 1) return fail(RGNN_EINVAL, "transposed B takes one part");
@@ -275,8 +291,8 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
     bool ok = false;
     {
         LaunchScope ls("typed_gemm", s);
-        if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, k, a.ntiles, s);
-        else if (a.K == 128 && a.Nc == 128) ok = dispatch_square<128, 128>(ep, k, a.ntiles, s);
+        if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, a.ep.dot_heads, k, a.ntiles, s);
+        else if (a.K == 128 && a.Nc == 128) ok = dispatch_square<128, 128>(ep, a.ep.dot_heads, k, a.ntiles, s);
         else if (a.K == 64 && a.Nc == 128) ok = dispatch_rect<64, 128>(ep, k, a.ntiles, s);
         else if (a.K == 128 && a.Nc == 64) ok = dispatch_rect<128, 64>(ep, k, a.ntiles, s);
         else if (a.K == 64 && a.Nc == 192 && ep == EP_SPLIT) {
