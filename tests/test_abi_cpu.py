@@ -31,7 +31,7 @@ def test_header_symbols_exported():
     assert declared <= set(rgnn.EXPORTED) | {"rgnn_graph_t"}
 
 
-@pytest.mark.parametrize("kind", ["random", "hub", "dups", "isolated", "empty", "complete"])
+@pytest.mark.parametrize("kind", ["random", "hub", "srchub", "dups", "isolated", "empty", "complete"])
 @pytest.mark.parametrize("seed", [0, 1])
 def test_host_graph_index_bit_exact(kind, seed):
     rgnn = _rgnn()

@@ -11,7 +11,7 @@ from helpers import TOL, Runner, row_err
 
 pytestmark = pytest.mark.gpu
 
-KINDS = ["random", "hub", "dups", "isolated", "empty"]
+KINDS = ["random", "hub", "srchub", "dups", "isolated", "empty"]
 
 
 @pytest.fixture(scope="module", autouse=True)

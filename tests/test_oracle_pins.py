@@ -16,7 +16,7 @@ import torch
 import oracle
 from workloads import tiny_graph, tiny_tensors
 
-KINDS = ["random", "hub", "dups", "isolated", "empty"]
+KINDS = ["random", "hub", "srchub", "dups", "isolated", "empty"]
 
 
 def dense_adj(g):

@@ -168,6 +168,7 @@ def tiny_graph(seed: int, N: int, E: int, R: int, T: int = 1, kind: str = "rando
 
     kind: "random"   uniform ends and relations (self-edges and duplicates occur);
           "hub"      half the edges point at node 0;
+          "srchub"   half the edges leave node 0;
           "complete" every ordered pair (s, t) once, including s == t, relation 0;
           "isolated" destinations drawn from the first half of the nodes only;
           "dups"     a few (u, v, r) triples repeated many times;
@@ -187,8 +188,8 @@ def tiny_graph(seed: int, N: int, E: int, R: int, T: int = 1, kind: str = "rando
         src = rng.integers(0, N, E, dtype=np.int32)
         dst = rng.integers(0, N, E, dtype=np.int32)
         rel = rng.integers(0, R, E, dtype=np.int32)
-        if kind == "hub":
-            dst[: E // 2] = 0
+        if kind in ("hub", "srchub"):
+            (dst if kind == "hub" else src)[: E // 2] = 0
             perm = rng.permutation(E)
             src, dst, rel = src[perm], dst[perm], rel[perm]
         elif kind == "isolated":
