@@ -155,13 +155,15 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     return c.off;
 }
 
-struct HgtWs { float *KV, *Q, *agg, *partial; };
+struct HgtWs { float *KV, *Q, *QP, *Wqp, *agg, *partial; };
 size_t hgt_layout(const rgnn_graph *g, int d, int H, void *base, HgtWs *w)
 {
     Carver c(base);
     HgtWs x{};
     x.KV = c.take<float>((size_t)g->N * 2 * d);
     x.Q = c.take<float>((size_t)g->N * d);
+    x.QP = c.take<float>((size_t)g->V * d);
+    x.Wqp = c.take<float>((size_t)g->R * d * d);
     x.agg = c.take<float>((size_t)g->N * d);
     x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d));
     if (w) *w = x;
@@ -460,9 +462,17 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     ga.Y = w.KV; ga.ldy = 2 * d;
     ga.ep.Y2 = w.Q; ga.ep.ldy2 = d; ga.ep.split = 2 * d;
     if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r] (segment MM over relations)
+    if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) return st;
+    GemmArgs gq;
+    gq.X = w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
+    gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
+    gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
+    gq.Y = w.QP; gq.ldy = d;
+    if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
     HgtArgs ha;
-    ha.g = g; ha.KV = w.KV; ha.Q = w.Q; ha.Watt = Watt; ha.Wmsg = Wmsg; ha.mu = mu;
-    ha.scale = att_scale; ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
+    ha.g = g; ha.KV = w.KV; ha.QP = w.QP; ha.Wmsg = Wmsg;
+    ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
     if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
     if ((st = launch_merge_partials(g, d, heads, 1, w.partial, w.agg, nullptr, 0, s)) != RGNN_OK)
         return st;

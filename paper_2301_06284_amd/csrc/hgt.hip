@@ -4,20 +4,22 @@
 // side by side, 512 bytes per node at d = 64) and are gathered once per edge.
 // Both per-relation head matrices are moved to the destination side by linear
 // operator reordering (Section "Linear Operator Reordering"):
-//   a_e,i = (K_s,i Watt[r,i]) . Q_t,i  =  K_s,i . (Watt[r,i] Q_t,i^T)
+//   a_e,i = (K_s,i Watt[r,i]) . Q_t,i  =  K_s,i . (Q_t,i Watt[r,i]^T)
 //   sum_e alpha_e,i (V_s,i Wmsg[r,i])  =  (sum_e alpha_e,i V_s,i) Wmsg[r,i]
-// so Watt is applied once per (destination, relation) segment to the query,
-// and Wmsg once per segment to the attention-weighted value sum, instead of
-// once per edge.  The per-relation matrices are staged in LDS, shared by a
-// 1024-thread workgroup, when they fit.
+// The reordered query of every (destination, relation) segment, with the
+// prior mu[r] and the attention scale folded in, is one typed GEMM over the
+// segments (weights built by hgt_qp_weights_kernel); the traversal then only
+// dots each key row with its segment's query row.  Wmsg is applied once per
+// segment to the attention-weighted value sum, from LDS (shared by a
+// 1024-thread workgroup) when it fits.
 //
 // Work items are those of the RGAT traversal (at most kChunkEdges edges: a
 // bundle of small destinations or a piece of a large one), one per group of
 // 16 lanes; lane l holds features 4l..4l+3, so head i is lanes
 // [i*LH, (i+1)*LH) with LH = d_k / 4.  Each item first stages its edge
 // sources and segment / destination boundaries in LDS, then streams the
-// K|V rows of its edges, with their destinations' query rows, kU at a time
-// with the next kU in flight.
+// K|V rows of its edges, with their segments' query rows (L1 hits after a
+// segment's first edge), kU at a time with the next kU in flight.
 #include "rgnn_internal.h"
 #include "wave_ops.h"
 
@@ -43,10 +45,9 @@ constexpr int kBlock = 1024, GPB = kBlock / G;
 
 struct HStage {
     int eidx[kE];          // source node of each edge
-    int edst[kE];          // destination node of each edge
+    int evs[kE];           // item-local virtual segment of each edge
     int vptr[kE + 1];      // item-local edge offset of each virtual segment
     int vrel[kE];
-    float vmu[kE];         // mu[rel] * att_scale of each virtual segment
     int dptr[kDst + 1];    // item-local edge offset of each destination
 };
 
@@ -54,8 +55,7 @@ struct HK {
     int64_t n_items;
     const Item *items;
     const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *in_src;
-    const float *KV, *Q, *Watt, *Wmsg, *mu;
-    float scale;
+    const float *KV, *QP, *Wmsg;
     int R;
     float *agg, *partial;
 };
@@ -92,27 +92,6 @@ __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
     return y;
 }
 
-// y[k] = sum_j Mat[k][j] x[j]  (x . Mat^T), same distribution as above.
-template <int LH>
-__device__ __forceinline__ float4 head_matvec_t(float4 x, const float *Mt, int gl)
-{
-    constexpr int DK = LH * 4;
-    const int base = (gl / LH) * LH;
-    const int c0 = 4 * (gl % LH);
-    float4 y = zero4();
-#pragma unroll
-    for (int jj = 0; jj < LH; ++jj) {
-        const float4 xj = make_float4(head_bcast<LH>(x.x, jj, base), head_bcast<LH>(x.y, jj, base),
-                                      head_bcast<LH>(x.z, jj, base), head_bcast<LH>(x.w, jj, base));
-        y.x += dot4(ld4(Mt + (c0 + 0) * DK + 4 * jj), xj);
-        y.y += dot4(ld4(Mt + (c0 + 1) * DK + 4 * jj), xj);
-        y.z += dot4(ld4(Mt + (c0 + 2) * DK + 4 * jj), xj);
-        y.w += dot4(ld4(Mt + (c0 + 3) * DK + 4 * jj), xj);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    return y;
-}
-
 template <int H, bool LDSW>
 __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
 {
@@ -120,17 +99,13 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
     constexpr int MAT = H * DK * DK;            // floats per relation per matrix
     extern __shared__ float4 smem4[];
     float *smem = reinterpret_cast<float *>(smem4);
-    const int nW = LDSW ? 2 * k.R * MAT : 0;
+    const int nW = LDSW ? k.R * MAT : 0;
     HStage *stages = reinterpret_cast<HStage *>(smem + nW);
-    const float *Watt = k.Watt, *Wmsg = k.Wmsg;
+    const float *Wmsg = k.Wmsg;
     if (LDSW) {
         const int n4 = k.R * MAT / 4;
-        for (int i = threadIdx.x; i < n4; i += kBlock) {
-            smem4[i] = reinterpret_cast<const float4 *>(k.Watt)[i];
-            smem4[n4 + i] = reinterpret_cast<const float4 *>(k.Wmsg)[i];
-        }
-        Watt = smem;
-        Wmsg = smem + k.R * MAT;
+        for (int i = threadIdx.x; i < n4; i += kBlock) smem4[i] = reinterpret_cast<const float4 *>(k.Wmsg)[i];
+        Wmsg = smem;
     }
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     HStage &st = stages[gi];
@@ -143,10 +118,10 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
         e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
         slot = k.item_slot[item];
         for (int j = gl; j < nv; j += G) {
-            st.vptr[j] = k.vseg_ptr[vs0 + j] - e0;
-            const int r = k.vseg_rel[vs0 + j];
-            st.vrel[j] = r;
-            st.vmu[j] = k.mu[r] * k.scale;
+            const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
+            st.vptr[j] = a;
+            st.vrel[j] = k.vseg_rel[vs0 + j];
+            for (int e = a; e < b; ++e) st.evs[e] = j;
         }
         if (gl == 0) st.vptr[nv] = ne;
         auto dst_edge = [&](int jj) {
@@ -154,11 +129,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
             vs = vs < vs0 ? vs0 : (vs > vs0 + nv ? vs0 + nv : vs);
             return k.vseg_ptr[vs] - e0;
         };
-        for (int j = gl; j < nd; j += G) {
-            const int ea = dst_edge(j), eb = dst_edge(j + 1);
-            st.dptr[j] = ea;
-            for (int e = ea; e < eb; ++e) st.edst[e] = dst0 + j;
-        }
+        for (int j = gl; j < nd; j += G) st.dptr[j] = dst_edge(j);
         if (gl == 0) st.dptr[nd] = ne;
         for (int e = gl; e < ne; e += G) st.eidx[e] = k.in_src[e0 + e];
     }
@@ -167,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
 
     const int head = gl / LH;
     float m = -INFINITY, s = 0.f;
-    float4 agg = zero4(), vacc = zero4(), qp = zero4();
+    float4 agg = zero4(), vacc = zero4();
     auto flush = [&](int jj) {
         if (slot < 0) {
             st4(k.agg + (size_t)(dst0 + jj) * D + gl * 4, scale4(agg, s > 0.f ? 1.f / s : 0.f));
@@ -178,18 +149,12 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
         }
         m = -INFINITY; s = 0.f; agg = zero4();
     };
-    auto start_vseg = [&](int jv, float4 q) {
-        const size_t off = (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK;
-        qp = scale4(head_matvec_t<LH>(q, Watt + off, gl), st.vmu[jv]);
-        vacc = zero4();
-    };
     int j = 0, jv = 0;
     while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush(j); ++j; }
     if (ne > 0) {
         // Ping-pong batches: batch A is consumed while batch B is in flight.
-        // Each edge brings its K|V row and its destination's query row (the
-        // latter a cache hit after the destination's first edge); a segment is
-        // started from the query row of its first edge.
+        // Each edge brings its K|V row and its segment's reordered query row
+        // (a cache hit after the segment's first edge).
         float4 Ak[kU], Av[kU], Aq[kU], Bk[kU], Bv[kU], Bq[kU];
         auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], float4 (&Xq)[kU], int base) {
 #pragma unroll
@@ -198,7 +163,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
                 const size_t row = (size_t)st.eidx[e] * (2 * D);
                 Xk[u] = ld4(k.KV + row + gl * 4);
                 Xv[u] = ld4(k.KV + row + D + gl * 4);
-                Xq[u] = ld4(k.Q + (size_t)st.edst[e] * D + gl * 4);
+                Xq[u] = ld4(k.QP + (size_t)(vs0 + st.evs[e]) * D + gl * 4);
             }
         };
         auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
@@ -207,8 +172,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
                 if (e < ne) {
-                    if (e == st.vptr[jv]) start_vseg(jv, Xq[u]);
-                    const float a = gsum<LH>(dot4(Xk[u], qp));
+                    const float a = gsum<LH>(dot4(Xk[u], Xq[u]));
                     const float mn = fmaxf(m, a);
                     const float c1 = __expf(m - mn), c2 = __expf(a - mn);
                     s = s * c1 + c2;
@@ -218,6 +182,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
                     if (e + 1 == st.vptr[jv + 1]) {
                         const size_t off = (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK;
                         agg = add4(agg, head_vecmat<LH>(vacc, Wmsg + off, gl));
+                        vacc = zero4();
                         ++jv;
                         if (e + 1 == st.dptr[j + 1]) {
                             flush(j);
@@ -247,7 +212,22 @@ size_t stage_bytes() { return (size_t)GPB * sizeof(HStage); }
 size_t weight_bytes(int R, int heads)
 {
     const int dk = D / heads;
-    return (size_t)2 * R * heads * dk * dk * sizeof(float);
+    return (size_t)R * heads * dk * dk * sizeof(float);
+}
+
+// Wqp[r][j][n] = mu[r] * scale * Watt[r, i][n - i dk][j - i dk] when j and n
+// both fall in head i's columns, else 0.
+__global__ void hgt_qp_weights_kernel(const float *Watt, const float *mu, float scale, int R, int heads,
+                                      float *Wqp)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)R * D * D) return;
+    const int r = (int)(idx / (D * D)), j = (int)(idx / D % D), n = (int)(idx % D);
+    const int dk = D / heads, i = j / dk;
+    float v = 0.f;
+    if (n / dk == i)
+        v = mu[r] * scale * Watt[(((size_t)r * heads + i) * dk + (n - i * dk)) * dk + (j - i * dk)];
+    Wqp[idx] = v;
 }
 
 }  // namespace
@@ -261,8 +241,8 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
     k.vseg_rel = g->dev.vseg_rel; k.in_src = g->dev.in_src;
-    k.KV = a.KV; k.Q = a.Q; k.Watt = a.Watt; k.Wmsg = a.Wmsg; k.mu = a.mu;
-    k.scale = a.scale; k.R = g->R; k.agg = a.agg; k.partial = a.partial;
+    k.KV = a.KV; k.QP = a.QP; k.Wmsg = a.Wmsg;
+    k.R = g->R; k.agg = a.agg; k.partial = a.partial;
     const size_t wb = weight_bytes(g->R, a.heads);
     const bool use_lds = wb + stage_bytes() <= 160 * 1024;
     const size_t lds = stage_bytes() + (use_lds ? wb : 0);
@@ -291,6 +271,18 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute (HGT LDS)");
     e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt traversal launch");
+}
+
+rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
+                                  int heads, float *Wqp, hipStream_t s)
+{
+    if (d != D) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 64");
+    const int64_t n = (int64_t)R * D * D;
+    LaunchScope ls("hgt_qp_weights", s);
+    hipLaunchKernelGGL(hgt_qp_weights_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, Watt, mu, scale,
+                       R, heads, Wqp);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt_qp_weights launch");
 }
 
 }  // namespace rgnn

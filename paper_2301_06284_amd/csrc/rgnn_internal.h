@@ -193,15 +193,18 @@ rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
 struct HgtArgs {
     const rgnn_graph *g = nullptr;
     const float *KV = nullptr;     // [N, 2d]: K then V per node
-    const float *Q = nullptr;      // [N, d]
-    const float *Watt = nullptr, *Wmsg = nullptr, *mu = nullptr;
-    float scale = 0.25f;
+    const float *QP = nullptr;     // [V, d]: mu[r] * scale * Q_t Watt[r]^T per virtual segment
+    const float *Wmsg = nullptr;
     int heads = 4;
     int d = 64;
     float *agg = nullptr;          // [N, d]
     float *partial = nullptr;      // [slots, 2*heads + d]
 };
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
+// Wqp[r] (d x d) = mu[r] * scale * blockdiag over heads i of Watt[r, i]^T, so
+// that Q_t Wqp[r] is the reordered query of segment (t, r).
+rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
+                                  int heads, float *Wqp, hipStream_t s);
 
 // RGAT backward (backward.hip).  With need != NULL only stores the workspace
 // bytes the call needs.
