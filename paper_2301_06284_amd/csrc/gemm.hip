@@ -82,30 +82,29 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
     const int lane = tid & 63, wave = tid >> 6;
     const int li = lane & 15, q = lane >> 4;
 
-    // ---- stage W[type] transposed into LDS: Wt[n][k] = B[k][n] (float4 reads) ----
+    // Prologue, ordered so that its three latencies overlap: the weight tile
+    // W[type] is fetched into registers, then the row indices, then the first
+    // PF row blocks; W is written to LDS (transposed: Wt[n][k] = B[k][n]) only
+    // after all of them are in flight.
+    constexpr int NW = K * NC / 4 / 256;    // float4 of W per thread
+    static_assert(NW * 256 * 4 == K * NC, "weight tile must split evenly over the workgroup");
+    float4 wv[NW];
     {
         const int NP = NC / a.nparts;
-        for (int idx = tid; idx < K * NC / 4; idx += 256) {
-            if (a.trans_b) {               // stored [types][NC][K]: copy rows
+#pragma unroll
+        for (int t = 0; t < NW; ++t) {
+            const int idx = tid + 256 * t;
+            if (a.trans_b) {               // stored [types][NC][K]: rows of W^T
                 const int n = idx / (K / 4), k4 = (idx % (K / 4)) * 4;
-                const float4 w = *reinterpret_cast<const float4 *>(a.W0 + ((size_t)tile.type * NC + n) * K + k4);
-                *reinterpret_cast<float4 *>(&Wt[n * KP + k4]) = w;
+                wv[t] = *reinterpret_cast<const float4 *>(a.W0 + ((size_t)tile.type * NC + n) * K + k4);
             } else {                       // stored [types][K][NP] per part
                 const int k = idx / (NC / 4), n4 = (idx % (NC / 4)) * 4;
                 const int part = n4 / NP, nn = n4 % NP;
                 const float *Wp = part == 0 ? a.W0 : (part == 1 ? a.W1 : a.W2);
-                const float4 w = *reinterpret_cast<const float4 *>(Wp + ((size_t)tile.type * K + k) * NP + nn);
-                Wt[(n4 + 0) * KP + k] = w.x;
-                Wt[(n4 + 1) * KP + k] = w.y;
-                Wt[(n4 + 2) * KP + k] = w.z;
-                Wt[(n4 + 3) * KP + k] = w.w;
+                wv[t] = *reinterpret_cast<const float4 *>(Wp + ((size_t)tile.type * K + k) * NP + nn);
             }
         }
-        if (EP & EP_DOT)
-            for (int n = tid; n < NC; n += 256) dvs[n] = a.dot_vec[(size_t)tile.type * NC + n];
     }
-    __syncthreads();
-
     // Row blocks of this wave: rb = wave + 4 i, i < MB.  Lane (li, q) owns row
     // 16 rb + li of the block and, per column block cb, columns 16 cb + 4q .. +3.
     const int nrb = (tile.rows + 15) >> 4;
@@ -133,6 +132,26 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
     };
 #pragma unroll
     for (int i = 0; i < PF && i < MB; ++i) load_block(i);
+    {
+#pragma unroll
+        for (int t = 0; t < NW; ++t) {
+            const int idx = tid + 256 * t;
+            if (a.trans_b) {
+                const int n = idx / (K / 4), k4 = (idx % (K / 4)) * 4;
+                *reinterpret_cast<float4 *>(&Wt[n * KP + k4]) = wv[t];
+            } else {
+                const int k = idx / (NC / 4), n4 = (idx % (NC / 4)) * 4;
+                Wt[(n4 + 0) * KP + k] = wv[t].x;
+                Wt[(n4 + 1) * KP + k] = wv[t].y;
+                Wt[(n4 + 2) * KP + k] = wv[t].z;
+                Wt[(n4 + 3) * KP + k] = wv[t].w;
+            }
+        }
+        if (EP & EP_DOT)
+            for (int n = tid; n < NC; n += 256) dvs[n] = a.dot_vec[(size_t)tile.type * NC + n];
+    }
+    __syncthreads();   // W staged; the first row blocks are already in flight
+
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int rb = wave + 4 * i;
