@@ -135,6 +135,22 @@ def test_hgt_small(kind, heads):
     assert row_err(got, ref) <= TOL
 
 
+@pytest.mark.parametrize("heads,R", [(2, 12), (4, 24)])
+def test_hgt_many_relations(heads, R):
+    """Enough relations that the per-relation message matrices no longer fit
+    in LDS beside the staged items (the traversal reads them from memory)."""
+    g = graph("random", T=3, R=R, E=5000)
+    t = workloads.tiny_tensors(4, g, 64, 64, heads=heads)
+    scale = 1.0 / np.sqrt(64 // heads)
+    print(f"hgt heads={heads} R={R}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt(heads, scale)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=heads, att_scale=scale)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
 @pytest.mark.parametrize("flags", [0, 2, 4])
 def test_hgt_flags(flags):
     g = graph("hub", T=2, R=3)
