@@ -74,17 +74,21 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def time_steps(torch, fn, steps, warmup):
+def time_steps(torch, fn, steps, warmup, per_step=False):
+    """Mean ms per step over `steps` timed steps (events on the current stream,
+    which the library launches on); with per_step, also the list of step times."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
         fn()
-    b.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return a.elapsed_time(b) / steps
+    each = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    mean = ev[0].elapsed_time(ev[steps]) / steps
+    return (mean, each) if per_step else mean
 
 
 def kernel_profile(rgnn, torch, fn, steps):
@@ -220,11 +224,11 @@ def main():
         fn = (lambda ws=ws, p=p: rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"],
                                                    c.T["w_dst"], out, saved, ws, d, d, H, 0.2,
                                                    0, p))
-        ms = time_steps(torch, fn, K, W)
+        ms, each = time_steps(torch, fn, K, W, per_step=True)
         kern = kernel_profile(rgnn, torch, fn, max(3, K // 2))
-        plans[p] = (ms, kern, fn)
+        plans[p] = (ms, kern, fn, each)
         del ws
-    ms, kern, fn = plans[plan]
+    ms, kern, fn, each = plans[plan]
     model = rgat_tf_model(inf, d, H) if plan == rgnn.PLAN_TRANSFORM_FIRST else rgat_af_model(inf, d)
     kname, kms, kgbs, ktfl, km = roofline_of(kern, model)
     E = inf["num_edges"]
@@ -247,6 +251,22 @@ def main():
     log("cpu baseline")
     cpu = None if args.no_cpu else cpu_baseline(c, args.cpu_seconds)
     line_kernels = {k: {"launches_per_step": n, "mean_ms": round(m, 4)} for k, (n, m) in kern.items()}
+    # every modelled kernel of the headline: algorithmic and counter GB/s against
+    # the HBM peak, and the GEMM's MFMA utilisation against the fp32 dense peak
+    for k, m in model.items():
+        if k not in kern:
+            continue
+        kms_k = kern[k][1]
+        ent = line_kernels[k]
+        ent["model_bytes"] = m["bytes"]
+        ent["model_gbs"] = round(m["bytes"] / (kms_k * 1e-3) / 1e9, 1)
+        ent["model_frac"] = round(ent["model_gbs"] / HBM_PEAK_GBS, 4)
+        tr = counter_traffic("rgat_am_like_880k", k)
+        ent["counter_bytes"] = tr
+        ent["counter_gbs"] = None if tr is None else round(tr / (kms_k * 1e-3) / 1e9, 1)
+        if k == "typed_gemm":
+            ent["mfma_tflops"] = round(m["flops"] / (kms_k * 1e-3) / 1e12, 2)
+            ent["mfma_frac"] = round(ent["mfma_tflops"] / FP32_PEAK_TFLOPS, 4)
     c.close()
     del out, saved
 
@@ -329,6 +349,7 @@ def main():
         "steps": K,
         "warmup": W,
         "ms_per_step": ms,
+        "ms_median": float(np.median(each)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
