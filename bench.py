@@ -111,17 +111,21 @@ def rgat_tf_model(info, d, H):
     Gathered rows count once per edge, node rows once per node, index arrays once."""
     E, N, U, V = info["num_edges"], info["num_nodes"], info["num_src_pairs"], info["num_vsegs"]
     R, I = info["num_rels"], info["num_items"]
+    # With one head the traversal forms the source term from the gathered
+    # message row (a dot with w_src); with several the GEMM writes it per pair
+    # and the traversal gathers it per edge.
+    st = 0 if H == 1 else 4 * H
     return {
-        # per pair: gather index, h row read, message row write, attention scalar write;
+        # per pair: gather index, h row read, message row write (+ source terms);
         # W_r and w_src once per relation
-        "typed_gemm": dict(bytes=U * (4 + 4 * d + 4 * d + 4 * H) + R * (4 * d * d + 4 * d),
-                           flops=2.0 * U * d * d + 2.0 * U * d),
-        # per edge: pair index, message row, attention scalar; per destination:
-        # h_v row, output row, (max, sum); per segment: offset and relation;
-        # per item: descriptor and slot; reordered vectors once
-        "rgat_traverse_tf": dict(bytes=E * (4 + 4 * d + 4 * H) + N * (4 * d + 4 * d + 8 * H + 4)
-                                 + V * 8 + I * 20 + R * H * d * 4,
-                                 flops=E * (2.0 * d + 10)),
+        "typed_gemm": dict(bytes=U * (4 + 4 * d + 4 * d + st) + R * (4 * d * d + 4 * d),
+                           flops=2.0 * U * d * d + (2.0 * U * d if H > 1 else 0.0)),
+        # per edge: pair index, message row (+ source term); per destination:
+        # h_v row, output row, (max, sum); per segment: offset, relation and
+        # destination term; per item: descriptor and slot; w_src once
+        "rgat_traverse_tf": dict(bytes=E * (4 + 4 * d + st) + N * (4 * d + 4 * d + 8 * H + 4)
+                                 + V * 12 + I * 20 + R * H * d * 4,
+                                 flops=E * (2.0 * d + 10) + (E * 2.0 * d if H == 1 else 0.0)),
     }
 
 

@@ -401,10 +401,13 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
         ga.Y = w.M; ga.ldy = d_out;
-        ga.ep.dot_vec = w_src; ga.ep.dot_out = w.atts; ga.ep.dot_heads = heads;
+        // with several heads the GEMM also emits the per-pair source terms; one
+        // head forms them in the traversal from the gathered message row
+        if (heads > 1) { ga.ep.dot_vec = w_src; ga.ep.dot_out = w.atts; ga.ep.dot_heads = heads; }
         if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         TravArgs ta;
         ta.g = g; ta.h = h; ta.M = w.M; ta.atts = w.atts; ta.wtp = w.wtp; ta.vatt = w.vatt;
+        if (heads == 1) ta.wsp = w_src;
         ta.slope = neg_slope; ta.heads = heads; ta.d = d_out;
         ta.out = out; ta.saved = saved; ta.partial = w.partial;
         if ((st = launch_rgat_traverse_tf(ta, s)) != RGNN_OK) return st;

@@ -300,6 +300,84 @@ __global__ __launch_bounds__(256) void rgat_tf_kernel(TK k)
     aggregate_item<D, H, true>(k, it, st, k.M, gl, head, pm, ps);
 }
 
+// ---------------------------------------------------------------- RGAT, transform-first, one head
+// One pass per item with an online softmax: the source term M[p] . w_src[r] is
+// formed from the gathered message row itself, so neither a per-pair source
+// term (a 4-byte random gather per edge) nor a logit staging pass is needed.
+// The running maximum, denominator and weighted row sum of the current
+// destination are rescaled as the maximum grows; a destination's result is
+// written when its last edge is consumed.  k.wsp holds w_src [R, D].
+template <int D>
+__global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
+{
+    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int kU = 4;   // each entry carries two rows: half the batch of the other traversals
+    __shared__ Stage<1> stage[GPB];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    Stage<1> &st = stage[gi];
+    const ItemHdr it = item_header(k, (int64_t)blockIdx.x * GPB + gi);
+    stage_item<G, 1, 0>(k, it, st, k.e2u, gl);
+    __syncthreads();
+    if (!it.valid) return;
+    int j = 0;
+    float m = -INFINITY, s = 0.f;
+    float4 acc = zero4();
+    auto flush = [&](int jj) {
+        const size_t v = (size_t)it.dst0 + jj;
+        if (it.slot < 0) {
+            st4(k.out + v * D + gl * 4, scale4(acc, s > 0.f ? 1.f / s : 0.f));
+            if (k.saved && gl == 0) {
+                k.saved[v * 2] = s > 0.f ? m : 0.f;
+                k.saved[v * 2 + 1] = s;
+            }
+        } else {
+            float *pr = k.partial + (size_t)it.slot * (2 + D);
+            if (gl == 0) { pr[0] = m; pr[1] = s; }
+            st4(pr + 2 + gl * 4, acc);
+        }
+        m = -INFINITY; s = 0.f; acc = zero4();
+    };
+    if (it.ne > 0) {
+        // ping-pong batches of (message row, w_src row) per edge
+        float4 A[kU], Aw[kU], B[kU], Bw[kU];
+        auto load = [&](float4 (&X)[kU], float4 (&Xw)[kU], int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u < it.ne ? base + u : it.ne - 1;
+                X[u] = ld4(k.M + (size_t)st.eidx[e] * D + gl * 4);
+                Xw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
+            }
+        };
+        auto consume = [&](const float4 (&X)[kU], const float4 (&Xw)[kU], int base) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int e = base + u;
+                const float src_term = gsum<G>(dot4(X[u], Xw[u]));
+                if (e < it.ne) {
+                    while (e >= st.dptr[j + 1]) { flush(j); ++j; }
+                    const float z = leaky(src_term + st.vw[st.evs[e]], k.slope);
+                    const float mn = fmaxf(m, z);
+                    const float c1 = __expf(m - mn), c2 = __expf(z - mn);
+                    s = s * c1 + c2;
+                    acc = lin4(acc, c1, X[u], c2);
+                    m = mn;
+                }
+            }
+        };
+        load(A, Aw, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
+            load(B, Bw, e0 + kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(A, Aw, e0);
+            load(A, Aw, e0 + 2 * kU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(B, Bw, e0 + kU);
+        }
+    }
+    for (; j < it.nd; ++j) flush(j);
+}
+
 // ---------------------------------------------------------------- RGCN, transform-first
 template <int D>
 __global__ __launch_bounds__(256) void rgcn_tf_kernel(TK k)
@@ -462,7 +540,12 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     LaunchScope ls("rgat_traverse_tf", s);
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
 #define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
-    if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
+    if (a.heads == 1 && a.wsp) {   // single pass, source term from the message row
+        if (a.d == 64) hipLaunchKernelGGL((rgat_tf1_kernel<64>), dim3(nb), dim3(256), 0, s, k);
+        else if (a.d == 128) hipLaunchKernelGGL((rgat_tf1_kernel<128>), dim3(nb), dim3(256), 0, s, k);
+        else return fail(RGNN_EUNSUPPORTED, "RGAT traversal: unsupported d");
+    }
+    else if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
     else if (a.d == 64 && a.heads == 2) RGAT_TF(64, 2);
     else if (a.d == 64 && a.heads == 4) RGAT_TF(64, 4);
     else if (a.d == 128 && a.heads == 1) RGAT_TF(128, 1);
