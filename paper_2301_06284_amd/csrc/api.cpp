@@ -471,7 +471,7 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     gq.X = w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
     gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
     gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
-    gq.Y = w.QP; gq.ldy = d;
+    gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = heads;
     if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
     HgtArgs ha;
     ha.g = g; ha.KV = w.KV; ha.QP = w.QP; ha.Wmsg = Wmsg;

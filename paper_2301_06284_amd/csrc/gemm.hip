@@ -49,7 +49,8 @@ enum : int {
     EP_RESID = 4,    // Y[row] += residual[row]
     EP_ACC = 8,      // Y[row] += old Y[row]
     EP_RELU = 16,    // max(0, .) last
-    EP_SPLIT = 32    // columns >= split go to Y2
+    EP_SPLIT = 32,   // columns >= split go to Y2
+    EP_BDIAG = 64    // W[type] is block-diagonal in DH blocks: off-diagonal products skipped
 };
 
 struct GemmK {
@@ -73,7 +74,8 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
     constexpr int NCB = NC / 16;        // 16-column blocks
     constexpr int KC = K / 16;          // 16-wide k chunks (4 MFMA steps each)
     constexpr int MB = kGemmTileRows / 64;
-    constexpr int CBH = NCB / DH;       // column blocks per dot-product head
+    constexpr int CBH = NCB / DH;       // column blocks per dot-product head / diagonal block
+    constexpr int KCH = KC / DH;        // k chunks per diagonal block
     __shared__ float Wt[NC * KP];
     __shared__ float dvs[(EP & EP_DOT) ? NC : 1];
 
@@ -188,24 +190,27 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
         asm volatile("" ::: "memory");
+        // with EP_BDIAG only the k chunks of a column block's own diagonal
+        // block contribute (a compile-time test after unrolling)
+        auto live = [](int c, int cb) { return !(EP & EP_BDIAG) || c / KCH == cb / CBH; };
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
             float4 b[NCB];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                b[cb] = *reinterpret_cast<const float4 *>(&Wt[(cb * 16 + li) * KP + c * 16 + q * 4]);
+                if (live(c, cb)) b[cb] = *reinterpret_cast<const float4 *>(&Wt[(cb * 16 + li) * KP + c * 16 + q * 4]);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].x, acur[c].x, acc[cb], 0, 0, 0);
+                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].x, acur[c].x, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].y, acur[c].y, acc[cb], 0, 0, 0);
+                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].y, acur[c].y, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].z, acur[c].z, acc[cb], 0, 0, 0);
+                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].z, acur[c].z, acc[cb], 0, 0, 0);
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].w, acur[c].w, acc[cb], 0, 0, 0);
+                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].w, acur[c].w, acc[cb], 0, 0, 0);
         }
         // (d) epilogue
         float4 o[NCB];
@@ -271,6 +276,13 @@ bool dispatch_square(int ep, int heads, const GemmK &k, int64_t n, hipStream_t s
     case EP_ACC: launch_k<K, NC, EP_ACC>(k, n, s); return true;
     case EP_ACC | EP_RELU: launch_k<K, NC, EP_ACC | EP_RELU>(k, n, s); return true;
     case EP_RESID: launch_k<K, NC, EP_RESID>(k, n, s); return true;
+    case EP_BDIAG:
+        switch (heads) {
+        case 1: launch_k<K, NC, 0>(k, n, s); return true;
+        case 2: launch_k<K, NC, EP_BDIAG, 2>(k, n, s); return true;
+        case 4: launch_k<K, NC, EP_BDIAG, 4>(k, n, s); return true;
+        default: return false;
+        }
     default: return false;
     }
 }
@@ -306,12 +318,16 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
         return fail(RGNN_EUNSUPPORTED, "dot-product heads must own whole 16-column blocks");
     const int ep = (a.ep.dot_out ? EP_DOT : 0) | (a.ep.row_scale ? EP_SCALE : 0) |
                    (a.ep.residual ? EP_RESID : 0) | (a.ep.accumulate ? EP_ACC : 0) |
-                   (a.ep.relu ? EP_RELU : 0) | (a.ep.Y2 ? EP_SPLIT : 0);
+                   (a.ep.relu ? EP_RELU : 0) | (a.ep.Y2 ? EP_SPLIT : 0) |
+                   (a.ep.diag_blocks > 1 ? EP_BDIAG : 0);
+    if ((ep & EP_BDIAG) && ep != EP_BDIAG)
+        return fail(RGNN_EUNSUPPORTED, "block-diagonal weights take no epilogue");
+    const int heads = (ep & EP_BDIAG) ? a.ep.diag_blocks : a.ep.dot_heads;
     bool ok = false;
     {
         LaunchScope ls("typed_gemm", s);
-        if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, a.ep.dot_heads, k, a.ntiles, s);
-        else if (a.K == 128 && a.Nc == 128) ok = dispatch_square<128, 128>(ep, a.ep.dot_heads, k, a.ntiles, s);
+        if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, heads, k, a.ntiles, s);
+        else if (a.K == 128 && a.Nc == 128) ok = dispatch_square<128, 128>(ep, heads, k, a.ntiles, s);
         else if (a.K == 64 && a.Nc == 128) ok = dispatch_rect<64, 128>(ep, k, a.ntiles, s);
         else if (a.K == 128 && a.Nc == 64) ok = dispatch_rect<128, 64>(ep, k, a.ntiles, s);
         else if (a.K == 64 && a.Nc == 192 && ep == EP_SPLIT) {

@@ -134,6 +134,9 @@ struct GemmEpilogue {
     float *Y2 = nullptr;
     int64_t ldy2 = 0;
     int split = 0;
+    // W[type] is block-diagonal with this many equal blocks (> 1: the
+    // off-diagonal products are skipped; no other epilogue may be set).
+    int diag_blocks = 1;
 };
 
 struct GemmArgs {
