@@ -492,33 +492,59 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
                                                          float *yvec)
 {
     constexpr int KB = 64, P = 68;
+    constexpr int SL = KB * 16 / 256;   // float4 slots of each operand per thread and step
     __shared__ float As[KB * P];
     __shared__ float Bs[KB * P];
     __shared__ float4 yred[256];
     const Tile t = chunks[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int li = lane & 15, q = lane >> 4;
+    const int c4 = (tid & 15) * 4;      // this thread's columns in every slot
     floatx4 acc[4];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float4 yacc = zero4();   // columns (tid & 15) * 4 .. + 3
+    float4 yacc = zero4();
+    // Software pipeline over the chunk's 64-row steps: destination indices two
+    // steps ahead, rows one step ahead (registers), MFMAs on the LDS copy of
+    // the current step.  Rows past the chunk end are clamped to its last row
+    // and masked when written to LDS.
+    auto row_of = [&](int k0, int sl) {
+        const int rr = (tid >> 4) + 16 * sl;
+        return t.row0 + min(k0 + rr, t.rows - 1);
+    };
+    int vi[SL], vn[SL];
+    float4 ra[SL], rb[SL], rh[SL];
+    float ry[SL];
+    auto load_idx = [&](int k0, int (&v)[SL]) {
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) v[sl] = vsegdst_byrel[row_of(k0, sl)];
+    };
+    auto load_rows = [&](int k0, const int (&v)[SL]) {
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+            const int row = row_of(k0, sl);
+            ra[sl] = ld4(Sa + (size_t)row * D + c4);
+            rb[sl] = ld4(Gm + (size_t)v[sl] * D + c4);
+            rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
+            ry[sl] = ysum[row];
+        }
+    };
+    load_idx(0, vi);
+    load_rows(0, vi);
+    load_idx(KB, vn);
     for (int k0 = 0; k0 < t.rows; k0 += KB) {
-        __syncthreads();
-        // 64 rows x 64 floats of each operand: 16 float4 per row, 1024 float4 per operand
-        for (int idx = tid; idx < KB * 16; idx += 256) {
-            const int rr = idx >> 4, c4 = (idx & 15) * 4;
-            float4 a = zero4(), b = a;
-            if (k0 + rr < t.rows) {
-                const int row = t.row0 + k0 + rr;
-                const int v = vsegdst_byrel[row];
-                a = ld4(Sa + (size_t)row * D + c4);
-                b = ld4(Gm + (size_t)v * D + c4);
-                yacc = lin4(yacc, 1.f, ld4(h + (size_t)v * D + c4), ysum[row]);
-            }
-            *reinterpret_cast<float4 *>(&As[rr * P + c4]) = a;
-            *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = b;
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+            const int rr = (tid >> 4) + 16 * sl;
+            const bool ok = k0 + rr < t.rows;
+            *reinterpret_cast<float4 *>(&As[rr * P + c4]) = ok ? ra[sl] : zero4();
+            *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = ok ? rb[sl] : zero4();
+            if (ok) yacc = lin4(yacc, 1.f, rh[sl], ry[sl]);
         }
         __syncthreads();
+        load_rows(k0 + KB, vn);
+        load_idx(k0 + 2 * KB, vn);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll 4
         for (int kk = 0; kk < KB; kk += 4) {
             const float a = As[(kk + q) * P + w * 16 + li];
@@ -526,6 +552,7 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
             for (int cb = 0; cb < 4; ++cb)
                 acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bs[(kk + q) * P + cb * 16 + li], acc[cb], 0, 0, 0);
         }
+        __syncthreads();
     }
     float *out = partial + (size_t)blockIdx.x * D * D;
 #pragma unroll
