@@ -242,32 +242,53 @@ __device__ __forceinline__ void aggregate_item(const TK &k, const ItemHdr &it, c
 // out of the edge loop to one evaluation per (dst, rel) segment.
 // One group of D/4 lanes per kSegPerGroup consecutive segments, all loads of
 // a group issued together.
-constexpr int kSegPerGroup = 4;
+constexpr int kSegPerGroup = 8;
 
 template <int D, int H>
 __global__ __launch_bounds__(256) void seg_attn_kernel(TK k, int64_t V, const int32_t *vseg_dst)
 {
     constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int S = kSegPerGroup;
     const int gl = threadIdx.x % G;
-    const int64_t vs0 = ((int64_t)blockIdx.x * GPB + threadIdx.x / G) * kSegPerGroup;
+    const int64_t vs0 = ((int64_t)blockIdx.x * GPB + threadIdx.x / G) * S;
     if (vs0 >= V) return;
-    int v[kSegPerGroup], r[kSegPerGroup];
+    int v[S], r[S];
 #pragma unroll
-    for (int i = 0; i < kSegPerGroup; ++i) {
+    for (int i = 0; i < S; ++i) {
         const int64_t vs = vs0 + i < V ? vs0 + i : V - 1;
         v[i] = vseg_dst[vs];
         r[i] = k.vseg_rel[vs];
     }
-    float4 hv[kSegPerGroup];
+    // consecutive segments mostly share their destination: its row is loaded
+    // once and reused
+    float4 hv[S];
+    hv[0] = ld4(k.h + (size_t)v[0] * D + gl * 4);
 #pragma unroll
-    for (int i = 0; i < kSegPerGroup; ++i) hv[i] = ld4(k.h + (size_t)v[i] * D + gl * 4);
+    for (int i = 1; i < S; ++i)
+        hv[i] = v[i] == v[i - 1] ? hv[i - 1] : ld4(k.h + (size_t)v[i] * D + gl * 4);
+    float4 wt[S][H];
 #pragma unroll
-    for (int i = 0; i < kSegPerGroup; ++i) {
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+        for (int hh = 0; hh < H; ++hh) wt[i][hh] = ld4(k.wtp + ((size_t)r[i] * H + hh) * D + gl * 4);
+    // every lane ends with all S * H terms; lane l keeps terms l, l + G, ... and
+    // stores them (coalesced: the group's terms are contiguous in vatt)
+    constexpr int NM = (S * H + G - 1) / G;
+    float mine[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) mine[m] = 0.f;
+#pragma unroll
+    for (int i = 0; i < S; ++i)
 #pragma unroll
         for (int hh = 0; hh < H; ++hh) {
-            const float p = gsum<G>(dot4(hv[i], ld4(k.wtp + ((size_t)r[i] * H + hh) * D + gl * 4)));
-            if (gl == 0 && vs0 + i < V) k.vatt[(size_t)(vs0 + i) * H + hh] = p;
+            const float p = gsum<G>(dot4(hv[i], wt[i][hh]));
+            const int t = i * H + hh;
+            if (gl == t % G) mine[t / G] = p;
         }
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+        const int t = m * G + gl;
+        if (t < S * H && vs0 * H + t < V * H) k.vatt[(size_t)vs0 * H + t] = mine[m];
     }
 }
 
