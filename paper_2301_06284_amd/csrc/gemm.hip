@@ -185,65 +185,72 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
         // that the accumulator of lane (li, q) holds row li, columns 4q..4q+3
         // of each column block.  The W fragments are re-read from LDS for every
         // row block (keeping the whole weight tile in VGPRs would cap occupancy).
+        // Columns are produced in passes of at most four column blocks against
+        // the same loaded rows, which bounds the live accumulators and weight
+        // fragments (and so the VGPRs) of the wide shapes; each pass ends with
+        // its part of the epilogue.
+        constexpr int CBP = NCB < 4 ? NCB : 4;
         const float4 (&acur)[KC] = ab[i];
-        floatx4 acc[NCB];
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        asm volatile("" ::: "memory");
         // with EP_BDIAG only the k chunks of a column block's own diagonal
         // block contribute (a compile-time test after unrolling)
         auto live = [](int c, int cb) { return !(EP & EP_BDIAG) || c / KCH == cb / CBH; };
+        float dpart[DH];
 #pragma unroll
-        for (int c = 0; c < KC; ++c) {
-            float4 b[NCB];
+        for (int hh = 0; hh < DH; ++hh) dpart[hh] = 0.f;
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                if (live(c, cb)) b[cb] = *reinterpret_cast<const float4 *>(&Wt[(cb * 16 + li) * KP + c * 16 + q * 4]);
+        for (int c0 = 0; c0 < NCB; c0 += CBP) {
+            floatx4 acc[CBP];
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].x, acur[c].x, acc[cb], 0, 0, 0);
+            for (int j = 0; j < CBP; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+            asm volatile("" ::: "memory");
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].y, acur[c].y, acc[cb], 0, 0, 0);
+            for (int c = 0; c < KC; ++c) {
+                float4 b[CBP];
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].z, acur[c].z, acc[cb], 0, 0, 0);
+                for (int j = 0; j < CBP; ++j)
+                    if (live(c, c0 + j))
+                        b[j] = *reinterpret_cast<const float4 *>(&Wt[((c0 + j) * 16 + li) * KP + c * 16 + q * 4]);
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-                if (live(c, cb)) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[cb].w, acur[c].w, acc[cb], 0, 0, 0);
-        }
-        // (d) epilogue
-        float4 o[NCB];
+                for (int j = 0; j < CBP; ++j)
+                    if (live(c, c0 + j)) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].x, acur[c].x, acc[j], 0, 0, 0);
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            o[cb] = make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
-            if (EP & EP_SCALE) o[cb] = make_float4(o[cb].x * sc, o[cb].y * sc, o[cb].z * sc, o[cb].w * sc);
+                for (int j = 0; j < CBP; ++j)
+                    if (live(c, c0 + j)) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].y, acur[c].y, acc[j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j)
+                    if (live(c, c0 + j)) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].z, acur[c].z, acc[j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j)
+                    if (live(c, c0 + j)) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].w, acur[c].w, acc[j], 0, 0, 0);
+            }
+            // (d) epilogue of this pass
+#pragma unroll
+            for (int j = 0; j < CBP; ++j) {
+                const int cb = c0 + j;
+                float4 v = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+                if (EP & EP_SCALE) v = make_float4(v.x * sc, v.y * sc, v.z * sc, v.w * sc);
+                if (EP & EP_DOT) {
+                    const float4 d = *reinterpret_cast<const float4 *>(&dvs[cb * 16 + q * 4]);
+                    dpart[cb / CBH] += v.x * d.x + v.y * d.y + v.z * d.z + v.w * d.w;
+                }
+                if (!valid) continue;
+                if (EP & (EP_RESID | EP_ACC)) v = make_float4(v.x + ex[cb].x, v.y + ex[cb].y, v.z + ex[cb].z, v.w + ex[cb].w);
+                if (EP & EP_RELU) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
+                const int col = cb * 16 + q * 4;
+                if ((EP & EP_SPLIT) && cb * 16 >= a.split)
+                    *reinterpret_cast<float4 *>(a.Y2 + y * a.ldy2 + (col - a.split)) = v;
+                else
+                    *reinterpret_cast<float4 *>(a.Y + y * a.ldy + col) = v;
+            }
         }
         if (EP & EP_DOT) {
 #pragma unroll
             for (int hh = 0; hh < DH; ++hh) {
-                float part = 0.f;
-#pragma unroll
-                for (int cb = hh * CBH; cb < (hh + 1) * CBH; ++cb) {
-                    const float4 d = *reinterpret_cast<const float4 *>(&dvs[cb * 16 + q * 4]);
-                    part += o[cb].x * d.x + o[cb].y * d.y + o[cb].z * d.z + o[cb].w * d.w;
-                }
+                float part = dpart[hh];
                 part += __shfl_xor(part, 16);
                 part += __shfl_xor(part, 32);
                 if (valid && q == 0) a.dot_out[y * DH + hh] = part;
             }
-        }
-        if (!valid) continue;
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            float4 v = o[cb];
-            if (EP & (EP_RESID | EP_ACC)) v = make_float4(v.x + ex[cb].x, v.y + ex[cb].y, v.z + ex[cb].z, v.w + ex[cb].w);
-            if (EP & EP_RELU) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
-            const int col = cb * 16 + q * 4;
-            if ((EP & EP_SPLIT) && cb * 16 >= a.split)
-                *reinterpret_cast<float4 *>(a.Y2 + y * a.ldy2 + (col - a.split)) = v;
-            else
-                *reinterpret_cast<float4 *>(a.Y + y * a.ldy + col) = v;
         }
     }
 }
