@@ -142,7 +142,7 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     x.vatt = c.take<float>((size_t)g->V * H);
     if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
         x.M = c.take<float>((size_t)g->U_src * d_out);
-        x.atts = c.take<float>((size_t)g->U_src * H);
+        if (H > 1) x.atts = c.take<float>((size_t)g->U_src * H);   // one head: formed in the traversal
         x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
     } else {
         x.S = c.take<float>((size_t)g->V * d_in);

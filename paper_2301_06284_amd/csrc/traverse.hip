@@ -293,8 +293,10 @@ __global__ __launch_bounds__(256) void seg_attn_kernel(TK k, int64_t V, const in
 }
 
 // ---------------------------------------------------------------- RGAT, transform-first
-// Messages M[p] = h_u W_r and source terms atts[p] = M[p] . w_src[r] exist once
-// per unique (src, rel) pair (compact materialization).
+// Several heads: messages M[p] = h_u W_r and source terms atts[p] = M[p] . w_src[r]
+// exist once per unique (src, rel) pair (compact materialization); logits are
+// staged per edge, the softmax of each destination is taken over them, then
+// the message rows are aggregated with the weights.
 template <int D, int H>
 __global__ __launch_bounds__(256) void rgat_tf_kernel(TK k)
 {
@@ -561,15 +563,14 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     LaunchScope ls("rgat_traverse_tf", s);
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
 #define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
-    if (a.heads == 1 && a.wsp) {   // single pass, source term from the message row
+    if (a.heads == 1) {   // single pass, source term from the message row
+        if (!a.wsp) return fail(RGNN_EINVAL, "one-head RGAT traversal needs w_src");
         if (a.d == 64) hipLaunchKernelGGL((rgat_tf1_kernel<64>), dim3(nb), dim3(256), 0, s, k);
         else if (a.d == 128) hipLaunchKernelGGL((rgat_tf1_kernel<128>), dim3(nb), dim3(256), 0, s, k);
         else return fail(RGNN_EUNSUPPORTED, "RGAT traversal: unsupported d");
     }
-    else if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
     else if (a.d == 64 && a.heads == 2) RGAT_TF(64, 2);
     else if (a.d == 64 && a.heads == 4) RGAT_TF(64, 4);
-    else if (a.d == 128 && a.heads == 1) RGAT_TF(128, 1);
     else if (a.d == 128 && a.heads == 2) RGAT_TF(128, 2);
     else if (a.d == 128 && a.heads == 4) RGAT_TF(128, 4);
     else if (a.d == 128 && a.heads == 8) RGAT_TF(128, 8);
