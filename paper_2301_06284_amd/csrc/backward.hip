@@ -342,7 +342,7 @@ __global__ __launch_bounds__(256) void split_dst_term_kernel(const int32_t *spli
 struct SK {
     int64_t n_items;
     const Item *items;           // {node0, node1, q0, q1}: nodes and their out-edge range
-    const int32_t *out_ptr, *out_pos, *out_vseg, *out_rel, *e2u;
+    const int32_t *out_ptr, *out_pos, *out_vseg, *out_rel, *out_pair;
     const float *wsp, *dS, *ay;
     float *dh;                   // holds the destination terms on entry
     float *ypair;                // [U_src] sum of Y per compact (src, rel) pair, zeroed before
@@ -375,7 +375,7 @@ __global__ __launch_bounds__(256) void bwd_src_kernel(SK k)
             const int p = k.out_pos[q0 + e];
             st.evs[e] = k.out_vseg[q0 + e];
             st.erel[e] = k.out_rel[q0 + e];
-            st.epair[e] = k.e2u[p];
+            st.epair[e] = k.out_pair[q0 + e];
             const float2 a = reinterpret_cast<const float2 *>(k.ay)[p];
             st.ea[e] = a.x;
             st.ey[e] = a.y;
@@ -758,7 +758,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
         SK sk{};
         sk.n_items = g->n_oitems; sk.items = g->dev.oitems; sk.out_ptr = g->dev.out_ptr;
         sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.out_rel = g->dev.out_rel;
-        sk.e2u = g->dev.e2u; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.ypair = w.ypair;
+        sk.out_pair = g->dev.out_pair; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.ypair = w.ypair;
         LaunchScope ls("rgat_bwd_src", s);
         hipLaunchKernelGGL(bwd_src_kernel, dim3((unsigned)((g->n_oitems + 15) / 16)), dim3(256), 0, s, sk);
     }

@@ -209,9 +209,11 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             for (int64_t i = 0; i < g->V; ++i) x.vseg_pos[x.vseg_byrel[i]] = (int32_t)i;
             x.out_vseg.resize((size_t)E);
             x.out_rel.resize((size_t)E);
+            x.out_pair.resize((size_t)E);
             for (int64_t q = 0; q < E; ++q) {
                 x.out_vseg[q] = x.vseg_pos[pos_vseg[x.out_pos[q]]];
                 x.out_rel[q] = x.in_rel[x.out_pos[q]];
+                x.out_pair[q] = x.e2u[x.out_pos[q]];
             }
             // work items over out-edges: bundles of small sources, pieces of large ones
             x.oitems.clear();
@@ -294,7 +296,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
-    add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos);
+    add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
@@ -362,7 +364,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         g->host.in_src.swap(empty.in_src); g->host.in_rel.swap(empty.in_rel);
         g->host.in_eid.swap(empty.in_eid); g->host.e2u.swap(empty.e2u);
         g->host.out_pos.swap(empty.out_pos); g->host.out_vseg.swap(empty.out_vseg);
-        g->host.out_rel.swap(empty.out_rel);
+        g->host.out_rel.swap(empty.out_rel); g->host.out_pair.swap(empty.out_pair);
     }
     *out = g;
     return RGNN_OK;
