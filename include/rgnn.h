@@ -181,7 +181,13 @@ rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W, 
  *   h [N, d_in], W [R, d_in, d_out], w_src, w_dst [R, d_out], out [N, d_out].
  *   saved [N, heads, 2] or NULL: per destination and head the softmax maximum
  *   and denominator (max z, sum exp(z - max)), 0 for empty rows; needed by
- *   rgat_backward.  softmax_scope must be RGNN_SOFTMAX_PER_DST.
+ *   rgat_backward.
+ *   softmax_scope RGNN_SOFTMAX_PER_DST_REL takes the softmax over the in-edges
+ *   of v with relation r instead (each relation's messages are normalised on
+ *   their own; out_v sums the relations): it runs the aggregate-first plan
+ *   (heads == 1, d_in == d_out; size the workspace for
+ *   RGNN_PLAN_AGGREGATE_FIRST), requires saved == NULL, and returns
+ *   RGNN_EUNSUPPORTED for RGNN_PLAN_TRANSFORM_FIRST.
  *   d_in, d_out in {64, 128}; d_out / heads a multiple of 16.
  *   RGNN_PLAN_AGGREGATE_FIRST requires heads == 1. */
 rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,

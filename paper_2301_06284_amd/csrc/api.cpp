@@ -371,11 +371,18 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     if (!dim_ok(d_in) || !dim_ok(d_out)) return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128");
     if (heads <= 0 || d_out % heads) return fail(RGNN_EINVAL, "heads must divide d_out");
     if ((d_out / heads) % 16) return fail(RGNN_EUNSUPPORTED, "d_out / heads must be a multiple of 16");
-    if (softmax_scope == RGNN_SOFTMAX_PER_DST_REL)
-        return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) is not implemented");
-    if (softmax_scope != RGNN_SOFTMAX_PER_DST) return fail(RGNN_EINVAL, "unknown softmax scope");
+    if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
+        return fail(RGNN_EINVAL, "unknown softmax scope");
     if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
+    const bool per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
+    if (per_seg) {   // normalised per (dst, rel) segment: the aggregate-first plan
+        if (plan == RGNN_PLAN_TRANSFORM_FIRST)
+            return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) runs aggregate-first");
+        if (saved) return fail(RGNN_EINVAL, "saved holds per-destination statistics: pass NULL with "
+                                            "softmax per (destination, relation)");
+        plan = RGNN_PLAN_AGGREGATE_FIRST;
+    }
     plan = resolve_plan(g, RGNN_LAYER_RGAT, d_in, d_out, heads, plan);
     if (plan == RGNN_PLAN_AGGREGATE_FIRST && (heads != 1 || d_in != d_out))
         return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs heads == 1 and d_in == d_out");
@@ -421,7 +428,7 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         ta.heads = 1; ta.d = d_in; ta.S = w.S; ta.vstat = w.vstat; ta.saved = stats;
         ta.vscale = w.vscale;
         if ((st = launch_rgat_traverse_af(ta, s)) != RGNN_OK) return st;
-        if ((st = launch_vseg_stats(ta, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_stats(ta, per_seg, s)) != RGNN_OK) return st;
         GemmArgs ga;
         ga.X = w.S; ga.ldx = d_in; ga.gather = g->dev.vseg_byrel;
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;

@@ -120,9 +120,11 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         // ---- virtual segments: segments cut into pieces of at most C edges ----
         x.vseg_ptr.clear(); x.vseg_rel.clear(); x.vseg_dst.clear(); x.vseg_cnt.clear();
         x.dst_vsegptr.assign((size_t)N + 1, 0);
+        x.seg_vsegptr.assign((size_t)g->U_dst + 1, 0);
         for (int64_t v = 0; v < N; ++v) {
             for (int32_t s = x.dst_segptr[v]; s < x.dst_segptr[v + 1]; ++s) {
                 const int32_t b = x.seg_ptr[s], e = x.seg_ptr[s + 1];
+                x.seg_vsegptr[s] = (int32_t)x.vseg_ptr.size();
                 for (int32_t p = b; p < e; p += C) {
                     x.vseg_ptr.push_back(p);
                     x.vseg_rel.push_back(x.seg_rel[s]);
@@ -134,6 +136,11 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         }
         g->V = (int64_t)x.vseg_ptr.size();
         x.vseg_ptr.push_back((int32_t)E);
+        x.seg_vsegptr[(size_t)g->U_dst] = (int32_t)g->V;
+        x.big_seg.clear();
+        for (int64_t sg = 0; sg < g->U_dst; ++sg)
+            if (x.seg_vsegptr[sg + 1] - x.seg_vsegptr[sg] > kBigRange) x.big_seg.push_back((int32_t)sg);
+        g->n_big_seg = (int64_t)x.big_seg.size();
         // vsegs grouped by relation (stable: (rel, dst) order) for the typed GEMMs
         std::vector<int32_t> vperm((size_t)g->V);
         for (int64_t i = 0; i < g->V; ++i) vperm[i] = (int32_t)i;
@@ -289,6 +296,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
     add32(&d.split_slotptr, x.split_slotptr);
     add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
+    add32(&d.seg_vsegptr, x.seg_vsegptr); add32(&d.big_seg, x.big_seg);
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});

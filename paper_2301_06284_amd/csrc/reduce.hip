@@ -26,34 +26,40 @@ __device__ __forceinline__ float4 relu4(float4 a)
 // Destinations with more than kBigRange segments are left to the block kernel.
 // Also writes, per segment, the scale exp(m_seg - M_v) / Z_v that finishes the
 // softmax when the typed GEMM applies W_r to the segment's sum.
-__global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *dst_vsegptr,
+// Softmax groups are runs of consecutive virtual segments: those of one
+// destination (softmax per destination) or of one (dst, rel) segment (softmax
+// per destination and relation), given by the offsets grp_vsegptr.  saved
+// (per group: max, denominator) may be NULL.
+__global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *grp_vsegptr,
                                                          const float *vstat, float *saved,
                                                          float *vscale)
 {
     const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (v >= N) return;
-    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    const int b = grp_vsegptr[v], e = grp_vsegptr[v + 1];
     if (e - b > kBigRange) return;
     float M = -INFINITY;
     for (int i = b; i < e; ++i) M = fmaxf(M, vstat[(size_t)i * 2]);
     float Z = 0.f;
     for (int i = b; i < e; ++i) Z += vstat[(size_t)i * 2 + 1] * __expf(vstat[(size_t)i * 2] - M);
-    saved[v * 2] = b < e ? M : 0.f;
-    saved[v * 2 + 1] = Z;
+    if (saved) {
+        saved[v * 2] = b < e ? M : 0.f;
+        saved[v * 2 + 1] = Z;
+    }
     for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)i * 2] - M) / Z;
 }
 
-// One workgroup per destination with many segments: strided per-thread
-// partial (max, sum), combined in thread order through LDS.
-__global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_vdst,
-                                                             const int32_t *dst_vsegptr,
+// One workgroup per group with many segments: strided per-thread partial
+// (max, sum), combined in thread order through LDS.
+__global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_grp,
+                                                             const int32_t *grp_vsegptr,
                                                              const float *vstat, float *saved,
                                                              float *vscale)
 {
     __shared__ float sm[256], ss[256];
     __shared__ float fin[2];
-    const int v = big_vdst[blockIdx.x];
-    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    const int v = big_grp[blockIdx.x];
+    const int b = grp_vsegptr[v], e = grp_vsegptr[v + 1];
     float m = -INFINITY, s = 0.f;
     for (int i = b + (int)threadIdx.x; i < e; i += 256) {
         const float mi = vstat[(size_t)i * 2], si = vstat[(size_t)i * 2 + 1];
@@ -70,8 +76,10 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
         float Z = 0.f;
         for (int t = 0; t < 256; ++t)
             if (ss[t] > 0.f) Z += ss[t] * __expf(sm[t] - M);
-        saved[(size_t)v * 2] = M;
-        saved[(size_t)v * 2 + 1] = Z;
+        if (saved) {
+            saved[(size_t)v * 2] = M;
+            saved[(size_t)v * 2 + 1] = Z;
+        }
         fin[0] = M;
         fin[1] = Z;
     }
@@ -316,22 +324,28 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "merge_big launch");
 }
 
-rgnn_status launch_vseg_stats(const TravArgs &a, hipStream_t s)
+rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s)
 {
     const rgnn_graph *g = a.g;
-    if (g->N == 0) return RGNN_OK;
+    // softmax groups: destinations, or (dst, rel) segments
+    const int64_t n = per_segment ? g->U_dst : g->N;
+    const int32_t *ptr = per_segment ? g->dev.seg_vsegptr : g->dev.dst_vsegptr;
+    const int32_t *big = per_segment ? g->dev.big_seg : g->dev.big_vdst;
+    const int64_t nbig = per_segment ? g->n_big_seg : g->n_big_vdst;
+    float *saved = per_segment ? nullptr : a.saved;
+    if (n == 0) return RGNN_OK;
     {
         LaunchScope ls("vseg_stats", s);
-        hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(g->N, 256)), dim3(256), 0, s, g->N,
-                           g->dev.dst_vsegptr, a.vstat, a.saved, a.vscale);
+        hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, n, ptr, a.vstat,
+                           saved, a.vscale);
     }
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "vseg_stats launch");
-    if (g->n_big_vdst == 0) return RGNN_OK;
+    if (nbig == 0) return RGNN_OK;
     {
         LaunchScope ls("vseg_stats_big", s);
-        hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)g->n_big_vdst), dim3(256), 0, s,
-                           g->dev.big_vdst, g->dev.dst_vsegptr, a.vstat, a.saved, a.vscale);
+        hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)nbig), dim3(256), 0, s, big, ptr, a.vstat,
+                           saved, a.vscale);
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_stats_big launch");

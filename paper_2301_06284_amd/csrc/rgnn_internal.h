@@ -44,6 +44,8 @@ struct HostIndex {
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
     std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments
+    std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
+    std::vector<int32_t> big_seg;      // (dst, rel) segments with > kBigRange virtual segments
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
     std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
@@ -67,6 +69,7 @@ struct DeviceIndex {
     Item *items = nullptr;
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
+    int32_t *seg_vsegptr = nullptr, *big_seg = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
     int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr, *out_rel = nullptr;
@@ -87,7 +90,7 @@ struct rgnn_graph {
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0;
-    int64_t n_big_split = 0, n_big_vdst = 0;
+    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
@@ -190,7 +193,9 @@ rgnn_status launch_rgat_traverse_af(const TravArgs &a, hipStream_t s);
 rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
                                   const float *partial, float *out, float *saved, int relu,
                                   hipStream_t s);
-rgnn_status launch_vseg_stats(const TravArgs &a, hipStream_t s);
+// Per-piece softmax scales (and, per destination, saved (max, sum)) from the
+// pieces' partial states; per_segment: softmax per (dst, rel) segment.
+rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s);
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
                                int accumulate, int relu, hipStream_t s);
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);

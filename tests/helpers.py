@@ -79,14 +79,17 @@ class Runner:
         torch.cuda.synchronize()
         return out.cpu().numpy()
 
-    def rgat(self, heads=1, plan=0, slope=0.2, want_saved=False):
+    def rgat(self, heads=1, plan=0, slope=0.2, want_saved=False, scope=0):
         T, torch = self.T, self.torch
         d_in, d_out = T["W"].shape[1], T["W"].shape[2]
         out = torch.full((self.g["N"], d_out), float("nan"), device=self.dev)
-        saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev)
+        saved = None
+        if scope == 0:
+            saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev)
+        ws_plan = 2 if scope == 1 else plan   # per-(dst, rel) softmax runs aggregate-first
         self.rgnn.rgat_forward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved,
-                               self.ws(1, d_in, d_out, heads, plan), d_in, d_out, heads, slope,
-                               0, plan)
+                               self.ws(1, d_in, d_out, heads, ws_plan), d_in, d_out, heads, slope,
+                               scope, plan)
         torch.cuda.synchronize()
         if want_saved:
             return out.cpu().numpy(), saved

@@ -92,6 +92,16 @@ def test_workload2_rgat(plan):
     np.testing.assert_allclose(s[:, 1], sm[:, 0], rtol=1e-4)
 
 
+def test_workload2_rgat_per_relation_softmax():
+    g, t, run = load(2)
+    print("workload 2 rgat per-relation softmax", flush=True)
+    got = run.rgat(scope=1)
+    assert np.isfinite(got).all()
+    sel = sample_rows(g, 300, seed=5)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1, sel=sel)
+    assert row_err(got[sel], ref) <= TOL
+
+
 def test_workload3_hgt():
     g, t, run = load(3)
     print("workload 3 hgt", flush=True)

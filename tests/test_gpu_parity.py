@@ -121,6 +121,58 @@ def test_rgat_d128(plan, heads):
 
 
 @pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("d", [64, 128])
+def test_rgat_per_relation_softmax(kind, d):
+    """Softmax over the in-edges of one (destination, relation) segment."""
+    g = graph(kind)
+    t = workloads.tiny_tensors(21, g, d, d, att_var=1.0)
+    print(f"rgat per-relation softmax {kind} d={d}", flush=True)
+    run = Runner(g, t)
+    got = run.rgat(plan=0, scope=1)
+    again = run.rgat(plan=2, scope=1)
+    run.close()
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1)
+    assert row_err(got, ref) <= TOL
+    assert np.array_equal(got, again)
+
+
+def test_rgat_per_relation_softmax_big_segment():
+    """One (destination, relation) segment cut into more pieces than one
+    thread reduces (the workgroup-per-segment statistics path)."""
+    g = graph("hub", seed=22, N=200, E=6000, R=1)
+    t = workloads.tiny_tensors(22, g, 64, 64, att_var=1.0)
+    print("rgat per-relation softmax big segment", flush=True)
+    run = Runner(g, t)
+    got = run.rgat(scope=1)
+    run.close()
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1)
+    assert row_err(got, ref) <= TOL
+
+
+def test_rgat_per_relation_softmax_rejects():
+    import torch
+    from paper_2301_06284_amd import rgnn
+    g = graph("random", seed=23)
+    t = workloads.tiny_tensors(23, g, 64, 64)
+    print("rgat per-relation softmax argument checks", flush=True)
+    run = Runner(g, t)
+    T = run.T
+    out = torch.empty(g["N"], 64, device="cuda:0")
+    saved = torch.empty(g["N"], 1, 2, device="cuda:0")
+    ws = run.ws(1, 64, 64, 1, 2)
+    with pytest.raises(rgnn.RgnnError, match="aggregate-first"):
+        rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
+                          softmax_scope=rgnn.SOFTMAX_PER_DST_REL, plan=rgnn.PLAN_TRANSFORM_FIRST)
+    with pytest.raises(rgnn.RgnnError, match="saved"):
+        rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved, ws, 64, 64,
+                          softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
+    with pytest.raises(rgnn.RgnnError, match="heads"):
+        rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
+                          heads=2, softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
+    run.close()
+
+
+@pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("heads", [1, 2, 4])
 def test_hgt_small(kind, heads):
     g = graph(kind, T=4, R=7)
