@@ -1,7 +1,9 @@
 """Benchmark of the RGNN layer hot path on one MI355X.
 
 Headline (`value`): edges/s of one RGAT layer forward (all of its kernels:
-reordered attention vectors, typed GEMM, traversal, merges) on the am-like
+reordered attention vectors, destination terms, the fused gather-transform
+traversal or the typed GEMM and traversal, softmax statistics, reductions and
+merges, per the plan the library selects) on the am-like
 workload -- 880 000 nodes, 7 node types, 96 relations (Zipf 1.2), 5.7 M edges
 (power-law in-degree, exponent 2.1), d = 64, one head -- with every input
 resident in HBM.  One step = one layer forward; K steps are timed between two
@@ -130,17 +132,21 @@ def rgat_tf_model(info, d, H):
 
 
 def rgat_af_model(info, d):
-    E, N, V, R, I = (info["num_edges"], info["num_nodes"], info["num_vsegs"], info["num_rels"],
-                     info["num_items"])
+    """Algorithmic bytes / flops per launch of the aggregate-first RGAT kernels."""
+    E, N, V, R = info["num_edges"], info["num_nodes"], info["num_vsegs"], info["num_rels"]
     return {
-        # per edge: source index and h row; per segment: sum row and (max, sum) written;
-        # per destination: h_v row
-        "rgat_traverse_af": dict(bytes=E * (4 + 4 * d) + V * (4 * d + 8 + 8) + N * (4 * d + 4)
-                                 + I * 16 + 2 * R * d * 4, flops=E * (6.0 * d)),
-        # per segment row: gather index, S row read, T row write, stats and scale
-        "typed_gemm": dict(bytes=V * (4 + 4 * d + 4 * d + 4 + 8 + 8) + R * 4 * d * d,
-                           flops=2.0 * V * d * d),
-        "vseg_reduce": dict(bytes=V * 4 * d + N * (4 * d + 4), flops=V * d),
+        # per edge: source index and gathered h row; per segment: its table
+        # entry, destination term, T row and (max, sum) written; W_r and
+        # W_r w_src once per relation.  Flops: the segment transform on the
+        # matrix cores plus the per-edge dot and weighted accumulation.
+        "rgat_af_fused": dict(bytes=E * (4 + 4 * d) + V * (16 + 4 + 4 * d + 8) + R * (4 * d * d + 4 * d),
+                              flops=2.0 * V * d * d + E * 4.0 * d),
+        # all destinations (the kernel and its one-workgroup-per-hub sibling):
+        # per segment T row and scale read, per destination offsets and output row
+        "vseg_reduce": dict(bytes=V * (4 * d + 4) + N * (4 + 4 * d), flops=2.0 * V * d),
+        # per destination its h row (consecutive segments share it); per
+        # segment its destination, relation and term written; W_r w_dst per relation
+        "seg_attn": dict(bytes=N * 4 * d + V * 12 + R * 4 * d, flops=2.0 * V * d),
     }
 
 
@@ -268,7 +274,7 @@ def main():
         tr = counter_traffic("rgat_am_like_880k", k)
         ent["counter_bytes"] = tr
         ent["counter_gbs"] = None if tr is None else round(tr / (kms_k * 1e-3) / 1e9, 1)
-        if k == "typed_gemm":
+        if k in ("typed_gemm", "rgat_af_fused"):
             ent["mfma_tflops"] = round(m["flops"] / (kms_k * 1e-3) / 1e12, 2)
             ent["mfma_frac"] = round(ent["mfma_tflops"] / FP32_PEAK_TFLOPS, 4)
     c.close()

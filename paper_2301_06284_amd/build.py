@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "librgnn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["graph.cpp", "api.cpp", "gemm.hip", "traverse.hip", "reduce.hip", "hgt.hip",
-           "backward.hip"]
+           "backward.hip", "fused.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -97,11 +97,13 @@ void plan_bytes(const rgnn_graph *g, int layer, int d_in, int d_out, int H, doub
     const double bi = 4.0 * d_in, bo = 4.0 * d_out;
     if (layer == RGNN_LAYER_RGCN) {
         *tf = U * (bi + bo) + E * (4 + bo) + V * 12 + N * bo;
-        *af = E * (4 + bi) + V * (bi + 12) + V * (bi + bo) + V * bo + N * bo;
+        // fused: gathered rows + segment table + T written and read back
+        *af = E * (4 + bi) + V * (16 + 2 * bo) + N * bo;
     } else {
         *tf = U * (bi + bo + 4 * H) + E * (4 + bo + 4 * H) + V * 12 + N * (bi + bo + 8 * H);
-        *af = E * (4 + bi) + V * (bi + 20) + N * (bi + 8) + V * 8 + N * 8 + V * (bi + bo + 8) +
-              V * bo + N * bo;
+        // destination terms (h_v once per destination), fused traversal (rows,
+        // segment table, destination term, T, (max, sum)), statistics, reduce
+        *af = E * (4 + bi) + N * (bi + 8 + bo) + V * (48 + 2 * bo);
     }
 }
 
@@ -124,7 +126,6 @@ size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *bas
         x.M = c.take<float>((size_t)g->U_src * d_out);
         x.partial = c.take<float>((size_t)g->n_slots * (2 + d_out));
     } else {
-        x.S = c.take<float>((size_t)g->V * d_in);
         x.T = c.take<float>((size_t)g->V * d_out);
     }
     if (w) *w = x;
@@ -145,7 +146,6 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
         if (H > 1) x.atts = c.take<float>((size_t)g->U_src * H);   // one head: formed in the traversal
         x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
     } else {
-        x.S = c.take<float>((size_t)g->V * d_in);
         x.vstat = c.take<float>((size_t)g->V * 2);
         x.vscale = c.take<float>((size_t)g->V);
         x.T = c.take<float>((size_t)g->V * d_out);
@@ -336,16 +336,13 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
         if ((st = launch_merge_partials(g, d_out, 1, 0, w.partial, out, nullptr, ta.relu, s)) != RGNN_OK)
             return st;
     } else {
-        TravArgs ta;
-        ta.g = g; ta.h = h; ta.d = d_in; ta.S = w.S;
-        if ((st = launch_rgcn_traverse_af(ta, s)) != RGNN_OK) return st;
-        GemmArgs ga;
-        ga.X = w.S; ga.ldx = d_in; ga.gather = g->dev.vseg_byrel;
-        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
-        ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
-        ga.Y = w.T; ga.ldy = d_out; ga.scatter = g->dev.vseg_byrel;
-        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
-        if ((st = launch_vseg_reduce(g, w.T, d_out, out, 0, relu_in_traversal, s)) != RGNN_OK) return st;
+        // fused gather + per-(dst, rel) mean + W_r per virtual segment, then
+        // the segments of each destination summed
+        FusedArgs fa;
+        fa.g = g; fa.h = h; fa.W = W; fa.d_in = d_in; fa.d_out = d_out; fa.T = w.T;
+        if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_reduce(g, w.T, nullptr, d_out, out, 0, relu_in_traversal, s)) != RGNN_OK)
+            return st;
     }
     if (W0) {   // virtual self-loop h_v W0, accumulated into out (then the activation)
         GemmArgs ga;
@@ -421,22 +418,18 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         if ((st = launch_merge_partials(g, d_out, heads, 1, w.partial, out, saved, 0, s)) != RGNN_OK)
             return st;
     } else {
+        // fused gather + per-segment online softmax + W_r per virtual segment;
+        // the softmax is finished per destination (or per segment) when the
+        // segments are summed
         if ((st = launch_reorder_vec(W, w_src, g->R, d_in, d_out, 1, w.wsp, s)) != RGNN_OK) return st;
-        float *stats = saved ? saved : w.saved;
+        FusedArgs fa;
+        fa.g = g; fa.h = h; fa.W = W; fa.wsp = w.wsp; fa.vatt = w.vatt; fa.slope = neg_slope;
+        fa.d_in = d_in; fa.d_out = d_out; fa.softmax = 1; fa.T = w.T; fa.vstat = w.vstat;
+        if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
         TravArgs ta;
-        ta.g = g; ta.h = h; ta.wsp = w.wsp; ta.wtp = w.wtp; ta.vatt = w.vatt; ta.slope = neg_slope;
-        ta.heads = 1; ta.d = d_in; ta.S = w.S; ta.vstat = w.vstat; ta.saved = stats;
-        ta.vscale = w.vscale;
-        if ((st = launch_rgat_traverse_af(ta, s)) != RGNN_OK) return st;
+        ta.g = g; ta.vstat = w.vstat; ta.saved = saved ? saved : w.saved; ta.vscale = w.vscale;
         if ((st = launch_vseg_stats(ta, per_seg, s)) != RGNN_OK) return st;
-        GemmArgs ga;
-        ga.X = w.S; ga.ldx = d_in; ga.gather = g->dev.vseg_byrel;
-        ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
-        ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
-        ga.Y = w.T; ga.ldy = d_out; ga.scatter = g->dev.vseg_byrel;
-        ga.ep.row_scale = w.vscale;
-        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
-        if ((st = launch_vseg_reduce(g, w.T, d_out, out, 0, 0, s)) != RGNN_OK) return st;
+        if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
     }
     return RGNN_OK;
 }

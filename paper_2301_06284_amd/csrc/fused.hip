@@ -1,0 +1,343 @@
+// fused.hip -- fused gather -> segment sum -> typed transform for the
+// aggregate-first plan (Section "Graph-Semantic Optimizations": linear operator
+// reordering moves W_r after the per-(dst, rel) aggregation; Section "The GEMM
+// Template and the Traversal Template" gives the two halves fused here).
+//
+// For every virtual segment (one (dst, rel) pair, at most kChunkEdges in-edges)
+// the kernel forms the segment's weighted row sum S of the gathered source
+// rows h_u and immediately multiplies it by W_r on the matrix cores, writing
+// T = S W_r.  S never goes to memory.
+//
+// Work decomposition.  Segments are grouped by relation and, inside a
+// relation, ordered by edge count (largest first); a host-built tile table
+// gives each workgroup up to kFusedTileRows consecutive segments of one
+// relation, so W_r is staged once in LDS for the whole tile.  A wave takes 16
+// segments at a time -- one 16-row MFMA block -- and gathers them in the MFMA
+// operand layout itself: lane (li, q) owns segment li of the block and columns
+// 16c + 4q .. +3 of its rows, so every gathered row is four dwordx4 loads per
+// lane of four lanes, and the finished sums are already the B operand of
+// v_mfma_f32_16x16x4f32 (the same transposed-block scheme as the typed GEMM:
+// lane (li, q) receives row li, columns 4q .. 4q+3 of each 16-column block).
+// Because the 16 segments of a block have nearly equal edge counts, the edge
+// loop wastes few lane-steps.
+//
+// RGAT: per edge the source term h_u . (W_r w_src[r]) (reordered) is summed
+// over the four lanes of the row; with the segment's destination term it gives
+// the logit, and an online softmax keeps the running maximum m, the sum s and
+// the exp-weighted row sum.  T and (m, s) are written per segment; the
+// per-destination normalisation exp(m - M_v) / Z_v is applied when the
+// segments of a destination are summed.  RGCN: plain sums scaled by
+// 1 / c_{v,r}.  No atomics: results are bitwise reproducible.
+#include "rgnn_internal.h"
+#include "wave_ops.h"
+
+namespace rgnn {
+
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+__device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
+__device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
+__device__ __forceinline__ float leaky(float y, float slope) { return y > 0.f ? y : slope * y; }
+
+enum : int { kModeMean = 0, kModeSoftmax = 1 };
+
+struct FK {
+    const FusedRow *rows;
+    const Tile *tiles;           // pad = the tile's first position in src
+    int64_t ntiles, nedges;
+    const int32_t *src;          // source node of every in-edge, in fused order
+    const float *h, *W, *wsp, *vatt;
+    float slope;
+    float *T, *vstat;
+};
+
+// DI: input features, DO: output features, NWAVE: waves per workgroup,
+// KU: edges per gathered batch (two batches in flight).
+//
+// Gather layout: lane l serves rows l/8 and l/8 + 8 of the 16-row block, and
+// within each the features 32c + 4(l%8) .. +3 (c < DI/32), so one dwordx4
+// load instruction covers whole 128-byte lines of eight rows.  The finished
+// row sums are moved into the MFMA operand layout by lane permutes.
+template <int DI, int DO, int MODE, int NWAVE, int KU>
+__global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4))) void af_fused_kernel(FK k)
+{
+    constexpr int NT = 64 * NWAVE;
+    constexpr int KP = DI + 4;       // padded LDS row (conflict-free b128 reads)
+    constexpr int KC = DI / 16;      // MFMA k chunks
+    constexpr int CH = DI / 32;      // float4 chunks per lane and gathered row
+    constexpr int NCB = DO / 16;     // output column blocks
+    constexpr int CBP = NCB < 4 ? NCB : 4;
+    constexpr int NW = DI * DO / 4 / NT;
+    constexpr int NR = (kFusedTileRows + NT - 1) / NT;   // segment entries per thread
+    constexpr int NS = (kFusedTileEdges + NT - 1) / NT;  // source indices per thread
+    static_assert(NW * NT * 4 == DI * DO, "weight tile must split evenly over the workgroup");
+    __shared__ float Wt[DO * KP];
+    __shared__ float wsl[MODE == kModeSoftmax ? DI : 1];
+    __shared__ FusedRow srow[kFusedTileRows];
+    __shared__ int32_t ssrc[kFusedTileEdges];
+
+    const Tile tile = k.tiles[blockIdx.x];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, q = lane >> 4;       // MFMA layout
+    const int gr = lane >> 3, gp = lane & 7;       // gather layout: rows gr, gr + 8
+    const int r = tile.type;
+    const int64_t te0 = tile.pad;
+    const int tne = (int)((blockIdx.x + 1 < k.ntiles ? (int64_t)k.tiles[blockIdx.x + 1].pad : k.nedges) - te0);
+
+    // Stage: W_r, the tile's segment table and its source indices are all
+    // fetched into registers first (independent, coalesced loads), then
+    // written to LDS behind one barrier.  After it, the row gathers are the
+    // only loads that depend on another load.
+    float4 wv[NW];
+#pragma unroll
+    for (int t = 0; t < NW; ++t) {
+        const int idx = tid + NT * t;
+        const int kk = idx / (DO / 4), n4 = (idx % (DO / 4)) * 4;
+        wv[t] = ld4(k.W + ((size_t)r * DI + kk) * DO + n4);
+    }
+    FusedRow rv[NR];
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+        const int i = tid + NT * t;
+        rv[t] = k.rows[tile.row0 + (i < tile.rows ? i : 0)];
+    }
+    int sv[NS];
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+        const int i = tid + NT * t;
+        sv[t] = k.src[te0 + (i < tne ? i : 0)];
+    }
+    float wsv = 0.f;
+    if (MODE == kModeSoftmax && tid < DI) wsv = k.wsp[(size_t)r * DI + tid];
+#pragma unroll
+    for (int t = 0; t < NW; ++t) {
+        const int idx = tid + NT * t;
+        const int kk = idx / (DO / 4), n4 = (idx % (DO / 4)) * 4;
+        Wt[(n4 + 0) * KP + kk] = wv[t].x;
+        Wt[(n4 + 1) * KP + kk] = wv[t].y;
+        Wt[(n4 + 2) * KP + kk] = wv[t].z;
+        Wt[(n4 + 3) * KP + kk] = wv[t].w;
+    }
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+        const int i = tid + NT * t;
+        if (i < tile.rows) srow[i] = rv[t];
+    }
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+        const int i = tid + NT * t;
+        if (i < tne) ssrc[i] = sv[t];
+    }
+    if (MODE == kModeSoftmax && tid < DI) wsl[tid] = wsv;
+    __syncthreads();
+
+    const int nrb = (tile.rows + 15) >> 4;
+    for (int rb = wave; rb < nrb; rb += NWAVE) {
+        // the two gathered rows of this lane; rows past the tile's end repeat
+        // the block's first row (never longer than the block's longest) and
+        // store nothing
+        FusedRow fr[2];
+        bool valid[2];
+        const int32_t *ls[2];
+        float va[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            const int row = rb * 16 + gr + 8 * h2;
+            valid[h2] = row < tile.rows;
+            fr[h2] = srow[valid[h2] ? row : rb * 16];
+            ls[h2] = ssrc + (fr[h2].e0 - te0);
+            va[h2] = MODE == kModeSoftmax ? k.vatt[fr[h2].vs] : 0.f;
+        }
+        // edge count of the block's longest segment
+        float nm = gmax<32>(fmaxf((float)fr[0].ne, (float)fr[1].ne));
+        nm = fmaxf(nm, __shfl_xor(nm, 32));
+        const int nmax = __builtin_amdgcn_readfirstlane((int)nm);
+
+        float m[2] = {-INFINITY, -INFINITY}, s[2] = {0.f, 0.f};
+        float4 acc[2][CH];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+            for (int c = 0; c < CH; ++c) acc[h2][c] = make_float4(0.f, 0.f, 0.f, 0.f);
+
+        // ping-pong batches of KU edges of both rows (indices from LDS); a row
+        // already finished issues no gathers (most segments are one or two
+        // edges long)
+        float4 A[KU][2][CH], B[KU][2][CH];
+        auto load = [&](float4 (&X)[KU][2][CH], int t) {
+#pragma unroll
+            for (int u = 0; u < KU; ++u)
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    if (t + u < fr[h2].ne) {
+                        const int i = ls[h2][t + u];
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) X[u][h2][c] = ld4(k.h + (size_t)i * DI + c * 32 + gp * 4);
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) X[u][h2][c] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
+                }
+        };
+        auto consume = [&](const float4 (&X)[KU][2][CH], int t) {
+#pragma unroll
+            for (int u = 0; u < KU; ++u)
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    const float4 *x = X[u][h2];
+                    if (MODE == kModeSoftmax) {
+                        float p = 0.f;
+#pragma unroll
+                        for (int c = 0; c < CH; ++c)
+                            p += dot4(x[c], *reinterpret_cast<const float4 *>(&wsl[c * 32 + gp * 4]));
+                        p = gsum<8>(p);   // the row's eight lanes: identical sums
+                        if (t + u < fr[h2].ne) {
+                            const float z = leaky(p + va[h2], k.slope);
+                            const float mn = fmaxf(m[h2], z);
+                            const float c1 = __expf(m[h2] - mn), c2 = __expf(z - mn);
+                            s[h2] = s[h2] * c1 + c2;
+#pragma unroll
+                            for (int c = 0; c < CH; ++c) {
+                                float4 &a = acc[h2][c];
+                                a = make_float4(a.x * c1 + x[c].x * c2, a.y * c1 + x[c].y * c2,
+                                                a.z * c1 + x[c].z * c2, a.w * c1 + x[c].w * c2);
+                            }
+                            m[h2] = mn;
+                        }
+                    } else if (t + u < fr[h2].ne) {
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            float4 &a = acc[h2][c];
+                            a = make_float4(a.x + x[c].x, a.y + x[c].y, a.z + x[c].z, a.w + x[c].w);
+                        }
+                    }
+                }
+        };
+        load(A, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int t = 0; t < nmax; t += 2 * KU) {
+            load(B, t + KU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(A, t);
+            load(A, t + 2 * KU);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(B, t + KU);
+        }
+
+        // row sums -> MFMA operand layout by lane permutes: lane (li, q) takes
+        // features 16c + 4q .. +3 of row li, held by lane 8 (li % 8) + 4 (c % 2) + q
+        // in its chunk c / 2 of row set li / 8
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            if (MODE == kModeMean) {
+                const float sc = 1.f / (float)fr[h2].cnt;
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    float4 &a = acc[h2][c];
+                    a = make_float4(a.x * sc, a.y * sc, a.z * sc, a.w * sc);
+                }
+            }
+            if (MODE == kModeSoftmax && valid[h2] && gp == 0)
+                *reinterpret_cast<float2 *>(k.vstat + (size_t)fr[h2].vs * 2) = make_float2(m[h2], s[h2]);
+        }
+        const bool hi = li >= 8;
+        float4 sb[KC];
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+            const int sl = 8 * (li & 7) + 4 * (c & 1) + q;
+            const float4 a0 = acc[0][c >> 1], a1 = acc[1][c >> 1];
+            const float x0 = __shfl(a0.x, sl), x1 = __shfl(a1.x, sl);
+            const float y0 = __shfl(a0.y, sl), y1 = __shfl(a1.y, sl);
+            const float z0 = __shfl(a0.z, sl), z1 = __shfl(a1.z, sl);
+            const float w0 = __shfl(a0.w, sl), w1 = __shfl(a1.w, sl);
+            sb[c] = make_float4(hi ? x1 : x0, hi ? y1 : y0, hi ? z1 : z0, hi ? w1 : w0);
+        }
+        const bool ovalid = rb * 16 + li < tile.rows;
+        const int vso = srow[ovalid ? rb * 16 + li : rb * 16].vs;
+
+        // T = S W_r on the matrix cores: A = W_r^T fragments from LDS, B = the
+        // row sums (k-slot q of step (c, j) is feature 16c + 4q + j for both)
+#pragma unroll
+        for (int c0 = 0; c0 < NCB; c0 += CBP) {
+            floatx4 o[CBP];
+#pragma unroll
+            for (int j = 0; j < CBP; ++j) o[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                float4 b[CBP];
+#pragma unroll
+                for (int j = 0; j < CBP; ++j)
+                    b[j] = *reinterpret_cast<const float4 *>(&Wt[((c0 + j) * 16 + li) * KP + c * 16 + q * 4]);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j) o[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].x, sb[c].x, o[j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j) o[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].y, sb[c].y, o[j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j) o[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].z, sb[c].z, o[j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < CBP; ++j) o[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].w, sb[c].w, o[j], 0, 0, 0);
+            }
+            if (ovalid) {
+#pragma unroll
+                for (int j = 0; j < CBP; ++j)
+                    st4(k.T + (size_t)vso * DO + (c0 + j) * 16 + q * 4, make_float4(o[j][0], o[j][1], o[j][2], o[j][3]));
+            }
+        }
+    }
+}
+
+template <int DI, int DO, int MODE>
+void launch_shape(const FK &k, int64_t ntiles, hipStream_t s)
+{
+    // d = 128: the 64 KB weight tile is shared by eight waves; one batch of
+    // rows per wave in flight keeps the gathered rows within the VGPR budget
+    constexpr int NWAVE = (DI == 128 || DO == 128) ? 8 : 4;
+    constexpr int KU = DI == 128 ? 1 : 2;
+    hipLaunchKernelGGL((af_fused_kernel<DI, DO, MODE, NWAVE, KU>), dim3((unsigned)ntiles),
+                       dim3(64 * NWAVE), 0, s, k);
+}
+
+template <int MODE>
+bool dispatch(int di, int dout, const FK &k, int64_t n, hipStream_t s)
+{
+    if (di == 64 && dout == 64) launch_shape<64, 64, MODE>(k, n, s);
+    else if (di == 128 && dout == 128) launch_shape<128, 128, MODE>(k, n, s);
+    else if constexpr (MODE == kModeMean) {   // RGCN only: RGAT needs d_in == d_out
+        if (di == 64 && dout == 128) launch_shape<64, 128, MODE>(k, n, s);
+        else if (di == 128 && dout == 64) launch_shape<128, 64, MODE>(k, n, s);
+        else return false;
+    } else {
+        return false;
+    }
+    return true;
+}
+
+}  // namespace
+
+rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s)
+{
+    const rgnn_graph *g = a.g;
+    if (g->n_tiles_fused == 0) return RGNN_OK;
+    FK k{};
+    k.rows = g->dev.fused_rows; k.tiles = g->dev.tiles_fused;
+    k.ntiles = g->n_tiles_fused; k.nedges = g->E; k.src = g->dev.fused_src;
+    k.h = a.h; k.W = a.W; k.wsp = a.wsp; k.vatt = a.vatt; k.slope = a.slope;
+    k.T = a.T; k.vstat = a.vstat;
+    if (a.softmax && (!a.wsp || !a.vatt || !a.vstat))
+        return fail(RGNN_EINVAL, "fused softmax aggregation needs wsp, vatt and vstat");
+    bool ok;
+    {
+        LaunchScope ls(a.softmax ? "rgat_af_fused" : "rgcn_af_fused", s);
+        ok = a.softmax ? dispatch<kModeSoftmax>(a.d_in, a.d_out, k, g->n_tiles_fused, s)
+                       : dispatch<kModeMean>(a.d_in, a.d_out, k, g->n_tiles_fused, s);
+    }
+    if (!ok) return fail(RGNN_EUNSUPPORTED, "fused aggregation: d_in, d_out must be 64 or 128");
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "af_fused launch");
+}
+
+}  // namespace rgnn

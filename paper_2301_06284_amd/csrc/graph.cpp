@@ -151,6 +151,48 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         for (int32_t r = 0; r < R; ++r) x.rel_vsegptr[r + 1] += x.rel_vsegptr[r];
         x.vsegdst_byrel.resize((size_t)g->V);
         for (int64_t i = 0; i < g->V; ++i) x.vsegdst_byrel[i] = x.vseg_dst[x.vseg_byrel[i]];
+        // fused aggregate-first order: by relation, then edge count (largest
+        // first), then id; tiles of consecutive rows of one relation, cut at
+        // kFusedTileRows rows or (after the first 16-row block) kFusedTileEdges
+        // edges
+        {
+            std::vector<int32_t> fperm((size_t)g->V), fkey((size_t)g->V);
+            for (int64_t i = 0; i < g->V; ++i) {
+                fperm[i] = (int32_t)i;
+                fkey[i] = C - (x.vseg_ptr[i + 1] - x.vseg_ptr[i]);
+            }
+            counting_sort(fperm, fkey.data(), C, tmp, cnt);
+            counting_sort(fperm, x.vseg_rel.data(), R, tmp, cnt);
+            x.fused_rows.resize((size_t)g->V);
+            x.fused_src.resize((size_t)E);
+            int32_t fpos = 0;
+            for (int64_t i = 0; i < g->V; ++i) {
+                const int32_t vs = fperm[i];
+                const int32_t b = x.vseg_ptr[vs], n = x.vseg_ptr[vs + 1] - b;
+                x.fused_rows[i] = FusedRow{vs, fpos, n, x.vseg_cnt[vs]};
+                for (int32_t j = 0; j < n; ++j) x.fused_src[(size_t)fpos + j] = x.in_src[(size_t)b + j];
+                fpos += n;
+            }
+            x.tiles_fused.clear();
+            for (int32_t r = 0; r < R; ++r) {
+                const int32_t end = x.rel_vsegptr[r + 1];
+                int32_t r0 = x.rel_vsegptr[r];
+                while (r0 < end) {
+                    int32_t rows = 0, edges = 0;
+                    while (rows < kFusedTileRows && r0 + rows < end) {
+                        const int32_t nb = std::min<int32_t>(16, end - (r0 + rows));
+                        int32_t be = 0;
+                        for (int32_t j = 0; j < nb; ++j) be += x.fused_rows[r0 + rows + j].ne;
+                        if (rows > 0 && edges + be > kFusedTileEdges) break;
+                        rows += nb;
+                        edges += be;
+                    }
+                    x.tiles_fused.push_back(Tile{r, r0, rows, x.fused_rows[r0].e0});
+                    r0 += rows;
+                }
+            }
+            g->n_tiles_fused = (int64_t)x.tiles_fused.size();
+        }
 
         // ---- traversal work items ----
         x.items.clear(); x.item_slot.clear(); x.split_dst.clear();
@@ -303,6 +345,9 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_nodes, x.tiles_nodes.data(), x.tiles_nodes.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_fused, x.tiles_fused.data(), x.tiles_fused.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.fused_rows, x.fused_rows.data(), x.fused_rows.size() * sizeof(FusedRow)});
+    add32(&d.fused_src, x.fused_src);
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
     add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});

@@ -14,6 +14,10 @@ __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 __device__ __forceinline__ float4 scale4(float4 a, float s) { return make_float4(a.x * s, a.y * s, a.z * s, a.w * s); }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float4 fma4(float4 a, float s, float4 c)
+{
+    return make_float4(a.x * s + c.x, a.y * s + c.y, a.z * s + c.z, a.w * s + c.w);
+}
 __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 {
     return make_float4(a.x * s + b.x * t, a.y * s + b.y * t, a.z * s + b.z * t, a.w * s + b.w * t);
@@ -88,11 +92,12 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
     for (int i = b + (int)threadIdx.x; i < e; i += 256) vscale[i] = __expf(vstat[(size_t)i * 2] - M) * Zi;
 }
 
-// out_v (+)= sum of the transformed segment rows of v (then optional ReLU).
+// out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
+// ReLU).
 template <int D>
 __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
-                                                          const float *T, float *out,
-                                                          int accumulate, int relu)
+                                                          const float *T, const float *scale,
+                                                          float *out, int accumulate, int relu)
 {
     constexpr int G = D / 4, GPB = 256 / G;
     const int gl = threadIdx.x % G;
@@ -101,7 +106,10 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     if (e - b > kBigRange) return;
     float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b; i < e; ++i) acc = add4(acc, ld4(T + (size_t)i * D + gl * 4));
+    for (int i = b; i < e; ++i) {
+        const float4 t = ld4(T + (size_t)i * D + gl * 4);
+        acc = scale ? fma4(t, scale[i], acc) : add4(acc, t);
+    }
     st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
 
@@ -111,8 +119,8 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32
 template <int D>
 __global__ __launch_bounds__(1024) void vseg_reduce_big_kernel(const int32_t *big_vdst,
                                                                const int32_t *dst_vsegptr,
-                                                               const float *T, float *out,
-                                                               int accumulate, int relu)
+                                                               const float *T, const float *scale,
+                                                               float *out, int accumulate, int relu)
 {
     constexpr int G = D / 4, NG = 1024 / G;
     __shared__ float4 part[NG * G];
@@ -120,7 +128,10 @@ __global__ __launch_bounds__(1024) void vseg_reduce_big_kernel(const int32_t *bi
     const int v = big_vdst[blockIdx.x];
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b + gi; i < e; i += NG) acc = add4(acc, ld4(T + (size_t)i * D + gl * 4));
+    for (int i = b + gi; i < e; i += NG) {
+        const float4 t = ld4(T + (size_t)i * D + gl * 4);
+        acc = scale ? fma4(t, scale[i], acc) : add4(acc, t);
+    }
     part[gi * G + gl] = acc;
     __syncthreads();
     if (gi == 0) {
@@ -351,8 +362,8 @@ rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s)
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_stats_big launch");
 }
 
-rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
-                               int accumulate, int relu, hipStream_t s)
+rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
+                               float *out, int accumulate, int relu, hipStream_t s)
 {
     if (g->N == 0) return RGNN_OK;
     if (d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 64 or 128");
@@ -361,10 +372,10 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float
         const unsigned nb = blocks_for(g->N, 256 / (d / 4));
         if (d == 64)
             hipLaunchKernelGGL((vseg_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, T, out, accumulate, relu);
+                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
         else
             hipLaunchKernelGGL((vseg_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, T, out, accumulate, relu);
+                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
     }
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "vseg_reduce launch");
@@ -374,10 +385,10 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float
         const unsigned nb = (unsigned)g->n_big_vdst;
         if (d == 64)
             hipLaunchKernelGGL((vseg_reduce_big_kernel<64>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, T, out, accumulate, relu);
+                               g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
         else
             hipLaunchKernelGGL((vseg_reduce_big_kernel<128>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, T, out, accumulate, relu);
+                               g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce_big launch");

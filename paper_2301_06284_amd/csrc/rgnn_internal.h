@@ -18,12 +18,22 @@ constexpr int kChunkEdges = 64;
 constexpr int kMaxDstPerItem = 32;
 // Rows of one typed-GEMM tile (a tile never mixes weight types).
 constexpr int kGemmTileRows = 512;
+// fused aggregate-first tiles: at most this many segments of one relation and,
+// beyond the first 16-row block, at most this many in-edges
+constexpr int kFusedTileRows = 256;
+constexpr int kFusedTileEdges = 4096;
 // Reductions over more records than this (partials of a split destination,
 // segments of one destination) get a whole workgroup instead of one group.
 constexpr int kBigRange = 32;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
+};
+
+struct FusedRow {      // one virtual segment in the fused aggregate-first order
+    int32_t vs;           // virtual segment id
+    int32_t e0, ne;       // its in-edges' sources at [e0, e0 + ne) of the fused source list
+    int32_t cnt;          // edge count of its whole (dst, rel) segment
 };
 
 struct Item {          // one traversal work item
@@ -46,6 +56,9 @@ struct HostIndex {
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
     std::vector<int32_t> big_seg;      // (dst, rel) segments with > kBigRange virtual segments
+    std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
+    std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
+    std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
     std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
@@ -70,6 +83,9 @@ struct DeviceIndex {
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr;
+    FusedRow *fused_rows = nullptr;
+    int32_t *fused_src = nullptr;
+    Tile *tiles_fused = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
     int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr, *out_rel = nullptr;
@@ -89,7 +105,7 @@ struct rgnn_graph {
     int32_t chunk = rgnn::kChunkEdges;
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
-    int64_t n_tiles_outer = 0;
+    int64_t n_tiles_outer = 0, n_tiles_fused = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
@@ -176,7 +192,6 @@ struct TravArgs {
     float *out = nullptr;                // [N, d]
     float *saved = nullptr;              // [N, heads, 2] or NULL
     float *partial = nullptr;            // [slots, 2*heads + d]
-    float *S = nullptr;                  // aggregate-first: [V, d] per-vseg sums
     float *vstat = nullptr;              // aggregate-first: [V, 2] per-vseg (max, sum)
     float *vatt = nullptr;               // [V, heads] destination attention term per vseg
     float *vscale = nullptr;             // aggregate-first: [V] softmax scale per vseg
@@ -185,9 +200,7 @@ struct TravArgs {
 // vatt[vs, k] = h_v . wtp[r, k] for every virtual segment (v, r).
 rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s);
-rgnn_status launch_rgcn_traverse_af(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s);
-rgnn_status launch_rgat_traverse_af(const TravArgs &a, hipStream_t s);
 // Finish destinations split over several work items: combine their partials
 // (softmax: (max, sum) per head then the D-vector; else the D-vector only).
 rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
@@ -196,8 +209,27 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 // Per-piece softmax scales (and, per destination, saved (max, sum)) from the
 // pieces' partial states; per_segment: softmax per (dst, rel) segment.
 rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s);
-rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, int d, float *out,
-                               int accumulate, int relu, hipStream_t s);
+// out_v (+)= sum over v's virtual segments of scale[vs] * T[vs] (scale NULL: 1).
+rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
+                               float *out, int accumulate, int relu, hipStream_t s);
+
+// Fused aggregate-first gather + segment sum + transform: per virtual segment
+// T[vs] = S_vs W_r with S_vs the segment's mean of h_u (softmax == 0) or its
+// exp-weighted sum relative to the segment's own logit maximum (softmax == 1,
+// one head; (max, sum) to vstat[vs]).
+struct FusedArgs {
+    const rgnn_graph *g = nullptr;
+    const float *h = nullptr;     // [N, d_in]
+    const float *W = nullptr;     // [R, d_in, d_out]
+    const float *wsp = nullptr;   // [R, d_in] W_r w_src[r] (softmax)
+    const float *vatt = nullptr;  // [V] destination terms (softmax)
+    float slope = 0.2f;
+    int d_in = 64, d_out = 64;
+    int softmax = 0;
+    float *T = nullptr;           // [V, d_out]
+    float *vstat = nullptr;       // [V, 2] (softmax)
+};
+rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s);
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);
 rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
 

@@ -55,11 +55,11 @@ struct TK {
     const Item *items;
     const int32_t *item_slot;
     const int32_t *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_cnt;
-    const int32_t *in_src, *e2u;
+    const int32_t *e2u;
     const float *h, *M, *atts, *wsp, *wtp;
     float *vatt;
     float slope;
-    float *out, *saved, *partial, *S, *vstat;
+    float *out, *saved, *partial;
     int relu;
 };
 
@@ -71,10 +71,10 @@ TK make_tk(const TravArgs &a)
     k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
     k.vseg_rel = g->dev.vseg_rel; k.vseg_cnt = g->dev.vseg_cnt;
-    k.in_src = g->dev.in_src; k.e2u = g->dev.e2u;
+    k.e2u = g->dev.e2u;
     k.h = a.h; k.M = a.M; k.atts = a.atts; k.wsp = a.wsp; k.wtp = a.wtp; k.vatt = a.vatt;
     k.slope = a.slope;
-    k.out = a.out; k.saved = a.saved; k.partial = a.partial; k.S = a.S; k.vstat = a.vstat;
+    k.out = a.out; k.saved = a.saved; k.partial = a.partial;
     k.relu = a.relu;
     return k;
 }
@@ -418,119 +418,6 @@ __global__ __launch_bounds__(256) void rgcn_tf_kernel(TK k)
     aggregate_item<D, 1, false>(k, it, st, k.M, gl, 0, 0.f, 0.f);
 }
 
-// ---------------------------------------------------------------- RGCN, aggregate-first
-// S[vs] = (1 / c_{v,r}) sum of h_u over the segment's edges.
-template <int D>
-__global__ __launch_bounds__(256) void rgcn_af_kernel(TK k)
-{
-    constexpr int G = D / 4, GPB = 256 / G;
-    __shared__ Stage<1> stage[GPB];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    Stage<1> &st = stage[gi];
-    const ItemHdr it = item_header(k, (int64_t)blockIdx.x * GPB + gi);
-    stage_item<G, 1, 1>(k, it, st, k.in_src, gl);
-    __syncthreads();
-    if (!it.valid || it.ne == 0) return;
-    int j = 0;
-    float4 acc = zero4();
-    float4 A[kU], B[kU];   // ping-pong row buffers, as in aggregate_item
-    auto load = [&](float4 (&X)[kU], int base) {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int e = base + u < it.ne ? base + u : it.ne - 1;
-            X[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
-        }
-    };
-    auto consume = [&](const float4 (&X)[kU], int base) {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int e = base + u;
-            if (e < it.ne) {
-                acc = lin4(acc, 1.f, X[u], 1.f);
-                if (e + 1 == st.vptr[j + 1]) {
-                    st4(k.S + (size_t)(it.vs0 + j) * D + gl * 4, scale4(acc, st.vw[j]));
-                    acc = zero4();
-                    ++j;
-                }
-            }
-        }
-    };
-    load(A, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
-        load(B, e0 + kU);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(A, e0);
-        load(A, e0 + 2 * kU);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(B, e0 + kU);
-    }
-}
-
-// ---------------------------------------------------------------- RGAT, aggregate-first
-// Gathers h_u, computes the source term h_u . (W_r w_src[r]) (reordered) per
-// edge and writes, per virtual segment, the exp-weighted feature sum S
-// (relative to the segment's own maximum) and its (max, sum).  W_r is applied
-// afterwards by the typed GEMM, whose per-row scale exp(m_seg - M_v) / Z_v
-// finishes the softmax.
-template <int D>
-__global__ __launch_bounds__(256) void rgat_af_kernel(TK k)
-{
-    constexpr int G = D / 4, GPB = 256 / G;
-    __shared__ Stage<1> stage[GPB];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    Stage<1> &st = stage[gi];
-    const ItemHdr it = item_header(k, (int64_t)blockIdx.x * GPB + gi);
-    stage_item<G, 1, 0>(k, it, st, k.in_src, gl);
-    __syncthreads();
-    if (!it.valid || it.ne == 0) return;
-    int j = 0;
-    float m = -INFINITY, s = 0.f;
-    float4 acc = zero4();
-    // ping-pong buffers of gathered rows and their relations' w_src vectors
-    float4 A[kU], Aw[kU], B[kU], Bw[kU];
-    auto load = [&](float4 (&X)[kU], float4 (&Xw)[kU], int base) {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int e = base + u < it.ne ? base + u : it.ne - 1;
-            X[u] = ld4(k.h + (size_t)st.eidx[e] * D + gl * 4);
-            Xw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
-        }
-    };
-    auto consume = [&](const float4 (&X)[kU], const float4 (&Xw)[kU], int base) {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int e = base + u;
-            const float atts = gsum<G>(dot4(X[u], Xw[u]));
-            if (e < it.ne) {
-                const float z = leaky(atts + st.vw[j], k.slope);
-                const float mn = fmaxf(m, z);
-                const float c1 = __expf(m - mn), c2 = __expf(z - mn);
-                s = s * c1 + c2;
-                acc = lin4(acc, c1, X[u], c2);
-                m = mn;
-                if (e + 1 == st.vptr[j + 1]) {
-                    const size_t vs = (size_t)it.vs0 + j;
-                    st4(k.S + vs * D + gl * 4, acc);
-                    if (gl == 0) { k.vstat[vs * 2] = m; k.vstat[vs * 2 + 1] = s; }
-                    m = -INFINITY; s = 0.f; acc = zero4();
-                    ++j;
-                }
-            }
-        }
-    };
-    load(A, Aw, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int e0 = 0; e0 < it.ne; e0 += 2 * kU) {
-        load(B, Bw, e0 + kU);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(A, Aw, e0);
-        load(A, Aw, e0 + 2 * kU);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(B, Bw, e0 + kU);
-    }
-}
-
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 
 }  // namespace
@@ -580,20 +467,6 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "rgat_tf launch");
 }
 
-rgnn_status launch_rgat_traverse_af(const TravArgs &a, hipStream_t s)
-{
-    if (a.g->n_items == 0) return RGNN_OK;
-    if (a.heads != 1) return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs heads == 1");
-    TK k = make_tk(a);
-    LaunchScope ls("rgat_traverse_af", s);
-    const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
-    if (a.d == 64) hipLaunchKernelGGL((rgat_af_kernel<64>), dim3(nb), dim3(256), 0, s, k);
-    else if (a.d == 128) hipLaunchKernelGGL((rgat_af_kernel<128>), dim3(nb), dim3(256), 0, s, k);
-    else return fail(RGNN_EUNSUPPORTED, "RGAT traversal: d must be 64 or 128");
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "rgat_af launch");
-}
-
 rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s)
 {
     if (a.g->n_items == 0) return RGNN_OK;
@@ -605,19 +478,6 @@ rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s)
     else return fail(RGNN_EUNSUPPORTED, "RGCN traversal: d must be 64 or 128");
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "rgcn_tf launch");
-}
-
-rgnn_status launch_rgcn_traverse_af(const TravArgs &a, hipStream_t s)
-{
-    if (a.g->n_items == 0) return RGNN_OK;
-    TK k = make_tk(a);
-    LaunchScope ls("rgcn_traverse_af", s);
-    const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
-    if (a.d == 64) hipLaunchKernelGGL((rgcn_af_kernel<64>), dim3(nb), dim3(256), 0, s, k);
-    else if (a.d == 128) hipLaunchKernelGGL((rgcn_af_kernel<128>), dim3(nb), dim3(256), 0, s, k);
-    else return fail(RGNN_EUNSUPPORTED, "RGCN traversal: d must be 64 or 128");
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "rgcn_af launch");
 }
 
 }  // namespace rgnn
