@@ -117,7 +117,7 @@ int resolve_plan(const rgnn_graph *g, int layer, int d_in, int d_out, int H, int
 }
 
 // ---- workspace layouts ----
-struct RgcnWs { float *M, *partial, *S, *T; };
+struct RgcnWs { float *M, *partial, *T; };
 size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *base, RgcnWs *w)
 {
     Carver c(base);
@@ -132,7 +132,7 @@ size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *bas
     return c.off;
 }
 
-struct RgatWs { float *M, *atts, *wsp, *wtp, *vatt, *partial, *S, *vstat, *vscale, *T, *saved; };
+struct RgatWs { float *M, *atts, *wsp, *wtp, *vatt, *partial, *vstat, *vscale, *T; };
 size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, void *base,
                    RgatWs *w)
 {
@@ -149,7 +149,6 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
         x.vstat = c.take<float>((size_t)g->V * 2);
         x.vscale = c.take<float>((size_t)g->V);
         x.T = c.take<float>((size_t)g->V * d_out);
-        x.saved = c.take<float>((size_t)g->N * 2);
     }
     if (w) *w = x;
     return c.off;
@@ -426,10 +425,14 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         fa.g = g; fa.h = h; fa.W = W; fa.wsp = w.wsp; fa.vatt = w.vatt; fa.slope = neg_slope;
         fa.d_in = d_in; fa.d_out = d_out; fa.softmax = 1; fa.T = w.T; fa.vstat = w.vstat;
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
-        TravArgs ta;
-        ta.g = g; ta.vstat = w.vstat; ta.saved = saved ? saved : w.saved; ta.vscale = w.vscale;
-        if ((st = launch_vseg_stats(ta, per_seg, s)) != RGNN_OK) return st;
-        if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
+        if (per_seg) {
+            TravArgs ta;
+            ta.g = g; ta.vstat = w.vstat; ta.vscale = w.vscale;
+            if ((st = launch_seg_softmax_scale(ta, s)) != RGNN_OK) return st;
+            if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
+        } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, s)) != RGNN_OK) {
+            return st;
+        }
     }
     return RGNN_OK;
 }

@@ -1,10 +1,11 @@
 // reduce.hip -- per-destination reductions and small helpers of the layers:
 // merging the partial softmax states of destinations split over several work
-// items, per-destination softmax statistics and sums over (dst, rel) segment
-// rows for the aggregate-first plan, the reordered attention vectors
+// items, softmax statistics and sums over (dst, rel) segment rows for the
+// aggregate-first plan, the reordered attention vectors
 // W_r w[r] (linear operator reordering), fill / ReLU / add.
 // Every reduction runs in a fixed order, so results are reproducible bit for bit.
 #include "rgnn_internal.h"
+#include "wave_ops.h"
 
 namespace rgnn {
 
@@ -27,16 +28,12 @@ __device__ __forceinline__ float4 relu4(float4 a)
     return make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
 }
 
-// Destinations with more than kBigRange segments are left to the block kernel.
-// Also writes, per segment, the scale exp(m_seg - M_v) / Z_v that finishes the
-// softmax when the typed GEMM applies W_r to the segment's sum.
-// Softmax groups are runs of consecutive virtual segments: those of one
-// destination (softmax per destination) or of one (dst, rel) segment (softmax
-// per destination and relation), given by the offsets grp_vsegptr.  saved
-// (per group: max, denominator) may be NULL.
+// Softmax per (dst, rel) segment: a segment longer than kChunkEdges is cut into
+// several virtual segments, each with its own (max m_i, sum s_i); per virtual
+// segment the scale exp(m_i - M) / Z of its (dst, rel) segment is written.
+// Segments with more than kBigRange pieces are left to the block kernel.
 __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *grp_vsegptr,
-                                                         const float *vstat, float *saved,
-                                                         float *vscale)
+                                                         const float *vstat, float *vscale)
 {
     const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (v >= N) return;
@@ -46,10 +43,6 @@ __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_
     for (int i = b; i < e; ++i) M = fmaxf(M, vstat[(size_t)i * 2]);
     float Z = 0.f;
     for (int i = b; i < e; ++i) Z += vstat[(size_t)i * 2 + 1] * __expf(vstat[(size_t)i * 2] - M);
-    if (saved) {
-        saved[v * 2] = b < e ? M : 0.f;
-        saved[v * 2 + 1] = Z;
-    }
     for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)i * 2] - M) / Z;
 }
 
@@ -57,8 +50,7 @@ __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_
 // (max, sum), combined in thread order through LDS.
 __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_grp,
                                                              const int32_t *grp_vsegptr,
-                                                             const float *vstat, float *saved,
-                                                             float *vscale)
+                                                             const float *vstat, float *vscale)
 {
     __shared__ float sm[256], ss[256];
     __shared__ float fin[2];
@@ -80,10 +72,6 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
         float Z = 0.f;
         for (int t = 0; t < 256; ++t)
             if (ss[t] > 0.f) Z += ss[t] * __expf(sm[t] - M);
-        if (saved) {
-            saved[(size_t)v * 2] = M;
-            saved[(size_t)v * 2 + 1] = Z;
-        }
         fin[0] = M;
         fin[1] = Z;
     }
@@ -138,6 +126,104 @@ __global__ __launch_bounds__(1024) void vseg_reduce_big_kernel(const int32_t *bi
         float4 tot = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
         for (int j = 0; j < NG; ++j) tot = add4(tot, part[j * G + gl]);
         st4(out + (size_t)v * D + gl * 4, relu ? relu4(tot) : tot);
+    }
+}
+
+// ---------------------------------------------------------------- softmax reduction
+// Softmax per destination finished and summed in one pass: per destination v
+// with segments i (each with its own logit maximum m_i, sum s_i and
+// exp-weighted transformed row T_i relative to m_i):
+//   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
+// and saved[v] = (M, Z) ((0, 0) without in-edges).  A group of D/4 lanes per
+// destination; the statistics are taken over the group's lanes (fixed
+// butterfly), the rows summed in segment order.
+template <int D>
+__global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
+                                                             const float *vstat, const float *T,
+                                                             float *out, float *saved)
+{
+    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int NE = (kBigRange + G - 1) / G;   // statistics entries per lane
+    const int gl = threadIdx.x % G;
+    const int64_t v = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
+    if (v >= N) return;
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    if (e - b > kBigRange) return;
+    float mi[NE], si[NE];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) {
+        const int i = b + gl + j * G;
+        const float2 st = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2)
+                                : make_float2(-INFINITY, 0.f);
+        mi[j] = st.x;
+        si[j] = st.y;
+    }
+    float M = mi[0];
+#pragma unroll
+    for (int j = 1; j < NE; ++j) M = fmaxf(M, mi[j]);
+    M = gmax<G>(M);
+    float z = 0.f;
+#pragma unroll
+    for (int j = 0; j < NE; ++j) z += si[j] > 0.f ? si[j] * __expf(mi[j] - M) : 0.f;
+    const float Z = gsum<G>(z);
+    if (saved && gl == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(b < e ? M : 0.f, Z);
+    const float inv = Z > 0.f ? 1.f / Z : 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = b; i < e; ++i)
+        acc = fma4(ld4(T + (size_t)i * D + gl * 4), __expf(vstat[(size_t)i * 2] - M) * inv, acc);
+    st4(out + (size_t)v * D + gl * 4, acc);
+}
+
+// The same for destinations with more than kBigRange segments, one 1024-thread
+// workgroup each: maximum and denominator by workgroup reductions, then every
+// group of D/4 lanes sums a strided subset of the rows and the group sums are
+// added in group order.
+template <int D>
+__global__ __launch_bounds__(1024) void softmax_reduce_big_kernel(const int32_t *big_vdst,
+                                                                  const int32_t *dst_vsegptr,
+                                                                  const float *vstat, const float *T,
+                                                                  float *out, float *saved)
+{
+    constexpr int G = D / 4, NG = 1024 / G;
+    __shared__ float red[16];
+    __shared__ float4 part[NG * G];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int gl = tid % G, gi = tid / G;
+    const int v = big_vdst[blockIdx.x];
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    // maximum
+    float m = -INFINITY;
+    for (int i = b + tid; i < e; i += 1024) m = fmaxf(m, vstat[(size_t)i * 2]);
+    m = gmax<32>(m);
+    m = fmaxf(m, __shfl_xor(m, 32));
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    float M = red[0];
+    for (int w = 1; w < 16; ++w) M = fmaxf(M, red[w]);
+    __syncthreads();
+    // denominator
+    float z = 0.f;
+    for (int i = b + tid; i < e; i += 1024) {
+        const float2 st = *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2);
+        z += st.y * __expf(st.x - M);
+    }
+    z = gsum<32>(z);
+    z += __shfl_xor(z, 32);
+    if (lane == 0) red[wave] = z;
+    __syncthreads();
+    float Z = 0.f;
+    for (int w = 0; w < 16; ++w) Z += red[w];
+    if (saved && tid == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(M, Z);
+    const float inv = 1.f / Z;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = b + gi; i < e; i += NG)
+        acc = fma4(ld4(T + (size_t)i * D + gl * 4), __expf(vstat[(size_t)i * 2] - M) * inv, acc);
+    part[gi * G + gl] = acc;
+    __syncthreads();
+    if (gi == 0) {
+        float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < NG; ++j) tot = add4(tot, part[j * G + gl]);
+        st4(out + (size_t)v * D + gl * 4, tot);
     }
 }
 
@@ -335,31 +421,25 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "merge_big launch");
 }
 
-rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s)
+rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
 {
     const rgnn_graph *g = a.g;
-    // softmax groups: destinations, or (dst, rel) segments
-    const int64_t n = per_segment ? g->U_dst : g->N;
-    const int32_t *ptr = per_segment ? g->dev.seg_vsegptr : g->dev.dst_vsegptr;
-    const int32_t *big = per_segment ? g->dev.big_seg : g->dev.big_vdst;
-    const int64_t nbig = per_segment ? g->n_big_seg : g->n_big_vdst;
-    float *saved = per_segment ? nullptr : a.saved;
-    if (n == 0) return RGNN_OK;
+    if (g->U_dst == 0) return RGNN_OK;
     {
-        LaunchScope ls("vseg_stats", s);
-        hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, n, ptr, a.vstat,
-                           saved, a.vscale);
+        LaunchScope ls("seg_softmax_scale", s);
+        hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(g->U_dst, 256)), dim3(256), 0, s, g->U_dst,
+                           g->dev.seg_vsegptr, a.vstat, a.vscale);
     }
     hipError_t e = last();
-    if (e != hipSuccess) return hip_fail(e, "vseg_stats launch");
-    if (nbig == 0) return RGNN_OK;
+    if (e != hipSuccess) return hip_fail(e, "seg_softmax_scale launch");
+    if (g->n_big_seg == 0) return RGNN_OK;
     {
-        LaunchScope ls("vseg_stats_big", s);
-        hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)nbig), dim3(256), 0, s, big, ptr, a.vstat,
-                           saved, a.vscale);
+        LaunchScope ls("seg_softmax_scale_big", s);
+        hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)g->n_big_seg), dim3(256), 0, s,
+                           g->dev.big_seg, g->dev.seg_vsegptr, a.vstat, a.vscale);
     }
     e = last();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_stats_big launch");
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_softmax_scale_big launch");
 }
 
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
@@ -392,6 +472,38 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce_big launch");
+}
+
+rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
+                                  float *out, float *saved, hipStream_t s)
+{
+    if (g->N == 0) return RGNN_OK;
+    if (d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 64 or 128");
+    {
+        LaunchScope ls("softmax_reduce", s);
+        const unsigned nb = blocks_for(g->N, 256 / (d / 4));
+        if (d == 64)
+            hipLaunchKernelGGL((softmax_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, vstat, T, out, saved);
+        else
+            hipLaunchKernelGGL((softmax_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, vstat, T, out, saved);
+    }
+    hipError_t e = last();
+    if (e != hipSuccess) return hip_fail(e, "softmax_reduce launch");
+    if (g->n_big_vdst == 0) return RGNN_OK;
+    {
+        LaunchScope ls("softmax_reduce_big", s);
+        const unsigned nb = (unsigned)g->n_big_vdst;
+        if (d == 64)
+            hipLaunchKernelGGL((softmax_reduce_big_kernel<64>), dim3(nb), dim3(1024), 0, s,
+                               g->dev.big_vdst, g->dev.dst_vsegptr, vstat, T, out, saved);
+        else
+            hipLaunchKernelGGL((softmax_reduce_big_kernel<128>), dim3(nb), dim3(1024), 0, s,
+                               g->dev.big_vdst, g->dev.dst_vsegptr, vstat, T, out, saved);
+    }
+    e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "softmax_reduce_big launch");
 }
 
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s)

@@ -206,12 +206,18 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s);
 rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
                                   const float *partial, float *out, float *saved, int relu,
                                   hipStream_t s);
-// Per-piece softmax scales (and, per destination, saved (max, sum)) from the
-// pieces' partial states; per_segment: softmax per (dst, rel) segment.
-rgnn_status launch_vseg_stats(const TravArgs &a, int per_segment, hipStream_t s);
+// Softmax per (dst, rel) segment: per virtual segment the scale
+// exp(m_i - M_seg) / Z_seg from the pieces' (max, sum) in a.vstat, to a.vscale.
+rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s);
 // out_v (+)= sum over v's virtual segments of scale[vs] * T[vs] (scale NULL: 1).
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
                                float *out, int accumulate, int relu, hipStream_t s);
+
+// Softmax per destination finished from the per-segment (max, sum) in vstat
+// and the segments' transformed rows summed: out_v = sum_i exp(m_i - M_v) / Z_v
+// * T_i; saved[v] = (M_v, Z_v) when saved is not NULL.
+rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
+                                  float *out, float *saved, hipStream_t s);
 
 // Fused aggregate-first gather + segment sum + transform: per virtual segment
 // T[vs] = S_vs W_r with S_vs the segment's mean of h_u (softmax == 0) or its
