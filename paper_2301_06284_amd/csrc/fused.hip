@@ -185,7 +185,8 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
         };
         auto consume = [&](const float4 (&X)[KU][2][CH], int t) {
 #pragma unroll
-            for (int u = 0; u < KU; ++u)
+            for (int u = 0; u < KU; ++u) {
+                if (t + u >= nmax) break;   // past every row of the block (uniform)
 #pragma unroll
                 for (int h2 = 0; h2 < 2; ++h2) {
                     const float4 *x = X[u][h2];
@@ -196,9 +197,13 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                             p += dot4(x[c], *reinterpret_cast<const float4 *>(&wsl[c * 32 + gp * 4]));
                         p = gsum<8>(p);   // the row's eight lanes: identical sums
                         if (t + u < fr[h2].ne) {
+                            // online update with one exponential: the smaller of
+                            // the old maximum and z is scaled by exp(-|z - m|)
                             const float z = leaky(p + va[h2], k.slope);
-                            const float mn = fmaxf(m[h2], z);
-                            const float c1 = __expf(m[h2] - mn), c2 = __expf(z - mn);
+                            const bool up = z > m[h2];
+                            const float ex = __expf(up ? m[h2] - z : z - m[h2]);
+                            const float c1 = up ? ex : 1.f, c2 = up ? 1.f : ex;
+                            const float mn = up ? z : m[h2];
                             s[h2] = s[h2] * c1 + c2;
 #pragma unroll
                             for (int c = 0; c < CH; ++c) {
@@ -216,14 +221,19 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                         }
                     }
                 }
+            }
         };
+        // batches past the block's longest segment are neither loaded nor
+        // consumed (wave-uniform tests)
         load(A, 0);
         __builtin_amdgcn_sched_barrier(0);
         for (int t = 0; t < nmax; t += 2 * KU) {
-            load(B, t + KU);
+            const bool more_b = t + KU < nmax;
+            if (more_b) load(B, t + KU);
             __builtin_amdgcn_sched_barrier(0);
             consume(A, t);
-            load(A, t + 2 * KU);
+            if (!more_b) break;
+            if (t + 2 * KU < nmax) load(A, t + 2 * KU);
             __builtin_amdgcn_sched_barrier(0);
             consume(B, t + KU);
         }
@@ -256,8 +266,6 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
             const float w0 = __shfl(a0.w, sl), w1 = __shfl(a1.w, sl);
             sb[c] = make_float4(hi ? x1 : x0, hi ? y1 : y0, hi ? z1 : z0, hi ? w1 : w0);
         }
-        const bool ovalid = rb * 16 + li < tile.rows;
-        const int vso = srow[ovalid ? rb * 16 + li : rb * 16].vs;
 
         // T = S W_r on the matrix cores: A = W_r^T fragments from LDS, B = the
         // row sums (k-slot q of step (c, j) is feature 16c + 4q + j for both)
@@ -281,10 +289,26 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
 #pragma unroll
                 for (int j = 0; j < CBP; ++j) o[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[j].w, sb[c].w, o[j], 0, 0, 0);
             }
-            if (ovalid) {
+            // back to the row layout for the stores (whole 128-byte lines per
+            // instruction): lane (gr, gp) takes features 32c' + 4gp .. +3 of
+            // rows gr and gr + 8, held by lane row + 16 (gp % 4) in column
+            // block 2c' + gp / 4
 #pragma unroll
-                for (int j = 0; j < CBP; ++j)
-                    st4(k.T + (size_t)vso * DO + (c0 + j) * 16 + q * 4, make_float4(o[j][0], o[j][1], o[j][2], o[j][3]));
+            for (int cc = 0; cc < CBP / 2; ++cc) {
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    const int sl = gr + 8 * h2 + 16 * (gp & 3);
+                    const floatx4 lo = o[2 * cc], hi4 = o[2 * cc + 1];
+                    float v[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float a = __shfl(lo[t], sl), b = __shfl(hi4[t], sl);
+                        v[t] = gp >= 4 ? b : a;
+                    }
+                    if (valid[h2])
+                        st4(k.T + (size_t)fr[h2].vs * DO + (c0 / 2 + cc) * 32 + gp * 4,
+                            make_float4(v[0], v[1], v[2], v[3]));
+                }
             }
         }
     }

@@ -94,31 +94,53 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     if (e - b > kBigRange) return;
     float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b; i < e; ++i) {
-        const float4 t = ld4(T + (size_t)i * D + gl * 4);
-        acc = scale ? fma4(t, scale[i], acc) : add4(acc, t);
+    // rows in batches of four (all in flight together), summed in segment order
+    for (int i0 = b; i0 < e; i0 += 4) {
+        float4 t[4];
+        float sc[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (i0 + u < e) {
+                t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
+                sc[u] = scale ? scale[i0 + u] : 1.f;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < e) acc = scale ? fma4(t[u], sc[u], acc) : add4(acc, t[u]);
     }
     st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
 
-// One 1024-thread workgroup per destination with many segments: every group
-// of D/4 lanes sums a strided subset of the rows, the group sums are then
-// added in group order.
-template <int D>
-__global__ __launch_bounds__(1024) void vseg_reduce_big_kernel(const int32_t *big_vdst,
-                                                               const int32_t *dst_vsegptr,
-                                                               const float *T, const float *scale,
-                                                               float *out, int accumulate, int relu)
+// One workgroup of NTH threads per destination with many segments: every
+// group of D/4 lanes sums a strided subset of the rows (U in flight), the
+// group sums are then added in group order.
+template <int D, int NTH, int U>
+__global__ __launch_bounds__(NTH) void vseg_reduce_big_kernel(const int32_t *big_vdst,
+                                                              const int32_t *dst_vsegptr,
+                                                              const float *T, const float *scale,
+                                                              float *out, int accumulate, int relu)
 {
-    constexpr int G = D / 4, NG = 1024 / G;
+    constexpr int G = D / 4, NG = NTH / G;
     __shared__ float4 part[NG * G];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     const int v = big_vdst[blockIdx.x];
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b + gi; i < e; i += NG) {
-        const float4 t = ld4(T + (size_t)i * D + gl * 4);
-        acc = scale ? fma4(t, scale[i], acc) : add4(acc, t);
+    for (int i0 = b + gi; i0 < e; i0 += U * NG) {
+        float4 t[U];
+        float sc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * NG;
+            if (i < e) {
+                t[u] = ld4(T + (size_t)i * D + gl * 4);
+                sc[u] = scale ? scale[i] : 1.f;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (i0 + u * NG < e) acc = scale ? fma4(t[u], sc[u], acc) : add4(acc, t[u]);
     }
     part[gi * G + gl] = acc;
     __syncthreads();
@@ -168,56 +190,95 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const in
     const float Z = gsum<G>(z);
     if (saved && gl == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(b < e ? M : 0.f, Z);
     const float inv = Z > 0.f ? 1.f / Z : 0.f;
+    // rows in batches of four (all in flight together), summed in segment order
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b; i < e; ++i)
-        acc = fma4(ld4(T + (size_t)i * D + gl * 4), __expf(vstat[(size_t)i * 2] - M) * inv, acc);
+    for (int i0 = b; i0 < e; i0 += 4) {
+        float4 t[4];
+        float mu[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (i0 + u < e) {
+                t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
+                mu[u] = vstat[(size_t)(i0 + u) * 2];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < e) acc = fma4(t[u], __expf(mu[u] - M) * inv, acc);
+    }
     st4(out + (size_t)v * D + gl * 4, acc);
 }
 
-// The same for destinations with more than kBigRange segments, one 1024-thread
-// workgroup each: maximum and denominator by workgroup reductions, then every
-// group of D/4 lanes sums a strided subset of the rows and the group sums are
-// added in group order.
-template <int D>
-__global__ __launch_bounds__(1024) void softmax_reduce_big_kernel(const int32_t *big_vdst,
-                                                                  const int32_t *dst_vsegptr,
-                                                                  const float *vstat, const float *T,
-                                                                  float *out, float *saved)
+// The same for destinations with more than kBigRange segments, one workgroup
+// of NTH threads each: every thread folds its strided share of the (max, sum)
+// pairs into one online pair (four loads in flight), the maximum and the
+// denominator follow by workgroup reductions; then every group of D/4 lanes
+// sums a strided subset of the rows (U in flight) and the group sums are added
+// in group order.
+template <int D, int NTH, int U>
+__global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *big_vdst,
+                                                                 const int32_t *dst_vsegptr,
+                                                                 const float *vstat, const float *T,
+                                                                 float *out, float *saved)
 {
-    constexpr int G = D / 4, NG = 1024 / G;
-    __shared__ float red[16];
+    constexpr int G = D / 4, NG = NTH / G, NWV = NTH / 64;
+    __shared__ float red[NWV];
     __shared__ float4 part[NG * G];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int gl = tid % G, gi = tid / G;
     const int v = big_vdst[blockIdx.x];
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    float ml = -INFINITY, zl = 0.f;
+    for (int i0 = b + tid; i0 < e; i0 += 4 * NTH) {
+        float2 st[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * NTH;
+            st[u] = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2) : make_float2(-INFINITY, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (st[u].y > 0.f) {
+                const float mn = fmaxf(ml, st[u].x);
+                zl = zl * __expf(ml - mn) + st[u].y * __expf(st[u].x - mn);
+                ml = mn;
+            }
+        }
+    }
     // maximum
-    float m = -INFINITY;
-    for (int i = b + tid; i < e; i += 1024) m = fmaxf(m, vstat[(size_t)i * 2]);
-    m = gmax<32>(m);
+    float m = gmax<32>(ml);
     m = fmaxf(m, __shfl_xor(m, 32));
     if (lane == 0) red[wave] = m;
     __syncthreads();
     float M = red[0];
-    for (int w = 1; w < 16; ++w) M = fmaxf(M, red[w]);
+    for (int w = 1; w < NWV; ++w) M = fmaxf(M, red[w]);
     __syncthreads();
     // denominator
-    float z = 0.f;
-    for (int i = b + tid; i < e; i += 1024) {
-        const float2 st = *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2);
-        z += st.y * __expf(st.x - M);
-    }
+    float z = zl > 0.f ? zl * __expf(ml - M) : 0.f;
     z = gsum<32>(z);
     z += __shfl_xor(z, 32);
     if (lane == 0) red[wave] = z;
     __syncthreads();
     float Z = 0.f;
-    for (int w = 0; w < 16; ++w) Z += red[w];
+    for (int w = 0; w < NWV; ++w) Z += red[w];
     if (saved && tid == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(M, Z);
     const float inv = 1.f / Z;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = b + gi; i < e; i += NG)
-        acc = fma4(ld4(T + (size_t)i * D + gl * 4), __expf(vstat[(size_t)i * 2] - M) * inv, acc);
+    for (int i0 = b + gi; i0 < e; i0 += U * NG) {
+        float4 t[U];
+        float mu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * NG;
+            if (i < e) {
+                t[u] = ld4(T + (size_t)i * D + gl * 4);
+                mu[u] = vstat[(size_t)i * 2];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (i0 + u * NG < e) acc = fma4(t[u], __expf(mu[u] - M) * inv, acc);
+    }
     part[gi * G + gl] = acc;
     __syncthreads();
     if (gi == 0) {
@@ -460,15 +521,23 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "vseg_reduce launch");
     if (g->n_big_vdst == 0) return RGNN_OK;
+    const int64_t nmid = g->n_big_vdst - g->n_huge_vdst, nhuge = g->n_huge_vdst;
+    const int32_t *huge = g->dev.big_vdst + nmid;
     {
-        LaunchScope ls("vseg_reduce_big", s);
-        const unsigned nb = (unsigned)g->n_big_vdst;
-        if (d == 64)
-            hipLaunchKernelGGL((vseg_reduce_big_kernel<64>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
-        else
-            hipLaunchKernelGGL((vseg_reduce_big_kernel<128>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
+#define VRB(D, NTH, L, NB) hipLaunchKernelGGL((vseg_reduce_big_kernel<D, NTH, NTH == 1024 ? 16 : 4>), \
+                                              dim3((unsigned)(NB)), dim3(NTH), \
+                                              0, s, L, g->dev.dst_vsegptr, T, scale, out, accumulate, relu)
+        if (nmid) {
+            LaunchScope ls("vseg_reduce_big", s);
+            if (d == 64) VRB(64, 256, g->dev.big_vdst, nmid);
+            else VRB(128, 256, g->dev.big_vdst, nmid);
+        }
+        if (nhuge) {
+            LaunchScope ls("vseg_reduce_huge", s);
+            if (d == 64) VRB(64, 1024, huge, nhuge);
+            else VRB(128, 1024, huge, nhuge);
+        }
+#undef VRB
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce_big launch");
@@ -492,15 +561,22 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "softmax_reduce launch");
     if (g->n_big_vdst == 0) return RGNN_OK;
+    const int64_t nmid = g->n_big_vdst - g->n_huge_vdst, nhuge = g->n_huge_vdst;
+    const int32_t *huge = g->dev.big_vdst + nmid;
     {
-        LaunchScope ls("softmax_reduce_big", s);
-        const unsigned nb = (unsigned)g->n_big_vdst;
-        if (d == 64)
-            hipLaunchKernelGGL((softmax_reduce_big_kernel<64>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, vstat, T, out, saved);
-        else
-            hipLaunchKernelGGL((softmax_reduce_big_kernel<128>), dim3(nb), dim3(1024), 0, s,
-                               g->dev.big_vdst, g->dev.dst_vsegptr, vstat, T, out, saved);
+#define SRB(D, NTH, L, NB) hipLaunchKernelGGL((softmax_reduce_big_kernel<D, NTH, NTH == 1024 ? 16 : 4>), dim3((unsigned)(NB)), \
+                                              dim3(NTH), 0, s, L, g->dev.dst_vsegptr, vstat, T, out, saved)
+        if (nmid) {
+            LaunchScope ls("softmax_reduce_big", s);
+            if (d == 64) SRB(64, 256, g->dev.big_vdst, nmid);
+            else SRB(128, 256, g->dev.big_vdst, nmid);
+        }
+        if (nhuge) {
+            LaunchScope ls("softmax_reduce_huge", s);
+            if (d == 64) SRB(64, 1024, huge, nhuge);
+            else SRB(128, 1024, huge, nhuge);
+        }
+#undef SRB
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "softmax_reduce_big launch");

@@ -149,6 +149,25 @@ def test_rgat_per_relation_softmax_big_segment():
     assert row_err(got, ref) <= TOL
 
 
+@pytest.mark.parametrize("R", [1, 3])
+def test_huge_hub(R):
+    """A destination with more than 512 virtual segments (the 1024-thread
+    reductions) beside ones with 33..512 (the 256-thread reductions), through
+    every plan of RGCN and RGAT."""
+    g = graph("hub", seed=24, N=200, E=70000, R=R)
+    t = workloads.tiny_tensors(24, g, 64, 64, att_var=1.0)
+    print(f"huge hub R={R}", flush=True)
+    run = Runner(g, t)
+    ref_gcn = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])
+    ref_gat = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"])
+    for plan in (1, 2):
+        assert row_err(run.rgcn(plan=plan), ref_gcn) <= TOL
+        assert row_err(run.rgat(plan=plan), ref_gat) <= TOL
+    ref_rel = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1)
+    assert row_err(run.rgat(scope=1), ref_rel) <= TOL
+    run.close()
+
+
 def test_rgat_per_relation_softmax_rejects():
     import torch
     from paper_2301_06284_amd import rgnn
