@@ -392,7 +392,11 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     hipStream_t s = (hipStream_t)stream;
     // linear operator reordering: W_r w_dst[r] (and W_r w_src[r]) once per relation,
     // then the destination term h_v . (W_r w_dst[r]) once per (dst, rel) segment
-    if ((st = launch_reorder_vec(W, w_dst, g->R, d_in, d_out, heads, w.wtp, s)) != RGNN_OK) return st;
+    // (aggregate-first also needs W_r w_src[r]: both in one launch)
+    const bool af = plan == RGNN_PLAN_AGGREGATE_FIRST;
+    if ((st = launch_reorder_vec(W, g->R, d_in, d_out, heads, w_dst, w.wtp, af ? w_src : nullptr,
+                                 af ? w.wsp : nullptr, s)) != RGNN_OK)
+        return st;
     {
         TravArgs ta;
         ta.g = g; ta.h = h; ta.wtp = w.wtp; ta.heads = heads; ta.d = d_in; ta.vatt = w.vatt;
@@ -420,7 +424,6 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         // fused gather + per-segment online softmax + W_r per virtual segment;
         // the softmax is finished per destination (or per segment) when the
         // segments are summed
-        if ((st = launch_reorder_vec(W, w_src, g->R, d_in, d_out, 1, w.wsp, s)) != RGNN_OK) return st;
         FusedArgs fa;
         fa.g = g; fa.h = h; fa.W = W; fa.wsp = w.wsp; fa.vatt = w.vatt; fa.slope = neg_slope;
         fa.d_in = d_in; fa.d_out = d_out; fa.softmax = 1; fa.T = w.T; fa.vstat = w.vstat;

@@ -696,8 +696,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     bwd_layout(g, ws, &w);
     rgnn_status st;
     hipError_t e;
-    if ((st = launch_reorder_vec(W, w_src, g->R, D, D, 1, w.wsp, s)) != RGNN_OK) return st;
-    if ((st = launch_reorder_vec(W, w_dst, g->R, D, D, 1, w.wtp, s)) != RGNN_OK) return st;
+    if ((st = launch_reorder_vec(W, g->R, D, D, 1, w_src, w.wsp, w_dst, w.wtp, s)) != RGNN_OK) return st;
     {   // h_v . wt'_r per segment
         TravArgs ta;
         ta.g = g; ta.h = h; ta.wtp = w.wtp; ta.heads = 1; ta.d = D; ta.vatt = w.vatt;

@@ -14,6 +14,7 @@ namespace {
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 __device__ __forceinline__ float4 scale4(float4 a, float s) { return make_float4(a.x * s, a.y * s, a.z * s, a.w * s); }
+__device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 fma4(float4 a, float s, float4 c)
 {
@@ -409,22 +410,27 @@ __global__ void add_kernel(float *out, const float *a, const float *b, int64_t n
     if (i < n) out[i] = a[i] + b[i];
 }
 
-// Reordered attention vectors: out[r, k, i] = sum_{j in head k} W[r, i, j] v[r, j].
-__global__ __launch_bounds__(256) void reorder_vec_kernel(const float *W, const float *v, int R,
-                                                          int d_in, int d_out, int heads,
-                                                          float *out)
+// Reordered attention vectors (linear operator reordering): for every row
+// (r, i) of W_r, out[r, k, i] = W_r[i, k-cols] . v[r, k-cols] for one or two
+// vectors v.  A group of DO/4 lanes reads the W row once (one float4 per
+// lane) and reduces per head over DH/4 lanes.
+template <int DO, int DH>
+__global__ __launch_bounds__(256) void reorder_vec_kernel(const float *W, const float *v1,
+                                                          const float *v2, int R, int d_in,
+                                                          float *out1, float *out2)
 {
-    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (r, k, i)
-    if (idx >= (int64_t)R * heads * d_in) return;
-    const int i = (int)(idx % d_in);
-    const int k = (int)((idx / d_in) % heads);
-    const int r = (int)(idx / ((int64_t)d_in * heads));
-    const int dh = d_out / heads;
-    const float *Wr = W + ((size_t)r * d_in + i) * d_out + k * dh;
-    const float *vr = v + (size_t)r * d_out + k * dh;
-    float s = 0.f;
-    for (int j = 0; j < dh; ++j) s += Wr[j] * vr[j];
-    out[idx] = s;
+    constexpr int G = DO / 4, L = DH / 4, H = DO / DH;
+    const int gl = threadIdx.x % G;
+    const int64_t row = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;   // (r, i)
+    if (row >= (int64_t)R * d_in) return;
+    const int r = (int)(row / d_in), i = (int)(row % d_in), k = gl / L;
+    const float4 w = ld4(W + (size_t)row * DO + gl * 4);
+    const float a = gsum<L>(dot4(w, ld4(v1 + (size_t)r * DO + gl * 4)));
+    if (gl % L == 0) out1[((size_t)r * H + k) * d_in + i] = a;
+    if (v2) {
+        const float b = gsum<L>(dot4(w, ld4(v2 + (size_t)r * DO + gl * 4)));
+        if (gl % L == 0) out2[((size_t)r * H + k) * d_in + i] = b;
+    }
 }
 
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
@@ -609,13 +615,31 @@ rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hi
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "add launch");
 }
 
-rgnn_status launch_reorder_vec(const float *W, const float *v, int R, int d_in, int d_out,
-                               int heads, float *out, hipStream_t s)
+rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int heads,
+                               const float *v1, float *out1, const float *v2, float *out2,
+                               hipStream_t s)
 {
-    const int64_t n = (int64_t)R * heads * d_in;
-    LaunchScope ls("reorder_vec", s);
-    hipLaunchKernelGGL(reorder_vec_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, W, v, R,
-                       d_in, d_out, heads, out);
+    const int64_t rows = (int64_t)R * d_in;
+    if (rows == 0) return RGNN_OK;
+    if (d_out != 64 && d_out != 128) return fail(RGNN_EUNSUPPORTED, "reorder: d_out must be 64 or 128");
+    const unsigned nb = blocks_for(rows, 256 / (d_out / 4));
+    bool ok = true;
+    {
+        LaunchScope ls("reorder_vec", s);
+#define RV(DO, DH) hipLaunchKernelGGL((reorder_vec_kernel<DO, DH>), dim3(nb), dim3(256), 0, s, W, v1, v2, R, \
+                                      d_in, out1, out2)
+        const int dh = d_out / heads;
+        if (d_out == 64 && dh == 64) RV(64, 64);
+        else if (d_out == 64 && dh == 32) RV(64, 32);
+        else if (d_out == 64 && dh == 16) RV(64, 16);
+        else if (d_out == 128 && dh == 128) RV(128, 128);
+        else if (d_out == 128 && dh == 64) RV(128, 64);
+        else if (d_out == 128 && dh == 32) RV(128, 32);
+        else if (d_out == 128 && dh == 16) RV(128, 16);
+        else ok = false;
+#undef RV
+    }
+    if (!ok) return fail(RGNN_EUNSUPPORTED, "reorder: unsupported heads");
     hipError_t e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "reorder_vec launch");
 }

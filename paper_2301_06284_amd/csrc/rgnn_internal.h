@@ -177,9 +177,11 @@ struct GemmArgs {
 };
 rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s);
 
-// Reordered attention vectors: out[r, k, :] = W_r[:, k-cols] v[r, k-cols]
-rgnn_status launch_reorder_vec(const float *W, const float *v, int R, int d_in, int d_out,
-                               int heads, float *out, hipStream_t s);
+// Reordered attention vectors: out1[r, k, :] = W_r[:, k-cols] v1[r, k-cols]
+// and the same for v2 into out2 when v2 is not NULL (one launch).
+rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int heads,
+                               const float *v1, float *out1, const float *v2, float *out2,
+                               hipStream_t s);
 
 struct TravArgs {
     const rgnn_graph *g = nullptr;
