@@ -54,8 +54,10 @@ def _load():
                                             vp]
         _lib.oracle_rgat_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                               vp, vp, f64, vp, vp, vp, vp, vp, vp, vp]
+        _lib.oracle_rgcn_backward.argtypes = [i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp,
+                                              i32, vp, vp, vp, vp, vp, vp]
         for f in ("oracle_rgcn_forward", "oracle_rgat_forward", "oracle_hgt_forward",
-                  "oracle_rgat_backward", "oracle_num_threads"):
+                  "oracle_rgat_backward", "oracle_rgcn_backward", "oracle_num_threads"):
             getattr(_lib, f).restype = ctypes.c_int
     return _lib
 
@@ -169,6 +171,27 @@ def rgat_backward(g, h, W, w_src, w_dst, grad_out, heads=1, neg_slope=0.2,
                                       _p(dws), _p(dwd))
     _check(rc, "rgat_backward")
     return dh, dW, dws, dwd
+
+
+def rgcn_backward(g, h, W, W0, grad_out, relu=False, node_mask=None, rel_mask=None,
+                  want_dW0=True):
+    """Gradients of L = sum(out * grad_out) of the RGCN layer (chain rule on the
+    RGCN equation).  Returns (dh, dW, dW0); dW0 is None without W0 or when not
+    wanted; entries outside the masks are zero."""
+    h, W, G = map(_f32, (h, W, grad_out))
+    W0 = None if W0 is None else _f32(W0)
+    src, dst, rel = _i32(g["src"]), _i32(g["dst"]), _i32(g["rel"])
+    N, R = g["N"], g["R"]
+    d_in, d_out = W.shape[1], W.shape[2]
+    nm = None if node_mask is None else np.ascontiguousarray(node_mask, np.uint8)
+    rm = None if rel_mask is None else np.ascontiguousarray(rel_mask, np.uint8)
+    dh = np.zeros((N, d_in)); dW = np.zeros((R, d_in, d_out))
+    dW0 = np.zeros((d_in, d_out)) if (W0 is not None and want_dW0) else None
+    rc = _load().oracle_rgcn_backward(N, g["E"], R, d_in, d_out, _p(src), _p(dst), _p(rel),
+                                      _p(h), _p(W), _p(W0), int(bool(relu)), _p(G), _p(nm),
+                                      _p(rm), _p(dh), _p(dW), _p(dW0))
+    _check(rc, "rgcn_backward")
+    return dh, dW, dW0
 
 
 # --------------------------------------------------------------------------

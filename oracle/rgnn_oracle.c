@@ -1,6 +1,6 @@
 /*
  * rgnn_oracle.c -- plain, slow, fp64 CPU reference of the RGCN, RGAT and HGT
- * layers and of the RGAT backward pass.
+ * layers and of the RGAT and RGCN backward passes.
  *
  * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
  * benchmark's CPU-baseline leg may load this library.  It shares no code,
@@ -591,6 +591,105 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
     (void)x;
     free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
     free(xv); free(x); free(mx); free(sm); free(sv); free(need);
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* RGCN backward for the loss L = sum(out * G) (G = grad_out), from the paper's
+ * RGCN equation by the chain rule.  With the pre-activation
+ *   P_v = h_v W0 + sum_r sum_{u in N_v^r} h_u W_r / c_{v,r}
+ * and Gp_v = G_v * act'(P_v) (ReLU: 1 where P_v > 0, else 0; identity: 1):
+ *   dW_r += h_u^T Gp_v / c_{v,r},   dh_u += Gp_v W_r^T / c_{v,r}   per in-edge (u -> v, r)
+ *   dW0  += h_v^T Gp_v,             dh_v += Gp_v W0^T              per node (W0 given)
+ * node_mask / rel_mask (nullable) restrict dh and dW as for the RGAT backward;
+ * dW0 is computed when both W0 and dW0 are given.  Destinations are visited in
+ * increasing id and their in-edges in edge-id order. */
+int oracle_rgcn_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
+                         const int32_t *src, const int32_t *dst, const int32_t *rel,
+                         const float *h, const float *W, const float *W0, int32_t relu,
+                         const float *G, const uint8_t *node_mask, const uint8_t *rel_mask,
+                         double *dh, double *dW, double *dW0)
+{
+    if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_in > 512 || d_out <= 0 || d_out > 512)
+        return -1;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    const int want_w0 = W0 && dW0;
+    uint8_t *need = (uint8_t *)calloc((size_t)(N > 0 ? N : 1), 1);
+    int64_t *cnt = (int64_t *)malloc((size_t)(R > 0 ? R : 1) * sizeof(int64_t));
+    double *P = (double *)malloc((size_t)d_out * sizeof(double));
+    double *Gp = (double *)malloc((size_t)d_out * sizeof(double));
+    double *xv = (double *)malloc((size_t)d_in * sizeof(double));
+    double *xu = (double *)malloc((size_t)d_in * sizeof(double));
+    double *m = (double *)malloc((size_t)d_out * sizeof(double));
+    int err = !need || !cnt || !P || !Gp || !xv || !xu || !m;
+    if (!err) {
+        for (int64_t v = 0; v < N; ++v)
+            if (want_w0 || (W0 && (!node_mask || node_mask[v]))) need[v] = 1;
+        for (int64_t e = 0; e < E; ++e)
+            if ((!rel_mask || rel_mask[rel[e]]) || (!node_mask || node_mask[src[e]])) need[dst[e]] = 1;
+        memset(dh, 0, (size_t)N * d_in * sizeof(double));
+        memset(dW, 0, (size_t)R * d_in * d_out * sizeof(double));
+        if (want_w0) memset(dW0, 0, (size_t)d_in * d_out * sizeof(double));
+    }
+    for (int64_t v = 0; v < N && !err; ++v) {
+        if (!need[v]) continue;
+        const int64_t p0 = a.ptr[v], deg = a.ptr[v + 1] - p0;
+        for (int r = 0; r < R; ++r) cnt[r] = 0;
+        for (int64_t p = p0; p < p0 + deg; ++p) cnt[rel[a.eid[p]]]++;
+        load_row(h, v, d_in, xv);
+        const float *Gv = G + (size_t)v * d_out;
+        for (int j = 0; j < d_out; ++j) Gp[j] = (double)Gv[j];
+        if (relu) {   /* recompute the pre-activation */
+            for (int j = 0; j < d_out; ++j) P[j] = 0.0;
+            if (W0) {
+                vecmat(xv, W0, d_in, d_out, 0, d_out, m);
+                for (int j = 0; j < d_out; ++j) P[j] += m[j];
+            }
+            for (int64_t p = p0; p < p0 + deg; ++p) {
+                const int64_t e = a.eid[p];
+                load_row(h, src[e], d_in, xu);
+                vecmat(xu, W + (size_t)rel[e] * d_in * d_out, d_in, d_out, 0, d_out, m);
+                const double inv_c = 1.0 / (double)cnt[rel[e]];
+                for (int j = 0; j < d_out; ++j) P[j] += m[j] * inv_c;
+            }
+            for (int j = 0; j < d_out; ++j) if (!(P[j] > 0.0)) Gp[j] = 0.0;
+        }
+        if (W0) {
+            if (want_w0)
+                for (int i = 0; i < d_in; ++i)
+                    for (int j = 0; j < d_out; ++j) dW0[(size_t)i * d_out + j] += xv[i] * Gp[j];
+            if (!node_mask || node_mask[v])
+                for (int i = 0; i < d_in; ++i) {
+                    double s = 0.0;
+                    for (int j = 0; j < d_out; ++j) s += (double)W0[(size_t)i * d_out + j] * Gp[j];
+                    dh[(size_t)v * d_in + i] += s;
+                }
+        }
+        for (int64_t p = p0; p < p0 + deg; ++p) {
+            const int64_t e = a.eid[p];
+            const int r = rel[e];
+            const int64_t u = src[e];
+            const double inv_c = 1.0 / (double)cnt[r];
+            const float *Wr = W + (size_t)r * d_in * d_out;
+            if (!rel_mask || rel_mask[r]) {
+                load_row(h, u, d_in, xu);
+                for (int i = 0; i < d_in; ++i) {
+                    double *row = dW + ((size_t)r * d_in + i) * d_out;
+                    for (int j = 0; j < d_out; ++j) row[j] += xu[i] * Gp[j] * inv_c;
+                }
+            }
+            if (!node_mask || node_mask[u])
+                for (int i = 0; i < d_in; ++i) {
+                    double s = 0.0;
+                    for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * Gp[j];
+                    dh[(size_t)u * d_in + i] += s * inv_c;
+                }
+        }
+    }
+    free(need); free(cnt); free(P); free(Gp); free(xv); free(xu); free(m);
     free_in_lists(&a);
     return err ? -3 : 0;
 }

@@ -432,6 +432,72 @@ def test_rgat_backward_masks():
         np.testing.assert_allclose(a[2], b[2], rtol=1e-12, atol=1e-14)
 
 
+# ---------------------------------------------------------------- RGCN backward
+def rgcn_torch_dense(g, h, W, W0, relu):
+    A = torch.tensor(dense_adj(g))
+    c = A.sum(dim=2, keepdim=True)
+    An = torch.where(c > 0, A / torch.where(c > 0, c, torch.ones_like(c)), torch.zeros_like(A))
+    out = torch.einsum("rvu,ui,rij->vj", An, h, W)
+    if W0 is not None:
+        out = out + h @ W0
+    return torch.relu(out) if relu else out
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("self_loop,relu", [(True, False), (False, False), (True, True), (False, True)])
+def test_rgcn_backward_vs_autograd(kind, self_loop, relu):
+    g = tiny_graph(61, N=15, E=70, R=3, kind=kind)
+    t = tiny_tensors(61, g, 6, 5)
+    names = ("h", "W", "W0") if self_loop else ("h", "W")
+    ts = {k: torch.tensor(t[k], dtype=torch.float64, requires_grad=True) for k in names}
+    out = rgcn_torch_dense(g, ts["h"], ts["W"], ts.get("W0"), relu)
+    (out * torch.tensor(t["grad_out"][:, :5], dtype=torch.float64)).sum().backward()
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"] if self_loop else None,
+                                       t["grad_out"][:, :5].copy(), relu=relu)
+    np.testing.assert_allclose(dh, ts["h"].grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dW, ts["W"].grad.numpy(), rtol=1e-10, atol=1e-12)
+    if self_loop:
+        np.testing.assert_allclose(dW0, ts["W0"].grad.numpy(), rtol=1e-10, atol=1e-12)
+    else:
+        assert dW0 is None
+
+
+def test_rgcn_backward_finite_differences():
+    """Central differences of L = sum(out * G) for every parameter entry."""
+    g = tiny_graph(62, N=7, E=18, R=2, kind="dups")
+    t = tiny_tensors(62, g, 3, 4)
+    G = t["grad_out"][:, :4].copy()
+
+    def loss(tt):
+        return float((oracle.rgcn_forward(g, tt["h"], tt["W"], tt["W0"]) * G).sum())
+    grads = dict(zip(("h", "W", "W0"), oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], G)))
+    for k in grads:
+        base = t[k]
+        fd = np.zeros(base.shape)
+        for idx in np.ndindex(base.shape):
+            step = 1e-2 * max(1e-2, abs(float(base[idx])))
+            plus, minus = base.copy(), base.copy()
+            plus[idx] = np.float32(base[idx] + step)
+            minus[idx] = np.float32(base[idx] - step)
+            denom = float(plus[idx]) - float(minus[idx])
+            fd[idx] = (loss(dict(t, **{k: plus})) - loss(dict(t, **{k: minus}))) / denom
+        # the loss is linear in each parameter: differences are exact up to rounding
+        np.testing.assert_allclose(grads[k], fd, rtol=1e-6, atol=1e-7, err_msg=k)
+
+
+def test_rgcn_backward_masks():
+    g = tiny_graph(63, N=20, E=100, R=4, kind="hub")
+    t = tiny_tensors(63, g, 6, 6)
+    full = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], relu=True)
+    nm = np.zeros(20, np.uint8); nm[[0, 5, 19]] = 1
+    rm = np.zeros(4, np.uint8); rm[2] = 1
+    part = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], relu=True,
+                                node_mask=nm, rel_mask=rm, want_dW0=False)
+    np.testing.assert_allclose(part[0][nm == 1], full[0][nm == 1], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(part[1][2], full[1][2], rtol=1e-12, atol=1e-14)
+    assert part[2] is None
+
+
 # ---------------------------------------------------------------- integer preprocessing
 @pytest.mark.parametrize("kind", KINDS + ["complete"])
 def test_graph_index_against_python_sets(kind):
