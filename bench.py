@@ -14,7 +14,7 @@ device synchronisations.  The line also carries:
   cpu_baseline  the fp64 oracle timed on the host's cores on a bounded sample
                 of destinations of the same workload;
   layers        edges/s of the other layers and workloads (RGCN, HGT, RGCN and
-                RGAT at d = 128, RGAT backward, both RGAT plans).
+                RGAT at d = 128, RGAT and RGCN backward, both RGAT plans).
 """
 from __future__ import annotations
 
@@ -299,8 +299,26 @@ def main():
         kb = kernel_profile(rgnn, torch, fnb, max(3, K // 2))
         layers["rgat_bwd_am_like_880k"] = {"edges_per_s": E / (msb * 1e-3), "ms": msb,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in kb.items()}}
+        del wsb
+        # RGCN forward (with self-loop) and backward on the same graph
+        log("workload 5: RGCN forward and backward")
+        pr = rgnn.select_plan(c.G, rgnn.LAYER_RGCN, d, d, 1)[0]
+        wsr = c.ws(rgnn.LAYER_RGCN, d, d, 1, pr)
+        fnr = lambda: rgnn.rgcn_forward(c.G, c.T["h"], c.T["W"], c.T["W0"], out, wsr, d, d, 0, pr)
+        msr = time_steps(torch, fnr, K, W)
+        kr = kernel_profile(rgnn, torch, fnr, max(3, K // 2))
+        layers["rgcn_fwd_am_like_880k"] = {"edges_per_s": E / (msr * 1e-3), "ms": msr, "plan": names[pr],
+                                           "kernels_ms": {k: round(v[1], 4) for k, v in kr.items()}}
+        gW0 = torch.empty(d, d, device=c.dev)
+        wsrb = c.ws(rgnn.LAYER_RGCN_BACKWARD, d, d)
+        fnrb = lambda: rgnn.rgcn_backward(c.G, c.T["h"], c.T["W"], c.T["W0"], None, c.T["grad_out"], gh, gW,
+                                          gW0, wsrb, d, d, 0)
+        msrb = time_steps(torch, fnrb, K, W)
+        krb = kernel_profile(rgnn, torch, fnrb, max(3, K // 2))
+        layers["rgcn_bwd_am_like_880k"] = {"edges_per_s": E / (msrb * 1e-3), "ms": msrb,
+                                           "kernels_ms": {k: round(v[1], 4) for k, v in krb.items()}}
         c.close()
-        del out, saved, wsf, gh, gW, gs, gt, wsb
+        del out, saved, wsf, gh, gW, gs, gt, wsr, wsrb, gW0
 
         # ------------------------------------------------ HGT forward, workload 3
         log("workload 3: HGT forward")

@@ -66,7 +66,8 @@ typedef enum {
     RGNN_LAYER_RGAT = 1,
     RGNN_LAYER_HGT = 2,
     RGNN_LAYER_RGAT_BACKWARD = 3,
-    RGNN_LAYER_SEGMENT_GEMM = 4
+    RGNN_LAYER_SEGMENT_GEMM = 4,
+    RGNN_LAYER_RGCN_BACKWARD = 5
 } rgnn_layer;
 
 enum { RGNN_SOFTMAX_PER_DST = 0, RGNN_SOFTMAX_PER_DST_REL = 1 };
@@ -219,6 +220,25 @@ rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, const float *W,
                           const float *grad_out, float *grad_h, float *grad_W,
                           float *grad_w_src, float *grad_w_dst, void *ws, size_t ws_bytes,
                           void *stream);
+
+/* RGCN backward for the RGCN layer above: the chain rule of the RGCN
+ * equation (Section "Backward Propagation" derives the backward from the
+ * forward).  With P the pre-activation and Gp = grad_out * act'(P):
+ *   dW_r = sum over in-edges (u -> v, r) of h_u^T Gp_v / c_{v,r}
+ *   dh_u = sum over out-edges (u -> v, r) of Gp_v W_r^T / c_{v,r}  +  Gp_u W0^T
+ *   dW0  = sum_v h_v^T Gp_v
+ *   h [N, d_in], W [R, d_in, d_out], W0 [d_in, d_out] or NULL (as in the
+ *   forward), flags as in the forward (RGNN_FLAG_RELU: out = the forward's
+ *   output [N, d_out], which gives act' = [out > 0]; otherwise out may be NULL),
+ *   grad_out [N, d_out]; writes grad_h [N, d_in], grad_W [R, d_in, d_out] and,
+ *   when W0 and grad_W0 are both given, grad_W0 [d_in, d_out].
+ *   d_in = d_out = 64.  Workspace: rgnn_workspace_size(RGNN_LAYER_RGCN_BACKWARD).
+ *   Results are reproducible except the rows of sources with more than 64
+ *   out-edges, which are summed with float atomics. */
+rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W, const float *W0,
+                          int32_t d_in, int32_t d_out, int32_t flags, const float *out,
+                          const float *grad_out, float *grad_h, float *grad_W, float *grad_W0,
+                          void *ws, size_t ws_bytes, void *stream);
 
 /* Segment MM: the GEMM template of Section "The GEMM Template and the
  * Traversal Template", Y[S] = X[G] x W[T]:

@@ -19,7 +19,8 @@ LIB = os.path.join(PKG, "librgnn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["graph.cpp", "api.cpp", "gemm.hip", "traverse.hip", "reduce.hip", "hgt.hip",
-           "backward.hip", "fused.hip"]
+           "backward.hip", "fused.hip",
+           "rgcn_backward.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -294,6 +294,13 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
         *bytes = need;
         return RGNN_OK;
     }
+    case RGNN_LAYER_RGCN_BACKWARD: {
+        size_t need = 0;
+        rgcn_backward_impl(g, nullptr, nullptr, nullptr, d_in, d_out, 0, nullptr, nullptr, nullptr,
+                           nullptr, nullptr, nullptr, 0, nullptr, &need);
+        *bytes = need;
+        return RGNN_OK;
+    }
     default:
         return fail(RGNN_EINVAL, "unknown layer");
     }
@@ -519,6 +526,23 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
                               grad_h, grad_W, grad_w_src, grad_w_dst, ws, ws_bytes,
                               (hipStream_t)stream, nullptr);
+}
+
+extern "C" rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W,
+                                     const float *W0, int32_t d_in, int32_t d_out, int32_t flags,
+                                     const float *out, const float *grad_out, float *grad_h,
+                                     float *grad_W, float *grad_W0, void *ws, size_t ws_bytes,
+                                     void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !W || !grad_out || !grad_h || !grad_W) return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (flags & ~RGNN_FLAG_RELU) return fail(RGNN_EINVAL, "unknown RGCN flag");
+    if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGCN backward supports d = 64");
+    if ((flags & RGNN_FLAG_RELU) && !out)
+        return fail(RGNN_EINVAL, "RGCN backward with ReLU needs the forward output");
+    return rgcn_backward_impl(g, h, W, W0, d_in, d_out, flags, out, grad_out, grad_h, grad_W,
+                              W0 ? grad_W0 : nullptr, ws, ws_bytes, (hipStream_t)stream, nullptr);
 }
 
 // ------------------------------------------------------------------ segment MM

@@ -485,6 +485,9 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Chunk c covers rows [row0, row0 + rows) of the by-relation segment order:
 // partial[c] = sum over its segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out);
 // yvec[c]   = sum over its segments of ysum[seg] * h[dst(seg)].
+// YS: also sum ysum[row] * h[v] per chunk (the RGAT dwt' term); GATHER: the
+// second operand's row (and h's) is vsegdst[row], else the row itself.
+template <bool YS, bool GATHER>
 __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
                                                          const float *Sa,
                                                          const float *Gm, const float *h,
@@ -517,7 +520,7 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     float ry[SL];
     auto load_idx = [&](int k0, int (&v)[SL]) {
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) v[sl] = vsegdst_byrel[row_of(k0, sl)];
+        for (int sl = 0; sl < SL; ++sl) v[sl] = GATHER ? vsegdst_byrel[row_of(k0, sl)] : row_of(k0, sl);
     };
     auto load_rows = [&](int k0, const int (&v)[SL]) {
 #pragma unroll
@@ -525,8 +528,10 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
             const int row = row_of(k0, sl);
             ra[sl] = ld4(Sa + (size_t)row * D + c4);
             rb[sl] = ld4(Gm + (size_t)v[sl] * D + c4);
-            rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
-            ry[sl] = ysum[row];
+            if (YS) {
+                rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
+                ry[sl] = ysum[row];
+            }
         }
     };
     load_idx(0, vi);
@@ -539,7 +544,7 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
             const bool ok = k0 + rr < t.rows;
             *reinterpret_cast<float4 *>(&As[rr * P + c4]) = ok ? ra[sl] : zero4();
             *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = ok ? rb[sl] : zero4();
-            if (ok) yacc = lin4(yacc, 1.f, rh[sl], ry[sl]);
+            if (YS && ok) yacc = lin4(yacc, 1.f, rh[sl], ry[sl]);
         }
         __syncthreads();
         load_rows(k0 + KB, vn);
@@ -559,12 +564,14 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) out[(size_t)(w * 16 + q * 4 + v) * D + cb * 16 + li] = acc[cb][v];
-    yred[tid] = yacc;
-    __syncthreads();
-    if (tid < 16) {
-        float4 s = zero4();
-        for (int i = tid; i < 256; i += 16) s = add4(s, yred[i]);
-        st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
+    if (YS) {
+        yred[tid] = yacc;
+        __syncthreads();
+        if (tid < 16) {
+            float4 s = zero4();
+            for (int i = tid; i < 256; i += 16) s = add4(s, yred[i]);
+            st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
+        }
     }
 }
 
@@ -593,6 +600,8 @@ __global__ __launch_bounds__(1024) void bwd_reduce_kernel(const float *pvec, con
 
 // Per relation r (blockIdx.x) and 256 entries of dW_r (blockIdx.y): combine
 // chunk partials in order, add the rank-1 attention terms; dw_src, dw_dst.
+// ATT false: only the ordered sum of the chunk partials (dW of RGCN).
+template <bool ATT>
 __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial, const int32_t *rel_chunkptr,
                                                            const float *pws_all, const float *pwt_all,
                                                            const float *W, const float *w_src,
@@ -601,7 +610,7 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
 {
     __shared__ float pws[D], pwt[D];
     const int r = blockIdx.x, tid = threadIdx.x;
-    if (tid < D) {
+    if (ATT && tid < D) {
         pws[tid] = pws_all[(size_t)r * D + tid];
         pwt[tid] = pwt_all[(size_t)r * D + tid];
     }
@@ -610,12 +619,19 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
     {
         const int idx = blockIdx.y * 256 + tid;
         const int i = idx / D, j = idx % D;
+        // chunks in order, eight loads in flight
         float s = 0.f;
-        for (int c = c0; c < c1; ++c) s += partial[(size_t)c * D * D + idx];
-        s += pws[i] * w_src[(size_t)r * D + j] + pwt[i] * w_dst[(size_t)r * D + j];
+        for (int c = c0; c < c1; c += 8) {
+            float p[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) p[u] = c + u < c1 ? partial[(size_t)(c + u) * D * D + idx] : 0.f;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += p[u];
+        }
+        if (ATT) s += pws[i] * w_src[(size_t)r * D + j] + pwt[i] * w_dst[(size_t)r * D + j];
         dW[(size_t)r * D * D + idx] = s;
     }
-    if (blockIdx.y == 0 && tid < D) {
+    if (ATT && blockIdx.y == 0 && tid < D) {
         float a = 0.f, b = 0.f;
         for (int i = 0; i < D; ++i) {
             const float wij = W[((size_t)r * D + i) * D + tid];
@@ -680,6 +696,37 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
 }  // namespace
 
 int bwd_outer_rows() { return kOuterRows; }
+
+rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather,
+                                const float *X, const float *Gm, float *partial, hipStream_t s)
+{
+    if (nchunks == 0) return RGNN_OK;
+    {
+        LaunchScope ls("outer_gemm", s);
+        if (gather)
+            hipLaunchKernelGGL((outer_gemm_kernel<false, true>), dim3((unsigned)nchunks), dim3(256), 0, s,
+                               chunks, gather, X, Gm, nullptr, nullptr, partial, nullptr);
+        else
+            hipLaunchKernelGGL((outer_gemm_kernel<false, false>), dim3((unsigned)nchunks), dim3(256), 0, s,
+                               chunks, nullptr, X, Gm, nullptr, nullptr, partial, nullptr);
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "outer_gemm launch");
+}
+
+rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW,
+                             hipStream_t s)
+{
+    if (R == 0) return RGNN_OK;
+    {
+        LaunchScope ls("chunk_sum", s);
+        hipLaunchKernelGGL((bwd_finalize_kernel<false>), dim3((unsigned)R, D * D / 256), dim3(256), 0, s,
+                           partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr,
+                           nullptr);
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "chunk_sum launch");
+}
 
 rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
                                const float *w_src, const float *w_dst, int d_in, int d_out,
@@ -770,7 +817,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "pair_gemv launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
-        hipLaunchKernelGGL(outer_gemm_kernel, dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
+        hipLaunchKernelGGL((outer_gemm_kernel<true, true>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
                            g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, Gm, h, w.ysum,
                            w.partial, w.yvec);
     }
@@ -783,7 +830,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_reduce launch");
     {
         LaunchScope ls("rgat_bwd_finalize", s);
-        hipLaunchKernelGGL(bwd_finalize_kernel, dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
+        hipLaunchKernelGGL((bwd_finalize_kernel<true>), dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
                            g->dev.rel_chunkptr, w.pws, w.pwt, W, w_src, w_dst, dW, dws, dwt);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "finalize launch");

@@ -42,7 +42,7 @@ __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<floa
 __device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
 __device__ __forceinline__ float leaky(float y, float slope) { return y > 0.f ? y : slope * y; }
 
-enum : int { kModeMean = 0, kModeSoftmax = 1 };
+enum : int { kModeMean = 0, kModeSoftmax = 1, kModeSum = 2 };
 
 struct FK {
     const FusedRow *rows;
@@ -52,6 +52,8 @@ struct FK {
     const float *h, *W, *wsp, *vatt;
     float slope;
     float *T, *vstat;
+    const int32_t *pos;          // sums only: output row of each virtual segment
+    float *S;
 };
 
 // DI: input features, DO: output features, NWAVE: waves per workgroup,
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
     constexpr int NR = (kFusedTileRows + NT - 1) / NT;   // segment entries per thread
     constexpr int NS = (kFusedTileEdges + NT - 1) / NT;  // source indices per thread
     static_assert(NW * NT * 4 == DI * DO, "weight tile must split evenly over the workgroup");
-    __shared__ float Wt[DO * KP];
+    __shared__ float Wt[MODE == kModeSum ? 1 : DO * KP];
     __shared__ float wsl[MODE == kModeSoftmax ? DI : 1];
     __shared__ FusedRow srow[kFusedTileRows];
     __shared__ int32_t ssrc[kFusedTileEdges];
@@ -95,6 +97,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
     float4 wv[NW];
 #pragma unroll
     for (int t = 0; t < NW; ++t) {
+        if (MODE == kModeSum) break;
         const int idx = tid + NT * t;
         const int kk = idx / (DO / 4), n4 = (idx % (DO / 4)) * 4;
         wv[t] = ld4(k.W + ((size_t)r * DI + kk) * DO + n4);
@@ -115,6 +118,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
     if (MODE == kModeSoftmax && tid < DI) wsv = k.wsp[(size_t)r * DI + tid];
 #pragma unroll
     for (int t = 0; t < NW; ++t) {
+        if (MODE == kModeSum) break;
         const int idx = tid + NT * t;
         const int kk = idx / (DO / 4), n4 = (idx % (DO / 4)) * 4;
         Wt[(n4 + 0) * KP + kk] = wv[t].x;
@@ -238,6 +242,20 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
             consume(B, t + KU);
         }
 
+        if (MODE == kModeSum) {   // the segment means themselves, in the row layout
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                if (!valid[h2]) continue;
+                const float sc = 1.f / (float)fr[h2].cnt;
+                float *o = k.S + (size_t)k.pos[fr[h2].vs] * DI + gp * 4;
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const float4 a = acc[h2][c];
+                    st4(o + c * 32, make_float4(a.x * sc, a.y * sc, a.z * sc, a.w * sc));
+                }
+            }
+            continue;
+        }
         // row sums -> MFMA operand layout by lane permutes: lane (li, q) takes
         // features 16c + 4q .. +3 of row li, held by lane 8 (li % 8) + 4 (c % 2) + q
         // in its chunk c / 2 of row set li / 8
@@ -328,6 +346,12 @@ void launch_shape(const FK &k, int64_t ntiles, hipStream_t s)
 template <int MODE>
 bool dispatch(int di, int dout, const FK &k, int64_t n, hipStream_t s)
 {
+    if constexpr (MODE == kModeSum) {   // no transform: the output width is d_in
+        if (di == 64) launch_shape<64, 64, MODE>(k, n, s);
+        else if (di == 128) launch_shape<128, 128, MODE>(k, n, s);
+        else return false;
+        return true;
+    }
     if (di == 64 && dout == 64) launch_shape<64, 64, MODE>(k, n, s);
     else if (di == 128 && dout == 128) launch_shape<128, 128, MODE>(k, n, s);
     else if constexpr (MODE == kModeMean) {   // RGCN only: RGAT needs d_in == d_out
@@ -350,13 +374,15 @@ rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s)
     k.rows = g->dev.fused_rows; k.tiles = g->dev.tiles_fused;
     k.ntiles = g->n_tiles_fused; k.nedges = g->E; k.src = g->dev.fused_src;
     k.h = a.h; k.W = a.W; k.wsp = a.wsp; k.vatt = a.vatt; k.slope = a.slope;
-    k.T = a.T; k.vstat = a.vstat;
+    k.T = a.T; k.vstat = a.vstat; k.S = a.S; k.pos = g->dev.vseg_pos;
     if (a.softmax && (!a.wsp || !a.vatt || !a.vstat))
         return fail(RGNN_EINVAL, "fused softmax aggregation needs wsp, vatt and vstat");
+    if (a.S && a.softmax) return fail(RGNN_EINVAL, "segment means are for the mean aggregation");
     bool ok;
     {
-        LaunchScope ls(a.softmax ? "rgat_af_fused" : "rgcn_af_fused", s);
+        LaunchScope ls(a.softmax ? "rgat_af_fused" : (a.S ? "segment_means" : "rgcn_af_fused"), s);
         ok = a.softmax ? dispatch<kModeSoftmax>(a.d_in, a.d_out, k, g->n_tiles_fused, s)
+             : a.S     ? dispatch<kModeSum>(a.d_in, a.d_out, k, g->n_tiles_fused, s)
                        : dispatch<kModeMean>(a.d_in, a.d_out, k, g->n_tiles_fused, s);
     }
     if (!ok) return fail(RGNN_EUNSUPPORTED, "fused aggregation: d_in, d_out must be 64 or 128");

@@ -151,6 +151,8 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         for (int32_t r = 0; r < R; ++r) x.rel_vsegptr[r + 1] += x.rel_vsegptr[r];
         x.vsegdst_byrel.resize((size_t)g->V);
         for (int64_t i = 0; i < g->V; ++i) x.vsegdst_byrel[i] = x.vseg_dst[x.vseg_byrel[i]];
+        x.invcnt_byrel.resize((size_t)g->V);
+        for (int64_t i = 0; i < g->V; ++i) x.invcnt_byrel[i] = 1.f / (float)x.vseg_cnt[x.vseg_byrel[i]];
         // fused aggregate-first order: by relation, then edge count (largest
         // first), then id; tiles of consecutive rows of one relation, cut at
         // kFusedTileRows rows or (after the first 16-row block) kFusedTileEdges
@@ -309,6 +311,9 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         g->n_tiles_all = (int64_t)x.tiles_all.size();
         build_tiles(x.rel_vsegptr, bwd_outer_rows(), x.tiles_outer);
         g->n_tiles_outer = (int64_t)x.tiles_outer.size();
+        build_tiles(all, bwd_outer_rows(), x.tiles_nodes_outer);   // node chunks (self-loop dW0)
+        g->n_tiles_nodes_outer = (int64_t)x.tiles_nodes_outer.size();
+        x.nodes_chunkptr = {0, (int32_t)g->n_tiles_nodes_outer};
         x.rel_chunkptr.assign((size_t)R + 1, 0);
         for (const Tile &t : x.tiles_outer) x.rel_chunkptr[(size_t)t.type + 1]++;
         for (int32_t r = 0; r < R; ++r) x.rel_chunkptr[r + 1] += x.rel_chunkptr[r];
@@ -355,6 +360,10 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_nodes, x.tiles_nodes.data(), x.tiles_nodes.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_nodes_outer, x.tiles_nodes_outer.data(),
+                         x.tiles_nodes_outer.size() * sizeof(Tile)});
+    add32(&d.nodes_chunkptr, x.nodes_chunkptr);
+    parts.push_back(Part{(void **)&d.invcnt_byrel, x.invcnt_byrel.data(), x.invcnt_byrel.size() * sizeof(float)});
     parts.push_back(Part{(void **)&d.tiles_fused, x.tiles_fused.data(), x.tiles_fused.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.fused_rows, x.fused_rows.data(), x.fused_rows.size() * sizeof(FusedRow)});
     add32(&d.fused_src, x.fused_src);

@@ -65,6 +65,9 @@ struct HostIndex {
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
+    std::vector<float> invcnt_byrel;      // 1 / c_{v,r} of each virtual segment, by-relation order
+    std::vector<Tile> tiles_nodes_outer;  // outer-product chunks over all nodes
+    std::vector<int32_t> nodes_chunkptr;  // {0, number of node chunks}
     std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
     // out-edges (source-major view of the sorted in-edges), for the backward pass
     std::vector<int32_t> out_ptr, out_pos, out_vseg, out_rel, out_pair;
@@ -87,6 +90,9 @@ struct DeviceIndex {
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr;
+    float *invcnt_byrel = nullptr;
+    Tile *tiles_nodes_outer = nullptr;
+    int32_t *nodes_chunkptr = nullptr;
     FusedRow *fused_rows = nullptr;
     int32_t *fused_src = nullptr;
     Tile *tiles_fused = nullptr;
@@ -109,7 +115,7 @@ struct rgnn_graph {
     int32_t chunk = rgnn::kChunkEdges;
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
-    int64_t n_tiles_outer = 0, n_tiles_fused = 0;
+    int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_huge_vdst = 0, n_big_seg = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
@@ -240,8 +246,19 @@ struct FusedArgs {
     int softmax = 0;
     float *T = nullptr;           // [V, d_out]
     float *vstat = nullptr;       // [V, 2] (softmax)
+    // S given (softmax == 0): write the segment means S_vs = (1/c) sum h_u
+    // themselves, at the segment's by-relation position [V, d_in], no transform
+    float *S = nullptr;
 };
 rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s);
+
+// Outer-product chunks of the backward: partial[c] (D x D, D = 64) = sum over
+// the rows of chunk c of X[row]^T Gm[gather ? gather[row] : row].
+rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather,
+                                const float *X, const float *Gm, float *partial, hipStream_t s);
+// dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (D x D each).
+rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW,
+                             hipStream_t s);
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);
 rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
 
@@ -267,6 +284,12 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                                const float *w_src, const float *w_dst, int d_in, int d_out,
                                float slope, const float *saved, const float *Gm, float *dh,
                                float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
+                               hipStream_t s, size_t *need);
+
+// RGCN backward (rgcn_backward.hip), the same convention for need.
+rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float *W, const float *W0,
+                               int d_in, int d_out, int flags, const float *out, const float *Gm,
+                               float *dh, float *dW, float *dW0, void *ws, size_t ws_bytes,
                                hipStream_t s, size_t *need);
 
 }  // namespace rgnn

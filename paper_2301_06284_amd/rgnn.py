@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "librgnn.so")
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PLAN_AUTO, PLAN_TRANSFORM_FIRST, PLAN_AGGREGATE_FIRST = 0, 1, 2
 LAYER_RGCN, LAYER_RGAT, LAYER_HGT, LAYER_RGAT_BACKWARD, LAYER_SEGMENT_GEMM = 0, 1, 2, 3, 4
+LAYER_RGCN_BACKWARD = 5
 SOFTMAX_PER_DST, SOFTMAX_PER_DST_REL = 0, 1
 FLAG_RELU, FLAG_RESIDUAL, FLAG_A_LINEAR = 1, 2, 4
 GRAPH_HOST_ONLY = 1
@@ -31,7 +32,7 @@ INDEX_KINDS = {
 EXPORTED = [
     "rgnn_graph_create_coo", "rgnn_graph_create_csr", "rgnn_graph_destroy", "rgnn_graph_info",
     "rgnn_graph_export", "rgnn_workspace_size", "rgnn_select_plan", "rgcn_forward",
-    "rgat_forward", "hgt_forward", "rgat_backward", "rgnn_segment_gemm",
+    "rgat_forward", "hgt_forward", "rgat_backward", "rgcn_backward", "rgnn_segment_gemm",
     "rgnn_segment_gemm_workspace_size", "rgnn_profile_enable", "rgnn_profile_count",
     "rgnn_profile_read", "rgnn_profile_reset", "rgnn_last_error", "rgnn_version",
 ]
@@ -72,6 +73,7 @@ def _load():
         "rgat_forward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp, sz, vp],
         "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, sz, vp],
         "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rgcn_backward": [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp],
         "rgnn_segment_gemm": [vp, i64, vp, vp, i32, vp, i32, i32, vp, i64, vp, vp, sz, vp],
         "rgnn_segment_gemm_workspace_size": [i64, i32, P(sz)],
         "rgnn_profile_enable": [i32],
@@ -234,6 +236,13 @@ def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, out, ws, d, heads, att_sca
                             _ptr(Wmsg), _ptr(mu), d, heads, float(att_scale), flags, _ptr(out),
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(stream)))
+
+
+def rgcn_backward(g, h, W, W0, out, grad_out, grad_h, grad_W, grad_W0, ws, d_in, d_out, flags=0,
+                  stream=None):
+    _check(_lib.rgcn_backward(g.handle, _ptr(h), _ptr(W), _ptr(W0), d_in, d_out, flags, _ptr(out),
+                              _ptr(grad_out), _ptr(grad_h), _ptr(grad_W), _ptr(grad_W0), _ptr(ws),
+                              0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def rgat_backward(g, h, W, w_src, w_dst, saved, grad_out, grad_h, grad_W, grad_w_src,

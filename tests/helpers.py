@@ -119,5 +119,25 @@ class Runner:
         torch.cuda.synchronize()
         return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
 
+    def rgcn_backward(self, W0=True, relu=False, out=None):
+        """out: the forward output the ReLU derivative is read from (numpy);
+        None runs this library's forward first."""
+        T, torch, rgnn = self.T, self.torch, self.rgnn
+        d = T["W"].shape[1]
+        R = T["W"].shape[0]
+        flags = rgnn.FLAG_RELU if relu else 0
+        o = None
+        if relu:
+            if out is None:
+                out = self.rgcn(W0=W0, relu=True)
+            o = torch.from_numpy(np.ascontiguousarray(out, np.float32)).to(self.dev)
+        gh = torch.full((self.g["N"], d), float("nan"), device=self.dev)
+        gW = torch.full((R, d, d), float("nan"), device=self.dev)
+        gW0 = torch.full((d, d), float("nan"), device=self.dev) if W0 else None
+        rgnn.rgcn_backward(self.G, T["h"], T["W"], T["W0"] if W0 else None, o, T["grad_out"], gh, gW,
+                           gW0, self.ws(rgnn.LAYER_RGCN_BACKWARD, d, d), d, d, flags)
+        torch.cuda.synchronize()
+        return (gh.cpu().numpy(), gW.cpu().numpy(), None if gW0 is None else gW0.cpu().numpy())
+
     def close(self):
         self.G.close()

@@ -10,7 +10,7 @@ Workloads (seeded, see workloads/synth.py):
   2  RGAT   880 000 nodes / 5.7 M edges / 96 relations, d = 64
   3  HGT    1.9 M nodes / 21 M edges / 7 relations, d = 64 = 4 x 16
   4  RGCN, RGAT at d = 128 on 2.5 M nodes / 16 M edges / 535 relations
-  5  RGAT backward on workload 2's graph
+  5  RGAT and RGCN backward on workload 2's graph
 """
 import numpy as np
 import pytest
@@ -60,6 +60,18 @@ def test_workload1_rgcn_all_rows(plan):
     got = run.rgcn(W0=True, plan=plan)
     ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])
     assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("relu", [False, True])
+def test_workload1_rgcn_backward_all_rows(relu):
+    g, t, run = load(1)
+    print(f"workload 1 rgcn backward relu={relu}", flush=True)
+    out = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"], relu=True) if relu else None
+    gh, gW, gW0 = run.rgcn_backward(W0=True, relu=relu, out=out)
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], relu=relu)
+    assert row_err(gh, dh) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    assert row_err(gW0, dW0) <= TOL
 
 
 def test_workload1_graph_index_bit_exact():
@@ -154,3 +166,26 @@ def test_workload5_rgat_backward():
     assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64)) <= TOL
     assert row_err(gs[rels], dws[rels]) <= TOL
     assert row_err(gt[rels], dwt[rels]) <= TOL
+
+
+def test_workload5_rgcn_backward():
+    """RGCN backward (with self-loop, identity activation) on the 880k-node
+    graph: dh at sampled sources, dW at sampled relations, dW0 in full."""
+    g, t, run = load(5)
+    print("workload 5 rgcn backward", flush=True)
+    W0 = t["W0"]
+    gh, gW, gW0 = run.rgcn_backward(W0=True, relu=False)
+    for a in (gh, gW, gW0):
+        assert np.isfinite(a).all()
+    rng = np.random.default_rng(56)
+    relcount = np.bincount(g["rel"], minlength=g["R"])
+    rels = np.r_[np.argsort(relcount)[:3], [20]]
+    outdeg = np.bincount(g["src"], minlength=g["N"])
+    nodes = np.unique(np.r_[rng.choice(g["N"], 60, replace=False), np.argsort(-outdeg)[:4],
+                            np.flatnonzero(outdeg == 0)[:4]])
+    nm = np.zeros(g["N"], np.uint8); nm[nodes] = 1
+    rm = np.zeros(g["R"], np.uint8); rm[rels] = 1
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], W0, t["grad_out"], node_mask=nm, rel_mask=rm)
+    assert row_err(gh[nodes], dh[nodes]) <= TOL
+    assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64)) <= TOL
+    assert row_err(gW0, dW0) <= TOL

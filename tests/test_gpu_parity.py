@@ -252,6 +252,40 @@ def test_rgat_backward_small(kind):
     assert row_err(gt, dwt) <= TOL
 
 
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("W0,relu", [(True, False), (False, False), (True, True), (False, True)])
+def test_rgcn_backward_small(kind, W0, relu):
+    g = graph(kind, E=3000)
+    t = workloads.tiny_tensors(31, g, 64, 64)
+    w0 = t["W0"] if W0 else None
+    print(f"rgcn backward {kind} W0={W0} relu={relu}", flush=True)
+    # the ReLU derivative is read from the oracle's forward output, so both
+    # sides take the same mask
+    out = oracle.rgcn_forward(g, t["h"], t["W"], w0, relu=True) if relu else None
+    run = Runner(g, t)
+    gh, gW, gW0 = run.rgcn_backward(W0=W0, relu=relu, out=out)
+    run.close()
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], w0, t["grad_out"], relu=relu)
+    assert row_err(gh, dh) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    if W0:
+        assert row_err(gW0, dW0) <= TOL
+
+
+def test_rgcn_backward_after_forward():
+    """Forward then backward through this library (the mask from its own output)."""
+    g = graph("hub", seed=32, E=3000)
+    t = workloads.tiny_tensors(32, g, 64, 64)
+    print("rgcn forward + backward", flush=True)
+    run = Runner(g, t)
+    gh, gW, gW0 = run.rgcn_backward(W0=True, relu=True)
+    run.close()
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], relu=True)
+    assert row_err(gh, dh) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    assert row_err(gW0, dW0) <= TOL
+
+
 def test_forward_bitwise_deterministic():
     g = graph("hub", seed=12)
     t = workloads.tiny_tensors(12, g, 64, 64, heads=4, att_var=1.0)
