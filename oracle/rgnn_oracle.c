@@ -1,6 +1,6 @@
 /*
  * rgnn_oracle.c -- plain, slow, fp64 CPU reference of the RGCN, RGAT and HGT
- * layers and of the RGAT and RGCN backward passes.
+ * layers and of their backward passes.
  *
  * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
  * benchmark's CPU-baseline leg may load this library.  It shares no code,
@@ -690,6 +690,196 @@ int oracle_rgcn_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
         }
     }
     free(need); free(cnt); free(P); free(Gp); free(xv); free(xu); free(m);
+    free_in_lists(&a);
+    return err ? -3 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* HGT backward for the loss L = sum(out * G) (G = grad_out): the chain rule of
+ * the HGT layer above.  With c_r = mu[r] * att_scale and kw_e,i = K_s,i Watt[r][i]:
+ *   dagg_t = G_t Wa[tau(t)]^T (a_linear, else G_t);  dWa[tau(t)] += agg_t^T G_t
+ *   dh_t  += G_t                                              (residual)
+ *   for every in-edge e = (s -> t, r) and head i:
+ *     dalpha = dagg_t,i . msg_e,i;  s_t,i = sum_e alpha dalpha;  da = alpha (dalpha - s_t,i)
+ *     dmsg = alpha dagg_t,i:   dWmsg[r][i] += V_s,i^T dmsg;  dV_s,i += dmsg Wmsg[r][i]^T
+ *     dkw = da c_r Q_t,i:      dWatt[r][i] += K_s,i^T dkw;   dK_s,i += dkw Watt[r][i]^T
+ *     dQ_t,i += da c_r kw_e,i;  dmu[r] += da att_scale (kw_e,i . Q_t,i)
+ *   for every node n (X in K, Q, V):
+ *     dWx[tau(n)] += h_n^T dX_n;  dh_n += dX_n Wx[tau(n)]^T
+ * K, Q, V are computed once per node (node-level linears); every edge term is
+ * computed per edge.  Sums run over destinations in increasing id, their
+ * in-edges in edge-id order, then over nodes in increasing id.  dWa may be
+ * NULL when a_linear is 0. */
+int oracle_hgt_backward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d, int32_t heads,
+                        const int32_t *src, const int32_t *dst, const int32_t *rel,
+                        const int32_t *ntype, const float *h, const float *Wk, const float *Wq,
+                        const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
+                        const float *mu, double att_scale, int32_t residual, int32_t a_linear,
+                        const float *G, double *dh, double *dWk, double *dWq, double *dWv,
+                        double *dWa, double *dWatt, double *dWmsg, double *dmu)
+{
+    if (check_coo(N, E, R, src, dst, rel) || T <= 0 || d <= 0 || d > 512 || heads <= 0 ||
+        d % heads)
+        return -1;
+    for (int64_t n = 0; n < N; ++n)
+        if (ntype[n] < 0 || ntype[n] >= T) return -1;
+    const int H = heads, dk = d / heads;
+    in_lists a;
+    int rc = build_in_lists(N, E, dst, &a);
+    if (rc) { free_in_lists(&a); return rc; }
+    const size_t nd = (size_t)(N > 0 ? N : 1) * d;
+    double *K = (double *)malloc(nd * sizeof(double));
+    double *Q = (double *)malloc(nd * sizeof(double));
+    double *V = (double *)malloc(nd * sizeof(double));
+    double *dK = (double *)calloc(nd, sizeof(double));
+    double *dQ = (double *)calloc(nd, sizeof(double));
+    double *dV = (double *)calloc(nd, sizeof(double));
+    double *x = (double *)malloc((size_t)d * sizeof(double));
+    double *agg = (double *)malloc((size_t)d * sizeof(double));
+    double *dagg = (double *)malloc((size_t)d * sizeof(double));
+    double *sv = (double *)malloc((size_t)H * sizeof(double));
+    double *mx = (double *)malloc((size_t)H * sizeof(double));
+    double *sm = (double *)malloc((size_t)H * sizeof(double));
+    double *kw = NULL, *msg = NULL, *al = NULL, *dal = NULL;
+    int64_t cap = 0;
+    int err = !K || !Q || !V || !dK || !dQ || !dV || !x || !agg || !dagg || !sv || !mx || !sm;
+    if (!err) {
+        for (int64_t n = 0; n < N; ++n) {   /* node-level K, Q, V */
+            load_row(h, n, d, x);
+            const size_t wo = (size_t)ntype[n] * d * d;
+            vecmat(x, Wk + wo, d, d, 0, d, K + (size_t)n * d);
+            vecmat(x, Wq + wo, d, d, 0, d, Q + (size_t)n * d);
+            vecmat(x, Wv + wo, d, d, 0, d, V + (size_t)n * d);
+        }
+        memset(dh, 0, (size_t)N * d * sizeof(double));
+        memset(dWk, 0, (size_t)T * d * d * sizeof(double));
+        memset(dWq, 0, (size_t)T * d * d * sizeof(double));
+        memset(dWv, 0, (size_t)T * d * d * sizeof(double));
+        if (dWa) memset(dWa, 0, (size_t)T * d * d * sizeof(double));
+        memset(dWatt, 0, (size_t)R * H * dk * dk * sizeof(double));
+        memset(dWmsg, 0, (size_t)R * H * dk * dk * sizeof(double));
+        memset(dmu, 0, (size_t)R * sizeof(double));
+    }
+    for (int64_t t = 0; t < N && !err; ++t) {
+        const int64_t p0 = a.ptr[t], deg = a.ptr[t + 1] - p0;
+        const float *Gt = G + (size_t)t * d;
+        const double *Qt = Q + (size_t)t * d;
+        if (deg > cap) {
+            free(kw); free(msg); free(al); free(dal);
+            cap = deg;
+            kw = (double *)malloc((size_t)cap * d * sizeof(double));
+            msg = (double *)malloc((size_t)cap * d * sizeof(double));
+            al = (double *)malloc((size_t)cap * H * sizeof(double));
+            dal = (double *)malloc((size_t)cap * H * sizeof(double));
+            if (!kw || !msg || !al || !dal) { err = 1; break; }
+        }
+        /* forward: scores, softmax, messages, agg */
+        for (int64_t p = 0; p < deg; ++p) {
+            const int64_t e = a.eid[p0 + p];
+            const int64_t sn = src[e];
+            const int r = rel[e];
+            for (int i = 0; i < H; ++i) {
+                const float *Wat = Watt + ((size_t)r * H + i) * dk * dk;
+                const float *Wms = Wmsg + ((size_t)r * H + i) * dk * dk;
+                vecmat(K + (size_t)sn * d + i * dk, Wat, dk, dk, 0, dk, kw + p * d + i * dk);
+                vecmat(V + (size_t)sn * d + i * dk, Wms, dk, dk, 0, dk, msg + p * d + i * dk);
+                double dot = 0.0;
+                for (int j = 0; j < dk; ++j) dot += kw[p * d + i * dk + j] * Qt[i * dk + j];
+                al[p * H + i] = dot * (double)mu[r] * att_scale;
+            }
+        }
+        for (int i = 0; i < H; ++i) { mx[i] = -INFINITY; sm[i] = 0.0; sv[i] = 0.0; }
+        for (int64_t p = 0; p < deg; ++p)
+            for (int i = 0; i < H; ++i) if (al[p * H + i] > mx[i]) mx[i] = al[p * H + i];
+        for (int64_t p = 0; p < deg; ++p)
+            for (int i = 0; i < H; ++i) sm[i] += exp(al[p * H + i] - mx[i]);
+        for (int64_t p = 0; p < deg; ++p)
+            for (int i = 0; i < H; ++i) al[p * H + i] = exp(al[p * H + i] - mx[i]) / sm[i];
+        for (int j = 0; j < d; ++j) agg[j] = 0.0;
+        for (int64_t p = 0; p < deg; ++p)
+            for (int j = 0; j < d; ++j) agg[j] += al[p * H + j / dk] * msg[p * d + j];
+        /* output linear and residual */
+        if (a_linear) {
+            const float *Wat = Wa + (size_t)ntype[t] * d * d;
+            for (int i = 0; i < d; ++i) {
+                double s2 = 0.0;
+                for (int j = 0; j < d; ++j) s2 += (double)Wat[(size_t)i * d + j] * (double)Gt[j];
+                dagg[i] = s2;
+            }
+            if (dWa) {
+                double *dw = dWa + (size_t)ntype[t] * d * d;
+                for (int i = 0; i < d; ++i)
+                    for (int j = 0; j < d; ++j) dw[(size_t)i * d + j] += agg[i] * (double)Gt[j];
+            }
+        } else {
+            for (int j = 0; j < d; ++j) dagg[j] = (double)Gt[j];
+        }
+        if (residual)
+            for (int j = 0; j < d; ++j) dh[(size_t)t * d + j] += (double)Gt[j];
+        /* softmax backward */
+        for (int64_t p = 0; p < deg; ++p)
+            for (int i = 0; i < H; ++i) {
+                double da = 0.0;
+                for (int j = i * dk; j < (i + 1) * dk; ++j) da += dagg[j] * msg[p * d + j];
+                dal[p * H + i] = da;
+                sv[i] += al[p * H + i] * da;
+            }
+        for (int64_t p = 0; p < deg; ++p) {
+            const int64_t e = a.eid[p0 + p];
+            const int64_t sn = src[e];
+            const int r = rel[e];
+            const double c = (double)mu[r] * att_scale;
+            for (int i = 0; i < H; ++i) {
+                const double alpha = al[p * H + i];
+                const double da = alpha * (dal[p * H + i] - sv[i]);
+                const float *Wat = Watt + ((size_t)r * H + i) * dk * dk;
+                const float *Wms = Wmsg + ((size_t)r * H + i) * dk * dk;
+                double *dWat = dWatt + ((size_t)r * H + i) * dk * dk;
+                double *dWms = dWmsg + ((size_t)r * H + i) * dk * dk;
+                const double *Ks = K + (size_t)sn * d + i * dk, *Vs = V + (size_t)sn * d + i * dk;
+                const double *kwe = kw + p * d + i * dk, *Qti = Qt + i * dk;
+                const double *dg = dagg + i * dk;
+                for (int j = 0; j < dk; ++j)
+                    for (int k = 0; k < dk; ++k) {
+                        dWms[(size_t)j * dk + k] += Vs[j] * alpha * dg[k];
+                        dWat[(size_t)j * dk + k] += Ks[j] * da * c * Qti[k];
+                    }
+                for (int j = 0; j < dk; ++j) {
+                    double sv2 = 0.0, sk = 0.0;
+                    for (int k = 0; k < dk; ++k) {
+                        sv2 += alpha * dg[k] * (double)Wms[(size_t)j * dk + k];
+                        sk += da * c * Qti[k] * (double)Wat[(size_t)j * dk + k];
+                    }
+                    dV[(size_t)sn * d + i * dk + j] += sv2;
+                    dK[(size_t)sn * d + i * dk + j] += sk;
+                    dQ[(size_t)t * d + i * dk + j] += da * c * kwe[j];
+                }
+                double kq = 0.0;
+                for (int j = 0; j < dk; ++j) kq += kwe[j] * Qti[j];
+                dmu[r] += da * att_scale * kq;
+            }
+        }
+    }
+    /* node-level linears */
+    for (int64_t n = 0; n < N && !err; ++n) {
+        load_row(h, n, d, x);
+        const size_t wo = (size_t)ntype[n] * d * d;
+        const double *dx[3] = {dK + (size_t)n * d, dQ + (size_t)n * d, dV + (size_t)n * d};
+        const float *Wx[3] = {Wk + wo, Wq + wo, Wv + wo};
+        double *dWx[3] = {dWk + wo, dWq + wo, dWv + wo};
+        for (int m = 0; m < 3; ++m) {
+            for (int i = 0; i < d; ++i) {
+                double s2 = 0.0;
+                for (int j = 0; j < d; ++j) {
+                    dWx[m][(size_t)i * d + j] += x[i] * dx[m][j];
+                    s2 += dx[m][j] * (double)Wx[m][(size_t)i * d + j];
+                }
+                dh[(size_t)n * d + i] += s2;
+            }
+        }
+    }
+    free(K); free(Q); free(V); free(dK); free(dQ); free(dV); free(x); free(agg); free(dagg);
+    free(sv); free(mx); free(sm); free(kw); free(msg); free(al); free(dal);
     free_in_lists(&a);
     return err ? -3 : 0;
 }

@@ -498,6 +498,80 @@ def test_rgcn_backward_masks():
     assert part[2] is None
 
 
+# ---------------------------------------------------------------- HGT backward
+def hgt_torch_dense(g, p, H, scale, residual, a_linear):
+    """The HGT layer on dense per-relation adjacency (torch, for autograd)."""
+    N, R = g["N"], g["R"]
+    h = p["h"]
+    d = h.shape[1]
+    dk = d // H
+    nt = torch.tensor(g["ntype"], dtype=torch.long)
+    K = torch.einsum("ni,nij->nj", h, p["Wk"][nt]).reshape(N, H, dk)
+    Q = torch.einsum("ni,nij->nj", h, p["Wq"][nt]).reshape(N, H, dk)
+    V = torch.einsum("ni,nij->nj", h, p["Wv"][nt]).reshape(N, H, dk)
+    KW = torch.einsum("shc,rhcj->rshj", K, p["Watt"])
+    att = torch.einsum("rshj,thj->rtsh", KW, Q) * (p["mu"][:, None, None, None] * scale)
+    msg = torch.einsum("shc,rhcj->rshj", V, p["Wmsg"])
+    A = torch.tensor(dense_adj(g))
+    mask = (A > 0)[..., None].expand_as(att)
+    mx = torch.where(mask, att, torch.tensor(-torch.inf, dtype=att.dtype)).amax(dim=(0, 2), keepdim=True)
+    mx = torch.where(torch.isfinite(mx), mx, torch.zeros_like(mx)).detach()
+    ex = torch.exp(torch.where(mask, att, mx.expand_as(att)) - mx) * A[..., None]
+    den = ex.sum(dim=(0, 2), keepdim=True)
+    al = ex / torch.where(den > 0, den, torch.ones_like(den))
+    agg = torch.einsum("rtsh,rshj->thj", al, msg).reshape(N, d)
+    out = torch.einsum("ni,nij->nj", agg, p["Wa"][nt]) if a_linear else agg
+    return out + h if residual else out
+
+
+HGT_PARAMS = ("h", "Wk", "Wq", "Wv", "Wa", "Watt", "Wmsg", "mu")
+
+
+@pytest.mark.parametrize("kind,H", [("random", 1), ("hub", 2), ("dups", 4), ("isolated", 2), ("empty", 2)])
+@pytest.mark.parametrize("residual,a_linear", [(True, True), (False, False), (True, False)])
+def test_hgt_backward_vs_autograd(kind, H, residual, a_linear):
+    g = tiny_graph(71, N=13, E=60, R=3, T=3, kind=kind)
+    t = tiny_tensors(71, g, 8, 8, heads=H)
+    t["mu"] = (1.0 + 0.3 * np.arange(3)).astype(np.float32)   # distinct priors
+    scale = 0.7
+    ts = {k: torch.tensor(t[k], dtype=torch.float64, requires_grad=True) for k in HGT_PARAMS}
+    out = hgt_torch_dense(g, ts, H, scale, residual, a_linear)
+    Gt = t["grad_out"][:, :8].copy()
+    (out * torch.tensor(Gt, dtype=torch.float64)).sum().backward()
+    got = oracle.hgt_backward(g, *(t[k] for k in HGT_PARAMS), Gt, heads=H, att_scale=scale,
+                              residual=residual, a_linear=a_linear)
+    for k in HGT_PARAMS:
+        ref = ts[k].grad
+        if k == "Wa" and not a_linear:
+            assert got["dWa"] is None
+            continue
+        np.testing.assert_allclose(got["d" + k], ref.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+
+
+def test_hgt_backward_finite_differences():
+    """Central differences of L = sum(out * G) for every parameter entry."""
+    g = tiny_graph(72, N=6, E=16, R=2, T=2, kind="dups")
+    t = tiny_tensors(72, g, 4, 4, heads=2)
+    t["mu"] = np.array([1.0, 0.6], np.float32)
+    G = t["grad_out"][:, :4].copy()
+
+    def loss(tt):
+        out = oracle.hgt_forward(g, *(tt[k] for k in HGT_PARAMS), heads=2, att_scale=0.5)
+        return float((out * G).sum())
+    got = oracle.hgt_backward(g, *(t[k] for k in HGT_PARAMS), G, heads=2, att_scale=0.5)
+    for k in HGT_PARAMS:
+        base = t[k]
+        fd = np.zeros(base.shape)
+        for idx in np.ndindex(base.shape):
+            step = 1e-2 * max(1e-2, abs(float(base[idx])))
+            plus, minus = base.copy(), base.copy()
+            plus[idx] = np.float32(base[idx] + step)
+            minus[idx] = np.float32(base[idx] - step)
+            denom = float(plus[idx]) - float(minus[idx])
+            fd[idx] = (loss(dict(t, **{k: plus})) - loss(dict(t, **{k: minus}))) / denom
+        np.testing.assert_allclose(got["d" + k], fd, rtol=2e-3, atol=2e-4, err_msg=k)
+
+
 # ---------------------------------------------------------------- integer preprocessing
 @pytest.mark.parametrize("kind", KINDS + ["complete"])
 def test_graph_index_against_python_sets(kind):
