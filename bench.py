@@ -14,7 +14,7 @@ device synchronisations.  The line also carries:
   cpu_baseline  the fp64 oracle timed on the host's cores on a bounded sample
                 of destinations of the same workload;
   layers        edges/s of the other layers and workloads (RGCN, HGT, RGCN and
-                RGAT at d = 128, RGAT and RGCN backward, both RGAT plans).
+                RGAT at d = 128, RGAT, RGCN and HGT backward, both RGAT plans).
 """
 from __future__ import annotations
 
@@ -332,6 +332,21 @@ def main():
         kh = kernel_profile(rgnn, torch, fnh, max(3, K // 2))
         layers["hgt_fwd_mag_like_1p9m"] = {"edges_per_s": c.info["num_edges"] / (msh * 1e-3), "ms": msh,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in kh.items()}}
+        # HGT backward (recomputes the forward inside the call)
+        log("workload 3: HGT backward")
+        N3, R3, T3 = c.info["num_nodes"], c.info["num_rels"], c.g["T"]
+        grads = dict(dh=torch.empty(N3, d3, device=c.dev), dWk=torch.empty(T3, d3, d3, device=c.dev),
+                     dWq=torch.empty(T3, d3, d3, device=c.dev), dWv=torch.empty(T3, d3, d3, device=c.dev),
+                     dWa=torch.empty(T3, d3, d3, device=c.dev), dWatt=torch.empty(R3, 4, 16, 16, device=c.dev),
+                     dWmsg=torch.empty(R3, 4, 16, 16, device=c.dev), dmu=torch.empty(R3, device=c.dev))
+        wsb3 = c.ws(rgnn.LAYER_HGT_BACKWARD, d3, d3, 4)
+        fnhb = lambda: rgnn.hgt_backward(c.G, c.T["h"], c.T["Wk"], c.T["Wq"], c.T["Wv"], c.T["Wa"], c.T["Watt"],
+                                         c.T["Wmsg"], c.T["mu"], c.T["grad_out"], grads, wsb3, d3, 4, 0.25)
+        mshb = time_steps(torch, fnhb, K, W)
+        khb = kernel_profile(rgnn, torch, fnhb, max(3, K // 2))
+        layers["hgt_bwd_mag_like_1p9m"] = {"edges_per_s": c.info["num_edges"] / (mshb * 1e-3), "ms": mshb,
+                                           "kernels_ms": {k: round(v[1], 4) for k, v in khb.items()}}
+        del grads, wsb3
         c.close()
         del out, ws
 

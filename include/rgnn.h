@@ -67,7 +67,8 @@ typedef enum {
     RGNN_LAYER_HGT = 2,
     RGNN_LAYER_RGAT_BACKWARD = 3,
     RGNN_LAYER_SEGMENT_GEMM = 4,
-    RGNN_LAYER_RGCN_BACKWARD = 5
+    RGNN_LAYER_RGCN_BACKWARD = 5,
+    RGNN_LAYER_HGT_BACKWARD = 6
 } rgnn_layer;
 
 enum { RGNN_SOFTMAX_PER_DST = 0, RGNN_SOFTMAX_PER_DST_REL = 1 };
@@ -239,6 +240,23 @@ rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W,
                           int32_t d_in, int32_t d_out, int32_t flags, const float *out,
                           const float *grad_out, float *grad_h, float *grad_W, float *grad_W0,
                           void *ws, size_t ws_bytes, void *stream);
+
+/* HGT backward for the HGT layer above: the chain rule of its definition
+ * (Section "Backward Propagation" derives the backward from the forward) for
+ * the loss L = sum(out * grad_out).  Arguments as in hgt_forward plus
+ * grad_out [N, d]; writes grad_h [N, d], grad_Wk, grad_Wq, grad_Wv [T, d, d],
+ * grad_Wa [T, d, d] (with RGNN_FLAG_A_LINEAR; otherwise not written, may be
+ * NULL), grad_Watt, grad_Wmsg [R, heads, dk, dk] and grad_mu [R].  The forward
+ * is recomputed inside the call.  d = 64 with heads in {1, 2, 4}.  Workspace:
+ * rgnn_workspace_size(RGNN_LAYER_HGT_BACKWARD, d, d, heads).  Results are
+ * reproducible except the K|V gradient rows of sources with more than 64
+ * out-edges, which are summed with float atomics. */
+rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk, const float *Wq,
+                         const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
+                         const float *mu, int32_t d, int32_t heads, float att_scale, int32_t flags,
+                         const float *grad_out, float *grad_h, float *grad_Wk, float *grad_Wq,
+                         float *grad_Wv, float *grad_Wa, float *grad_Watt, float *grad_Wmsg,
+                         float *grad_mu, void *ws, size_t ws_bytes, void *stream);
 
 /* Segment MM: the GEMM template of Section "The GEMM Template and the
  * Traversal Template", Y[S] = X[G] x W[T]:

@@ -294,6 +294,14 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
         *bytes = need;
         return RGNN_OK;
     }
+    case RGNN_LAYER_HGT_BACKWARD: {
+        size_t need = 0;
+        hgt_backward_impl(g, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, d_out,
+                          heads, 0.f, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                          nullptr, nullptr, 0, nullptr, &need);
+        *bytes = need;
+        return RGNN_OK;
+    }
     case RGNN_LAYER_RGCN_BACKWARD: {
         size_t need = 0;
         rgcn_backward_impl(g, nullptr, nullptr, nullptr, d_in, d_out, 0, nullptr, nullptr, nullptr,
@@ -526,6 +534,30 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
                               grad_h, grad_W, grad_w_src, grad_w_dst, ws, ws_bytes,
                               (hipStream_t)stream, nullptr);
+}
+
+extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk,
+                                    const float *Wq, const float *Wv, const float *Wa,
+                                    const float *Watt, const float *Wmsg, const float *mu, int32_t d,
+                                    int32_t heads, float att_scale, int32_t flags, const float *grad_out,
+                                    float *grad_h, float *grad_Wk, float *grad_Wq, float *grad_Wv,
+                                    float *grad_Wa, float *grad_Watt, float *grad_Wmsg, float *grad_mu,
+                                    void *ws, size_t ws_bytes, void *stream)
+{
+    rgnn_status st = check_graph(g);
+    if (st != RGNN_OK) return st;
+    if (!h || !Wk || !Wq || !Wv || !Watt || !Wmsg || !mu || !grad_out || !grad_h || !grad_Wk ||
+        !grad_Wq || !grad_Wv || !grad_Watt || !grad_Wmsg || !grad_mu)
+        return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (flags & ~(RGNN_FLAG_RESIDUAL | RGNN_FLAG_A_LINEAR)) return fail(RGNN_EINVAL, "unknown HGT flag");
+    if ((flags & RGNN_FLAG_A_LINEAR) && !Wa) return fail(RGNN_EINVAL, "Wa is NULL");
+    if (d != 64) return fail(RGNN_EUNSUPPORTED, "HGT backward supports d = 64");
+    if (heads != 1 && heads != 2 && heads != 4)
+        return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2 or 4");
+    if (!std::isfinite(att_scale)) return fail(RGNN_EINVAL, "att_scale must be finite");
+    return hgt_backward_impl(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, d, heads, att_scale, flags, grad_out,
+                             grad_h, grad_Wk, grad_Wq, grad_Wv, (flags & RGNN_FLAG_A_LINEAR) ? grad_Wa : nullptr,
+                             grad_Watt, grad_Wmsg, grad_mu, ws, ws_bytes, (hipStream_t)stream, nullptr);
 }
 
 extern "C" rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W,

@@ -486,11 +486,12 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // partial[c] = sum over its segments of Sa[seg]^T (d_in) x G[dst(seg)] (d_out);
 // yvec[c]   = sum over its segments of ysum[seg] * h[dst(seg)].
 // YS: also sum ysum[row] * h[v] per chunk (the RGAT dwt' term); GATHER: the
-// second operand's row (and h's) is vsegdst[row], else the row itself.
-template <bool YS, bool GATHER>
+// second operand's row (and h's) is vsegdst[row], else the row itself; GA:
+// the first operand's row is gathered the same way.  lda, ldb: row strides.
+template <bool YS, bool GATHER, bool GA>
 __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
-                                                         const float *Sa,
-                                                         const float *Gm, const float *h,
+                                                         const float *Sa, int lda,
+                                                         const float *Gm, int ldb, const float *h,
                                                          const float *ysum, float *partial,
                                                          float *yvec)
 {
@@ -526,8 +527,8 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
 #pragma unroll
         for (int sl = 0; sl < SL; ++sl) {
             const int row = row_of(k0, sl);
-            ra[sl] = ld4(Sa + (size_t)row * D + c4);
-            rb[sl] = ld4(Gm + (size_t)v[sl] * D + c4);
+            ra[sl] = ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + c4);
+            rb[sl] = ld4(Gm + (size_t)v[sl] * ldb + c4);
             if (YS) {
                 rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
                 ry[sl] = ysum[row];
@@ -697,18 +698,23 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
 
 int bwd_outer_rows() { return kOuterRows; }
 
-rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather,
-                                const float *X, const float *Gm, float *partial, hipStream_t s)
+rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x,
+                                const float *X, int ldx, const float *Gm, int ldg, float *partial,
+                                hipStream_t s)
 {
     if (nchunks == 0) return RGNN_OK;
     {
         LaunchScope ls("outer_gemm", s);
-        if (gather)
-            hipLaunchKernelGGL((outer_gemm_kernel<false, true>), dim3((unsigned)nchunks), dim3(256), 0, s,
-                               chunks, gather, X, Gm, nullptr, nullptr, partial, nullptr);
+        const dim3 grid((unsigned)nchunks);
+        if (gather && gather_x)
+            hipLaunchKernelGGL((outer_gemm_kernel<false, true, true>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else if (gather)
+            hipLaunchKernelGGL((outer_gemm_kernel<false, true, false>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
         else
-            hipLaunchKernelGGL((outer_gemm_kernel<false, false>), dim3((unsigned)nchunks), dim3(256), 0, s,
-                               chunks, nullptr, X, Gm, nullptr, nullptr, partial, nullptr);
+            hipLaunchKernelGGL((outer_gemm_kernel<false, false, false>), grid, dim3(256), 0, s,
+                               chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
     }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "outer_gemm launch");
@@ -817,8 +823,8 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "pair_gemv launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
-        hipLaunchKernelGGL((outer_gemm_kernel<true, true>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
-                           g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, Gm, h, w.ysum,
+        hipLaunchKernelGGL((outer_gemm_kernel<true, true, false>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
+                           g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, D, Gm, D, h, w.ysum,
                            w.partial, w.yvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");

@@ -314,6 +314,12 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         build_tiles(all, bwd_outer_rows(), x.tiles_nodes_outer);   // node chunks (self-loop dW0)
         g->n_tiles_nodes_outer = (int64_t)x.tiles_nodes_outer.size();
         x.nodes_chunkptr = {0, (int32_t)g->n_tiles_nodes_outer};
+        // chunks over the nodes grouped by type (per-type weight gradients)
+        build_tiles(x.ntype_ptr, bwd_outer_rows(), x.tiles_types_outer);
+        g->n_tiles_types_outer = (int64_t)x.tiles_types_outer.size();
+        x.types_chunkptr.assign((size_t)T + 1, 0);
+        for (const Tile &t : x.tiles_types_outer) x.types_chunkptr[(size_t)t.type + 1]++;
+        for (int32_t t = 0; t < T; ++t) x.types_chunkptr[t + 1] += x.types_chunkptr[t];
         x.rel_chunkptr.assign((size_t)R + 1, 0);
         for (const Tile &t : x.tiles_outer) x.rel_chunkptr[(size_t)t.type + 1]++;
         for (int32_t r = 0; r < R; ++r) x.rel_chunkptr[r + 1] += x.rel_chunkptr[r];
@@ -363,6 +369,9 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_nodes_outer, x.tiles_nodes_outer.data(),
                          x.tiles_nodes_outer.size() * sizeof(Tile)});
     add32(&d.nodes_chunkptr, x.nodes_chunkptr);
+    parts.push_back(Part{(void **)&d.tiles_types_outer, x.tiles_types_outer.data(),
+                         x.tiles_types_outer.size() * sizeof(Tile)});
+    add32(&d.types_chunkptr, x.types_chunkptr);
     parts.push_back(Part{(void **)&d.invcnt_byrel, x.invcnt_byrel.data(), x.invcnt_byrel.size() * sizeof(float)});
     parts.push_back(Part{(void **)&d.tiles_fused, x.tiles_fused.data(), x.tiles_fused.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.fused_rows, x.fused_rows.data(), x.fused_rows.size() * sizeof(FusedRow)});

@@ -58,6 +58,7 @@ struct HK {
     const float *KV, *QP, *Wmsg;
     int R;
     float *agg, *partial;
+    float *saved;          // [N, H, 2] per destination and head (max, sum), or NULL
 };
 
 // Value of lane jj of this lane's head (LH aligned lanes).  A DPP quad
@@ -142,6 +143,9 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
     auto flush = [&](int jj) {
         if (slot < 0) {
             st4(k.agg + (size_t)(dst0 + jj) * D + gl * 4, scale4(agg, s > 0.f ? 1.f / s : 0.f));
+            if (k.saved && gl % LH == 0)
+                *reinterpret_cast<float2 *>(k.saved + ((size_t)(dst0 + jj) * H + head) * 2) =
+                    make_float2(s > 0.f ? m : 0.f, s);
         } else {
             float *pr = k.partial + (size_t)slot * (2 * H + D);
             if (gl % LH == 0) { pr[head * 2] = m; pr[head * 2 + 1] = s; }
@@ -242,7 +246,7 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
     k.vseg_rel = g->dev.vseg_rel; k.in_src = g->dev.in_src;
     k.KV = a.KV; k.QP = a.QP; k.Wmsg = a.Wmsg;
-    k.R = g->R; k.agg = a.agg; k.partial = a.partial;
+    k.R = g->R; k.agg = a.agg; k.partial = a.partial; k.saved = a.saved;
     const size_t wb = weight_bytes(g->R, a.heads);
     const bool use_lds = wb + stage_bytes() <= 160 * 1024;
     const size_t lds = stage_bytes() + (use_lds ? wb : 0);

@@ -222,15 +222,15 @@ rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float 
         FusedArgs fa;
         fa.g = g; fa.h = h; fa.d_in = D; fa.d_out = D; fa.S = w.Sb;
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
-        if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, w.Sb, Gp,
-                                      w.partial, s)) != RGNN_OK)
+        if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, 0, w.Sb, D,
+                                      Gp, D, w.partial, s)) != RGNN_OK)
             return st;
     }
     if ((st = launch_chunk_sum(w.partial, g->dev.rel_chunkptr, g->R, dW, s)) != RGNN_OK) return st;
     // dW0 = sum_v h_v^T Gp_v
     if (W0 && dW0) {
-        if ((st = launch_outer_chunks(g->dev.tiles_nodes_outer, g->n_tiles_nodes_outer, nullptr, h, Gp,
-                                      w.partial, s)) != RGNN_OK)
+        if ((st = launch_outer_chunks(g->dev.tiles_nodes_outer, g->n_tiles_nodes_outer, nullptr, 0, h, D, Gp,
+                                      D, w.partial, s)) != RGNN_OK)
             return st;
         if ((st = launch_chunk_sum(w.partial, g->dev.nodes_chunkptr, 1, dW0, s)) != RGNN_OK) return st;
     }

@@ -68,6 +68,8 @@ struct HostIndex {
     std::vector<float> invcnt_byrel;      // 1 / c_{v,r} of each virtual segment, by-relation order
     std::vector<Tile> tiles_nodes_outer;  // outer-product chunks over all nodes
     std::vector<int32_t> nodes_chunkptr;  // {0, number of node chunks}
+    std::vector<Tile> tiles_types_outer;  // outer-product chunks over the nodes of each type
+    std::vector<int32_t> types_chunkptr;  // chunks per node type [T+1]
     std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
     // out-edges (source-major view of the sorted in-edges), for the backward pass
     std::vector<int32_t> out_ptr, out_pos, out_vseg, out_rel, out_pair;
@@ -93,6 +95,8 @@ struct DeviceIndex {
     float *invcnt_byrel = nullptr;
     Tile *tiles_nodes_outer = nullptr;
     int32_t *nodes_chunkptr = nullptr;
+    Tile *tiles_types_outer = nullptr;
+    int32_t *types_chunkptr = nullptr;
     FusedRow *fused_rows = nullptr;
     int32_t *fused_src = nullptr;
     Tile *tiles_fused = nullptr;
@@ -115,7 +119,7 @@ struct rgnn_graph {
     int32_t chunk = rgnn::kChunkEdges;
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
-    int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0;
+    int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_huge_vdst = 0, n_big_seg = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
@@ -253,9 +257,11 @@ struct FusedArgs {
 rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s);
 
 // Outer-product chunks of the backward: partial[c] (D x D, D = 64) = sum over
-// the rows of chunk c of X[row]^T Gm[gather ? gather[row] : row].
-rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather,
-                                const float *X, const float *Gm, float *partial, hipStream_t s);
+// the rows of chunk c of X[x(row)]^T Gm[g(row)], g(row) = gather ? gather[row]
+// : row and x(row) = g(row) when gather_x, else row; ldx, ldg: row strides.
+rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x,
+                                const float *X, int ldx, const float *Gm, int ldg, float *partial,
+                                hipStream_t s);
 // dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (D x D each).
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW,
                              hipStream_t s);
@@ -271,6 +277,8 @@ struct HgtArgs {
     int d = 64;
     float *agg = nullptr;          // [N, d]
     float *partial = nullptr;      // [slots, 2*heads + d]
+    float *saved = nullptr;        // [N, heads, 2] softmax (max, sum) or NULL (split
+                                   // destinations: written by the partial merge)
 };
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
 // Wqp[r] (d x d) = mu[r] * scale * blockdiag over heads i of Watt[r, i]^T, so
@@ -285,6 +293,14 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                                float slope, const float *saved, const float *Gm, float *dh,
                                float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
                                hipStream_t s, size_t *need);
+
+// HGT backward (hgt_backward.hip), the same convention for need.
+rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
+                              const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
+                              const float *mu, int d, int heads, float att_scale, int flags,
+                              const float *Gm, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
+                              float *dWatt, float *dWmsg, float *dmu, void *ws, size_t ws_bytes,
+                              hipStream_t s, size_t *need);
 
 // RGCN backward (rgcn_backward.hip), the same convention for need.
 rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float *W, const float *W0,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "librgnn.so")
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PLAN_AUTO, PLAN_TRANSFORM_FIRST, PLAN_AGGREGATE_FIRST = 0, 1, 2
 LAYER_RGCN, LAYER_RGAT, LAYER_HGT, LAYER_RGAT_BACKWARD, LAYER_SEGMENT_GEMM = 0, 1, 2, 3, 4
-LAYER_RGCN_BACKWARD = 5
+LAYER_RGCN_BACKWARD, LAYER_HGT_BACKWARD = 5, 6
 SOFTMAX_PER_DST, SOFTMAX_PER_DST_REL = 0, 1
 FLAG_RELU, FLAG_RESIDUAL, FLAG_A_LINEAR = 1, 2, 4
 GRAPH_HOST_ONLY = 1
@@ -32,7 +32,8 @@ INDEX_KINDS = {
 EXPORTED = [
     "rgnn_graph_create_coo", "rgnn_graph_create_csr", "rgnn_graph_destroy", "rgnn_graph_info",
     "rgnn_graph_export", "rgnn_workspace_size", "rgnn_select_plan", "rgcn_forward",
-    "rgat_forward", "hgt_forward", "rgat_backward", "rgcn_backward", "rgnn_segment_gemm",
+    "rgat_forward", "hgt_forward", "rgat_backward", "rgcn_backward", "hgt_backward",
+    "rgnn_segment_gemm",
     "rgnn_segment_gemm_workspace_size", "rgnn_profile_enable", "rgnn_profile_count",
     "rgnn_profile_read", "rgnn_profile_reset", "rgnn_last_error", "rgnn_version",
 ]
@@ -74,6 +75,8 @@ def _load():
         "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, sz, vp],
         "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
         "rgcn_backward": [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp],
+        "hgt_backward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp,
+                         vp, vp, vp, sz, vp],
         "rgnn_segment_gemm": [vp, i64, vp, vp, i32, vp, i32, i32, vp, i64, vp, vp, sz, vp],
         "rgnn_segment_gemm_workspace_size": [i64, i32, P(sz)],
         "rgnn_profile_enable": [i32],
@@ -236,6 +239,17 @@ def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, out, ws, d, heads, att_sca
                             _ptr(Wmsg), _ptr(mu), d, heads, float(att_scale), flags, _ptr(out),
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(stream)))
+
+
+def hgt_backward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, grad_out, grads, ws, d, heads, att_scale,
+                 flags=FLAG_RESIDUAL | FLAG_A_LINEAR, stream=None):
+    """grads: dict of output tensors dh, dWk, dWq, dWv, dWa (or None), dWatt, dWmsg, dmu."""
+    _check(_lib.hgt_backward(g.handle, _ptr(h), _ptr(Wk), _ptr(Wq), _ptr(Wv), _ptr(Wa), _ptr(Watt),
+                             _ptr(Wmsg), _ptr(mu), d, heads, float(att_scale), flags, _ptr(grad_out),
+                             _ptr(grads["dh"]), _ptr(grads["dWk"]), _ptr(grads["dWq"]), _ptr(grads["dWv"]),
+                             _ptr(grads.get("dWa")), _ptr(grads["dWatt"]), _ptr(grads["dWmsg"]),
+                             _ptr(grads["dmu"]), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                             _stream(stream)))
 
 
 def rgcn_backward(g, h, W, W0, out, grad_out, grad_h, grad_W, grad_W0, ws, d_in, d_out, flags=0,

@@ -119,6 +119,22 @@ class Runner:
         torch.cuda.synchronize()
         return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
 
+    def hgt_backward(self, heads, scale, flags=None):
+        T, torch, rgnn = self.T, self.torch, self.rgnn
+        d = T["h"].shape[1]
+        flags = rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR if flags is None else flags
+        N, R, NT = self.g["N"], T["Watt"].shape[0], T["Wk"].shape[0]
+        dk = d // heads
+        nan = lambda *shape: torch.full(shape, float("nan"), device=self.dev)
+        grads = dict(dh=nan(N, d), dWk=nan(NT, d, d), dWq=nan(NT, d, d), dWv=nan(NT, d, d),
+                     dWa=nan(NT, d, d) if flags & rgnn.FLAG_A_LINEAR else None,
+                     dWatt=nan(R, heads, dk, dk), dWmsg=nan(R, heads, dk, dk), dmu=nan(R))
+        rgnn.hgt_backward(self.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
+                          T["mu"], T["grad_out"], grads, self.ws(rgnn.LAYER_HGT_BACKWARD, d, d, heads),
+                          d, heads, scale, flags)
+        torch.cuda.synchronize()
+        return {k: (None if v is None else v.cpu().numpy()) for k, v in grads.items()}
+
     def rgcn_backward(self, W0=True, relu=False, out=None):
         """out: the forward output the ReLU derivative is read from (numpy);
         None runs this library's forward first."""

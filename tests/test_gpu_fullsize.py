@@ -189,3 +189,28 @@ def test_workload5_rgcn_backward():
     assert row_err(gh[nodes], dh[nodes]) <= TOL
     assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64)) <= TOL
     assert row_err(gW0, dW0) <= TOL
+
+
+@pytest.mark.parametrize("kind,heads", [("random", 4), ("hub", 2)])
+def test_hgt_backward_mid_size(kind, heads):
+    """HGT backward on a 20 000-node / 300 000-edge graph with 7 relations and
+    4 node types (thousands of work items and GEMM tiles, split destinations
+    for the hub kind), checked in full against the oracle (the 21 M-edge
+    workload itself is beyond the fp64 oracle's budget; bench.py runs it)."""
+    g = workloads.tiny_graph(36, N=20000, E=300000, R=7, T=4, kind=kind)
+    t = workloads.tiny_tensors(36, g, 64, 64, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)
+    scale = 1.0 / np.sqrt(64 // heads)
+    print(f"hgt backward mid-size {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(heads, scale)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=heads, att_scale=scale)
+    dk = 64 // heads
+    assert row_err(got["dh"], ref["dh"]) <= TOL
+    for k in ("dWk", "dWq", "dWv", "dWa"):
+        assert row_err(got[k].reshape(-1, 64), ref[k].reshape(-1, 64)) <= TOL, k
+    for k in ("dWatt", "dWmsg"):
+        assert row_err(got[k].reshape(-1, dk), ref[k].reshape(-1, dk)) <= TOL, k
+    assert row_err(got["dmu"].reshape(1, -1), ref["dmu"].reshape(1, -1)) <= TOL

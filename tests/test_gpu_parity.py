@@ -286,6 +286,66 @@ def test_rgcn_backward_after_forward():
     assert row_err(gW0, dW0) <= TOL
 
 
+def check_hgt_grads(got, ref, heads):
+    dk = 64 // heads
+    assert row_err(got["dh"], ref["dh"]) <= TOL
+    for k in ("dWk", "dWq", "dWv", "dWa"):
+        if ref[k] is None:
+            continue
+        assert row_err(got[k].reshape(-1, 64), ref[k].reshape(-1, 64)) <= TOL, k
+    for k in ("dWatt", "dWmsg"):
+        assert row_err(got[k].reshape(-1, dk), ref[k].reshape(-1, dk)) <= TOL, k
+    assert row_err(got["dmu"].reshape(1, -1), ref["dmu"].reshape(1, -1)) <= TOL
+
+
+def hgt_case(kind, heads, seed, flags=None, R=7, T=4, E=4000, scale=None):
+    g = graph(kind, seed=seed, T=T, R=R, E=E)
+    t = workloads.tiny_tensors(seed, g, 64, 64, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(R)).astype(np.float32)   # distinct priors
+    scale = 1.0 / np.sqrt(64 // heads) if scale is None else scale
+    return g, t, scale
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("heads", [1, 2, 4])
+def test_hgt_backward_small(kind, heads):
+    g, t, scale = hgt_case(kind, heads, 33)
+    print(f"hgt backward {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(heads, scale)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=heads, att_scale=scale)
+    check_hgt_grads(got, ref, heads)
+
+
+@pytest.mark.parametrize("flags", [0, 2, 4])
+def test_hgt_backward_flags(flags):
+    g, t, scale = hgt_case("hub", 4, 34, R=3, T=2)
+    print(f"hgt backward flags={flags}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(4, 0.3, flags=flags)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=4, att_scale=0.3,
+                              residual=bool(flags & 2), a_linear=bool(flags & 4))
+    check_hgt_grads(got, ref, 4)
+    if not flags & 4:
+        assert got["dWa"] is None
+
+
+@pytest.mark.parametrize("heads,R", [(2, 12), (4, 24)])
+def test_hgt_backward_many_relations(heads, R):
+    g, t, scale = hgt_case("random", heads, 35, R=R, T=3, E=5000)
+    print(f"hgt backward heads={heads} R={R}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(heads, scale)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=heads, att_scale=scale)
+    check_hgt_grads(got, ref, heads)
+
+
 def test_forward_bitwise_deterministic():
     g = graph("hub", seed=12)
     t = workloads.tiny_tensors(12, g, 64, 64, heads=4, att_var=1.0)

@@ -137,7 +137,7 @@ def _normal(rng, shape, var: float) -> np.ndarray:
 
 
 def make_tensors(k: int, g: dict, layer: str | None = None) -> dict:
-    """Features, weights and (workloads 1, 2, 5) the loss weight for workload k.
+    """Features, weights and (workloads 1, 2, 3, 5) the loss weight for workload k.
     Variances: features and weights 1/fan_in, attention vectors 0.1, HGT head
     blocks 1/d_k, loss weight 1."""
     c = CONFIGS[k]
@@ -160,6 +160,7 @@ def make_tensors(k: int, g: dict, layer: str | None = None) -> dict:
         out["Watt"] = _normal(a_rng, (R, H, dk, dk), 1.0 / dk)
         out["Wmsg"] = _normal(a_rng, (R, H, dk, dk), 1.0 / dk)
         out["mu"] = np.ones(R, np.float32)
+        out["grad_out"] = _normal(l_rng, (N, d), 1.0)
     return out
 
 
