@@ -42,6 +42,10 @@ def parse():
     p.add_argument("--only", choices=["headline", "all"], default="all",
                    help="headline: time only the RGAT workload of the headline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline leg")
+    p.add_argument("--sweep", action="store_true",
+                   help="instead of the benchmark line: the optimization ablation (compact "
+                        "materialization x linear operator reordering, and the fused "
+                        "aggregate-first plan) for RGAT and RGCN at d = 64 and d = 128")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a 1 GiB device copy (reference for HBM byte counters)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -205,12 +209,59 @@ def cpu_baseline(ctx, target_s):
                        f"destinations of the 880000-node workload, {edges} in-edges, {dt:.1f} s")}
 
 
+def sweep(args):
+    """The analogue of the paper's optimization table on the synthetic graphs:
+    per layer and hidden size, the ms per forward of transform-first without and
+    with compact materialization (graph flag) and without and with linear
+    operator reordering of the attention's destination term (RGAT plan 3 vs 1),
+    and of the fused aggregate-first plan, with the plan the model selects."""
+    import torch
+    from paper_2301_06284_amd import rgnn
+    torch.cuda.set_device(0)
+    K, W = args.steps, args.warmup
+    rows = []
+    for wk, d, name in ((2, 64, "am_like_880k"), (4, 128, "wikikg2_like_2p5m")):
+        log(f"sweep: workload {wk}")
+        c = Ctx(wk)
+        Gn = rgnn.Graph.from_dict(c.g, compact=False)
+        E = c.info["num_edges"]
+        out = torch.empty(c.info["num_nodes"], d, device=c.dev)
+        for lname, layer in (("rgat", rgnn.LAYER_RGAT), ("rgcn", rgnn.LAYER_RGCN)):
+            auto = rgnn.select_plan(c.G, layer, d, d, 1)[0]
+            cases = [("vanilla", False, 3), ("compact", True, 3), ("reorder", False, 1),
+                     ("compact+reorder", True, 1), ("aggregate-first fused", True, 2)]
+            if layer == rgnn.LAYER_RGCN:
+                cases = [("vanilla", False, 1), ("compact", True, 1), ("aggregate-first fused", True, 2)]
+            for label, compact, plan in cases:
+                G = c.G if compact else Gn
+                ws = torch.empty(max(rgnn.workspace_size(G, layer, d, d, 1, plan), 256),
+                                 dtype=torch.uint8, device=c.dev)
+                if layer == rgnn.LAYER_RGAT:
+                    fn = lambda: rgnn.rgat_forward(G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, None,
+                                                   ws, d, d, 1, 0.2, 0, plan)
+                else:
+                    fn = lambda: rgnn.rgcn_forward(G, c.T["h"], c.T["W"], c.T["W0"], out, ws, d, d, 0, plan)
+                ms = time_steps(torch, fn, K, W)
+                rows.append({"workload": name, "d": d, "layer": lname, "variant": label,
+                             "plan": plan, "compact": compact, "ms": round(ms, 4),
+                             "edges_per_s": E / (ms * 1e-3), "auto_selects": plan == auto and compact})
+                log(f"  {lname} {label}: {ms:.3f} ms")
+                del ws
+        Gn.close()
+        c.close()
+        del out
+    print(json.dumps({"sweep": rows}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU sharding "
               "of this path is a design note, not an implementation.", file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        sweep(args)
+        return
     import torch
     from paper_2301_06284_amd import rgnn
     assert torch.cuda.is_available(), "bench.py needs a GPU"

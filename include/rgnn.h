@@ -58,7 +58,13 @@ typedef enum {
     RGNN_PLAN_AUTO = 0,              /* pick the plan with fewer modelled HBM bytes */
     RGNN_PLAN_TRANSFORM_FIRST = 1,   /* M = h W_r once per unique (src, rel) pair    */
                                      /* (compact materialization), then gather M     */
-    RGNN_PLAN_AGGREGATE_FIRST = 2    /* gather h, sum per (dst, rel), then apply W_r */
+    RGNN_PLAN_AGGREGATE_FIRST = 2,   /* gather h, sum per (dst, rel), then apply W_r */
+    RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED = 3
+                                     /* RGAT only: transform-first with the          */
+                                     /* destination attention term taken from the    */
+                                     /* materialized h_v W_r row of every (dst, rel) */
+                                     /* segment instead of h_v . (W_r w_dst[r]): the */
+                                     /* layer without linear operator reordering     */
 } rgnn_plan;
 
 typedef enum {
@@ -79,7 +85,12 @@ enum {
     RGNN_FLAG_A_LINEAR = 4    /* HGT: apply the per-node-type output linear A         */
 };
 
-enum { RGNN_GRAPH_HOST_ONLY = 1 };   /* build the index on the host only (no device) */
+enum {
+    RGNN_GRAPH_HOST_ONLY = 1,    /* build the index on the host only (no device) */
+    RGNN_GRAPH_NO_COMPACT = 2    /* one materialized row per edge instead of per unique
+                                    (src, rel) pair: the vanilla materialization that
+                                    Section "Compact Tensor Materialization" improves on */
+};
 
 typedef struct {
     int64_t num_nodes;           /* N                                           */
@@ -127,7 +138,9 @@ typedef enum {
  *   num_nodes N, num_ntypes T >= 1, num_rels R >= 1, num_edges E (0 allowed).
  *   src, dst, rel: HOST int32 arrays [E]; ntype: HOST int32 [N] (NULL = all 0).
  *   The arrays are read during the call only.
- *   flags: 0 or RGNN_GRAPH_HOST_ONLY (no device memory; only info/export work).
+ *   flags: RGNN_GRAPH_HOST_ONLY (no device memory; only info/export work),
+ *   RGNN_GRAPH_NO_COMPACT (transform-first plans materialize one row per edge;
+ *   num_src_pairs = E), or 0.
  *   stream: hipStream_t for the uploads (the call synchronises it).
  * Errors: RGNN_ERANGE for ids outside [0,N) / [0,R) / [0,T) or N, E >= 2^31;
  *         RGNN_EINVAL for NULL arrays or non-positive R, T; RGNN_ENOMEM. */

@@ -141,10 +141,12 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     x.wsp = c.take<float>((size_t)g->R * H * d_in);
     x.wtp = c.take<float>((size_t)g->R * H * d_in);
     x.vatt = c.take<float>((size_t)g->V * H);
-    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED) {
         x.M = c.take<float>((size_t)g->U_src * d_out);
         if (H > 1) x.atts = c.take<float>((size_t)g->U_src * H);   // one head: formed in the traversal
         x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
+        if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)   // h_v W_r per segment
+            x.T = c.take<float>((size_t)g->V * d_out);
     } else {
         x.vstat = c.take<float>((size_t)g->V * 2);
         x.vscale = c.take<float>((size_t)g->V);
@@ -275,7 +277,9 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
 {
     if (!g || !bytes) return fail(RGNN_EINVAL, "NULL argument");
     if (heads <= 0) return fail(RGNN_EINVAL, "heads must be positive");
-    if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
+    if (plan < 0 || plan > 3) return fail(RGNN_EINVAL, "unknown plan");
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED && layer != RGNN_LAYER_RGAT)
+        return fail(RGNN_EINVAL, "the unreordered transform-first plan is an RGAT plan");
     switch (layer) {
     case RGNN_LAYER_RGCN:
         *bytes = rgcn_layout(g, d_in, d_out, resolve_plan(g, layer, d_in, d_out, 1, plan), nullptr, nullptr);
@@ -384,11 +388,11 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     if ((d_out / heads) % 16) return fail(RGNN_EUNSUPPORTED, "d_out / heads must be a multiple of 16");
     if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
         return fail(RGNN_EINVAL, "unknown softmax scope");
-    if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
+    if (plan < 0 || plan > 3) return fail(RGNN_EINVAL, "unknown plan");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
     const bool per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
     if (per_seg) {   // normalised per (dst, rel) segment: the aggregate-first plan
-        if (plan == RGNN_PLAN_TRANSFORM_FIRST)
+        if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)
             return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) runs aggregate-first");
         if (saved) return fail(RGNN_EINVAL, "saved holds per-destination statistics: pass NULL with "
                                             "softmax per (destination, relation)");
@@ -397,7 +401,7 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     plan = resolve_plan(g, RGNN_LAYER_RGAT, d_in, d_out, heads, plan);
     if (plan == RGNN_PLAN_AGGREGATE_FIRST && (heads != 1 || d_in != d_out))
         return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs heads == 1 and d_in == d_out");
-    if (plan == RGNN_PLAN_TRANSFORM_FIRST && d_in != d_out)
+    if (plan != RGNN_PLAN_AGGREGATE_FIRST && d_in != d_out)
         return fail(RGNN_EUNSUPPORTED, "RGAT needs d_in == d_out");
     const size_t need = rgat_layout(g, d_in, d_out, heads, plan, nullptr, nullptr);
     if (!ws || ws_bytes < need)
@@ -409,15 +413,25 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     // then the destination term h_v . (W_r w_dst[r]) once per (dst, rel) segment
     // (aggregate-first also needs W_r w_src[r]: both in one launch)
     const bool af = plan == RGNN_PLAN_AGGREGATE_FIRST;
-    if ((st = launch_reorder_vec(W, g->R, d_in, d_out, heads, w_dst, w.wtp, af ? w_src : nullptr,
-                                 af ? w.wsp : nullptr, s)) != RGNN_OK)
-        return st;
-    {
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED) {
+        // without reordering: the segment's h_v W_r row is materialized and its
+        // dot products with w_dst[r] taken in the GEMM epilogue
+        GemmArgs gd;
+        gd.X = h; gd.ldx = d_in; gd.gather = g->dev.vsegdst_byrel;
+        gd.W[0] = W; gd.K = d_in; gd.Nc = d_out;
+        gd.tiles = g->dev.tiles_vsegs; gd.ntiles = g->n_tiles_vsegs;
+        gd.Y = w.T; gd.ldy = d_out; gd.scatter = g->dev.vseg_byrel;
+        gd.ep.dot_vec = w_dst; gd.ep.dot_out = w.vatt; gd.ep.dot_heads = heads;
+        if ((st = launch_typed_gemm(gd, s)) != RGNN_OK) return st;
+    } else {
+        if ((st = launch_reorder_vec(W, g->R, d_in, d_out, heads, w_dst, w.wtp, af ? w_src : nullptr,
+                                     af ? w.wsp : nullptr, s)) != RGNN_OK)
+            return st;
         TravArgs ta;
         ta.g = g; ta.h = h; ta.wtp = w.wtp; ta.heads = heads; ta.d = d_in; ta.vatt = w.vatt;
         if ((st = launch_seg_attn(ta, s)) != RGNN_OK) return st;
     }
-    if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
+    if (plan != RGNN_PLAN_AGGREGATE_FIRST) {
         GemmArgs ga;
         ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;

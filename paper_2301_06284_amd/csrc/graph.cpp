@@ -45,8 +45,9 @@ void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vecto
 
 rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
                              const int32_t *dst, const int32_t *rel, const int32_t *ntype,
-                             rgnn_graph *g)
+                             int32_t flags, rgnn_graph *g)
 {
+    const bool compact = !(flags & RGNN_GRAPH_NO_COMPACT);
     HostIndex &x = g->host;
     g->N = N; g->E = E; g->R = R; g->T = T;
     const int C = g->chunk;
@@ -87,7 +88,8 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         }
         g->U_dst = (int64_t)x.seg_ptr.size();
         x.seg_ptr.push_back((int32_t)E);
-        // ---- compact (rel, src) map: LSD passes src, rel over edge ids ----
+        // ---- compact (rel, src) map: LSD passes src, rel over edge ids; without
+        //      compaction every edge keeps its own row (vanilla materialization) ----
         for (int64_t e = 0; e < E; ++e) perm[e] = (int32_t)e;
         counting_sort(perm, src, N, tmp, cnt);
         counting_sort(perm, rel, R, tmp, cnt);
@@ -96,7 +98,7 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.uniq_rel_ptr.assign((size_t)R + 1, 0);
         for (int64_t i = 0; i < E; ++i) {
             const int32_t e = perm[i];
-            if (i == 0 || rel[e] != rel[perm[i - 1]] || src[e] != src[perm[i - 1]]) {
+            if (!compact || i == 0 || rel[e] != rel[perm[i - 1]] || src[e] != src[perm[i - 1]]) {
                 x.uniq_src.push_back(src[e]);
                 x.uniq_rel_ptr[(size_t)rel[e] + 1]++;
             }
@@ -414,7 +416,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         return fail(RGNN_ERANGE, "node and edge counts must be below 2^31 - 1");
     if (R <= 0 || T <= 0) return fail(RGNN_EINVAL, "num_rels and num_ntypes must be positive");
     if (E > 0 && (!src || !dst || !rel)) return fail(RGNN_EINVAL, "NULL edge array");
-    if (flags & ~RGNN_GRAPH_HOST_ONLY) return fail(RGNN_EINVAL, "unknown graph flag");
+    if (flags & ~(RGNN_GRAPH_HOST_ONLY | RGNN_GRAPH_NO_COMPACT)) return fail(RGNN_EINVAL, "unknown graph flag");
     for (int64_t e = 0; e < E; ++e) {
         if (src[e] < 0 || src[e] >= N || dst[e] < 0 || dst[e] >= N)
             return fail(RGNN_ERANGE, "edge " + std::to_string(e) + ": node id out of range");
@@ -427,7 +429,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
                 return fail(RGNN_ERANGE, "node " + std::to_string(n) + ": node type out of range");
     rgnn_graph *g = new (std::nothrow) rgnn_graph();
     if (!g) return fail(RGNN_ENOMEM, "host allocation failed");
-    rgnn_status st = build_host_index(N, T, R, E, src, dst, rel, ntype, g);
+    rgnn_status st = build_host_index(N, T, R, E, src, dst, rel, ntype, flags, g);
     if (st != RGNN_OK) { delete g; return st; }
     if (!(flags & RGNN_GRAPH_HOST_ONLY)) {
         int dev = 0;

@@ -135,7 +135,7 @@ rgnn_status hip_fail(hipError_t e, const char *what);
 // ---- graph building (graph.cpp) ----
 rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
                              const int32_t *dst, const int32_t *rel, const int32_t *ntype,
-                             rgnn_graph *g);
+                             int32_t flags, rgnn_graph *g);
 void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vector<Tile> &out);
 int bwd_outer_rows();
 rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s);

@@ -17,11 +17,12 @@ LIB_PATH = os.path.join(_HERE, "librgnn.so")
 
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PLAN_AUTO, PLAN_TRANSFORM_FIRST, PLAN_AGGREGATE_FIRST = 0, 1, 2
+PLAN_TRANSFORM_FIRST_UNREORDERED = 3
 LAYER_RGCN, LAYER_RGAT, LAYER_HGT, LAYER_RGAT_BACKWARD, LAYER_SEGMENT_GEMM = 0, 1, 2, 3, 4
 LAYER_RGCN_BACKWARD, LAYER_HGT_BACKWARD = 5, 6
 SOFTMAX_PER_DST, SOFTMAX_PER_DST_REL = 0, 1
 FLAG_RELU, FLAG_RESIDUAL, FLAG_A_LINEAR = 1, 2, 4
-GRAPH_HOST_ONLY = 1
+GRAPH_HOST_ONLY, GRAPH_NO_COMPACT = 1, 2
 
 INDEX_KINDS = {
     "dst_rowptr": 0, "in_src": 1, "in_rel": 2, "in_eid": 3, "seg_ptr": 4, "seg_rel": 5,
@@ -140,13 +141,14 @@ class Graph:
         self._h = handle
 
     @classmethod
-    def from_coo(cls, N, T, R, src, dst, rel, ntype=None, host_only=False, stream=None):
+    def from_coo(cls, N, T, R, src, dst, rel, ntype=None, host_only=False, stream=None,
+                 compact=True):
         src, dst, rel = _host(src, np.int32), _host(dst, np.int32), _host(rel, np.int32)
         ntype = _host(ntype, np.int32)
         h = ctypes.c_void_p()
+        flags = (GRAPH_HOST_ONLY if host_only else 0) | (0 if compact else GRAPH_NO_COMPACT)
         st = _lib.rgnn_graph_create_coo(int(N), int(T), int(R), len(src), _np_ptr(src),
-                                        _np_ptr(dst), _np_ptr(rel), _np_ptr(ntype),
-                                        GRAPH_HOST_ONLY if host_only else 0,
+                                        _np_ptr(dst), _np_ptr(rel), _np_ptr(ntype), flags,
                                         None if host_only else _stream(stream), ctypes.byref(h))
         _check(st)
         return cls(h)
@@ -164,9 +166,9 @@ class Graph:
         return cls(h)
 
     @classmethod
-    def from_dict(cls, g, host_only=False):
+    def from_dict(cls, g, host_only=False, compact=True):
         return cls.from_coo(g["N"], g["T"], g["R"], g["src"], g["dst"], g["rel"], g["ntype"],
-                            host_only=host_only)
+                            host_only=host_only, compact=compact)
 
     @property
     def handle(self):

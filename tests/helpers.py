@@ -56,13 +56,13 @@ def sample_rows(g, n_random=400, seed=0):
 class Runner:
     """Runs the library's layers on one device with torch-owned buffers."""
 
-    def __init__(self, g, t, device="cuda:0"):
+    def __init__(self, g, t, device="cuda:0", compact=True):
         import torch
         from paper_2301_06284_amd import rgnn
         self.torch, self.rgnn = torch, rgnn
         self.dev = torch.device(device)
         self.g = g
-        self.G = rgnn.Graph.from_dict(g)
+        self.G = rgnn.Graph.from_dict(g, compact=compact)
         self.T = {k: torch.from_numpy(np.ascontiguousarray(v)).to(self.dev) for k, v in t.items()}
 
     def ws(self, layer, d_in, d_out, heads=1, plan=0):

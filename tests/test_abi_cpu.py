@@ -23,7 +23,7 @@ def test_header_symbols_exported():
     rgnn = _rgnn()
     hdr = open(os.path.join(ROOT, "include", "rgnn.h")).read()
     hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
-    declared = set(re.findall(r"\b(rgnn_\w+|rgcn_forward|rgat_forward|hgt_forward|rgat_backward)\s*\(", hdr))
+    declared = set(re.findall(r"\b(?:rgnn_status|const char\s*\*)\s*(\w+)\s*\(", hdr))
     assert declared, "no declarations found"
     lib = ctypes.CDLL(rgnn.LIB_PATH)
     for name in sorted(declared):
@@ -127,3 +127,23 @@ def test_product_does_not_import_oracle():
                     assert all(not a.name.startswith("oracle") for a in node.names), fn
                 if isinstance(node, ast.ImportFrom):
                     assert not (node.module or "").startswith("oracle"), fn
+
+
+def test_graph_without_compaction_host_only():
+    """RGNN_GRAPH_NO_COMPACT: one materialized row per edge, in (rel, src,
+    edge id) order; everything else as with compaction."""
+    rgnn = _rgnn()
+    g = workloads.tiny_graph(39, N=50, E=400, R=4, kind="dups")
+    a = rgnn.Graph.from_dict(g, host_only=True)
+    b = rgnn.Graph.from_dict(g, host_only=True, compact=False)
+    ia, ib = a.info(), b.info()
+    assert ib["num_src_pairs"] == g["E"] < ia["num_src_pairs"] + g["E"]
+    assert ia["num_src_pairs"] < g["E"]   # the dups graph has repeated (src, rel) pairs
+    order = np.lexsort((np.arange(g["E"]), g["src"], g["rel"]))
+    np.testing.assert_array_equal(b.export("uniq_src"), g["src"][order])
+    e2u = b.export("edge2uniq")
+    inv = np.empty(g["E"], np.int64); inv[order] = np.arange(g["E"])
+    np.testing.assert_array_equal(e2u, inv[b.export("in_eid")])
+    for k in ("dst_rowptr", "in_src", "in_rel", "in_eid", "seg_ptr", "out_pos"):
+        np.testing.assert_array_equal(a.export(k), b.export(k), err_msg=k)
+    a.close(); b.close()

@@ -346,6 +346,36 @@ def test_hgt_backward_many_relations(heads, R):
     check_hgt_grads(got, ref, heads)
 
 
+@pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
+@pytest.mark.parametrize("heads", [1, 2])
+def test_rgat_ablation_plans(kind, heads):
+    """Transform-first with and without compact materialization (graph flag)
+    and with and without linear operator reordering of the destination term
+    all give the layer's output."""
+    g = graph(kind, seed=37)
+    t = workloads.tiny_tensors(37, g, 64, 64, heads=heads, att_var=1.0)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads)
+    for compact in (True, False):
+        print(f"rgat ablation {kind} heads={heads} compact={compact}", flush=True)
+        run = Runner(g, t, compact=compact)
+        if not compact:
+            assert run.G.info()["num_src_pairs"] == g["E"]
+        for plan in (1, 3):
+            assert row_err(run.rgat(heads=heads, plan=plan), ref) <= TOL, (compact, plan)
+        run.close()
+
+
+@pytest.mark.parametrize("kind", ["random", "hub"])
+def test_rgcn_without_compaction(kind):
+    g = graph(kind, seed=38)
+    t = workloads.tiny_tensors(38, g, 64, 64)
+    print(f"rgcn no compaction {kind}", flush=True)
+    run = Runner(g, t, compact=False)
+    got = run.rgcn(plan=1)
+    run.close()
+    assert row_err(got, oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])) <= TOL
+
+
 def test_forward_bitwise_deterministic():
     g = graph("hub", seed=12)
     t = workloads.tiny_tensors(12, g, 64, 64, heads=4, att_var=1.0)
