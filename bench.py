@@ -117,21 +117,16 @@ def rgat_tf_model(info, d, H):
     Gathered rows count once per edge, node rows once per node, index arrays once."""
     E, N, U, V = info["num_edges"], info["num_nodes"], info["num_src_pairs"], info["num_vsegs"]
     R, I = info["num_rels"], info["num_items"]
-    # With one head the traversal forms the source term from the gathered
-    # message row (a dot with w_src); with several the GEMM writes it per pair
-    # and the traversal gathers it per edge.
-    st = 0 if H == 1 else 4 * H
     return {
-        # per pair: gather index, h row read, message row write (+ source terms);
-        # W_r and w_src once per relation
-        "typed_gemm": dict(bytes=U * (4 + 4 * d + 4 * d + st) + R * (4 * d * d + 4 * d),
-                           flops=2.0 * U * d * d + (2.0 * U * d if H > 1 else 0.0)),
-        # per edge: pair index, message row (+ source term); per destination:
-        # h_v row, output row, (max, sum); per segment: offset, relation and
-        # destination term; per item: descriptor and slot; w_src once
-        "rgat_traverse_tf": dict(bytes=E * (4 + 4 * d + st) + N * (4 * d + 4 * d + 8 * H + 4)
-                                 + V * 12 + I * 20 + R * H * d * 4,
-                                 flops=E * (2.0 * d + 10) + (E * 2.0 * d if H == 1 else 0.0)),
+        # per pair: gather index, h row read, message row write; W_r once per relation
+        "typed_gemm": dict(bytes=U * (4 + 4 * d + 4 * d) + R * 4 * d * d, flops=2.0 * U * d * d),
+        # per edge: pair index, message row (the per-head source terms are formed
+        # from it with w_src); per destination: output row, (max, sum) per head;
+        # per segment: offset, relation and destination terms; per item:
+        # descriptor and slot; w_src once per relation
+        "rgat_traverse_tf": dict(bytes=E * (4 + 4 * d) + N * (4 * d + 8 * H + 4)
+                                 + V * (8 + 4 * H) + I * 20 + R * d * 4,
+                                 flops=E * (4.0 * d + 10 * H)),
     }
 
 
@@ -295,6 +290,19 @@ def main():
     E = inf["num_edges"]
     value = E / (ms * 1e-3)
     names = {1: "transform_first", 2: "aggregate_first"}
+    if args.only == "all":
+        # several heads (transform-first; the per-head source terms come from the
+        # gathered message rows)
+        log("workload 2: RGAT forward, 4 heads")
+        ws4 = c.ws(rgnn.LAYER_RGAT, d, d, 4, rgnn.PLAN_TRANSFORM_FIRST)
+        sv4 = torch.empty(inf["num_nodes"], 4, 2, device=c.dev)
+        fn4 = lambda: rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, sv4, ws4,
+                                        d, d, 4, 0.2, 0, rgnn.PLAN_TRANSFORM_FIRST)
+        m4h = time_steps(torch, fn4, K, W)
+        k4h = kernel_profile(rgnn, torch, fn4, max(3, K // 2))
+        layers["rgat_fwd_am_like_880k_4heads"] = {"edges_per_s": inf["num_edges"] / (m4h * 1e-3), "ms": m4h,
+                                                  "kernels_ms": {k: round(v[1], 4) for k, v in k4h.items()}}
+        del ws4, sv4
     if other in plans:
         layers["rgat_fwd_am_like_880k_" + names[other]] = {
             "edges_per_s": E / (plans[other][0] * 1e-3), "ms": plans[other][0],

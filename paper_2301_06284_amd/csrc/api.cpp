@@ -100,7 +100,7 @@ void plan_bytes(const rgnn_graph *g, int layer, int d_in, int d_out, int H, doub
         // fused: gathered rows + segment table + T written and read back
         *af = E * (4 + bi) + V * (16 + 2 * bo) + N * bo;
     } else {
-        *tf = U * (bi + bo + 4 * H) + E * (4 + bo + 4 * H) + V * 12 + N * (bi + bo + 8 * H);
+        *tf = U * (bi + bo) + E * (4 + bo) + V * (12 + 4 * H) + N * (bi + bo + 8 * H);
         // destination terms (h_v once per destination), fused traversal (rows,
         // segment table, destination term, T, (max, sum)), statistics, reduce
         *af = E * (4 + bi) + N * (bi + 8 + bo) + V * (48 + 2 * bo);
@@ -132,7 +132,7 @@ size_t rgcn_layout(const rgnn_graph *g, int d_in, int d_out, int plan, void *bas
     return c.off;
 }
 
-struct RgatWs { float *M, *atts, *wsp, *wtp, *vatt, *partial, *vstat, *vscale, *T; };
+struct RgatWs { float *M, *wsp, *wtp, *vatt, *partial, *vstat, *vscale, *T; };
 size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, void *base,
                    RgatWs *w)
 {
@@ -143,7 +143,6 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     x.vatt = c.take<float>((size_t)g->V * H);
     if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED) {
         x.M = c.take<float>((size_t)g->U_src * d_out);
-        if (H > 1) x.atts = c.take<float>((size_t)g->U_src * H);   // one head: formed in the traversal
         x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
         if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)   // h_v W_r per segment
             x.T = c.take<float>((size_t)g->V * d_out);
@@ -437,13 +436,11 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
         ga.Y = w.M; ga.ldy = d_out;
-        // with several heads the GEMM also emits the per-pair source terms; one
-        // head forms them in the traversal from the gathered message row
-        if (heads > 1) { ga.ep.dot_vec = w_src; ga.ep.dot_out = w.atts; ga.ep.dot_heads = heads; }
         if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        // the per-head source terms are formed in the traversal from the gathered
+        // message row itself (no per-pair term is materialized)
         TravArgs ta;
-        ta.g = g; ta.h = h; ta.M = w.M; ta.atts = w.atts; ta.wtp = w.wtp; ta.vatt = w.vatt;
-        if (heads == 1) ta.wsp = w_src;
+        ta.g = g; ta.h = h; ta.M = w.M; ta.wtp = w.wtp; ta.vatt = w.vatt; ta.wsp = w_src;
         ta.slope = neg_slope; ta.heads = heads; ta.d = d_out;
         ta.out = out; ta.saved = saved; ta.partial = w.partial;
         if ((st = launch_rgat_traverse_tf(ta, s)) != RGNN_OK) return st;

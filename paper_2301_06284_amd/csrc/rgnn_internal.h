@@ -197,10 +197,9 @@ struct TravArgs {
     const rgnn_graph *g = nullptr;
     const float *h = nullptr;            // node features [N, d_in]
     const float *M = nullptr;            // compact messages [U_src, d_out] (transform-first)
-    const float *atts = nullptr;         // [U_src, heads] (transform-first RGAT)
     const float *wsp = nullptr;          // vector dotted with each gathered row for the source
                                          // term: [R, d_in] W_r w_src (aggregate-first), or
-                                         // [R, d_out] w_src (one-head transform-first)
+                                         // [R, d_out] w_src (transform-first, per head slice)
     const float *wtp = nullptr;          // [R, heads, d_in] reordered w_dst
     float slope = 0.2f;
     int heads = 1;

@@ -56,7 +56,7 @@ struct TK {
     const int32_t *item_slot;
     const int32_t *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_cnt;
     const int32_t *e2u;
-    const float *h, *M, *atts, *wsp, *wtp;
+    const float *h, *M, *wsp, *wtp;
     float *vatt;
     float slope;
     float *out, *saved, *partial;
@@ -72,7 +72,7 @@ TK make_tk(const TravArgs &a)
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
     k.vseg_rel = g->dev.vseg_rel; k.vseg_cnt = g->dev.vseg_cnt;
     k.e2u = g->dev.e2u;
-    k.h = a.h; k.M = a.M; k.atts = a.atts; k.wsp = a.wsp; k.wtp = a.wtp; k.vatt = a.vatt;
+    k.h = a.h; k.M = a.M; k.wsp = a.wsp; k.wtp = a.wtp; k.vatt = a.vatt;
     k.slope = a.slope;
     k.out = a.out; k.saved = a.saved; k.partial = a.partial;
     k.relu = a.relu;
@@ -137,43 +137,6 @@ __device__ __forceinline__ void stage_item(const TK &k, const ItemHdr &it, Stage
         st.dptr[j] = k.vseg_ptr[vs] - it.e0;
     }
     for (int e = gl; e < it.ne; e += G) st.eidx[e] = eidx_src[it.e0 + e];
-}
-
-// Phase 3: per destination softmax over the staged logits.  Writes the edge
-// weights (normalised for whole destinations, relative to the piece maximum
-// for pieces of split ones) and the destination's (max, sum).  For a piece,
-// the (max, sum) of head `head` are returned through pm, ps.
-template <int G, int H>
-__device__ __forceinline__ void softmax_item(const TK &k, const ItemHdr &it, Stage<H> &st, int gl,
-                                             int head, float &pm, float &ps)
-{
-    constexpr int LH = G / H;   // lanes per head (features of one head)
-    if (!it.valid) return;
-    for (int j = 0; j < it.nd; ++j) {
-        const int a = st.dptr[j], b = st.dptr[j + 1];
-        const int v = it.dst0 + j;
-#pragma unroll
-        for (int hh = 0; hh < H; ++hh) {
-            float m = -INFINITY;
-            for (int e = a + gl; e < b; e += G) m = fmaxf(m, st.ew[e * H + hh]);
-            m = gmax<G>(m);
-            float s = 0.f;
-            for (int e = a + gl; e < b; e += G) s += __expf(st.ew[e * H + hh] - m);
-            s = gsum<G>(s);
-            const float inv = (it.slot < 0 && s > 0.f) ? 1.f / s : 1.f;
-            for (int e = a + gl; e < b; e += G) st.ew[e * H + hh] = __expf(st.ew[e * H + hh] - m) * inv;
-            if (it.slot < 0) {
-                if (k.saved && gl == 0) {
-                    k.saved[((size_t)v * H + hh) * 2] = b > a ? m : 0.f;
-                    k.saved[((size_t)v * H + hh) * 2 + 1] = s;
-                }
-            } else if (hh == head) {
-                pm = m;
-                ps = s;
-            }
-        }
-        (void)LH;
-    }
 }
 
 // Phase 4 (destination flush): weighted sums of gathered rows, written per
@@ -293,53 +256,25 @@ __global__ __launch_bounds__(256) void seg_attn_kernel(TK k, int64_t V, const in
 }
 
 // ---------------------------------------------------------------- RGAT, transform-first
-// Several heads: messages M[p] = h_u W_r and source terms atts[p] = M[p] . w_src[r]
-// exist once per unique (src, rel) pair (compact materialization); logits are
-// staged per edge, the softmax of each destination is taken over them, then
-// the message rows are aggregated with the weights.
-template <int D, int H>
-__global__ __launch_bounds__(256) void rgat_tf_kernel(TK k)
-{
-    constexpr int G = D / 4, GPB = 256 / G, LH = D / H / 4;
-    __shared__ Stage<H> stage[GPB];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    Stage<H> &st = stage[gi];
-    const ItemHdr it = item_header(k, (int64_t)blockIdx.x * GPB + gi);
-    const int head = gl / LH;
-    stage_item<G, H, 0>(k, it, st, k.e2u, gl);
-    __syncthreads();
-    if (it.valid) {   // phase 2: logits, edge-parallel
-        for (int e = gl; e < it.ne; e += G) {
-            const int p = st.eidx[e], j = st.evs[e];
-#pragma unroll
-            for (int hh = 0; hh < H; ++hh)
-                st.ew[e * H + hh] = leaky(k.atts[(size_t)p * H + hh] + st.vw[j * H + hh], k.slope);
-        }
-    }
-    __syncthreads();
-    float pm = 0.f, ps = 0.f;
-    softmax_item<G, H>(k, it, st, gl, head, pm, ps);
-    __syncthreads();
-    aggregate_item<D, H, true>(k, it, st, k.M, gl, head, pm, ps);
-}
-
-// ---------------------------------------------------------------- RGAT, transform-first, one head
-// One pass per item with an online softmax: the source term M[p] . w_src[r] is
-// formed from the gathered message row itself, so neither a per-pair source
-// term (a 4-byte random gather per edge) nor a logit staging pass is needed.
-// The running maximum, denominator and weighted row sum of the current
-// destination are rescaled as the maximum grows; a destination's result is
+// One pass per item with an online softmax per head: the source term of head
+// k, M[p][k-cols] . w_src[r][k-cols], is formed from the gathered message row
+// itself (a sum over the head's lanes), so the attention term rides in the
+// message row's own read -- neither a per-pair source term (a random gather
+// per edge) nor a logit staging pass is needed.  Each lane's four features
+// belong to one head; the running maximum, denominator and weighted row sum of
+// that head are rescaled as the maximum grows, and a destination's result is
 // written when its last edge is consumed.  k.wsp holds w_src [R, D].
-template <int D>
+template <int D, int H>
 __global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
 {
-    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int G = D / 4, GPB = 256 / G, LH = G / H;
     constexpr int kU = 4;   // each entry carries two rows: half the batch of the other traversals
-    __shared__ Stage<1> stage[GPB];
+    __shared__ Stage<H> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    Stage<1> &st = stage[gi];
+    const int head = gl / LH;
+    Stage<H> &st = stage[gi];
     const ItemHdr it = item_header(k, (int64_t)blockIdx.x * GPB + gi);
-    stage_item<G, 1, 0>(k, it, st, k.e2u, gl);
+    stage_item<G, H, 0>(k, it, st, k.e2u, gl);
     __syncthreads();
     if (!it.valid) return;
     int j = 0;
@@ -349,14 +284,14 @@ __global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
         const size_t v = (size_t)it.dst0 + jj;
         if (it.slot < 0) {
             st4(k.out + v * D + gl * 4, scale4(acc, s > 0.f ? 1.f / s : 0.f));
-            if (k.saved && gl == 0) {
-                k.saved[v * 2] = s > 0.f ? m : 0.f;
-                k.saved[v * 2 + 1] = s;
+            if (k.saved && gl % LH == 0) {
+                k.saved[(v * H + head) * 2] = s > 0.f ? m : 0.f;
+                k.saved[(v * H + head) * 2 + 1] = s;
             }
         } else {
-            float *pr = k.partial + (size_t)it.slot * (2 + D);
-            if (gl == 0) { pr[0] = m; pr[1] = s; }
-            st4(pr + 2 + gl * 4, acc);
+            float *pr = k.partial + (size_t)it.slot * (2 * H + D);
+            if (gl % LH == 0) { pr[head * 2] = m; pr[head * 2 + 1] = s; }
+            st4(pr + 2 * H + gl * 4, acc);
         }
         m = -INFINITY; s = 0.f; acc = zero4();
     };
@@ -375,10 +310,10 @@ __global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
-                const float src_term = gsum<G>(dot4(X[u], Xw[u]));
+                const float src_term = gsum<LH>(dot4(X[u], Xw[u]));
                 if (e < it.ne) {
                     while (e >= st.dptr[j + 1]) { flush(j); ++j; }
-                    const float z = leaky(src_term + st.vw[st.evs[e]], k.slope);
+                    const float z = leaky(src_term + st.vw[st.evs[e] * H + head], k.slope);
                     const float mn = fmaxf(m, z);
                     const float c1 = __expf(m - mn), c2 = __expf(z - mn);
                     s = s * c1 + c2;
@@ -449,15 +384,12 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     TK k = make_tk(a);
     LaunchScope ls("rgat_traverse_tf", s);
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
-#define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
-    if (a.heads == 1) {   // single pass, source term from the message row
-        if (!a.wsp) return fail(RGNN_EINVAL, "one-head RGAT traversal needs w_src");
-        if (a.d == 64) hipLaunchKernelGGL((rgat_tf1_kernel<64>), dim3(nb), dim3(256), 0, s, k);
-        else if (a.d == 128) hipLaunchKernelGGL((rgat_tf1_kernel<128>), dim3(nb), dim3(256), 0, s, k);
-        else return fail(RGNN_EUNSUPPORTED, "RGAT traversal: unsupported d");
-    }
+    if (!a.wsp) return fail(RGNN_EINVAL, "RGAT traversal needs w_src");
+#define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf1_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
+    if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
     else if (a.d == 64 && a.heads == 2) RGAT_TF(64, 2);
     else if (a.d == 64 && a.heads == 4) RGAT_TF(64, 4);
+    else if (a.d == 128 && a.heads == 1) RGAT_TF(128, 1);
     else if (a.d == 128 && a.heads == 2) RGAT_TF(128, 2);
     else if (a.d == 128 && a.heads == 4) RGAT_TF(128, 4);
     else if (a.d == 128 && a.heads == 8) RGAT_TF(128, 8);
