@@ -205,20 +205,31 @@ def cpu_baseline(ctx, target_s):
 
 
 def sweep(args):
-    """The analogue of the paper's optimization table on the synthetic graphs:
-    per layer and hidden size, the ms per forward of transform-first without and
+    """The analogue of the paper's optimization table and hidden-size curve on
+    the synthetic graphs (the 880k-node graph at d = 32, 64, 128; the 2.5M-node
+    graph at d = 128): per layer and hidden size, the ms per forward of
+    transform-first without and
     with compact materialization (graph flag) and without and with linear
     operator reordering of the attention's destination term (RGAT plan 3 vs 1),
     and of the fused aggregate-first plan, with the plan the model selects."""
     import torch
     from paper_2301_06284_amd import rgnn
     torch.cuda.set_device(0)
+    import workloads
     K, W = args.steps, args.warmup
     rows = []
-    for wk, d, name in ((2, 64, "am_like_880k"), (4, 128, "wikikg2_like_2p5m")):
-        log(f"sweep: workload {wk}")
-        c = Ctx(wk)
-        Gn = rgnn.Graph.from_dict(c.g, compact=False)
+    runs = [(2, d, "am_like_880k") for d in (32, 64, 128)] + [(4, 128, "wikikg2_like_2p5m")]
+    c = Gn = None
+    for wk, d, name in runs:
+        log(f"sweep: workload {wk}, d = {d}")
+        if c is None or c.k != wk:
+            if c is not None:
+                Gn.close()
+                c.close()
+            c = Ctx(wk)
+            Gn = rgnn.Graph.from_dict(c.g, compact=False)
+        # the hidden-size sweep: same graph, tensors of width d
+        c.T = {n: torch.from_numpy(v).to(c.dev) for n, v in workloads.make_tensors(wk, c.g, "rgat", d).items()}
         E = c.info["num_edges"]
         out = torch.empty(c.info["num_nodes"], d, device=c.dev)
         for lname, layer in (("rgat", rgnn.LAYER_RGAT), ("rgcn", rgnn.LAYER_RGCN)):
@@ -242,9 +253,9 @@ def sweep(args):
                              "edges_per_s": E / (ms * 1e-3), "auto_selects": plan == auto and compact})
                 log(f"  {lname} {label}: {ms:.3f} ms")
                 del ws
-        Gn.close()
-        c.close()
         del out
+    Gn.close()
+    c.close()
     print(json.dumps({"sweep": rows}))
 
 

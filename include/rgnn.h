@@ -183,7 +183,8 @@ rgnn_status rgnn_select_plan(const rgnn_graph_t *g, int32_t layer, int32_t d_in,
  *   out_v = act( h_v W0 + sum_r sum_{u in N_v^r} h_u W_r / c_{v,r} )
  * c_{v,r} = number of in-edges of v with relation r (duplicates counted).
  *   h [N, d_in], W [R, d_in, d_out], W0 [d_in, d_out] or NULL (no self-loop),
- *   out [N, d_out].  flags: RGNN_FLAG_RELU.  d_in, d_out in {64, 128}. */
+ *   out [N, d_out].  flags: RGNN_FLAG_RELU.  d_in, d_out in {64, 128}, or
+ *   d_in = d_out = 32. */
 rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W, const float *W0,
                          int32_t d_in, int32_t d_out, int32_t flags, int32_t plan, float *out,
                          void *ws, size_t ws_bytes, void *stream);
@@ -203,7 +204,7 @@ rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W, 
  *   (heads == 1, d_in == d_out; size the workspace for
  *   RGNN_PLAN_AGGREGATE_FIRST), requires saved == NULL, and returns
  *   RGNN_EUNSUPPORTED for RGNN_PLAN_TRANSFORM_FIRST.
- *   d_in, d_out in {64, 128}; d_out / heads a multiple of 16.
+ *   d_in, d_out in {64, 128}, or d_in = d_out = 32; d_out / heads a multiple of 16.
  *   RGNN_PLAN_AGGREGATE_FIRST requires heads == 1. */
 rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
                          const float *w_src, const float *w_dst, int32_t d_in, int32_t d_out,
@@ -277,7 +278,8 @@ rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk,
  * where t(i) is the segment of i given by type_ptr (HOST int64 [T+1],
  * type_ptr[0] = 0, type_ptr[T] = M, rows of one type contiguous).
  *   X [*, ldx >= K], W [T, K, Nc], Y [*, ldy >= Nc]; gather, scatter: DEVICE
- *   int32 [M] or NULL for the identity.  K in {64, 128}, Nc in {64, 128}.
+ *   int32 [M] or NULL for the identity.  K in {64, 128}, Nc in {64, 128}, or
+ *   K = Nc = 32.
  *   Rows written twice through `scatter` race; the caller avoids that. */
 rgnn_status rgnn_segment_gemm(const float *X, int64_t ldx, const int32_t *gather,
                               const int64_t *type_ptr, int32_t num_types, const float *W,

@@ -88,7 +88,13 @@ rgnn_status check_graph(const rgnn_graph *g)
     return RGNN_OK;
 }
 
-bool dim_ok(int d) { return d == 64 || d == 128; }
+// feature widths of the RGCN / RGAT layers: 64 and 128 in any combination,
+// 32 only as d_in = d_out = 32
+bool dims_ok(int d_in, int d_out)
+{
+    if (d_in == 32 || d_out == 32) return d_in == d_out;
+    return (d_in == 64 || d_in == 128) && (d_out == 64 || d_out == 128);
+}
 
 // ---- modelled HBM bytes of the two plans (gathered rows counted per edge) ----
 void plan_bytes(const rgnn_graph *g, int layer, int d_in, int d_out, int H, double *tf, double *af)
@@ -326,7 +332,8 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
     rgnn_status st = check_graph(g);
     if (st != RGNN_OK) return st;
     if (!h || !W || !out) return fail(RGNN_EINVAL, "NULL tensor pointer");
-    if (!dim_ok(d_in) || !dim_ok(d_out)) return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128");
+    if (!dims_ok(d_in, d_out))
+        return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128, or both 32");
     if (flags & ~RGNN_FLAG_RELU) return fail(RGNN_EINVAL, "unknown RGCN flag");
     if (plan < 0 || plan > 2) return fail(RGNN_EINVAL, "unknown plan");
     plan = resolve_plan(g, RGNN_LAYER_RGCN, d_in, d_out, 1, plan);
@@ -382,7 +389,8 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     rgnn_status st = check_graph(g);
     if (st != RGNN_OK) return st;
     if (!h || !W || !w_src || !w_dst || !out) return fail(RGNN_EINVAL, "NULL tensor pointer");
-    if (!dim_ok(d_in) || !dim_ok(d_out)) return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128");
+    if (!dims_ok(d_in, d_out))
+        return fail(RGNN_EUNSUPPORTED, "d_in, d_out must be 64 or 128, or both 32");
     if (heads <= 0 || d_out % heads) return fail(RGNN_EINVAL, "heads must divide d_out");
     if ((d_out / heads) % 16) return fail(RGNN_EUNSUPPORTED, "d_out / heads must be a multiple of 16");
     if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
@@ -604,8 +612,7 @@ extern "C" rgnn_status rgnn_segment_gemm(const float *X, int64_t ldx, const int3
 {
     if (!X || !W || !Y || !type_ptr) return fail(RGNN_EINVAL, "NULL pointer");
     if (num_types <= 0) return fail(RGNN_EINVAL, "num_types must be positive");
-    if (!((K == 64 || K == 128) && (Nc == 64 || Nc == 128)))
-        return fail(RGNN_EUNSUPPORTED, "K and Nc must be 64 or 128");
+    if (!dims_ok(K, Nc)) return fail(RGNN_EUNSUPPORTED, "K and Nc must be 64 or 128, or both 32");
     if (ldx < K || ldy < Nc) return fail(RGNN_EINVAL, "leading dimension too small");
     if (type_ptr[0] != 0) return fail(RGNN_EINVAL, "type_ptr[0] must be 0");
     for (int t = 0; t < num_types; ++t)

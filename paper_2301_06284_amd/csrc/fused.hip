@@ -347,12 +347,14 @@ template <int MODE>
 bool dispatch(int di, int dout, const FK &k, int64_t n, hipStream_t s)
 {
     if constexpr (MODE == kModeSum) {   // no transform: the output width is d_in
-        if (di == 64) launch_shape<64, 64, MODE>(k, n, s);
+        if (di == 32) launch_shape<32, 32, MODE>(k, n, s);
+        else if (di == 64) launch_shape<64, 64, MODE>(k, n, s);
         else if (di == 128) launch_shape<128, 128, MODE>(k, n, s);
         else return false;
         return true;
     }
-    if (di == 64 && dout == 64) launch_shape<64, 64, MODE>(k, n, s);
+    if (di == 32 && dout == 32) launch_shape<32, 32, MODE>(k, n, s);
+    else if (di == 64 && dout == 64) launch_shape<64, 64, MODE>(k, n, s);
     else if (di == 128 && dout == 128) launch_shape<128, 128, MODE>(k, n, s);
     else if constexpr (MODE == kModeMean) {   // RGCN only: RGAT needs d_in == d_out
         if (di == 64 && dout == 128) launch_shape<64, 128, MODE>(k, n, s);
@@ -385,7 +387,7 @@ rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s)
              : a.S     ? dispatch<kModeSum>(a.d_in, a.d_out, k, g->n_tiles_fused, s)
                        : dispatch<kModeMean>(a.d_in, a.d_out, k, g->n_tiles_fused, s);
     }
-    if (!ok) return fail(RGNN_EUNSUPPORTED, "fused aggregation: d_in, d_out must be 64 or 128");
+    if (!ok) return fail(RGNN_EUNSUPPORTED, "fused aggregation: unsupported (d_in, d_out)");
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "af_fused launch");
 }

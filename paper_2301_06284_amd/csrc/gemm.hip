@@ -261,7 +261,7 @@ void launch_k(const GemmK &k, int64_t ntiles, hipStream_t s)
     hipLaunchKernelGGL((typed_gemm_kernel<K, NC, EP, DH>), dim3((unsigned)ntiles), dim3(256), 0, s, k);
 }
 
-// Epilogues instantiated per shape: square shapes serve every layer; the
+// Epilogues instantiated per shape: square shapes (32, 64, 128) serve every layer; the
 // rectangular ones serve RGCN with d_in != d_out and the segment-MM entry
 // point; 64 x 192 is the fused K|V|Q projection of HGT.
 template <int K, int NC>
@@ -273,7 +273,9 @@ bool dispatch_square(int ep, int heads, const GemmK &k, int64_t n, hipStream_t s
         switch (heads) {
         case 1: launch_k<K, NC, EP_DOT, 1>(k, n, s); return true;
         case 2: launch_k<K, NC, EP_DOT, 2>(k, n, s); return true;
-        case 4: launch_k<K, NC, EP_DOT, 4>(k, n, s); return true;
+        case 4:
+            if constexpr (NC >= 64) { launch_k<K, NC, EP_DOT, 4>(k, n, s); return true; }
+            return false;
         case 8:
             if constexpr (NC >= 128) { launch_k<K, NC, EP_DOT, 8>(k, n, s); return true; }
             return false;
@@ -287,7 +289,9 @@ bool dispatch_square(int ep, int heads, const GemmK &k, int64_t n, hipStream_t s
         switch (heads) {
         case 1: launch_k<K, NC, 0>(k, n, s); return true;
         case 2: launch_k<K, NC, EP_BDIAG, 2>(k, n, s); return true;
-        case 4: launch_k<K, NC, EP_BDIAG, 4>(k, n, s); return true;
+        case 4:
+            if constexpr (NC >= 64) { launch_k<K, NC, EP_BDIAG, 4>(k, n, s); return true; }
+            return false;
         default: return false;
         }
     default: return false;
@@ -333,7 +337,8 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
     bool ok = false;
     {
         LaunchScope ls("typed_gemm", s);
-        if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, heads, k, a.ntiles, s);
+        if (a.K == 32 && a.Nc == 32) ok = dispatch_square<32, 32>(ep, heads, k, a.ntiles, s);
+        else if (a.K == 64 && a.Nc == 64) ok = dispatch_square<64, 64>(ep, heads, k, a.ntiles, s);
         else if (a.K == 128 && a.Nc == 128) ok = dispatch_square<128, 128>(ep, heads, k, a.ntiles, s);
         else if (a.K == 64 && a.Nc == 128) ok = dispatch_rect<64, 128>(ep, k, a.ntiles, s);
         else if (a.K == 128 && a.Nc == 64) ok = dispatch_rect<128, 64>(ep, k, a.ntiles, s);

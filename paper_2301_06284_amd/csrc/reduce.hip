@@ -452,10 +452,13 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 #define MERGE(D, H, SM) hipLaunchKernelGGL((merge_kernel<D, H, SM>), dim3(nb), dim3(256), 0, s, \
                                            g->n_split, sd, sp, partial, out, saved, relu)
         if (!softmax) {
-            if (d == 64) MERGE(64, 1, false);
+            if (d == 32) MERGE(32, 1, false);
+            else if (d == 64) MERGE(64, 1, false);
             else if (d == 128) MERGE(128, 1, false);
-            else return fail(RGNN_EUNSUPPORTED, "merge: d must be 64 or 128");
-        } else if (d == 64 && heads == 1) MERGE(64, 1, true);
+            else return fail(RGNN_EUNSUPPORTED, "merge: d must be 32, 64 or 128");
+        } else if (d == 32 && heads == 1) MERGE(32, 1, true);
+        else if (d == 32 && heads == 2) MERGE(32, 2, true);
+        else if (d == 64 && heads == 1) MERGE(64, 1, true);
         else if (d == 64 && heads == 2) MERGE(64, 2, true);
         else if (d == 64 && heads == 4) MERGE(64, 4, true);
         else if (d == 128 && heads == 1) MERGE(128, 1, true);
@@ -473,9 +476,12 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 #define MERGEB(D, H, SM) hipLaunchKernelGGL((merge_big_kernel<D, H, SM>), dim3(nbig), dim3(1024), 0, \
                                             s, bs, sd, sp, partial, out, saved, relu)
         if (!softmax) {
-            if (d == 64) MERGEB(64, 1, false);
+            if (d == 32) MERGEB(32, 1, false);
+            else if (d == 64) MERGEB(64, 1, false);
             else MERGEB(128, 1, false);
-        } else if (d == 64 && heads == 1) MERGEB(64, 1, true);
+        } else if (d == 32 && heads == 1) MERGEB(32, 1, true);
+        else if (d == 32 && heads == 2) MERGEB(32, 2, true);
+        else if (d == 64 && heads == 1) MERGEB(64, 1, true);
         else if (d == 64 && heads == 2) MERGEB(64, 2, true);
         else if (d == 64 && heads == 4) MERGEB(64, 4, true);
         else if (d == 128 && heads == 1) MERGEB(128, 1, true);
@@ -513,11 +519,14 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
                                float *out, int accumulate, int relu, hipStream_t s)
 {
     if (g->N == 0) return RGNN_OK;
-    if (d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 64 or 128");
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 32, 64 or 128");
     {
         LaunchScope ls("vseg_reduce", s);
         const unsigned nb = blocks_for(g->N, 256 / (d / 4));
-        if (d == 64)
+        if (d == 32)
+            hipLaunchKernelGGL((vseg_reduce_kernel<32>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
+        else if (d == 64)
             hipLaunchKernelGGL((vseg_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
                                g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
         else
@@ -535,12 +544,14 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
                                               0, s, L, g->dev.dst_vsegptr, T, scale, out, accumulate, relu)
         if (nmid) {
             LaunchScope ls("vseg_reduce_big", s);
-            if (d == 64) VRB(64, 256, g->dev.big_vdst, nmid);
+            if (d == 32) VRB(32, 256, g->dev.big_vdst, nmid);
+            else if (d == 64) VRB(64, 256, g->dev.big_vdst, nmid);
             else VRB(128, 256, g->dev.big_vdst, nmid);
         }
         if (nhuge) {
             LaunchScope ls("vseg_reduce_huge", s);
-            if (d == 64) VRB(64, 1024, huge, nhuge);
+            if (d == 32) VRB(32, 1024, huge, nhuge);
+            else if (d == 64) VRB(64, 1024, huge, nhuge);
             else VRB(128, 1024, huge, nhuge);
         }
 #undef VRB
@@ -553,11 +564,14 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
                                   float *out, float *saved, hipStream_t s)
 {
     if (g->N == 0) return RGNN_OK;
-    if (d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 64 or 128");
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 32, 64 or 128");
     {
         LaunchScope ls("softmax_reduce", s);
         const unsigned nb = blocks_for(g->N, 256 / (d / 4));
-        if (d == 64)
+        if (d == 32)
+            hipLaunchKernelGGL((softmax_reduce_kernel<32>), dim3(nb), dim3(256), 0, s, g->N,
+                               g->dev.dst_vsegptr, vstat, T, out, saved);
+        else if (d == 64)
             hipLaunchKernelGGL((softmax_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
                                g->dev.dst_vsegptr, vstat, T, out, saved);
         else
@@ -574,12 +588,14 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
                                               dim3(NTH), 0, s, L, g->dev.dst_vsegptr, vstat, T, out, saved)
         if (nmid) {
             LaunchScope ls("softmax_reduce_big", s);
-            if (d == 64) SRB(64, 256, g->dev.big_vdst, nmid);
+            if (d == 32) SRB(32, 256, g->dev.big_vdst, nmid);
+            else if (d == 64) SRB(64, 256, g->dev.big_vdst, nmid);
             else SRB(128, 256, g->dev.big_vdst, nmid);
         }
         if (nhuge) {
             LaunchScope ls("softmax_reduce_huge", s);
-            if (d == 64) SRB(64, 1024, huge, nhuge);
+            if (d == 32) SRB(32, 1024, huge, nhuge);
+            else if (d == 64) SRB(64, 1024, huge, nhuge);
             else SRB(128, 1024, huge, nhuge);
         }
 #undef SRB
@@ -621,7 +637,8 @@ rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int h
 {
     const int64_t rows = (int64_t)R * d_in;
     if (rows == 0) return RGNN_OK;
-    if (d_out != 64 && d_out != 128) return fail(RGNN_EUNSUPPORTED, "reorder: d_out must be 64 or 128");
+    if (d_out != 32 && d_out != 64 && d_out != 128)
+        return fail(RGNN_EUNSUPPORTED, "reorder: d_out must be 32, 64 or 128");
     const unsigned nb = blocks_for(rows, 256 / (d_out / 4));
     bool ok = true;
     {
@@ -629,7 +646,9 @@ rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int h
 #define RV(DO, DH) hipLaunchKernelGGL((reorder_vec_kernel<DO, DH>), dim3(nb), dim3(256), 0, s, W, v1, v2, R, \
                                       d_in, out1, out2)
         const int dh = d_out / heads;
-        if (d_out == 64 && dh == 64) RV(64, 64);
+        if (d_out == 32 && dh == 32) RV(32, 32);
+        else if (d_out == 32 && dh == 16) RV(32, 16);
+        else if (d_out == 64 && dh == 64) RV(64, 64);
         else if (d_out == 64 && dh == 32) RV(64, 32);
         else if (d_out == 64 && dh == 16) RV(64, 16);
         else if (d_out == 128 && dh == 128) RV(128, 128);

@@ -365,7 +365,9 @@ rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s)
     const unsigned nb = blocks_for((a.g->V + kSegPerGroup - 1) / kSegPerGroup, 256 / (a.d / 4));
 #define SA(D, H) hipLaunchKernelGGL((seg_attn_kernel<D, H>), dim3(nb), dim3(256), 0, s, k, a.g->V, \
                                     a.g->dev.vseg_dst)
-    if (a.d == 64 && a.heads == 1) SA(64, 1);
+    if (a.d == 32 && a.heads == 1) SA(32, 1);
+    else if (a.d == 32 && a.heads == 2) SA(32, 2);
+    else if (a.d == 64 && a.heads == 1) SA(64, 1);
     else if (a.d == 64 && a.heads == 2) SA(64, 2);
     else if (a.d == 64 && a.heads == 4) SA(64, 4);
     else if (a.d == 128 && a.heads == 1) SA(128, 1);
@@ -386,7 +388,9 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
     if (!a.wsp) return fail(RGNN_EINVAL, "RGAT traversal needs w_src");
 #define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf1_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
-    if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
+    if (a.d == 32 && a.heads == 1) RGAT_TF(32, 1);
+    else if (a.d == 32 && a.heads == 2) RGAT_TF(32, 2);
+    else if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);
     else if (a.d == 64 && a.heads == 2) RGAT_TF(64, 2);
     else if (a.d == 64 && a.heads == 4) RGAT_TF(64, 4);
     else if (a.d == 128 && a.heads == 1) RGAT_TF(128, 1);
@@ -405,9 +409,10 @@ rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s)
     TK k = make_tk(a);
     LaunchScope ls("rgcn_traverse_tf", s);
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
-    if (a.d == 64) hipLaunchKernelGGL((rgcn_tf_kernel<64>), dim3(nb), dim3(256), 0, s, k);
+    if (a.d == 32) hipLaunchKernelGGL((rgcn_tf_kernel<32>), dim3(nb), dim3(256), 0, s, k);
+    else if (a.d == 64) hipLaunchKernelGGL((rgcn_tf_kernel<64>), dim3(nb), dim3(256), 0, s, k);
     else if (a.d == 128) hipLaunchKernelGGL((rgcn_tf_kernel<128>), dim3(nb), dim3(256), 0, s, k);
-    else return fail(RGNN_EUNSUPPORTED, "RGCN traversal: d must be 64 or 128");
+    else return fail(RGNN_EUNSUPPORTED, "RGCN traversal: d must be 32, 64 or 128");
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "rgcn_tf launch");
 }

@@ -11,6 +11,7 @@ Workloads (seeded, see workloads/synth.py):
   3  HGT    1.9 M nodes / 21 M edges / 7 relations, d = 64 = 4 x 16
   4  RGCN, RGAT at d = 128 on 2.5 M nodes / 16 M edges / 535 relations
   5  RGAT and RGCN backward on workload 2's graph
+Workload 2's graph also runs at d = 32 (the hidden-size sweep).
 """
 import numpy as np
 import pytest
@@ -112,6 +113,26 @@ def test_workload2_rgat_per_relation_softmax():
     sel = sample_rows(g, 300, seed=5)
     ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1, sel=sel)
     assert row_err(got[sel], ref) <= TOL
+
+
+@pytest.mark.parametrize("layer", ["rgat", "rgcn"])
+def test_workload2_graph_d32(layer):
+    """The hidden-size sweep's narrow end: workload 2's graph with d = 32
+    tensors, both plans."""
+    g, _, _ = load(2)
+    t = workloads.make_tensors(2, g, "rgat", 32)
+    run = Runner(g, t)
+    sel = sample_rows(g, 200, seed=32)
+    if layer == "rgat":
+        ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], sel=sel)
+    else:
+        ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"], sel=sel)
+    for plan in (1, 2):
+        print(f"workload 2 graph d=32 {layer} plan={plan}", flush=True)
+        got = run.rgat(plan=plan) if layer == "rgat" else run.rgcn(W0=True, plan=plan)
+        assert np.isfinite(got).all()
+        assert row_err(got[sel], ref) <= TOL
+    run.close()
 
 
 def test_workload3_hgt():

@@ -38,7 +38,7 @@ def test_device_graph_index_bit_exact(kind):
     G.close()
 
 
-@pytest.mark.parametrize("K,Nc", [(64, 64), (128, 128), (64, 128), (128, 64)])
+@pytest.mark.parametrize("K,Nc", [(32, 32), (64, 64), (128, 128), (64, 128), (128, 64)])
 def test_segment_gemm(K, Nc):
     import torch
     from paper_2301_06284_amd import rgnn
@@ -121,7 +121,72 @@ def test_rgat_d128(plan, heads):
 
 
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("plan", [1, 2])
+@pytest.mark.parametrize("W0,relu", [(True, True), (False, False)])
+def test_rgcn_d32(kind, plan, W0, relu):
+    """Hidden size 32 (the narrow end of the hidden-size sweep)."""
+    g = graph(kind, seed=41)
+    t = workloads.tiny_tensors(41, g, 32, 32)
+    print(f"rgcn d32 {kind} plan={plan} W0={W0} relu={relu}", flush=True)
+    run = Runner(g, t)
+    got = run.rgcn(W0=W0, relu=relu, plan=plan)
+    ref = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"] if W0 else None, relu=relu)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (3, 1), (1, 2)])
+def test_rgat_d32(kind, plan, heads):
+    g = graph(kind, seed=42)
+    t = workloads.tiny_tensors(42, g, 32, 32, heads=heads, att_var=1.0)
+    print(f"rgat d32 {kind} plan={plan} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got, saved = run.rgat(heads=heads, plan=plan, want_saved=True)
+    ref, mx, sm = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads,
+                                      want_stats=True)
+    run.close()
+    assert row_err(got, ref) <= TOL
+    sv = saved.cpu().numpy()
+    np.testing.assert_allclose(sv[..., 0], mx, rtol=1e-4, atol=1e-4)
+    np.testing.assert_allclose(sv[..., 1], sm, rtol=1e-4, atol=1e-5)
+
+
+def test_d32_huge_hub():
+    """d = 32 through the 256- and 1024-thread reductions and the split
+    destination merges (a hub with thousands of in-edges)."""
+    g = graph("hub", seed=43, N=200, E=70000, R=3)
+    t = workloads.tiny_tensors(43, g, 32, 32, att_var=1.0)
+    print("d32 huge hub", flush=True)
+    run = Runner(g, t)
+    ref_gcn = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"])
+    ref_gat = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"])
+    for plan in (1, 2):
+        assert row_err(run.rgcn(plan=plan), ref_gcn) <= TOL
+        assert row_err(run.rgat(plan=plan), ref_gat) <= TOL
+    ref_rel = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], scope=1)
+    assert row_err(run.rgat(scope=1), ref_rel) <= TOL
+    run.close()
+
+
+def test_d32_rejects_mixed_widths():
+    import torch
+    from paper_2301_06284_amd import rgnn
+    g = graph("random", seed=44)
+    t = workloads.tiny_tensors(44, g, 32, 64)
+    print("d32 mixed widths rejected", flush=True)
+    run = Runner(g, t)
+    T = run.T
+    out = torch.empty(g["N"], 64, device="cuda:0")
+    ws = run.ws(0, 32, 64, 1, 1)
+    with pytest.raises(rgnn.RgnnError) as e:
+        rgnn.rgcn_forward(run.G, T["h"], T["W"], None, out, ws, 32, 64, plan=rgnn.PLAN_TRANSFORM_FIRST)
+    assert e.value.status == rgnn.EUNSUPPORTED
+    run.close()
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_rgat_per_relation_softmax(kind, d):
     """Softmax over the in-edges of one (destination, relation) segment."""
     g = graph(kind)

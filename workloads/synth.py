@@ -136,14 +136,15 @@ def _normal(rng, shape, var: float) -> np.ndarray:
     return (rng.standard_normal(shape, dtype=np.float32) * np.float32(np.sqrt(var)))
 
 
-def make_tensors(k: int, g: dict, layer: str | None = None) -> dict:
+def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None) -> dict:
     """Features, weights and (workloads 1, 2, 3, 5) the loss weight for workload k.
     Variances: features and weights 1/fan_in, attention vectors 0.1, HGT head
-    blocks 1/d_k, loss weight 1."""
+    blocks 1/d_k, loss weight 1.  `d` overrides the workload's hidden size (the
+    hidden-size sweep)."""
     c = CONFIGS[k]
     _, _, f_rng, w_rng, a_rng, l_rng = _streams(k)
     layer = layer or c["layers"][0]
-    N, R, T, d = g["N"], c["R"], c["T"], c["d"]
+    N, R, T, d = g["N"], c["R"], c["T"], d or c["d"]
     out = dict(h=_normal(f_rng, (N, d), 1.0 / d))
     if layer in ("rgcn", "rgat", "rgat_bwd"):
         out["W"] = _normal(w_rng, (R, d, d), 1.0 / d)
