@@ -467,7 +467,7 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
             ta.g = g; ta.vstat = w.vstat; ta.vscale = w.vscale;
             if ((st = launch_seg_softmax_scale(ta, s)) != RGNN_OK) return st;
             if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
-        } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, s)) != RGNN_OK) {
+        } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, w.vscale, s)) != RGNN_OK) {
             return st;
         }
     }

@@ -12,22 +12,23 @@
 // relation, ordered by edge count (largest first); a host-built tile table
 // gives each workgroup up to kFusedTileRows consecutive segments of one
 // relation, so W_r is staged once in LDS for the whole tile.  A wave takes 16
-// segments at a time -- one 16-row MFMA block -- and gathers them in the MFMA
-// operand layout itself: lane (li, q) owns segment li of the block and columns
-// 16c + 4q .. +3 of its rows, so every gathered row is four dwordx4 loads per
-// lane of four lanes, and the finished sums are already the B operand of
-// v_mfma_f32_16x16x4f32 (the same transposed-block scheme as the typed GEMM:
-// lane (li, q) receives row li, columns 4q .. 4q+3 of each 16-column block).
-// Because the 16 segments of a block have nearly equal edge counts, the edge
-// loop wastes few lane-steps.
+// segments at a time -- one 16-row MFMA block.  The rows are gathered with
+// eight adjacent lanes per source row (whole 128-byte lines per load
+// instruction), summed, and moved into the B-operand layout of
+// v_mfma_f32_16x16x4f32 by lane permutes; the products are permuted back to
+// the row layout for the stores.  Because the 16 segments of a block have
+// nearly equal edge counts, the edge loop wastes few lane-steps, and the first
+// gathers of a wave's next block are issued before the current block's
+// transform so that loads stay in flight.
 //
 // RGAT: per edge the source term h_u . (W_r w_src[r]) (reordered) is summed
-// over the four lanes of the row; with the segment's destination term it gives
-// the logit, and an online softmax keeps the running maximum m, the sum s and
-// the exp-weighted row sum.  T and (m, s) are written per segment; the
-// per-destination normalisation exp(m - M_v) / Z_v is applied when the
-// segments of a destination are summed.  RGCN: plain sums scaled by
-// 1 / c_{v,r}.  No atomics: results are bitwise reproducible.
+// over the eight lanes of the row; with the segment's destination term it
+// gives the logit, and an online softmax keeps the running maximum m, the sum
+// s and the exp-weighted row sum.  T is written per segment (row vs), (m, s)
+// per segment in the fused order (sequential stores; the reductions find them
+// through vseg_fpos); the per-destination normalisation exp(m - M_v) / Z_v is
+// applied when the segments of a destination are summed.  RGCN: plain sums
+// scaled by 1 / c_{v,r}.  No atomics: results are bitwise reproducible.
 #include "rgnn_internal.h"
 #include "wave_ops.h"
 
@@ -63,15 +64,15 @@ struct FK {
 // within each the features 32c + 4(l%8) .. +3 (c < DI/32), so one dwordx4
 // load instruction covers whole 128-byte lines of eight rows.  The finished
 // row sums are moved into the MFMA operand layout by lane permutes.
-template <int DI, int DO, int MODE, int NWAVE, int KU>
-__global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4))) void af_fused_kernel(FK k)
+template <int DI, int DO, int MODE, int NWAVE, int KU, int WPE>
+__global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE))) void af_fused_kernel(FK k)
 {
     constexpr int NT = 64 * NWAVE;
     constexpr int KP = DI + 4;       // padded LDS row (conflict-free b128 reads)
     constexpr int KC = DI / 16;      // MFMA k chunks
     constexpr int CH = DI / 32;      // float4 chunks per lane and gathered row
     constexpr int NCB = DO / 16;     // output column blocks
-    constexpr int CBP = NCB < 4 ? NCB : 4;
+    constexpr int CBP = 2;           // output column blocks per MFMA pass
     constexpr int NW = DI * DO / 4 / NT;
     constexpr int NR = (kFusedTileRows + NT - 1) / NT;   // segment entries per thread
     constexpr int NS = (kFusedTileEdges + NT - 1) / NT;  // source indices per thread
@@ -140,27 +141,61 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
     __syncthreads();
 
     const int nrb = (tile.rows + 15) >> 4;
-    for (int rb = wave; rb < nrb; rb += NWAVE) {
-        // the two gathered rows of this lane; rows past the tile's end repeat
-        // the block's first row (never longer than the block's longest) and
-        // store nothing
+    // One 16-row block's gathered rows, as this lane sees them: rows past the
+    // tile's end repeat the block's first row (never longer than the block's
+    // longest) and store nothing.
+    struct Blk {
         FusedRow fr[2];
         bool valid[2];
-        const int32_t *ls[2];
-        float va[2];
+        int lso[2];      // first source index of the row in ssrc
+        int fp[2];       // position of the row in the fused order
+        float va[2];     // destination attention term
+        int nmax;        // edge count of the block's longest segment
+    };
+    auto setup = [&](int rb, Blk &b) {
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
             const int row = rb * 16 + gr + 8 * h2;
-            valid[h2] = row < tile.rows;
-            fr[h2] = srow[valid[h2] ? row : rb * 16];
-            ls[h2] = ssrc + (fr[h2].e0 - te0);
-            va[h2] = MODE == kModeSoftmax ? k.vatt[fr[h2].vs] : 0.f;
+            b.valid[h2] = row < tile.rows;
+            b.fp[h2] = (int)tile.row0 + row;
+            b.fr[h2] = srow[b.valid[h2] ? row : rb * 16];
+            b.lso[h2] = (int)(b.fr[h2].e0 - te0);
+            b.va[h2] = MODE == kModeSoftmax ? k.vatt[b.fr[h2].vs] : 0.f;
         }
-        // edge count of the block's longest segment
-        float nm = gmax<32>(fmaxf((float)fr[0].ne, (float)fr[1].ne));
+        float nm = gmax<32>(fmaxf((float)b.fr[0].ne, (float)b.fr[1].ne));
         nm = fmaxf(nm, __shfl_xor(nm, 32));
-        const int nmax = __builtin_amdgcn_readfirstlane((int)nm);
-
+        b.nmax = __builtin_amdgcn_readfirstlane((int)nm);
+    };
+    // batches of KU edges of both rows (indices from LDS); a row already
+    // finished issues no gathers (most segments are one or two edges long)
+    float4 A[KU][2][CH], B[KU][2][CH];
+    auto load = [&](const Blk &b, float4 (&X)[KU][2][CH], int t) {
+#pragma unroll
+        for (int u = 0; u < KU; ++u)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                if (t + u < b.fr[h2].ne) {
+                    const int i = ssrc[b.lso[h2] + t + u];
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) X[u][h2][c] = ld4(k.h + (size_t)i * DI + c * 32 + gp * 4);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) X[u][h2][c] = make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+            }
+    };
+    // The first batch of a wave's next block is issued before the current
+    // block's transform and stores, so a wave always has gathers in flight
+    // (blocks of one- and two-edge segments are a single batch).
+    Blk cur;
+    if (wave < nrb) {
+        setup(wave, cur);
+        load(cur, A, 0);
+    }
+    for (int rb = wave; rb < nrb; rb += NWAVE) {
+        const FusedRow (&fr)[2] = cur.fr;
+        const bool (&valid)[2] = cur.valid;
+        const int nmax = cur.nmax;
         float m[2] = {-INFINITY, -INFINITY}, s[2] = {0.f, 0.f};
         float4 acc[2][CH];
 #pragma unroll
@@ -168,25 +203,6 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
 #pragma unroll
             for (int c = 0; c < CH; ++c) acc[h2][c] = make_float4(0.f, 0.f, 0.f, 0.f);
 
-        // ping-pong batches of KU edges of both rows (indices from LDS); a row
-        // already finished issues no gathers (most segments are one or two
-        // edges long)
-        float4 A[KU][2][CH], B[KU][2][CH];
-        auto load = [&](float4 (&X)[KU][2][CH], int t) {
-#pragma unroll
-            for (int u = 0; u < KU; ++u)
-#pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2) {
-                    if (t + u < fr[h2].ne) {
-                        const int i = ls[h2][t + u];
-#pragma unroll
-                        for (int c = 0; c < CH; ++c) X[u][h2][c] = ld4(k.h + (size_t)i * DI + c * 32 + gp * 4);
-                    } else {
-#pragma unroll
-                        for (int c = 0; c < CH; ++c) X[u][h2][c] = make_float4(0.f, 0.f, 0.f, 0.f);
-                    }
-                }
-        };
         auto consume = [&](const float4 (&X)[KU][2][CH], int t) {
 #pragma unroll
             for (int u = 0; u < KU; ++u) {
@@ -203,7 +219,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                         if (t + u < fr[h2].ne) {
                             // online update with one exponential: the smaller of
                             // the old maximum and z is scaled by exp(-|z - m|)
-                            const float z = leaky(p + va[h2], k.slope);
+                            const float z = leaky(p + cur.va[h2], k.slope);
                             const bool up = z > m[h2];
                             const float ex = __expf(up ? m[h2] - z : z - m[h2]);
                             const float c1 = up ? ex : 1.f, c2 = up ? 1.f : ex;
@@ -227,20 +243,26 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                 }
             }
         };
-        // batches past the block's longest segment are neither loaded nor
-        // consumed (wave-uniform tests)
-        load(A, 0);
+        // ping-pong: batch 0 is already in A; batches past the block's
+        // longest segment are neither loaded nor consumed (wave-uniform tests)
         __builtin_amdgcn_sched_barrier(0);
         for (int t = 0; t < nmax; t += 2 * KU) {
             const bool more_b = t + KU < nmax;
-            if (more_b) load(B, t + KU);
+            if (more_b) load(cur, B, t + KU);
             __builtin_amdgcn_sched_barrier(0);
             consume(A, t);
             if (!more_b) break;
-            if (t + 2 * KU < nmax) load(A, t + 2 * KU);
+            if (t + 2 * KU < nmax) load(cur, A, t + 2 * KU);
             __builtin_amdgcn_sched_barrier(0);
             consume(B, t + KU);
         }
+        // the next block's first batch goes out now
+        Blk nxt = cur;
+        if (rb + NWAVE < nrb) {
+            setup(rb + NWAVE, nxt);
+            load(nxt, A, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
 
         if (MODE == kModeSum) {   // the segment means themselves, in the row layout
 #pragma unroll
@@ -254,6 +276,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                     st4(o + c * 32, make_float4(a.x * sc, a.y * sc, a.z * sc, a.w * sc));
                 }
             }
+            cur = nxt;
             continue;
         }
         // row sums -> MFMA operand layout by lane permutes: lane (li, q) takes
@@ -270,7 +293,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                 }
             }
             if (MODE == kModeSoftmax && valid[h2] && gp == 0)
-                *reinterpret_cast<float2 *>(k.vstat + (size_t)fr[h2].vs * 2) = make_float2(m[h2], s[h2]);
+                *reinterpret_cast<float2 *>(k.vstat + (size_t)cur.fp[h2] * 2) = make_float2(m[h2], s[h2]);
         }
         const bool hi = li >= 8;
         float4 sb[KC];
@@ -329,6 +352,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(4)))
                 }
             }
         }
+        cur = nxt;
     }
 }
 
@@ -339,7 +363,10 @@ void launch_shape(const FK &k, int64_t ntiles, hipStream_t s)
     // rows per wave in flight keeps the gathered rows within the VGPR budget
     constexpr int NWAVE = (DI == 128 || DO == 128) ? 8 : 4;
     constexpr int KU = DI == 128 ? 1 : 2;
-    hipLaunchKernelGGL((af_fused_kernel<DI, DO, MODE, NWAVE, KU>), dim3((unsigned)ntiles),
+    // waves per SIMD the LDS allows; the 128 x 64 mean shape gets the register
+    // budget of three
+    constexpr int WPE = (DI == 128 && DO == 64) ? 3 : 4;
+    hipLaunchKernelGGL((af_fused_kernel<DI, DO, MODE, NWAVE, KU, WPE>), dim3((unsigned)ntiles),
                        dim3(64 * NWAVE), 0, s, k);
 }
 

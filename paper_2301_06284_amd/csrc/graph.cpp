@@ -169,11 +169,13 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             counting_sort(fperm, x.vseg_rel.data(), R, tmp, cnt);
             x.fused_rows.resize((size_t)g->V);
             x.fused_src.resize((size_t)E);
+            x.vseg_fpos.resize((size_t)g->V);
             int32_t fpos = 0;
             for (int64_t i = 0; i < g->V; ++i) {
                 const int32_t vs = fperm[i];
                 const int32_t b = x.vseg_ptr[vs], n = x.vseg_ptr[vs + 1] - b;
                 x.fused_rows[i] = FusedRow{vs, fpos, n, x.vseg_cnt[vs]};
+                x.vseg_fpos[vs] = (int32_t)i;
                 for (int32_t j = 0; j < n; ++j) x.fused_src[(size_t)fpos + j] = x.in_src[(size_t)b + j];
                 fpos += n;
             }
@@ -378,6 +380,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.tiles_fused, x.tiles_fused.data(), x.tiles_fused.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.fused_rows, x.fused_rows.data(), x.fused_rows.size() * sizeof(FusedRow)});
     add32(&d.fused_src, x.fused_src);
+    add32(&d.vseg_fpos, x.vseg_fpos);
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
     add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});

@@ -30,28 +30,34 @@ __device__ __forceinline__ float4 relu4(float4 a)
 }
 
 // Softmax per (dst, rel) segment: a segment longer than kChunkEdges is cut into
-// several virtual segments, each with its own (max m_i, sum s_i); per virtual
-// segment the scale exp(m_i - M) / Z of its (dst, rel) segment is written.
-// Segments with more than kBigRange pieces are left to the block kernel.
+// several virtual segments, each with its own (max m_i, sum s_i), stored at the
+// segment's fused position fpos[i]; per virtual segment the scale
+// exp(m_i - M) / Z of its (dst, rel) segment is written.  Segments with more
+// than kBigRange pieces are left to the block kernel.
 __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *grp_vsegptr,
-                                                         const float *vstat, float *vscale)
+                                                         const int32_t *fpos, const float *vstat,
+                                                         float *vscale)
 {
     const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (v >= N) return;
     const int b = grp_vsegptr[v], e = grp_vsegptr[v + 1];
     if (e - b > kBigRange) return;
     float M = -INFINITY;
-    for (int i = b; i < e; ++i) M = fmaxf(M, vstat[(size_t)i * 2]);
+    for (int i = b; i < e; ++i) M = fmaxf(M, vstat[(size_t)fpos[i] * 2]);
     float Z = 0.f;
-    for (int i = b; i < e; ++i) Z += vstat[(size_t)i * 2 + 1] * __expf(vstat[(size_t)i * 2] - M);
-    for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)i * 2] - M) / Z;
+    for (int i = b; i < e; ++i) {
+        const float2 st = *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2);
+        Z += st.y * __expf(st.x - M);
+    }
+    for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)fpos[i] * 2] - M) / Z;
 }
 
 // One workgroup per group with many segments: strided per-thread partial
 // (max, sum), combined in thread order through LDS.
 __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_grp,
                                                              const int32_t *grp_vsegptr,
-                                                             const float *vstat, float *vscale)
+                                                             const int32_t *fpos, const float *vstat,
+                                                             float *vscale)
 {
     __shared__ float sm[256], ss[256];
     __shared__ float fin[2];
@@ -59,7 +65,8 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
     const int b = grp_vsegptr[v], e = grp_vsegptr[v + 1];
     float m = -INFINITY, s = 0.f;
     for (int i = b + (int)threadIdx.x; i < e; i += 256) {
-        const float mi = vstat[(size_t)i * 2], si = vstat[(size_t)i * 2 + 1];
+        const float2 st = *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2);
+        const float mi = st.x, si = st.y;
         const float mn = fmaxf(m, mi);
         s = s * __expf(m - mn) + si * __expf(mi - mn);
         m = mn;
@@ -78,7 +85,7 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
     }
     __syncthreads();
     const float M = fin[0], Zi = 1.f / fin[1];
-    for (int i = b + (int)threadIdx.x; i < e; i += 256) vscale[i] = __expf(vstat[(size_t)i * 2] - M) * Zi;
+    for (int i = b + (int)threadIdx.x; i < e; i += 256) vscale[i] = __expf(vstat[(size_t)fpos[i] * 2] - M) * Zi;
 }
 
 // out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
@@ -155,15 +162,16 @@ __global__ __launch_bounds__(NTH) void vseg_reduce_big_kernel(const int32_t *big
 // ---------------------------------------------------------------- softmax reduction
 // Softmax per destination finished and summed in one pass: per destination v
 // with segments i (each with its own logit maximum m_i, sum s_i and
-// exp-weighted transformed row T_i relative to m_i):
+// exp-weighted transformed row T_i relative to m_i; (m_i, s_i) stored at the
+// segment's fused position fpos[i]):
 //   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
 // and saved[v] = (M, Z) ((0, 0) without in-edges).  A group of D/4 lanes per
 // destination; the statistics are taken over the group's lanes (fixed
 // butterfly), the rows summed in segment order.
 template <int D>
 __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
-                                                             const float *vstat, const float *T,
-                                                             float *out, float *saved)
+                                                             const int32_t *fpos, const float *vstat,
+                                                             const float *T, float *out, float *saved)
 {
     constexpr int G = D / 4, GPB = 256 / G;
     constexpr int NE = (kBigRange + G - 1) / G;   // statistics entries per lane
@@ -172,11 +180,21 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const in
     if (v >= N) return;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     if (e - b > kBigRange) return;
+    // rows in batches of four, two batches in flight; the first goes out before
+    // the statistics are gathered (the rows do not depend on them)
+    float4 ta[4], tb[4];
+    auto load = [&](float4 (&t)[4], int i0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < e) t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
+    };
+    load(ta, b);
+    // lane gl holds the statistics of segments b + gl + j G
     float mi[NE], si[NE];
 #pragma unroll
     for (int j = 0; j < NE; ++j) {
         const int i = b + gl + j * G;
-        const float2 st = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2)
+        const float2 st = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2)
                                 : make_float2(-INFINITY, 0.f);
         mi[j] = st.x;
         si[j] = st.y;
@@ -191,21 +209,29 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const in
     const float Z = gsum<G>(z);
     if (saved && gl == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(b < e ? M : 0.f, Z);
     const float inv = Z > 0.f ? 1.f / Z : 0.f;
-    // rows in batches of four (all in flight together), summed in segment order
+    float w[NE];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) w[j] = si[j] > 0.f ? __expf(mi[j] - M) * inv : 0.f;
+    // summed in segment order; segment b + r takes its weight from lane r % G
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i0 = b; i0 < e; i0 += 4) {
-        float4 t[4];
-        float mu[4];
+    auto consume = [&](const float4 (&t)[4], int i0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            if (i0 + u < e) {
-                t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
-                mu[u] = vstat[(size_t)(i0 + u) * 2];
-            }
-        }
+            const int r = i0 + u - b, jr = r / G;
+            float x = w[0];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (i0 + u < e) acc = fma4(t[u], __expf(mu[u] - M) * inv, acc);
+            for (int j = 1; j < NE; ++j) x = jr == j ? w[j] : x;
+            const float wu = __shfl(x, r % G, G);
+            if (i0 + u < e) acc = fma4(t[u], wu, acc);
+        }
+    };
+    for (int i0 = b; i0 < e; i0 += 8) {
+        const bool more = i0 + 4 < e;
+        if (more) load(tb, i0 + 4);
+        consume(ta, i0);
+        if (!more) break;
+        if (i0 + 8 < e) load(ta, i0 + 8);
+        consume(tb, i0 + 4);
     }
     st4(out + (size_t)v * D + gl * 4, acc);
 }
@@ -213,14 +239,17 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const in
 // The same for destinations with more than kBigRange segments, one workgroup
 // of NTH threads each: every thread folds its strided share of the (max, sum)
 // pairs into one online pair (four loads in flight), the maximum and the
-// denominator follow by workgroup reductions; then every group of D/4 lanes
-// sums a strided subset of the rows (U in flight) and the group sums are added
-// in group order.
+// denominator follow by workgroup reductions; every thread then writes the
+// weights exp(m_i - M) / Z of its share to scale[i] (segment order, so the row
+// pass reads them without the fused-position indirection); then every group of
+// D/4 lanes sums a strided subset of the rows (U in flight) and the group sums
+// are added in group order.
 template <int D, int NTH, int U>
 __global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *big_vdst,
                                                                  const int32_t *dst_vsegptr,
-                                                                 const float *vstat, const float *T,
-                                                                 float *out, float *saved)
+                                                                 const int32_t *fpos, const float *vstat,
+                                                                 const float *T, float *out, float *saved,
+                                                                 float *scale)
 {
     constexpr int G = D / 4, NG = NTH / G, NWV = NTH / 64;
     __shared__ float red[NWV];
@@ -235,7 +264,7 @@ __global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int i = i0 + u * NTH;
-            st[u] = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)i * 2) : make_float2(-INFINITY, 0.f);
+            st[u] = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2) : make_float2(-INFINITY, 0.f);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -264,21 +293,33 @@ __global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *
     for (int w = 0; w < NWV; ++w) Z += red[w];
     if (saved && tid == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(M, Z);
     const float inv = 1.f / Z;
+    for (int i0 = b + tid; i0 < e; i0 += 4 * NTH) {
+        float mu[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * NTH;
+            mu[u] = i < e ? vstat[(size_t)fpos[i] * 2] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u * NTH < e) scale[i0 + u * NTH] = __expf(mu[u] - M) * inv;
+    }
+    __syncthreads();   // the weights are read by other threads of the workgroup
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int i0 = b + gi; i0 < e; i0 += U * NG) {
         float4 t[U];
-        float mu[U];
+        float wu[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int i = i0 + u * NG;
             if (i < e) {
                 t[u] = ld4(T + (size_t)i * D + gl * 4);
-                mu[u] = vstat[(size_t)i * 2];
+                wu[u] = scale[i];
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (i0 + u * NG < e) acc = fma4(t[u], __expf(mu[u] - M) * inv, acc);
+            if (i0 + u * NG < e) acc = fma4(t[u], wu[u], acc);
     }
     part[gi * G + gl] = acc;
     __syncthreads();
@@ -501,7 +542,7 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
     {
         LaunchScope ls("seg_softmax_scale", s);
         hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(g->U_dst, 256)), dim3(256), 0, s, g->U_dst,
-                           g->dev.seg_vsegptr, a.vstat, a.vscale);
+                           g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale);
     }
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "seg_softmax_scale launch");
@@ -509,7 +550,7 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
     {
         LaunchScope ls("seg_softmax_scale_big", s);
         hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)g->n_big_seg), dim3(256), 0, s,
-                           g->dev.big_seg, g->dev.seg_vsegptr, a.vstat, a.vscale);
+                           g->dev.big_seg, g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale);
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_softmax_scale_big launch");
@@ -561,7 +602,7 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
 }
 
 rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
-                                  float *out, float *saved, hipStream_t s)
+                                  float *out, float *saved, float *scale, hipStream_t s)
 {
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 32, 64 or 128");
@@ -570,13 +611,13 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
         const unsigned nb = blocks_for(g->N, 256 / (d / 4));
         if (d == 32)
             hipLaunchKernelGGL((softmax_reduce_kernel<32>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, vstat, T, out, saved);
+                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
         else if (d == 64)
             hipLaunchKernelGGL((softmax_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, vstat, T, out, saved);
+                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
         else
             hipLaunchKernelGGL((softmax_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, vstat, T, out, saved);
+                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
     }
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "softmax_reduce launch");
@@ -585,7 +626,7 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
     const int32_t *huge = g->dev.big_vdst + nmid;
     {
 #define SRB(D, NTH, L, NB) hipLaunchKernelGGL((softmax_reduce_big_kernel<D, NTH, NTH == 1024 ? 16 : 4>), dim3((unsigned)(NB)), \
-                                              dim3(NTH), 0, s, L, g->dev.dst_vsegptr, vstat, T, out, saved)
+                                              dim3(NTH), 0, s, L, g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved, scale)
         if (nmid) {
             LaunchScope ls("softmax_reduce_big", s);
             if (d == 32) SRB(32, 256, g->dev.big_vdst, nmid);

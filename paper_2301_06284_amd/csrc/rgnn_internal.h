@@ -63,6 +63,7 @@ struct HostIndex {
     std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
     std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
+    std::vector<int32_t> vseg_fpos;    // position of each vseg in fused_rows [V]
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
     std::vector<float> invcnt_byrel;      // 1 / c_{v,r} of each virtual segment, by-relation order
@@ -99,6 +100,7 @@ struct DeviceIndex {
     int32_t *types_chunkptr = nullptr;
     FusedRow *fused_rows = nullptr;
     int32_t *fused_src = nullptr;
+    int32_t *vseg_fpos = nullptr;
     Tile *tiles_fused = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
@@ -207,7 +209,7 @@ struct TravArgs {
     float *out = nullptr;                // [N, d]
     float *saved = nullptr;              // [N, heads, 2] or NULL
     float *partial = nullptr;            // [slots, 2*heads + d]
-    float *vstat = nullptr;              // aggregate-first: [V, 2] per-vseg (max, sum)
+    float *vstat = nullptr;              // aggregate-first: [V, 2] per-vseg (max, sum), fused order
     float *vatt = nullptr;               // [V, heads] destination attention term per vseg
     float *vscale = nullptr;             // aggregate-first: [V] softmax scale per vseg
     int relu = 0;
@@ -229,15 +231,16 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
                                float *out, int accumulate, int relu, hipStream_t s);
 
 // Softmax per destination finished from the per-segment (max, sum) in vstat
-// and the segments' transformed rows summed: out_v = sum_i exp(m_i - M_v) / Z_v
-// * T_i; saved[v] = (M_v, Z_v) when saved is not NULL.
+// (fused order) and the segments' transformed rows summed: out_v = sum_i
+// exp(m_i - M_v) / Z_v * T_i; saved[v] = (M_v, Z_v) when saved is not NULL.
+// scale [V]: scratch (the weights of destinations with many segments).
 rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
-                                  float *out, float *saved, hipStream_t s);
+                                  float *out, float *saved, float *scale, hipStream_t s);
 
 // Fused aggregate-first gather + segment sum + transform: per virtual segment
 // T[vs] = S_vs W_r with S_vs the segment's mean of h_u (softmax == 0) or its
 // exp-weighted sum relative to the segment's own logit maximum (softmax == 1,
-// one head; (max, sum) to vstat[vs]).
+// one head; (max, sum) to vstat at the fused position).
 struct FusedArgs {
     const rgnn_graph *g = nullptr;
     const float *h = nullptr;     // [N, d_in]
@@ -248,7 +251,7 @@ struct FusedArgs {
     int d_in = 64, d_out = 64;
     int softmax = 0;
     float *T = nullptr;           // [V, d_out]
-    float *vstat = nullptr;       // [V, 2] (softmax)
+    float *vstat = nullptr;       // [V, 2] (softmax), indexed by fused position
     // S given (softmax == 0): write the segment means S_vs = (1/c) sum h_u
     // themselves, at the segment's by-relation position [V, d_in], no transform
     float *S = nullptr;
