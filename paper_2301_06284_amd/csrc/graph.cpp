@@ -240,19 +240,14 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.big_split.clear();
         for (int64_t i = 0; i < g->n_split; ++i)
             if (x.split_slotptr[i + 1] - x.split_slotptr[i] > kBigRange) x.big_split.push_back((int32_t)i);
-        // destinations with many segments: those with at most kHugeRange
-        // first, then the larger ones (each part in id order)
+        // destinations with many segments, largest first (ties in id order):
+        // their reductions take whole workgroups at the front of the grid
         x.big_vdst.clear();
-        for (int64_t u = 0; u < N; ++u) {
-            const int32_t n = x.dst_vsegptr[u + 1] - x.dst_vsegptr[u];
-            if (n > kBigRange && n <= kHugeRange) x.big_vdst.push_back((int32_t)u);
-        }
-        g->n_huge_vdst = 0;
         for (int64_t u = 0; u < N; ++u)
-            if (x.dst_vsegptr[u + 1] - x.dst_vsegptr[u] > kHugeRange) {
-                x.big_vdst.push_back((int32_t)u);
-                ++g->n_huge_vdst;
-            }
+            if (x.dst_vsegptr[u + 1] - x.dst_vsegptr[u] > kBigRange) x.big_vdst.push_back((int32_t)u);
+        std::stable_sort(x.big_vdst.begin(), x.big_vdst.end(), [&](int32_t a, int32_t b) {
+            return x.dst_vsegptr[a + 1] - x.dst_vsegptr[a] > x.dst_vsegptr[b + 1] - x.dst_vsegptr[b];
+        });
         g->n_big_split = (int64_t)x.big_split.size();
         g->n_big_vdst = (int64_t)x.big_vdst.size();
 

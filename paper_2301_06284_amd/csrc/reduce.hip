@@ -88,51 +88,17 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
     for (int i = b + (int)threadIdx.x; i < e; i += 256) vscale[i] = __expf(vstat[(size_t)fpos[i] * 2] - M) * Zi;
 }
 
-// out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
-// ReLU).
-template <int D>
-__global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
-                                                          const float *T, const float *scale,
-                                                          float *out, int accumulate, int relu)
-{
-    constexpr int G = D / 4, GPB = 256 / G;
-    const int gl = threadIdx.x % G;
-    const int64_t v = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
-    if (v >= N) return;
-    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    if (e - b > kBigRange) return;
-    float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    // rows in batches of four (all in flight together), summed in segment order
-    for (int i0 = b; i0 < e; i0 += 4) {
-        float4 t[4];
-        float sc[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            if (i0 + u < e) {
-                t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
-                sc[u] = scale ? scale[i0 + u] : 1.f;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (i0 + u < e) acc = scale ? fma4(t[u], sc[u], acc) : add4(acc, t[u]);
-    }
-    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
-}
-
-// One workgroup of NTH threads per destination with many segments: every
-// group of D/4 lanes sums a strided subset of the rows (U in flight), the
-// group sums are then added in group order.
+// Destinations with more than kBigRange segments get one workgroup of NTH
+// threads each, at the front of the grid (largest first, so they start
+// early and overlap the rest): every group of D/4 lanes sums a strided subset
+// of the rows (U in flight), the group sums are then added in group order.
 template <int D, int NTH, int U>
-__global__ __launch_bounds__(NTH) void vseg_reduce_big_kernel(const int32_t *big_vdst,
-                                                              const int32_t *dst_vsegptr,
-                                                              const float *T, const float *scale,
-                                                              float *out, int accumulate, int relu)
+__device__ __forceinline__ void vseg_reduce_big(int v, const int32_t *dst_vsegptr, const float *T,
+                                                const float *scale, float *out, int accumulate, int relu)
 {
     constexpr int G = D / 4, NG = NTH / G;
     __shared__ float4 part[NG * G];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int v = big_vdst[blockIdx.x];
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int i0 = b + gi; i0 < e; i0 += U * NG) {
@@ -159,85 +125,47 @@ __global__ __launch_bounds__(NTH) void vseg_reduce_big_kernel(const int32_t *big
     }
 }
 
-// ---------------------------------------------------------------- softmax reduction
-// Softmax per destination finished and summed in one pass: per destination v
-// with segments i (each with its own logit maximum m_i, sum s_i and
-// exp-weighted transformed row T_i relative to m_i; (m_i, s_i) stored at the
-// segment's fused position fpos[i]):
-//   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
-// and saved[v] = (M, Z) ((0, 0) without in-edges).  A group of D/4 lanes per
-// destination; the statistics are taken over the group's lanes (fixed
-// butterfly), the rows summed in segment order.
+// out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
+// ReLU).  Blocks [0, nbig) take the destinations of big_vdst; the others a
+// group of D/4 lanes per destination.
 template <int D>
-__global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const int32_t *dst_vsegptr,
-                                                             const int32_t *fpos, const float *vstat,
-                                                             const float *T, float *out, float *saved)
+__global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbig, const int32_t *big_vdst,
+                                                          const int32_t *dst_vsegptr,
+                                                          const float *T, const float *scale,
+                                                          float *out, int accumulate, int relu)
 {
+    if ((int64_t)blockIdx.x < nbig) {
+        vseg_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, T, scale, out, accumulate, relu);
+        return;
+    }
     constexpr int G = D / 4, GPB = 256 / G;
-    constexpr int NE = (kBigRange + G - 1) / G;   // statistics entries per lane
     const int gl = threadIdx.x % G;
-    const int64_t v = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
+    const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
     if (v >= N) return;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     if (e - b > kBigRange) return;
-    // rows in batches of four, two batches in flight; the first goes out before
-    // the statistics are gathered (the rows do not depend on them)
-    float4 ta[4], tb[4];
-    auto load = [&](float4 (&t)[4], int i0) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (i0 + u < e) t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
-    };
-    load(ta, b);
-    // lane gl holds the statistics of segments b + gl + j G
-    float mi[NE], si[NE];
-#pragma unroll
-    for (int j = 0; j < NE; ++j) {
-        const int i = b + gl + j * G;
-        const float2 st = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2)
-                                : make_float2(-INFINITY, 0.f);
-        mi[j] = st.x;
-        si[j] = st.y;
-    }
-    float M = mi[0];
-#pragma unroll
-    for (int j = 1; j < NE; ++j) M = fmaxf(M, mi[j]);
-    M = gmax<G>(M);
-    float z = 0.f;
-#pragma unroll
-    for (int j = 0; j < NE; ++j) z += si[j] > 0.f ? si[j] * __expf(mi[j] - M) : 0.f;
-    const float Z = gsum<G>(z);
-    if (saved && gl == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(b < e ? M : 0.f, Z);
-    const float inv = Z > 0.f ? 1.f / Z : 0.f;
-    float w[NE];
-#pragma unroll
-    for (int j = 0; j < NE; ++j) w[j] = si[j] > 0.f ? __expf(mi[j] - M) * inv : 0.f;
-    // summed in segment order; segment b + r takes its weight from lane r % G
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    auto consume = [&](const float4 (&t)[4], int i0) {
+    float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    // rows in batches of four (all in flight together), summed in segment order
+    for (int i0 = b; i0 < e; i0 += 4) {
+        float4 t[4];
+        float sc[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int r = i0 + u - b, jr = r / G;
-            float x = w[0];
-#pragma unroll
-            for (int j = 1; j < NE; ++j) x = jr == j ? w[j] : x;
-            const float wu = __shfl(x, r % G, G);
-            if (i0 + u < e) acc = fma4(t[u], wu, acc);
+            if (i0 + u < e) {
+                t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
+                sc[u] = scale ? scale[i0 + u] : 1.f;
+            }
         }
-    };
-    for (int i0 = b; i0 < e; i0 += 8) {
-        const bool more = i0 + 4 < e;
-        if (more) load(tb, i0 + 4);
-        consume(ta, i0);
-        if (!more) break;
-        if (i0 + 8 < e) load(ta, i0 + 8);
-        consume(tb, i0 + 4);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < e) acc = scale ? fma4(t[u], sc[u], acc) : add4(acc, t[u]);
     }
-    st4(out + (size_t)v * D + gl * 4, acc);
+    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
 
-// The same for destinations with more than kBigRange segments, one workgroup
-// of NTH threads each: every thread folds its strided share of the (max, sum)
+// ---------------------------------------------------------------- softmax reduction
+// Destinations with more than kBigRange segments: one workgroup of NTH threads
+// each, at the front of the grid (largest first); every thread folds its strided share of the (max, sum)
 // pairs into one online pair (four loads in flight), the maximum and the
 // denominator follow by workgroup reductions; every thread then writes the
 // weights exp(m_i - M) / Z of its share to scale[i] (segment order, so the row
@@ -245,18 +173,15 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, const in
 // D/4 lanes sums a strided subset of the rows (U in flight) and the group sums
 // are added in group order.
 template <int D, int NTH, int U>
-__global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *big_vdst,
-                                                                 const int32_t *dst_vsegptr,
-                                                                 const int32_t *fpos, const float *vstat,
-                                                                 const float *T, float *out, float *saved,
-                                                                 float *scale)
+__device__ __forceinline__ void softmax_reduce_big(int v, const int32_t *dst_vsegptr, const int32_t *fpos,
+                                                   const float *vstat, const float *T, float *out,
+                                                   float *saved, float *scale)
 {
     constexpr int G = D / 4, NG = NTH / G, NWV = NTH / 64;
     __shared__ float red[NWV];
     __shared__ float4 part[NG * G];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int gl = tid % G, gi = tid / G;
-    const int v = big_vdst[blockIdx.x];
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     float ml = -INFINITY, zl = 0.f;
     for (int i0 = b + tid; i0 < e; i0 += 4 * NTH) {
@@ -328,6 +253,89 @@ __global__ __launch_bounds__(NTH) void softmax_reduce_big_kernel(const int32_t *
         for (int j = 0; j < NG; ++j) tot = add4(tot, part[j * G + gl]);
         st4(out + (size_t)v * D + gl * 4, tot);
     }
+}
+
+// Softmax per destination finished and summed in one pass: per destination v
+// with segments i (each with its own logit maximum m_i, sum s_i and
+// exp-weighted transformed row T_i relative to m_i; (m_i, s_i) stored at the
+// segment's fused position fpos[i]):
+//   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
+// and saved[v] = (M, Z) ((0, 0) without in-edges).  Blocks [0, nbig) take the
+// destinations of big_vdst; the others a group of D/4 lanes per destination,
+// the statistics taken over the group's lanes (fixed butterfly), the rows
+// summed in segment order.
+template <int D>
+__global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t nbig, const int32_t *big_vdst,
+                                                             const int32_t *dst_vsegptr,
+                                                             const int32_t *fpos, const float *vstat,
+                                                             const float *T, float *out, float *saved,
+                                                             float *scale)
+{
+    if ((int64_t)blockIdx.x < nbig) {
+        softmax_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, fpos, vstat, T, out, saved, scale);
+        return;
+    }
+    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int NE = (kBigRange + G - 1) / G;   // statistics entries per lane
+    const int gl = threadIdx.x % G;
+    const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
+    if (v >= N) return;
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
+    if (e - b > kBigRange) return;
+    // rows in batches of four, two batches in flight; the first goes out before
+    // the statistics are gathered (the rows do not depend on them)
+    float4 ta[4], tb[4];
+    auto load = [&](float4 (&t)[4], int i0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < e) t[u] = ld4(T + (size_t)(i0 + u) * D + gl * 4);
+    };
+    load(ta, b);
+    // lane gl holds the statistics of segments b + gl + j G
+    float mi[NE], si[NE];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) {
+        const int i = b + gl + j * G;
+        const float2 st = i < e ? *reinterpret_cast<const float2 *>(vstat + (size_t)fpos[i] * 2)
+                                : make_float2(-INFINITY, 0.f);
+        mi[j] = st.x;
+        si[j] = st.y;
+    }
+    float M = mi[0];
+#pragma unroll
+    for (int j = 1; j < NE; ++j) M = fmaxf(M, mi[j]);
+    M = gmax<G>(M);
+    float z = 0.f;
+#pragma unroll
+    for (int j = 0; j < NE; ++j) z += si[j] > 0.f ? si[j] * __expf(mi[j] - M) : 0.f;
+    const float Z = gsum<G>(z);
+    if (saved && gl == 0) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(b < e ? M : 0.f, Z);
+    const float inv = Z > 0.f ? 1.f / Z : 0.f;
+    float w[NE];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) w[j] = si[j] > 0.f ? __expf(mi[j] - M) * inv : 0.f;
+    // summed in segment order; segment b + r takes its weight from lane r % G
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto consume = [&](const float4 (&t)[4], int i0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int r = i0 + u - b, jr = r / G;
+            float x = w[0];
+#pragma unroll
+            for (int j = 1; j < NE; ++j) x = jr == j ? w[j] : x;
+            const float wu = __shfl(x, r % G, G);
+            if (i0 + u < e) acc = fma4(t[u], wu, acc);
+        }
+    };
+    for (int i0 = b; i0 < e; i0 += 8) {
+        const bool more = i0 + 4 < e;
+        if (more) load(tb, i0 + 4);
+        consume(ta, i0);
+        if (!more) break;
+        if (i0 + 8 < e) load(ta, i0 + 8);
+        consume(tb, i0 + 4);
+    }
+    st4(out + (size_t)v * D + gl * 4, acc);
 }
 
 // ---------------------------------------------------------------- merges
@@ -561,44 +569,19 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
 {
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 32, 64 or 128");
+    const int64_t nbig = g->n_big_vdst;
+    const unsigned nb = (unsigned)nbig + blocks_for(g->N, 256 / (d / 4));
     {
         LaunchScope ls("vseg_reduce", s);
-        const unsigned nb = blocks_for(g->N, 256 / (d / 4));
-        if (d == 32)
-            hipLaunchKernelGGL((vseg_reduce_kernel<32>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
-        else if (d == 64)
-            hipLaunchKernelGGL((vseg_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
-        else
-            hipLaunchKernelGGL((vseg_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, T, scale, out, accumulate, relu);
+#define VR(D) hipLaunchKernelGGL((vseg_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
+                                 g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu)
+        if (d == 32) VR(32);
+        else if (d == 64) VR(64);
+        else VR(128);
+#undef VR
     }
     hipError_t e = last();
-    if (e != hipSuccess) return hip_fail(e, "vseg_reduce launch");
-    if (g->n_big_vdst == 0) return RGNN_OK;
-    const int64_t nmid = g->n_big_vdst - g->n_huge_vdst, nhuge = g->n_huge_vdst;
-    const int32_t *huge = g->dev.big_vdst + nmid;
-    {
-#define VRB(D, NTH, L, NB) hipLaunchKernelGGL((vseg_reduce_big_kernel<D, NTH, NTH == 1024 ? 16 : 4>), \
-                                              dim3((unsigned)(NB)), dim3(NTH), \
-                                              0, s, L, g->dev.dst_vsegptr, T, scale, out, accumulate, relu)
-        if (nmid) {
-            LaunchScope ls("vseg_reduce_big", s);
-            if (d == 32) VRB(32, 256, g->dev.big_vdst, nmid);
-            else if (d == 64) VRB(64, 256, g->dev.big_vdst, nmid);
-            else VRB(128, 256, g->dev.big_vdst, nmid);
-        }
-        if (nhuge) {
-            LaunchScope ls("vseg_reduce_huge", s);
-            if (d == 32) VRB(32, 1024, huge, nhuge);
-            else if (d == 64) VRB(64, 1024, huge, nhuge);
-            else VRB(128, 1024, huge, nhuge);
-        }
-#undef VRB
-    }
-    e = last();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce_big launch");
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "vseg_reduce launch");
 }
 
 rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
@@ -606,43 +589,21 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
 {
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 32, 64 or 128");
+    if (g->n_big_vdst && !scale) return fail(RGNN_EINVAL, "softmax reduce needs its scale scratch");
+    const int64_t nbig = g->n_big_vdst;
+    const unsigned nb = (unsigned)nbig + blocks_for(g->N, 256 / (d / 4));
     {
         LaunchScope ls("softmax_reduce", s);
-        const unsigned nb = blocks_for(g->N, 256 / (d / 4));
-        if (d == 32)
-            hipLaunchKernelGGL((softmax_reduce_kernel<32>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
-        else if (d == 64)
-            hipLaunchKernelGGL((softmax_reduce_kernel<64>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
-        else
-            hipLaunchKernelGGL((softmax_reduce_kernel<128>), dim3(nb), dim3(256), 0, s, g->N,
-                               g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved);
+#define SR(D) hipLaunchKernelGGL((softmax_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
+                                 g->dev.big_vdst, g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, \
+                                 saved, scale)
+        if (d == 32) SR(32);
+        else if (d == 64) SR(64);
+        else SR(128);
+#undef SR
     }
     hipError_t e = last();
-    if (e != hipSuccess) return hip_fail(e, "softmax_reduce launch");
-    if (g->n_big_vdst == 0) return RGNN_OK;
-    const int64_t nmid = g->n_big_vdst - g->n_huge_vdst, nhuge = g->n_huge_vdst;
-    const int32_t *huge = g->dev.big_vdst + nmid;
-    {
-#define SRB(D, NTH, L, NB) hipLaunchKernelGGL((softmax_reduce_big_kernel<D, NTH, NTH == 1024 ? 16 : 4>), dim3((unsigned)(NB)), \
-                                              dim3(NTH), 0, s, L, g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, saved, scale)
-        if (nmid) {
-            LaunchScope ls("softmax_reduce_big", s);
-            if (d == 32) SRB(32, 256, g->dev.big_vdst, nmid);
-            else if (d == 64) SRB(64, 256, g->dev.big_vdst, nmid);
-            else SRB(128, 256, g->dev.big_vdst, nmid);
-        }
-        if (nhuge) {
-            LaunchScope ls("softmax_reduce_huge", s);
-            if (d == 32) SRB(32, 1024, huge, nhuge);
-            else if (d == 64) SRB(64, 1024, huge, nhuge);
-            else SRB(128, 1024, huge, nhuge);
-        }
-#undef SRB
-    }
-    e = last();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "softmax_reduce_big launch");
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "softmax_reduce launch");
 }
 
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s)

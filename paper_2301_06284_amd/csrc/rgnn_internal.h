@@ -25,9 +25,6 @@ constexpr int kFusedTileEdges = 4096;
 // Reductions over more records than this (partials of a split destination,
 // segments of one destination) get a whole workgroup instead of one group.
 constexpr int kBigRange = 32;
-// destinations with more than this many virtual segments are reduced by
-// 1024-thread workgroups, smaller "big" ones by 256-thread workgroups
-constexpr int kHugeRange = 512;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
@@ -56,8 +53,8 @@ struct HostIndex {
     std::vector<Item> items;
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
     std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
-    std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments; the
-                                      // last n_huge_vdst have > kHugeRange
+    std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments,
+                                      // largest first
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
     std::vector<int32_t> big_seg;      // (dst, rel) segments with > kBigRange virtual segments
     std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
@@ -122,7 +119,7 @@ struct rgnn_graph {
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
-    int64_t n_big_split = 0, n_big_vdst = 0, n_huge_vdst = 0, n_big_seg = 0;
+    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;

@@ -216,9 +216,9 @@ def test_rgat_per_relation_softmax_big_segment():
 
 @pytest.mark.parametrize("R", [1, 3])
 def test_huge_hub(R):
-    """A destination with more than 512 virtual segments (the 1024-thread
-    reductions) beside ones with 33..512 (the 256-thread reductions), through
-    every plan of RGCN and RGAT."""
+    """Destinations with hundreds to thousands of virtual segments (the
+    workgroup-per-destination reductions at the front of the reduction grid)
+    beside ordinary ones, through every plan of RGCN and RGAT."""
     g = graph("hub", seed=24, N=200, E=70000, R=R)
     t = workloads.tiny_tensors(24, g, 64, 64, att_var=1.0)
     print(f"huge hub R={R}", flush=True)
