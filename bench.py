@@ -140,9 +140,12 @@ def rgat_af_model(info, d):
         # matrix cores plus the per-edge dot and weighted accumulation.
         "rgat_af_fused": dict(bytes=E * (4 + 4 * d) + V * (16 + 4 + 4 * d + 8) + R * (4 * d * d + 4 * d),
                               flops=2.0 * V * d * d + E * 4.0 * d),
-        # all destinations (the kernel and its one-workgroup-per-hub sibling):
+        # all destinations (groups of lanes, and whole workgroups for hubs):
         # per segment T row and scale read, per destination offsets and output row
         "vseg_reduce": dict(bytes=V * (4 * d + 4) + N * (4 + 4 * d), flops=2.0 * V * d),
+        # per segment T row, fused position and (max, sum); per destination
+        # offsets, output row and saved (max, sum)
+        "softmax_reduce": dict(bytes=V * (4 * d + 4 + 8) + N * (4 + 4 * d + 8), flops=2.0 * V * d),
         # per destination its h row (consecutive segments share it); per
         # segment its destination, relation and term written; W_r w_dst per relation
         "seg_attn": dict(bytes=N * 4 * d + V * 12 + R * 4 * d, flops=2.0 * V * d),
