@@ -373,6 +373,17 @@ def main():
         layers["rgat_bwd_am_like_880k"] = {"edges_per_s": E / (msb * 1e-3), "ms": msb,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in kb.items()}}
         del wsb
+        # four heads: one masked one-head pass per head
+        saved4 = torch.empty(inf["num_nodes"], 4, 2, device=c.dev)
+        ws4 = c.ws(rgnn.LAYER_RGAT, d, d, 4)
+        rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, saved4, ws4, d, d, 4)
+        del ws4
+        wsb4 = c.ws(rgnn.LAYER_RGAT_BACKWARD, d, d, 4)
+        fnb4 = lambda: rgnn.rgat_backward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], saved4,
+                                          c.T["grad_out"], gh, gW, gs, gt, wsb4, d, d, 4)
+        msb4 = time_steps(torch, fnb4, K, W)
+        layers["rgat_bwd_am_like_880k_4heads"] = {"edges_per_s": E / (msb4 * 1e-3), "ms": msb4}
+        del wsb4, saved4
         # RGCN forward (with self-loop) and backward on the same graph
         log("workload 5: RGCN forward and backward")
         pr = rgnn.select_plan(c.G, rgnn.LAYER_RGCN, d, d, 1)[0]

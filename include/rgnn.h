@@ -227,8 +227,13 @@ rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, 
 
 /* RGAT backward (Section "Backward Propagation") for the forward above with
  * softmax per destination: given grad_out = dL/dout [N, d_out] and the
- * forward's `saved`, writes dL/dh [N, d_in], dL/dW [R, d_in, d_out],
- * dL/dw_src and dL/dw_dst [R, d_out].  heads == 1. */
+ * forward's `saved` [N, heads, 2], writes dL/dh [N, d_in], dL/dW [R, d_in, d_out],
+ * dL/dw_src and dL/dw_dst [R, d_out].  d_in = d_out = 64, heads in {1, 2, 4}.
+ * Several heads run as one pass per head over the weights, attention vectors
+ * and grad_out with the other heads' columns zeroed (each head's logits,
+ * softmax and messages read only its own columns, so the per-head gradients
+ * add up to the exact ones); the cost grows with the heads.  Workspace:
+ * rgnn_workspace_size(RGNN_LAYER_RGAT_BACKWARD, d_in, d_out, heads). */
 rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, const float *W,
                           const float *w_src, const float *w_dst, int32_t d_in, int32_t d_out,
                           int32_t heads, float neg_slope, const float *saved,

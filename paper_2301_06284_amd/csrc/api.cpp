@@ -161,6 +161,39 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     return c.off;
 }
 
+// Multi-head RGAT backward as a sum of one-head passes.  Head k reads only
+// the columns C_k of W_r, w_src[r], w_dst[r] and of the loss weight: with
+// those of every other head set to zero, the one-head layer computes head k's
+// logits, softmax and messages exactly, and its loss is head k's share of L.
+// So the gradients of L are the sums over k of the one-head gradients of the
+// masked problem (the masked entries receive exact zeros: their messages are
+// zero and their loss and attention weights are zero).
+struct BwdHeadsWs { float *Wm, *wsm, *wdm, *Gm, *sv, *dh, *dW, *dws, *dwd; void *inner; size_t inner_bytes; };
+size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, void *base, BwdHeadsWs *w)
+{
+    size_t inner = 0;
+    rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, nullptr, nullptr,
+                       nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &inner);
+    Carver c(base);
+    BwdHeadsWs x{};
+    x.inner = c.take<char>(inner);
+    x.inner_bytes = inner;
+    if (H > 1) {
+        const size_t R = (size_t)g->R, N = (size_t)g->N;
+        x.Wm = c.take<float>(R * d_in * d_out);
+        x.wsm = c.take<float>(R * d_out);
+        x.wdm = c.take<float>(R * d_out);
+        x.Gm = c.take<float>(N * d_out);
+        x.sv = c.take<float>(N * 2);
+        x.dh = c.take<float>(N * d_in);
+        x.dW = c.take<float>(R * d_in * d_out);
+        x.dws = c.take<float>(R * d_out);
+        x.dwd = c.take<float>(R * d_out);
+    }
+    if (w) *w = x;
+    return c.off;
+}
+
 struct HgtWs { float *KV, *Q, *QP, *Wqp, *agg, *partial; };
 size_t hgt_layout(const rgnn_graph *g, int d, int H, void *base, HgtWs *w)
 {
@@ -296,13 +329,9 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
     case RGNN_LAYER_HGT:
         *bytes = hgt_layout(g, d_out, heads, nullptr, nullptr);
         return RGNN_OK;
-    case RGNN_LAYER_RGAT_BACKWARD: {
-        size_t need = 0;
-        rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, nullptr,
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
-        *bytes = need;
+    case RGNN_LAYER_RGAT_BACKWARD:
+        *bytes = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
         return RGNN_OK;
-    }
     case RGNN_LAYER_HGT_BACKWARD: {
         size_t need = 0;
         hgt_backward_impl(g, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, d_out,
@@ -547,12 +576,42 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     if (!h || !W || !w_src || !w_dst || !saved || !grad_out || !grad_h || !grad_W ||
         !grad_w_src || !grad_w_dst)
         return fail(RGNN_EINVAL, "NULL tensor pointer");
-    if (heads != 1) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports heads == 1");
     if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d = 64");
+    if (heads != 1 && heads != 2 && heads != 4)
+        return fail(RGNN_EUNSUPPORTED, "RGAT backward heads must be 1, 2 or 4");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
-    return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
-                              grad_h, grad_W, grad_w_src, grad_w_dst, ws, ws_bytes,
-                              (hipStream_t)stream, nullptr);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t need = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
+    if (!ws || ws_bytes < need)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    BwdHeadsWs w;
+    rgat_bwd_heads_layout(g, d_in, d_out, heads, ws, &w);
+    if (heads == 1)
+        return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
+                                  grad_h, grad_W, grad_w_src, grad_w_dst, w.inner, w.inner_bytes, s,
+                                  nullptr);
+    const int64_t R = g->R, N = g->N, dh = d_out / heads;
+    for (int k = 0; k < heads; ++k) {
+        const int c0 = (int)(k * dh), c1 = (int)((k + 1) * dh);
+        if ((st = launch_mask_cols(W, w.Wm, R * d_in, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_mask_cols(grad_out, w.Gm, N, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_head_stats(saved, w.sv, N, heads, k, s)) != RGNN_OK) return st;
+        // head 0 writes the outputs, the others add to them
+        float *oh = k ? w.dh : grad_h, *oW = k ? w.dW : grad_W;
+        float *os = k ? w.dws : grad_w_src, *od = k ? w.dwd : grad_w_dst;
+        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, w.sv, w.Gm,
+                                     oh, oW, os, od, w.inner, w.inner_bytes, s, nullptr)) != RGNN_OK)
+            return st;
+        if (k) {
+            if ((st = launch_add(grad_h, grad_h, w.dh, N * d_in, s)) != RGNN_OK) return st;
+            if ((st = launch_add(grad_W, grad_W, w.dW, R * d_in * d_out, s)) != RGNN_OK) return st;
+            if ((st = launch_add(grad_w_src, grad_w_src, w.dws, R * d_out, s)) != RGNN_OK) return st;
+            if ((st = launch_add(grad_w_dst, grad_w_dst, w.dwd, R * d_out, s)) != RGNN_OK) return st;
+        }
+    }
+    return RGNN_OK;
 }
 
 extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk,

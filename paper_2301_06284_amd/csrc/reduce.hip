@@ -459,6 +459,23 @@ __global__ void add_kernel(float *out, const float *a, const float *b, int64_t n
     if (i < n) out[i] = a[i] + b[i];
 }
 
+// out[i, j] = in[i, j] for columns c0 <= j < c1, else 0 ([rows, d], row-major)
+__global__ void mask_cols_kernel(const float *in, float *out, int64_t n, int d, int c0, int c1)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int j = (int)(i % d);
+    out[i] = (j >= c0 && j < c1) ? in[i] : 0.f;
+}
+
+// out[v] = saved[v, k] for the (max, sum) pairs of one head ([N, H, 2] -> [N, 2])
+__global__ void head_stats_kernel(const float *saved, float *out, int64_t N, int H, int k)
+{
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (v >= N) return;
+    *reinterpret_cast<float2 *>(out + v * 2) = *reinterpret_cast<const float2 *>(saved + (v * H + k) * 2);
+}
+
 // Reordered attention vectors (linear operator reordering): for every row
 // (r, i) of W_r, out[r, k, i] = W_r[i, k-cols] . v[r, k-cols] for one or two
 // vectors v.  A group of DO/4 lanes reads the W row once (one float4 per
@@ -631,6 +648,25 @@ rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hi
     hipLaunchKernelGGL(add_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, out, a, b, n);
     hipError_t e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "add launch");
+}
+
+rgnn_status launch_mask_cols(const float *in, float *out, int64_t rows, int d, int c0, int c1, hipStream_t s)
+{
+    const int64_t n = rows * d;
+    if (n == 0) return RGNN_OK;
+    LaunchScope ls("mask_cols", s);
+    hipLaunchKernelGGL(mask_cols_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, in, out, n, d, c0, c1);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "mask_cols launch");
+}
+
+rgnn_status launch_head_stats(const float *saved, float *out, int64_t N, int H, int k, hipStream_t s)
+{
+    if (N == 0) return RGNN_OK;
+    LaunchScope ls("head_stats", s);
+    hipLaunchKernelGGL(head_stats_kernel, dim3(blocks_for(N, 256)), dim3(256), 0, s, saved, out, N, H, k);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "head_stats launch");
 }
 
 rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int heads,

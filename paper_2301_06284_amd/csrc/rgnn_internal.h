@@ -138,6 +138,10 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
 void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vector<Tile> &out);
 int bwd_outer_rows();
 rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s);
+// out [rows, d] = in with the columns outside [c0, c1) set to 0
+rgnn_status launch_mask_cols(const float *in, float *out, int64_t rows, int d, int c0, int c1, hipStream_t s);
+// out [N, 2] = saved [N, H, 2] of head k
+rgnn_status launch_head_stats(const float *saved, float *out, int64_t N, int H, int k, hipStream_t s);
 
 // ---- profiling (api.cpp) ----
 struct LaunchScope {   // records a hipEvent pair around one kernel launch when profiling

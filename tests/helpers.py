@@ -105,17 +105,17 @@ class Runner:
         torch.cuda.synchronize()
         return out.cpu().numpy()
 
-    def rgat_backward(self, slope=0.2):
+    def rgat_backward(self, slope=0.2, heads=1):
         T, torch, rgnn = self.T, self.torch, self.rgnn
         d = T["W"].shape[1]
         R = T["W"].shape[0]
-        _, saved = self.rgat(heads=1, slope=slope, want_saved=True)
+        _, saved = self.rgat(heads=heads, slope=slope, want_saved=True)
         gh = torch.full((self.g["N"], d), float("nan"), device=self.dev)
         gW = torch.full((R, d, d), float("nan"), device=self.dev)
         gs = torch.full((R, d), float("nan"), device=self.dev)
         gt = torch.full((R, d), float("nan"), device=self.dev)
         rgnn.rgat_backward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], saved, T["grad_out"],
-                           gh, gW, gs, gt, self.ws(3, d, d), d, d, 1, slope)
+                           gh, gW, gs, gt, self.ws(3, d, d, heads), d, d, heads, slope)
         torch.cuda.synchronize()
         return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
 
