@@ -53,7 +53,7 @@ def _load():
                                             vp, vp, vp, vp, vp, vp, vp, f64, i32, i32, i64, vp,
                                             vp]
         _lib.oracle_rgat_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
-                                              vp, vp, f64, vp, vp, vp, vp, vp, vp, vp]
+                                              vp, vp, f64, i32, vp, vp, vp, vp, vp, vp, vp]
         _lib.oracle_rgcn_backward.argtypes = [i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp,
                                               i32, vp, vp, vp, vp, vp, vp]
         _lib.oracle_hgt_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
@@ -157,10 +157,12 @@ def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, heads, att_scale=None,
     return out
 
 
-def rgat_backward(g, h, W, w_src, w_dst, grad_out, heads=1, neg_slope=0.2,
+def rgat_backward(g, h, W, w_src, w_dst, grad_out, heads=1, neg_slope=0.2, scope=0,
                   node_mask=None, rel_mask=None):
-    """Gradients of L = sum(out * grad_out) of the RGAT layer (scope 0).
-    Returns (dh, dW, dw_src, dw_dst); entries outside the masks are zero."""
+    """Gradients of L = sum(out * grad_out) of the RGAT layer with the softmax
+    over each destination's in-edges (scope 0) or over its in-edges of one
+    relation (scope 1).  Returns (dh, dW, dw_src, dw_dst); entries outside the
+    masks are zero."""
     h, W, w_src, w_dst, G = map(_f32, (h, W, w_src, w_dst, grad_out))
     src, dst, rel = _i32(g["src"]), _i32(g["dst"]), _i32(g["rel"])
     N, R = g["N"], g["R"]
@@ -171,7 +173,7 @@ def rgat_backward(g, h, W, w_src, w_dst, grad_out, heads=1, neg_slope=0.2,
     dws = np.zeros((R, d_out)); dwd = np.zeros((R, d_out))
     rc = _load().oracle_rgat_backward(N, g["E"], R, d_in, d_out, heads, _p(src), _p(dst),
                                       _p(rel), _p(h), _p(W), _p(w_src), _p(w_dst),
-                                      float(neg_slope), _p(G), _p(nm), _p(rm), _p(dh), _p(dW),
+                                      float(neg_slope), int(scope), _p(G), _p(nm), _p(rm), _p(dh), _p(dW),
                                       _p(dws), _p(dwd))
     _check(rc, "rgat_backward")
     return dh, dW, dws, dwd

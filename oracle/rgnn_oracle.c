@@ -435,11 +435,12 @@ int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
 
 /* ------------------------------------------------------------------------ */
 /* RGAT backward for the loss L = sum(out * G) (G = grad_out), softmax over all
- * in-edges of the destination (scope 0).  With the forward's notation and
- * Y_e,k = dL/dy_e,k:
+ * in-edges of the destination (scope 0) or over its in-edges of one relation
+ * (scope 1; the groups below are then the (v, r) segments).  With the
+ * forward's notation and Y_e,k = dL/dy_e,k:
  *   dalpha_e,k = sum_{j in k} G_v[j] m_e[j]
- *   s_v,k      = sum_{e in in(v)} alpha_e,k dalpha_e,k
- *   Y_e,k      = alpha_e,k (dalpha_e,k - s_v,k) * (1 if y_e,k > 0 else slope)
+ *   s_g,k      = sum_{e in group g} alpha_e,k dalpha_e,k     (g: e's group)
+ *   Y_e,k      = alpha_e,k (dalpha_e,k - s_g,k) * (1 if y_e,k > 0 else slope)
  *   dm_e[j]    = alpha_e,k G_v[j] + Y_e,k w_src[r][j]     (message and atts paths)
  *   dt_e[j]    = Y_e,k w_dst[r][j]                          (attt path)
  *   dW_r      += h_u^T dm_e + h_v^T dt_e
@@ -453,8 +454,9 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
                          int32_t heads, const int32_t *src, const int32_t *dst,
                          const int32_t *rel, const float *h, const float *W,
                          const float *w_src, const float *w_dst, double neg_slope,
-                         const float *G, const uint8_t *node_mask, const uint8_t *rel_mask,
-                         double *dh, double *dW, double *dw_src, double *dw_dst)
+                         int32_t scope, const float *G, const uint8_t *node_mask,
+                         const uint8_t *rel_mask, double *dh, double *dW, double *dw_src,
+                         double *dw_dst)
 {
     if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_in > 512 || d_out <= 0 ||
         heads <= 0 || d_out % heads)
@@ -483,9 +485,13 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
     int64_t cap = 0;
     double *xv = (double *)malloc((size_t)d_in * sizeof(double));
     double *x = (double *)malloc((size_t)d_in * sizeof(double));
-    double *mx = (double *)malloc((size_t)H * sizeof(double));
-    double *sm = (double *)malloc((size_t)H * sizeof(double));
-    double *sv = (double *)malloc((size_t)H * sizeof(double));
+    /* softmax statistics and s per normalisation group and head: one group per
+     * destination (scope 0) or per (destination, relation) segment (scope 1),
+     * indexed by the relation */
+    const int NGRP = scope ? R : 1;
+    double *mx = (double *)malloc((size_t)NGRP * H * sizeof(double));
+    double *sm = (double *)malloc((size_t)NGRP * H * sizeof(double));
+    double *sv = (double *)malloc((size_t)NGRP * H * sizeof(double));
     if (!xv || !x || !mx || !sm || !sv) err = 1;
     for (int64_t v = 0; v < N && !err; ++v) {
         if (!need[v]) continue;
@@ -522,20 +528,22 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
                 al[q * H + k] = y > 0.0 ? y : neg_slope * y;
             }
         }
-        for (int k = 0; k < H; ++k) { mx[k] = -INFINITY; sm[k] = 0.0; sv[k] = 0.0; }
+#define GRP(q) ((scope ? rel[a.eid[p0 + (q)]] : 0) * H)
         for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) if (al[q * H + k] > mx[k]) mx[k] = al[q * H + k];
+            for (int k = 0; k < H; ++k) { mx[GRP(q) + k] = -INFINITY; sm[GRP(q) + k] = 0.0; sv[GRP(q) + k] = 0.0; }
         for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) sm[k] += exp(al[q * H + k] - mx[k]);
+            for (int k = 0; k < H; ++k) if (al[q * H + k] > mx[GRP(q) + k]) mx[GRP(q) + k] = al[q * H + k];
         for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) al[q * H + k] = exp(al[q * H + k] - mx[k]) / sm[k];
-        /* dalpha and s_v */
+            for (int k = 0; k < H; ++k) sm[GRP(q) + k] += exp(al[q * H + k] - mx[GRP(q) + k]);
+        for (int64_t q = 0; q < deg; ++q)
+            for (int k = 0; k < H; ++k) al[q * H + k] = exp(al[q * H + k] - mx[GRP(q) + k]) / sm[GRP(q) + k];
+        /* dalpha and s (per normalisation group) */
         const float *Gv = G + (size_t)v * d_out;
         for (int64_t q = 0; q < deg; ++q)
             for (int k = 0; k < H; ++k) {
                 double da = 0.0;
                 for (int j = k * dh_; j < (k + 1) * dh_; ++j) da += (double)Gv[j] * msg[q * d_out + j];
-                sv[k] += al[q * H + k] * da;
+                sv[GRP(q) + k] += al[q * H + k] * da;
                 dm[q * d_out + k * dh_] = da;   /* stash dalpha in the first slot */
             }
         for (int64_t q = 0; q < deg; ++q) {
@@ -544,7 +552,7 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
             for (int k = 0; k < H; ++k) {
                 const double y = Y[q * H + k];
                 const double da = dm[q * d_out + k * dh_];
-                const double dz = al[q * H + k] * (da - sv[k]);
+                const double dz = al[q * H + k] * (da - sv[GRP(q) + k]);
                 Y[q * H + k] = dz * (y > 0.0 ? 1.0 : neg_slope);
             }
             for (int j = 0; j < d_out; ++j) {
@@ -588,6 +596,7 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
             }
         }
     }
+#undef GRP
     (void)x;
     free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
     free(xv); free(x); free(mx); free(sm); free(sv); free(need);

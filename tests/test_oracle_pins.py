@@ -361,7 +361,7 @@ def test_hgt_zero_attention_weight_is_mean():
 
 
 # ---------------------------------------------------------------- RGAT backward
-def rgat_torch_dense(g, h, W, ws, wt, H, slope):
+def rgat_torch_dense(g, h, W, ws, wt, H, slope, scope=0):
     R, N = g["R"], g["N"]
     d_out = W.shape[2]
     dh = d_out // H
@@ -371,11 +371,12 @@ def rgat_torch_dense(g, h, W, ws, wt, H, slope):
     Tt = torch.einsum("rvhc,rhc->rvh", M, wt.reshape(R, H, dh))
     Z = torch.nn.functional.leaky_relu(S[:, None] + Tt[:, :, None], slope)
     mask = (A > 0)[..., None].expand_as(Z)
-    mx = torch.where(mask, Z, torch.tensor(-torch.inf, dtype=Z.dtype)).amax(dim=(0, 2), keepdim=True)
+    dims = (0, 2) if scope == 0 else (2,)   # per destination, or per (relation, destination)
+    mx = torch.where(mask, Z, torch.tensor(-torch.inf, dtype=Z.dtype)).amax(dim=dims, keepdim=True)
     mx = torch.where(torch.isfinite(mx), mx, torch.zeros_like(mx)).detach()
     Zc = torch.where(mask, Z, mx.expand_as(Z))
     ex = torch.exp(Zc - mx) * A[..., None]
-    den = ex.sum(dim=(0, 2), keepdim=True)
+    den = ex.sum(dim=dims, keepdim=True)
     den = torch.where(den > 0, den, torch.ones_like(den))
     al = ex / den
     return torch.einsum("rvuh,ruhc->vhc", al, M).reshape(N, d_out)
@@ -393,6 +394,57 @@ def test_rgat_backward_vs_autograd(kind, H):
                                             t["grad_out"], heads=H)
     for got, k in [(dh, "h"), (dW, "W"), (dws, "w_src"), (dwd, "w_dst")]:
         np.testing.assert_allclose(got, ts[k].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+
+
+@pytest.mark.parametrize("kind,H", [("random", 1), ("dups", 1), ("hub", 2)])
+def test_rgat_backward_per_relation_softmax_vs_autograd(kind, H):
+    """Softmax per (destination, relation) segment: dense per-relation
+    softmax in torch, differentiated by autograd."""
+    g = tiny_graph(54, N=14, E=80, R=3, kind=kind)
+    t = tiny_tensors(54, g, 6, 8, heads=H, att_var=1.0)
+    ts = {k: torch.tensor(t[k], dtype=torch.float64, requires_grad=True)
+          for k in ("h", "W", "w_src", "w_dst")}
+    out = rgat_torch_dense(g, ts["h"], ts["W"], ts["w_src"], ts["w_dst"], H, 0.2, scope=1)
+    ref_fwd = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=H, scope=1)
+    np.testing.assert_allclose(out.detach().numpy(), ref_fwd, rtol=1e-10, atol=1e-12)
+    (out * torch.tensor(t["grad_out"], dtype=torch.float64)).sum().backward()
+    dh, dW, dws, dwd = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"],
+                                            t["grad_out"], heads=H, scope=1)
+    for got, k in [(dh, "h"), (dW, "W"), (dws, "w_src"), (dwd, "w_dst")]:
+        np.testing.assert_allclose(got, ts[k].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+
+
+def test_rgat_backward_per_relation_one_relation_is_per_destination():
+    """With one relation the two softmax scopes coincide."""
+    g = tiny_graph(55, N=12, E=60, R=1, kind="hub")
+    t = tiny_tensors(55, g, 6, 6, att_var=1.0)
+    a = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], scope=0)
+    b = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], scope=1)
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, rtol=1e-13, atol=1e-15)
+
+
+def test_rgat_backward_per_relation_finite_differences():
+    g = tiny_graph(56, N=6, E=18, R=2, kind="dups")
+    t = tiny_tensors(56, g, 3, 4, att_var=1.0)
+    G = t["grad_out"]
+
+    def loss(tt):
+        out = oracle.rgat_forward(g, tt["h"], tt["W"], tt["w_src"], tt["w_dst"], scope=1)
+        return float((out * G).sum())
+    grads = dict(zip(("h", "W", "w_src", "w_dst"),
+                     oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], G, scope=1)))
+    for k in grads:
+        base = t[k]
+        fd = np.zeros(base.shape)
+        for idx in np.ndindex(base.shape):
+            step = 1e-2 * max(1e-2, abs(float(base[idx])))
+            plus, minus = base.copy(), base.copy()
+            plus[idx] = np.float32(base[idx] + step)
+            minus[idx] = np.float32(base[idx] - step)
+            denom = float(plus[idx]) - float(minus[idx])
+            fd[idx] = (loss(dict(t, **{k: plus})) - loss(dict(t, **{k: minus}))) / denom
+        np.testing.assert_allclose(grads[k], fd, rtol=2e-3, atol=2e-4, err_msg=k)
 
 
 def test_rgat_backward_finite_differences():
