@@ -373,6 +373,19 @@ def main():
         layers["rgat_bwd_am_like_880k"] = {"edges_per_s": E / (msb * 1e-3), "ms": msb,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in kb.items()}}
         del wsb
+        # softmax per (dst, rel) segment: forward (aggregate-first) and backward
+        savedr = torch.empty(inf["num_dst_segments"], 2, device=c.dev)
+        wsr1 = c.ws(rgnn.LAYER_RGAT, d, d, 1, rgnn.PLAN_AGGREGATE_FIRST)
+        rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, savedr, wsr1, d, d,
+                          softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
+        del wsr1
+        wsbr = c.ws(rgnn.LAYER_RGAT_BACKWARD, d, d)
+        fnbr = lambda: rgnn.rgat_backward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], savedr,
+                                          c.T["grad_out"], gh, gW, gs, gt, wsbr, d, d,
+                                          softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
+        msbr = time_steps(torch, fnbr, K, W)
+        layers["rgat_bwd_am_like_880k_per_relation_softmax"] = {"edges_per_s": E / (msbr * 1e-3), "ms": msbr}
+        del wsbr, savedr
         # four heads: one masked one-head pass per head
         saved4 = torch.empty(inf["num_nodes"], 4, 2, device=c.dev)
         ws4 = c.ws(rgnn.LAYER_RGAT, d, d, 4)

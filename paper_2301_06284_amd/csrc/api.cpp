@@ -172,7 +172,7 @@ struct BwdHeadsWs { float *Wm, *wsm, *wdm, *Gm, *sv, *dh, *dW, *dws, *dwd; void 
 size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, void *base, BwdHeadsWs *w)
 {
     size_t inner = 0;
-    rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, nullptr, nullptr,
+    rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, 0, nullptr, nullptr,
                        nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &inner);
     Carver c(base);
     BwdHeadsWs x{};
@@ -430,8 +430,6 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     if (per_seg) {   // normalised per (dst, rel) segment: the aggregate-first plan
         if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)
             return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) runs aggregate-first");
-        if (saved) return fail(RGNN_EINVAL, "saved holds per-destination statistics: pass NULL with "
-                                            "softmax per (destination, relation)");
         plan = RGNN_PLAN_AGGREGATE_FIRST;
     }
     plan = resolve_plan(g, RGNN_LAYER_RGAT, d_in, d_out, heads, plan);
@@ -493,7 +491,7 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
         if (per_seg) {
             TravArgs ta;
-            ta.g = g; ta.vstat = w.vstat; ta.vscale = w.vscale;
+            ta.g = g; ta.vstat = w.vstat; ta.vscale = w.vscale; ta.saved = saved;   // [U_dst, 2]
             if ((st = launch_seg_softmax_scale(ta, s)) != RGNN_OK) return st;
             if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
         } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, w.vscale, s)) != RGNN_OK) {
@@ -567,18 +565,25 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
 extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, const float *W,
                                      const float *w_src, const float *w_dst, int32_t d_in,
                                      int32_t d_out, int32_t heads, float neg_slope,
-                                     const float *saved, const float *grad_out, float *grad_h,
+                                     int32_t softmax_scope, const float *saved,
+                                     const float *grad_out, float *grad_h,
                                      float *grad_W, float *grad_w_src, float *grad_w_dst,
                                      void *ws, size_t ws_bytes, void *stream)
 {
     rgnn_status st = check_graph(g);
     if (st != RGNN_OK) return st;
-    if (!h || !W || !w_src || !w_dst || !saved || !grad_out || !grad_h || !grad_W ||
-        !grad_w_src || !grad_w_dst)
+    if (!h || !W || !w_src || !w_dst || !grad_out || !grad_h || !grad_W || !grad_w_src || !grad_w_dst)
         return fail(RGNN_EINVAL, "NULL tensor pointer");
+    if (!saved && (softmax_scope == RGNN_SOFTMAX_PER_DST_REL ? g->U_dst : g->N) > 0)
+        return fail(RGNN_EINVAL, "saved is NULL");
     if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d = 64");
     if (heads != 1 && heads != 2 && heads != 4)
         return fail(RGNN_EUNSUPPORTED, "RGAT backward heads must be 1, 2 or 4");
+    if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
+        return fail(RGNN_EINVAL, "unknown softmax scope");
+    const int per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
+    if (per_seg && heads != 1)
+        return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) has one head");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
     hipStream_t s = (hipStream_t)stream;
     const size_t need = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
@@ -587,9 +592,9 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     BwdHeadsWs w;
     rgat_bwd_heads_layout(g, d_in, d_out, heads, ws, &w);
     if (heads == 1)
-        return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, saved, grad_out,
-                                  grad_h, grad_W, grad_w_src, grad_w_dst, w.inner, w.inner_bytes, s,
-                                  nullptr);
+        return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, per_seg, saved,
+                                  grad_out, grad_h, grad_W, grad_w_src, grad_w_dst, w.inner,
+                                  w.inner_bytes, s, nullptr);
     const int64_t R = g->R, N = g->N, dh = d_out / heads;
     for (int k = 0; k < heads; ++k) {
         const int c0 = (int)(k * dh), c1 = (int)((k + 1) * dh);
@@ -601,7 +606,7 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
         // head 0 writes the outputs, the others add to them
         float *oh = k ? w.dh : grad_h, *oW = k ? w.dW : grad_W;
         float *os = k ? w.dws : grad_w_src, *od = k ? w.dwd : grad_w_dst;
-        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, w.sv, w.Gm,
+        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, 0, w.sv, w.Gm,
                                      oh, oW, os, od, w.inner, w.inner_bytes, s, nullptr)) != RGNN_OK)
             return st;
         if (k) {

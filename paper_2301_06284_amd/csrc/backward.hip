@@ -1,5 +1,7 @@
 // backward.hip -- RGAT backward pass (Section "Backward Propagation") for one
-// head and d = 64, softmax over each destination's in-edges.
+// head and d = 64, softmax over each destination's in-edges, or over each
+// (destination, relation) segment (the per-relation variant: M, Z and s below
+// are then per segment).
 //
 // With G = dL/dout, the forward's per-destination softmax maximum M_v and
 // denominator Z_v, and the reordered vectors ws'_r = W_r w_src[r],
@@ -69,6 +71,8 @@ struct BK {
     const Item *items;
     const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_pos, *in_src;
     const float *h, *wsp, *wtp, *saved, *dS, *vatt, *sv_in;
+    const int32_t *vseg_seg;   // per-segment softmax: segment of each vseg (row of saved)
+    float *svs;                // per-segment softmax: [V] s per vseg, then per segment
     float slope;
     float *Sa;       // [V, D]  sum alpha h_u per segment (by-relation order)
     float *ssum;     // [slots] s_v partial of each piece of a split destination
@@ -77,6 +81,7 @@ struct BK {
     float *dh;       // [N, D]  destination terms written here
 };
 
+template <bool SEG>
 struct BStage {
     int eidx[kE];        // source of each edge
     int evs[kE];         // item-local segment of each edge
@@ -89,6 +94,7 @@ struct BStage {
     float eda[kE];       // dalpha of each edge
     int dptr[kDst + 1];  // item-local first edge of each destination
     float dM[kDst], dZi[kDst], dsv[kDst];   // per destination: M_v, 1/Z_v, s_v
+    float vM[SEG ? kE : 1], vZi[SEG ? kE : 1];   // per segment (per-segment softmax): M, 1/Z
 };
 
 // PHASE 0: every item.  Whole destinations run all passes; pieces of split
@@ -96,13 +102,17 @@ struct BStage {
 //          (signed alpha, dalpha) in ay.
 // PHASE 1: pieces of split destinations only: pass 2 with the merged s_v (their
 //          destination term is summed by split_dst_term_kernel).
-template <int PHASE>
+// SEG (softmax per (dst, rel) segment): PHASE 0 runs pass 1 for every item,
+//          writing each vseg's part of s to svs and parking (alpha, dalpha);
+//          once the parts are summed per segment, PHASE 1 runs passes 2 and 3
+//          for every item (pass 3 for whole destinations only).
+template <int PHASE, bool SEG>
 __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
 {
     constexpr int GPB = 256 / G;
-    __shared__ BStage stage[GPB];
+    __shared__ BStage<SEG> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    BStage &st = stage[gi];
+    BStage<SEG> &st = stage[gi];
     const int64_t item = (int64_t)blockIdx.x * GPB + gi;
     bool valid = item < k.n_items;
     int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
@@ -111,7 +121,7 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
         slot = k.item_slot[item];
         dst0 = x.dst0; nd = x.dst1 - x.dst0; vs0 = x.vs0; nv = x.vs1 - x.vs0;
         e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
-        if (PHASE == 1 && slot < 0) valid = false;
+        if (PHASE == 1 && !SEG && slot < 0) valid = false;
     }
     if (valid) {
         for (int j = gl; j < nv; j += G) {
@@ -120,6 +130,11 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
             st.vrel[j] = k.vseg_rel[vs0 + j];
             st.vpos[j] = k.vseg_pos[vs0 + j];
             st.vatt[j] = k.vatt[vs0 + j];
+            if (SEG && PHASE == 0) {
+                const float2 sz = *reinterpret_cast<const float2 *>(k.saved + (size_t)k.vseg_seg[vs0 + j] * 2);
+                st.vM[j] = sz.x;
+                st.vZi[j] = sz.y > 0.f ? 1.f / sz.y : 0.f;
+            }
             for (int e = a; e < b; ++e) st.evs[e] = j;
         }
         if (gl == 0) st.vptr[nv] = ne;
@@ -132,10 +147,12 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
             st.dptr[j] = k.vseg_ptr[vs0 + a] - e0;
             for (int jv = a; jv < b; ++jv) st.vdj[jv] = j;
             const int64_t v = dst0 + j;
-            const float Z = k.saved[v * 2 + 1];
-            st.dM[j] = k.saved[v * 2];
-            st.dZi[j] = Z > 0.f ? 1.f / Z : 0.f;
-            if (PHASE == 1) st.dsv[j] = k.sv_in[v];
+            if (!SEG) {
+                const float Z = k.saved[v * 2 + 1];
+                st.dM[j] = k.saved[v * 2];
+                st.dZi[j] = Z > 0.f ? 1.f / Z : 0.f;
+                if (PHASE == 1) st.dsv[j] = k.sv_in[v];
+            }
         }
         if (gl == 0) st.dptr[nd] = ne;
         for (int e = gl; e < ne; e += G) {
@@ -178,7 +195,8 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
                 if (e < ne) {
                     const float y = ys + st.vatt[jv];
                     const float z = y > 0.f ? y : k.slope * y;
-                    const float al = __expf(z - st.dM[j]) * st.dZi[j];
+                    const float al = SEG ? __expf(z - st.vM[jv]) * st.vZi[jv]
+                                         : __expf(z - st.dM[j]) * st.dZi[j];
                     s += al * da;
                     sa = lin4(sa, 1.f, Xh[u], al);
                     if (gl == 0) {
@@ -188,13 +206,19 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
                     if (e + 1 == st.vptr[jv + 1]) {
                         st4(k.Sa + (size_t)st.vpos[jv] * D + gl * 4, sa);
                         sa = zero4();
+                        if (SEG) {
+                            if (gl == 0) k.svs[vs0 + jv] = s;
+                            s = 0.f;
+                        }
                         ++jv;
                         if (e + 1 == st.dptr[j + 1]) {
-                            if (gl == 0) {
-                                if (slot < 0) st.dsv[j] = s;
-                                else k.ssum[slot] = s;
+                            if (!SEG) {
+                                if (gl == 0) {
+                                    if (slot < 0) st.dsv[j] = s;
+                                    else k.ssum[slot] = s;
+                                }
+                                s = 0.f;
                             }
-                            s = 0.f;
                             ++j;
                             while (j < nd && st.dptr[j + 1] == st.dptr[j]) ++j;
                         }
@@ -215,15 +239,15 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
     }
     __syncthreads();
 
-    const bool fin = valid && (PHASE == 1 || slot < 0);   // this launch finishes the item
-    if (PHASE == 0 && valid && slot >= 0) {
+    const bool fin = valid && (PHASE == 1 || (!SEG && slot < 0));   // this launch finishes the item
+    if (PHASE == 0 && valid && (SEG || slot >= 0)) {
         for (int e = gl; e < ne; e += G)
             reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(st.ea[e], st.eda[e]);
     }
     // pass 2: Y per edge and its sum per segment (segment-parallel over lanes)
     if (fin) {
         for (int jv = gl; jv < nv; jv += G) {
-            const float sv = st.dsv[st.vdj[jv]];
+            const float sv = SEG ? k.svs[vs0 + jv] : st.dsv[st.vdj[jv]];
             float ys = 0.f;
             for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) {
                 const float a = st.ea[e];
@@ -239,7 +263,7 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
     __syncthreads();
     // pass 3: destination term dh_v = sum over v's segments of ysum * wt'_r,
     // streaming the wt' rows of the item's segments in ping-pong batches
-    if (PHASE == 0 && fin) {
+    if (fin && slot < 0 && (PHASE == 0 || SEG)) {
         float4 acc = zero4();
         int j = 0;
         auto flush_to = [&](int jn) {   // finish destinations [j, jn)
@@ -313,6 +337,41 @@ __global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_spl
         for (int j = 0; j < 256; ++j) t += part[j];
         sv[split_dst[i]] = t;
     }
+}
+
+// Per-segment softmax: s of a (dst, rel) segment cut into several vsegs is
+// the sum of its vsegs' parts (in vseg order), written back to each of them.
+__global__ __launch_bounds__(256) void merge_seg_s_kernel(int64_t U, const int32_t *seg_vsegptr, float *svs)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= U) return;
+    const int b = seg_vsegptr[i], e = seg_vsegptr[i + 1];
+    if (e - b <= 1 || e - b > kBigRange) return;
+    float s = 0.f;
+    for (int vs = b; vs < e; ++vs) s += svs[vs];
+    for (int vs = b; vs < e; ++vs) svs[vs] = s;
+}
+
+// The same for segments with more than kBigRange vsegs: one workgroup each,
+// thread parts added in thread order.
+__global__ __launch_bounds__(256) void merge_seg_s_big_kernel(const int32_t *big_seg, const int32_t *seg_vsegptr,
+                                                              float *svs)
+{
+    __shared__ float part[256];
+    __shared__ float tot;
+    const int sg = big_seg[blockIdx.x];
+    const int b = seg_vsegptr[sg], e = seg_vsegptr[sg + 1];
+    float s = 0.f;
+    for (int vs = b + (int)threadIdx.x; vs < e; vs += 256) s += svs[vs];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float t = 0.f;
+        for (int i = 0; i < 256; ++i) t += part[i];
+        tot = t;
+    }
+    __syncthreads();
+    for (int vs = b + (int)threadIdx.x; vs < e; vs += 256) svs[vs] = tot;
 }
 
 // Destination term of a split destination (its segments span several work
@@ -653,7 +712,7 @@ __global__ void zero_kernel(float *p, int64_t n)
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct BwdWs {
-    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *svs, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
 };
 
 size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
@@ -674,6 +733,7 @@ size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
     x.Sa = take((size_t)g->V * D);
     x.ssum = take((size_t)std::max<int64_t>(g->n_slots, 1));
     x.sv = take((size_t)std::max<int64_t>(g->N, 1));
+    x.svs = take((size_t)std::max<int64_t>(g->V, 1));
     x.ay = take((size_t)g->E * 2);
     x.ysum = take((size_t)std::max<int64_t>(g->V, 1));
     x.ypair = take((size_t)std::max<int64_t>(g->U_src, 1));
@@ -736,9 +796,9 @@ rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int 
 
 rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
                                const float *w_src, const float *w_dst, int d_in, int d_out,
-                               float slope, const float *saved, const float *Gm, float *dh,
-                               float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
-                               hipStream_t s, size_t *need)
+                               float slope, int per_seg, const float *saved, const float *Gm,
+                               float *dh, float *dW, float *dws, float *dwt, void *ws,
+                               size_t ws_bytes, hipStream_t s, size_t *need)
 {
     const size_t bytes = bwd_layout(g, nullptr, nullptr);
     if (need) { *need = bytes; return RGNN_OK; }
@@ -769,12 +829,41 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     k.vseg_pos = g->dev.vseg_pos; k.wtp = w.wtp; k.dh = dh;
     k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
-    k.ysum = w.ysum;
-    if (g->n_items) {
+    k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs;
+    if (g->n_items && per_seg) {
         const dim3 grid((unsigned)((g->n_items + 15) / 16));
         {
             LaunchScope ls("rgat_bwd_traverse", s);
-            hipLaunchKernelGGL((bwd_traverse_kernel<0>), grid, dim3(256), 0, s, k);
+            hipLaunchKernelGGL((bwd_traverse_kernel<0, true>), grid, dim3(256), 0, s, k);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
+        {
+            LaunchScope ls("rgat_bwd_merge_seg_s", s);
+            if (g->U_dst)
+                hipLaunchKernelGGL(merge_seg_s_kernel, dim3((unsigned)((g->U_dst + 255) / 256)), dim3(256), 0,
+                                   s, g->U_dst, g->dev.seg_vsegptr, w.svs);
+            if (g->n_big_seg)
+                hipLaunchKernelGGL(merge_seg_s_big_kernel, dim3((unsigned)g->n_big_seg), dim3(256), 0, s,
+                                   g->dev.big_seg, g->dev.seg_vsegptr, w.svs);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_seg_s launch");
+        {
+            LaunchScope ls("rgat_bwd_traverse_seg", s);
+            hipLaunchKernelGGL((bwd_traverse_kernel<1, true>), grid, dim3(256), 0, s, k);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
+        if (g->n_split) {
+            LaunchScope ls("rgat_bwd_split_dst_term", s);
+            hipLaunchKernelGGL(split_dst_term_kernel, dim3((unsigned)g->n_split), dim3(256), 0, s,
+                               g->dev.split_dst, g->dev.dst_vsegptr, g->dev.vseg_rel, g->dev.vseg_pos,
+                               w.ysum, w.wtp, dh);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
+    } else if (g->n_items) {
+        const dim3 grid((unsigned)((g->n_items + 15) / 16));
+        {
+            LaunchScope ls("rgat_bwd_traverse", s);
+            hipLaunchKernelGGL((bwd_traverse_kernel<0, false>), grid, dim3(256), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
@@ -792,7 +881,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
             {
                 LaunchScope ls("rgat_bwd_traverse_split", s);
-                hipLaunchKernelGGL((bwd_traverse_kernel<1>), grid, dim3(256), 0, s, k);
+                hipLaunchKernelGGL((bwd_traverse_kernel<1, false>), grid, dim3(256), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
             {

@@ -120,7 +120,7 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         for (int32_t t = 0; t < T; ++t) x.ntype_ptr[t + 1] += x.ntype_ptr[t];
 
         // ---- virtual segments: segments cut into pieces of at most C edges ----
-        x.vseg_ptr.clear(); x.vseg_rel.clear(); x.vseg_dst.clear(); x.vseg_cnt.clear();
+        x.vseg_ptr.clear(); x.vseg_rel.clear(); x.vseg_dst.clear(); x.vseg_cnt.clear(); x.vseg_seg.clear();
         x.dst_vsegptr.assign((size_t)N + 1, 0);
         x.seg_vsegptr.assign((size_t)g->U_dst + 1, 0);
         for (int64_t v = 0; v < N; ++v) {
@@ -132,6 +132,7 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
                     x.vseg_rel.push_back(x.seg_rel[s]);
                     x.vseg_dst.push_back((int32_t)v);
                     x.vseg_cnt.push_back(e - b);
+                    x.vseg_seg.push_back(s);
                 }
             }
             x.dst_vsegptr[v + 1] = (int32_t)x.vseg_ptr.size();
@@ -376,6 +377,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.fused_rows, x.fused_rows.data(), x.fused_rows.size() * sizeof(FusedRow)});
     add32(&d.fused_src, x.fused_src);
     add32(&d.vseg_fpos, x.vseg_fpos);
+    add32(&d.vseg_seg, x.vseg_seg);
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
     add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});

@@ -32,11 +32,12 @@ __device__ __forceinline__ float4 relu4(float4 a)
 // Softmax per (dst, rel) segment: a segment longer than kChunkEdges is cut into
 // several virtual segments, each with its own (max m_i, sum s_i), stored at the
 // segment's fused position fpos[i]; per virtual segment the scale
-// exp(m_i - M) / Z of its (dst, rel) segment is written.  Segments with more
-// than kBigRange pieces are left to the block kernel.
+// exp(m_i - M) / Z of its (dst, rel) segment is written, and (M, Z) to
+// saved[segment] when saved is not NULL.  Segments with more than kBigRange
+// pieces are left to the block kernel.
 __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_t *grp_vsegptr,
                                                          const int32_t *fpos, const float *vstat,
-                                                         float *vscale)
+                                                         float *vscale, float *saved)
 {
     const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (v >= N) return;
@@ -50,6 +51,7 @@ __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_
         Z += st.y * __expf(st.x - M);
     }
     for (int i = b; i < e; ++i) vscale[i] = __expf(vstat[(size_t)fpos[i] * 2] - M) / Z;
+    if (saved) *reinterpret_cast<float2 *>(saved + v * 2) = make_float2(M, Z);
 }
 
 // One workgroup per group with many segments: strided per-thread partial
@@ -57,7 +59,7 @@ __global__ __launch_bounds__(256) void vseg_stats_kernel(int64_t N, const int32_
 __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_grp,
                                                              const int32_t *grp_vsegptr,
                                                              const int32_t *fpos, const float *vstat,
-                                                             float *vscale)
+                                                             float *vscale, float *saved)
 {
     __shared__ float sm[256], ss[256];
     __shared__ float fin[2];
@@ -82,6 +84,7 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
             if (ss[t] > 0.f) Z += ss[t] * __expf(sm[t] - M);
         fin[0] = M;
         fin[1] = Z;
+        if (saved) *reinterpret_cast<float2 *>(saved + (size_t)v * 2) = make_float2(M, Z);
     }
     __syncthreads();
     const float M = fin[0], Zi = 1.f / fin[1];
@@ -567,7 +570,7 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
     {
         LaunchScope ls("seg_softmax_scale", s);
         hipLaunchKernelGGL(vseg_stats_kernel, dim3(blocks_for(g->U_dst, 256)), dim3(256), 0, s, g->U_dst,
-                           g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale);
+                           g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale, a.saved);
     }
     hipError_t e = last();
     if (e != hipSuccess) return hip_fail(e, "seg_softmax_scale launch");
@@ -575,7 +578,7 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
     {
         LaunchScope ls("seg_softmax_scale_big", s);
         hipLaunchKernelGGL(vseg_stats_big_kernel, dim3((unsigned)g->n_big_seg), dim3(256), 0, s,
-                           g->dev.big_seg, g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale);
+                           g->dev.big_seg, g->dev.seg_vsegptr, g->dev.vseg_fpos, a.vstat, a.vscale, a.saved);
     }
     e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_softmax_scale_big launch");

@@ -61,6 +61,7 @@ struct HostIndex {
     std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
     std::vector<int32_t> vseg_fpos;    // position of each vseg in fused_rows [V]
+    std::vector<int32_t> vseg_seg;     // (dst, rel) segment of each vseg [V]
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
     std::vector<float> invcnt_byrel;      // 1 / c_{v,r} of each virtual segment, by-relation order
@@ -98,6 +99,7 @@ struct DeviceIndex {
     FusedRow *fused_rows = nullptr;
     int32_t *fused_src = nullptr;
     int32_t *vseg_fpos = nullptr;
+    int32_t *vseg_seg = nullptr;
     Tile *tiles_fused = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
@@ -289,13 +291,14 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
                                   int heads, float *Wqp, hipStream_t s);
 
-// RGAT backward (backward.hip).  With need != NULL only stores the workspace
-// bytes the call needs.
+// RGAT backward (backward.hip), one head.  per_seg: softmax per (dst, rel)
+// segment, saved [U_dst, 2]; else per destination, saved [N, 2].  With
+// need != NULL only stores the workspace bytes the call needs.
 rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
                                const float *w_src, const float *w_dst, int d_in, int d_out,
-                               float slope, const float *saved, const float *Gm, float *dh,
-                               float *dW, float *dws, float *dwt, void *ws, size_t ws_bytes,
-                               hipStream_t s, size_t *need);
+                               float slope, int per_seg, const float *saved, const float *Gm,
+                               float *dh, float *dW, float *dws, float *dwt, void *ws,
+                               size_t ws_bytes, hipStream_t s, size_t *need);
 
 // HGT backward (hgt_backward.hip), the same convention for need.
 rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,

@@ -74,7 +74,7 @@ def _load():
         "rgcn_forward": [vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, sz, vp],
         "rgat_forward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp, sz, vp],
         "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, sz, vp],
-        "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
         "rgcn_backward": [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp],
         "hgt_backward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp,
                          vp, vp, vp, sz, vp],
@@ -262,9 +262,11 @@ def rgcn_backward(g, h, W, W0, out, grad_out, grad_h, grad_W, grad_W0, ws, d_in,
 
 
 def rgat_backward(g, h, W, w_src, w_dst, saved, grad_out, grad_h, grad_W, grad_w_src,
-                  grad_w_dst, ws, d_in, d_out, heads=1, neg_slope=0.2, stream=None):
+                  grad_w_dst, ws, d_in, d_out, heads=1, neg_slope=0.2,
+                  softmax_scope=SOFTMAX_PER_DST, stream=None):
     _check(_lib.rgat_backward(g.handle, _ptr(h), _ptr(W), _ptr(w_src), _ptr(w_dst), d_in, d_out,
-                              heads, float(neg_slope), _ptr(saved), _ptr(grad_out), _ptr(grad_h),
+                              heads, float(neg_slope), softmax_scope, _ptr(saved), _ptr(grad_out),
+                              _ptr(grad_h),
                               _ptr(grad_W), _ptr(grad_w_src), _ptr(grad_w_dst), _ptr(ws),
                               0 if ws is None else ws.numel() * ws.element_size(),
                               _stream(stream)))

@@ -86,6 +86,8 @@ class Runner:
         saved = None
         if scope == 0:
             saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev)
+        elif want_saved:   # per (dst, rel) segment
+            saved = torch.full((self.G.info()["num_dst_segments"], 2), float("nan"), device=self.dev)
         ws_plan = 2 if scope == 1 else plan   # per-(dst, rel) softmax runs aggregate-first
         self.rgnn.rgat_forward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved,
                                self.ws(1, d_in, d_out, heads, ws_plan), d_in, d_out, heads, slope,
@@ -105,17 +107,17 @@ class Runner:
         torch.cuda.synchronize()
         return out.cpu().numpy()
 
-    def rgat_backward(self, slope=0.2, heads=1):
+    def rgat_backward(self, slope=0.2, heads=1, scope=0):
         T, torch, rgnn = self.T, self.torch, self.rgnn
         d = T["W"].shape[1]
         R = T["W"].shape[0]
-        _, saved = self.rgat(heads=heads, slope=slope, want_saved=True)
+        _, saved = self.rgat(heads=heads, slope=slope, want_saved=True, scope=scope)
         gh = torch.full((self.g["N"], d), float("nan"), device=self.dev)
         gW = torch.full((R, d, d), float("nan"), device=self.dev)
         gs = torch.full((R, d), float("nan"), device=self.dev)
         gt = torch.full((R, d), float("nan"), device=self.dev)
         rgnn.rgat_backward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], saved, T["grad_out"],
-                           gh, gW, gs, gt, self.ws(3, d, d, heads), d, d, heads, slope)
+                           gh, gW, gs, gt, self.ws(3, d, d, heads), d, d, heads, slope, scope)
         torch.cuda.synchronize()
         return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
 

@@ -189,6 +189,29 @@ def test_workload5_rgat_backward():
     assert row_err(gt[rels], dwt[rels]) <= TOL
 
 
+def test_workload5_rgat_backward_per_relation_softmax():
+    """The per-(dst, rel) softmax backward on the 880k-node graph, sampled as
+    above (the oracle visits only the destinations that feed the sample)."""
+    g, t, run = load(5)
+    print("workload 5 rgat backward per-relation softmax", flush=True)
+    gh, gW, gs, gt = run.rgat_backward(scope=1)
+    for a in (gh, gW, gs, gt):
+        assert np.isfinite(a).all()
+    rng = np.random.default_rng(6)
+    relcount = np.bincount(g["rel"], minlength=g["R"])
+    rels = np.r_[np.argsort(relcount)[:3], [17]]
+    nodes = rng.choice(g["N"], 60, replace=False)
+    nm = np.zeros(g["N"], np.uint8); nm[nodes] = 1
+    rm = np.zeros(g["R"], np.uint8); rm[rels] = 1
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"],
+                                            t["grad_out"], scope=1, node_mask=nm, rel_mask=rm)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh[nodes], dh[nodes], structural_zero=isolated[nodes], cancel_floor=1e-6) <= TOL
+    assert row_err(gW[rels].reshape(-1, 64), dW[rels].reshape(-1, 64), cancel_floor=1e-6) <= TOL
+    assert row_err(gs[rels], dws[rels], cancel_floor=1e-6) <= TOL
+    assert row_err(gt[rels], dwt[rels], cancel_floor=1e-6) <= TOL
+
+
 def test_workload5_rgcn_backward():
     """RGCN backward (with self-loop, identity activation) on the 880k-node
     graph: dh at sampled sources, dW at sampled relations, dW0 in full."""

@@ -247,9 +247,6 @@ def test_rgat_per_relation_softmax_rejects():
     with pytest.raises(rgnn.RgnnError, match="aggregate-first"):
         rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
                           softmax_scope=rgnn.SOFTMAX_PER_DST_REL, plan=rgnn.PLAN_TRANSFORM_FIRST)
-    with pytest.raises(rgnn.RgnnError, match="saved"):
-        rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved, ws, 64, 64,
-                          softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
     with pytest.raises(rgnn.RgnnError, match="heads"):
         rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
                           heads=2, softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
@@ -315,6 +312,52 @@ def test_rgat_backward_small(kind):
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
     assert row_err(gs, dws) <= TOL
     assert row_err(gt, dwt) <= TOL
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_rgat_backward_per_relation_softmax(kind):
+    """Softmax per (dst, rel) segment: the forward's per-segment (max, sum)
+    feed the backward; s is summed per segment."""
+    g = graph(kind, E=3000)
+    t = workloads.tiny_tensors(47, g, 64, 64, att_var=1.0)
+    print(f"rgat backward per-relation softmax {kind}", flush=True)
+    run = Runner(g, t)
+    gh, gW, gs, gt = run.rgat_backward(scope=1)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                            scope=1)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    # a relation whose segments each repeat one (src, rel) pair has uniform
+    # attention, Y = 0 on all its edges and zero w_dst / w_src gradients by
+    # cancellation (fp64 ~1e-17, fp32 ~1e-8)
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64), cancel_floor=1e-6) <= TOL
+    assert row_err(gs, dws, cancel_floor=1e-6) <= TOL
+    assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
+
+
+def test_rgat_backward_per_relation_softmax_hub_segments():
+    """Segments cut into many pieces (one relation, a 5000-edge hub: more
+    than 32 pieces in one segment) and destinations split over work items."""
+    g = graph("hub", seed=48, N=400, E=12000, R=1)
+    t = workloads.tiny_tensors(48, g, 64, 64, att_var=1.0)
+    print("rgat backward per-relation softmax hub segments", flush=True)
+    run = Runner(g, t)
+    _, saved = run.rgat(scope=1, want_saved=True)
+    sv = saved.cpu().numpy()
+    assert np.isfinite(sv).all() and (sv[:, 1] >= 1 - 1e-5).all()
+    gh, gW, gs, gt = run.rgat_backward(scope=1)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                            scope=1)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    # a relation whose segments each repeat one (src, rel) pair has uniform
+    # attention, Y = 0 on all its edges and zero w_dst / w_src gradients by
+    # cancellation (fp64 ~1e-17, fp32 ~1e-8)
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64), cancel_floor=1e-6) <= TOL
+    assert row_err(gs, dws, cancel_floor=1e-6) <= TOL
+    assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
 
 
 @pytest.mark.parametrize("kind", KINDS)
