@@ -259,6 +259,25 @@ def sweep(args):
         del out
     Gn.close()
     c.close()
+    # HGT on the 1.9M-node graph at d = 32, 64, 128 with d_k = 16 (2, 4, 8 heads)
+    c = Ctx(3)
+    E = c.info["num_edges"]
+    for d in (32, 64, 128):
+        H = d // 16
+        log(f"sweep: workload 3, HGT d = {d}, {H} heads")
+        c.T = {n: torch.from_numpy(v).to(c.dev) for n, v in workloads.make_tensors(3, c.g, "hgt", d, heads=H).items()}
+        out = torch.empty(c.info["num_nodes"], d, device=c.dev)
+        ws = torch.empty(max(rgnn.workspace_size(c.G, rgnn.LAYER_HGT, d, d, H), 256), dtype=torch.uint8,
+                         device=c.dev)
+        T = c.T
+        fn = lambda: rgnn.hgt_forward(c.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
+                                      T["mu"], out, ws, d, H, 0.25, rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR)
+        ms = time_steps(torch, fn, K, W)
+        rows.append({"workload": "mag_like_1p9m", "d": d, "layer": "hgt", "heads": H,
+                     "variant": "reordered segment queries", "ms": round(ms, 4), "edges_per_s": E / (ms * 1e-3)})
+        log(f"  hgt d={d}: {ms:.3f} ms")
+        del ws, out
+    c.close()
     print(json.dumps({"sweep": rows}))
 
 

@@ -220,7 +220,8 @@ rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
  *   agg_t = concat_i sum_e alpha_e,i msg_e,i
  *   out_t = agg_t Wa[tau(t)] (RGNN_FLAG_A_LINEAR, else agg_t) + h_t (RGNN_FLAG_RESIDUAL)
  *   h [N, d]; Wk, Wq, Wv, Wa [T, d, d]; Watt, Wmsg [R, heads, dk, dk]; mu [R].
- *   d = 64 with heads in {1, 2, 4}. */
+ *   d in {32, 64, 128}, heads in {1, 2, 4, 8} with dk = d / heads >= 16
+ *   (hgt_backward: d = 64, heads in {1, 2, 4}). */
 rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, const float *Wq,
                         const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                         const float *mu, int32_t d, int32_t heads, float att_scale, int32_t flags,

@@ -514,8 +514,9 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         return fail(RGNN_EINVAL, "NULL tensor pointer");
     if ((flags & RGNN_FLAG_A_LINEAR) && !Wa) return fail(RGNN_EINVAL, "Wa is NULL");
     if (flags & ~(RGNN_FLAG_RESIDUAL | RGNN_FLAG_A_LINEAR)) return fail(RGNN_EINVAL, "unknown HGT flag");
-    if (d != 64) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 64");
-    if (heads != 1 && heads != 2 && heads != 4) return fail(RGNN_EUNSUPPORTED, "HGT heads must be 1, 2 or 4");
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 32, 64 or 128");
+    if (!(heads == 1 || heads == 2 || heads == 4 || heads == 8) || d / heads < 16)
+        return fail(RGNN_EUNSUPPORTED, "HGT heads must be 1, 2, 4 or 8 with d / heads >= 16");
     if (!std::isfinite(att_scale)) return fail(RGNN_EINVAL, "att_scale must be finite");
     const size_t need = hgt_layout(g, d, heads, nullptr, nullptr);
     if (!ws || ws_bytes < need)
@@ -523,15 +524,29 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     HgtWs w;
     hgt_layout(g, d, heads, ws, &w);
     hipStream_t s = (hipStream_t)stream;
-    // K | V | Q of every node in one node-typed GEMM (segment MM over node types)
+    // K | V | Q of every node by node-typed GEMMs (segment MM over node types):
+    // one GEMM with the three weights side by side at d = 64, one per
+    // projection otherwise (a 3d-wide weight tile would not fit LDS at 128)
     GemmArgs ga;
     ga.X = h; ga.ldx = d; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
-    ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
-    ga.K = d; ga.Nc = 3 * d;
+    ga.K = d;
     ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
-    ga.Y = w.KV; ga.ldy = 2 * d;
-    ga.ep.Y2 = w.Q; ga.ep.ldy2 = d; ga.ep.split = 2 * d;
-    if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    if (d == 64) {
+        ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
+        ga.Nc = 3 * d;
+        ga.Y = w.KV; ga.ldy = 2 * d;
+        ga.ep.Y2 = w.Q; ga.ep.ldy2 = d; ga.ep.split = 2 * d;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    } else {
+        ga.Nc = d;
+        const float *Wp[3] = {Wk, Wv, Wq};
+        float *Yp[3] = {w.KV, w.KV + d, w.Q};
+        const int64_t ld[3] = {2 * d, 2 * d, d};
+        for (int p = 0; p < 3; ++p) {
+            ga.W[0] = Wp[p]; ga.Y = Yp[p]; ga.ldy = ld[p];
+            if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        }
+    }
     // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r] (segment MM over relations)
     if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) return st;
     GemmArgs gq;

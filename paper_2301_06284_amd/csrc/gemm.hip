@@ -292,6 +292,9 @@ bool dispatch_square(int ep, int heads, const GemmK &k, int64_t n, hipStream_t s
         case 4:
             if constexpr (NC >= 64) { launch_k<K, NC, EP_BDIAG, 4>(k, n, s); return true; }
             return false;
+        case 8:
+            if constexpr (NC >= 128) { launch_k<K, NC, EP_BDIAG, 8>(k, n, s); return true; }
+            return false;
         default: return false;
         }
     default: return false;

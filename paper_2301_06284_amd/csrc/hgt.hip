@@ -1,7 +1,7 @@
-// hgt.hip -- HGT edge traversal for d = 64 (heads x d_k = 64).
+// hgt.hip -- HGT edge traversal for d = heads x d_k in {32, 64, 128}.
 //
-// Keys and values of every node come from one node-typed GEMM (K|V stored
-// side by side, 512 bytes per node at d = 64) and are gathered once per edge.
+// Keys and values of every node come from node-typed GEMMs (K|V stored side
+// by side, 512 bytes per node at d = 64) and are gathered once per edge.
 // Both per-relation head matrices are moved to the destination side by linear
 // operator reordering (Section "Linear Operator Reordering"):
 //   a_e,i = (K_s,i Watt[r,i]) . Q_t,i  =  K_s,i . (Q_t,i Watt[r,i]^T)
@@ -15,7 +15,7 @@
 //
 // Work items are those of the RGAT traversal (at most kChunkEdges edges: a
 // bundle of small destinations or a piece of a large one), one per group of
-// 16 lanes; lane l holds features 4l..4l+3, so head i is lanes
+// d / 4 lanes; lane l holds features 4l..4l+3, so head i is lanes
 // [i*LH, (i+1)*LH) with LH = d_k / 4.  Each item first stages its edge
 // sources and segment / destination boundaries in LDS, then streams the
 // K|V rows of its edges, with their segments' query rows (L1 hits after a
@@ -38,10 +38,17 @@ __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 
-constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 constexpr int kU = 2;                    // gathered K|V rows per batch
-constexpr int kBlock = 1024, GPB = kBlock / G;
+
+// Launch shape at width D: a group of D/4 lanes per work item; 1024-lane
+// workgroups (512 at d = 32, whose 128 item stages would not fit in LDS).
+template <int D>
+struct HS {
+    static constexpr int G = D / 4;
+    static constexpr int NTH = D == 32 ? 512 : 1024;
+    static constexpr int GPB = NTH / G;
+};
 
 struct HStage {
     int eidx[kE];          // source node of each edge
@@ -65,7 +72,7 @@ struct HK {
 // broadcast would serve LH = 4 without the LDS crossbar, but it lets the LDS
 // matrix rows of several steps be hoisted ahead of their FMAs and the 1024-lane
 // launch bound then spills; ds_bpermute keeps one step live at a time.
-template <int LH>
+template <int G>
 __device__ __forceinline__ float head_bcast(float v, int jj, int base)
 {
     return __shfl(v, base + jj, G);
@@ -73,7 +80,7 @@ __device__ __forceinline__ float head_bcast(float v, int jj, int base)
 
 // y[4 values of this lane] = x_head (1 x dk) . Mat (dk x dk), Mat row-major,
 // with x_head distributed over the head's LH lanes (4 values each).
-template <int LH>
+template <int LH, int G>
 __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
 {
     constexpr int DK = LH * 4;
@@ -82,8 +89,8 @@ __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
     float4 y = zero4();
 #pragma unroll
     for (int jj = 0; jj < LH; ++jj) {
-        const float x0 = head_bcast<LH>(x.x, jj, base), x1 = head_bcast<LH>(x.y, jj, base);
-        const float x2 = head_bcast<LH>(x.z, jj, base), x3 = head_bcast<LH>(x.w, jj, base);
+        const float x0 = head_bcast<G>(x.x, jj, base), x1 = head_bcast<G>(x.y, jj, base);
+        const float x2 = head_bcast<G>(x.z, jj, base), x3 = head_bcast<G>(x.w, jj, base);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 0) * DK + c0), x0);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 1) * DK + c0), x1);
         y = lin4(y, 1.f, ld4(Mt + (4 * jj + 2) * DK + c0), x2);
@@ -93,9 +100,10 @@ __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
     return y;
 }
 
-template <int H, bool LDSW>
-__global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
+template <int D, int H, bool LDSW>
+__global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
 {
+    constexpr int G = HS<D>::G, GPB = HS<D>::GPB, kBlock = HS<D>::NTH;
     constexpr int DK = D / H, LH = DK / 4;
     constexpr int MAT = H * DK * DK;            // floats per relation per matrix
     extern __shared__ float4 smem4[];
@@ -185,7 +193,7 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
                     m = mn;
                     if (e + 1 == st.vptr[jv + 1]) {
                         const size_t off = (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK;
-                        agg = add4(agg, head_vecmat<LH>(vacc, Wmsg + off, gl));
+                        agg = add4(agg, head_vecmat<LH, G>(vacc, Wmsg + off, gl));
                         vacc = zero4();
                         ++jv;
                         if (e + 1 == st.dptr[j + 1]) {
@@ -211,9 +219,10 @@ __global__ __launch_bounds__(kBlock) void hgt_kernel(HK k)
     while (j < nd) { flush(j); ++j; }
 }
 
-size_t stage_bytes() { return (size_t)GPB * sizeof(HStage); }
+template <int D>
+size_t stage_bytes() { return (size_t)HS<D>::GPB * sizeof(HStage); }
 
-size_t weight_bytes(int R, int heads)
+size_t weight_bytes(int D, int R, int heads)
 {
     const int dk = D / heads;
     return (size_t)R * heads * dk * dk * sizeof(float);
@@ -221,8 +230,8 @@ size_t weight_bytes(int R, int heads)
 
 // Wqp[r][j][n] = mu[r] * scale * Watt[r, i][n - i dk][j - i dk] when j and n
 // both fall in head i's columns, else 0.
-__global__ void hgt_qp_weights_kernel(const float *Watt, const float *mu, float scale, int R, int heads,
-                                      float *Wqp)
+__global__ void hgt_qp_weights_kernel(const float *Watt, const float *mu, float scale, int R, int D,
+                                      int heads, float *Wqp)
 {
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (idx >= (int64_t)R * D * D) return;
@@ -234,44 +243,54 @@ __global__ void hgt_qp_weights_kernel(const float *Watt, const float *mu, float 
     Wqp[idx] = v;
 }
 
+template <int D, int H>
+hipError_t launch_hgt_shape(const HK &k, int64_t n_items, int R, hipStream_t s)
+{
+    const size_t wb = weight_bytes(D, R, H);
+    const bool use_lds = wb + stage_bytes<D>() <= 160 * 1024;
+    const size_t lds = stage_bytes<D>() + (use_lds ? wb : 0);
+    const unsigned nb = (unsigned)((n_items + HS<D>::GPB - 1) / HS<D>::GPB);
+    hipError_t e;
+    if (use_lds) {
+        e = hipFuncSetAttribute((const void *)hgt_kernel<D, H, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds);
+        if (e == hipSuccess)
+            hipLaunchKernelGGL((hgt_kernel<D, H, true>), dim3(nb), dim3(HS<D>::NTH), lds, s, k);
+    } else {
+        e = hipFuncSetAttribute((const void *)hgt_kernel<D, H, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds);
+        if (e == hipSuccess)
+            hipLaunchKernelGGL((hgt_kernel<D, H, false>), dim3(nb), dim3(HS<D>::NTH), lds, s, k);
+    }
+    return e;
+}
+
 }  // namespace
 
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
 {
     const rgnn_graph *g = a.g;
     if (g->n_items == 0) return RGNN_OK;
-    if (a.d != D) return fail(RGNN_EUNSUPPORTED, "HGT traversal supports d = 64");
     HK k{};
     k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
     k.vseg_rel = g->dev.vseg_rel; k.in_src = g->dev.in_src;
     k.KV = a.KV; k.QP = a.QP; k.Wmsg = a.Wmsg;
     k.R = g->R; k.agg = a.agg; k.partial = a.partial; k.saved = a.saved;
-    const size_t wb = weight_bytes(g->R, a.heads);
-    const bool use_lds = wb + stage_bytes() <= 160 * 1024;
-    const size_t lds = stage_bytes() + (use_lds ? wb : 0);
-    const unsigned nb = (unsigned)((g->n_items + GPB - 1) / GPB);
     LaunchScope ls("hgt_traverse", s);
-    hipError_t e = hipSuccess;
-#define HGT(H)                                                                                  \
-    do {                                                                                        \
-        if (use_lds) {                                                                          \
-            e = hipFuncSetAttribute((const void *)hgt_kernel<H, true>,                          \
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
-            if (e == hipSuccess)                                                                \
-                hipLaunchKernelGGL((hgt_kernel<H, true>), dim3(nb), dim3(kBlock), lds, s, k);   \
-        } else {                                                                                \
-            e = hipFuncSetAttribute((const void *)hgt_kernel<H, false>,                         \
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
-            if (e == hipSuccess)                                                                \
-                hipLaunchKernelGGL((hgt_kernel<H, false>), dim3(nb), dim3(kBlock), lds, s, k);  \
-        }                                                                                       \
-    } while (0)
-    if (a.heads == 1) HGT(1);
-    else if (a.heads == 2) HGT(2);
-    else if (a.heads == 4) HGT(4);
-    else return fail(RGNN_EUNSUPPORTED, "HGT traversal supports heads in {1, 2, 4}");
-#undef HGT
+    hipError_t e;
+    const int64_t n = g->n_items;
+    const int R = g->R;
+    if (a.d == 32 && a.heads == 1) e = launch_hgt_shape<32, 1>(k, n, R, s);
+    else if (a.d == 32 && a.heads == 2) e = launch_hgt_shape<32, 2>(k, n, R, s);
+    else if (a.d == 64 && a.heads == 1) e = launch_hgt_shape<64, 1>(k, n, R, s);
+    else if (a.d == 64 && a.heads == 2) e = launch_hgt_shape<64, 2>(k, n, R, s);
+    else if (a.d == 64 && a.heads == 4) e = launch_hgt_shape<64, 4>(k, n, R, s);
+    else if (a.d == 128 && a.heads == 1) e = launch_hgt_shape<128, 1>(k, n, R, s);
+    else if (a.d == 128 && a.heads == 2) e = launch_hgt_shape<128, 2>(k, n, R, s);
+    else if (a.d == 128 && a.heads == 4) e = launch_hgt_shape<128, 4>(k, n, R, s);
+    else if (a.d == 128 && a.heads == 8) e = launch_hgt_shape<128, 8>(k, n, R, s);
+    else return fail(RGNN_EUNSUPPORTED, "HGT traversal: unsupported (d, heads)");
     if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute (HGT LDS)");
     e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt traversal launch");
@@ -280,11 +299,12 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
                                   int heads, float *Wqp, hipStream_t s)
 {
-    if (d != D) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 64");
-    const int64_t n = (int64_t)R * D * D;
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 32, 64, 128");
+    const int64_t n = (int64_t)R * d * d;
+    if (n == 0) return RGNN_OK;
     LaunchScope ls("hgt_qp_weights", s);
     hipLaunchKernelGGL(hgt_qp_weights_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, Watt, mu, scale,
-                       R, heads, Wqp);
+                       R, d, heads, Wqp);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt_qp_weights launch");
 }

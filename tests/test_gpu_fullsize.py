@@ -146,6 +146,26 @@ def test_workload3_hgt():
     assert row_err(got[sel], ref) <= TOL
 
 
+@pytest.mark.parametrize("d,heads", [(32, 2), (128, 8)])
+def test_workload3_graph_hgt_hidden_sizes(d, heads):
+    """HGT on workload 3's graph with d = 32 and 128 tensors (the
+    hidden-size sweep), sampled rows."""
+    g, _, _ = load(3)
+    H = heads
+    dk = d // H
+    t = workloads.make_tensors(3, g, "hgt", d, heads=H)
+    run = Runner(g, t)
+    scale = 1.0 / np.sqrt(dk)
+    print(f"workload 3 graph hgt d={d} heads={H}", flush=True)
+    got = run.hgt(H, scale)
+    run.close()
+    assert np.isfinite(got).all()
+    sel = sample_rows(g, 200, seed=d)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=H, att_scale=scale, sel=sel)
+    assert row_err(got[sel], ref) <= TOL
+
+
 @pytest.mark.parametrize("plan", [1, 2])
 def test_workload4_rgcn(plan):
     g, t, run = load(4)

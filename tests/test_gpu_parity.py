@@ -268,6 +268,24 @@ def test_hgt_small(kind, heads):
     assert row_err(got, ref) <= TOL
 
 
+@pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
+@pytest.mark.parametrize("d,heads", [(32, 1), (32, 2), (128, 1), (128, 2), (128, 4), (128, 8)])
+def test_hgt_hidden_sizes(kind, d, heads):
+    """HGT at d = 32 and 128 (the hidden-size sweep), every head count with
+    d_k >= 16; R = 7 keeps W_msg in LDS except at d = 128 with one or two
+    heads (global reads)."""
+    g = graph(kind, T=4, R=7)
+    t = workloads.tiny_tensors(49, g, d, d, heads=heads)
+    scale = 1.0 / np.sqrt(d // heads)
+    print(f"hgt d={d} {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt(heads, scale)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=heads, att_scale=scale)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
 @pytest.mark.parametrize("heads,R", [(2, 12), (4, 24)])
 def test_hgt_many_relations(heads, R):
     """Enough relations that the per-relation message matrices no longer fit

@@ -136,11 +136,12 @@ def _normal(rng, shape, var: float) -> np.ndarray:
     return (rng.standard_normal(shape, dtype=np.float32) * np.float32(np.sqrt(var)))
 
 
-def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None) -> dict:
+def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None,
+                 heads: int | None = None) -> dict:
     """Features, weights and (workloads 1, 2, 3, 5) the loss weight for workload k.
     Variances: features and weights 1/fan_in, attention vectors 0.1, HGT head
-    blocks 1/d_k, loss weight 1.  `d` overrides the workload's hidden size (the
-    hidden-size sweep)."""
+    blocks 1/d_k, loss weight 1.  `d` and `heads` override the workload's
+    hidden size and HGT head count (the hidden-size sweep)."""
     c = CONFIGS[k]
     _, _, f_rng, w_rng, a_rng, l_rng = _streams(k)
     layer = layer or c["layers"][0]
@@ -154,7 +155,7 @@ def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None
         if layer == "rgat_bwd" or k in (1, 2, 5):
             out["grad_out"] = _normal(l_rng, (N, d), 1.0)
     if layer == "hgt":
-        H = c["heads"]
+        H = heads or c["heads"]
         dk = d // H
         for name in ("Wk", "Wq", "Wv", "Wa"):
             out[name] = _normal(w_rng, (T, d, d), 1.0 / d)
