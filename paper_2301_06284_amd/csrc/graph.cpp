@@ -241,6 +241,16 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.big_split.clear();
         for (int64_t i = 0; i < g->n_split; ++i)
             if (x.split_slotptr[i + 1] - x.split_slotptr[i] > kBigRange) x.big_split.push_back((int32_t)i);
+        x.big_chunkptr.assign(1, 0);
+        x.chunk_lo.clear(); x.chunk_hi.clear();
+        for (int32_t i : x.big_split) {
+            for (int32_t sl = x.split_slotptr[i]; sl < x.split_slotptr[i + 1]; sl += kMergeChunk) {
+                x.chunk_lo.push_back(sl);
+                x.chunk_hi.push_back(std::min<int32_t>(sl + kMergeChunk, x.split_slotptr[i + 1]));
+            }
+            x.big_chunkptr.push_back((int32_t)x.chunk_lo.size());
+        }
+        g->n_big_chunks = (int64_t)x.chunk_lo.size();
         // destinations with many segments, largest first (ties in id order):
         // their reductions take whole workgroups at the front of the grid
         x.big_vdst.clear();
@@ -359,6 +369,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
     add32(&d.split_slotptr, x.split_slotptr);
     add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
+    add32(&d.big_chunkptr, x.big_chunkptr); add32(&d.chunk_lo, x.chunk_lo); add32(&d.chunk_hi, x.chunk_hi);
     add32(&d.seg_vsegptr, x.seg_vsegptr); add32(&d.big_seg, x.big_seg);
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});

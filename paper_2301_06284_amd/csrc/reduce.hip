@@ -382,47 +382,59 @@ __global__ __launch_bounds__(256) void merge_kernel(int64_t n_split, const int32
     st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
 
-// One 1024-thread workgroup per destination split over many items: each
-// group of D/4 lanes merges a strided subset of the partials, then group 0
-// merges the group states in group order.
+// Destinations split over many items, level 1: a 256-thread workgroup per
+// chunk of at most kMergeChunk partials; each group of D/4 lanes merges a
+// strided subset (four records in flight), group 0 merges the group states in
+// group order and writes the chunk's merged record over its first partial
+// (softmax: per head the maximum, the sum relative to it and the row sum;
+// sums: the row sum).
 template <int D, int H, bool SOFTMAX>
-__global__ __launch_bounds__(1024) void merge_big_kernel(const int32_t *big_split,
-                                                         const int32_t *split_dst,
-                                                         const int32_t *split_slotptr,
-                                                         const float *partial, float *out,
-                                                         float *saved, int relu)
+__global__ __launch_bounds__(256) void merge_chunk_kernel(const int32_t *chunk_lo, const int32_t *chunk_hi,
+                                                          float *partial)
 {
-    constexpr int G = D / 4, NG = 1024 / G, LH = D / H / 4;
+    constexpr int G = D / 4, NG = 256 / G, LH = D / H / 4;
     constexpr int REC = SOFTMAX ? 2 * H + D : 2 + D;
     constexpr int OFF = SOFTMAX ? 2 * H : 2;
+    constexpr int U = 4;
     __shared__ float4 pacc[NG * G];
     __shared__ float pm[NG * H], ps[NG * H];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int i = big_split[blockIdx.x];
-    const int v = split_dst[i];
-    const int b = split_slotptr[i], e = split_slotptr[i + 1];
+    const int b = chunk_lo[blockIdx.x], e = chunk_hi[blockIdx.x];
     const int head = gl / LH;
     float m = -INFINITY, s = 0.f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sl = b + gi; sl < e; sl += NG) {
-        const float *pr = partial + (size_t)sl * REC;
-        const float4 a = ld4(pr + OFF + gl * 4);
-        if (SOFTMAX) {
-            const float mi = pr[head * 2], si = pr[head * 2 + 1];
-            const float mn = fmaxf(m, mi);
-            const float c1 = __expf(m - mn), c2 = __expf(mi - mn);
-            s = s * c1 + si * c2;
-            acc = lin4(acc, c1, a, c2);
-            m = mn;
-        } else {
-            acc = add4(acc, a);
+    for (int sl0 = b + gi; sl0 < e; sl0 += U * NG) {
+        float4 a[U];
+        float mi[U], si[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int sl = sl0 + u * NG;
+            if (sl < e) {
+                const float *pr = partial + (size_t)sl * REC;
+                a[u] = ld4(pr + OFF + gl * 4);
+                if (SOFTMAX) { mi[u] = pr[head * 2]; si[u] = pr[head * 2 + 1]; }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (sl0 + u * NG >= e) break;
+            if (SOFTMAX) {
+                const float mn = fmaxf(m, mi[u]);
+                const float c1 = __expf(m - mn), c2 = __expf(mi[u] - mn);
+                s = s * c1 + si[u] * c2;
+                acc = lin4(acc, c1, a[u], c2);
+                m = mn;
+            } else {
+                acc = add4(acc, a[u]);
+            }
         }
     }
     pacc[gi * G + gl] = acc;
     if (gl % LH == 0) { pm[gi * H + head] = m; ps[gi * H + head] = s; }
-    __syncthreads();
+    __syncthreads();   // every partial of the chunk has been read
     if (gi != 0) return;
     float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+    float *pr = partial + (size_t)b * REC;
     if (SOFTMAX) {
         float M = -INFINITY;
         for (int j = 0; j < NG; ++j) M = fmaxf(M, pm[j * H + head]);
@@ -433,15 +445,69 @@ __global__ __launch_bounds__(1024) void merge_big_kernel(const int32_t *big_spli
             Z += ps[j * H + head] * c;
             tot = lin4(tot, 1.f, pacc[j * G + gl], c);
         }
-        tot = scale4(tot, Z > 0.f ? 1.f / Z : 0.f);
-        if (saved && gl % LH == 0) {
-            saved[((size_t)v * H + head) * 2] = M;
-            saved[((size_t)v * H + head) * 2 + 1] = Z;
-        }
+        if (gl % LH == 0) { pr[head * 2] = M; pr[head * 2 + 1] = Z; }
     } else {
         for (int j = 0; j < NG; ++j) tot = add4(tot, pacc[j * G + gl]);
     }
-    st4(out + (size_t)v * D + gl * 4, relu ? relu4(tot) : tot);
+    st4(pr + OFF + gl * 4, tot);
+}
+
+// Level 2: a group of D/4 lanes per split destination merges its chunks'
+// records in chunk order (four in flight) and writes the output row (and
+// the softmax statistics).
+template <int D, int H, bool SOFTMAX>
+__global__ __launch_bounds__(256) void merge_chunks_final_kernel(int64_t nbig, const int32_t *big_split,
+                                                                 const int32_t *split_dst,
+                                                                 const int32_t *big_chunkptr,
+                                                                 const int32_t *chunk_lo, const float *partial,
+                                                                 float *out, float *saved, int relu)
+{
+    constexpr int G = D / 4, GPB = 256 / G, LH = D / H / 4;
+    constexpr int REC = SOFTMAX ? 2 * H + D : 2 + D;
+    constexpr int OFF = SOFTMAX ? 2 * H : 2;
+    constexpr int U = 4;
+    const int gl = threadIdx.x % G;
+    const int64_t j = (int64_t)blockIdx.x * GPB + threadIdx.x / G;
+    if (j >= nbig) return;
+    const int v = split_dst[big_split[j]];
+    const int c0 = big_chunkptr[j], c1 = big_chunkptr[j + 1];
+    const int head = gl / LH;
+    float m = -INFINITY, s = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int cb = c0; cb < c1; cb += U) {
+        float4 a[U];
+        float mi[U], si[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cb + u < c1) {
+                const float *pr = partial + (size_t)chunk_lo[cb + u] * REC;
+                a[u] = ld4(pr + OFF + gl * 4);
+                if (SOFTMAX) { mi[u] = pr[head * 2]; si[u] = pr[head * 2 + 1]; }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cb + u >= c1) break;
+            if (SOFTMAX) {
+                if (!(si[u] > 0.f)) continue;
+                const float mn = fmaxf(m, mi[u]);
+                const float e1 = __expf(m - mn), e2 = __expf(mi[u] - mn);
+                s = s * e1 + si[u] * e2;
+                acc = lin4(acc, e1, a[u], e2);
+                m = mn;
+            } else {
+                acc = add4(acc, a[u]);
+            }
+        }
+    }
+    if (SOFTMAX) {
+        acc = scale4(acc, s > 0.f ? 1.f / s : 0.f);
+        if (saved && gl % LH == 0) {
+            saved[((size_t)v * H + head) * 2] = m;
+            saved[((size_t)v * H + head) * 2 + 1] = s;
+        }
+    }
+    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
 
 __global__ void fill_kernel(float *p, int64_t n, float v)
@@ -509,7 +575,7 @@ hipError_t last() { return hipGetLastError(); }
 }  // namespace
 
 rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
-                                  const float *partial, float *out, float *saved, int relu,
+                                  float *partial, float *out, float *saved, int relu,
                                   hipStream_t s)
 {
     if (g->n_split == 0) return RGNN_OK;
@@ -542,8 +608,15 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
     if (nbig == 0) return RGNN_OK;
     {
         LaunchScope ls("merge_partials_big", s);
-#define MERGEB(D, H, SM) hipLaunchKernelGGL((merge_big_kernel<D, H, SM>), dim3(nbig), dim3(1024), 0, \
-                                            s, bs, sd, sp, partial, out, saved, relu)
+        const unsigned nc = (unsigned)g->n_big_chunks, nf = blocks_for(nbig, 256 / (d / 4));
+        const int32_t *clo = g->dev.chunk_lo, *chi = g->dev.chunk_hi, *cp = g->dev.big_chunkptr;
+#define MERGEB(D, H, SM)                                                                             \
+    do {                                                                                             \
+        hipLaunchKernelGGL((merge_chunk_kernel<D, H, SM>), dim3(nc), dim3(256), 0, s, clo, chi,      \
+                           partial);                                                                 \
+        hipLaunchKernelGGL((merge_chunks_final_kernel<D, H, SM>), dim3(nf), dim3(256), 0, s, nbig,   \
+                           bs, sd, cp, clo, partial, out, saved, relu);                              \
+    } while (0)
         if (!softmax) {
             if (d == 32) MERGEB(32, 1, false);
             else if (d == 64) MERGEB(64, 1, false);
@@ -560,7 +633,7 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 #undef MERGEB
     }
     e = last();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "merge_big launch");
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "merge_partials_big launch");
 }
 
 rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)

@@ -25,6 +25,9 @@ constexpr int kFusedTileEdges = 4096;
 // Reductions over more records than this (partials of a split destination,
 // segments of one destination) get a whole workgroup instead of one group.
 constexpr int kBigRange = 32;
+// the partials of a destination split over more than kBigRange items are
+// merged in two levels: chunks of kMergeChunk partials, then the chunks
+constexpr int kMergeChunk = 128;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
@@ -53,6 +56,8 @@ struct HostIndex {
     std::vector<Item> items;
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
     std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
+    std::vector<int32_t> big_chunkptr;  // chunks of each big split [n_big_split + 1]
+    std::vector<int32_t> chunk_lo, chunk_hi;   // slot range of each chunk [n_big_chunks]
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments,
                                       // largest first
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
@@ -90,6 +95,7 @@ struct DeviceIndex {
     Item *items = nullptr;
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
+    int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr;
     float *invcnt_byrel = nullptr;
     Tile *tiles_nodes_outer = nullptr;
@@ -121,7 +127,7 @@ struct rgnn_graph {
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
-    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0;
+    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
     int64_t n_oitems = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
@@ -223,8 +229,10 @@ rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s);
 // Finish destinations split over several work items: combine their partials
 // (softmax: (max, sum) per head then the D-vector; else the D-vector only).
+// The partials of destinations with many pieces are overwritten (the chunk
+// records of the two-level merge).
 rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int softmax,
-                                  const float *partial, float *out, float *saved, int relu,
+                                  float *partial, float *out, float *saved, int relu,
                                   hipStream_t s);
 // Softmax per (dst, rel) segment: per virtual segment the scale
 // exp(m_i - M_seg) / Z_seg from the pieces' (max, sum) in a.vstat, to a.vscale.
