@@ -244,18 +244,25 @@ __global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
         for (int e = gl; e < ne; e += G)
             reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(st.ea[e], st.eda[e]);
     }
-    // pass 2: Y per edge and its sum per segment (segment-parallel over lanes)
+    // pass 2: Y per edge (edge-parallel over lanes, coalesced (alpha, Y)
+    // stores; Y kept in eda), then its sum per segment (segment-parallel,
+    // edges in order)
+    if (fin) {
+        for (int e = gl; e < ne; e += G) {
+            const int jv = st.evs[e];
+            const float sv = SEG ? k.svs[vs0 + jv] : st.dsv[st.vdj[jv]];
+            const float a = st.ea[e];
+            const float al = fabsf(a);
+            const float Y = al * (st.eda[e] - sv) * (signbit(a) ? k.slope : 1.f);
+            reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
+            st.eda[e] = Y;
+        }
+    }
+    __syncthreads();
     if (fin) {
         for (int jv = gl; jv < nv; jv += G) {
-            const float sv = SEG ? k.svs[vs0 + jv] : st.dsv[st.vdj[jv]];
             float ys = 0.f;
-            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) {
-                const float a = st.ea[e];
-                const float al = fabsf(a);
-                const float Y = al * (st.eda[e] - sv) * (signbit(a) ? k.slope : 1.f);
-                ys += Y;
-                reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
-            }
+            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) ys += st.eda[e];
             k.ysum[st.vpos[jv]] = ys;
             st.vatt[jv] = ys;
         }
@@ -375,24 +382,44 @@ __global__ __launch_bounds__(256) void merge_seg_s_big_kernel(const int32_t *big
 }
 
 // Destination term of a split destination (its segments span several work
-// items): one workgroup per destination, segments strided over 16-lane groups
-// and combined in group order.
-__global__ __launch_bounds__(256) void split_dst_term_kernel(const int32_t *split_dst, const int32_t *dst_vsegptr,
+// items): one workgroup of NTH threads per destination, segments strided over
+// 16-lane groups (U in flight) and combined in group order.  Destinations
+// split over more than kBigRange items (the hubs) take 1024-thread
+// workgroups in a launch of their own (BIG).
+template <int NTH, int U, bool BIG>
+__global__ __launch_bounds__(NTH) void split_dst_term_kernel(const int32_t *big_split, const int32_t *split_slotptr,
+                                                             const int32_t *split_dst, const int32_t *dst_vsegptr,
                                                              const int32_t *vseg_rel, const int32_t *vseg_pos,
                                                              const float *ysum, const float *wtp, float *dh)
 {
-    constexpr int NG = 256 / G;
+    constexpr int NG = NTH / G;
     __shared__ float4 part[NG][G];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int v = split_dst[blockIdx.x];
+    const int i = BIG ? big_split[blockIdx.x] : (int)blockIdx.x;
+    if (!BIG && split_slotptr[i + 1] - split_slotptr[i] > kBigRange) return;
+    const int v = split_dst[i];
+    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     float4 acc = zero4();
-    for (int vs = dst_vsegptr[v] + gi; vs < dst_vsegptr[v + 1]; vs += NG)
-        acc = lin4(acc, 1.f, ld4(wtp + (size_t)vseg_rel[vs] * D + gl * 4), ysum[vseg_pos[vs]]);
+    for (int vs0 = b + gi; vs0 < e; vs0 += U * NG) {
+        float4 w[U];
+        float y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int vs = vs0 + u * NG;
+            if (vs < e) {
+                w[u] = ld4(wtp + (size_t)vseg_rel[vs] * D + gl * 4);
+                y[u] = ysum[vseg_pos[vs]];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (vs0 + u * NG < e) acc = lin4(acc, 1.f, w[u], y[u]);
+    }
     part[gi][gl] = acc;
     __syncthreads();
     if (gi == 0) {
         float4 t = zero4();
-        for (int i = 0; i < NG; ++i) t = add4(t, part[i][gl]);
+        for (int j = 0; j < NG; ++j) t = add4(t, part[j][gl]);
         st4(dh + (size_t)v * D + gl * 4, t);
     }
 }
@@ -754,6 +781,17 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
     return hipGetLastError();
 }
 
+void launch_split_dst_term(const rgnn_graph *g, const float *ysum, const float *wtp, float *dh, hipStream_t s)
+{
+    const DeviceIndex &x = g->dev;
+    hipLaunchKernelGGL((split_dst_term_kernel<256, 4, false>), dim3((unsigned)g->n_split), dim3(256), 0, s,
+                       nullptr, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, ysum, wtp, dh);
+    if (g->n_big_split)
+        hipLaunchKernelGGL((split_dst_term_kernel<1024, 8, true>), dim3((unsigned)g->n_big_split), dim3(1024), 0,
+                           s, x.big_split, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos,
+                           ysum, wtp, dh);
+}
+
 }  // namespace
 
 int bwd_outer_rows() { return kOuterRows; }
@@ -854,9 +892,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
             LaunchScope ls("rgat_bwd_split_dst_term", s);
-            hipLaunchKernelGGL(split_dst_term_kernel, dim3((unsigned)g->n_split), dim3(256), 0, s,
-                               g->dev.split_dst, g->dev.dst_vsegptr, g->dev.vseg_rel, g->dev.vseg_pos,
-                               w.ysum, w.wtp, dh);
+            launch_split_dst_term(g, w.ysum, w.wtp, dh, s);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
     } else if (g->n_items) {
@@ -886,9 +922,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
             {
                 LaunchScope ls("rgat_bwd_split_dst_term", s);
-                hipLaunchKernelGGL(split_dst_term_kernel, dim3((unsigned)g->n_split), dim3(256), 0, s,
-                                   g->dev.split_dst, g->dev.dst_vsegptr, g->dev.vseg_rel, g->dev.vseg_pos,
-                                   w.ysum, w.wtp, dh);
+                launch_split_dst_term(g, w.ysum, w.wtp, dh, s);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
         }
