@@ -547,16 +547,26 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
             if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         }
     }
-    // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r] (segment MM over relations)
-    if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) return st;
-    GemmArgs gq;
-    gq.X = w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
-    gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
-    gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
-    gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = heads;
-    if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
     HgtArgs ha;
-    ha.g = g; ha.KV = w.KV; ha.QP = w.QP; ha.Wmsg = Wmsg;
+    ha.g = g; ha.KV = w.KV; ha.Wmsg = Wmsg;
+    if (d == 128 && hgt_fused_query_fits(g->R, d, heads)) {
+        // the traversal forms each segment's reordered query Q_t (mu scale Watt[r]^T)
+        // from LDS-resident blocks at the segment's first edge.  Measured on the
+        // 1.9M-node graph this wins only at d = 128 (the 128-wide segment-query
+        // GEMM it replaces is MFMA-bound); at d = 32 and 64 the per-segment
+        // vector-matrix product in the traversal costs more than the GEMM.
+        ha.QP = nullptr; ha.Q = w.Q; ha.Watt = Watt; ha.mu = mu; ha.scale = att_scale;
+    } else {
+        // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r] (segment MM over relations)
+        if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) return st;
+        GemmArgs gq;
+        gq.X = w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
+        gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
+        gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
+        gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = heads;
+        if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
+        ha.QP = w.QP;
+    }
     ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
     if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
     if ((st = launch_merge_partials(g, d, heads, 1, w.partial, w.agg, nullptr, 0, s)) != RGNN_OK)

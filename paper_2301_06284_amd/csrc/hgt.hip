@@ -50,19 +50,23 @@ struct HS {
     static constexpr int GPB = NTH / G;
 };
 
+template <bool FQ>
 struct HStage {
     int eidx[kE];          // source node of each edge
     int evs[kE];           // item-local virtual segment of each edge
     int vptr[kE + 1];      // item-local edge offset of each virtual segment
     int vrel[kE];
     int dptr[kDst + 1];    // item-local edge offset of each destination
+    int vdst[FQ ? kE : 1]; // destination of each virtual segment (queries formed in the kernel)
 };
 
 struct HK {
     int64_t n_items;
     const Item *items;
-    const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *in_src;
+    const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_dst, *in_src;
     const float *KV, *QP, *Wmsg;
+    const float *Q, *Watt, *mu;   // queries formed in the kernel: Q [N, d], Watt, mu, scale
+    float scale;
     int R;
     float *agg, *partial;
     float *saved;          // [N, H, 2] per destination and head (max, sum), or NULL
@@ -80,14 +84,16 @@ __device__ __forceinline__ float head_bcast(float v, int jj, int base)
 
 // y[4 values of this lane] = x_head (1 x dk) . Mat (dk x dk), Mat row-major,
 // with x_head distributed over the head's LH lanes (4 values each).
-template <int LH, int G>
+// ROLLED: a loop instead of LH unrolled steps (one code copy where several
+// call sites are inlined into the unrolled edge loop).
+template <int LH, int G, bool ROLLED = false>
 __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
 {
     constexpr int DK = LH * 4;
     const int base = (gl / LH) * LH;     // first lane of this head within the group
     const int c0 = 4 * (gl % LH);
     float4 y = zero4();
-#pragma unroll
+#pragma unroll(ROLLED ? 1 : LH)
     for (int jj = 0; jj < LH; ++jj) {
         const float x0 = head_bcast<G>(x.x, jj, base), x1 = head_bcast<G>(x.y, jj, base);
         const float x2 = head_bcast<G>(x.z, jj, base), x3 = head_bcast<G>(x.w, jj, base);
@@ -100,24 +106,38 @@ __device__ __forceinline__ float4 head_vecmat(float4 x, const float *Mt, int gl)
     return y;
 }
 
-template <int D, int H, bool LDSW>
+// FQ: the reordered query of each segment, Q_t,i (mu[r] scale Watt[r, i]^T),
+// is formed in the kernel at the segment's first edge from LDS-resident
+// blocks (requires LDSW), with the next segment's Q row already in flight,
+// instead of being read from a materialized [V, d] array.
+template <int D, int H, bool LDSW, bool FQ>
 __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
 {
+    static_assert(!FQ || LDSW, "kernel-formed queries keep both weight sets in LDS");
     constexpr int G = HS<D>::G, GPB = HS<D>::GPB, kBlock = HS<D>::NTH;
     constexpr int DK = D / H, LH = DK / 4;
     constexpr int MAT = H * DK * DK;            // floats per relation per matrix
     extern __shared__ float4 smem4[];
     float *smem = reinterpret_cast<float *>(smem4);
     const int nW = LDSW ? k.R * MAT : 0;
-    HStage *stages = reinterpret_cast<HStage *>(smem + nW);
+    const int nQ = FQ ? k.R * MAT : 0;
+    HStage<FQ> *stages = reinterpret_cast<HStage<FQ> *>(smem + nW + nQ);
     const float *Wmsg = k.Wmsg;
     if (LDSW) {
         const int n4 = k.R * MAT / 4;
         for (int i = threadIdx.x; i < n4; i += kBlock) smem4[i] = reinterpret_cast<const float4 *>(k.Wmsg)[i];
         Wmsg = smem;
     }
+    float *Wq = smem + nW;   // [R][H][j][n] = mu[r] scale Watt[r, i][n][j]
+    if (FQ) {
+        for (int idx = threadIdx.x; idx < nQ; idx += kBlock) {
+            const int r = idx / MAT, rem = idx % MAT;
+            const int i = rem / (DK * DK), j = rem / DK % DK, n = rem % DK;
+            Wq[idx] = k.mu[r] * k.scale * k.Watt[(((size_t)r * H + i) * DK + n) * DK + j];
+        }
+    }
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    HStage &st = stages[gi];
+    HStage<FQ> &st = stages[gi];
     const int64_t item = (int64_t)blockIdx.x * GPB + gi;
     const bool valid = item < k.n_items;
     int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
@@ -130,6 +150,7 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
             const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
             st.vptr[j] = a;
             st.vrel[j] = k.vseg_rel[vs0 + j];
+            if (FQ) st.vdst[j] = k.vseg_dst[vs0 + j];
             for (int e = a; e < b; ++e) st.evs[e] = j;
         }
         if (gl == 0) st.vptr[nv] = ne;
@@ -163,6 +184,8 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
     };
     int j = 0, jv = 0;
     while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush(j); ++j; }
+    float4 qcur = zero4(), qp = zero4();   // FQ: Q row of segment jv's destination; its query
+    if (FQ && ne > 0) qcur = ld4(k.Q + (size_t)st.vdst[0] * D + gl * 4);
     if (ne > 0) {
         // Ping-pong batches: batch A is consumed while batch B is in flight.
         // Each edge brings its K|V row and its segment's reordered query row
@@ -175,7 +198,7 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
                 const size_t row = (size_t)st.eidx[e] * (2 * D);
                 Xk[u] = ld4(k.KV + row + gl * 4);
                 Xv[u] = ld4(k.KV + row + D + gl * 4);
-                Xq[u] = ld4(k.QP + (size_t)(vs0 + st.evs[e]) * D + gl * 4);
+                if (!FQ) Xq[u] = ld4(k.QP + (size_t)(vs0 + st.evs[e]) * D + gl * 4);
             }
         };
         auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
@@ -184,7 +207,12 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
                 if (e < ne) {
-                    const float a = gsum<LH>(dot4(Xk[u], Xq[u]));
+                    if (FQ && e == st.vptr[jv]) {   // first edge of segment jv: form its query
+                        qp = head_vecmat<LH, G, true>(qcur, Wq + (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK, gl);
+                        if (jv + 1 < nv && st.vdst[jv + 1] != st.vdst[jv])
+                            qcur = ld4(k.Q + (size_t)st.vdst[jv + 1] * D + gl * 4);
+                    }
+                    const float a = gsum<LH>(dot4(Xk[u], FQ ? qp : Xq[u]));
                     const float mn = fmaxf(m, a);
                     const float c1 = __expf(m - mn), c2 = __expf(a - mn);
                     s = s * c1 + c2;
@@ -219,8 +247,8 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
     while (j < nd) { flush(j); ++j; }
 }
 
-template <int D>
-size_t stage_bytes() { return (size_t)HS<D>::GPB * sizeof(HStage); }
+template <int D, bool FQ>
+size_t stage_bytes() { return (size_t)HS<D>::GPB * sizeof(HStage<FQ>); }
 
 size_t weight_bytes(int D, int R, int heads)
 {
@@ -247,22 +275,31 @@ template <int D, int H>
 hipError_t launch_hgt_shape(const HK &k, int64_t n_items, int R, hipStream_t s)
 {
     const size_t wb = weight_bytes(D, R, H);
-    const bool use_lds = wb + stage_bytes<D>() <= 160 * 1024;
-    const size_t lds = stage_bytes<D>() + (use_lds ? wb : 0);
     const unsigned nb = (unsigned)((n_items + HS<D>::GPB - 1) / HS<D>::GPB);
     hipError_t e;
-    if (use_lds) {
-        e = hipFuncSetAttribute((const void *)hgt_kernel<D, H, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)lds);
-        if (e == hipSuccess)
-            hipLaunchKernelGGL((hgt_kernel<D, H, true>), dim3(nb), dim3(HS<D>::NTH), lds, s, k);
+#define HGT_LAUNCH(LDSW, FQ, LDS)                                                                          \
+    do {                                                                                                   \
+        e = hipFuncSetAttribute((const void *)hgt_kernel<D, H, LDSW, FQ>,                                  \
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)(LDS));                   \
+        if (e == hipSuccess)                                                                               \
+            hipLaunchKernelGGL((hgt_kernel<D, H, LDSW, FQ>), dim3(nb), dim3(HS<D>::NTH), (LDS), s, k);     \
+    } while (0)
+    if (!k.QP) {   // queries formed in the kernel (the caller checked that both weight sets fit)
+        if constexpr (D == 128) HGT_LAUNCH(true, true, (stage_bytes<D, true>() + 2 * wb));
+        else e = hipErrorInvalidValue;
+    } else if (wb + stage_bytes<D, false>() <= 160 * 1024) {
+        HGT_LAUNCH(true, false, (stage_bytes<D, false>() + wb));
     } else {
-        e = hipFuncSetAttribute((const void *)hgt_kernel<D, H, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)lds);
-        if (e == hipSuccess)
-            hipLaunchKernelGGL((hgt_kernel<D, H, false>), dim3(nb), dim3(HS<D>::NTH), lds, s, k);
+        HGT_LAUNCH(false, false, (stage_bytes<D, false>()));
     }
+#undef HGT_LAUNCH
     return e;
+}
+
+template <int D>
+bool fused_query_fits(int R, int heads)
+{
+    return stage_bytes<D, true>() + 2 * weight_bytes(D, R, heads) <= 160 * 1024;
 }
 
 }  // namespace
@@ -274,8 +311,11 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     HK k{};
     k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
     k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr;
-    k.vseg_rel = g->dev.vseg_rel; k.in_src = g->dev.in_src;
+    k.vseg_rel = g->dev.vseg_rel; k.vseg_dst = g->dev.vseg_dst; k.in_src = g->dev.in_src;
     k.KV = a.KV; k.QP = a.QP; k.Wmsg = a.Wmsg;
+    k.Q = a.Q; k.Watt = a.Watt; k.mu = a.mu; k.scale = a.scale;
+    if (!a.QP && !(a.Q && a.Watt && a.mu && hgt_fused_query_fits(g->R, a.d, a.heads)))
+        return fail(RGNN_EINVAL, "HGT traversal without segment queries needs Q, Watt, mu and LDS room");
     k.R = g->R; k.agg = a.agg; k.partial = a.partial; k.saved = a.saved;
     LaunchScope ls("hgt_traverse", s);
     hipError_t e;
@@ -294,6 +334,12 @@ rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s)
     if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute (HGT LDS)");
     e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt traversal launch");
+}
+
+bool hgt_fused_query_fits(int R, int d, int heads)
+{
+    // instantiated at d = 128 only, the width where it beats the segment-query GEMM
+    return d == 128 && fused_query_fits<128>(R, heads);
 }
 
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,

@@ -284,7 +284,11 @@ rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
 struct HgtArgs {
     const rgnn_graph *g = nullptr;
     const float *KV = nullptr;     // [N, 2d]: K then V per node
-    const float *QP = nullptr;     // [V, d]: mu[r] * scale * Q_t Watt[r]^T per virtual segment
+    const float *QP = nullptr;     // [V, d]: mu[r] * scale * Q_t Watt[r]^T per virtual segment,
+                                   // or NULL: formed in the kernel from Q, Watt, mu, scale
+                                   // (when hgt_fused_query_fits)
+    const float *Q = nullptr, *Watt = nullptr, *mu = nullptr;
+    float scale = 1.f;
     const float *Wmsg = nullptr;
     int heads = 4;
     int d = 64;
@@ -294,6 +298,9 @@ struct HgtArgs {
                                    // destinations: written by the partial merge)
 };
 rgnn_status launch_hgt_traverse(const HgtArgs &a, hipStream_t s);
+// Whether the traversal can form the segment queries itself (d = 128, both
+// per-relation weight sets and the work-item stages in one workgroup's LDS).
+bool hgt_fused_query_fits(int R, int d, int heads);
 // Wqp[r] (d x d) = mu[r] * scale * blockdiag over heads i of Watt[r, i]^T, so
 // that Q_t Wqp[r] is the reordered query of segment (t, r).
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
