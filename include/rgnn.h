@@ -201,12 +201,15 @@ rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W, 
  *   softmax_scope RGNN_SOFTMAX_PER_DST_REL takes the softmax over the in-edges
  *   of v with relation r instead (each relation's messages are normalised on
  *   their own; out_v sums the relations): it runs the aggregate-first plan
- *   (heads == 1, d_in == d_out; size the workspace for
- *   RGNN_PLAN_AGGREGATE_FIRST) and returns RGNN_EUNSUPPORTED for
- *   RGNN_PLAN_TRANSFORM_FIRST; saved is then [num_dst_segments, 2], the
- *   (max, sum) of each (dst, rel) segment in (dst, rel) order, or NULL.
+ *   (d_in == d_out; size the workspace for RGNN_PLAN_AGGREGATE_FIRST with the
+ *   head count; several heads run one pass per head over the weights and
+ *   attention vectors with the other heads' columns zeroed, the outputs
+ *   summed) and returns RGNN_EUNSUPPORTED for RGNN_PLAN_TRANSFORM_FIRST;
+ *   saved is then [num_dst_segments, heads, 2], the (max, sum) of each
+ *   (dst, rel) segment in (dst, rel) order, or NULL.
  *   d_in, d_out in {64, 128}, or d_in = d_out = 32; d_out / heads a multiple of 16.
- *   RGNN_PLAN_AGGREGATE_FIRST requires heads == 1. */
+ *   RGNN_PLAN_AGGREGATE_FIRST requires heads == 1 with the per-destination
+ *   softmax. */
 rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
                          const float *w_src, const float *w_dst, int32_t d_in, int32_t d_out,
                          int32_t heads, float neg_slope, int32_t softmax_scope, int32_t plan,
@@ -231,8 +234,8 @@ rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, 
  * grad_out = dL/dout [N, d_out] and the forward's `saved`, writes dL/dh
  * [N, d_in], dL/dW [R, d_in, d_out], dL/dw_src and dL/dw_dst [R, d_out].
  * softmax_scope as in the forward: RGNN_SOFTMAX_PER_DST with saved
- * [N, heads, 2]; RGNN_SOFTMAX_PER_DST_REL (heads == 1) with the forward's
- * per-segment saved [num_dst_segments, 2].  d_in = d_out = 64, heads in {1, 2, 4}.
+ * [N, heads, 2]; RGNN_SOFTMAX_PER_DST_REL with the forward's per-segment
+ * saved [num_dst_segments, heads, 2].  d_in = d_out = 64, heads in {1, 2, 4}.
  * Several heads run as one pass per head over the weights, attention vectors
  * and grad_out with the other heads' columns zeroed (each head's logits,
  * softmax and messages read only its own columns, so the per-head gradients

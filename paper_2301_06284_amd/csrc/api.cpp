@@ -184,12 +184,33 @@ size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, vo
         x.wsm = c.take<float>(R * d_out);
         x.wdm = c.take<float>(R * d_out);
         x.Gm = c.take<float>(N * d_out);
-        x.sv = c.take<float>(N * 2);
+        x.sv = c.take<float>(std::max<size_t>(N, (size_t)g->U_dst) * 2);
         x.dh = c.take<float>(N * d_in);
         x.dW = c.take<float>(R * d_in * d_out);
         x.dws = c.take<float>(R * d_out);
         x.dwd = c.take<float>(R * d_out);
     }
+    if (w) *w = x;
+    return c.off;
+}
+
+// Softmax per (dst, rel) segment with several heads: the one-head
+// aggregate-first workspace plus the masked weights, one head's output and
+// its per-segment statistics.
+struct HeadsAfWs { float *Wm, *wsm, *wdm, *outk, *sk; void *inner; size_t inner_bytes; };
+size_t rgat_heads_af_layout(const rgnn_graph *g, int d, int H, void *base, HeadsAfWs *w)
+{
+    const size_t inner = rgat_layout(g, d, d, 1, RGNN_PLAN_AGGREGATE_FIRST, nullptr, nullptr);
+    Carver c(base);
+    HeadsAfWs x{};
+    x.inner = c.take<char>(inner);
+    x.inner_bytes = inner;
+    (void)H;
+    x.Wm = c.take<float>((size_t)g->R * d * d);
+    x.wsm = c.take<float>((size_t)g->R * d);
+    x.wdm = c.take<float>((size_t)g->R * d);
+    x.outk = c.take<float>((size_t)g->N * d);
+    x.sk = c.take<float>((size_t)std::max<int64_t>(g->U_dst, 1) * 2);
     if (w) *w = x;
     return c.off;
 }
@@ -323,8 +344,11 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
         *bytes = rgcn_layout(g, d_in, d_out, resolve_plan(g, layer, d_in, d_out, 1, plan), nullptr, nullptr);
         return RGNN_OK;
     case RGNN_LAYER_RGAT:
-        *bytes = rgat_layout(g, d_in, d_out, heads, resolve_plan(g, layer, d_in, d_out, heads, plan),
-                             nullptr, nullptr);
+        if (plan == RGNN_PLAN_AGGREGATE_FIRST && heads > 1)   // per-(dst, rel) softmax, several heads
+            *bytes = rgat_heads_af_layout(g, d_out, heads, nullptr, nullptr);
+        else
+            *bytes = rgat_layout(g, d_in, d_out, heads, resolve_plan(g, layer, d_in, d_out, heads, plan),
+                                 nullptr, nullptr);
         return RGNN_OK;
     case RGNN_LAYER_HGT:
         *bytes = hgt_layout(g, d_out, heads, nullptr, nullptr);
@@ -409,6 +433,10 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
 }
 
 // ------------------------------------------------------------------ RGAT
+rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *W, const float *w_src,
+                              const float *w_dst, int d_in, int d_out, int heads, float neg_slope, bool per_seg,
+                              int plan, float *out, float *saved, void *ws, size_t ws_bytes, hipStream_t s);
+
 extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
                                     const float *w_src, const float *w_dst, int32_t d_in,
                                     int32_t d_out, int32_t heads, float neg_slope,
@@ -433,16 +461,54 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         plan = RGNN_PLAN_AGGREGATE_FIRST;
     }
     plan = resolve_plan(g, RGNN_LAYER_RGAT, d_in, d_out, heads, plan);
-    if (plan == RGNN_PLAN_AGGREGATE_FIRST && (heads != 1 || d_in != d_out))
-        return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs heads == 1 and d_in == d_out");
     if (plan != RGNN_PLAN_AGGREGATE_FIRST && d_in != d_out)
         return fail(RGNN_EUNSUPPORTED, "RGAT needs d_in == d_out");
+    if (plan == RGNN_PLAN_AGGREGATE_FIRST && d_in != d_out)
+        return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs d_in == d_out");
+    if (plan == RGNN_PLAN_AGGREGATE_FIRST && heads != 1 && !per_seg)
+        return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT with several heads is for the softmax per "
+                                       "(destination, relation)");
+    hipStream_t s = (hipStream_t)stream;
+    if (heads == 1 || !per_seg)
+        return rgat_forward_impl(g, h, W, w_src, w_dst, d_in, d_out, heads, neg_slope, per_seg, plan, out,
+                                 saved, ws, ws_bytes, s);
+    // softmax per (dst, rel) segment with several heads: one masked one-head
+    // aggregate-first pass per head (head k reads only its columns of W_r,
+    // w_src[r] and w_dst[r], so the masked pass computes exactly head k's
+    // output columns and zeros elsewhere); outputs summed, statistics
+    // interleaved into saved [U_dst, heads, 2]
+    const size_t need = rgat_heads_af_layout(g, d_out, heads, nullptr, nullptr);
+    if (!ws || ws_bytes < need)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    HeadsAfWs w;
+    rgat_heads_af_layout(g, d_out, heads, ws, &w);
+    const int64_t R = g->R, N = g->N, dk = d_out / heads;
+    for (int k = 0; k < heads; ++k) {
+        const int c0 = (int)(k * dk), c1 = (int)((k + 1) * dk);
+        if ((st = launch_mask_cols(W, w.Wm, R * d_in, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
+        if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
+        float *ok = k ? w.outk : out;
+        if ((st = rgat_forward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, 1, neg_slope, true,
+                                    RGNN_PLAN_AGGREGATE_FIRST, ok, saved ? w.sk : nullptr, w.inner,
+                                    w.inner_bytes, s)) != RGNN_OK)
+            return st;
+        if (k && (st = launch_add(out, out, w.outk, N * d_out, s)) != RGNN_OK) return st;
+        if (saved && (st = launch_head_stats_scatter(w.sk, saved, g->U_dst, heads, k, s)) != RGNN_OK) return st;
+    }
+    return RGNN_OK;
+}
+
+rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *W, const float *w_src,
+                              const float *w_dst, int d_in, int d_out, int heads, float neg_slope, bool per_seg,
+                              int plan, float *out, float *saved, void *ws, size_t ws_bytes, hipStream_t s)
+{
+    rgnn_status st;
     const size_t need = rgat_layout(g, d_in, d_out, heads, plan, nullptr, nullptr);
     if (!ws || ws_bytes < need)
         return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
     RgatWs w;
     rgat_layout(g, d_in, d_out, heads, plan, ws, &w);
-    hipStream_t s = (hipStream_t)stream;
     // linear operator reordering: W_r w_dst[r] (and W_r w_src[r]) once per relation,
     // then the destination term h_v . (W_r w_dst[r]) once per (dst, rel) segment
     // (aggregate-first also needs W_r w_src[r]: both in one launch)
@@ -607,8 +673,6 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
         return fail(RGNN_EINVAL, "unknown softmax scope");
     const int per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
-    if (per_seg && heads != 1)
-        return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) has one head");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
     hipStream_t s = (hipStream_t)stream;
     const size_t need = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
@@ -627,11 +691,11 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
         if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_mask_cols(grad_out, w.Gm, N, d_out, c0, c1, s)) != RGNN_OK) return st;
-        if ((st = launch_head_stats(saved, w.sv, N, heads, k, s)) != RGNN_OK) return st;
+        if ((st = launch_head_stats(saved, w.sv, per_seg ? g->U_dst : N, heads, k, s)) != RGNN_OK) return st;
         // head 0 writes the outputs, the others add to them
         float *oh = k ? w.dh : grad_h, *oW = k ? w.dW : grad_W;
         float *os = k ? w.dws : grad_w_src, *od = k ? w.dwd : grad_w_dst;
-        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, 0, w.sv, w.Gm,
+        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, per_seg, w.sv, w.Gm,
                                      oh, oW, os, od, w.inner, w.inner_bytes, s, nullptr)) != RGNN_OK)
             return st;
         if (k) {

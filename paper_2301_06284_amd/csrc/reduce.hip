@@ -537,6 +537,14 @@ __global__ void mask_cols_kernel(const float *in, float *out, int64_t n, int d, 
     out[i] = (j >= c0 && j < c1) ? in[i] : 0.f;
 }
 
+// saved[v, k] = in[v] for the (max, sum) pairs of one head ([N, 2] -> [N, H, 2])
+__global__ void head_stats_scatter_kernel(const float *in, float *saved, int64_t N, int H, int k)
+{
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (v >= N) return;
+    *reinterpret_cast<float2 *>(saved + (v * H + k) * 2) = *reinterpret_cast<const float2 *>(in + v * 2);
+}
+
 // out[v] = saved[v, k] for the (max, sum) pairs of one head ([N, H, 2] -> [N, 2])
 __global__ void head_stats_kernel(const float *saved, float *out, int64_t N, int H, int k)
 {
@@ -743,6 +751,15 @@ rgnn_status launch_head_stats(const float *saved, float *out, int64_t N, int H, 
     hipLaunchKernelGGL(head_stats_kernel, dim3(blocks_for(N, 256)), dim3(256), 0, s, saved, out, N, H, k);
     hipError_t e = last();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "head_stats launch");
+}
+
+rgnn_status launch_head_stats_scatter(const float *in, float *saved, int64_t N, int H, int k, hipStream_t s)
+{
+    if (N == 0) return RGNN_OK;
+    LaunchScope ls("head_stats", s);
+    hipLaunchKernelGGL(head_stats_scatter_kernel, dim3(blocks_for(N, 256)), dim3(256), 0, s, in, saved, N, H, k);
+    hipError_t e = last();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "head_stats_scatter launch");
 }
 
 rgnn_status launch_reorder_vec(const float *W, int R, int d_in, int d_out, int heads,

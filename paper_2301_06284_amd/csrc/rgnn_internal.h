@@ -148,8 +148,9 @@ int bwd_outer_rows();
 rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s);
 // out [rows, d] = in with the columns outside [c0, c1) set to 0
 rgnn_status launch_mask_cols(const float *in, float *out, int64_t rows, int d, int c0, int c1, hipStream_t s);
-// out [N, 2] = saved [N, H, 2] of head k
+// out [N, 2] = saved [N, H, 2] of head k, and the converse
 rgnn_status launch_head_stats(const float *saved, float *out, int64_t N, int H, int k, hipStream_t s);
+rgnn_status launch_head_stats_scatter(const float *in, float *saved, int64_t N, int H, int k, hipStream_t s);
 
 // ---- profiling (api.cpp) ----
 struct LaunchScope {   // records a hipEvent pair around one kernel launch when profiling

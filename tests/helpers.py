@@ -87,7 +87,7 @@ class Runner:
         if scope == 0:
             saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev)
         elif want_saved:   # per (dst, rel) segment
-            saved = torch.full((self.G.info()["num_dst_segments"], 2), float("nan"), device=self.dev)
+            saved = torch.full((self.G.info()["num_dst_segments"], heads, 2), float("nan"), device=self.dev)
         ws_plan = 2 if scope == 1 else plan   # per-(dst, rel) softmax runs aggregate-first
         self.rgnn.rgat_forward(self.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, saved,
                                self.ws(1, d_in, d_out, heads, ws_plan), d_in, d_out, heads, slope,

@@ -247,9 +247,6 @@ def test_rgat_per_relation_softmax_rejects():
     with pytest.raises(rgnn.RgnnError, match="aggregate-first"):
         rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
                           softmax_scope=rgnn.SOFTMAX_PER_DST_REL, plan=rgnn.PLAN_TRANSFORM_FIRST)
-    with pytest.raises(rgnn.RgnnError, match="heads"):
-        rgnn.rgat_forward(run.G, T["h"], T["W"], T["w_src"], T["w_dst"], out, None, ws, 64, 64,
-                          heads=2, softmax_scope=rgnn.SOFTMAX_PER_DST_REL)
     run.close()
 
 
@@ -354,6 +351,32 @@ def test_rgat_backward_per_relation_softmax(kind):
     assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
 
 
+@pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
+@pytest.mark.parametrize("heads", [2, 4])
+def test_rgat_per_relation_softmax_multihead(kind, heads):
+    """Softmax per (dst, rel) segment with several heads: forward and
+    backward as one masked one-head pass per head, against the oracle."""
+    g = graph(kind, E=3000)
+    t = workloads.tiny_tensors(50, g, 64, 64, heads=heads, att_var=1.0)
+    print(f"rgat per-relation softmax {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got, saved = run.rgat(heads=heads, scope=1, want_saved=True)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads, scope=1)
+    assert row_err(got, ref) <= TOL
+    sv = saved.cpu().numpy()
+    if len(sv):
+        assert np.isfinite(sv).all() and (sv[..., 1] >= 1 - 1e-5).all()
+    gh, gW, gs, gt = run.rgat_backward(heads=heads, scope=1)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                            heads=heads, scope=1)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64), cancel_floor=1e-6) <= TOL
+    assert row_err(gs, dws, cancel_floor=1e-6) <= TOL
+    assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
+
+
 def test_rgat_backward_per_relation_softmax_hub_segments():
     """Segments cut into many pieces (one relation, a 5000-edge hub: more
     than 32 pieces in one segment) and destinations split over work items."""
@@ -363,7 +386,7 @@ def test_rgat_backward_per_relation_softmax_hub_segments():
     run = Runner(g, t)
     _, saved = run.rgat(scope=1, want_saved=True)
     sv = saved.cpu().numpy()
-    assert np.isfinite(sv).all() and (sv[:, 1] >= 1 - 1e-5).all()
+    assert np.isfinite(sv).all() and (sv[..., 1] >= 1 - 1e-5).all()
     gh, gW, gs, gt = run.rgat_backward(scope=1)
     run.close()
     dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
