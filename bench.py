@@ -487,6 +487,28 @@ def main():
                 "edges_per_s": c.info["num_edges"] / (m4 * 1e-3), "ms": m4, "plan": names[p4],
                 "kernels_ms": {k: round(v[1], 4) for k, v in k4.items()}}
             del ws
+        # backward at d = 128 (the loss weight of the workload's generator)
+        N4, R4 = c.info["num_nodes"], c.info["num_rels"]
+        saved4 = torch.empty(N4, 1, 2, device=c.dev)
+        ws = c.ws(rgnn.LAYER_RGAT, d4, d4, 1)
+        rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, saved4, ws, d4, d4)
+        del ws
+        gh = torch.empty(N4, d4, device=c.dev)
+        gW, gs, gt = (torch.empty(R4, d4, d4, device=c.dev), torch.empty(R4, d4, device=c.dev),
+                      torch.empty(R4, d4, device=c.dev))
+        ws = c.ws(rgnn.LAYER_RGAT_BACKWARD, d4, d4)
+        fb4 = lambda: rgnn.rgat_backward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], saved4,
+                                         c.T["grad_out"], gh, gW, gs, gt, ws, d4, d4)
+        mb4 = time_steps(torch, fb4, K, W)
+        layers["rgat_bwd_wikikg2_like_2p5m_d128"] = {"edges_per_s": c.info["num_edges"] / (mb4 * 1e-3), "ms": mb4}
+        del ws
+        gW0 = torch.empty(d4, d4, device=c.dev)
+        ws = c.ws(rgnn.LAYER_RGCN_BACKWARD, d4, d4)
+        fr4 = lambda: rgnn.rgcn_backward(c.G, c.T["h"], c.T["W"], c.T["W0"], None, c.T["grad_out"], gh, gW,
+                                         gW0, ws, d4, d4, 0)
+        mr4 = time_steps(torch, fr4, K, W)
+        layers["rgcn_bwd_wikikg2_like_2p5m_d128"] = {"edges_per_s": c.info["num_edges"] / (mr4 * 1e-3), "ms": mr4}
+        del ws, gh, gW, gs, gt, gW0, saved4
         c.close()
         del out
 

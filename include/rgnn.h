@@ -235,7 +235,8 @@ rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, 
  * [N, d_in], dL/dW [R, d_in, d_out], dL/dw_src and dL/dw_dst [R, d_out].
  * softmax_scope as in the forward: RGNN_SOFTMAX_PER_DST with saved
  * [N, heads, 2]; RGNN_SOFTMAX_PER_DST_REL with the forward's per-segment
- * saved [num_dst_segments, heads, 2].  d_in = d_out = 64, heads in {1, 2, 4}.
+ * saved [num_dst_segments, heads, 2].  d_in = d_out in {32, 64, 128}, d_out / heads
+ * a multiple of 16.
  * Several heads run as one pass per head over the weights, attention vectors
  * and grad_out with the other heads' columns zeroed (each head's logits,
  * softmax and messages read only its own columns, so the per-head gradients
@@ -259,7 +260,7 @@ rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, const float *W,
  *   output [N, d_out], which gives act' = [out > 0]; otherwise out may be NULL),
  *   grad_out [N, d_out]; writes grad_h [N, d_in], grad_W [R, d_in, d_out] and,
  *   when W0 and grad_W0 are both given, grad_W0 [d_in, d_out].
- *   d_in = d_out = 64.  Workspace: rgnn_workspace_size(RGNN_LAYER_RGCN_BACKWARD).
+ *   d_in = d_out in {32, 64, 128}.  Workspace: rgnn_workspace_size(RGNN_LAYER_RGCN_BACKWARD).
  *   Results are reproducible except the rows of sources with more than 64
  *   out-edges, which are summed with float atomics. */
 rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W, const float *W0,

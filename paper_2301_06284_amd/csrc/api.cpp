@@ -667,9 +667,10 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
         return fail(RGNN_EINVAL, "NULL tensor pointer");
     if (!saved && (softmax_scope == RGNN_SOFTMAX_PER_DST_REL ? g->U_dst : g->N) > 0)
         return fail(RGNN_EINVAL, "saved is NULL");
-    if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d = 64");
-    if (heads != 1 && heads != 2 && heads != 4)
-        return fail(RGNN_EUNSUPPORTED, "RGAT backward heads must be 1, 2 or 4");
+    if (d_in != d_out || (d_in != 32 && d_in != 64 && d_in != 128))
+        return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d_in = d_out in {32, 64, 128}");
+    if (heads <= 0 || d_out % heads || (d_out / heads) % 16)
+        return fail(RGNN_EUNSUPPORTED, "RGAT backward heads must give d_out / heads a multiple of 16");
     if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
         return fail(RGNN_EINVAL, "unknown softmax scope");
     const int per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
@@ -742,7 +743,8 @@ extern "C" rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, cons
     if (st != RGNN_OK) return st;
     if (!h || !W || !grad_out || !grad_h || !grad_W) return fail(RGNN_EINVAL, "NULL tensor pointer");
     if (flags & ~RGNN_FLAG_RELU) return fail(RGNN_EINVAL, "unknown RGCN flag");
-    if (d_in != 64 || d_out != 64) return fail(RGNN_EUNSUPPORTED, "RGCN backward supports d = 64");
+    if (d_in != d_out || (d_in != 32 && d_in != 64 && d_in != 128))
+        return fail(RGNN_EUNSUPPORTED, "RGCN backward supports d_in = d_out in {32, 64, 128}");
     if ((flags & RGNN_FLAG_RELU) && !out)
         return fail(RGNN_EINVAL, "RGCN backward with ReLU needs the forward output");
     return rgcn_backward_impl(g, h, W, W0, d_in, d_out, flags, out, grad_out, grad_h, grad_W,

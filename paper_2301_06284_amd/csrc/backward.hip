@@ -1,5 +1,5 @@
 // backward.hip -- RGAT backward pass (Section "Backward Propagation") for one
-// head and d = 64, softmax over each destination's in-edges, or over each
+// head and d in {32, 64, 128}, softmax over each destination's in-edges, or over each
 // (destination, relation) segment (the per-relation variant: M, Z and s below
 // are then per segment).
 //
@@ -46,8 +46,10 @@ namespace rgnn {
 
 namespace {
 
-constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
+// threads per workgroup of the item traversals at width D: 16 items per
+// workgroup (their LDS stages), so 128 threads at d = 32
+constexpr int item_threads(int D) { return D == 32 ? 128 : 256; }
 constexpr int kU = 4;              // rows per prefetch batch in the traversals
 constexpr int kOuterRows = 2048;   // segments per outer-product K-chunk
 
@@ -106,10 +108,10 @@ struct BStage {
 //          writing each vseg's part of s to svs and parking (alpha, dalpha);
 //          once the parts are summed per segment, PHASE 1 runs passes 2 and 3
 //          for every item (pass 3 for whole destinations only).
-template <int PHASE, bool SEG>
-__global__ __launch_bounds__(256) void bwd_traverse_kernel(BK k)
+template <int D, int PHASE, bool SEG>
+__global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
 {
-    constexpr int GPB = 256 / G;
+    constexpr int G = D / 4, GPB = item_threads(D) / G;
     __shared__ BStage<SEG> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     BStage<SEG> &st = stage[gi];
@@ -386,13 +388,13 @@ __global__ __launch_bounds__(256) void merge_seg_s_big_kernel(const int32_t *big
 // 16-lane groups (U in flight) and combined in group order.  Destinations
 // split over more than kBigRange items (the hubs) take 1024-thread
 // workgroups in a launch of their own (BIG).
-template <int NTH, int U, bool BIG>
+template <int D, int NTH, int U, bool BIG>
 __global__ __launch_bounds__(NTH) void split_dst_term_kernel(const int32_t *big_split, const int32_t *split_slotptr,
                                                              const int32_t *split_dst, const int32_t *dst_vsegptr,
                                                              const int32_t *vseg_rel, const int32_t *vseg_pos,
                                                              const float *ysum, const float *wtp, float *dh)
 {
-    constexpr int NG = NTH / G;
+    constexpr int G = D / 4, NG = NTH / G;
     __shared__ float4 part[NG][G];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     const int i = BIG ? big_split[blockIdx.x] : (int)blockIdx.x;
@@ -443,9 +445,10 @@ struct SStage {
     int optr[kDst + 1];  // item-local first out-edge of each source
 };
 
-__global__ __launch_bounds__(256) void bwd_src_kernel(SK k)
+template <int D>
+__global__ __launch_bounds__(item_threads(D)) void bwd_src_kernel(SK k)
 {
-    constexpr int GPB = 256 / G;
+    constexpr int G = D / 4, GPB = item_threads(D) / G;
     __shared__ SStage stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     SStage &st = stage[gi];
@@ -535,10 +538,11 @@ __global__ __launch_bounds__(256) void bwd_src_kernel(SK k)
 // pvec[t] = sum over the compact pairs of tile t (one relation) of
 // ypair[pair] * h[src(pair)]; lanes of 16-lane groups over features, groups
 // over pairs, combined in group order.
+template <int D>
 __global__ __launch_bounds__(256) void pair_gemv_kernel(const Tile *tiles, const int32_t *uniq_src,
                                                         const float *ypair, const float *h, float *pvec)
 {
-    constexpr int NG = 256 / G;
+    constexpr int G = D / 4, NG = 256 / G;
     __shared__ float4 part[NG][G];
     const Tile t = tiles[blockIdx.x];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
@@ -574,7 +578,9 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // YS: also sum ysum[row] * h[v] per chunk (the RGAT dwt' term); GATHER: the
 // second operand's row (and h's) is vsegdst[row], else the row itself; GA:
 // the first operand's row is gathered the same way.  lda, ldb: row strides.
-template <bool YS, bool GATHER, bool GA>
+// A workgroup computes one 64 x 64 tile of the D x D product (blockIdx.y: the
+// tile, four at D = 128); at D = 32 the columns past D read as zeros.
+template <int D, bool YS, bool GATHER, bool GA>
 __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
                                                          const float *Sa, int lda,
                                                          const float *Gm, int ldb, const float *h,
@@ -583,13 +589,19 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
 {
     constexpr int KB = 64, P = 68;
     constexpr int SL = KB * 16 / 256;   // float4 slots of each operand per thread and step
+    constexpr int NT = D > 64 ? D / 64 : 1;   // tiles per side
     __shared__ float As[KB * P];
     __shared__ float Bs[KB * P];
     __shared__ float4 yred[256];
     const Tile t = chunks[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int li = lane & 15, q = lane >> 4;
+    const int a0 = NT > 1 ? 64 * ((int)blockIdx.y / NT) : 0;   // tile origin
+    const int b0 = NT > 1 ? 64 * ((int)blockIdx.y % NT) : 0;
     const int c4 = (tid & 15) * 4;      // this thread's columns in every slot
+    constexpr bool FULL = D >= 64;      // every tile column is a column of the product
+    const bool aok = FULL || a0 + c4 < D, bok = FULL || b0 + c4 < D;
+    const bool ys = YS && b0 == 0;      // the dwt' sum once per A column range
     floatx4 acc[4];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -613,10 +625,10 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
 #pragma unroll
         for (int sl = 0; sl < SL; ++sl) {
             const int row = row_of(k0, sl);
-            ra[sl] = ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + c4);
-            rb[sl] = ld4(Gm + (size_t)v[sl] * ldb + c4);
+            ra[sl] = aok ? ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + a0 + c4) : zero4();
+            rb[sl] = bok ? ld4(Gm + (size_t)v[sl] * ldb + b0 + c4) : zero4();
             if (YS) {
-                rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
+                rh[sl] = ys && aok ? ld4(h + (size_t)v[sl] * D + a0 + c4) : zero4();
                 ry[sl] = ysum[row];
             }
         }
@@ -650,20 +662,24 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) out[(size_t)(w * 16 + q * 4 + v) * D + cb * 16 + li] = acc[cb][v];
-    if (YS) {
+        for (int v = 0; v < 4; ++v) {
+            const int i = a0 + w * 16 + q * 4 + v, jc = b0 + cb * 16 + li;
+            if (FULL || (i < D && jc < D)) out[(size_t)i * D + jc] = acc[cb][v];
+        }
+    if (ys) {
         yred[tid] = yacc;
         __syncthreads();
-        if (tid < 16) {
+        if (tid < 16 && (FULL || a0 + tid * 4 < D)) {
             float4 s = zero4();
             for (int i = tid; i < 256; i += 16) s = add4(s, yred[i]);
-            st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
+            st4(yvec + (size_t)blockIdx.x * D + a0 + tid * 4, s);
         }
     }
 }
 
 // Per relation r: pws = sum of r's pair-tile vectors, pwt = sum of r's
 // segment-chunk vectors, both in a fixed order.
+template <int D>
 __global__ __launch_bounds__(1024) void bwd_reduce_kernel(const float *pvec, const int32_t *rel_pairtileptr,
                                                           const float *yvec, const int32_t *rel_chunkptr,
                                                           float *pws, float *pwt)
@@ -688,7 +704,7 @@ __global__ __launch_bounds__(1024) void bwd_reduce_kernel(const float *pvec, con
 // Per relation r (blockIdx.x) and 256 entries of dW_r (blockIdx.y): combine
 // chunk partials in order, add the rank-1 attention terms; dw_src, dw_dst.
 // ATT false: only the ordered sum of the chunk partials (dW of RGCN).
-template <bool ATT>
+template <int D, bool ATT>
 __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial, const int32_t *rel_chunkptr,
                                                            const float *pws_all, const float *pwt_all,
                                                            const float *W, const float *w_src,
@@ -742,7 +758,7 @@ struct BwdWs {
     float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *svs, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
 };
 
-size_t bwd_layout(const rgnn_graph *g, void *base, BwdWs *w)
+size_t bwd_layout(const rgnn_graph *g, int D, void *base, BwdWs *w)
 {
     char *b = (char *)base;
     size_t off = 0;
@@ -781,70 +797,84 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
     return hipGetLastError();
 }
 
+template <int D>
 void launch_split_dst_term(const rgnn_graph *g, const float *ysum, const float *wtp, float *dh, hipStream_t s)
 {
     const DeviceIndex &x = g->dev;
-    hipLaunchKernelGGL((split_dst_term_kernel<256, 4, false>), dim3((unsigned)g->n_split), dim3(256), 0, s,
+    hipLaunchKernelGGL((split_dst_term_kernel<D, 256, 4, false>), dim3((unsigned)g->n_split), dim3(256), 0, s,
                        nullptr, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, ysum, wtp, dh);
     if (g->n_big_split)
-        hipLaunchKernelGGL((split_dst_term_kernel<1024, 8, true>), dim3((unsigned)g->n_big_split), dim3(1024), 0,
-                           s, x.big_split, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos,
+        hipLaunchKernelGGL((split_dst_term_kernel<D, 1024, 8, true>), dim3((unsigned)g->n_big_split), dim3(1024),
+                           0, s, x.big_split, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos,
                            ysum, wtp, dh);
 }
+
+// 64 x 64 tiles of the D x D outer products
+constexpr unsigned outer_tiles(int D) { return D > 64 ? (unsigned)(D / 64) * (D / 64) : 1u; }
 
 }  // namespace
 
 int bwd_outer_rows() { return kOuterRows; }
 
+template <int D>
+void outer_chunks_d(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x, const float *X,
+                    int ldx, const float *Gm, int ldg, float *partial, hipStream_t s)
+{
+    const dim3 grid((unsigned)nchunks, outer_tiles(D));
+    if (gather && gather_x)
+        hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, true>), grid, dim3(256), 0, s,
+                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    else if (gather)
+        hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, false>), grid, dim3(256), 0, s,
+                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    else
+        hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, false>), grid, dim3(256), 0, s,
+                           chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+}
+
 rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x,
-                                const float *X, int ldx, const float *Gm, int ldg, float *partial,
+                                const float *X, int ldx, const float *Gm, int ldg, float *partial, int d,
                                 hipStream_t s)
 {
     if (nchunks == 0) return RGNN_OK;
     {
         LaunchScope ls("outer_gemm", s);
-        const dim3 grid((unsigned)nchunks);
-        if (gather && gather_x)
-            hipLaunchKernelGGL((outer_gemm_kernel<false, true, true>), grid, dim3(256), 0, s,
-                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
-        else if (gather)
-            hipLaunchKernelGGL((outer_gemm_kernel<false, true, false>), grid, dim3(256), 0, s,
-                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
-        else
-            hipLaunchKernelGGL((outer_gemm_kernel<false, false, false>), grid, dim3(256), 0, s,
-                               chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        if (d == 32) outer_chunks_d<32>(chunks, nchunks, gather, gather_x, X, ldx, Gm, ldg, partial, s);
+        else if (d == 64) outer_chunks_d<64>(chunks, nchunks, gather, gather_x, X, ldx, Gm, ldg, partial, s);
+        else if (d == 128) outer_chunks_d<128>(chunks, nchunks, gather, gather_x, X, ldx, Gm, ldg, partial, s);
+        else return fail(RGNN_EUNSUPPORTED, "outer products: d must be 32, 64 or 128");
     }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "outer_gemm launch");
 }
 
-rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW,
+rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s)
 {
     if (R == 0) return RGNN_OK;
     {
         LaunchScope ls("chunk_sum", s);
-        hipLaunchKernelGGL((bwd_finalize_kernel<false>), dim3((unsigned)R, D * D / 256), dim3(256), 0, s,
-                           partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr,
-                           nullptr);
+#define CS(D) hipLaunchKernelGGL((bwd_finalize_kernel<D, false>), dim3((unsigned)R, D * D / 256), dim3(256), 0, s, \
+                                 partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr, nullptr)
+        if (d == 32) CS(32);
+        else if (d == 64) CS(64);
+        else if (d == 128) CS(128);
+        else return fail(RGNN_EUNSUPPORTED, "chunk sums: d must be 32, 64 or 128");
+#undef CS
     }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "chunk_sum launch");
 }
 
-rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
-                               const float *w_src, const float *w_dst, int d_in, int d_out,
-                               float slope, int per_seg, const float *saved, const float *Gm,
-                               float *dh, float *dW, float *dws, float *dwt, void *ws,
-                               size_t ws_bytes, hipStream_t s, size_t *need)
+namespace {
+
+template <int D>
+rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W, const float *w_src,
+                            const float *w_dst, float slope, int per_seg, const float *saved, const float *Gm,
+                            float *dh, float *dW, float *dws, float *dwt, void *ws, hipStream_t s)
 {
-    const size_t bytes = bwd_layout(g, nullptr, nullptr);
-    if (need) { *need = bytes; return RGNN_OK; }
-    if (d_in != D || d_out != D) return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d = 64");
-    if (!ws || ws_bytes < bytes)
-        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
     BwdWs w;
-    bwd_layout(g, ws, &w);
+    bwd_layout(g, D, ws, &w);
     rgnn_status st;
     hipError_t e;
     if ((st = launch_reorder_vec(W, g->R, D, D, 1, w_src, w.wsp, w_dst, w.wtp, s)) != RGNN_OK) return st;
@@ -869,10 +899,11 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
     k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs;
     if (g->n_items && per_seg) {
-        const dim3 grid((unsigned)((g->n_items + 15) / 16));
+        constexpr int GPB = item_threads(D) / (D / 4);
+        const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
         {
             LaunchScope ls("rgat_bwd_traverse", s);
-            hipLaunchKernelGGL((bwd_traverse_kernel<0, true>), grid, dim3(256), 0, s, k);
+            hipLaunchKernelGGL((bwd_traverse_kernel<D, 0, true>), grid, dim3(item_threads(D)), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         {
@@ -887,19 +918,20 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_seg_s launch");
         {
             LaunchScope ls("rgat_bwd_traverse_seg", s);
-            hipLaunchKernelGGL((bwd_traverse_kernel<1, true>), grid, dim3(256), 0, s, k);
+            hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, true>), grid, dim3(item_threads(D)), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
             LaunchScope ls("rgat_bwd_split_dst_term", s);
-            launch_split_dst_term(g, w.ysum, w.wtp, dh, s);
+            launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, s);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
     } else if (g->n_items) {
-        const dim3 grid((unsigned)((g->n_items + 15) / 16));
+        constexpr int GPB = item_threads(D) / (D / 4);
+        const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
         {
             LaunchScope ls("rgat_bwd_traverse", s);
-            hipLaunchKernelGGL((bwd_traverse_kernel<0, false>), grid, dim3(256), 0, s, k);
+            hipLaunchKernelGGL((bwd_traverse_kernel<D, 0, false>), grid, dim3(item_threads(D)), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
@@ -917,12 +949,12 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
             {
                 LaunchScope ls("rgat_bwd_traverse_split", s);
-                hipLaunchKernelGGL((bwd_traverse_kernel<1, false>), grid, dim3(256), 0, s, k);
+                hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, false>), grid, dim3(item_threads(D)), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
             {
                 LaunchScope ls("rgat_bwd_split_dst_term", s);
-                launch_split_dst_term(g, w.ysum, w.wtp, dh, s);
+                launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, s);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
         }
@@ -935,35 +967,57 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
         sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.out_rel = g->dev.out_rel;
         sk.out_pair = g->dev.out_pair; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.ypair = w.ypair;
         LaunchScope ls("rgat_bwd_src", s);
-        hipLaunchKernelGGL(bwd_src_kernel, dim3((unsigned)((g->n_oitems + 15) / 16)), dim3(256), 0, s, sk);
+        constexpr int GPB = item_threads(D) / (D / 4);
+        hipLaunchKernelGGL(bwd_src_kernel<D>, dim3((unsigned)((g->n_oitems + GPB - 1) / GPB)), dim3(item_threads(D)),
+                           0, s, sk);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_src launch");
     if (g->n_tiles_pairs) {   // dws' per pair tile
         LaunchScope ls("rgat_bwd_pair_gemv", s);
-        hipLaunchKernelGGL(pair_gemv_kernel, dim3((unsigned)g->n_tiles_pairs), dim3(256), 0, s,
+        hipLaunchKernelGGL(pair_gemv_kernel<D>, dim3((unsigned)g->n_tiles_pairs), dim3(256), 0, s,
                            g->dev.tiles_pairs, g->dev.uniq_src, w.ypair, h, w.pvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "pair_gemv launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
-        hipLaunchKernelGGL((outer_gemm_kernel<true, true, false>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
+        hipLaunchKernelGGL((outer_gemm_kernel<D, true, true, false>), dim3((unsigned)g->n_tiles_outer, outer_tiles(D)),
+                           dim3(256), 0, s,
                            g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, D, Gm, D, h, w.ysum,
                            w.partial, w.yvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");
     {
         LaunchScope ls("rgat_bwd_reduce", s);
-        hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g->R), dim3(1024), 0, s, w.pvec,
+        hipLaunchKernelGGL(bwd_reduce_kernel<D>, dim3((unsigned)g->R), dim3(1024), 0, s, w.pvec,
                            g->dev.rel_pairtileptr, w.yvec, g->dev.rel_chunkptr, w.pws, w.pwt);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_reduce launch");
     {
         LaunchScope ls("rgat_bwd_finalize", s);
-        hipLaunchKernelGGL((bwd_finalize_kernel<true>), dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
+        hipLaunchKernelGGL((bwd_finalize_kernel<D, true>), dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
                            g->dev.rel_chunkptr, w.pws, w.pwt, W, w_src, w_dst, dW, dws, dwt);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "finalize launch");
     return RGNN_OK;
+}
+
+}  // namespace
+
+rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float *W,
+                               const float *w_src, const float *w_dst, int d_in, int d_out,
+                               float slope, int per_seg, const float *saved, const float *Gm,
+                               float *dh, float *dW, float *dws, float *dwt, void *ws,
+                               size_t ws_bytes, hipStream_t s, size_t *need)
+{
+    const size_t bytes = bwd_layout(g, d_in, nullptr, nullptr);
+    if (need) { *need = bytes; return RGNN_OK; }
+    if (d_in != d_out || (d_in != 32 && d_in != 64 && d_in != 128))
+        return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d_in = d_out in {32, 64, 128}");
+    if (!ws || ws_bytes < bytes)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
+    if (d_in == 32) return rgat_backward_d<32>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
+    if (d_in == 64) return rgat_backward_d<64>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
+    return rgat_backward_d<128>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
 }
 
 }  // namespace rgnn

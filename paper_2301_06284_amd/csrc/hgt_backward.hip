@@ -427,9 +427,9 @@ rgnn_status type_outer(const rgnn_graph *g, const float *X, int ldx, const float
                        float *dW, hipStream_t s)
 {
     rgnn_status st = launch_outer_chunks(g->dev.tiles_types_outer, g->n_tiles_types_outer, g->dev.ntype_perm, 1,
-                                         X, ldx, Y, ldy, chunks, s);
+                                         X, ldx, Y, ldy, chunks, D, s);
     if (st != RGNN_OK) return st;
-    return launch_chunk_sum(chunks, g->dev.types_chunkptr, g->T, dW, s);
+    return launch_chunk_sum(chunks, g->dev.types_chunkptr, g->T, dW, D, s);
 }
 
 }  // namespace
@@ -545,16 +545,16 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
     if ((st = launch_vseg_reduce(g, w.Tq, nullptr, D, w.dQ, 0, 0, s)) != RGNN_OK) return st;
     if (g->V > 0) {
         if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, 0, w.dQP, D, w.Q,
-                                      D, w.chunks, s)) != RGNN_OK)
+                                      D, w.chunks, D, s)) != RGNN_OK)
             return st;
     }
-    if ((st = launch_chunk_sum(w.chunks, g->dev.rel_chunkptr, g->R, w.OT, s)) != RGNN_OK) return st;
+    if ((st = launch_chunk_sum(w.chunks, g->dev.rel_chunkptr, g->R, w.OT, D, s)) != RGNN_OK) return st;
     if (g->V > 0) {
         if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, 0, w.Sal, D, dagg,
-                                      D, w.chunks, s)) != RGNN_OK)
+                                      D, w.chunks, D, s)) != RGNN_OK)
             return st;
     }
-    if ((st = launch_chunk_sum(w.chunks, g->dev.rel_chunkptr, g->R, w.M2, s)) != RGNN_OK) return st;
+    if ((st = launch_chunk_sum(w.chunks, g->dev.rel_chunkptr, g->R, w.M2, D, s)) != RGNN_OK) return st;
     if (g->R > 0) {
         {
             LaunchScope ls("hgt_bwd_rel", s);

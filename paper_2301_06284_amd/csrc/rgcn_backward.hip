@@ -1,7 +1,7 @@
 // rgcn_backward.hip -- RGCN backward pass for the loss L = sum(out * G), the
 // chain rule applied to the paper's RGCN equation (Section "Backward
 // Propagation" generates it from the forward; here it is written out), for
-// d_in = d_out = 64.  With the pre-activation P and Gp = G * act'(P):
+// d_in = d_out in {32, 64, 128}.  With the pre-activation P and Gp = G * act'(P):
 //   dS_seg = Gp_v W_r^T / c_{v,r}            per virtual segment (v, r)
 //   dh_u   = sum over u's out-edges of dS_seg(e)  +  Gp_u W0^T
 //   dW_r   = sum over r's segments of Sbar_seg^T Gp_v,  Sbar_seg = (1/c) sum_{u in seg} h_u
@@ -23,7 +23,6 @@ namespace rgnn {
 
 namespace {
 
-constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 constexpr int kU = 4;   // dS rows per prefetch batch
 
@@ -52,13 +51,14 @@ struct RStage {
     int optr[kDst + 1];  // item-local first out-edge of each source
 };
 
-// dh_u += sum of the dS rows of u's out-edges; one group of 16 lanes per
+// dh_u += sum of the dS rows of u's out-edges; one group of D/4 lanes per
 // out-edge work item (bundles of small sources or pieces of large ones).
+template <int D>
 __global__ __launch_bounds__(256) void rgcn_bwd_src_kernel(int64_t n_items, const Item *items,
                                                            const int32_t *out_ptr, const int32_t *out_vseg,
                                                            const float *dS, float *dh)
 {
-    constexpr int GPB = 256 / G;
+    constexpr int G = D / 4, GPB = 256 / G;
     __shared__ RStage stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     RStage &st = stage[gi];
@@ -137,7 +137,7 @@ inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct RgcnBwdWs { float *Gp, *dS, *Sb, *partial; };
 
-size_t rgcn_bwd_layout(const rgnn_graph *g, void *base, RgcnBwdWs *w)
+size_t rgcn_bwd_layout(const rgnn_graph *g, int D, void *base, RgcnBwdWs *w)
 {
     char *b = (char *)base;
     size_t off = 0;
@@ -156,22 +156,14 @@ size_t rgcn_bwd_layout(const rgnn_graph *g, void *base, RgcnBwdWs *w)
     return off;
 }
 
-}  // namespace
-
-rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float *W, const float *W0,
-                               int d_in, int d_out, int flags, const float *out, const float *Gm,
-                               float *dh, float *dW, float *dW0, void *ws, size_t ws_bytes,
-                               hipStream_t s, size_t *need)
+template <int D>
+rgnn_status rgcn_backward_d(const rgnn_graph *g, const float *h, const float *W, const float *W0, int relu,
+                            const float *out, const float *Gm, float *dh, float *dW, float *dW0, void *ws,
+                            hipStream_t s)
 {
-    const int relu = (flags & RGNN_FLAG_RELU) ? 1 : 0;
-    const size_t bytes = rgcn_bwd_layout(g, nullptr, nullptr);
-    if (need) { *need = bytes; return RGNN_OK; }
-    if (d_in != D || d_out != D) return fail(RGNN_EUNSUPPORTED, "RGCN backward supports d = 64");
-    if (relu && !out) return fail(RGNN_EINVAL, "RGCN backward with ReLU needs the forward output");
-    if (!ws || ws_bytes < bytes)
-        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
+    constexpr int G = D / 4;
     RgcnBwdWs w;
-    rgcn_bwd_layout(g, ws, &w);
+    rgcn_bwd_layout(g, D, ws, &w);
     rgnn_status st;
     hipError_t e;
     const float *Gp = Gm;
@@ -212,7 +204,7 @@ rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float 
     if (g->n_oitems > 0) {
         {
             LaunchScope ls("rgcn_bwd_src", s);
-            hipLaunchKernelGGL(rgcn_bwd_src_kernel, dim3(blocks_for(g->n_oitems, 256 / G)), dim3(256), 0, s,
+            hipLaunchKernelGGL(rgcn_bwd_src_kernel<D>, dim3(blocks_for(g->n_oitems, 256 / G)), dim3(256), 0, s,
                                g->n_oitems, g->dev.oitems, g->dev.out_ptr, g->dev.out_vseg, w.dS, dh);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgcn_bwd_src launch");
@@ -223,18 +215,38 @@ rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float 
         fa.g = g; fa.h = h; fa.d_in = D; fa.d_out = D; fa.S = w.Sb;
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
         if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, 0, w.Sb, D,
-                                      Gp, D, w.partial, s)) != RGNN_OK)
+                                      Gp, D, w.partial, D, s)) != RGNN_OK)
             return st;
     }
-    if ((st = launch_chunk_sum(w.partial, g->dev.rel_chunkptr, g->R, dW, s)) != RGNN_OK) return st;
+    if ((st = launch_chunk_sum(w.partial, g->dev.rel_chunkptr, g->R, dW, D, s)) != RGNN_OK) return st;
     // dW0 = sum_v h_v^T Gp_v
     if (W0 && dW0) {
         if ((st = launch_outer_chunks(g->dev.tiles_nodes_outer, g->n_tiles_nodes_outer, nullptr, 0, h, D, Gp,
-                                      D, w.partial, s)) != RGNN_OK)
+                                      D, w.partial, D, s)) != RGNN_OK)
             return st;
-        if ((st = launch_chunk_sum(w.partial, g->dev.nodes_chunkptr, 1, dW0, s)) != RGNN_OK) return st;
+        if ((st = launch_chunk_sum(w.partial, g->dev.nodes_chunkptr, 1, dW0, D, s)) != RGNN_OK) return st;
     }
     return RGNN_OK;
+}
+
+}  // namespace
+
+rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float *W, const float *W0,
+                               int d_in, int d_out, int flags, const float *out, const float *Gm,
+                               float *dh, float *dW, float *dW0, void *ws, size_t ws_bytes,
+                               hipStream_t s, size_t *need)
+{
+    const int relu = (flags & RGNN_FLAG_RELU) ? 1 : 0;
+    const size_t bytes = rgcn_bwd_layout(g, d_in, nullptr, nullptr);
+    if (need) { *need = bytes; return RGNN_OK; }
+    if (d_in != d_out || (d_in != 32 && d_in != 64 && d_in != 128))
+        return fail(RGNN_EUNSUPPORTED, "RGCN backward supports d_in = d_out in {32, 64, 128}");
+    if (relu && !out) return fail(RGNN_EINVAL, "RGCN backward with ReLU needs the forward output");
+    if (!ws || ws_bytes < bytes)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
+    if (d_in == 32) return rgcn_backward_d<32>(g, h, W, W0, relu, out, Gm, dh, dW, dW0, ws, s);
+    if (d_in == 64) return rgcn_backward_d<64>(g, h, W, W0, relu, out, Gm, dh, dW, dW0, ws, s);
+    return rgcn_backward_d<128>(g, h, W, W0, relu, out, Gm, dh, dW, dW0, ws, s);
 }
 
 }  // namespace rgnn

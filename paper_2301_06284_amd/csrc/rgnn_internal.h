@@ -270,14 +270,15 @@ struct FusedArgs {
 };
 rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s);
 
-// Outer-product chunks of the backward: partial[c] (D x D, D = 64) = sum over
-// the rows of chunk c of X[x(row)]^T Gm[g(row)], g(row) = gather ? gather[row]
-// : row and x(row) = g(row) when gather_x, else row; ldx, ldg: row strides.
+// Outer-product chunks of the backward: partial[c] (d x d, d in {32, 64, 128})
+// = sum over the rows of chunk c of X[x(row)]^T Gm[g(row)], g(row) = gather ?
+// gather[row] : row and x(row) = g(row) when gather_x, else row; ldx, ldg: row
+// strides.
 rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x,
-                                const float *X, int ldx, const float *Gm, int ldg, float *partial,
+                                const float *X, int ldx, const float *Gm, int ldg, float *partial, int d,
                                 hipStream_t s);
-// dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (D x D each).
-rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW,
+// dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (d x d each).
+rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s);
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);
 rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);

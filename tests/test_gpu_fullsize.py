@@ -188,6 +188,34 @@ def test_workload4_rgat(plan):
     assert row_err(got[sel], ref) <= TOL
 
 
+@pytest.mark.parametrize("layer", ["rgat", "rgcn"])
+def test_workload4_backward_d128(layer):
+    """RGAT and RGCN backward at d = 128 on the 2.5M-node graph (hubs of up
+    to 5e5 in-edges, 535 relations), sampled like workload 5's."""
+    g, t, run = load(4)
+    print(f"workload 4 {layer} backward d=128", flush=True)
+    rng = np.random.default_rng(41)
+    relcount = np.bincount(g["rel"], minlength=g["R"])
+    rels = np.r_[np.argsort(relcount)[:3], [7]]
+    nodes = rng.choice(g["N"], 40, replace=False)
+    nm = np.zeros(g["N"], np.uint8); nm[nodes] = 1
+    rm = np.zeros(g["R"], np.uint8); rm[rels] = 1
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    if layer == "rgat":
+        gh, gW, gs, gt = run.rgat_backward()
+        dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                                node_mask=nm, rel_mask=rm)
+        assert row_err(gs[rels], dws[rels], cancel_floor=1e-6) <= TOL
+        assert row_err(gt[rels], dwt[rels], cancel_floor=1e-6) <= TOL
+    else:
+        gh, gW, _ = run.rgcn_backward(W0=True)
+        dh, dW, _ = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], node_mask=nm,
+                                         rel_mask=rm, want_dW0=False)
+    assert np.isfinite(gh).all() and np.isfinite(gW).all()
+    assert row_err(gh[nodes], dh[nodes], structural_zero=isolated[nodes], cancel_floor=1e-6) <= TOL
+    assert row_err(gW[rels].reshape(-1, 128), dW[rels].reshape(-1, 128), cancel_floor=1e-6) <= TOL
+
+
 def test_workload5_rgat_backward():
     g, t, run = load(5)
     print("workload 5 rgat backward", flush=True)

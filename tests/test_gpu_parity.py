@@ -401,6 +401,46 @@ def test_rgat_backward_per_relation_softmax_hub_segments():
     assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
 
 
+@pytest.mark.parametrize("kind", ["random", "hub", "srchub", "dups", "empty"])
+@pytest.mark.parametrize("d,heads,scope", [(32, 1, 0), (32, 2, 0), (32, 1, 1), (128, 1, 0), (128, 8, 0),
+                                           (128, 1, 1)])
+def test_rgat_backward_hidden_sizes(kind, d, heads, scope):
+    """RGAT backward at d = 32 and 128 (the outer products as 64 x 64 tiles:
+    one zero-padded tile at 32, four at 128)."""
+    g = graph(kind, E=3000)
+    t = workloads.tiny_tensors(51, g, d, d, heads=heads, att_var=1.0)
+    print(f"rgat backward d={d} heads={heads} scope={scope} {kind}", flush=True)
+    run = Runner(g, t)
+    gh, gW, gs, gt = run.rgat_backward(heads=heads, scope=scope)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
+                                            heads=heads, scope=scope)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, d), dW.reshape(-1, d), cancel_floor=1e-6) <= TOL
+    assert row_err(gs, dws, cancel_floor=1e-6) <= TOL
+    assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
+
+
+@pytest.mark.parametrize("kind", ["random", "hub", "srchub", "dups", "empty"])
+@pytest.mark.parametrize("d", [32, 128])
+@pytest.mark.parametrize("W0,relu", [(True, True), (False, False)])
+def test_rgcn_backward_hidden_sizes(kind, d, W0, relu):
+    g = graph(kind, seed=52)
+    t = workloads.tiny_tensors(52, g, d, d)
+    print(f"rgcn backward d={d} {kind} W0={W0} relu={relu}", flush=True)
+    run = Runner(g, t)
+    out = oracle.rgcn_forward(g, t["h"], t["W"], t["W0"] if W0 else None, relu=True) if relu else None
+    gh, gW, gW0 = run.rgcn_backward(W0=W0, relu=relu, out=out)
+    run.close()
+    dh, dW, dW0 = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"] if W0 else None, t["grad_out"], relu=relu)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=None if W0 else isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, d), dW.reshape(-1, d), cancel_floor=1e-6) <= TOL
+    if W0:
+        assert row_err(gW0, dW0) <= TOL
+
+
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("heads", [2, 4])
 def test_rgat_backward_multihead(kind, heads):

@@ -138,7 +138,7 @@ def _normal(rng, shape, var: float) -> np.ndarray:
 
 def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None,
                  heads: int | None = None) -> dict:
-    """Features, weights and (workloads 1, 2, 3, 5) the loss weight for workload k.
+    """Features, weights and (workloads 1 to 5) the loss weight for workload k.
     Variances: features and weights 1/fan_in, attention vectors 0.1, HGT head
     blocks 1/d_k, loss weight 1.  `d` and `heads` override the workload's
     hidden size and HGT head count (the hidden-size sweep)."""
@@ -152,7 +152,7 @@ def make_tensors(k: int, g: dict, layer: str | None = None, d: int | None = None
         out["W0"] = _normal(w_rng, (d, d), 1.0 / d)
         out["w_src"] = _normal(a_rng, (R, d), 0.1)
         out["w_dst"] = _normal(a_rng, (R, d), 0.1)
-        if layer == "rgat_bwd" or k in (1, 2, 5):
+        if layer == "rgat_bwd" or k in (1, 2, 4, 5):
             out["grad_out"] = _normal(l_rng, (N, d), 1.0)
     if layer == "hgt":
         H = heads or c["heads"]
