@@ -256,6 +256,32 @@ def sweep(args):
                              "edges_per_s": E / (ms * 1e-3), "auto_selects": plan == auto and compact})
                 log(f"  {lname} {label}: {ms:.3f} ms")
                 del ws
+        if wk == 2:   # training: the backward passes at this width
+            N2, R2 = c.info["num_nodes"], c.info["num_rels"]
+            saved = torch.empty(N2, 1, 2, device=c.dev)
+            ws = torch.empty(max(rgnn.workspace_size(c.G, rgnn.LAYER_RGAT, d, d, 1), 256), dtype=torch.uint8,
+                             device=c.dev)
+            rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, saved, ws, d, d)
+            del ws
+            Gd = torch.from_numpy(workloads.make_tensors(5, c.g, "rgat_bwd", d)["grad_out"]).to(c.dev)
+            gh = torch.empty(N2, d, device=c.dev)
+            gW, gs, gt, gW0 = (torch.empty(R2, d, d, device=c.dev), torch.empty(R2, d, device=c.dev),
+                               torch.empty(R2, d, device=c.dev), torch.empty(d, d, device=c.dev))
+            for lname, layer in (("rgat", rgnn.LAYER_RGAT_BACKWARD), ("rgcn", rgnn.LAYER_RGCN_BACKWARD)):
+                ws = torch.empty(max(rgnn.workspace_size(c.G, layer, d, d, 1), 256), dtype=torch.uint8,
+                                 device=c.dev)
+                if lname == "rgat":
+                    fn = lambda: rgnn.rgat_backward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], saved,
+                                                    Gd, gh, gW, gs, gt, ws, d, d)
+                else:
+                    fn = lambda: rgnn.rgcn_backward(c.G, c.T["h"], c.T["W"], c.T["W0"], None, Gd, gh, gW, gW0,
+                                                    ws, d, d, 0)
+                ms = time_steps(torch, fn, K, W)
+                rows.append({"workload": name, "d": d, "layer": lname, "variant": "backward", "ms": round(ms, 4),
+                             "edges_per_s": E / (ms * 1e-3)})
+                log(f"  {lname} backward: {ms:.3f} ms")
+                del ws
+            del saved, Gd, gh, gW, gs, gt, gW0
         del out
     Gn.close()
     c.close()
