@@ -302,7 +302,22 @@ def sweep(args):
         rows.append({"workload": "mag_like_1p9m", "d": d, "layer": "hgt", "heads": H,
                      "variant": "reordered segment queries", "ms": round(ms, 4), "edges_per_s": E / (ms * 1e-3)})
         log(f"  hgt d={d}: {ms:.3f} ms")
-        del ws, out
+        del ws
+        # backward (forward recomputed inside)
+        Nn, R3, T3, dk = c.info["num_nodes"], c.info["num_rels"], c.info["num_ntypes"], d // H
+        grads = dict(dh=torch.empty(Nn, d, device=c.dev),
+                     **{k: torch.empty(T3, d, d, device=c.dev) for k in ("dWk", "dWq", "dWv", "dWa")},
+                     dWatt=torch.empty(R3, H, dk, dk, device=c.dev), dWmsg=torch.empty(R3, H, dk, dk, device=c.dev),
+                     dmu=torch.empty(R3, device=c.dev))
+        ws = torch.empty(max(rgnn.workspace_size(c.G, rgnn.LAYER_HGT_BACKWARD, d, d, H), 256), dtype=torch.uint8,
+                         device=c.dev)
+        fb = lambda: rgnn.hgt_backward(c.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
+                                       T["mu"], T["grad_out"], grads, ws, d, H, 0.25)
+        ms = time_steps(torch, fb, K, W)
+        rows.append({"workload": "mag_like_1p9m", "d": d, "layer": "hgt", "heads": H, "variant": "backward",
+                     "ms": round(ms, 4), "edges_per_s": E / (ms * 1e-3)})
+        log(f"  hgt backward d={d}: {ms:.3f} ms")
+        del ws, out, grads
     c.close()
     print(json.dumps({"sweep": rows}))
 

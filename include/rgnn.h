@@ -223,8 +223,7 @@ rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
  *   agg_t = concat_i sum_e alpha_e,i msg_e,i
  *   out_t = agg_t Wa[tau(t)] (RGNN_FLAG_A_LINEAR, else agg_t) + h_t (RGNN_FLAG_RESIDUAL)
  *   h [N, d]; Wk, Wq, Wv, Wa [T, d, d]; Watt, Wmsg [R, heads, dk, dk]; mu [R].
- *   d in {32, 64, 128}, heads in {1, 2, 4, 8} with dk = d / heads >= 16
- *   (hgt_backward: d = 64, heads in {1, 2, 4}). */
+ *   d in {32, 64, 128}, heads in {1, 2, 4, 8} with dk = d / heads >= 16. */
 rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, const float *Wq,
                         const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                         const float *mu, int32_t d, int32_t heads, float att_scale, int32_t flags,
@@ -274,7 +273,7 @@ rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W,
  * grad_out [N, d]; writes grad_h [N, d], grad_Wk, grad_Wq, grad_Wv [T, d, d],
  * grad_Wa [T, d, d] (with RGNN_FLAG_A_LINEAR; otherwise not written, may be
  * NULL), grad_Watt, grad_Wmsg [R, heads, dk, dk] and grad_mu [R].  The forward
- * is recomputed inside the call.  d = 64 with heads in {1, 2, 4}.  Workspace:
+ * is recomputed inside the call.  d in {32, 64, 128}, d / heads >= 16.  Workspace:
  * rgnn_workspace_size(RGNN_LAYER_HGT_BACKWARD, d, d, heads).  Results are
  * reproducible except the K|V gradient rows of sources with more than 64
  * out-edges, which are summed with float atomics. */

@@ -724,9 +724,9 @@ extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const
         return fail(RGNN_EINVAL, "NULL tensor pointer");
     if (flags & ~(RGNN_FLAG_RESIDUAL | RGNN_FLAG_A_LINEAR)) return fail(RGNN_EINVAL, "unknown HGT flag");
     if ((flags & RGNN_FLAG_A_LINEAR) && !Wa) return fail(RGNN_EINVAL, "Wa is NULL");
-    if (d != 64) return fail(RGNN_EUNSUPPORTED, "HGT backward supports d = 64");
-    if (heads != 1 && heads != 2 && heads != 4)
-        return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2 or 4");
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "HGT backward supports d = 32, 64 or 128");
+    if (!(heads == 1 || heads == 2 || heads == 4 || heads == 8) || d / heads < 16)
+        return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2, 4 or 8 with d / heads >= 16");
     if (!std::isfinite(att_scale)) return fail(RGNN_EINVAL, "att_scale must be finite");
     return hgt_backward_impl(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, d, heads, att_scale, flags, grad_out,
                              grad_h, grad_Wk, grad_Wq, grad_Wv, (flags & RGNN_FLAG_A_LINEAR) ? grad_Wa : nullptr,

@@ -1,7 +1,7 @@
 // hgt_backward.hip -- HGT backward pass for the loss L = sum(out * G), the
 // chain rule of the HGT layer (Section "Backward Propagation" derives the
-// backward from the forward; here it is written out), for d = 64 and 1, 2 or 4
-// heads.  With the forward's reordered segment queries QP_vs = c_r Q_t
+// backward from the forward; here it is written out), for d in {32, 64, 128}
+// and d / heads >= 16.  With the forward's reordered segment queries QP_vs = c_r Q_t
 // Watt[r]^T per head (c_r = mu[r] * scale), the per-edge score a_e = K_s . QP_vs,
 // alpha_e its softmax over the destination's in-edges (saved max M_t and sum
 // Z_t), and dagg = G Wa^T (or G):
@@ -35,11 +35,8 @@ namespace rgnn {
 
 namespace {
 
-constexpr int D = 64, G = 16;
 constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 constexpr int kU = 2;             // edges per prefetch batch
-constexpr int GPB = 256 / G;
-constexpr int kMaxHeads = 4;
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
@@ -55,7 +52,7 @@ __device__ __forceinline__ void atomic_add4(float *p, float4 v)
 }
 
 // Wmt[r][i dk + b][i dk + a] = Wmsg[r][i][a][b]: block-diagonal W_msg^T per head.
-__global__ void hgt_msgT_weights_kernel(const float *Wmsg, int R, int heads, float *Wmt)
+__global__ void hgt_msgT_weights_kernel(const float *Wmsg, int R, int D, int heads, float *Wmt)
 {
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (idx >= (int64_t)R * D * D) return;
@@ -67,14 +64,15 @@ __global__ void hgt_msgT_weights_kernel(const float *Wmsg, int R, int heads, flo
 }
 
 // ---------------------------------------------------------------- destination-major pass
+template <int H>
 struct DStage {
     int eidx[kE];                  // source node of each edge
     int evs[kE];                   // item-local virtual segment of each edge
     int vptr[kE + 1];              // item-local first edge of each virtual segment
     int vpos[kE];                  // by-relation position of each virtual segment
     int dptr[kDst + 1];            // item-local first edge of each destination
-    float dm[kDst * kMaxHeads];    // per destination and head: softmax max
-    float dzi[kDst * kMaxHeads];   // and 1 / sum
+    float dm[kDst * H];            // per destination and head: softmax max
+    float dzi[kDst * H];           // and 1 / sum
 };
 
 struct DKArgs {
@@ -85,13 +83,14 @@ struct DKArgs {
     float *Sal, *Aac, *Bac, *sfin, *spart;
 };
 
-template <int H>
+template <int D, int H>
 __global__ __launch_bounds__(256) void hgt_bwd_dst_kernel(DKArgs k)
 {
+    constexpr int G = D / 4, GPB = 256 / G;
     constexpr int DKH = D / H, LH = DKH / 4;
-    __shared__ DStage stage[GPB];
+    __shared__ DStage<H> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    DStage &st = stage[gi];
+    DStage<H> &st = stage[gi];
     const int64_t item = (int64_t)blockIdx.x * GPB + gi;
     const bool valid = item < k.n_items;
     int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
@@ -210,7 +209,7 @@ __global__ __launch_bounds__(256) void hgt_bwd_merge_s_kernel(int64_t n_split, i
 }
 
 // dQP = A - s_t B per by-relation segment row (head blocks of dk features).
-__global__ __launch_bounds__(256) void hgt_bwd_dqp_kernel(int64_t V, int heads, const int32_t *vsegdst_byrel,
+__global__ __launch_bounds__(256) void hgt_bwd_dqp_kernel(int64_t V, int D, int heads, const int32_t *vsegdst_byrel,
                                                           const float *A, const float *B,
                                                           const float *sfin, float *dQP)
 {
@@ -238,9 +237,10 @@ struct SKArgs {
     float *dKV;          // zero on entry
 };
 
-template <int H>
+template <int D, int H>
 __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
 {
+    constexpr int G = D / 4, GPB = 256 / G;
     constexpr int DKH = D / H, LH = DKH / 4;
     __shared__ SStageH stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
@@ -338,7 +338,7 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
 // Per relation: dWatt, dWmsg from the head blocks of OT = sum dQP^T Q and
 // M2 = sum Salpha^T dagg, and dmu = scale * <OT head blocks, Watt> (fixed order).
 __global__ __launch_bounds__(256) void hgt_bwd_rel_kernel(const float *OT, const float *M2, const float *Watt,
-                                                          const float *mu, float scale, int heads,
+                                                          const float *mu, float scale, int D, int heads,
                                                           float *dWatt, float *dWmsg, float *dmu)
 {
     __shared__ float red[256];
@@ -376,7 +376,7 @@ struct HgtBwdWs {
         *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2;
 };
 
-size_t hgt_bwd_layout(const rgnn_graph *g, int H, void *base, HgtBwdWs *w)
+size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w)
 {
     char *b = (char *)base;
     size_t off = 0;
@@ -409,7 +409,7 @@ hipError_t zero4(float *p, int64_t n, hipStream_t s)
 }
 
 // Y = X W[type]^T over the nodes grouped by type (typed GEMM, B = W^T).
-rgnn_status node_gemm_t(const rgnn_graph *g, const float *X, int64_t ldx, const float *W, float *Y,
+rgnn_status node_gemm_t(const rgnn_graph *g, int D, const float *X, int64_t ldx, const float *W, float *Y,
                         const float *residual, int accumulate, hipStream_t s)
 {
     GemmArgs ga;
@@ -423,7 +423,7 @@ rgnn_status node_gemm_t(const rgnn_graph *g, const float *X, int64_t ldx, const 
 }
 
 // dW[type] = sum over the nodes n of the type of X[n]^T Y[n].
-rgnn_status type_outer(const rgnn_graph *g, const float *X, int ldx, const float *Y, int ldy, float *chunks,
+rgnn_status type_outer(const rgnn_graph *g, int D, const float *X, int ldx, const float *Y, int ldy, float *chunks,
                        float *dW, hipStream_t s)
 {
     rgnn_status st = launch_outer_chunks(g->dev.tiles_types_outer, g->n_tiles_types_outer, g->dev.ntype_perm, 1,
@@ -432,37 +432,41 @@ rgnn_status type_outer(const rgnn_graph *g, const float *X, int ldx, const float
     return launch_chunk_sum(chunks, g->dev.types_chunkptr, g->T, dW, D, s);
 }
 
-}  // namespace
-
-rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
-                              const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
-                              const float *mu, int d, int heads, float att_scale, int flags,
-                              const float *Gm, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
-                              float *dWatt, float *dWmsg, float *dmu, void *ws, size_t ws_bytes,
-                              hipStream_t s, size_t *need)
+template <int D>
+rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
+                           const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
+                           const float *mu, int H, float att_scale, int flags, const float *Gm, float *dh,
+                           float *dWk, float *dWq, float *dWv, float *dWa, float *dWatt, float *dWmsg,
+                           float *dmu, void *ws, hipStream_t s)
 {
-    const int H = heads;
-    const size_t bytes = hgt_bwd_layout(g, H > 0 ? H : 1, nullptr, nullptr);
-    if (need) { *need = bytes; return RGNN_OK; }
-    if (d != D) return fail(RGNN_EUNSUPPORTED, "HGT backward supports d = 64");
-    if (H != 1 && H != 2 && H != 4) return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2 or 4");
-    if (!ws || ws_bytes < bytes)
-        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
+    constexpr int G = D / 4, GPB = 256 / G;
     const bool a_linear = (flags & RGNN_FLAG_A_LINEAR) != 0;
     HgtBwdWs w;
-    hgt_bwd_layout(g, H, ws, &w);
+    hgt_bwd_layout(g, D, H, ws, &w);
     rgnn_status st;
     hipError_t e;
     // ---- forward recomputation, with the per-destination softmax statistics
     {
         GemmArgs ga;
         ga.X = h; ga.ldx = D; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
-        ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
-        ga.K = D; ga.Nc = 3 * D;
+        ga.K = D;
         ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
-        ga.Y = w.KV; ga.ldy = 2 * D;
-        ga.ep.Y2 = w.Q; ga.ep.ldy2 = D; ga.ep.split = 2 * D;
-        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        if (D == 64) {   // K | V | Q in one GEMM
+            ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
+            ga.Nc = 3 * D;
+            ga.Y = w.KV; ga.ldy = 2 * D;
+            ga.ep.Y2 = w.Q; ga.ep.ldy2 = D; ga.ep.split = 2 * D;
+            if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        } else {
+            ga.Nc = D;
+            const float *Wp[3] = {Wk, Wv, Wq};
+            float *Yp[3] = {w.KV, w.KV + D, w.Q};
+            const int64_t ld[3] = {2 * D, 2 * D, D};
+            for (int p = 0; p < 3; ++p) {
+                ga.W[0] = Wp[p]; ga.Y = Yp[p]; ga.ldy = ld[p];
+                if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+            }
+        }
     }
     if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, D, H, w.Wqp, s)) != RGNN_OK) return st;
     {
@@ -483,16 +487,16 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
     // ---- output linear: dagg = G Wa^T, dWa = sum agg^T G per node type
     const float *dagg = Gm;
     if (a_linear) {
-        if ((st = node_gemm_t(g, Gm, D, Wa, w.dagg, nullptr, 0, s)) != RGNN_OK) return st;
+        if ((st = node_gemm_t(g, D, Gm, D, Wa, w.dagg, nullptr, 0, s)) != RGNN_OK) return st;
         dagg = w.dagg;
-        if (dWa && (st = type_outer(g, w.agg, D, Gm, D, w.chunks, dWa, s)) != RGNN_OK) return st;
+        if (dWa && (st = type_outer(g, D, w.agg, D, Gm, D, w.chunks, dWa, s)) != RGNN_OK) return st;
     }
     // ---- dP = dagg_t Wmsg[r]^T per segment (vseg order)
     if (g->V > 0) {
         {
             const int64_t n = (int64_t)g->R * D * D;
             LaunchScope ls("hgt_msgT_weights", s);
-            hipLaunchKernelGGL(hgt_msgT_weights_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, Wmsg, g->R, H,
+            hipLaunchKernelGGL(hgt_msgT_weights_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, Wmsg, g->R, D, H,
                                w.Wmt);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "msgT weights launch");
@@ -514,9 +518,12 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
         const unsigned nb = blocks_for(g->n_items, GPB);
         {
             LaunchScope ls("hgt_bwd_dst", s);
-            if (H == 1) hipLaunchKernelGGL(hgt_bwd_dst_kernel<1>, dim3(nb), dim3(256), 0, s, k);
-            else if (H == 2) hipLaunchKernelGGL(hgt_bwd_dst_kernel<2>, dim3(nb), dim3(256), 0, s, k);
-            else hipLaunchKernelGGL(hgt_bwd_dst_kernel<4>, dim3(nb), dim3(256), 0, s, k);
+            if (H == 1) hipLaunchKernelGGL((hgt_bwd_dst_kernel<D, 1>), dim3(nb), dim3(256), 0, s, k);
+            else if (H == 2) hipLaunchKernelGGL((hgt_bwd_dst_kernel<D, 2>), dim3(nb), dim3(256), 0, s, k);
+            else if constexpr (D >= 64) {
+                if (H == 4) hipLaunchKernelGGL((hgt_bwd_dst_kernel<D, 4>), dim3(nb), dim3(256), 0, s, k);
+                else if constexpr (D >= 128) hipLaunchKernelGGL((hgt_bwd_dst_kernel<D, 8>), dim3(nb), dim3(256), 0, s, k);
+            }
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_dst launch");
     }
@@ -533,7 +540,7 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
         {
             LaunchScope ls("hgt_bwd_dqp", s);
             hipLaunchKernelGGL(hgt_bwd_dqp_kernel, dim3(blocks_for(g->V * (D / 4), 256)), dim3(256), 0, s, g->V,
-                               H, g->dev.vsegdst_byrel, w.Aac, w.Bac, w.sfin, w.dQP);
+                               D, H, g->dev.vsegdst_byrel, w.Aac, w.Bac, w.sfin, w.dQP);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_dqp launch");
         GemmArgs gt;
@@ -559,7 +566,7 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
         {
             LaunchScope ls("hgt_bwd_rel", s);
             hipLaunchKernelGGL(hgt_bwd_rel_kernel, dim3((unsigned)g->R), dim3(256), 0, s, w.OT, w.M2, Watt, mu,
-                               att_scale, H, dWatt, dWmsg, dmu);
+                               att_scale, D, H, dWatt, dWmsg, dmu);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_rel launch");
     }
@@ -573,21 +580,49 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
         const unsigned nb = blocks_for(g->n_oitems, GPB);
         {
             LaunchScope ls("hgt_bwd_src", s);
-            if (H == 1) hipLaunchKernelGGL(hgt_bwd_src_kernel<1>, dim3(nb), dim3(256), 0, s, k);
-            else if (H == 2) hipLaunchKernelGGL(hgt_bwd_src_kernel<2>, dim3(nb), dim3(256), 0, s, k);
-            else hipLaunchKernelGGL(hgt_bwd_src_kernel<4>, dim3(nb), dim3(256), 0, s, k);
+            if (H == 1) hipLaunchKernelGGL((hgt_bwd_src_kernel<D, 1>), dim3(nb), dim3(256), 0, s, k);
+            else if (H == 2) hipLaunchKernelGGL((hgt_bwd_src_kernel<D, 2>), dim3(nb), dim3(256), 0, s, k);
+            else if constexpr (D >= 64) {
+                if (H == 4) hipLaunchKernelGGL((hgt_bwd_src_kernel<D, 4>), dim3(nb), dim3(256), 0, s, k);
+                else if constexpr (D >= 128) hipLaunchKernelGGL((hgt_bwd_src_kernel<D, 8>), dim3(nb), dim3(256), 0, s, k);
+            }
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_src launch");
     }
     // ---- node-level linears: dh and the per-type weight gradients
     const float *res = (flags & RGNN_FLAG_RESIDUAL) ? Gm : nullptr;
-    if ((st = node_gemm_t(g, w.dKV, 2 * D, Wk, dh, res, 0, s)) != RGNN_OK) return st;
-    if ((st = node_gemm_t(g, w.dKV + D, 2 * D, Wv, dh, nullptr, 1, s)) != RGNN_OK) return st;
-    if ((st = node_gemm_t(g, w.dQ, D, Wq, dh, nullptr, 1, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, h, D, w.dKV, 2 * D, w.chunks, dWk, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, h, D, w.dKV + D, 2 * D, w.chunks, dWv, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, h, D, w.dQ, D, w.chunks, dWq, s)) != RGNN_OK) return st;
+    if ((st = node_gemm_t(g, D, w.dKV, 2 * D, Wk, dh, res, 0, s)) != RGNN_OK) return st;
+    if ((st = node_gemm_t(g, D, w.dKV + D, 2 * D, Wv, dh, nullptr, 1, s)) != RGNN_OK) return st;
+    if ((st = node_gemm_t(g, D, w.dQ, D, Wq, dh, nullptr, 1, s)) != RGNN_OK) return st;
+    if ((st = type_outer(g, D, h, D, w.dKV, 2 * D, w.chunks, dWk, s)) != RGNN_OK) return st;
+    if ((st = type_outer(g, D, h, D, w.dKV + D, 2 * D, w.chunks, dWv, s)) != RGNN_OK) return st;
+    if ((st = type_outer(g, D, h, D, w.dQ, D, w.chunks, dWq, s)) != RGNN_OK) return st;
     return RGNN_OK;
+}
+
+}  // namespace
+
+rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
+                              const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
+                              const float *mu, int d, int heads, float att_scale, int flags,
+                              const float *Gm, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
+                              float *dWatt, float *dWmsg, float *dmu, void *ws, size_t ws_bytes,
+                              hipStream_t s, size_t *need)
+{
+    const int H = heads;
+    const size_t bytes = hgt_bwd_layout(g, d, H > 0 ? H : 1, nullptr, nullptr);
+    if (need) { *need = bytes; return RGNN_OK; }
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "HGT backward supports d = 32, 64 or 128");
+    if (!(H == 1 || H == 2 || H == 4 || H == 8) || d / H < 16)
+        return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2, 4 or 8 with d / heads >= 16");
+    if (!ws || ws_bytes < bytes)
+        return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
+#define HB(D) hgt_backward_d<D>(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, H, att_scale, flags, Gm, dh, dWk, dWq, dWv, \
+                                dWa, dWatt, dWmsg, dmu, ws, s)
+    if (d == 32) return HB(32);
+    if (d == 64) return HB(64);
+    return HB(128);
+#undef HB
 }
 
 }  // namespace rgnn

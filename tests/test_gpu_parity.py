@@ -523,13 +523,13 @@ def test_rgcn_backward_after_forward():
     assert row_err(gW0, dW0) <= TOL
 
 
-def check_hgt_grads(got, ref, heads):
-    dk = 64 // heads
+def check_hgt_grads(got, ref, heads, d=64):
+    dk = d // heads
     assert row_err(got["dh"], ref["dh"]) <= TOL
     for k in ("dWk", "dWq", "dWv", "dWa"):
         if ref[k] is None:
             continue
-        assert row_err(got[k].reshape(-1, 64), ref[k].reshape(-1, 64)) <= TOL, k
+        assert row_err(got[k].reshape(-1, d), ref[k].reshape(-1, d)) <= TOL, k
     for k in ("dWatt", "dWmsg"):
         assert row_err(got[k].reshape(-1, dk), ref[k].reshape(-1, dk)) <= TOL, k
     assert row_err(got["dmu"].reshape(1, -1), ref["dmu"].reshape(1, -1)) <= TOL
@@ -554,6 +554,22 @@ def test_hgt_backward_small(kind, heads):
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=heads, att_scale=scale)
     check_hgt_grads(got, ref, heads)
+
+
+@pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
+@pytest.mark.parametrize("d,heads", [(32, 1), (32, 2), (128, 2), (128, 8)])
+def test_hgt_backward_hidden_sizes(kind, d, heads):
+    g = graph(kind, T=4, R=7, E=3000)
+    t = workloads.tiny_tensors(53, g, d, d, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)   # distinct priors
+    scale = 1.0 / np.sqrt(d // heads)
+    print(f"hgt backward d={d} heads={heads} {kind}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(heads, scale)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=heads, att_scale=scale)
+    check_hgt_grads(got, ref, heads, d)
 
 
 @pytest.mark.parametrize("flags", [0, 2, 4])
