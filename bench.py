@@ -293,17 +293,19 @@ def sweep(args):
         log(f"sweep: workload 3, HGT d = {d}, {H} heads")
         c.T = {n: torch.from_numpy(v).to(c.dev) for n, v in workloads.make_tensors(3, c.g, "hgt", d, heads=H).items()}
         out = torch.empty(c.info["num_nodes"], d, device=c.dev)
+        saved = torch.empty(c.info["num_nodes"], H, 2, device=c.dev)
         ws = torch.empty(max(rgnn.workspace_size(c.G, rgnn.LAYER_HGT, d, d, H), 256), dtype=torch.uint8,
                          device=c.dev)
         T = c.T
         fn = lambda: rgnn.hgt_forward(c.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
-                                      T["mu"], out, ws, d, H, 0.25, rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR)
+                                      T["mu"], out, ws, d, H, 0.25, rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR,
+                                      saved=saved)
         ms = time_steps(torch, fn, K, W)
         rows.append({"workload": "mag_like_1p9m", "d": d, "layer": "hgt", "heads": H,
                      "variant": "reordered segment queries", "ms": round(ms, 4), "edges_per_s": E / (ms * 1e-3)})
         log(f"  hgt d={d}: {ms:.3f} ms")
         del ws
-        # backward (forward recomputed inside)
+        # backward from the forward's softmax statistics
         Nn, R3, T3, dk = c.info["num_nodes"], c.info["num_rels"], c.info["num_ntypes"], d // H
         grads = dict(dh=torch.empty(Nn, d, device=c.dev),
                      **{k: torch.empty(T3, d, d, device=c.dev) for k in ("dWk", "dWq", "dWv", "dWa")},
@@ -312,12 +314,12 @@ def sweep(args):
         ws = torch.empty(max(rgnn.workspace_size(c.G, rgnn.LAYER_HGT_BACKWARD, d, d, H), 256), dtype=torch.uint8,
                          device=c.dev)
         fb = lambda: rgnn.hgt_backward(c.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
-                                       T["mu"], T["grad_out"], grads, ws, d, H, 0.25)
+                                       T["mu"], T["grad_out"], grads, ws, d, H, 0.25, saved=saved)
         ms = time_steps(torch, fb, K, W)
         rows.append({"workload": "mag_like_1p9m", "d": d, "layer": "hgt", "heads": H, "variant": "backward",
                      "ms": round(ms, 4), "edges_per_s": E / (ms * 1e-3)})
         log(f"  hgt backward d={d}: {ms:.3f} ms")
-        del ws, out, grads
+        del ws, out, grads, saved
     c.close()
     print(json.dumps({"sweep": rows}))
 
@@ -482,14 +484,17 @@ def main():
         c = Ctx(3)
         d3 = 64
         out = torch.empty(c.info["num_nodes"], d3, device=c.dev)
+        saved3 = torch.empty(c.info["num_nodes"], 4, 2, device=c.dev)
         ws = c.ws(rgnn.LAYER_HGT, d3, d3, 4)
         fnh = lambda: rgnn.hgt_forward(c.G, c.T["h"], c.T["Wk"], c.T["Wq"], c.T["Wv"], c.T["Wa"],
-                                       c.T["Watt"], c.T["Wmsg"], c.T["mu"], out, ws, d3, 4, 0.25)
+                                       c.T["Watt"], c.T["Wmsg"], c.T["mu"], out, ws, d3, 4, 0.25,
+                                       saved=saved3)
         msh = time_steps(torch, fnh, K, W)
         kh = kernel_profile(rgnn, torch, fnh, max(3, K // 2))
         layers["hgt_fwd_mag_like_1p9m"] = {"edges_per_s": c.info["num_edges"] / (msh * 1e-3), "ms": msh,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in kh.items()}}
-        # HGT backward (recomputes the forward inside the call)
+        # HGT backward from the forward's softmax statistics (the forward above
+        # wrote them), and without them (the forward traversal recomputed inside)
         log("workload 3: HGT backward")
         N3, R3, T3 = c.info["num_nodes"], c.info["num_rels"], c.g["T"]
         grads = dict(dh=torch.empty(N3, d3, device=c.dev), dWk=torch.empty(T3, d3, d3, device=c.dev),
@@ -498,12 +503,18 @@ def main():
                      dWmsg=torch.empty(R3, 4, 16, 16, device=c.dev), dmu=torch.empty(R3, device=c.dev))
         wsb3 = c.ws(rgnn.LAYER_HGT_BACKWARD, d3, d3, 4)
         fnhb = lambda: rgnn.hgt_backward(c.G, c.T["h"], c.T["Wk"], c.T["Wq"], c.T["Wv"], c.T["Wa"], c.T["Watt"],
-                                         c.T["Wmsg"], c.T["mu"], c.T["grad_out"], grads, wsb3, d3, 4, 0.25)
+                                         c.T["Wmsg"], c.T["mu"], c.T["grad_out"], grads, wsb3, d3, 4, 0.25,
+                                         saved=saved3)
         mshb = time_steps(torch, fnhb, K, W)
         khb = kernel_profile(rgnn, torch, fnhb, max(3, K // 2))
         layers["hgt_bwd_mag_like_1p9m"] = {"edges_per_s": c.info["num_edges"] / (mshb * 1e-3), "ms": mshb,
                                            "kernels_ms": {k: round(v[1], 4) for k, v in khb.items()}}
-        del grads, wsb3
+        fnhr = lambda: rgnn.hgt_backward(c.G, c.T["h"], c.T["Wk"], c.T["Wq"], c.T["Wv"], c.T["Wa"], c.T["Watt"],
+                                         c.T["Wmsg"], c.T["mu"], c.T["grad_out"], grads, wsb3, d3, 4, 0.25)
+        mshr = time_steps(torch, fnhr, K, W)
+        layers["hgt_bwd_mag_like_1p9m_forward_recomputed"] = {"edges_per_s": c.info["num_edges"] / (mshr * 1e-3),
+                                                               "ms": mshr}
+        del grads, wsb3, saved3
         c.close()
         del out, ws
 

@@ -223,11 +223,14 @@ rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
  *   agg_t = concat_i sum_e alpha_e,i msg_e,i
  *   out_t = agg_t Wa[tau(t)] (RGNN_FLAG_A_LINEAR, else agg_t) + h_t (RGNN_FLAG_RESIDUAL)
  *   h [N, d]; Wk, Wq, Wv, Wa [T, d, d]; Watt, Wmsg [R, heads, dk, dk]; mu [R].
+ *   saved: NULL, or [N, heads, 2] written with each destination's softmax
+ *   maximum and sum per head ((0, 0) for a destination without in-edges), which
+ *   hgt_backward takes to skip recomputing the forward traversal.
  *   d in {32, 64, 128}, heads in {1, 2, 4, 8} with dk = d / heads >= 16. */
 rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const float *Wk, const float *Wq,
                         const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                         const float *mu, int32_t d, int32_t heads, float att_scale, int32_t flags,
-                        float *out, void *ws, size_t ws_bytes, void *stream);
+                        float *out, float *saved, void *ws, size_t ws_bytes, void *stream);
 
 /* RGAT backward (Section "Backward Propagation") for the forward above: given
  * grad_out = dL/dout [N, d_out] and the forward's `saved`, writes dL/dh
@@ -272,17 +275,21 @@ rgnn_status rgcn_backward(const rgnn_graph_t *g, const float *h, const float *W,
  * the loss L = sum(out * grad_out).  Arguments as in hgt_forward plus
  * grad_out [N, d]; writes grad_h [N, d], grad_Wk, grad_Wq, grad_Wv [T, d, d],
  * grad_Wa [T, d, d] (with RGNN_FLAG_A_LINEAR; otherwise not written, may be
- * NULL), grad_Watt, grad_Wmsg [R, heads, dk, dk] and grad_mu [R].  The forward
- * is recomputed inside the call.  d in {32, 64, 128}, d / heads >= 16.  Workspace:
+ * NULL), grad_Watt, grad_Wmsg [R, heads, dk, dk] and grad_mu [R].  saved: the
+ * forward's softmax statistics [N, heads, 2] from hgt_forward with the same
+ * inputs, or NULL, in which case the forward traversal is recomputed inside
+ * the call (with saved given, the aggregate that grad_Wa needs is rebuilt from
+ * the backward's own per-segment sums instead).  d in {32, 64, 128},
+ * d / heads >= 16.  Workspace:
  * rgnn_workspace_size(RGNN_LAYER_HGT_BACKWARD, d, d, heads).  Results are
  * reproducible except the K|V gradient rows of sources with more than 64
  * out-edges, which are summed with float atomics. */
 rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk, const float *Wq,
                          const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                          const float *mu, int32_t d, int32_t heads, float att_scale, int32_t flags,
-                         const float *grad_out, float *grad_h, float *grad_Wk, float *grad_Wq,
-                         float *grad_Wv, float *grad_Wa, float *grad_Watt, float *grad_Wmsg,
-                         float *grad_mu, void *ws, size_t ws_bytes, void *stream);
+                         const float *grad_out, const float *saved, float *grad_h, float *grad_Wk,
+                         float *grad_Wq, float *grad_Wv, float *grad_Wa, float *grad_Watt,
+                         float *grad_Wmsg, float *grad_mu, void *ws, size_t ws_bytes, void *stream);
 
 /* Segment MM: the GEMM template of Section "The GEMM Template and the
  * Traversal Template", Y[S] = X[G] x W[T]:

@@ -360,7 +360,7 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
         size_t need = 0;
         hgt_backward_impl(g, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, d_out,
                           heads, 0.f, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                          nullptr, nullptr, 0, nullptr, &need);
+                          nullptr, nullptr, nullptr, 0, nullptr, &need);
         *bytes = need;
         return RGNN_OK;
     }
@@ -572,7 +572,7 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
                                    const float *Wq, const float *Wv, const float *Wa,
                                    const float *Watt, const float *Wmsg, const float *mu,
                                    int32_t d, int32_t heads, float att_scale, int32_t flags,
-                                   float *out, void *ws, size_t ws_bytes, void *stream)
+                                   float *out, float *saved, void *ws, size_t ws_bytes, void *stream)
 {
     rgnn_status st = check_graph(g);
     if (st != RGNN_OK) return st;
@@ -633,9 +633,9 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
         ha.QP = w.QP;
     }
-    ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial;
+    ha.heads = heads; ha.d = d; ha.agg = w.agg; ha.partial = w.partial; ha.saved = saved;
     if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
-    if ((st = launch_merge_partials(g, d, heads, 1, w.partial, w.agg, nullptr, 0, s)) != RGNN_OK)
+    if ((st = launch_merge_partials(g, d, heads, 1, w.partial, w.agg, saved, 0, s)) != RGNN_OK)
         return st;
     if (flags & RGNN_FLAG_A_LINEAR) {
         GemmArgs gb;
@@ -713,7 +713,8 @@ extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const
                                     const float *Wq, const float *Wv, const float *Wa,
                                     const float *Watt, const float *Wmsg, const float *mu, int32_t d,
                                     int32_t heads, float att_scale, int32_t flags, const float *grad_out,
-                                    float *grad_h, float *grad_Wk, float *grad_Wq, float *grad_Wv,
+                                    const float *saved, float *grad_h, float *grad_Wk, float *grad_Wq,
+                                    float *grad_Wv,
                                     float *grad_Wa, float *grad_Watt, float *grad_Wmsg, float *grad_mu,
                                     void *ws, size_t ws_bytes, void *stream)
 {
@@ -729,7 +730,7 @@ extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const
         return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2, 4 or 8 with d / heads >= 16");
     if (!std::isfinite(att_scale)) return fail(RGNN_EINVAL, "att_scale must be finite");
     return hgt_backward_impl(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, d, heads, att_scale, flags, grad_out,
-                             grad_h, grad_Wk, grad_Wq, grad_Wv, (flags & RGNN_FLAG_A_LINEAR) ? grad_Wa : nullptr,
+                             saved, grad_h, grad_Wk, grad_Wq, grad_Wv, (flags & RGNN_FLAG_A_LINEAR) ? grad_Wa : nullptr,
                              grad_Watt, grad_Wmsg, grad_mu, ws, ws_bytes, (hipStream_t)stream, nullptr);
 }
 

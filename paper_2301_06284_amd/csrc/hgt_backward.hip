@@ -435,9 +435,9 @@ rgnn_status type_outer(const rgnn_graph *g, int D, const float *X, int ldx, cons
 template <int D>
 rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
                            const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
-                           const float *mu, int H, float att_scale, int flags, const float *Gm, float *dh,
-                           float *dWk, float *dWq, float *dWv, float *dWa, float *dWatt, float *dWmsg,
-                           float *dmu, void *ws, hipStream_t s)
+                           const float *mu, int H, float att_scale, int flags, const float *Gm,
+                           const float *saved, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
+                           float *dWatt, float *dWmsg, float *dmu, void *ws, hipStream_t s)
 {
     constexpr int G = D / 4, GPB = 256 / G;
     const bool a_linear = (flags & RGNN_FLAG_A_LINEAR) != 0;
@@ -445,7 +445,9 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     hgt_bwd_layout(g, D, H, ws, &w);
     rgnn_status st;
     hipError_t e;
-    // ---- forward recomputation, with the per-destination softmax statistics
+    // ---- forward recomputation: K | V | Q, the segment queries and, without the
+    //      forward's statistics, the traversal that yields them and agg
+    const float *stats = saved ? saved : w.saved;
     {
         GemmArgs ga;
         ga.X = h; ga.ldx = D; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
@@ -477,19 +479,20 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         gq.Y = w.QP; gq.ldy = D; gq.ep.diag_blocks = H;
         if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
     }
-    {
+    if (!saved) {
         HgtArgs ha;
         ha.g = g; ha.KV = w.KV; ha.QP = w.QP; ha.Wmsg = Wmsg;
         ha.heads = H; ha.d = D; ha.agg = w.agg; ha.partial = w.partial; ha.saved = w.saved;
         if ((st = launch_hgt_traverse(ha, s)) != RGNN_OK) return st;
         if ((st = launch_merge_partials(g, D, H, 1, w.partial, w.agg, w.saved, 0, s)) != RGNN_OK) return st;
     }
-    // ---- output linear: dagg = G Wa^T, dWa = sum agg^T G per node type
+    // ---- output linear: dagg = G Wa^T, dWa = sum agg^T G per node type (with
+    //      the forward's statistics agg is rebuilt after the destination pass)
     const float *dagg = Gm;
     if (a_linear) {
         if ((st = node_gemm_t(g, D, Gm, D, Wa, w.dagg, nullptr, 0, s)) != RGNN_OK) return st;
         dagg = w.dagg;
-        if (dWa && (st = type_outer(g, D, w.agg, D, Gm, D, w.chunks, dWa, s)) != RGNN_OK) return st;
+        if (dWa && !saved && (st = type_outer(g, D, w.agg, D, Gm, D, w.chunks, dWa, s)) != RGNN_OK) return st;
     }
     // ---- dP = dagg_t Wmsg[r]^T per segment (vseg order)
     if (g->V > 0) {
@@ -513,7 +516,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         k.n_items = g->n_items; k.items = g->dev.items; k.item_slot = g->dev.item_slot;
         k.dst_vsegptr = g->dev.dst_vsegptr; k.vseg_ptr = g->dev.vseg_ptr; k.in_src = g->dev.in_src;
         k.vseg_pos = g->dev.vseg_pos;
-        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.saved = w.saved;
+        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.saved = stats;
         k.Sal = w.Sal; k.Aac = w.Aac; k.Bac = w.Bac; k.sfin = w.sfin; k.spart = w.spart;
         const unsigned nb = blocks_for(g->n_items, GPB);
         {
@@ -534,6 +537,20 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
                                g->n_split, H, g->dev.split_dst, g->dev.split_slotptr, w.spart, w.sfin);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_merge_s launch");
+    }
+    // ---- agg_t = sum over t's segments of Salpha_vs Wmsg[r] (the messages are
+    //      linear in V_s, so the alpha-weighted V sums of the destination pass
+    //      give the forward's aggregate), then dWa = sum agg^T G per node type
+    if (a_linear && dWa && saved) {
+        if (g->V > 0) {
+            GemmArgs gm;
+            gm.X = w.Sal; gm.ldx = D; gm.W[0] = w.Wmt; gm.trans_b = 1; gm.K = D; gm.Nc = D;
+            gm.tiles = g->dev.tiles_vsegs; gm.ntiles = g->n_tiles_vsegs;
+            gm.Y = w.Tq; gm.ldy = D; gm.scatter = g->dev.vseg_byrel; gm.ep.diag_blocks = H;
+            if ((st = launch_typed_gemm(gm, s)) != RGNN_OK) return st;
+        }
+        if ((st = launch_vseg_reduce(g, w.Tq, nullptr, D, w.agg, 0, 0, s)) != RGNN_OK) return st;
+        if ((st = type_outer(g, D, w.agg, D, Gm, D, w.chunks, dWa, s)) != RGNN_OK) return st;
     }
     // ---- dQP, dQ and the per-relation weight gradients
     if (g->V > 0) {
@@ -576,7 +593,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         SKArgs k{};
         k.n_items = g->n_oitems; k.items = g->dev.oitems; k.out_ptr = g->dev.out_ptr;
         k.out_vseg = g->dev.out_vseg; k.vseg_byrel = g->dev.vseg_byrel; k.vsegdst_byrel = g->dev.vsegdst_byrel;
-        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.saved = w.saved; k.sfin = w.sfin; k.dKV = w.dKV;
+        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.saved = stats; k.sfin = w.sfin; k.dKV = w.dKV;
         const unsigned nb = blocks_for(g->n_oitems, GPB);
         {
             LaunchScope ls("hgt_bwd_src", s);
@@ -605,9 +622,9 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
 rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
                               const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                               const float *mu, int d, int heads, float att_scale, int flags,
-                              const float *Gm, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
-                              float *dWatt, float *dWmsg, float *dmu, void *ws, size_t ws_bytes,
-                              hipStream_t s, size_t *need)
+                              const float *Gm, const float *saved, float *dh, float *dWk, float *dWq,
+                              float *dWv, float *dWa, float *dWatt, float *dWmsg, float *dmu, void *ws,
+                              size_t ws_bytes, hipStream_t s, size_t *need)
 {
     const int H = heads;
     const size_t bytes = hgt_bwd_layout(g, d, H > 0 ? H : 1, nullptr, nullptr);
@@ -617,8 +634,8 @@ rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *
         return fail(RGNN_EUNSUPPORTED, "HGT backward heads must be 1, 2, 4 or 8 with d / heads >= 16");
     if (!ws || ws_bytes < bytes)
         return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
-#define HB(D) hgt_backward_d<D>(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, H, att_scale, flags, Gm, dh, dWk, dWq, dWv, \
-                                dWa, dWatt, dWmsg, dmu, ws, s)
+#define HB(D) hgt_backward_d<D>(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, H, att_scale, flags, Gm, saved, dh, dWk, \
+                                dWq, dWv, dWa, dWatt, dWmsg, dmu, ws, s)
     if (d == 32) return HB(32);
     if (d == 64) return HB(64);
     return HB(128);

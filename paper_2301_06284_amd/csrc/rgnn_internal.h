@@ -321,9 +321,9 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
 rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
                               const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                               const float *mu, int d, int heads, float att_scale, int flags,
-                              const float *Gm, float *dh, float *dWk, float *dWq, float *dWv, float *dWa,
-                              float *dWatt, float *dWmsg, float *dmu, void *ws, size_t ws_bytes,
-                              hipStream_t s, size_t *need);
+                              const float *Gm, const float *saved, float *dh, float *dWk, float *dWq,
+                              float *dWv, float *dWa, float *dWatt, float *dWmsg, float *dmu, void *ws,
+                              size_t ws_bytes, hipStream_t s, size_t *need);
 
 // RGCN backward (rgcn_backward.hip), the same convention for need.
 rgnn_status rgcn_backward_impl(const rgnn_graph *g, const float *h, const float *W, const float *W0,

@@ -73,11 +73,11 @@ def _load():
         "rgnn_select_plan": [vp, i32, i32, i32, i32, P(i32), P(ctypes.c_double), P(ctypes.c_double)],
         "rgcn_forward": [vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, sz, vp],
         "rgat_forward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp, sz, vp],
-        "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, sz, vp],
+        "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, vp, sz, vp],
         "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
         "rgcn_backward": [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp],
         "hgt_backward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp,
-                         vp, vp, vp, sz, vp],
+                         vp, vp, vp, vp, sz, vp],
         "rgnn_segment_gemm": [vp, i64, vp, vp, i32, vp, i32, i32, vp, i64, vp, vp, sz, vp],
         "rgnn_segment_gemm_workspace_size": [i64, i32, P(sz)],
         "rgnn_profile_enable": [i32],
@@ -236,19 +236,21 @@ def rgat_forward(g, h, W, w_src, w_dst, out, saved, ws, d_in, d_out, heads=1, ne
 
 
 def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, out, ws, d, heads, att_scale,
-                flags=FLAG_RESIDUAL | FLAG_A_LINEAR, stream=None):
+                flags=FLAG_RESIDUAL | FLAG_A_LINEAR, stream=None, saved=None):
+    """saved: None or a [N, heads, 2] tensor for the softmax statistics."""
     _check(_lib.hgt_forward(g.handle, _ptr(h), _ptr(Wk), _ptr(Wq), _ptr(Wv), _ptr(Wa), _ptr(Watt),
                             _ptr(Wmsg), _ptr(mu), d, heads, float(att_scale), flags, _ptr(out),
-                            _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                            _ptr(saved), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(stream)))
 
 
 def hgt_backward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, grad_out, grads, ws, d, heads, att_scale,
-                 flags=FLAG_RESIDUAL | FLAG_A_LINEAR, stream=None):
-    """grads: dict of output tensors dh, dWk, dWq, dWv, dWa (or None), dWatt, dWmsg, dmu."""
+                 flags=FLAG_RESIDUAL | FLAG_A_LINEAR, stream=None, saved=None):
+    """grads: dict of output tensors dh, dWk, dWq, dWv, dWa (or None), dWatt, dWmsg, dmu.
+    saved: the forward's statistics (hgt_forward's saved), or None to recompute them."""
     _check(_lib.hgt_backward(g.handle, _ptr(h), _ptr(Wk), _ptr(Wq), _ptr(Wv), _ptr(Wa), _ptr(Watt),
                              _ptr(Wmsg), _ptr(mu), d, heads, float(att_scale), flags, _ptr(grad_out),
-                             _ptr(grads["dh"]), _ptr(grads["dWk"]), _ptr(grads["dWq"]), _ptr(grads["dWv"]),
+                             _ptr(saved), _ptr(grads["dh"]), _ptr(grads["dWk"]), _ptr(grads["dWq"]), _ptr(grads["dWv"]),
                              _ptr(grads.get("dWa")), _ptr(grads["dWatt"]), _ptr(grads["dWmsg"]),
                              _ptr(grads["dmu"]), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                              _stream(stream)))

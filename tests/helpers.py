@@ -97,14 +97,18 @@ class Runner:
             return out.cpu().numpy(), saved
         return out.cpu().numpy()
 
-    def hgt(self, heads, scale, flags=None):
+    def hgt(self, heads, scale, flags=None, want_saved=False):
+        """want_saved: also return the softmax statistics [N, heads, 2] (a device tensor)."""
         T, torch, rgnn = self.T, self.torch, self.rgnn
         d = T["h"].shape[1]
         flags = rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR if flags is None else flags
         out = torch.full((self.g["N"], d), float("nan"), device=self.dev)
+        saved = torch.full((self.g["N"], heads, 2), float("nan"), device=self.dev) if want_saved else None
         rgnn.hgt_forward(self.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
-                         T["mu"], out, self.ws(2, d, d, heads), d, heads, scale, flags)
+                         T["mu"], out, self.ws(2, d, d, heads), d, heads, scale, flags, saved=saved)
         torch.cuda.synchronize()
+        if want_saved:
+            return out.cpu().numpy(), saved
         return out.cpu().numpy()
 
     def rgat_backward(self, slope=0.2, heads=1, scope=0):
@@ -121,7 +125,9 @@ class Runner:
         torch.cuda.synchronize()
         return gh.cpu().numpy(), gW.cpu().numpy(), gs.cpu().numpy(), gt.cpu().numpy()
 
-    def hgt_backward(self, heads, scale, flags=None):
+    def hgt_backward(self, heads, scale, flags=None, use_saved=False):
+        """use_saved: run this library's forward first and hand its softmax
+        statistics to the backward (otherwise the backward recomputes them)."""
         T, torch, rgnn = self.T, self.torch, self.rgnn
         d = T["h"].shape[1]
         flags = rgnn.FLAG_RESIDUAL | rgnn.FLAG_A_LINEAR if flags is None else flags
@@ -131,9 +137,10 @@ class Runner:
         grads = dict(dh=nan(N, d), dWk=nan(NT, d, d), dWq=nan(NT, d, d), dWv=nan(NT, d, d),
                      dWa=nan(NT, d, d) if flags & rgnn.FLAG_A_LINEAR else None,
                      dWatt=nan(R, heads, dk, dk), dWmsg=nan(R, heads, dk, dk), dmu=nan(R))
+        saved = self.hgt(heads, scale, flags, want_saved=True)[1] if use_saved else None
         rgnn.hgt_backward(self.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
                           T["mu"], T["grad_out"], grads, self.ws(rgnn.LAYER_HGT_BACKWARD, d, d, heads),
-                          d, heads, scale, flags)
+                          d, heads, scale, flags, saved=saved)
         torch.cuda.synchronize()
         return {k: (None if v is None else v.cpu().numpy()) for k, v in grads.items()}
 

@@ -283,8 +283,9 @@ def test_workload5_rgcn_backward():
     assert row_err(gW0, dW0) <= TOL
 
 
-@pytest.mark.parametrize("kind,heads", [("random", 4), ("hub", 2)])
-def test_hgt_backward_mid_size(kind, heads):
+@pytest.mark.parametrize("kind,heads,use_saved", [("random", 4, False), ("hub", 2, False), ("random", 4, True),
+                                                   ("hub", 2, True)])
+def test_hgt_backward_mid_size(kind, heads, use_saved):
     """HGT backward on a 20 000-node / 300 000-edge graph with 7 relations and
     4 node types (thousands of work items and GEMM tiles, split destinations
     for the hub kind), checked in full against the oracle (the 21 M-edge
@@ -293,9 +294,9 @@ def test_hgt_backward_mid_size(kind, heads):
     t = workloads.tiny_tensors(36, g, 64, 64, heads=heads)
     t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)
     scale = 1.0 / np.sqrt(64 // heads)
-    print(f"hgt backward mid-size {kind} heads={heads}", flush=True)
+    print(f"hgt backward mid-size {kind} heads={heads} saved={use_saved}", flush=True)
     run = Runner(g, t)
-    got = run.hgt_backward(heads, scale)
+    got = run.hgt_backward(heads, scale, use_saved=use_saved)
     run.close()
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=heads, att_scale=scale)

@@ -543,41 +543,44 @@ def hgt_case(kind, heads, seed, flags=None, R=7, T=4, E=4000, scale=None):
     return g, t, scale
 
 
+@pytest.mark.parametrize("use_saved", [False, True])
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("heads", [1, 2, 4])
-def test_hgt_backward_small(kind, heads):
+def test_hgt_backward_small(kind, heads, use_saved):
     g, t, scale = hgt_case(kind, heads, 33)
-    print(f"hgt backward {kind} heads={heads}", flush=True)
+    print(f"hgt backward {kind} heads={heads} saved={use_saved}", flush=True)
     run = Runner(g, t)
-    got = run.hgt_backward(heads, scale)
+    got = run.hgt_backward(heads, scale, use_saved=use_saved)
     run.close()
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=heads, att_scale=scale)
     check_hgt_grads(got, ref, heads)
 
 
+@pytest.mark.parametrize("use_saved", [False, True])
 @pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
 @pytest.mark.parametrize("d,heads", [(32, 1), (32, 2), (128, 2), (128, 8)])
-def test_hgt_backward_hidden_sizes(kind, d, heads):
+def test_hgt_backward_hidden_sizes(kind, d, heads, use_saved):
     g = graph(kind, T=4, R=7, E=3000)
     t = workloads.tiny_tensors(53, g, d, d, heads=heads)
     t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)   # distinct priors
     scale = 1.0 / np.sqrt(d // heads)
-    print(f"hgt backward d={d} heads={heads} {kind}", flush=True)
+    print(f"hgt backward d={d} heads={heads} {kind} saved={use_saved}", flush=True)
     run = Runner(g, t)
-    got = run.hgt_backward(heads, scale)
+    got = run.hgt_backward(heads, scale, use_saved=use_saved)
     run.close()
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=heads, att_scale=scale)
     check_hgt_grads(got, ref, heads, d)
 
 
+@pytest.mark.parametrize("use_saved", [False, True])
 @pytest.mark.parametrize("flags", [0, 2, 4])
-def test_hgt_backward_flags(flags):
+def test_hgt_backward_flags(flags, use_saved):
     g, t, scale = hgt_case("hub", 4, 34, R=3, T=2)
-    print(f"hgt backward flags={flags}", flush=True)
+    print(f"hgt backward flags={flags} saved={use_saved}", flush=True)
     run = Runner(g, t)
-    got = run.hgt_backward(4, 0.3, flags=flags)
+    got = run.hgt_backward(4, 0.3, flags=flags, use_saved=use_saved)
     run.close()
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=4, att_scale=0.3,
@@ -597,6 +600,43 @@ def test_hgt_backward_many_relations(heads, R):
     ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
                               t["mu"], t["grad_out"], heads=heads, att_scale=scale)
     check_hgt_grads(got, ref, heads)
+
+
+@pytest.mark.parametrize("kind", ["random", "hub", "isolated", "empty"])
+@pytest.mark.parametrize("d,heads", [(64, 4), (128, 8), (32, 2)])
+def test_hgt_forward_saved_statistics(kind, d, heads):
+    """The forward's optional softmax statistics: the output is the same with
+    and without them; per destination and head, the maximum is the largest
+    logit (a_e of the layer's definition, formed here in fp64 from the same
+    inputs) and the sum is sum_e exp(a_e - max); (0, 0) without in-edges."""
+    g = graph(kind, T=4, R=7, E=3000)
+    t = workloads.tiny_tensors(54, g, d, d, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)
+    scale = 1.0 / np.sqrt(d // heads)
+    print(f"hgt forward saved d={d} heads={heads} {kind}", flush=True)
+    run = Runner(g, t)
+    plain = run.hgt(heads, scale)
+    out, saved = run.hgt(heads, scale, want_saved=True)
+    sv = saved.cpu().numpy()
+    run.close()
+    np.testing.assert_array_equal(out, plain)
+    # logits of the definition: (K_s,i Watt[r,i]) . Q_t,i * mu[r] * scale
+    dk = d // heads
+    h = t["h"].astype(np.float64)
+    nt = g["ntype"]
+    K = np.einsum("nd,nde->ne", h, t["Wk"].astype(np.float64)[nt]).reshape(-1, heads, dk)
+    Q = np.einsum("nd,nde->ne", h, t["Wq"].astype(np.float64)[nt]).reshape(-1, heads, dk)
+    src, dst, rel = g["src"], g["dst"], g["rel"]
+    KW = np.einsum("ehk,ehkl->ehl", K[src], t["Watt"].astype(np.float64)[rel])
+    a = (KW * Q[dst]).sum(-1) * t["mu"].astype(np.float64)[rel][:, None] * scale   # [E, heads]
+    M = np.full((g["N"], heads), -np.inf)
+    np.maximum.at(M, dst, a)
+    Z = np.zeros((g["N"], heads))
+    np.add.at(Z, dst, np.exp(a - M[dst]))
+    has = np.bincount(dst, minlength=g["N"]) > 0
+    assert np.all(sv[~has] == 0)
+    np.testing.assert_allclose(sv[has, :, 0], M[has], rtol=1e-5, atol=1e-5)
+    np.testing.assert_allclose(sv[has, :, 1], Z[has], rtol=1e-4)
 
 
 @pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
