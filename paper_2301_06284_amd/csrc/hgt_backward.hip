@@ -234,7 +234,7 @@ struct SKArgs {
     const Item *items;
     const int32_t *out_ptr, *out_vseg, *vseg_byrel, *vsegdst_byrel;
     const float *KV, *QP, *dP, *saved, *sfin;
-    float *dKV;          // zero on entry
+    float *dKV;          // rows of split sources zero on entry; every other row written here
 };
 
 template <int D, int H>
@@ -270,7 +270,15 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
         if (gl == 0) st.optr[nn] = nq;
     }
     __syncthreads();
-    if (!valid || nq == 0) return;
+    if (!valid) return;
+    // sources of a bundle without out-edges get zero rows
+    for (int jj = 0; jj < nn; ++jj)
+        if (st.optr[jj + 1] == st.optr[jj]) {
+            float *p = k.dKV + (size_t)(n0 + jj) * (2 * D) + gl * 4;
+            st4(p, zero4());
+            st4(p + D, zero4());
+        }
+    if (nq == 0) return;
     const int head = gl / LH;
     int j = 0;
     while (st.optr[j + 1] == st.optr[j]) ++j;   // first source with out-edges
@@ -362,10 +370,11 @@ __global__ __launch_bounds__(256) void hgt_bwd_rel_kernel(const float *OT, const
     }
 }
 
-__global__ __launch_bounds__(256) void zero4_kernel(float *p, int64_t n4)
+// zero the rows (w floats each, w a multiple of 4) listed in rows
+__global__ __launch_bounds__(256) void zero_rows_kernel(const int32_t *rows, int64_t n, int w, float *p)
 {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i < n4) st4(p + i * 4, zero4());
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x, q = w / 4;
+    if (i < n * q) st4(p + (size_t)rows[i / q] * w + (i % q) * 4, zero4());
 }
 
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
@@ -398,14 +407,6 @@ size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w
     x.chunks = take(nchunks * D * D); x.OT = take(R * D * D); x.M2 = take(R * D * D);
     if (w) *w = x;
     return off;
-}
-
-hipError_t zero4(float *p, int64_t n, hipStream_t s)
-{
-    if (n <= 0) return hipSuccess;
-    LaunchScope ls("zero", s);
-    hipLaunchKernelGGL(zero4_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, p, n / 4);
-    return hipGetLastError();
 }
 
 // Y = X W[type]^T over the nodes grouped by type (typed GEMM, B = W^T).
@@ -587,8 +588,16 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_rel launch");
     }
-    // ---- source-major pass: dK | dV per source
-    if ((e = zero4(w.dKV, g->N * 2 * D, s)) != hipSuccess) return hip_fail(e, "zero launch");
+    // ---- source-major pass: dK | dV per source (the rows of sources split over
+    //      several items are summed with atomics and start from zero)
+    if (g->n_osplit > 0) {
+        {
+            LaunchScope ls("zero", s);
+            hipLaunchKernelGGL(zero_rows_kernel, dim3(blocks_for(g->n_osplit * (2 * D / 4), 256)), dim3(256), 0, s,
+                               g->dev.osplit, g->n_osplit, 2 * D, w.dKV);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "zero launch");
+    }
     if (g->n_oitems > 0) {
         SKArgs k{};
         k.n_items = g->n_oitems; k.items = g->dev.oitems; k.out_ptr = g->dev.out_ptr;

@@ -62,6 +62,7 @@ struct HostIndex {
                                       // largest first
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
     std::vector<int32_t> big_seg;      // (dst, rel) segments with > kBigRange virtual segments
+    std::vector<int32_t> osplit;       // sources whose out-edges span several out-edge items
     std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
     std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
@@ -96,7 +97,7 @@ struct DeviceIndex {
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
-    int32_t *seg_vsegptr = nullptr, *big_seg = nullptr;
+    int32_t *seg_vsegptr = nullptr, *big_seg = nullptr, *osplit = nullptr;
     float *invcnt_byrel = nullptr;
     Tile *tiles_nodes_outer = nullptr;
     int32_t *nodes_chunkptr = nullptr;
@@ -128,7 +129,7 @@ struct rgnn_graph {
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
-    int64_t n_oitems = 0;
+    int64_t n_oitems = 0, n_osplit = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };

@@ -138,9 +138,11 @@ class Runner:
                      dWa=nan(NT, d, d) if flags & rgnn.FLAG_A_LINEAR else None,
                      dWatt=nan(R, heads, dk, dk), dWmsg=nan(R, heads, dk, dk), dmu=nan(R))
         saved = self.hgt(heads, scale, flags, want_saved=True)[1] if use_saved else None
+        # workspace filled with NaN bytes: a row the backward reads without
+        # having written it shows up in the gradients
+        ws = self.ws(rgnn.LAYER_HGT_BACKWARD, d, d, heads).fill_(255)
         rgnn.hgt_backward(self.G, T["h"], T["Wk"], T["Wq"], T["Wv"], T["Wa"], T["Watt"], T["Wmsg"],
-                          T["mu"], T["grad_out"], grads, self.ws(rgnn.LAYER_HGT_BACKWARD, d, d, heads),
-                          d, heads, scale, flags, saved=saved)
+                          T["mu"], T["grad_out"], grads, ws, d, heads, scale, flags, saved=saved)
         torch.cuda.synchronize()
         return {k: (None if v is None else v.cpu().numpy()) for k, v in grads.items()}
 
