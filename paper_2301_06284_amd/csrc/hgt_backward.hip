@@ -208,6 +208,17 @@ __global__ __launch_bounds__(256) void hgt_bwd_merge_s_kernel(int64_t n_split, i
     sfin[(size_t)split_dst[i] * heads + hh] = s;
 }
 
+// Per destination and head, (max, 1 / sum, s, 0) in one 16-byte record, so that
+// the source-major pass reads one line per out-edge for them instead of two.
+__global__ __launch_bounds__(256) void hgt_bwd_pack_kernel(int64_t n, const float *saved, const float *sfin,
+                                                           float4 *rec)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const float2 mz = *reinterpret_cast<const float2 *>(saved + i * 2);
+    rec[i] = make_float4(mz.x, mz.y > 0.f ? 1.f / mz.y : 0.f, sfin[i], 0.f);
+}
+
 // dQP = A - s_t B per by-relation segment row (head blocks of dk features).
 __global__ __launch_bounds__(256) void hgt_bwd_dqp_kernel(int64_t V, int D, int heads, const int32_t *vsegdst_byrel,
                                                           const float *A, const float *B,
@@ -233,7 +244,8 @@ struct SKArgs {
     int64_t n_items;
     const Item *items;
     const int32_t *out_ptr, *out_vseg, *vseg_byrel, *vsegdst_byrel;
-    const float *KV, *QP, *dP, *saved, *sfin;
+    const float *KV, *QP, *dP;
+    const float4 *rec;   // [N, H] (max, 1 / sum, s, 0) per destination and head
     float *dKV;          // rows of split sources zero on entry; every other row written here
 };
 
@@ -286,10 +298,9 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
     // ping-pong batches of (K row, V row of the source, QP and dP rows of the
     // segment, the destination's max, sum and s for this head)
     float4 Ak[kU], Av[kU], Aq[kU], Ap[kU], Bk[kU], Bv[kU], Bq[kU], Bp[kU];
-    float2 Am[kU], Bm[kU];
-    float As[kU], Bs[kU];
+    float4 Am[kU], Bm[kU];
     auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], float4 (&Xq)[kU], float4 (&Xp)[kU],
-                    float2 (&Xm)[kU], float (&Xs)[kU], int b0) {
+                    float4 (&Xm)[kU], int b0) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const int e = b0 + u < nq ? b0 + u : nq - 1;
@@ -300,20 +311,19 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
             Xv[u] = ld4(k.KV + row + D + gl * 4);
             Xq[u] = ld4(k.QP + vrow + gl * 4);
             Xp[u] = ld4(k.dP + vrow + gl * 4);
-            Xm[u] = *reinterpret_cast<const float2 *>(k.saved + th * 2);
-            Xs[u] = k.sfin[th];
+            Xm[u] = k.rec[th];
         }
     };
     auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
-                       const float4 (&Xp)[kU], const float2 (&Xm)[kU], const float (&Xs)[kU], int b0) {
+                       const float4 (&Xp)[kU], const float4 (&Xm)[kU], int b0) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const int e = b0 + u;
             if (e < nq) {
                 const float a = gsum<LH>(dot4(Xk[u], Xq[u]));
                 const float dal = gsum<LH>(dot4(Xv[u], Xp[u]));
-                const float al = __expf(a - Xm[u].x) / Xm[u].y;
-                dk = axpy4(dk, al * (dal - Xs[u]), Xq[u]);
+                const float al = __expf(a - Xm[u].x) * Xm[u].y;
+                dk = axpy4(dk, al * (dal - Xm[u].z), Xq[u]);
                 dv = axpy4(dv, al, Xp[u]);
                 if (e + 1 == st.optr[j + 1]) {   // the source's last out-edge in this item
                     float *p = k.dKV + (size_t)(n0 + j) * (2 * D) + gl * 4;
@@ -331,15 +341,15 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
             }
         }
     };
-    load(Ak, Av, Aq, Ap, Am, As, 0);
+    load(Ak, Av, Aq, Ap, Am, 0);
     __builtin_amdgcn_sched_barrier(0);
     for (int eb = 0; eb < nq; eb += 2 * kU) {
-        load(Bk, Bv, Bq, Bp, Bm, Bs, eb + kU);
+        load(Bk, Bv, Bq, Bp, Bm, eb + kU);
         __builtin_amdgcn_sched_barrier(0);
-        consume(Ak, Av, Aq, Ap, Am, As, eb);
-        load(Ak, Av, Aq, Ap, Am, As, eb + 2 * kU);
+        consume(Ak, Av, Aq, Ap, Am, eb);
+        load(Ak, Av, Aq, Ap, Am, eb + 2 * kU);
         __builtin_amdgcn_sched_barrier(0);
-        consume(Bk, Bv, Bq, Bp, Bm, Bs, eb + kU);
+        consume(Bk, Bv, Bq, Bp, Bm, eb + kU);
     }
 }
 
@@ -382,7 +392,7 @@ inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct HgtBwdWs {
     float *KV, *Q, *Wqp, *QP, *agg, *partial, *saved, *dagg, *Wmt, *dP, *Sal, *Aac, *Bac, *sfin,
-        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2;
+        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2, *rec;
 };
 
 size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w)
@@ -405,6 +415,7 @@ size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w
     x.sfin = take(N * H); x.spart = take(slots * H);
     x.dQP = take(V * D); x.Tq = take(V * D); x.dQ = take(N * D); x.dKV = take(N * 2 * D);
     x.chunks = take(nchunks * D * D); x.OT = take(R * D * D); x.M2 = take(R * D * D);
+    x.rec = take(N * H * 4);
     if (w) *w = x;
     return off;
 }
@@ -588,6 +599,14 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_rel launch");
     }
+    if (g->N > 0) {
+        {
+            LaunchScope ls("hgt_bwd_pack", s);
+            hipLaunchKernelGGL(hgt_bwd_pack_kernel, dim3(blocks_for(g->N * H, 256)), dim3(256), 0, s, g->N * H,
+                               stats, w.sfin, reinterpret_cast<float4 *>(w.rec));
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_pack launch");
+    }
     // ---- source-major pass: dK | dV per source (the rows of sources split over
     //      several items are summed with atomics and start from zero)
     if (g->n_osplit > 0) {
@@ -602,7 +621,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         SKArgs k{};
         k.n_items = g->n_oitems; k.items = g->dev.oitems; k.out_ptr = g->dev.out_ptr;
         k.out_vseg = g->dev.out_vseg; k.vseg_byrel = g->dev.vseg_byrel; k.vsegdst_byrel = g->dev.vsegdst_byrel;
-        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.saved = stats; k.sfin = w.sfin; k.dKV = w.dKV;
+        k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.rec = reinterpret_cast<const float4 *>(w.rec); k.dKV = w.dKV;
         const unsigned nb = blocks_for(g->n_oitems, GPB);
         {
             LaunchScope ls("hgt_bwd_src", s);
