@@ -348,6 +348,14 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
         else if (a.K == 64 && a.Nc == 192 && ep == EP_SPLIT) {
             launch_k<64, 192, EP_SPLIT>(k, a.ntiles, s);
             ok = true;
+        } else if (a.K == 192 && a.Nc == 64 && (ep == 0 || ep == EP_RESID)) {   // three weights stacked in K
+            if (ep) launch_k<192, 64, EP_RESID>(k, a.ntiles, s);
+            else launch_k<192, 64, 0>(k, a.ntiles, s);
+            ok = true;
+        } else if (a.K == 96 && a.Nc == 32 && (ep == 0 || ep == EP_RESID)) {
+            if (ep) launch_k<96, 32, EP_RESID>(k, a.ntiles, s);
+            else launch_k<96, 32, 0>(k, a.ntiles, s);
+            ok = true;
         }
     }
     if (!ok) return fail(RGNN_EUNSUPPORTED, "typed GEMM: unsupported shape / epilogue combination");

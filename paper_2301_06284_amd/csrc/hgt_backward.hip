@@ -246,7 +246,8 @@ struct SKArgs {
     const int32_t *out_ptr, *out_vseg, *vseg_byrel, *vsegdst_byrel;
     const float *KV, *QP, *dP;
     const float4 *rec;   // [N, H] (max, 1 / sum, s, 0) per destination and head
-    float *dKV;          // rows of split sources zero on entry; every other row written here
+    float *dKV;          // [N, 3D] dK | dV | dQ rows: dK | dV of split sources zero on entry,
+                         // of every other source written here
 };
 
 template <int D, int H>
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
     // sources of a bundle without out-edges get zero rows
     for (int jj = 0; jj < nn; ++jj)
         if (st.optr[jj + 1] == st.optr[jj]) {
-            float *p = k.dKV + (size_t)(n0 + jj) * (2 * D) + gl * 4;
+            float *p = k.dKV + (size_t)(n0 + jj) * (3 * D) + gl * 4;
             st4(p, zero4());
             st4(p + D, zero4());
         }
@@ -326,7 +327,7 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
                 dk = axpy4(dk, al * (dal - Xm[u].z), Xq[u]);
                 dv = axpy4(dv, al, Xp[u]);
                 if (e + 1 == st.optr[j + 1]) {   // the source's last out-edge in this item
-                    float *p = k.dKV + (size_t)(n0 + j) * (2 * D) + gl * 4;
+                    float *p = k.dKV + (size_t)(n0 + j) * (3 * D) + gl * 4;
                     if (split) {
                         atomic_add4(p, dk);
                         atomic_add4(p + D, dv);
@@ -380,11 +381,24 @@ __global__ __launch_bounds__(256) void hgt_bwd_rel_kernel(const float *OT, const
     }
 }
 
-// zero the rows (w floats each, w a multiple of 4) listed in rows
-__global__ __launch_bounds__(256) void zero_rows_kernel(const int32_t *rows, int64_t n, int w, float *p)
+// zero the first w floats (w a multiple of 4) of the rows (stride ld) listed in rows
+__global__ __launch_bounds__(256) void zero_rows_kernel(const int32_t *rows, int64_t n, int w, int ld, float *p)
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x, q = w / 4;
-    if (i < n * q) st4(p + (size_t)rows[i / q] * w + (i % q) * 4, zero4());
+    if (i < n * q) st4(p + (size_t)rows[i / q] * ld + (i % q) * 4, zero4());
+}
+
+// Wc[t][n][j D + k] = W_j[t][n][k] for (W_0, W_1, W_2) = (Wk, Wv, Wq): the three
+// transposed weights side by side, so that dh = [dK | dV | dQ] Wc^T is one GEMM.
+__global__ __launch_bounds__(256) void hgt_cat_weights_kernel(const float *Wk, const float *Wv, const float *Wq,
+                                                              int T, int D, float *Wc)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)T * D * 3 * D) return;
+    const int64_t row = idx / (3 * D);
+    const int c = (int)(idx % (3 * D)), j = c / D, k = c % D;
+    const float *W = j == 0 ? Wk : (j == 1 ? Wv : Wq);
+    Wc[idx] = W[row * D + k];
 }
 
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
@@ -392,7 +406,7 @@ inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct HgtBwdWs {
     float *KV, *Q, *Wqp, *QP, *agg, *partial, *saved, *dagg, *Wmt, *dP, *Sal, *Aac, *Bac, *sfin,
-        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2, *rec;
+        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2, *rec, *Wc;
 };
 
 size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w)
@@ -413,7 +427,9 @@ size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w
     x.dagg = take(N * D); x.Wmt = take(R * D * D); x.dP = take(V * D);
     x.Sal = take(V * D); x.Aac = take(V * D); x.Bac = take(V * D);
     x.sfin = take(N * H); x.spart = take(slots * H);
-    x.dQP = take(V * D); x.Tq = take(V * D); x.dQ = take(N * D); x.dKV = take(N * 2 * D);
+    x.dQP = take(V * D); x.Tq = take(V * D); x.dKV = take(N * 3 * D);
+    x.dQ = x.dKV ? x.dKV + 2 * D : nullptr;   // dK | dV | dQ side by side per node
+    x.Wc = take((size_t)g->T * D * 3 * D);
     x.chunks = take(nchunks * D * D); x.OT = take(R * D * D); x.M2 = take(R * D * D);
     x.rec = take(N * H * 4);
     if (w) *w = x;
@@ -578,7 +594,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         gt.Y = w.Tq; gt.ldy = D; gt.scatter = g->dev.vseg_byrel; gt.ep.diag_blocks = H;
         if ((st = launch_typed_gemm(gt, s)) != RGNN_OK) return st;
     }
-    if ((st = launch_vseg_reduce(g, w.Tq, nullptr, D, w.dQ, 0, 0, s)) != RGNN_OK) return st;
+    if ((st = launch_vseg_reduce(g, w.Tq, nullptr, D, w.dQ, 0, 0, s, 3 * D)) != RGNN_OK) return st;
     if (g->V > 0) {
         if ((st = launch_outer_chunks(g->dev.tiles_outer, g->n_tiles_outer, g->dev.vsegdst_byrel, 0, w.dQP, D, w.Q,
                                       D, w.chunks, D, s)) != RGNN_OK)
@@ -613,7 +629,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         {
             LaunchScope ls("zero", s);
             hipLaunchKernelGGL(zero_rows_kernel, dim3(blocks_for(g->n_osplit * (2 * D / 4), 256)), dim3(256), 0, s,
-                               g->dev.osplit, g->n_osplit, 2 * D, w.dKV);
+                               g->dev.osplit, g->n_osplit, 2 * D, 3 * D, w.dKV);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "zero launch");
     }
@@ -636,12 +652,29 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     }
     // ---- node-level linears: dh and the per-type weight gradients
     const float *res = (flags & RGNN_FLAG_RESIDUAL) ? Gm : nullptr;
-    if ((st = node_gemm_t(g, D, w.dKV, 2 * D, Wk, dh, res, 0, s)) != RGNN_OK) return st;
-    if ((st = node_gemm_t(g, D, w.dKV + D, 2 * D, Wv, dh, nullptr, 1, s)) != RGNN_OK) return st;
-    if ((st = node_gemm_t(g, D, w.dQ, D, Wq, dh, nullptr, 1, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, D, h, D, w.dKV, 2 * D, w.chunks, dWk, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, D, h, D, w.dKV + D, 2 * D, w.chunks, dWv, s)) != RGNN_OK) return st;
-    if ((st = type_outer(g, D, h, D, w.dQ, D, w.chunks, dWq, s)) != RGNN_OK) return st;
+    if constexpr (D <= 64) {   // dh = [dK | dV | dQ] [Wk | Wv | Wq]^T in one GEMM (K = 3D)
+        if (g->T > 0) {
+            const int64_t n = (int64_t)g->T * D * 3 * D;
+            LaunchScope ls("hgt_cat_weights", s);
+            hipLaunchKernelGGL(hgt_cat_weights_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, Wk, Wv, Wq, g->T,
+                               D, w.Wc);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "cat weights launch");
+        GemmArgs ga;
+        ga.X = w.dKV; ga.ldx = 3 * D; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
+        ga.W[0] = w.Wc; ga.trans_b = 1; ga.K = 3 * D; ga.Nc = D;
+        ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
+        ga.Y = dh; ga.ldy = D;
+        if (res) { ga.ep.residual = res; ga.ep.ld_res = D; }
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    } else {   // a 3D-deep weight tile would not fit LDS at D = 128
+        if ((st = node_gemm_t(g, D, w.dKV, 3 * D, Wk, dh, res, 0, s)) != RGNN_OK) return st;
+        if ((st = node_gemm_t(g, D, w.dKV + D, 3 * D, Wv, dh, nullptr, 1, s)) != RGNN_OK) return st;
+        if ((st = node_gemm_t(g, D, w.dQ, 3 * D, Wq, dh, nullptr, 1, s)) != RGNN_OK) return st;
+    }
+    if ((st = type_outer(g, D, h, D, w.dKV, 3 * D, w.chunks, dWk, s)) != RGNN_OK) return st;
+    if ((st = type_outer(g, D, h, D, w.dKV + D, 3 * D, w.chunks, dWv, s)) != RGNN_OK) return st;
+    if ((st = type_outer(g, D, h, D, w.dQ, 3 * D, w.chunks, dWq, s)) != RGNN_OK) return st;
     return RGNN_OK;
 }
 

@@ -97,7 +97,8 @@ __global__ __launch_bounds__(256) void vseg_stats_big_kernel(const int32_t *big_
 // of the rows (U in flight), the group sums are then added in group order.
 template <int D, int NTH, int U>
 __device__ __forceinline__ void vseg_reduce_big(int v, const int32_t *dst_vsegptr, const float *T,
-                                                const float *scale, float *out, int accumulate, int relu)
+                                                const float *scale, float *out, int64_t ldo, int accumulate,
+                                                int relu)
 {
     constexpr int G = D / 4, NG = NTH / G;
     __shared__ float4 part[NG * G];
@@ -122,23 +123,23 @@ __device__ __forceinline__ void vseg_reduce_big(int v, const int32_t *dst_vsegpt
     part[gi * G + gl] = acc;
     __syncthreads();
     if (gi == 0) {
-        float4 tot = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 tot = accumulate ? ld4(out + (size_t)v * ldo + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
         for (int j = 0; j < NG; ++j) tot = add4(tot, part[j * G + gl]);
-        st4(out + (size_t)v * D + gl * 4, relu ? relu4(tot) : tot);
+        st4(out + (size_t)v * ldo + gl * 4, relu ? relu4(tot) : tot);
     }
 }
 
 // out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
-// ReLU).  Blocks [0, nbig) take the destinations of big_vdst; the others a
-// group of D/4 lanes per destination.
+// ReLU), out rows ldo floats apart.  Blocks [0, nbig) take the destinations of
+// big_vdst; the others a group of D/4 lanes per destination.
 template <int D>
 __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbig, const int32_t *big_vdst,
                                                           const int32_t *dst_vsegptr,
                                                           const float *T, const float *scale,
-                                                          float *out, int accumulate, int relu)
+                                                          float *out, int64_t ldo, int accumulate, int relu)
 {
     if ((int64_t)blockIdx.x < nbig) {
-        vseg_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, T, scale, out, accumulate, relu);
+        vseg_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, T, scale, out, ldo, accumulate, relu);
         return;
     }
     constexpr int G = D / 4, GPB = 256 / G;
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbi
     if (v >= N) return;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
     if (e - b > kBigRange) return;
-    float4 acc = accumulate ? ld4(out + (size_t)v * D + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 acc = accumulate ? ld4(out + (size_t)v * ldo + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     // rows in batches of four (all in flight together), summed in segment order
     for (int i0 = b; i0 < e; i0 += 4) {
         float4 t[4];
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbi
         for (int u = 0; u < 4; ++u)
             if (i0 + u < e) acc = scale ? fma4(t[u], sc[u], acc) : add4(acc, t[u]);
     }
-    st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
+    st4(out + (size_t)v * ldo + gl * 4, relu ? relu4(acc) : acc);
 }
 
 // ---------------------------------------------------------------- softmax reduction
@@ -666,8 +667,9 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
 }
 
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
-                               float *out, int accumulate, int relu, hipStream_t s)
+                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo)
 {
+    if (ldo == 0) ldo = d;
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 32, 64 or 128");
     const int64_t nbig = g->n_big_vdst;
@@ -675,7 +677,7 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
     {
         LaunchScope ls("vseg_reduce", s);
 #define VR(D) hipLaunchKernelGGL((vseg_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
-                                 g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, accumulate, relu)
+                                 g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, ldo, accumulate, relu)
         if (d == 32) VR(32);
         else if (d == 64) VR(64);
         else VR(128);

@@ -239,9 +239,10 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 // Softmax per (dst, rel) segment: per virtual segment the scale
 // exp(m_i - M_seg) / Z_seg from the pieces' (max, sum) in a.vstat, to a.vscale.
 rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s);
-// out_v (+)= sum over v's virtual segments of scale[vs] * T[vs] (scale NULL: 1).
+// out_v (+)= sum over v's virtual segments of scale[vs] * T[vs] (scale NULL: 1);
+// out rows ldo floats apart (0: d).
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
-                               float *out, int accumulate, int relu, hipStream_t s);
+                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo = 0);
 
 // Softmax per destination finished from the per-segment (max, sum) in vstat
 // (fused order) and the segments' transformed rows summed: out_v = sum_i
