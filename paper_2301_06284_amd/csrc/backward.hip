@@ -434,6 +434,7 @@ struct SK {
     const float *wsp, *dS, *ay;
     float *dh;                   // holds the destination terms on entry
     float *ypair;                // [U_src] sum of Y per compact (src, rel) pair, zeroed before
+                                 // (written by a store, or by atomics for split sources)
 };
 
 struct SStage {
@@ -509,7 +510,12 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_src_kernel(SK k)
                 const bool node_end = e + 1 == st.optr[j + 1];
                 // the last out-edge of the item always ends its source
                 if (node_end || st.erel[e + 1] != st.erel[e]) {
-                    if (gl == 0) atomicAdd(k.ypair + st.epair[e], ysrc);
+                    // a pair's out-edges lie in one item unless its source is
+                    // split, so only pieces of split sources need the atomic
+                    if (gl == 0) {
+                        if (split) atomicAdd(k.ypair + st.epair[e], ysrc);
+                        else k.ypair[st.epair[e]] = ysrc;
+                    }
                     ysrc = 0.f;
                 }
                 if (node_end) {
