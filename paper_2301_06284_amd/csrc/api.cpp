@@ -167,8 +167,11 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
 // logits, softmax and messages exactly, and its loss is head k's share of L.
 // So the gradients of L are the sums over k of the one-head gradients of the
 // masked problem (the masked entries receive exact zeros: their messages are
-// zero and their loss and attention weights are zero).
-struct BwdHeadsWs { float *Wm, *wsm, *wdm, *Gm, *sv, *dh, *dW, *dws, *dwd; void *inner; size_t inner_bytes; };
+// zero and their loss and attention weights are zero).  The loss weight itself
+// needs no mask: it enters the one-head backward only through G W_r^T, where
+// the masked W_r drops the other heads' columns, and through the outer
+// products G^T Sa, whose other columns the pass leaves out of dW.
+struct BwdHeadsWs { float *Wm, *wsm, *wdm, *sv; void *inner; size_t inner_bytes; };
 size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, void *base, BwdHeadsWs *w)
 {
     size_t inner = 0;
@@ -183,12 +186,7 @@ size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, vo
         x.Wm = c.take<float>(R * d_in * d_out);
         x.wsm = c.take<float>(R * d_out);
         x.wdm = c.take<float>(R * d_out);
-        x.Gm = c.take<float>(N * d_out);
         x.sv = c.take<float>(std::max<size_t>(N, (size_t)g->U_dst) * 2);
-        x.dh = c.take<float>(N * d_in);
-        x.dW = c.take<float>(R * d_in * d_out);
-        x.dws = c.take<float>(R * d_out);
-        x.dwd = c.take<float>(R * d_out);
     }
     if (w) *w = x;
     return c.off;
@@ -691,20 +689,16 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
         if ((st = launch_mask_cols(W, w.Wm, R * d_in, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
-        if ((st = launch_mask_cols(grad_out, w.Gm, N, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_head_stats(saved, w.sv, per_seg ? g->U_dst : N, heads, k, s)) != RGNN_OK) return st;
-        // head 0 writes the outputs, the others add to them
-        float *oh = k ? w.dh : grad_h, *oW = k ? w.dW : grad_W;
-        float *os = k ? w.dws : grad_w_src, *od = k ? w.dwd : grad_w_dst;
-        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, per_seg, w.sv, w.Gm,
-                                     oh, oW, os, od, w.inner, w.inner_bytes, s, nullptr)) != RGNN_OK)
+        // grad_out goes in whole: dS = grad_out W_k^T sees only head k's columns
+        // through the masked weights, and the outer products keep only those
+        // columns of dW.  Head 0 writes the outputs, the others add to them.
+        BwdHead hd;
+        hd.col0 = c0; hd.col1 = c1; hd.acc = k > 0;
+        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, per_seg, w.sv, grad_out,
+                                     grad_h, grad_W, grad_w_src, grad_w_dst, w.inner, w.inner_bytes, s, nullptr,
+                                     hd)) != RGNN_OK)
             return st;
-        if (k) {
-            if ((st = launch_add(grad_h, grad_h, w.dh, N * d_in, s)) != RGNN_OK) return st;
-            if ((st = launch_add(grad_W, grad_W, w.dW, R * d_in * d_out, s)) != RGNN_OK) return st;
-            if ((st = launch_add(grad_w_src, grad_w_src, w.dws, R * d_out, s)) != RGNN_OK) return st;
-            if ((st = launch_add(grad_w_dst, grad_w_dst, w.dwd, R * d_out, s)) != RGNN_OK) return st;
-        }
     }
     return RGNN_OK;
 }

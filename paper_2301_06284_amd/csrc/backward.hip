@@ -80,7 +80,8 @@ struct BK {
     float *ssum;     // [slots] s_v partial of each piece of a split destination
     float *ay;       // [E, 2]  per sorted in-edge: (alpha, Y); pieces hold (signed alpha, dalpha) in between
     float *ysum;     // [V]     sum of Y per segment (by-relation order)
-    float *dh;       // [N, D]  destination terms written here
+    float *dh;       // [N, D]  destination terms written (acc_dh: added) here
+    int acc_dh;
 };
 
 template <bool SEG>
@@ -277,7 +278,8 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
         int j = 0;
         auto flush_to = [&](int jn) {   // finish destinations [j, jn)
             while (j < jn) {
-                st4(k.dh + (size_t)(dst0 + j) * D + gl * 4, acc);
+                float *p = k.dh + (size_t)(dst0 + j) * D + gl * 4;
+                st4(p, k.acc_dh ? add4(acc, ld4(p)) : acc);
                 acc = zero4();
                 ++j;
             }
@@ -392,7 +394,8 @@ template <int D, int NTH, int U, bool BIG>
 __global__ __launch_bounds__(NTH) void split_dst_term_kernel(const int32_t *big_split, const int32_t *split_slotptr,
                                                              const int32_t *split_dst, const int32_t *dst_vsegptr,
                                                              const int32_t *vseg_rel, const int32_t *vseg_pos,
-                                                             const float *ysum, const float *wtp, float *dh)
+                                                             const float *ysum, const float *wtp, float *dh,
+                                                             int acc_dh)
 {
     constexpr int G = D / 4, NG = NTH / G;
     __shared__ float4 part[NG][G];
@@ -422,7 +425,8 @@ __global__ __launch_bounds__(NTH) void split_dst_term_kernel(const int32_t *big_
     if (gi == 0) {
         float4 t = zero4();
         for (int j = 0; j < NG; ++j) t = add4(t, part[j][gl]);
-        st4(dh + (size_t)v * D + gl * 4, t);
+        float *p = dh + (size_t)v * D + gl * 4;
+        st4(p, acc_dh ? add4(t, ld4(p)) : t);
     }
 }
 
@@ -715,7 +719,7 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
                                                            const float *pws_all, const float *pwt_all,
                                                            const float *W, const float *w_src,
                                                            const float *w_dst, float *dW, float *dws,
-                                                           float *dwt)
+                                                           float *dwt, int col0, int col1, int acc)
 {
     __shared__ float pws[D], pwt[D];
     const int r = blockIdx.x, tid = threadIdx.x;
@@ -737,7 +741,9 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
 #pragma unroll
             for (int u = 0; u < 8; ++u) s += p[u];
         }
+        if (j < col0 || j >= col1) s = 0.f;
         if (ATT) s += pws[i] * w_src[(size_t)r * D + j] + pwt[i] * w_dst[(size_t)r * D + j];
+        if (acc) s += dW[(size_t)r * D * D + idx];
         dW[(size_t)r * D * D + idx] = s;
     }
     if (ATT && blockIdx.y == 0 && tid < D) {
@@ -746,6 +752,10 @@ __global__ __launch_bounds__(256) void bwd_finalize_kernel(const float *partial,
             const float wij = W[((size_t)r * D + i) * D + tid];
             a += pws[i] * wij;
             b += pwt[i] * wij;
+        }
+        if (acc) {
+            a += dws[(size_t)r * D + tid];
+            b += dwt[(size_t)r * D + tid];
         }
         dws[(size_t)r * D + tid] = a;
         dwt[(size_t)r * D + tid] = b;
@@ -804,15 +814,17 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
 }
 
 template <int D>
-void launch_split_dst_term(const rgnn_graph *g, const float *ysum, const float *wtp, float *dh, hipStream_t s)
+void launch_split_dst_term(const rgnn_graph *g, const float *ysum, const float *wtp, float *dh, int acc_dh,
+                           hipStream_t s)
 {
     const DeviceIndex &x = g->dev;
     hipLaunchKernelGGL((split_dst_term_kernel<D, 256, 4, false>), dim3((unsigned)g->n_split), dim3(256), 0, s,
-                       nullptr, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, ysum, wtp, dh);
+                       nullptr, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, ysum, wtp, dh,
+                       acc_dh);
     if (g->n_big_split)
         hipLaunchKernelGGL((split_dst_term_kernel<D, 1024, 8, true>), dim3((unsigned)g->n_big_split), dim3(1024),
                            0, s, x.big_split, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos,
-                           ysum, wtp, dh);
+                           ysum, wtp, dh, acc_dh);
 }
 
 // 64 x 64 tiles of the D x D outer products
@@ -861,7 +873,8 @@ rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int 
     {
         LaunchScope ls("chunk_sum", s);
 #define CS(D) hipLaunchKernelGGL((bwd_finalize_kernel<D, false>), dim3((unsigned)R, D * D / 256), dim3(256), 0, s, \
-                                 partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr, nullptr)
+                                 partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr, nullptr, \
+                                 0, D, 0)
         if (d == 32) CS(32);
         else if (d == 64) CS(64);
         else if (d == 128) CS(128);
@@ -877,7 +890,7 @@ namespace {
 template <int D>
 rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W, const float *w_src,
                             const float *w_dst, float slope, int per_seg, const float *saved, const float *Gm,
-                            float *dh, float *dW, float *dws, float *dwt, void *ws, hipStream_t s)
+                            float *dh, float *dW, float *dws, float *dwt, void *ws, hipStream_t s, BwdHead hd)
 {
     BwdWs w;
     bwd_layout(g, D, ws, &w);
@@ -903,7 +916,7 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
     k.vseg_pos = g->dev.vseg_pos; k.wtp = w.wtp; k.dh = dh;
     k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
-    k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs;
+    k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs; k.acc_dh = hd.acc;
     if (g->n_items && per_seg) {
         constexpr int GPB = item_threads(D) / (D / 4);
         const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
@@ -929,7 +942,7 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
             LaunchScope ls("rgat_bwd_split_dst_term", s);
-            launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, s);
+            launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, hd.acc, s);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
     } else if (g->n_items) {
@@ -960,7 +973,7 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
             {
                 LaunchScope ls("rgat_bwd_split_dst_term", s);
-                launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, s);
+                launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, hd.acc, s);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
         }
@@ -1001,7 +1014,8 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
     {
         LaunchScope ls("rgat_bwd_finalize", s);
         hipLaunchKernelGGL((bwd_finalize_kernel<D, true>), dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, w.partial,
-                           g->dev.rel_chunkptr, w.pws, w.pwt, W, w_src, w_dst, dW, dws, dwt);
+                           g->dev.rel_chunkptr, w.pws, w.pwt, W, w_src, w_dst, dW, dws, dwt, hd.col0, hd.col1,
+                           hd.acc);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "finalize launch");
     return RGNN_OK;
@@ -1013,7 +1027,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                                const float *w_src, const float *w_dst, int d_in, int d_out,
                                float slope, int per_seg, const float *saved, const float *Gm,
                                float *dh, float *dW, float *dws, float *dwt, void *ws,
-                               size_t ws_bytes, hipStream_t s, size_t *need)
+                               size_t ws_bytes, hipStream_t s, size_t *need, BwdHead hd)
 {
     const size_t bytes = bwd_layout(g, d_in, nullptr, nullptr);
     if (need) { *need = bytes; return RGNN_OK; }
@@ -1021,9 +1035,9 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
         return fail(RGNN_EUNSUPPORTED, "RGAT backward supports d_in = d_out in {32, 64, 128}");
     if (!ws || ws_bytes < bytes)
         return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(bytes) + " bytes");
-    if (d_in == 32) return rgat_backward_d<32>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
-    if (d_in == 64) return rgat_backward_d<64>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
-    return rgat_backward_d<128>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s);
+    if (d_in == 32) return rgat_backward_d<32>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s, hd);
+    if (d_in == 64) return rgat_backward_d<64>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s, hd);
+    return rgat_backward_d<128>(g, h, W, w_src, w_dst, slope, per_seg, saved, Gm, dh, dW, dws, dwt, ws, s, hd);
 }
 
 }  // namespace rgnn

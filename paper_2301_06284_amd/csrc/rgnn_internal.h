@@ -310,6 +310,14 @@ bool hgt_fused_query_fits(int R, int d, int heads);
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
                                   int heads, float *Wqp, hipStream_t s);
 
+// One head's share of a several-head RGAT backward run as one-head passes:
+// only the output columns [col0, col1) of dW take the outer products (the
+// weights and attention vectors the pass gets are zero outside them), and with
+// acc the pass adds dh, dW, dw_src, dw_dst to what the outputs hold.
+struct BwdHead {
+    int col0 = 0, col1 = 1 << 30, acc = 0;
+};
+
 // RGAT backward (backward.hip), one head.  per_seg: softmax per (dst, rel)
 // segment, saved [U_dst, 2]; else per destination, saved [N, 2].  With
 // need != NULL only stores the workspace bytes the call needs.
@@ -317,7 +325,7 @@ rgnn_status rgat_backward_impl(const rgnn_graph *g, const float *h, const float 
                                const float *w_src, const float *w_dst, int d_in, int d_out,
                                float slope, int per_seg, const float *saved, const float *Gm,
                                float *dh, float *dW, float *dws, float *dwt, void *ws,
-                               size_t ws_bytes, hipStream_t s, size_t *need);
+                               size_t ws_bytes, hipStream_t s, size_t *need, BwdHead hd = BwdHead());
 
 // HGT backward (hgt_backward.hip), the same convention for need.
 rgnn_status hgt_backward_impl(const rgnn_graph *g, const float *h, const float *Wk, const float *Wq,
