@@ -48,7 +48,7 @@ typedef enum {
     RGNN_ERANGE = -2,        /* an id out of range, or a count too large           */
     RGNN_ENOMEM = -3,        /* host or device allocation failed (graph creation)  */
     RGNN_EDEVICE = -4,       /* a HIP runtime call failed                          */
-    RGNN_EUNSUPPORTED = -5   /* valid request this build does not implement        */
+    RGNN_EUNSUPPORTED = -5   /* valid request the library does not implement      */
 } rgnn_status;
 
 /* Which side of the aggregation the relation weight W_r is applied on
