@@ -146,6 +146,28 @@ def test_workload3_hgt():
     assert row_err(got[sel], ref) <= TOL
 
 
+def test_workload3_hgt_saved_and_backward():
+    """The full 21 M-edge HGT layer: the forward's saved softmax statistics
+    leave its output unchanged and satisfy the per-destination properties, and
+    the backward from them agrees with the backward that recomputes them
+    (a property at any size; the oracle checks both on the mid-size graphs)."""
+    g, t, run = load(3)
+    print("workload 3 hgt saved statistics and backward", flush=True)
+    plain = run.hgt(4, 0.25)
+    out, saved = run.hgt(4, 0.25, want_saved=True)
+    np.testing.assert_array_equal(out, plain)
+    check_properties(g, out, saved)
+    del saved
+    a = run.hgt_backward(4, 0.25, use_saved=True)
+    b = run.hgt_backward(4, 0.25, use_saved=False)
+    for k in ("dh", "dWk", "dWq", "dWv", "dWa"):
+        assert np.isfinite(a[k]).all(), k
+        assert row_err(a[k].reshape(-1, 64), b[k].reshape(-1, 64)) <= 1e-5, k
+    for k in ("dWatt", "dWmsg"):
+        assert row_err(a[k].reshape(-1, 16), b[k].reshape(-1, 16)) <= 1e-5, k
+    assert row_err(a["dmu"].reshape(1, -1), b["dmu"].reshape(1, -1)) <= 1e-5
+
+
 @pytest.mark.parametrize("d,heads", [(32, 2), (128, 8)])
 def test_workload3_graph_hgt_hidden_sizes(d, heads):
     """HGT on workload 3's graph with d = 32 and 128 tensors (the
