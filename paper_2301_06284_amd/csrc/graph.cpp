@@ -281,10 +281,14 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             x.out_vseg.resize((size_t)E);
             x.out_rel.resize((size_t)E);
             x.out_pair.resize((size_t)E);
+            x.out_vs.resize((size_t)E);
+            x.out_dst.resize((size_t)E);
             for (int64_t q = 0; q < E; ++q) {
                 x.out_vseg[q] = x.vseg_pos[pos_vseg[x.out_pos[q]]];
                 x.out_rel[q] = x.in_rel[x.out_pos[q]];
                 x.out_pair[q] = x.e2u[x.out_pos[q]];
+                x.out_vs[q] = pos_vseg[x.out_pos[q]];
+                x.out_dst[q] = x.vseg_dst[x.out_vs[q]];
             }
             // work items over out-edges: bundles of small sources, pieces of large ones
             x.oitems.clear();
@@ -394,6 +398,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.vseg_seg, x.vseg_seg);
     add32(&d.out_ptr, x.out_ptr); add32(&d.out_pos, x.out_pos); add32(&d.out_vseg, x.out_vseg);
     add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
+    add32(&d.out_vs, x.out_vs); add32(&d.out_dst, x.out_dst);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
@@ -462,6 +467,7 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         g->host.in_eid.swap(empty.in_eid); g->host.e2u.swap(empty.e2u);
         g->host.out_pos.swap(empty.out_pos); g->host.out_vseg.swap(empty.out_vseg);
         g->host.out_rel.swap(empty.out_rel); g->host.out_pair.swap(empty.out_pair);
+        g->host.out_vs.swap(empty.out_vs); g->host.out_dst.swap(empty.out_dst);
     }
     *out = g;
     return RGNN_OK;

@@ -243,7 +243,8 @@ struct SStageH {
 struct SKArgs {
     int64_t n_items;
     const Item *items;
-    const int32_t *out_ptr, *out_vseg, *vseg_byrel, *vsegdst_byrel;
+    const int32_t *out_ptr;
+    const int32_t *out_vs, *out_dst;   // per out-edge: vseg (QP / dP row) and destination, read in order
     const float *KV, *QP, *dP;
     const float4 *rec;   // [N, H] (max, 1 / sum, s, 0) per destination and head
     float *dKV;          // [N, 3D] dK | dV | dQ rows: dK | dV of split sources zero on entry,
@@ -267,9 +268,8 @@ __global__ __launch_bounds__(256) void hgt_bwd_src_kernel(SKArgs k)
         n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
         split = nn == 1 && k.out_ptr[n0 + 1] - k.out_ptr[n0] > nq;
         for (int e = gl; e < nq; e += G) {
-            const int pos = k.out_vseg[q0 + e];
-            st.ev[e] = k.vseg_byrel[pos];
-            st.et[e] = k.vsegdst_byrel[pos];
+            st.ev[e] = k.out_vs[q0 + e];
+            st.et[e] = k.out_dst[q0 + e];
         }
         auto opos = [&](int jj) {
             const int q = k.out_ptr[n0 + jj];
@@ -636,7 +636,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     if (g->n_oitems > 0) {
         SKArgs k{};
         k.n_items = g->n_oitems; k.items = g->dev.oitems; k.out_ptr = g->dev.out_ptr;
-        k.out_vseg = g->dev.out_vseg; k.vseg_byrel = g->dev.vseg_byrel; k.vsegdst_byrel = g->dev.vsegdst_byrel;
+        k.out_vs = g->dev.out_vs; k.out_dst = g->dev.out_dst;
         k.KV = w.KV; k.QP = w.QP; k.dP = w.dP; k.rec = reinterpret_cast<const float4 *>(w.rec); k.dKV = w.dKV;
         const unsigned nb = blocks_for(g->n_oitems, GPB);
         {

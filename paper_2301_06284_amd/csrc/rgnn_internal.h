@@ -78,6 +78,7 @@ struct HostIndex {
     std::vector<int32_t> rel_pairtileptr;   // compact-pair GEMM tiles per relation [R+1]
     // out-edges (source-major view of the sorted in-edges), for the backward pass
     std::vector<int32_t> out_ptr, out_pos, out_vseg, out_rel, out_pair;
+    std::vector<int32_t> out_vs, out_dst;   // per out-edge: its in-edge's vseg id and destination
     std::vector<int32_t> vseg_pos;       // position of each vseg in the by-relation order
     std::vector<Item> oitems;            // {node0, node1, q0, q1} over out-edge offsets
 };
@@ -111,7 +112,7 @@ struct DeviceIndex {
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
     int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr, *out_rel = nullptr;
-    int32_t *out_pair = nullptr;
+    int32_t *out_pair = nullptr, *out_vs = nullptr, *out_dst = nullptr;
     int32_t *vseg_pos = nullptr;
     Item *oitems = nullptr;
 };
