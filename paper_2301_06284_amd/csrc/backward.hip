@@ -82,6 +82,8 @@ struct BK {
     float *ysum;     // [V]     sum of Y per segment (by-relation order)
     float *dh;       // [N, D]  destination terms written (acc_dh: added) here
     int acc_dh;
+    const int32_t *split_items;   // PHASE 1 without SEG runs over these items only
+    int64_t n_split_items;
 };
 
 template <bool SEG>
@@ -116,7 +118,10 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
     __shared__ BStage<SEG> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     BStage<SEG> &st = stage[gi];
-    const int64_t item = (int64_t)blockIdx.x * GPB + gi;
+    const int64_t gidx = (int64_t)blockIdx.x * GPB + gi;
+    // the second launch of the per-destination softmax serves only the pieces
+    // of split destinations and takes them from their list
+    const int64_t item = PHASE == 1 && !SEG ? (gidx < k.n_split_items ? k.split_items[gidx] : k.n_items) : gidx;
     bool valid = item < k.n_items;
     int dst0 = 0, nd = 0, vs0 = 0, nv = 0, e0 = 0, ne = 0, slot = -1;
     if (valid) {
@@ -917,6 +922,7 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
     k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
     k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs; k.acc_dh = hd.acc;
+    k.split_items = g->dev.split_items; k.n_split_items = g->n_split_items;
     if (g->n_items && per_seg) {
         constexpr int GPB = item_threads(D) / (D / 4);
         const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
@@ -968,7 +974,8 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
             {
                 LaunchScope ls("rgat_bwd_traverse_split", s);
-                hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, false>), grid, dim3(item_threads(D)), 0, s, k);
+                const dim3 sgrid((unsigned)((g->n_split_items + GPB - 1) / GPB));
+                hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, false>), sgrid, dim3(item_threads(D)), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
             {

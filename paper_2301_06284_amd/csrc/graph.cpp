@@ -236,6 +236,10 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             }
         }
         g->n_items = (int64_t)x.items.size();
+        x.split_items.clear();
+        for (int64_t i = 0; i < g->n_items; ++i)
+            if (x.item_slot[i] >= 0) x.split_items.push_back((int32_t)i);
+        g->n_split_items = (int64_t)x.split_items.size();
         g->n_split = (int64_t)x.split_dst.size();
         g->n_slots = slots;
         x.big_split.clear();
@@ -373,7 +377,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.vseg_byrel, x.vseg_byrel); add32(&d.rel_vsegptr, x.rel_vsegptr);
     add32(&d.vsegdst_byrel, x.vsegdst_byrel); add32(&d.rel_chunkptr, x.rel_chunkptr);
     add32(&d.rel_pairtileptr, x.rel_pairtileptr);
-    add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst);
+    add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst); add32(&d.split_items, x.split_items);
     add32(&d.split_slotptr, x.split_slotptr);
     add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
     add32(&d.big_chunkptr, x.big_chunkptr); add32(&d.chunk_lo, x.chunk_lo); add32(&d.chunk_hi, x.chunk_hi);

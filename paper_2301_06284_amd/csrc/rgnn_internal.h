@@ -55,6 +55,7 @@ struct HostIndex {
     std::vector<int32_t> vseg_byrel, rel_vsegptr, vsegdst_byrel;
     std::vector<Item> items;
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
+    std::vector<int32_t> split_items;   // items that are pieces of split destinations (slot >= 0)
     std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
     std::vector<int32_t> big_chunkptr;  // chunks of each big split [n_big_split + 1]
     std::vector<int32_t> chunk_lo, chunk_hi;   // slot range of each chunk [n_big_chunks]
@@ -95,7 +96,7 @@ struct DeviceIndex {
     int32_t *dst_vsegptr = nullptr, *vseg_byrel = nullptr, *rel_vsegptr = nullptr;
     int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr, *rel_pairtileptr = nullptr;
     Item *items = nullptr;
-    int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr;
+    int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr, *split_items = nullptr;
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr, *osplit = nullptr;
@@ -130,7 +131,7 @@ struct rgnn_graph {
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
-    int64_t n_oitems = 0, n_osplit = 0;
+    int64_t n_oitems = 0, n_osplit = 0, n_split_items = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
