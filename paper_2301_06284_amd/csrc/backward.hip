@@ -6,15 +6,25 @@
 // With G = dL/dout, the forward's per-destination softmax maximum M_v and
 // denominator Z_v, and the reordered vectors ws'_r = W_r w_src[r],
 // wt'_r = W_r w_dst[r]:
-//   alpha_e  = exp(leaky(h_u.ws'_r + h_v.wt'_r) - M_v) / Z_v
+//   q_e      = exp(leaky(h_u.ws'_r + h_v.wt'_r) - M_v)
+//   Z'_v     = sum_e q_e,   alpha_e = q_e / Z'_v
 //   dalpha_e = G_v . (h_u W_r) = h_u . dS_{v,r},   dS_{v,r} = G_v W_r^T
-//   s_v      = sum_e alpha_e dalpha_e
+//   s_v      = sum_e alpha_e dalpha_e = S'_v / Z'_v,   S'_v = sum_e q_e dalpha_e
 //   Y_e      = alpha_e (dalpha_e - s_v) leaky'(y_e)
+//            = alpha_e ((dalpha_e Z'_v - S'_v) / Z'_v) leaky'(y_e)
 //   dh_u    += alpha_e dS_{v,r} + Y_e ws'_r       (u as a source)
 //   dh_v    += Y_e wt'_r                          (v as a destination)
 //   dW_r     = sum_seg (sum_e alpha_e h_u)^T G_v  +  dws'_r^T w_src[r] + dwt'_r^T w_dst[r]
 //              with dws'_r = sum_e Y_e h_u,  dwt'_r = sum_e Y_e h_v
 //   dw_src[r] = dws'_r W_r,   dw_dst[r] = dwt'_r W_r
+//
+// The denominator Z'_v is summed here from the backward's own logits rather
+// than taken from the forward (whose logits may round differently, e.g. when
+// they were formed from the message rows): the alpha that enters Y then sums
+// to one in this pass's own arithmetic, and a softmax whose Jacobian vanishes
+// exactly (one in-edge: dalpha Z' - S' = dalpha q - q dalpha = 0) gives an
+// exact zero.  M_v only shifts the exponent.  Sa (below), which is summed
+// before Z'_v is known, takes the forward's Z_v.
 //
 // Kernel sequence:
 //   1. dS by the typed GEMM (B = W_r^T) over the (dst, rel) segments, and the
@@ -57,6 +67,14 @@ __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 __device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ float2 add2(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+// a * b - c with the product rounded on its own (never fused into an FMA), so
+// that a * b - c is exactly 0 whenever c was formed as the rounded product b * a
+__device__ __forceinline__ float mul_sub_exact(float a, float b, float c)
+{
+#pragma clang fp contract(off)
+    return a * b - c;
+}
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 {
@@ -72,12 +90,13 @@ struct BK {
     int64_t n_items;
     const Item *items;
     const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_pos, *in_src;
-    const float *h, *wsp, *wtp, *saved, *dS, *vatt, *sv_in;
+    const float *h, *wsp, *wtp, *saved, *dS, *vatt;
+    const float2 *sv_in;       // [N] merged (S', Z') of split destinations
     const int32_t *vseg_seg;   // per-segment softmax: segment of each vseg (row of saved)
-    float *svs;                // per-segment softmax: [V] s per vseg, then per segment
+    float2 *svs;               // per-segment softmax: [V] (S', Z') per vseg, then per segment
     float slope;
     float *Sa;       // [V, D]  sum alpha h_u per segment (by-relation order)
-    float *ssum;     // [slots] s_v partial of each piece of a split destination
+    float2 *ssum;    // [slots] (S', Z') partial of each piece of a split destination
     float *ay;       // [E, 2]  per sorted in-edge: (alpha, Y); pieces hold (signed alpha, dalpha) in between
     float *ysum;     // [V]     sum of Y per segment (by-relation order)
     float *dh;       // [N, D]  destination terms written (acc_dh: added) here
@@ -95,20 +114,21 @@ struct BStage {
     int vpos[kE];        // by-relation position of each segment (row of dS, Sa, ysum)
     int vdj[kE];         // item-local destination of each segment
     float vatt[kE];      // h_v . wt'_r of each segment, then its sum of Y
-    float ea[kE];        // alpha of each edge, sign bit set where the logit is <= 0
+    float ea[kE];        // q of each edge, sign bit set where the logit is <= 0
     float eda[kE];       // dalpha of each edge
     int dptr[kDst + 1];  // item-local first edge of each destination
-    float dM[kDst], dZi[kDst], dsv[kDst];   // per destination: M_v, 1/Z_v, s_v
+    float dM[kDst], dZi[kDst];   // per destination: the forward's M_v and 1/Z_v
+    float dsv[kDst], dzs[kDst];  // per destination: S'_v and Z'_v of this pass
     float vM[SEG ? kE : 1], vZi[SEG ? kE : 1];   // per segment (per-segment softmax): M, 1/Z
 };
 
 // PHASE 0: every item.  Whole destinations run all passes; pieces of split
-//          destinations run pass 1, leave their part of s_v in ssum and park
-//          (signed alpha, dalpha) in ay.
+//          destinations run pass 1, leave their part of (S', Z') in ssum and park
+//          (signed q, dalpha) in ay.
 // PHASE 1: pieces of split destinations only: pass 2 with the merged s_v (their
 //          destination term is summed by split_dst_term_kernel).
 // SEG (softmax per (dst, rel) segment): PHASE 0 runs pass 1 for every item,
-//          writing each vseg's part of s to svs and parking (alpha, dalpha);
+//          writing each vseg's part of (S', Z') to svs and parking (q, dalpha);
 //          once the parts are summed per segment, PHASE 1 runs passes 2 and 3
 //          for every item (pass 3 for whole destinations only).
 template <int D, int PHASE, bool SEG>
@@ -159,7 +179,11 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
                 const float Z = k.saved[v * 2 + 1];
                 st.dM[j] = k.saved[v * 2];
                 st.dZi[j] = Z > 0.f ? 1.f / Z : 0.f;
-                if (PHASE == 1) st.dsv[j] = k.sv_in[v];
+                if (PHASE == 1) {
+                    const float2 sz = k.sv_in[v];
+                    st.dsv[j] = sz.x;
+                    st.dzs[j] = sz.y;
+                }
             }
         }
         if (gl == 0) st.dptr[nd] = ne;
@@ -179,7 +203,7 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
     if (PHASE == 0 && valid && ne > 0) {
         int j = 0, jv = 0;
         while (st.dptr[j + 1] == st.dptr[j]) ++j;   // first destination with edges
-        float s = 0.f;
+        float s = 0.f, zs = 0.f;
         float4 sa = zero4();
         // ping-pong batches of (source row, ws'_r row, dS row) per edge
         float4 Ah[kU], Aw[kU], Ad[kU], Bh[kU], Bw[kU], Bd[kU];
@@ -203,29 +227,36 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
                 if (e < ne) {
                     const float y = ys + st.vatt[jv];
                     const float z = y > 0.f ? y : k.slope * y;
-                    const float al = SEG ? __expf(z - st.vM[jv]) * st.vZi[jv]
-                                         : __expf(z - st.dM[j]) * st.dZi[j];
-                    s += al * da;
+                    const float q = SEG ? __expf(z - st.vM[jv]) : __expf(z - st.dM[j]);
+                    const float al = q * (SEG ? st.vZi[jv] : st.dZi[j]);   // for Sa only
+                    s += q * da;
+                    zs += q;
                     sa = lin4(sa, 1.f, Xh[u], al);
                     if (gl == 0) {
-                        st.ea[e] = y > 0.f ? al : -al;
+                        st.ea[e] = y > 0.f ? q : -q;
                         st.eda[e] = da;
                     }
                     if (e + 1 == st.vptr[jv + 1]) {
                         st4(k.Sa + (size_t)st.vpos[jv] * D + gl * 4, sa);
                         sa = zero4();
                         if (SEG) {
-                            if (gl == 0) k.svs[vs0 + jv] = s;
+                            if (gl == 0) k.svs[vs0 + jv] = make_float2(s, zs);
                             s = 0.f;
+                            zs = 0.f;
                         }
                         ++jv;
                         if (e + 1 == st.dptr[j + 1]) {
                             if (!SEG) {
                                 if (gl == 0) {
-                                    if (slot < 0) st.dsv[j] = s;
-                                    else k.ssum[slot] = s;
+                                    if (slot < 0) {
+                                        st.dsv[j] = s;
+                                        st.dzs[j] = zs;
+                                    } else {
+                                        k.ssum[slot] = make_float2(s, zs);
+                                    }
                                 }
                                 s = 0.f;
+                                zs = 0.f;
                             }
                             ++j;
                             while (j < nd && st.dptr[j + 1] == st.dptr[j]) ++j;
@@ -258,10 +289,11 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
     if (fin) {
         for (int e = gl; e < ne; e += G) {
             const int jv = st.evs[e];
-            const float sv = SEG ? k.svs[vs0 + jv] : st.dsv[st.vdj[jv]];
+            const float2 sz = SEG ? k.svs[vs0 + jv] : make_float2(st.dsv[st.vdj[jv]], st.dzs[st.vdj[jv]]);
             const float a = st.ea[e];
-            const float al = fabsf(a);
-            const float Y = al * (st.eda[e] - sv) * (signbit(a) ? k.slope : 1.f);
+            const float al = sz.y > 0.f ? fabsf(a) / sz.y : 0.f;
+            const float dz = sz.y > 0.f ? mul_sub_exact(st.eda[e], sz.y, sz.x) / sz.y : 0.f;
+            const float Y = al * dz * (signbit(a) ? k.slope : 1.f);
             reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
             st.eda[e] = Y;
         }
@@ -325,13 +357,13 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
 
 __global__ __launch_bounds__(256) void merge_s_kernel(int64_t n_split, const int32_t *split_dst,
                                                       const int32_t *split_slotptr,
-                                                      const float *ssum, float *sv)
+                                                      const float2 *ssum, float2 *sv)
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n_split) return;
     if (split_slotptr[i + 1] - split_slotptr[i] > kBigRange) return;
-    float s = 0.f;
-    for (int sl = split_slotptr[i]; sl < split_slotptr[i + 1]; ++sl) s += ssum[sl];
+    float2 s = make_float2(0.f, 0.f);
+    for (int sl = split_slotptr[i]; sl < split_slotptr[i + 1]; ++sl) s = add2(s, ssum[sl]);
     sv[split_dst[i]] = s;
 }
 
@@ -340,50 +372,50 @@ __global__ __launch_bounds__(256) void merge_s_kernel(int64_t n_split, const int
 __global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_split,
                                                           const int32_t *split_dst,
                                                           const int32_t *split_slotptr,
-                                                          const float *ssum, float *sv)
+                                                          const float2 *ssum, float2 *sv)
 {
-    __shared__ float part[256];
+    __shared__ float2 part[256];
     const int i = big_split[blockIdx.x];
-    float s = 0.f;
-    for (int sl = split_slotptr[i] + (int)threadIdx.x; sl < split_slotptr[i + 1]; sl += 256) s += ssum[sl];
+    float2 s = make_float2(0.f, 0.f);
+    for (int sl = split_slotptr[i] + (int)threadIdx.x; sl < split_slotptr[i + 1]; sl += 256) s = add2(s, ssum[sl]);
     part[threadIdx.x] = s;
     __syncthreads();
     if (threadIdx.x == 0) {
-        float t = 0.f;
-        for (int j = 0; j < 256; ++j) t += part[j];
+        float2 t = make_float2(0.f, 0.f);
+        for (int j = 0; j < 256; ++j) t = add2(t, part[j]);
         sv[split_dst[i]] = t;
     }
 }
 
-// Per-segment softmax: s of a (dst, rel) segment cut into several vsegs is
-// the sum of its vsegs' parts (in vseg order), written back to each of them.
-__global__ __launch_bounds__(256) void merge_seg_s_kernel(int64_t U, const int32_t *seg_vsegptr, float *svs)
+// Per-segment softmax: (S', Z') of a (dst, rel) segment cut into several
+// vsegs is the sum of its vsegs' parts (in vseg order), written back to each.
+__global__ __launch_bounds__(256) void merge_seg_s_kernel(int64_t U, const int32_t *seg_vsegptr, float2 *svs)
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= U) return;
     const int b = seg_vsegptr[i], e = seg_vsegptr[i + 1];
     if (e - b <= 1 || e - b > kBigRange) return;
-    float s = 0.f;
-    for (int vs = b; vs < e; ++vs) s += svs[vs];
+    float2 s = make_float2(0.f, 0.f);
+    for (int vs = b; vs < e; ++vs) s = add2(s, svs[vs]);
     for (int vs = b; vs < e; ++vs) svs[vs] = s;
 }
 
 // The same for segments with more than kBigRange vsegs: one workgroup each,
 // thread parts added in thread order.
 __global__ __launch_bounds__(256) void merge_seg_s_big_kernel(const int32_t *big_seg, const int32_t *seg_vsegptr,
-                                                              float *svs)
+                                                              float2 *svs)
 {
-    __shared__ float part[256];
-    __shared__ float tot;
+    __shared__ float2 part[256];
+    __shared__ float2 tot;
     const int sg = big_seg[blockIdx.x];
     const int b = seg_vsegptr[sg], e = seg_vsegptr[sg + 1];
-    float s = 0.f;
-    for (int vs = b + (int)threadIdx.x; vs < e; vs += 256) s += svs[vs];
+    float2 s = make_float2(0.f, 0.f);
+    for (int vs = b + (int)threadIdx.x; vs < e; vs += 256) s = add2(s, svs[vs]);
     part[threadIdx.x] = s;
     __syncthreads();
     if (threadIdx.x == 0) {
-        float t = 0.f;
-        for (int i = 0; i < 256; ++i) t += part[i];
+        float2 t = make_float2(0.f, 0.f);
+        for (int i = 0; i < 256; ++i) t = add2(t, part[i]);
         tot = t;
     }
     __syncthreads();
@@ -776,7 +808,8 @@ __global__ void zero_kernel(float *p, int64_t n)
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct BwdWs {
-    float *wsp, *wtp, *vatt, *dS, *Sa, *ssum, *sv, *svs, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
+    float2 *ssum, *sv, *svs;
 };
 
 size_t bwd_layout(const rgnn_graph *g, int D, void *base, BwdWs *w)
@@ -795,9 +828,9 @@ size_t bwd_layout(const rgnn_graph *g, int D, void *base, BwdWs *w)
     x.vatt = take((size_t)std::max<int64_t>(g->V, 1));
     x.dS = take((size_t)g->V * D);
     x.Sa = take((size_t)g->V * D);
-    x.ssum = take((size_t)std::max<int64_t>(g->n_slots, 1));
-    x.sv = take((size_t)std::max<int64_t>(g->N, 1));
-    x.svs = take((size_t)std::max<int64_t>(g->V, 1));
+    x.ssum = (float2 *)take((size_t)std::max<int64_t>(g->n_slots, 1) * 2);
+    x.sv = (float2 *)take((size_t)std::max<int64_t>(g->N, 1) * 2);
+    x.svs = (float2 *)take((size_t)std::max<int64_t>(g->V, 1) * 2);
     x.ay = take((size_t)g->E * 2);
     x.ysum = take((size_t)std::max<int64_t>(g->V, 1));
     x.ypair = take((size_t)std::max<int64_t>(g->U_src, 1));

@@ -111,11 +111,12 @@ class Runner:
             return out.cpu().numpy(), saved
         return out.cpu().numpy()
 
-    def rgat_backward(self, slope=0.2, heads=1, scope=0):
+    def rgat_backward(self, slope=0.2, heads=1, scope=0, plan=0):
+        """plan: the forward plan whose saved statistics the backward takes."""
         T, torch, rgnn = self.T, self.torch, self.rgnn
         d = T["W"].shape[1]
         R = T["W"].shape[0]
-        _, saved = self.rgat(heads=heads, slope=slope, want_saved=True, scope=scope)
+        _, saved = self.rgat(heads=heads, slope=slope, want_saved=True, scope=scope, plan=plan)
         gh = torch.full((self.g["N"], d), float("nan"), device=self.dev)
         gW = torch.full((R, d, d), float("nan"), device=self.dev)
         gs = torch.full((R, d), float("nan"), device=self.dev)

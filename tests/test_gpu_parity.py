@@ -462,17 +462,17 @@ def test_rgat_backward_multihead(kind, heads):
 
 def test_rgat_backward_multihead_mid_size():
     """Four heads on a 200k-edge graph with hubs (split destinations and
-    sources with many out-edges), every gradient in full.
+    sources with many out-edges), every gradient in full, at the standard
+    cancellation floor.
 
-    The backward takes alpha from the forward's saved (max, sum); the
-    multi-head forward (transform-first) rounds its logits along another path
-    than the backward's reordered recomputation, so alpha carries a relative
-    error of about |z| * 2^-24.  A handful of sources here have only out-edges
-    into the 10^5-edge hub (each contribution scaled by alpha ~ 1e-5) and one
-    in-edge (an exactly cancelling one-edge softmax Jacobian): their dh norm is
-    ~1e-5 of the median and holds that rounding at the scale of alpha |dalpha|.
-    Rows below 1e-3 of the median norm are measured against 1e-3 of the median
-    (an absolute error of 1e-7 of the median row)."""
+    The multi-head forward (transform-first) forms its logits from the message
+    rows, the backward from h . (W_r w_src): the two round differently.  The
+    backward sums its own softmax denominator, so its alpha sums to one in its
+    own arithmetic.  This graph has sources whose only out-edges enter the
+    10^5-edge hub (dh norm ~1e-5 of the median) and whose one in-edge forms a
+    one-edge softmax, whose Jacobian is exactly zero: with alpha normalised by
+    the forward's denominator instead, that zero came out as ~1e-7 |dalpha|,
+    a 3e-4 row error."""
     g = workloads.tiny_graph(46, N=20000, E=200000, R=12, T=2, kind="hub")
     t = workloads.tiny_tensors(46, g, 64, 64, heads=4, att_var=1.0)
     print("rgat backward heads=4 mid size", flush=True)
@@ -481,9 +481,26 @@ def test_rgat_backward_multihead_mid_size():
     run.close()
     dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=4)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
-    nrm = np.linalg.norm(dh, axis=1)
-    assert (nrm < 1e-3 * np.median(nrm)).sum() <= 10   # the rows described above, no more
-    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-3) <= TOL
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    assert row_err(gs, dws) <= TOL
+    assert row_err(gt, dwt) <= TOL
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_rgat_backward_mid_size_one_head(plan):
+    """The graph above with one head, from the saved statistics of either
+    forward plan (transform-first forms the source logit from the message
+    row, aggregate-first from h . (W_r w_src)), standard cancellation floor."""
+    g = workloads.tiny_graph(46, N=20000, E=200000, R=12, T=2, kind="hub")
+    t = workloads.tiny_tensors(46, g, 64, 64, heads=1, att_var=1.0)
+    print(f"rgat backward heads=1 mid size forward plan={plan}", flush=True)
+    run = Runner(g, t)
+    gh, gW, gs, gt = run.rgat_backward(heads=1, plan=plan)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
     assert row_err(gs, dws) <= TOL
     assert row_err(gt, dwt) <= TOL
