@@ -58,7 +58,7 @@ def _load():
                                               i32, vp, vp, vp, vp, vp, vp]
         _lib.oracle_hgt_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                              vp, vp, vp, vp, vp, vp, vp, f64, i32, i32, vp, vp,
-                                             vp, vp, vp, vp, vp, vp, vp]
+                                             vp, vp, vp, vp, vp, vp, vp, vp, vp]
         for f in ("oracle_rgcn_forward", "oracle_rgat_forward", "oracle_hgt_forward",
                   "oracle_rgat_backward", "oracle_rgcn_backward", "oracle_hgt_backward",
                   "oracle_num_threads"):
@@ -201,10 +201,13 @@ def rgcn_backward(g, h, W, W0, grad_out, relu=False, node_mask=None, rel_mask=No
 
 
 def hgt_backward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, grad_out, heads, att_scale=None,
-                 residual=True, a_linear=True):
+                 residual=True, a_linear=True, node_mask=None, rel_mask=None):
     """Gradients of L = sum(out * grad_out) of the HGT layer (chain rule of its
     definition).  Returns a dict with dh, dWk, dWq, dWv, dWa (None without the
-    output linear), dWatt, dWmsg, dmu."""
+    output linear), dWatt, dWmsg, dmu.  node_mask / rel_mask (uint8 [N] / [R],
+    optional): dh only for the flagged nodes, dWatt / dWmsg / dmu only for the
+    flagged relations; with either mask the node-type weight gradients are
+    left zero."""
     h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, G = map(_f32, (h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, grad_out))
     src, dst, rel, nt = _i32(g["src"]), _i32(g["dst"]), _i32(g["rel"]), _i32(g["ntype"])
     N, R, T = g["N"], g["R"], g["T"]
@@ -216,10 +219,12 @@ def hgt_backward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, grad_out, heads, att_scal
                dWv=np.zeros((T, d, d)), dWa=np.zeros((T, d, d)) if a_linear else None,
                dWatt=np.zeros((R, heads, dk, dk)), dWmsg=np.zeros((R, heads, dk, dk)),
                dmu=np.zeros(R))
+    nm = None if node_mask is None else np.ascontiguousarray(node_mask, np.uint8)
+    rm = None if rel_mask is None else np.ascontiguousarray(rel_mask, np.uint8)
     rc = _load().oracle_hgt_backward(N, g["E"], R, T, d, heads, _p(src), _p(dst), _p(rel), _p(nt),
                                      _p(h), _p(Wk), _p(Wq), _p(Wv), _p(Wa), _p(Watt), _p(Wmsg),
                                      _p(mu), float(att_scale), int(bool(residual)),
-                                     int(bool(a_linear)), _p(G), _p(out["dh"]), _p(out["dWk"]),
+                                     int(bool(a_linear)), _p(G), _p(nm), _p(rm), _p(out["dh"]), _p(out["dWk"]),
                                      _p(out["dWq"]), _p(out["dWv"]), _p(out["dWa"]),
                                      _p(out["dWatt"]), _p(out["dWmsg"]), _p(out["dmu"]))
     _check(rc, "hgt_backward")

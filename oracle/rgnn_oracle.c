@@ -449,7 +449,150 @@ int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
  * node_mask (nullable): compute dh only for nodes with node_mask[n] != 0
  * rel_mask  (nullable): compute dW, dw_src, dw_dst only for those relations.
  * Entries outside the masks are left at zero.  Only destinations that feed a
- * requested entry are visited. */
+ * requested entry are visited.
+ *
+ * Every sum over edges runs in one fixed order, the "global edge order":
+ * destinations in increasing id, each destination's in-edges in increasing
+ * edge id.  The work is spread over threads in three stages, none of which
+ * changes that order for any output entry:
+ *   A. per destination (threads over destinations): the forward recomputed
+ *      edge by edge, the softmax, dalpha, s and Y; alpha and Y are kept per
+ *      edge;
+ *   B. per requested relation (threads over relations x blocks of output
+ *      rows or columns): dW_r, dw_src[r], dw_dst[r] summed over r's edges in
+ *      the global order, with m_e and t_e recomputed from h and W_r;
+ *   C. per requested node n (threads over nodes): dh_n summed over the edges
+ *      that touch n in the global order (an edge that is both an out-edge and
+ *      an in-edge of n adds its source term first). */
+typedef struct {
+    int64_t N, E;
+    int32_t R, d_in, d_out, H, scope;
+    const int32_t *src, *dst, *rel;
+    const float *h, *W, *w_src, *w_dst, *G;
+    double slope;
+    const in_lists *a;
+    double *AL, *YY;   /* [E, H] alpha and Y by edge id */
+} rgat_bwd_ctx;
+
+typedef struct {
+    double *msg, *t, *al, *y, *da, *mx, *sm, *sv;
+    int64_t cap;
+} rgat_bwd_scratch;
+
+static int rgat_bwd_reserve(rgat_bwd_scratch *s, int64_t deg, int d_out, int H, int R)
+{
+    if (!s->mx) {
+        s->mx = (double *)malloc((size_t)R * H * sizeof(double));
+        s->sm = (double *)malloc((size_t)R * H * sizeof(double));
+        s->sv = (double *)malloc((size_t)R * H * sizeof(double));
+        if (!s->mx || !s->sm || !s->sv) return -3;
+    }
+    if (deg <= s->cap) return 0;
+    free(s->msg); free(s->t); free(s->al); free(s->y); free(s->da);
+    s->cap = deg;
+    s->msg = (double *)malloc((size_t)deg * d_out * sizeof(double));
+    s->t = (double *)malloc((size_t)deg * d_out * sizeof(double));
+    s->al = (double *)malloc((size_t)deg * H * sizeof(double));
+    s->y = (double *)malloc((size_t)deg * H * sizeof(double));
+    s->da = (double *)malloc((size_t)deg * H * sizeof(double));
+    if (!s->msg || !s->t || !s->al || !s->y || !s->da) { s->cap = 0; return -3; }
+    return 0;
+}
+
+static void rgat_bwd_scratch_free(rgat_bwd_scratch *s)
+{
+    free(s->msg); free(s->t); free(s->al); free(s->y); free(s->da);
+    free(s->mx); free(s->sm); free(s->sv);
+}
+
+/* Stage A for destination v: alpha and Y of its in-edges.  inner: spread the
+ * per-edge recomputation over threads (for destinations with many edges). */
+static int rgat_bwd_dst(const rgat_bwd_ctx *c, int64_t v, int inner, rgat_bwd_scratch *sc)
+{
+    const int H = c->H, d_in = c->d_in, d_out = c->d_out, dh_ = d_out / H;
+    const int64_t p0 = c->a->ptr[v], deg = c->a->ptr[v + 1] - p0;
+    if (deg == 0) return 0;
+    if (rgat_bwd_reserve(sc, deg, d_out, H, c->R)) return -3;
+    double xv[512];
+    load_row(c->h, v, d_in, xv);
+    double *msg = sc->msg, *t = sc->t, *al = sc->al, *Y = sc->y, *dal = sc->da;
+    /* forward recomputation: messages, t_e, logits */
+#pragma omp parallel for schedule(static) if (inner)
+    for (int64_t q = 0; q < deg; ++q) {
+        double xl[512];
+        const int64_t e = c->a->eid[p0 + q];
+        const int r = c->rel[e];
+        const float *Wr = c->W + (size_t)r * d_in * d_out;
+        load_row(c->h, c->src[e], d_in, xl);
+        vecmat(xl, Wr, d_in, d_out, 0, d_out, msg + q * d_out);
+        vecmat(xv, Wr, d_in, d_out, 0, d_out, t + q * d_out);
+        for (int k = 0; k < H; ++k) {
+            double y = 0.0;
+            for (int j = k * dh_; j < (k + 1) * dh_; ++j)
+                y += msg[q * d_out + j] * (double)c->w_src[(size_t)r * d_out + j] +
+                     t[q * d_out + j] * (double)c->w_dst[(size_t)r * d_out + j];
+            Y[q * H + k] = y;          /* pre-activation, kept for the derivative */
+            al[q * H + k] = y > 0.0 ? y : c->slope * y;
+        }
+    }
+    double *mx = sc->mx, *sm = sc->sm, *sv = sc->sv;
+#define GRP(q) ((c->scope ? c->rel[c->a->eid[p0 + (q)]] : 0) * H)
+    for (int64_t q = 0; q < deg; ++q)
+        for (int k = 0; k < H; ++k) { mx[GRP(q) + k] = -INFINITY; sm[GRP(q) + k] = 0.0; sv[GRP(q) + k] = 0.0; }
+    for (int64_t q = 0; q < deg; ++q)
+        for (int k = 0; k < H; ++k) if (al[q * H + k] > mx[GRP(q) + k]) mx[GRP(q) + k] = al[q * H + k];
+    for (int64_t q = 0; q < deg; ++q)
+        for (int k = 0; k < H; ++k) sm[GRP(q) + k] += exp(al[q * H + k] - mx[GRP(q) + k]);
+    for (int64_t q = 0; q < deg; ++q)
+        for (int k = 0; k < H; ++k) al[q * H + k] = exp(al[q * H + k] - mx[GRP(q) + k]) / sm[GRP(q) + k];
+    /* dalpha and s (per normalisation group) */
+    const float *Gv = c->G + (size_t)v * d_out;
+    for (int64_t q = 0; q < deg; ++q)
+        for (int k = 0; k < H; ++k) {
+            double da = 0.0;
+            for (int j = k * dh_; j < (k + 1) * dh_; ++j) da += (double)Gv[j] * msg[q * d_out + j];
+            sv[GRP(q) + k] += al[q * H + k] * da;
+            dal[q * H + k] = da;
+        }
+    for (int64_t q = 0; q < deg; ++q) {
+        const int64_t e = c->a->eid[p0 + q];
+        for (int k = 0; k < H; ++k) {
+            const double y = Y[q * H + k];
+            const double dz = al[q * H + k] * (dal[q * H + k] - sv[GRP(q) + k]);
+            c->AL[e * H + k] = al[q * H + k];
+            c->YY[e * H + k] = dz * (y > 0.0 ? 1.0 : c->slope);
+        }
+    }
+#undef GRP
+    return 0;
+}
+
+/* dm_e (message and source-attention paths) and dt_e (destination-attention
+ * path) of edge e, from its alpha and Y. */
+static void rgat_bwd_edge_grads(const rgat_bwd_ctx *c, int64_t e, double *dm, double *dtv)
+{
+    const int H = c->H, d_out = c->d_out, dh_ = d_out / H;
+    const int r = c->rel[e];
+    const float *Gv = c->G + (size_t)c->dst[e] * d_out;
+    for (int j = 0; j < d_out; ++j) {
+        const int k = j / dh_;
+        if (dm) dm[j] = c->AL[e * H + k] * (double)Gv[j] + c->YY[e * H + k] * (double)c->w_src[(size_t)r * d_out + j];
+        if (dtv) dtv[j] = c->YY[e * H + k] * (double)c->w_dst[(size_t)r * d_out + j];
+    }
+}
+
+/* dst_row[i] += sum_j W_r[i][j] g[j] */
+static void add_matvec_t(const float *Wr, int d_in, int d_out, const double *g, double *dst_row)
+{
+    for (int i = 0; i < d_in; ++i) {
+        double s = 0.0;
+        for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * g[j];
+        dst_row[i] += s;
+    }
+}
+
+#define RGAT_BWD_ROWS 8   /* dW rows, or dw columns, per stage-B job */
+
 int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t d_out,
                          int32_t heads, const int32_t *src, const int32_t *dst,
                          const int32_t *rel, const float *h, const float *W,
@@ -459,147 +602,137 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
                          double *dw_dst)
 {
     if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_in > 512 || d_out <= 0 ||
-        heads <= 0 || d_out % heads)
+        d_out > 512 || heads <= 0 || d_out % heads)
         return -1;
-    const int H = heads, dh_ = d_out / heads;
+    const int H = heads;
     in_lists a;
     int rc = build_in_lists(N, E, dst, &a);
     if (rc) { free_in_lists(&a); return rc; }
-    /* destinations whose in-edges contribute to a requested entry */
-    uint8_t *need = (uint8_t *)calloc((size_t)(N > 0 ? N : 1), 1);
-    if (!need) { free_in_lists(&a); return -3; }
-    for (int64_t e = 0; e < E; ++e) {
-        const int want_rel = rel_mask ? rel_mask[rel[e]] != 0 : 1;
-        const int want_node = node_mask ? (node_mask[src[e]] || node_mask[dst[e]]) : 1;
-        if (want_rel || want_node) need[dst[e]] = 1;
-    }
     memset(dh, 0, (size_t)N * d_in * sizeof(double));
     memset(dW, 0, (size_t)R * d_in * d_out * sizeof(double));
     memset(dw_src, 0, (size_t)R * d_out * sizeof(double));
     memset(dw_dst, 0, (size_t)R * d_out * sizeof(double));
-    int err = 0;
-    /* Destinations are processed one at a time in increasing id; the work of a
-     * destination is split over threads by output entry, so every sum is
-     * accumulated in a fixed order. */
-    double *msg = NULL, *t = NULL, *al = NULL, *Y = NULL, *dm = NULL, *dtv = NULL;
-    int64_t cap = 0;
-    double *xv = (double *)malloc((size_t)d_in * sizeof(double));
-    double *x = (double *)malloc((size_t)d_in * sizeof(double));
-    /* softmax statistics and s per normalisation group and head: one group per
-     * destination (scope 0) or per (destination, relation) segment (scope 1),
-     * indexed by the relation */
-    const int NGRP = scope ? R : 1;
-    double *mx = (double *)malloc((size_t)NGRP * H * sizeof(double));
-    double *sm = (double *)malloc((size_t)NGRP * H * sizeof(double));
-    double *sv = (double *)malloc((size_t)NGRP * H * sizeof(double));
-    if (!xv || !x || !mx || !sm || !sv) err = 1;
-    for (int64_t v = 0; v < N && !err; ++v) {
-        if (!need[v]) continue;
-        const int64_t p0 = a.ptr[v], deg = a.ptr[v + 1] - p0;
-        if (deg == 0) continue;
-        if (deg > cap) {
-            free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
-            cap = deg;
-            msg = (double *)malloc((size_t)cap * d_out * sizeof(double));
-            t = (double *)malloc((size_t)cap * d_out * sizeof(double));
-            al = (double *)malloc((size_t)cap * H * sizeof(double));
-            Y = (double *)malloc((size_t)cap * H * sizeof(double));
-            dm = (double *)malloc((size_t)cap * d_out * sizeof(double));
-            dtv = (double *)malloc((size_t)cap * d_out * sizeof(double));
-            if (!msg || !t || !al || !Y || !dm || !dtv) { err = 1; break; }
+    /* destinations whose in-edges contribute to a requested entry */
+    const size_t E1 = (size_t)(E > 0 ? E : 1), N1 = (size_t)(N > 0 ? N : 1);
+    uint8_t *need = (uint8_t *)calloc(N1, 1);
+    double *AL = (double *)malloc(E1 * H * sizeof(double));
+    double *YY = (double *)malloc(E1 * H * sizeof(double));
+    int64_t *relptr = (int64_t *)calloc((size_t)R + 1, sizeof(int64_t));
+    int64_t *reledge = (int64_t *)malloc(E1 * sizeof(int64_t));
+    int64_t *outptr = (int64_t *)calloc(N1 + 1, sizeof(int64_t));
+    int64_t *outpos = (int64_t *)malloc(E1 * sizeof(int64_t));
+    int err = !need || !AL || !YY || !relptr || !reledge || !outptr || !outpos;
+    if (!err) {
+        for (int64_t e = 0; e < E; ++e) {
+            const int want_rel = rel_mask ? rel_mask[rel[e]] != 0 : 1;
+            const int want_node = node_mask ? (node_mask[src[e]] || node_mask[dst[e]]) : 1;
+            if (want_rel || want_node) need[dst[e]] = 1;
         }
-        load_row(h, v, d_in, xv);
-        /* forward recomputation: messages, t_e, logits, softmax */
-#pragma omp parallel for schedule(static) if (deg >= 64)
-        for (int64_t q = 0; q < deg; ++q) {
-            double xl[512];
-            const int64_t e = a.eid[p0 + q];
-            const int r = rel[e];
+        /* relations' edge lists and sources' out-edge positions, both in the
+         * global edge order (positions p index a.eid) */
+        for (int64_t e = 0; e < E; ++e) { relptr[rel[e] + 1]++; outptr[src[e] + 1]++; }
+        for (int r = 0; r < R; ++r) relptr[r + 1] += relptr[r];
+        for (int64_t n = 0; n < N; ++n) outptr[n + 1] += outptr[n];
+        int64_t *rf = (int64_t *)malloc((size_t)R * sizeof(int64_t));
+        int64_t *of = (int64_t *)malloc(N1 * sizeof(int64_t));
+        if (!rf || !of) {
+            err = 1;
+        } else {
+            memcpy(rf, relptr, (size_t)R * sizeof(int64_t));
+            memcpy(of, outptr, (size_t)N * sizeof(int64_t));
+            for (int64_t p = 0; p < E; ++p) {
+                const int64_t e = a.eid[p];
+                reledge[rf[rel[e]]++] = e;
+                outpos[of[src[e]]++] = p;
+            }
+        }
+        free(rf); free(of);
+    }
+    rgat_bwd_ctx c = {N, E, R, d_in, d_out, H, scope, src, dst, rel, h, W, w_src, w_dst, G,
+                      neg_slope, &a, AL, YY};
+    /* stage A */
+    if (!err) {
+#pragma omp parallel reduction(| : err)
+        {
+            rgat_bwd_scratch sc = {0};
+#pragma omp for schedule(dynamic, 16)
+            for (int64_t v = 0; v < N; ++v)
+                if (need[v] && a.ptr[v + 1] - a.ptr[v] <= BIG_ROW && rgat_bwd_dst(&c, v, 0, &sc)) err = 1;
+            rgat_bwd_scratch_free(&sc);
+        }
+    }
+    if (!err) {
+        rgat_bwd_scratch sc = {0};
+        for (int64_t v = 0; v < N && !err; ++v)
+            if (need[v] && a.ptr[v + 1] - a.ptr[v] > BIG_ROW && rgat_bwd_dst(&c, v, 1, &sc)) err = 1;
+        rgat_bwd_scratch_free(&sc);
+    }
+    /* stage B: jobs (relation, block of dW rows) then (relation, block of dw columns) */
+    if (!err) {
+        const int nbi = (d_in + RGAT_BWD_ROWS - 1) / RGAT_BWD_ROWS;
+        const int nbj = (d_out + RGAT_BWD_ROWS - 1) / RGAT_BWD_ROWS;
+        const int64_t njobs = (int64_t)R * (nbi + nbj);
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t job = 0; job < njobs; ++job) {
+            const int r = (int)(job / (nbi + nbj)), b = (int)(job % (nbi + nbj));
+            if (rel_mask && !rel_mask[r]) continue;
             const float *Wr = W + (size_t)r * d_in * d_out;
-            for (int i = 0; i < d_in; ++i) xl[i] = (double)h[(size_t)src[e] * d_in + i];
-            vecmat(xl, Wr, d_in, d_out, 0, d_out, msg + q * d_out);
-            vecmat(xv, Wr, d_in, d_out, 0, d_out, t + q * d_out);
-            for (int k = 0; k < H; ++k) {
-                double y = 0.0;
-                for (int j = k * dh_; j < (k + 1) * dh_; ++j)
-                    y += msg[q * d_out + j] * (double)w_src[(size_t)r * d_out + j] +
-                         t[q * d_out + j] * (double)w_dst[(size_t)r * d_out + j];
-                Y[q * H + k] = y;          /* pre-activation, reused below */
-                al[q * H + k] = y > 0.0 ? y : neg_slope * y;
-            }
-        }
-#define GRP(q) ((scope ? rel[a.eid[p0 + (q)]] : 0) * H)
-        for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) { mx[GRP(q) + k] = -INFINITY; sm[GRP(q) + k] = 0.0; sv[GRP(q) + k] = 0.0; }
-        for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) if (al[q * H + k] > mx[GRP(q) + k]) mx[GRP(q) + k] = al[q * H + k];
-        for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) sm[GRP(q) + k] += exp(al[q * H + k] - mx[GRP(q) + k]);
-        for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) al[q * H + k] = exp(al[q * H + k] - mx[GRP(q) + k]) / sm[GRP(q) + k];
-        /* dalpha and s (per normalisation group) */
-        const float *Gv = G + (size_t)v * d_out;
-        for (int64_t q = 0; q < deg; ++q)
-            for (int k = 0; k < H; ++k) {
-                double da = 0.0;
-                for (int j = k * dh_; j < (k + 1) * dh_; ++j) da += (double)Gv[j] * msg[q * d_out + j];
-                sv[GRP(q) + k] += al[q * H + k] * da;
-                dm[q * d_out + k * dh_] = da;   /* stash dalpha in the first slot */
-            }
-        for (int64_t q = 0; q < deg; ++q) {
-            const int64_t e = a.eid[p0 + q];
-            const int r = rel[e];
-            for (int k = 0; k < H; ++k) {
-                const double y = Y[q * H + k];
-                const double da = dm[q * d_out + k * dh_];
-                const double dz = al[q * H + k] * (da - sv[GRP(q) + k]);
-                Y[q * H + k] = dz * (y > 0.0 ? 1.0 : neg_slope);
-            }
-            for (int j = 0; j < d_out; ++j) {
-                const int k = j / dh_;
-                dm[q * d_out + j] = al[q * H + k] * (double)Gv[j] + Y[q * H + k] * (double)w_src[(size_t)r * d_out + j];
-                dtv[q * d_out + j] = Y[q * H + k] * (double)w_dst[(size_t)r * d_out + j];
-            }
-        }
-        /* scatter in edge-id order; parallel over output entries */
-        for (int64_t q = 0; q < deg; ++q) {
-            const int64_t e = a.eid[p0 + q];
-            const int r = rel[e];
-            const int64_t u = src[e];
-            const float *Wr = W + (size_t)r * d_in * d_out;
-            if (!rel_mask || rel_mask[r]) {
-#pragma omp parallel for schedule(static) if (d_in * d_out >= 1 << 16)
-                for (int i = 0; i < d_in; ++i) {
-                    const double hu = (double)h[(size_t)u * d_in + i], hv = xv[i];
-                    double *row = dW + ((size_t)r * d_in + i) * d_out;
-                    for (int j = 0; j < d_out; ++j) row[j] += hu * dm[q * d_out + j] + hv * dtv[q * d_out + j];
+            double dm[512], dtv[512], xu[512], xv[512], mb[RGAT_BWD_ROWS], tb[RGAT_BWD_ROWS];
+            if (b < nbi) {
+                const int i0 = b * RGAT_BWD_ROWS, i1 = i0 + RGAT_BWD_ROWS < d_in ? i0 + RGAT_BWD_ROWS : d_in;
+                for (int64_t q = relptr[r]; q < relptr[r + 1]; ++q) {
+                    const int64_t e = reledge[q];
+                    rgat_bwd_edge_grads(&c, e, dm, dtv);
+                    for (int i = i0; i < i1; ++i) {
+                        const double hu = (double)h[(size_t)src[e] * d_in + i];
+                        const double hv = (double)h[(size_t)dst[e] * d_in + i];
+                        double *row = dW + ((size_t)r * d_in + i) * d_out;
+                        for (int j = 0; j < d_out; ++j) row[j] += hu * dm[j] + hv * dtv[j];
+                    }
                 }
-                for (int j = 0; j < d_out; ++j) {
-                    const int k = j / dh_;
-                    dw_src[(size_t)r * d_out + j] += Y[q * H + k] * msg[q * d_out + j];
-                    dw_dst[(size_t)r * d_out + j] += Y[q * H + k] * t[q * d_out + j];
-                }
-            }
-            if (!node_mask || node_mask[u]) {
-                for (int i = 0; i < d_in; ++i) {
-                    double s = 0.0;
-                    for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * dm[q * d_out + j];
-                    dh[(size_t)u * d_in + i] += s;
-                }
-            }
-            if (!node_mask || node_mask[v]) {
-                for (int i = 0; i < d_in; ++i) {
-                    double s = 0.0;
-                    for (int j = 0; j < d_out; ++j) s += (double)Wr[(size_t)i * d_out + j] * dtv[q * d_out + j];
-                    dh[(size_t)v * d_in + i] += s;
+            } else {
+                const int j0 = (b - nbi) * RGAT_BWD_ROWS;
+                const int nj = j0 + RGAT_BWD_ROWS < d_out ? RGAT_BWD_ROWS : d_out - j0;
+                const int dh_ = d_out / H;
+                for (int64_t q = relptr[r]; q < relptr[r + 1]; ++q) {
+                    const int64_t e = reledge[q];
+                    load_row(h, src[e], d_in, xu);
+                    load_row(h, dst[e], d_in, xv);
+                    vecmat(xu, Wr, d_in, d_out, j0, nj, mb);
+                    vecmat(xv, Wr, d_in, d_out, j0, nj, tb);
+                    for (int jj = 0; jj < nj; ++jj) {
+                        const double y = YY[e * H + (j0 + jj) / dh_];
+                        dw_src[(size_t)r * d_out + j0 + jj] += y * mb[jj];
+                        dw_dst[(size_t)r * d_out + j0 + jj] += y * tb[jj];
+                    }
                 }
             }
         }
     }
-#undef GRP
-    (void)x;
-    free(msg); free(t); free(al); free(Y); free(dm); free(dtv);
-    free(xv); free(x); free(mx); free(sm); free(sv); free(need);
+    /* stage C: dh of the requested nodes, merging each node's out-edges and
+     * in-edges by their position in the global order */
+    if (!err) {
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t n = 0; n < N; ++n) {
+            if (node_mask && !node_mask[n]) continue;
+            double g[512];
+            double *row = dh + (size_t)n * d_in;
+            int64_t po = outptr[n], pi = a.ptr[n];
+            const int64_t po1 = outptr[n + 1], pi1 = a.ptr[n + 1];
+            while (po < po1 || pi < pi1) {
+                if (po < po1 && (pi >= pi1 || outpos[po] <= pi)) {   /* n as the source */
+                    const int64_t e = a.eid[outpos[po++]];
+                    rgat_bwd_edge_grads(&c, e, g, NULL);
+                    add_matvec_t(W + (size_t)rel[e] * d_in * d_out, d_in, d_out, g, row);
+                } else {                                             /* n as the destination */
+                    const int64_t e = a.eid[pi++];
+                    rgat_bwd_edge_grads(&c, e, NULL, g);
+                    add_matvec_t(W + (size_t)rel[e] * d_in * d_out, d_in, d_out, g, row);
+                }
+            }
+        }
+    }
+    free(need); free(AL); free(YY); free(relptr); free(reledge); free(outptr); free(outpos);
     free_in_lists(&a);
     return err ? -3 : 0;
 }
@@ -716,50 +849,156 @@ int oracle_rgcn_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
  *   for every node n (X in K, Q, V):
  *     dWx[tau(n)] += h_n^T dX_n;  dh_n += dX_n Wx[tau(n)]^T
  * K, Q, V are computed once per node (node-level linears); every edge term is
- * computed per edge.  Sums run over destinations in increasing id, their
- * in-edges in edge-id order, then over nodes in increasing id.  dWa may be
+ * computed per edge.  Every sum over edges runs in the global edge order
+ * (destinations in increasing id, each one's in-edges in increasing edge id),
+ * every sum over nodes in increasing node id.  The work is spread over
+ * threads in stages that keep those orders for every output entry:
+ *   A. per destination: scores, softmax, messages, agg, dagg, s; alpha, da
+ *      and kw . Q kept per edge, dQ per destination;
+ *   B. per relation (and head, and row of the head block): dWatt, dWmsg,
+ *      dmu over the relation's edges; per node type and row: dWa;
+ *   C. per source: dK and dV over its out-edges;
+ *   D. per node type, projection and row: dWk, dWq, dWv; per node: dh.
+ * node_mask (nullable): dh only for those nodes; rel_mask (nullable): dWatt,
+ * dWmsg and dmu only for those relations.  With either mask the node-type
+ * weight gradients (dWk, dWq, dWv, dWa) are not computed (left zero), and
+ * only the destinations that feed a requested entry are visited.  dWa may be
  * NULL when a_linear is 0. */
+typedef struct {
+    int64_t N, E;
+    int32_t R, T, d, H;
+    const int32_t *src, *dst, *rel, *ntype;
+    const float *Wa, *Watt, *Wmsg, *mu, *G;
+    double att_scale;
+    int32_t a_linear;
+    const in_lists *a;
+    const double *K, *Q, *V;
+    double *agg, *dagg, *dQ;     /* [N, d] */
+    double *AL, *DA, *KQ;        /* [E, H] alpha, da and kw . Q by edge id */
+} hgt_bwd_ctx;
+
+static int hgt_bwd_dst(const hgt_bwd_ctx *c, int64_t t, double **kwbuf, double **msgbuf, double **albuf,
+                       double **dalbuf, int64_t *cap)
+{
+    const int H = c->H, d = c->d, dk = d / H;
+    const int64_t p0 = c->a->ptr[t], deg = c->a->ptr[t + 1] - p0;
+    if (deg > *cap) {
+        free(*kwbuf); free(*msgbuf); free(*albuf); free(*dalbuf);
+        *cap = deg;
+        *kwbuf = (double *)malloc((size_t)deg * d * sizeof(double));
+        *msgbuf = (double *)malloc((size_t)deg * d * sizeof(double));
+        *albuf = (double *)malloc((size_t)deg * H * sizeof(double));
+        *dalbuf = (double *)malloc((size_t)deg * H * sizeof(double));
+        if (!*kwbuf || !*msgbuf || !*albuf || !*dalbuf) { *cap = 0; return -3; }
+    }
+    double *kw = *kwbuf, *msg = *msgbuf, *al = *albuf, *dal = *dalbuf;
+    const float *Gt = c->G + (size_t)t * d;
+    const double *Qt = c->Q + (size_t)t * d;
+    double *agg = c->agg + (size_t)t * d, *dagg = c->dagg + (size_t)t * d, *dQt = c->dQ + (size_t)t * d;
+    double mx[64], sm[64], sv[64];
+    /* forward: scores, softmax, messages, agg */
+    for (int64_t p = 0; p < deg; ++p) {
+        const int64_t e = c->a->eid[p0 + p];
+        const int64_t sn = c->src[e];
+        const int r = c->rel[e];
+        for (int i = 0; i < H; ++i) {
+            const float *Wat = c->Watt + ((size_t)r * H + i) * dk * dk;
+            const float *Wms = c->Wmsg + ((size_t)r * H + i) * dk * dk;
+            vecmat(c->K + (size_t)sn * d + i * dk, Wat, dk, dk, 0, dk, kw + p * d + i * dk);
+            vecmat(c->V + (size_t)sn * d + i * dk, Wms, dk, dk, 0, dk, msg + p * d + i * dk);
+            double dot = 0.0;
+            for (int j = 0; j < dk; ++j) dot += kw[p * d + i * dk + j] * Qt[i * dk + j];
+            al[p * H + i] = dot * (double)c->mu[r] * c->att_scale;
+        }
+    }
+    for (int i = 0; i < H; ++i) { mx[i] = -INFINITY; sm[i] = 0.0; sv[i] = 0.0; }
+    for (int64_t p = 0; p < deg; ++p)
+        for (int i = 0; i < H; ++i) if (al[p * H + i] > mx[i]) mx[i] = al[p * H + i];
+    for (int64_t p = 0; p < deg; ++p)
+        for (int i = 0; i < H; ++i) sm[i] += exp(al[p * H + i] - mx[i]);
+    for (int64_t p = 0; p < deg; ++p)
+        for (int i = 0; i < H; ++i) al[p * H + i] = exp(al[p * H + i] - mx[i]) / sm[i];
+    for (int j = 0; j < d; ++j) agg[j] = 0.0;
+    for (int64_t p = 0; p < deg; ++p)
+        for (int j = 0; j < d; ++j) agg[j] += al[p * H + j / dk] * msg[p * d + j];
+    /* output linear */
+    if (c->a_linear) {
+        const float *Wat = c->Wa + (size_t)c->ntype[t] * d * d;
+        for (int i = 0; i < d; ++i) {
+            double s2 = 0.0;
+            for (int j = 0; j < d; ++j) s2 += (double)Wat[(size_t)i * d + j] * (double)Gt[j];
+            dagg[i] = s2;
+        }
+    } else {
+        for (int j = 0; j < d; ++j) dagg[j] = (double)Gt[j];
+    }
+    /* softmax backward */
+    for (int64_t p = 0; p < deg; ++p)
+        for (int i = 0; i < H; ++i) {
+            double da = 0.0;
+            for (int j = i * dk; j < (i + 1) * dk; ++j) da += dagg[j] * msg[p * d + j];
+            dal[p * H + i] = da;
+            sv[i] += al[p * H + i] * da;
+        }
+    for (int j = 0; j < d; ++j) dQt[j] = 0.0;
+    for (int64_t p = 0; p < deg; ++p) {
+        const int64_t e = c->a->eid[p0 + p];
+        const int r = c->rel[e];
+        const double cr = (double)c->mu[r] * c->att_scale;
+        for (int i = 0; i < H; ++i) {
+            const double alpha = al[p * H + i];
+            const double da = alpha * (dal[p * H + i] - sv[i]);
+            const double *kwe = kw + p * d + i * dk, *Qti = Qt + i * dk;
+            for (int j = 0; j < dk; ++j) dQt[i * dk + j] += da * cr * kwe[j];
+            double kq = 0.0;
+            for (int j = 0; j < dk; ++j) kq += kwe[j] * Qti[j];
+            c->AL[e * H + i] = alpha;
+            c->DA[e * H + i] = da;
+            c->KQ[e * H + i] = kq;
+        }
+    }
+    return 0;
+}
+
 int oracle_hgt_backward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d, int32_t heads,
                         const int32_t *src, const int32_t *dst, const int32_t *rel,
                         const int32_t *ntype, const float *h, const float *Wk, const float *Wq,
                         const float *Wv, const float *Wa, const float *Watt, const float *Wmsg,
                         const float *mu, double att_scale, int32_t residual, int32_t a_linear,
-                        const float *G, double *dh, double *dWk, double *dWq, double *dWv,
+                        const float *G, const uint8_t *node_mask, const uint8_t *rel_mask,
+                        double *dh, double *dWk, double *dWq, double *dWv,
                         double *dWa, double *dWatt, double *dWmsg, double *dmu)
 {
     if (check_coo(N, E, R, src, dst, rel) || T <= 0 || d <= 0 || d > 512 || heads <= 0 ||
-        d % heads)
+        heads > 64 || d % heads)
         return -1;
     for (int64_t n = 0; n < N; ++n)
         if (ntype[n] < 0 || ntype[n] >= T) return -1;
     const int H = heads, dk = d / heads;
+    const int full = !node_mask && !rel_mask;
     in_lists a;
     int rc = build_in_lists(N, E, dst, &a);
     if (rc) { free_in_lists(&a); return rc; }
-    const size_t nd = (size_t)(N > 0 ? N : 1) * d;
+    const size_t nd = (size_t)(N > 0 ? N : 1) * d, E1 = (size_t)(E > 0 ? E : 1), N1 = (size_t)(N > 0 ? N : 1);
     double *K = (double *)malloc(nd * sizeof(double));
     double *Q = (double *)malloc(nd * sizeof(double));
     double *V = (double *)malloc(nd * sizeof(double));
     double *dK = (double *)calloc(nd, sizeof(double));
     double *dQ = (double *)calloc(nd, sizeof(double));
     double *dV = (double *)calloc(nd, sizeof(double));
-    double *x = (double *)malloc((size_t)d * sizeof(double));
-    double *agg = (double *)malloc((size_t)d * sizeof(double));
-    double *dagg = (double *)malloc((size_t)d * sizeof(double));
-    double *sv = (double *)malloc((size_t)H * sizeof(double));
-    double *mx = (double *)malloc((size_t)H * sizeof(double));
-    double *sm = (double *)malloc((size_t)H * sizeof(double));
-    double *kw = NULL, *msg = NULL, *al = NULL, *dal = NULL;
-    int64_t cap = 0;
-    int err = !K || !Q || !V || !dK || !dQ || !dV || !x || !agg || !dagg || !sv || !mx || !sm;
+    double *agg = (double *)calloc(nd, sizeof(double));
+    double *dagg = (double *)calloc(nd, sizeof(double));
+    double *AL = (double *)malloc(E1 * H * sizeof(double));
+    double *DA = (double *)malloc(E1 * H * sizeof(double));
+    double *KQ = (double *)malloc(E1 * H * sizeof(double));
+    uint8_t *need = (uint8_t *)calloc(N1, 1);
+    int64_t *relptr = (int64_t *)calloc((size_t)R + 1, sizeof(int64_t));
+    int64_t *reledge = (int64_t *)malloc(E1 * sizeof(int64_t));
+    int64_t *outptr = (int64_t *)calloc(N1 + 1, sizeof(int64_t));
+    int64_t *outedge = (int64_t *)malloc(E1 * sizeof(int64_t));
+    int err = !K || !Q || !V || !dK || !dQ || !dV || !agg || !dagg || !AL || !DA || !KQ || !need ||
+              !relptr || !reledge || !outptr || !outedge;
     if (!err) {
-        for (int64_t n = 0; n < N; ++n) {   /* node-level K, Q, V */
-            load_row(h, n, d, x);
-            const size_t wo = (size_t)ntype[n] * d * d;
-            vecmat(x, Wk + wo, d, d, 0, d, K + (size_t)n * d);
-            vecmat(x, Wq + wo, d, d, 0, d, Q + (size_t)n * d);
-            vecmat(x, Wv + wo, d, d, 0, d, V + (size_t)n * d);
-        }
         memset(dh, 0, (size_t)N * d * sizeof(double));
         memset(dWk, 0, (size_t)T * d * d * sizeof(double));
         memset(dWq, 0, (size_t)T * d * d * sizeof(double));
@@ -768,127 +1007,160 @@ int oracle_hgt_backward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d, i
         memset(dWatt, 0, (size_t)R * H * dk * dk * sizeof(double));
         memset(dWmsg, 0, (size_t)R * H * dk * dk * sizeof(double));
         memset(dmu, 0, (size_t)R * sizeof(double));
-    }
-    for (int64_t t = 0; t < N && !err; ++t) {
-        const int64_t p0 = a.ptr[t], deg = a.ptr[t + 1] - p0;
-        const float *Gt = G + (size_t)t * d;
-        const double *Qt = Q + (size_t)t * d;
-        if (deg > cap) {
-            free(kw); free(msg); free(al); free(dal);
-            cap = deg;
-            kw = (double *)malloc((size_t)cap * d * sizeof(double));
-            msg = (double *)malloc((size_t)cap * d * sizeof(double));
-            al = (double *)malloc((size_t)cap * H * sizeof(double));
-            dal = (double *)malloc((size_t)cap * H * sizeof(double));
-            if (!kw || !msg || !al || !dal) { err = 1; break; }
+        for (int64_t e = 0; e < E; ++e) {
+            const int want = full || (rel_mask && rel_mask[rel[e]]) ||
+                             (node_mask && (node_mask[src[e]] || node_mask[dst[e]]));
+            if (want) need[dst[e]] = 1;
         }
-        /* forward: scores, softmax, messages, agg */
-        for (int64_t p = 0; p < deg; ++p) {
-            const int64_t e = a.eid[p0 + p];
-            const int64_t sn = src[e];
-            const int r = rel[e];
-            for (int i = 0; i < H; ++i) {
-                const float *Wat = Watt + ((size_t)r * H + i) * dk * dk;
-                const float *Wms = Wmsg + ((size_t)r * H + i) * dk * dk;
-                vecmat(K + (size_t)sn * d + i * dk, Wat, dk, dk, 0, dk, kw + p * d + i * dk);
-                vecmat(V + (size_t)sn * d + i * dk, Wms, dk, dk, 0, dk, msg + p * d + i * dk);
-                double dot = 0.0;
-                for (int j = 0; j < dk; ++j) dot += kw[p * d + i * dk + j] * Qt[i * dk + j];
-                al[p * H + i] = dot * (double)mu[r] * att_scale;
-            }
-        }
-        for (int i = 0; i < H; ++i) { mx[i] = -INFINITY; sm[i] = 0.0; sv[i] = 0.0; }
-        for (int64_t p = 0; p < deg; ++p)
-            for (int i = 0; i < H; ++i) if (al[p * H + i] > mx[i]) mx[i] = al[p * H + i];
-        for (int64_t p = 0; p < deg; ++p)
-            for (int i = 0; i < H; ++i) sm[i] += exp(al[p * H + i] - mx[i]);
-        for (int64_t p = 0; p < deg; ++p)
-            for (int i = 0; i < H; ++i) al[p * H + i] = exp(al[p * H + i] - mx[i]) / sm[i];
-        for (int j = 0; j < d; ++j) agg[j] = 0.0;
-        for (int64_t p = 0; p < deg; ++p)
-            for (int j = 0; j < d; ++j) agg[j] += al[p * H + j / dk] * msg[p * d + j];
-        /* output linear and residual */
-        if (a_linear) {
-            const float *Wat = Wa + (size_t)ntype[t] * d * d;
-            for (int i = 0; i < d; ++i) {
-                double s2 = 0.0;
-                for (int j = 0; j < d; ++j) s2 += (double)Wat[(size_t)i * d + j] * (double)Gt[j];
-                dagg[i] = s2;
-            }
-            if (dWa) {
-                double *dw = dWa + (size_t)ntype[t] * d * d;
-                for (int i = 0; i < d; ++i)
-                    for (int j = 0; j < d; ++j) dw[(size_t)i * d + j] += agg[i] * (double)Gt[j];
-            }
+        if (node_mask)
+            for (int64_t n = 0; n < N; ++n) if (node_mask[n]) need[n] = 1;   /* dQ of n */
+        /* relations' edges and sources' out-edges, both in the global order */
+        for (int64_t e = 0; e < E; ++e) { relptr[rel[e] + 1]++; outptr[src[e] + 1]++; }
+        for (int r = 0; r < R; ++r) relptr[r + 1] += relptr[r];
+        for (int64_t n = 0; n < N; ++n) outptr[n + 1] += outptr[n];
+        int64_t *rf = (int64_t *)malloc((size_t)R * sizeof(int64_t));
+        int64_t *of = (int64_t *)malloc(N1 * sizeof(int64_t));
+        if (!rf || !of) {
+            err = 1;
         } else {
-            for (int j = 0; j < d; ++j) dagg[j] = (double)Gt[j];
-        }
-        if (residual)
-            for (int j = 0; j < d; ++j) dh[(size_t)t * d + j] += (double)Gt[j];
-        /* softmax backward */
-        for (int64_t p = 0; p < deg; ++p)
-            for (int i = 0; i < H; ++i) {
-                double da = 0.0;
-                for (int j = i * dk; j < (i + 1) * dk; ++j) da += dagg[j] * msg[p * d + j];
-                dal[p * H + i] = da;
-                sv[i] += al[p * H + i] * da;
+            memcpy(rf, relptr, (size_t)R * sizeof(int64_t));
+            memcpy(of, outptr, (size_t)N * sizeof(int64_t));
+            for (int64_t p = 0; p < E; ++p) {
+                const int64_t e = a.eid[p];
+                reledge[rf[rel[e]]++] = e;
+                outedge[of[src[e]]++] = e;
             }
-        for (int64_t p = 0; p < deg; ++p) {
-            const int64_t e = a.eid[p0 + p];
-            const int64_t sn = src[e];
-            const int r = rel[e];
-            const double c = (double)mu[r] * att_scale;
-            for (int i = 0; i < H; ++i) {
-                const double alpha = al[p * H + i];
-                const double da = alpha * (dal[p * H + i] - sv[i]);
-                const float *Wat = Watt + ((size_t)r * H + i) * dk * dk;
-                const float *Wms = Wmsg + ((size_t)r * H + i) * dk * dk;
-                double *dWat = dWatt + ((size_t)r * H + i) * dk * dk;
-                double *dWms = dWmsg + ((size_t)r * H + i) * dk * dk;
-                const double *Ks = K + (size_t)sn * d + i * dk, *Vs = V + (size_t)sn * d + i * dk;
-                const double *kwe = kw + p * d + i * dk, *Qti = Qt + i * dk;
-                const double *dg = dagg + i * dk;
-                for (int j = 0; j < dk; ++j)
+        }
+        free(rf); free(of);
+    }
+    if (!err) {   /* node-level K, Q, V */
+#pragma omp parallel for schedule(static)
+        for (int64_t n = 0; n < N; ++n) {
+            double x[512];
+            load_row(h, n, d, x);
+            const size_t wo = (size_t)ntype[n] * d * d;
+            vecmat(x, Wk + wo, d, d, 0, d, K + (size_t)n * d);
+            vecmat(x, Wq + wo, d, d, 0, d, Q + (size_t)n * d);
+            vecmat(x, Wv + wo, d, d, 0, d, V + (size_t)n * d);
+        }
+    }
+    hgt_bwd_ctx c = {N, E, R, T, d, H, src, dst, rel, ntype, Wa, Watt, Wmsg, mu, G, att_scale, a_linear,
+                     &a, K, Q, V, agg, dagg, dQ, AL, DA, KQ};
+    /* stage A */
+    if (!err) {
+#pragma omp parallel reduction(| : err)
+        {
+            double *kw = NULL, *msg = NULL, *al = NULL, *dal = NULL;
+            int64_t cap = 0;
+#pragma omp for schedule(dynamic, 16)
+            for (int64_t t = 0; t < N; ++t)
+                if (need[t] && hgt_bwd_dst(&c, t, &kw, &msg, &al, &dal, &cap)) err = 1;
+            free(kw); free(msg); free(al); free(dal);
+        }
+    }
+    /* stage B: dWatt / dWmsg rows per (relation, head, row), dmu per relation,
+     * dWa rows per (node type, row) */
+    if (!err) {
+        const int64_t n_att = (int64_t)R * H * dk, n_mu = R, n_wa = (full && a_linear && dWa) ? (int64_t)T * d : 0;
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t job = 0; job < n_att + n_mu + n_wa; ++job) {
+            if (job < n_att) {
+                const int r = (int)(job / (H * dk)), i = (int)(job / dk % H), j = (int)(job % dk);
+                if (rel_mask && !rel_mask[r]) continue;
+                const double cr = (double)mu[r] * att_scale;
+                double *dWms = dWmsg + (((size_t)r * H + i) * dk + j) * dk;
+                double *dWat = dWatt + (((size_t)r * H + i) * dk + j) * dk;
+                for (int64_t q = relptr[r]; q < relptr[r + 1]; ++q) {
+                    const int64_t e = reledge[q];
+                    const double alpha = AL[e * H + i], da = DA[e * H + i];
+                    const double Vs = V[(size_t)src[e] * d + i * dk + j], Ks = K[(size_t)src[e] * d + i * dk + j];
+                    const double *dg = dagg + (size_t)dst[e] * d + i * dk, *Qti = Q + (size_t)dst[e] * d + i * dk;
                     for (int k = 0; k < dk; ++k) {
-                        dWms[(size_t)j * dk + k] += Vs[j] * alpha * dg[k];
-                        dWat[(size_t)j * dk + k] += Ks[j] * da * c * Qti[k];
+                        dWms[k] += Vs * alpha * dg[k];
+                        dWat[k] += Ks * da * cr * Qti[k];
                     }
-                for (int j = 0; j < dk; ++j) {
-                    double sv2 = 0.0, sk = 0.0;
-                    for (int k = 0; k < dk; ++k) {
-                        sv2 += alpha * dg[k] * (double)Wms[(size_t)j * dk + k];
-                        sk += da * c * Qti[k] * (double)Wat[(size_t)j * dk + k];
-                    }
-                    dV[(size_t)sn * d + i * dk + j] += sv2;
-                    dK[(size_t)sn * d + i * dk + j] += sk;
-                    dQ[(size_t)t * d + i * dk + j] += da * c * kwe[j];
                 }
-                double kq = 0.0;
-                for (int j = 0; j < dk; ++j) kq += kwe[j] * Qti[j];
-                dmu[r] += da * att_scale * kq;
+            } else if (job < n_att + n_mu) {
+                const int r = (int)(job - n_att);
+                if (rel_mask && !rel_mask[r]) continue;
+                for (int64_t q = relptr[r]; q < relptr[r + 1]; ++q) {
+                    const int64_t e = reledge[q];
+                    for (int i = 0; i < H; ++i) dmu[r] += DA[e * H + i] * att_scale * KQ[e * H + i];
+                }
+            } else {
+                const int64_t w = job - n_att - n_mu;
+                const int ty = (int)(w / d), i = (int)(w % d);
+                double *row = dWa + ((size_t)ty * d + i) * d;
+                for (int64_t t = 0; t < N; ++t) {
+                    if (ntype[t] != ty) continue;
+                    const double ai = agg[(size_t)t * d + i];
+                    const float *Gt = G + (size_t)t * d;
+                    for (int j = 0; j < d; ++j) row[j] += ai * (double)Gt[j];
+                }
             }
         }
     }
-    /* node-level linears */
-    for (int64_t n = 0; n < N && !err; ++n) {
-        load_row(h, n, d, x);
-        const size_t wo = (size_t)ntype[n] * d * d;
-        const double *dx[3] = {dK + (size_t)n * d, dQ + (size_t)n * d, dV + (size_t)n * d};
-        const float *Wx[3] = {Wk + wo, Wq + wo, Wv + wo};
-        double *dWx[3] = {dWk + wo, dWq + wo, dWv + wo};
-        for (int m = 0; m < 3; ++m) {
-            for (int i = 0; i < d; ++i) {
-                double s2 = 0.0;
-                for (int j = 0; j < d; ++j) {
-                    dWx[m][(size_t)i * d + j] += x[i] * dx[m][j];
-                    s2 += dx[m][j] * (double)Wx[m][(size_t)i * d + j];
+    /* stage C: dK and dV per source over its out-edges */
+    if (!err) {
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t sn = 0; sn < N; ++sn) {
+            if (!full && !(node_mask && node_mask[sn])) continue;
+            for (int64_t q = outptr[sn]; q < outptr[sn + 1]; ++q) {
+                const int64_t e = outedge[q], t = dst[e];
+                const int r = rel[e];
+                const double cr = (double)mu[r] * att_scale;
+                for (int i = 0; i < H; ++i) {
+                    const double alpha = AL[e * H + i], da = DA[e * H + i];
+                    const float *Wat = Watt + ((size_t)r * H + i) * dk * dk;
+                    const float *Wms = Wmsg + ((size_t)r * H + i) * dk * dk;
+                    const double *dg = dagg + (size_t)t * d + i * dk, *Qti = Q + (size_t)t * d + i * dk;
+                    for (int j = 0; j < dk; ++j) {
+                        double sv2 = 0.0, sk = 0.0;
+                        for (int k = 0; k < dk; ++k) {
+                            sv2 += alpha * dg[k] * (double)Wms[(size_t)j * dk + k];
+                            sk += da * cr * Qti[k] * (double)Wat[(size_t)j * dk + k];
+                        }
+                        dV[(size_t)sn * d + i * dk + j] += sv2;
+                        dK[(size_t)sn * d + i * dk + j] += sk;
+                    }
                 }
-                dh[(size_t)n * d + i] += s2;
             }
         }
     }
-    free(K); free(Q); free(V); free(dK); free(dQ); free(dV); free(x); free(agg); free(dagg);
-    free(sv); free(mx); free(sm); free(kw); free(msg); free(al); free(dal);
+    /* stage D: node-type weights (per type, projection and row) and dh (per node) */
+    if (!err && full) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t job = 0; job < (int64_t)T * 3 * d; ++job) {
+            const int ty = (int)(job / (3 * d)), m = (int)(job / d % 3), i = (int)(job % d);
+            const double *dX = m == 0 ? dK : (m == 1 ? dQ : dV);
+            double *row = (m == 0 ? dWk : (m == 1 ? dWq : dWv)) + ((size_t)ty * d + i) * d;
+            for (int64_t n = 0; n < N; ++n) {
+                if (ntype[n] != ty) continue;
+                const double xi = (double)h[(size_t)n * d + i];
+                for (int j = 0; j < d; ++j) row[j] += xi * dX[(size_t)n * d + j];
+            }
+        }
+    }
+    if (!err) {
+#pragma omp parallel for schedule(static)
+        for (int64_t n = 0; n < N; ++n) {
+            if (node_mask && !node_mask[n]) continue;
+            double *row = dh + (size_t)n * d;
+            if (residual)
+                for (int j = 0; j < d; ++j) row[j] += (double)G[(size_t)n * d + j];
+            const size_t wo = (size_t)ntype[n] * d * d;
+            const double *dx[3] = {dK + (size_t)n * d, dQ + (size_t)n * d, dV + (size_t)n * d};
+            const float *Wx[3] = {Wk + wo, Wq + wo, Wv + wo};
+            for (int m = 0; m < 3; ++m)
+                for (int i = 0; i < d; ++i) {
+                    double s2 = 0.0;
+                    for (int j = 0; j < d; ++j) s2 += dx[m][j] * (double)Wx[m][(size_t)i * d + j];
+                    row[i] += s2;
+                }
+        }
+    }
+    free(K); free(Q); free(V); free(dK); free(dQ); free(dV); free(agg); free(dagg);
+    free(AL); free(DA); free(KQ); free(need); free(relptr); free(reledge); free(outptr); free(outedge);
     free_in_lists(&a);
     return err ? -3 : 0;
 }

@@ -624,6 +624,27 @@ def test_hgt_backward_finite_differences():
         np.testing.assert_allclose(got["d" + k], fd, rtol=2e-3, atol=2e-4, err_msg=k)
 
 
+def test_hgt_backward_masks():
+    """The masked mode (used at full size) gives the full computation's values
+    on the requested entries, zeros elsewhere, and no node-type weights."""
+    g = tiny_graph(73, N=30, E=200, R=3, T=2, kind="hub")
+    t = tiny_tensors(73, g, 8, 8, heads=2)
+    t["mu"] = np.array([1.0, 0.6, 1.3], np.float32)
+    G = t["grad_out"][:, :8].copy()
+    full = oracle.hgt_backward(g, *(t[k] for k in HGT_PARAMS), G, heads=2, att_scale=0.5)
+    nm = np.zeros(30, np.uint8); nm[[0, 3, 29]] = 1
+    rm = np.zeros(3, np.uint8); rm[1] = 1
+    part = oracle.hgt_backward(g, *(t[k] for k in HGT_PARAMS), G, heads=2, att_scale=0.5,
+                               node_mask=nm, rel_mask=rm)
+    np.testing.assert_allclose(part["dh"][nm == 1], full["dh"][nm == 1], rtol=1e-12, atol=1e-14)
+    assert (part["dh"][nm == 0] == 0).all()
+    for k in ("dWatt", "dWmsg", "dmu"):
+        np.testing.assert_allclose(part[k][1], full[k][1], rtol=1e-12, atol=1e-14, err_msg=k)
+        assert (part[k][[0, 2]] == 0).all(), k
+    for k in ("dWk", "dWq", "dWv", "dWa"):
+        assert (part[k] == 0).all(), k
+
+
 # ---------------------------------------------------------------- integer preprocessing
 @pytest.mark.parametrize("kind", KINDS + ["complete"])
 def test_graph_index_against_python_sets(kind):
