@@ -42,17 +42,6 @@ def row_err(got, ref, structural_zero=None, cancel_floor=0.0) -> float:
     return err
 
 
-def sample_rows(g, n_random=400, seed=0):
-    """Destinations to check at full size: the largest in-degrees (hubs split
-    over many work items), some without in-edges, and a random sample."""
-    deg = np.bincount(g["dst"], minlength=g["N"])
-    rng = np.random.default_rng(seed)
-    top = np.argsort(-deg, kind="stable")[:6]
-    empty = np.flatnonzero(deg == 0)[:40]
-    rnd = rng.choice(g["N"], size=min(n_random, g["N"]), replace=False)
-    return np.unique(np.concatenate([top, empty, rnd])).astype(np.int32)
-
-
 class Runner:
     """Runs the library's layers on one device with torch-owned buffers."""
 
