@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librgnn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["graph.cpp", "api.cpp", "gemm.hip", "traverse.hip", "reduce.hip", "hgt.hip",
+SOURCES = ["status.cpp", "graph.cpp", "api.cpp", "gemm.hip", "traverse.hip", "reduce.hip", "hgt.hip",
            "backward.hip", "fused.hip",
            "rgcn_backward.hip", "hgt_backward.hip"]
 

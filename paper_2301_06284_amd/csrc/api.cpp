@@ -12,22 +12,6 @@
 
 namespace rgnn {
 
-namespace {
-thread_local std::string g_err;
-}
-
-rgnn_status fail(rgnn_status st, const std::string &msg)
-{
-    g_err = msg;
-    return st;
-}
-
-rgnn_status hip_fail(hipError_t e, const char *what)
-{
-    g_err = std::string(what) + ": " + hipGetErrorString(e);
-    return RGNN_EDEVICE;
-}
-
 // ------------------------------------------------------------------ profiling
 namespace {
 struct ProfRec {
@@ -243,9 +227,6 @@ size_t segment_gemm_layout(int64_t M, int32_t T, void *base, Tile **tiles, int64
 }  // namespace rgnn
 
 using namespace rgnn;
-
-extern "C" const char *rgnn_last_error(void) { return g_err.c_str(); }
-extern "C" const char *rgnn_version(void) { return "librgnn 0.1 (gfx950, fp32)"; }
 
 extern "C" rgnn_status rgnn_profile_enable(int32_t on)
 {

@@ -61,7 +61,6 @@ constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 // workgroup (their LDS stages), so 128 threads at d = 32
 constexpr int item_threads(int D) { return D == 32 ? 128 : 256; }
 constexpr int kU = 4;              // rows per prefetch batch in the traversals
-constexpr int kOuterRows = 2048;   // segments per outer-product K-chunk
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
@@ -870,7 +869,6 @@ constexpr unsigned outer_tiles(int D) { return D > 64 ? (unsigned)(D / 64) * (D 
 
 }  // namespace
 
-int bwd_outer_rows() { return kOuterRows; }
 
 template <int D>
 void outer_chunks_d(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x, const float *X,

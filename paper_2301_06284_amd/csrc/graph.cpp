@@ -330,13 +330,13 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         g->n_tiles_vsegs = (int64_t)x.tiles_vsegs.size();
         g->n_tiles_nodes = (int64_t)x.tiles_nodes.size();
         g->n_tiles_all = (int64_t)x.tiles_all.size();
-        build_tiles(x.rel_vsegptr, bwd_outer_rows(), x.tiles_outer);
+        build_tiles(x.rel_vsegptr, kOuterRows, x.tiles_outer);
         g->n_tiles_outer = (int64_t)x.tiles_outer.size();
-        build_tiles(all, bwd_outer_rows(), x.tiles_nodes_outer);   // node chunks (self-loop dW0)
+        build_tiles(all, kOuterRows, x.tiles_nodes_outer);   // node chunks (self-loop dW0)
         g->n_tiles_nodes_outer = (int64_t)x.tiles_nodes_outer.size();
         x.nodes_chunkptr = {0, (int32_t)g->n_tiles_nodes_outer};
         // chunks over the nodes grouped by type (per-type weight gradients)
-        build_tiles(x.ntype_ptr, bwd_outer_rows(), x.tiles_types_outer);
+        build_tiles(x.ntype_ptr, kOuterRows, x.tiles_types_outer);
         g->n_tiles_types_outer = (int64_t)x.tiles_types_outer.size();
         x.types_chunkptr.assign((size_t)T + 1, 0);
         for (const Tile &t : x.tiles_types_outer) x.types_chunkptr[(size_t)t.type + 1]++;

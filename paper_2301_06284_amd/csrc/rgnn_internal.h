@@ -28,6 +28,8 @@ constexpr int kBigRange = 32;
 // the partials of a destination split over more than kBigRange items are
 // merged in two levels: chunks of kMergeChunk partials, then the chunks
 constexpr int kMergeChunk = 128;
+// rows (segments or nodes) per K-chunk of the backward outer-product GEMMs
+constexpr int kOuterRows = 2048;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
@@ -147,7 +149,6 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
                              const int32_t *dst, const int32_t *rel, const int32_t *ntype,
                              int32_t flags, rgnn_graph *g);
 void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vector<Tile> &out);
-int bwd_outer_rows();
 rgnn_status launch_add(float *out, const float *a, const float *b, int64_t n, hipStream_t s);
 // out [rows, d] = in with the columns outside [c0, c1) set to 0
 rgnn_status launch_mask_cols(const float *in, float *out, int64_t rows, int d, int c0, int c1, hipStream_t s);
