@@ -12,6 +12,10 @@
 //   s_v      = sum_e alpha_e dalpha_e = S'_v / Z'_v,   S'_v = sum_e q_e dalpha_e
 //   Y_e      = alpha_e (dalpha_e - s_v) leaky'(y_e)
 //            = alpha_e ((dalpha_e Z'_v - S'_v) / Z'_v) leaky'(y_e)
+//   ysum_g   = sum_{e in segment g} Y_e
+//            = ((A+_g Z'_v - S'_v B+_g) + slope (A-_g Z'_v - S'_v B-_g)) / Z'_v^2
+//            with A+-_g = sum q_e dalpha_e, B+-_g = sum q_e over g's edges with
+//            positive (+) and non-positive (-) logits
 //   dh_u    += alpha_e dS_{v,r} + Y_e ws'_r       (u as a source)
 //   dh_v    += Y_e wt'_r                          (v as a destination)
 //   dW_r     = sum_seg (sum_e alpha_e h_u)^T G_v  +  dws'_r^T w_src[r] + dwt'_r^T w_dst[r]
@@ -24,7 +28,12 @@
 // to one in this pass's own arithmetic, and a softmax whose Jacobian vanishes
 // exactly (one in-edge: dalpha Z' - S' = dalpha q - q dalpha = 0) gives an
 // exact zero.  M_v only shifts the exponent.  Sa (below), which is summed
-// before Z'_v is known, takes the forward's Z_v.
+// before Z'_v is known, takes the forward's Z_v.  The per-segment sum of Y
+// is formed from sums accumulated in the same order and with the same
+// operations as S' and Z', so that when a segment holds all of a softmax
+// group's edges and their logits share a sign (sum Y = 0 exactly: the
+// softmax Jacobian's rows sum to zero) A = S' and B = Z' bit for bit and the
+// sum is an exact zero, as in exact arithmetic.
 //
 // Kernel sequence:
 //   1. dS by the typed GEMM (B = W_r^T) over the (dst, rel) segments, and the
@@ -73,6 +82,13 @@ __device__ __forceinline__ float mul_sub_exact(float a, float b, float c)
 {
 #pragma clang fp contract(off)
     return a * b - c;
+}
+// a * b - c * d with both products rounded on their own: exactly 0 when
+// (a, b) and (c, d) are the same pair of values
+__device__ __forceinline__ float cross_diff(float a, float b, float c, float d)
+{
+#pragma clang fp contract(off)
+    return a * b - c * d;
 }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
@@ -228,7 +244,7 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
                     const float z = y > 0.f ? y : k.slope * y;
                     const float q = SEG ? __expf(z - st.vM[jv]) : __expf(z - st.dM[j]);
                     const float al = q * (SEG ? st.vZi[jv] : st.dZi[j]);   // for Sa only
-                    s += q * da;
+                    s = __builtin_fmaf(q, da, s);   // same operation as the segment sums of pass 2
                     zs += q;
                     sa = lin4(sa, 1.f, Xh[u], al);
                     if (gl == 0) {
@@ -294,14 +310,26 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
             const float dz = sz.y > 0.f ? mul_sub_exact(st.eda[e], sz.y, sz.x) / sz.y : 0.f;
             const float Y = al * dz * (signbit(a) ? k.slope : 1.f);
             reinterpret_cast<float2 *>(k.ay)[e0 + e] = make_float2(al, Y);
-            st.eda[e] = Y;
         }
     }
     __syncthreads();
     if (fin) {
         for (int jv = gl; jv < nv; jv += G) {
-            float ys = 0.f;
-            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) ys += st.eda[e];
+            const float2 sz = SEG ? k.svs[vs0 + jv] : make_float2(st.dsv[st.vdj[jv]], st.dzs[st.vdj[jv]]);
+            float ap = 0.f, bp = 0.f, an = 0.f, bn = 0.f;
+            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) {
+                const float a = st.ea[e], q = fabsf(a);
+                if (signbit(a)) {
+                    an = __builtin_fmaf(q, st.eda[e], an);
+                    bn += q;
+                } else {
+                    ap = __builtin_fmaf(q, st.eda[e], ap);
+                    bp += q;
+                }
+            }
+            const float ys = sz.y > 0.f ? (cross_diff(ap, sz.y, sz.x, bp) + k.slope * cross_diff(an, sz.y, sz.x, bn)) /
+                                              (sz.y * sz.y)
+                                        : 0.f;
             k.ysum[st.vpos[jv]] = ys;
             st.vatt[jv] = ys;
         }
