@@ -215,6 +215,20 @@ rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
                          int32_t heads, float neg_slope, int32_t softmax_scope, int32_t plan,
                          float *out, float *saved, void *ws, size_t ws_bytes, void *stream);
 
+/* rgat_forward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid allocation).  Arguments, results and errors as in
+ * rgat_forward; the workspace lives in a static device array of 64 MiB that
+ * every GPU the library runs on holds from the first call until the process
+ * ends.  RGNN_ERANGE when rgnn_workspace_size() for these arguments exceeds
+ * 64 MiB (for one head at d = 64 that is roughly 2.4e5 (dst, rel) segments).
+ * The call allocates nothing.  Calls that overlap on one GPU share the array
+ * and race: serialise them (one stream, or events between streams). */
+rgnn_status rgat_forward_noalloc(const rgnn_graph_t *g, const float *h, const float *W,
+                                 const float *w_src, const float *w_dst, int32_t d_in, int32_t d_out,
+                                 int32_t heads, float neg_slope, int32_t softmax_scope, int32_t plan,
+                                 float *out, float *saved, void *stream);
+
 /* HGT layer.  With K_n = h_n Wk[tau(n)], Q_n = h_n Wq[tau(n)],
  * V_n = h_n Wv[tau(n)] split into `heads` blocks of dk = d / heads, per in-edge
  * e = (s -> t, r) and head i:

@@ -33,7 +33,7 @@ INDEX_KINDS = {
 EXPORTED = [
     "rgnn_graph_create_coo", "rgnn_graph_create_csr", "rgnn_graph_destroy", "rgnn_graph_info",
     "rgnn_graph_export", "rgnn_workspace_size", "rgnn_select_plan", "rgcn_forward",
-    "rgat_forward", "hgt_forward", "rgat_backward", "rgcn_backward", "hgt_backward",
+    "rgat_forward", "rgat_forward_noalloc", "hgt_forward", "rgat_backward", "rgcn_backward", "hgt_backward",
     "rgnn_segment_gemm",
     "rgnn_segment_gemm_workspace_size", "rgnn_profile_enable", "rgnn_profile_count",
     "rgnn_profile_read", "rgnn_profile_reset", "rgnn_last_error", "rgnn_version",
@@ -73,6 +73,7 @@ def _load():
         "rgnn_select_plan": [vp, i32, i32, i32, i32, P(i32), P(ctypes.c_double), P(ctypes.c_double)],
         "rgcn_forward": [vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, sz, vp],
         "rgat_forward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp, sz, vp],
+        "rgat_forward_noalloc": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp],
         "hgt_forward": [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp, vp, sz, vp],
         "rgat_backward": [vp, vp, vp, vp, vp, i32, i32, i32, f32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
         "rgcn_backward": [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp],
@@ -233,6 +234,14 @@ def rgat_forward(g, h, W, w_src, w_dst, out, saved, ws, d_in, d_out, heads=1, ne
                              heads, float(neg_slope), softmax_scope, plan, _ptr(out), _ptr(saved),
                              _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                              _stream(stream)))
+
+
+def rgat_forward_noalloc(g, h, W, w_src, w_dst, out, saved, d_in, d_out, heads=1, neg_slope=0.2,
+                         softmax_scope=SOFTMAX_PER_DST, plan=PLAN_AUTO, stream=None):
+    """rgat_forward with the workspace in the library's static device scratch."""
+    _check(_lib.rgat_forward_noalloc(g.handle, _ptr(h), _ptr(W), _ptr(w_src), _ptr(w_dst), d_in, d_out,
+                                     heads, float(neg_slope), softmax_scope, plan, _ptr(out), _ptr(saved),
+                                     _stream(stream)))
 
 
 def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, out, ws, d, heads, att_scale,
