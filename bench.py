@@ -448,7 +448,7 @@ def main():
         msbr = time_steps(torch, fnbr, K, W)
         layers["rgat_bwd_am_like_880k_per_relation_softmax"] = {"edges_per_s": E / (msbr * 1e-3), "ms": msbr}
         del wsbr, savedr
-        # four heads: one masked one-head pass per head
+        # four heads: one pass over all heads (gradients in the message space)
         saved4 = torch.empty(inf["num_nodes"], 4, 2, device=c.dev)
         ws4 = c.ws(rgnn.LAYER_RGAT, d, d, 4)
         rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, saved4, ws4, d, d, 4)
@@ -457,7 +457,9 @@ def main():
         fnb4 = lambda: rgnn.rgat_backward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], saved4,
                                           c.T["grad_out"], gh, gW, gs, gt, wsb4, d, d, 4)
         msb4 = time_steps(torch, fnb4, K, W)
-        layers["rgat_bwd_am_like_880k_4heads"] = {"edges_per_s": E / (msb4 * 1e-3), "ms": msb4}
+        kb4 = kernel_profile(rgnn, torch, fnb4, max(3, K // 2))
+        layers["rgat_bwd_am_like_880k_4heads"] = {"edges_per_s": E / (msb4 * 1e-3), "ms": msb4,
+                                                  "kernels_ms": {k: round(v[1], 4) for k, v in kb4.items()}}
         del wsb4, saved4
         # RGCN forward (with self-loop) and backward on the same graph
         log("workload 5: RGCN forward and backward")

@@ -20,7 +20,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["status.cpp", "graph.cpp", "api.cpp", "gemm.hip", "traverse.hip", "reduce.hip", "hgt.hip",
            "backward.hip", "fused.hip",
-           "rgcn_backward.hip", "hgt_backward.hip", "noalloc.hip"]
+           "rgcn_backward.hip", "hgt_backward.hip", "noalloc.hip", "backward_heads.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -145,35 +145,18 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     return c.off;
 }
 
-// Multi-head RGAT backward as a sum of one-head passes.  Head k reads only
-// the columns C_k of W_r, w_src[r], w_dst[r] and of the loss weight: with
-// those of every other head set to zero, the one-head layer computes head k's
-// logits, softmax and messages exactly, and its loss is head k's share of L.
-// So the gradients of L are the sums over k of the one-head gradients of the
-// masked problem (the masked entries receive exact zeros: their messages are
-// zero and their loss and attention weights are zero).  The loss weight itself
-// needs no mask: it enters the one-head backward only through G W_r^T, where
-// the masked W_r drops the other heads' columns, and through the outer
-// products G^T Sa, whose other columns the pass leaves out of dW.
-struct BwdHeadsWs { float *Wm, *wsm, *wdm, *sv; void *inner; size_t inner_bytes; };
-size_t rgat_bwd_heads_layout(const rgnn_graph *g, int d_in, int d_out, int H, void *base, BwdHeadsWs *w)
+// RGAT backward workspace: the one-head backward (input space) or the
+// several-head backward (message space, backward_heads.hip).
+size_t rgat_bwd_layout(const rgnn_graph *g, int d_in, int d_out, int H)
 {
-    size_t inner = 0;
-    rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, 0, nullptr, nullptr,
-                       nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &inner);
-    Carver c(base);
-    BwdHeadsWs x{};
-    x.inner = c.take<char>(inner);
-    x.inner_bytes = inner;
-    if (H > 1) {
-        const size_t R = (size_t)g->R, N = (size_t)g->N;
-        x.Wm = c.take<float>(R * d_in * d_out);
-        x.wsm = c.take<float>(R * d_out);
-        x.wdm = c.take<float>(R * d_out);
-        x.sv = c.take<float>(std::max<size_t>(N, (size_t)g->U_dst) * 2);
-    }
-    if (w) *w = x;
-    return c.off;
+    size_t need = 0;
+    if (H > 1)
+        rgat_backward_heads_impl(g, nullptr, nullptr, nullptr, nullptr, d_out, H, 0.f, 0, nullptr, nullptr,
+                                 nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
+    else
+        rgat_backward_impl(g, nullptr, nullptr, nullptr, nullptr, d_in, d_out, 0.f, 0, nullptr, nullptr,
+                           nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
+    return need;
 }
 
 // Softmax per (dst, rel) segment with several heads: the one-head
@@ -333,7 +316,7 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
         *bytes = hgt_layout(g, d_out, heads, nullptr, nullptr);
         return RGNN_OK;
     case RGNN_LAYER_RGAT_BACKWARD:
-        *bytes = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
+        *bytes = rgat_bwd_layout(g, d_in, d_out, heads);
         return RGNN_OK;
     case RGNN_LAYER_HGT_BACKWARD: {
         size_t need = 0;
@@ -655,33 +638,14 @@ extern "C" rgnn_status rgat_backward(const rgnn_graph_t *g, const float *h, cons
     const int per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
     hipStream_t s = (hipStream_t)stream;
-    const size_t need = rgat_bwd_heads_layout(g, d_in, d_out, heads, nullptr, nullptr);
+    const size_t need = rgat_bwd_layout(g, d_in, d_out, heads);
     if (!ws || ws_bytes < need)
         return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
-    BwdHeadsWs w;
-    rgat_bwd_heads_layout(g, d_in, d_out, heads, ws, &w);
     if (heads == 1)
-        return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, per_seg, saved,
-                                  grad_out, grad_h, grad_W, grad_w_src, grad_w_dst, w.inner,
-                                  w.inner_bytes, s, nullptr);
-    const int64_t R = g->R, N = g->N, dh = d_out / heads;
-    for (int k = 0; k < heads; ++k) {
-        const int c0 = (int)(k * dh), c1 = (int)((k + 1) * dh);
-        if ((st = launch_mask_cols(W, w.Wm, R * d_in, d_out, c0, c1, s)) != RGNN_OK) return st;
-        if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
-        if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
-        if ((st = launch_head_stats(saved, w.sv, per_seg ? g->U_dst : N, heads, k, s)) != RGNN_OK) return st;
-        // grad_out goes in whole: dS = grad_out W_k^T sees only head k's columns
-        // through the masked weights, and the outer products keep only those
-        // columns of dW.  Head 0 writes the outputs, the others add to them.
-        BwdHead hd;
-        hd.col0 = c0; hd.col1 = c1; hd.acc = k > 0;
-        if ((st = rgat_backward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, neg_slope, per_seg, w.sv, grad_out,
-                                     grad_h, grad_W, grad_w_src, grad_w_dst, w.inner, w.inner_bytes, s, nullptr,
-                                     hd)) != RGNN_OK)
-            return st;
-    }
-    return RGNN_OK;
+        return rgat_backward_impl(g, h, W, w_src, w_dst, d_in, d_out, neg_slope, per_seg, saved, grad_out, grad_h,
+                                  grad_W, grad_w_src, grad_w_dst, ws, ws_bytes, s, nullptr);
+    return rgat_backward_heads_impl(g, h, W, w_src, w_dst, d_out, heads, neg_slope, per_seg, saved, grad_out,
+                                    grad_h, grad_W, grad_w_src, grad_w_dst, ws, ws_bytes, s, nullptr);
 }
 
 extern "C" rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk,

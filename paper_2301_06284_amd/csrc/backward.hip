@@ -651,7 +651,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // yvec[c]   = sum over its segments of ysum[seg] * h[dst(seg)].
 // YS: also sum ysum[row] * h[v] per chunk (the RGAT dwt' term); GATHER: the
 // second operand's row (and h's) is vsegdst[row], else the row itself; GA:
-// the first operand's row is gathered the same way.  lda, ldb: row strides.
+// the first operand's row is vsegdst[row], else the row itself.  lda, ldb:
+// row strides.
 // A workgroup computes one 64 x 64 tile of the D x D product (blockIdx.y: the
 // tile, four at D = 128); at D = 32 the columns past D read as zeros.
 template <int D, bool YS, bool GATHER, bool GA>
@@ -693,14 +694,14 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     float ry[SL];
     auto load_idx = [&](int k0, int (&v)[SL]) {
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) v[sl] = GATHER ? vsegdst_byrel[row_of(k0, sl)] : row_of(k0, sl);
+        for (int sl = 0; sl < SL; ++sl) v[sl] = (GATHER || GA) ? vsegdst_byrel[row_of(k0, sl)] : row_of(k0, sl);
     };
     auto load_rows = [&](int k0, const int (&v)[SL]) {
 #pragma unroll
         for (int sl = 0; sl < SL; ++sl) {
             const int row = row_of(k0, sl);
             ra[sl] = aok ? ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + a0 + c4) : zero4();
-            rb[sl] = bok ? ld4(Gm + (size_t)v[sl] * ldb + b0 + c4) : zero4();
+            rb[sl] = bok ? ld4(Gm + (size_t)(GATHER ? v[sl] : row) * ldb + b0 + c4) : zero4();
             if (YS) {
                 rh[sl] = ys && aok ? ld4(h + (size_t)v[sl] * D + a0 + c4) : zero4();
                 ry[sl] = ysum[row];
@@ -903,7 +904,10 @@ void outer_chunks_d(const Tile *chunks, int64_t nchunks, const int32_t *gather, 
                     int ldx, const float *Gm, int ldg, float *partial, hipStream_t s)
 {
     const dim3 grid((unsigned)nchunks, outer_tiles(D));
-    if (gather && gather_x)
+    if (gather && gather_x == 2)   // only the first operand gathered
+        hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, true>), grid, dim3(256), 0, s,
+                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    else if (gather && gather_x)
         hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, true>), grid, dim3(256), 0, s,
                            chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
     else if (gather)

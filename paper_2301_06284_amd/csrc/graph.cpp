@@ -347,6 +347,24 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.rel_pairtileptr.assign((size_t)R + 1, 0);
         for (const Tile &t : x.tiles_pairs) x.rel_pairtileptr[(size_t)t.type + 1]++;
         for (int32_t r = 0; r < R; ++r) x.rel_pairtileptr[r + 1] += x.rel_pairtileptr[r];
+        // outer-product chunks over the pairs of each relation
+        build_tiles(x.uniq_rel_ptr, kOuterRows, x.tiles_outer_pairs);
+        g->n_tiles_outer_pairs = (int64_t)x.tiles_outer_pairs.size();
+        x.rel_pairchunkptr.assign((size_t)R + 1, 0);
+        for (const Tile &t : x.tiles_outer_pairs) x.rel_pairchunkptr[(size_t)t.type + 1]++;
+        for (int32_t r = 0; r < R; ++r) x.rel_pairchunkptr[r + 1] += x.rel_pairchunkptr[r];
+        // compact pairs in source-major order: a stable pass by source over the
+        // (rel, src) order gives (src, rel)
+        {
+            std::vector<int32_t> pp((size_t)g->U_src);
+            for (int64_t i = 0; i < g->U_src; ++i) pp[i] = (int32_t)i;
+            counting_sort(pp, x.uniq_src.data(), N, tmp, cnt);
+            x.pair_smpos.resize((size_t)g->U_src);
+            for (int64_t i = 0; i < g->U_src; ++i) x.pair_smpos[pp[i]] = (int32_t)i;
+            x.src_pairptr.assign((size_t)N + 1, 0);
+            for (int64_t i = 0; i < g->U_src; ++i) x.src_pairptr[(size_t)x.uniq_src[i] + 1]++;
+            for (int64_t u = 0; u < N; ++u) x.src_pairptr[u + 1] += x.src_pairptr[u];
+        }
     } catch (const std::bad_alloc &) {
         return fail(RGNN_ENOMEM, "host allocation failed while building the graph index");
     }
@@ -404,6 +422,10 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.out_rel, x.out_rel); add32(&d.vseg_pos, x.vseg_pos); add32(&d.out_pair, x.out_pair);
     add32(&d.out_vs, x.out_vs); add32(&d.out_dst, x.out_dst);
     parts.push_back(Part{(void **)&d.oitems, x.oitems.data(), x.oitems.size() * sizeof(Item)});
+    add32(&d.src_pairptr, x.src_pairptr); add32(&d.pair_smpos, x.pair_smpos);
+    add32(&d.rel_pairchunkptr, x.rel_pairchunkptr);
+    parts.push_back(Part{(void **)&d.tiles_outer_pairs, x.tiles_outer_pairs.data(),
+                         x.tiles_outer_pairs.size() * sizeof(Tile)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
     total = std::max<size_t>(total, 256);

@@ -84,6 +84,11 @@ struct HostIndex {
     std::vector<int32_t> out_vs, out_dst;   // per out-edge: its in-edge's vseg id and destination
     std::vector<int32_t> vseg_pos;       // position of each vseg in the by-relation order
     std::vector<Item> oitems;            // {node0, node1, q0, q1} over out-edge offsets
+    // compact pairs in source-major order (several-head backward)
+    std::vector<int32_t> src_pairptr;    // [N+1] pairs of each source in that order
+    std::vector<int32_t> pair_smpos;     // [U_src] position of each pair in that order
+    std::vector<Tile> tiles_outer_pairs;  // outer-product chunks over the pairs of each relation
+    std::vector<int32_t> rel_pairchunkptr;   // those chunks per relation [R+1]
 };
 
 // Device copies (one allocation, carved).
@@ -118,6 +123,8 @@ struct DeviceIndex {
     int32_t *out_pair = nullptr, *out_vs = nullptr, *out_dst = nullptr;
     int32_t *vseg_pos = nullptr;
     Item *oitems = nullptr;
+    int32_t *src_pairptr = nullptr, *pair_smpos = nullptr, *rel_pairchunkptr = nullptr;
+    Tile *tiles_outer_pairs = nullptr;
 };
 
 }  // namespace rgnn
@@ -133,7 +140,7 @@ struct rgnn_graph {
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
-    int64_t n_oitems = 0, n_osplit = 0, n_split_items = 0;
+    int64_t n_oitems = 0, n_osplit = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
@@ -285,6 +292,12 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
 // dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (d x d each).
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s);
+// RGAT backward with several heads (2 to 8, d / heads >= 16) in one pass over
+// the graph; need != NULL: only the workspace size.
+rgnn_status rgat_backward_heads_impl(const rgnn_graph *g, const float *h, const float *W, const float *w_src,
+                                     const float *w_dst, int d, int heads, float slope, int per_seg,
+                                     const float *saved, const float *Gm, float *dh, float *dW, float *dws,
+                                     float *dwt, void *ws, size_t ws_bytes, hipStream_t s, size_t *need);
 rgnn_status launch_fill(float *p, int64_t n, float v, hipStream_t s);
 rgnn_status launch_relu(float *p, int64_t n, hipStream_t s);
 

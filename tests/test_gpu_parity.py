@@ -354,8 +354,9 @@ def test_rgat_backward_per_relation_softmax(kind):
 @pytest.mark.parametrize("kind", ["random", "hub", "dups", "empty"])
 @pytest.mark.parametrize("heads", [2, 4])
 def test_rgat_per_relation_softmax_multihead(kind, heads):
-    """Softmax per (dst, rel) segment with several heads: forward and
-    backward as one masked one-head pass per head, against the oracle."""
+    """Softmax per (dst, rel) segment with several heads: the forward as one
+    masked one-head pass per head, the backward in one pass over all heads,
+    against the oracle."""
     g = graph(kind, E=3000)
     t = workloads.tiny_tensors(50, g, 64, 64, heads=heads, att_var=1.0)
     print(f"rgat per-relation softmax {kind} heads={heads}", flush=True)
@@ -402,11 +403,13 @@ def test_rgat_backward_per_relation_softmax_hub_segments():
 
 
 @pytest.mark.parametrize("kind", ["random", "hub", "srchub", "dups", "empty"])
-@pytest.mark.parametrize("d,heads,scope", [(32, 1, 0), (32, 2, 0), (32, 1, 1), (128, 1, 0), (128, 8, 0),
+@pytest.mark.parametrize("d,heads,scope", [(32, 1, 0), (32, 2, 0), (32, 2, 1), (32, 1, 1), (64, 2, 1), (64, 4, 1),
+                                           (128, 1, 0), (128, 2, 0), (128, 4, 1), (128, 8, 0), (128, 8, 1),
                                            (128, 1, 1)])
 def test_rgat_backward_hidden_sizes(kind, d, heads, scope):
-    """RGAT backward at d = 32 and 128 (the outer products as 64 x 64 tiles:
-    one zero-padded tile at 32, four at 128)."""
+    """RGAT backward at d = 32, 64 and 128, one to eight heads, both softmax
+    scopes (the outer products as 64 x 64 tiles: one zero-padded tile at 32,
+    four at 128)."""
     g = graph(kind, E=3000)
     t = workloads.tiny_tensors(51, g, d, d, heads=heads, att_var=1.0)
     print(f"rgat backward d={d} heads={heads} scope={scope} {kind}", flush=True)
@@ -444,7 +447,7 @@ def test_rgcn_backward_hidden_sizes(kind, d, W0, relu):
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("heads", [2, 4])
 def test_rgat_backward_multihead(kind, heads):
-    """Several heads: one masked one-head pass per head, summed."""
+    """Several heads in one backward pass (gradients in the message space)."""
     g = graph(kind, E=3000)
     t = workloads.tiny_tensors(45, g, 64, 64, heads=heads, att_var=1.0)
     print(f"rgat backward {kind} heads={heads}", flush=True)
@@ -460,8 +463,9 @@ def test_rgat_backward_multihead(kind, heads):
     assert row_err(gt, dwt) <= TOL
 
 
-def test_rgat_backward_multihead_mid_size():
-    """Four heads on a 200k-edge graph with hubs (split destinations and
+@pytest.mark.parametrize("d,heads", [(64, 2), (64, 4), (128, 8)])
+def test_rgat_backward_multihead_mid_size(d, heads):
+    """Several heads on a 200k-edge graph with hubs (split destinations and
     sources with many out-edges), every gradient in full, at the standard
     cancellation floor.
 
@@ -474,15 +478,15 @@ def test_rgat_backward_multihead_mid_size():
     the forward's denominator instead, that zero came out as ~1e-7 |dalpha|,
     a 3e-4 row error."""
     g = workloads.tiny_graph(46, N=20000, E=200000, R=12, T=2, kind="hub")
-    t = workloads.tiny_tensors(46, g, 64, 64, heads=4, att_var=1.0)
-    print("rgat backward heads=4 mid size", flush=True)
+    t = workloads.tiny_tensors(46, g, d, d, heads=heads, att_var=1.0)
+    print(f"rgat backward d={d} heads={heads} mid size", flush=True)
     run = Runner(g, t)
-    gh, gW, gs, gt = run.rgat_backward(heads=4)
+    gh, gW, gs, gt = run.rgat_backward(heads=heads)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=4)
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=heads)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
-    assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
+    assert row_err(gW.reshape(-1, d), dW.reshape(-1, d)) <= TOL
     assert row_err(gs, dws) <= TOL
     assert row_err(gt, dwt) <= TOL
 
