@@ -59,12 +59,19 @@ typedef enum {
     RGNN_PLAN_TRANSFORM_FIRST = 1,   /* M = h W_r once per unique (src, rel) pair    */
                                      /* (compact materialization), then gather M     */
     RGNN_PLAN_AGGREGATE_FIRST = 2,   /* gather h, sum per (dst, rel), then apply W_r */
-    RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED = 3
+    RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED = 3,
                                      /* RGAT only: transform-first with the          */
                                      /* destination attention term taken from the    */
                                      /* materialized h_v W_r row of every (dst, rel) */
                                      /* segment instead of h_v . (W_r w_dst[r]): the */
                                      /* layer without linear operator reordering     */
+    RGNN_PLAN_TRANSFORM_FIRST_ATTMSG = 4
+                                     /* RGAT only: transform-first whose materialized */
+                                     /* rows hold the message and, after it, the      */
+                                     /* heads' source attention terms m . w_src[r]    */
+                                     /* (one tensor for attention and message, the    */
+                                     /* proposal of Section "Discussion and Future    */
+                                     /* Work"; rows padded to 16-byte multiples)      */
 } rgnn_plan;
 
 typedef enum {
@@ -202,14 +209,14 @@ rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const float *W, 
  *   of v with relation r instead (each relation's messages are normalised on
  *   their own; out_v sums the relations): it runs the aggregate-first plan
  *   (d_in == d_out; size the workspace for RGNN_PLAN_AGGREGATE_FIRST with the
- *   head count; several heads run one pass per head over the weights and
- *   attention vectors with the other heads' columns zeroed, the outputs
- *   summed) and returns RGNN_EUNSUPPORTED for RGNN_PLAN_TRANSFORM_FIRST;
+ *   head count) and returns RGNN_EUNSUPPORTED for the transform-first plans;
  *   saved is then [num_dst_segments, heads, 2], the (max, sum) of each
  *   (dst, rel) segment in (dst, rel) order, or NULL.
  *   d_in, d_out in {64, 128}, or d_in = d_out = 32; d_out / heads a multiple of 16.
- *   RGNN_PLAN_AGGREGATE_FIRST requires heads == 1 with the per-destination
- *   softmax. */
+ *   Aggregate-first with several heads (either softmax) runs one pass per
+ *   head over the weights and attention vectors with the other heads'
+ *   columns zeroed, the outputs summed: exact, at the cost of one pass per
+ *   head, so RGNN_PLAN_AUTO picks transform-first for several heads. */
 rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const float *W,
                          const float *w_src, const float *w_dst, int32_t d_in, int32_t d_out,
                          int32_t heads, float neg_slope, int32_t softmax_scope, int32_t plan,

@@ -131,8 +131,10 @@ size_t rgat_layout(const rgnn_graph *g, int d_in, int d_out, int H, int plan, vo
     x.wsp = c.take<float>((size_t)g->R * H * d_in);
     x.wtp = c.take<float>((size_t)g->R * H * d_in);
     x.vatt = c.take<float>((size_t)g->V * H);
-    if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED) {
-        x.M = c.take<float>((size_t)g->U_src * d_out);
+    if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED ||
+        plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG) {
+        const int ldm = plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG ? att_row_ld(d_out, H) : d_out;
+        x.M = c.take<float>((size_t)g->U_src * ldm);
         x.partial = c.take<float>((size_t)g->n_slots * (2 * H + d_out));
         if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)   // h_v W_r per segment
             x.T = c.take<float>((size_t)g->V * d_out);
@@ -159,9 +161,9 @@ size_t rgat_bwd_layout(const rgnn_graph *g, int d_in, int d_out, int H)
     return need;
 }
 
-// Softmax per (dst, rel) segment with several heads: the one-head
-// aggregate-first workspace plus the masked weights, one head's output and
-// its per-segment statistics.
+// Aggregate-first with several heads: the one-head aggregate-first workspace
+// plus the masked weights, one head's output and its softmax statistics (per
+// destination or per (dst, rel) segment).
 struct HeadsAfWs { float *Wm, *wsm, *wdm, *outk, *sk; void *inner; size_t inner_bytes; };
 size_t rgat_heads_af_layout(const rgnn_graph *g, int d, int H, void *base, HeadsAfWs *w)
 {
@@ -175,7 +177,7 @@ size_t rgat_heads_af_layout(const rgnn_graph *g, int d, int H, void *base, Heads
     x.wsm = c.take<float>((size_t)g->R * d);
     x.wdm = c.take<float>((size_t)g->R * d);
     x.outk = c.take<float>((size_t)g->N * d);
-    x.sk = c.take<float>((size_t)std::max<int64_t>(g->U_dst, 1) * 2);
+    x.sk = c.take<float>((size_t)std::max<int64_t>(std::max(g->U_dst, g->N), 1) * 2);
     if (w) *w = x;
     return c.off;
 }
@@ -298,9 +300,10 @@ extern "C" rgnn_status rgnn_workspace_size(const rgnn_graph_t *g, int32_t layer,
 {
     if (!g || !bytes) return fail(RGNN_EINVAL, "NULL argument");
     if (heads <= 0) return fail(RGNN_EINVAL, "heads must be positive");
-    if (plan < 0 || plan > 3) return fail(RGNN_EINVAL, "unknown plan");
-    if (plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED && layer != RGNN_LAYER_RGAT)
-        return fail(RGNN_EINVAL, "the unreordered transform-first plan is an RGAT plan");
+    if (plan < 0 || plan > 4) return fail(RGNN_EINVAL, "unknown plan");
+    if ((plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED || plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG) &&
+        layer != RGNN_LAYER_RGAT)
+        return fail(RGNN_EINVAL, "the unreordered and attention+message transform-first plans are RGAT plans");
     switch (layer) {
     case RGNN_LAYER_RGCN:
         *bytes = rgcn_layout(g, d_in, d_out, resolve_plan(g, layer, d_in, d_out, 1, plan), nullptr, nullptr);
@@ -414,11 +417,12 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
     if ((d_out / heads) % 16) return fail(RGNN_EUNSUPPORTED, "d_out / heads must be a multiple of 16");
     if (softmax_scope != RGNN_SOFTMAX_PER_DST && softmax_scope != RGNN_SOFTMAX_PER_DST_REL)
         return fail(RGNN_EINVAL, "unknown softmax scope");
-    if (plan < 0 || plan > 3) return fail(RGNN_EINVAL, "unknown plan");
+    if (plan < 0 || plan > 4) return fail(RGNN_EINVAL, "unknown plan");
     if (!std::isfinite(neg_slope)) return fail(RGNN_EINVAL, "neg_slope must be finite");
     const bool per_seg = softmax_scope == RGNN_SOFTMAX_PER_DST_REL;
     if (per_seg) {   // normalised per (dst, rel) segment: the aggregate-first plan
-        if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED)
+        if (plan == RGNN_PLAN_TRANSFORM_FIRST || plan == RGNN_PLAN_TRANSFORM_FIRST_UNREORDERED ||
+            plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG)
             return fail(RGNN_EUNSUPPORTED, "softmax per (destination, relation) runs aggregate-first");
         plan = RGNN_PLAN_AGGREGATE_FIRST;
     }
@@ -427,18 +431,15 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         return fail(RGNN_EUNSUPPORTED, "RGAT needs d_in == d_out");
     if (plan == RGNN_PLAN_AGGREGATE_FIRST && d_in != d_out)
         return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT needs d_in == d_out");
-    if (plan == RGNN_PLAN_AGGREGATE_FIRST && heads != 1 && !per_seg)
-        return fail(RGNN_EUNSUPPORTED, "aggregate-first RGAT with several heads is for the softmax per "
-                                       "(destination, relation)");
     hipStream_t s = (hipStream_t)stream;
-    if (heads == 1 || !per_seg)
+    if (heads == 1 || plan != RGNN_PLAN_AGGREGATE_FIRST)
         return rgat_forward_impl(g, h, W, w_src, w_dst, d_in, d_out, heads, neg_slope, per_seg, plan, out,
                                  saved, ws, ws_bytes, s);
-    // softmax per (dst, rel) segment with several heads: one masked one-head
-    // aggregate-first pass per head (head k reads only its columns of W_r,
-    // w_src[r] and w_dst[r], so the masked pass computes exactly head k's
-    // output columns and zeros elsewhere); outputs summed, statistics
-    // interleaved into saved [U_dst, heads, 2]
+    // aggregate-first with several heads: one masked one-head aggregate-first
+    // pass per head (head k reads only its columns of W_r, w_src[r] and
+    // w_dst[r], so the masked pass computes exactly head k's logits, softmax
+    // and output columns, and zeros elsewhere); outputs summed, statistics
+    // interleaved into saved [N or U_dst, heads, 2]
     const size_t need = rgat_heads_af_layout(g, d_out, heads, nullptr, nullptr);
     if (!ws || ws_bytes < need)
         return fail(RGNN_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
@@ -451,12 +452,13 @@ extern "C" rgnn_status rgat_forward(const rgnn_graph_t *g, const float *h, const
         if ((st = launch_mask_cols(w_src, w.wsm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
         if ((st = launch_mask_cols(w_dst, w.wdm, R, d_out, c0, c1, s)) != RGNN_OK) return st;
         float *ok = k ? w.outk : out;
-        if ((st = rgat_forward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, 1, neg_slope, true,
+        if ((st = rgat_forward_impl(g, h, w.Wm, w.wsm, w.wdm, d_in, d_out, 1, neg_slope, per_seg,
                                     RGNN_PLAN_AGGREGATE_FIRST, ok, saved ? w.sk : nullptr, w.inner,
                                     w.inner_bytes, s)) != RGNN_OK)
             return st;
         if (k && (st = launch_add(out, out, w.outk, N * d_out, s)) != RGNN_OK) return st;
-        if (saved && (st = launch_head_stats_scatter(w.sk, saved, g->U_dst, heads, k, s)) != RGNN_OK) return st;
+        if (saved && (st = launch_head_stats_scatter(w.sk, saved, per_seg ? g->U_dst : N, heads, k, s)) != RGNN_OK)
+            return st;
     }
     return RGNN_OK;
 }
@@ -494,16 +496,22 @@ rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *
         if ((st = launch_seg_attn(ta, s)) != RGNN_OK) return st;
     }
     if (plan != RGNN_PLAN_AGGREGATE_FIRST) {
+        const bool attmsg = plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG;
         GemmArgs ga;
         ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
-        ga.Y = w.M; ga.ldy = d_out;
+        ga.Y = w.M; ga.ldy = attmsg ? att_row_ld(d_out, heads) : d_out;
+        if (attmsg) {   // the source terms m . w_src[r] per head, written after each row's message
+            ga.ep.dot_vec = w_src; ga.ep.dot_out = w.M + d_out; ga.ep.dot_heads = heads; ga.ep.dot_ld = ga.ldy;
+        }
         if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         // the per-head source terms are formed in the traversal from the gathered
-        // message row itself (no per-pair term is materialized)
+        // message row itself (no per-pair term is materialized), or read from
+        // the attention+message row
         TravArgs ta;
         ta.g = g; ta.h = h; ta.M = w.M; ta.wtp = w.wtp; ta.vatt = w.vatt; ta.wsp = w_src;
+        ta.att_in_row = attmsg;
         ta.slope = neg_slope; ta.heads = heads; ta.d = d_out;
         ta.out = out; ta.saved = saved; ta.partial = w.partial;
         if ((st = launch_rgat_traverse_tf(ta, s)) != RGNN_OK) return st;

@@ -62,7 +62,7 @@ struct GemmK {
     float *Y; int64_t ldy;
     const int32_t *scatter;
     const float *row_scale;
-    const float *dot_vec; float *dot_out;
+    const float *dot_vec; float *dot_out; int64_t dot_ld;
     const float *residual; int64_t ld_res;
     float *Y2; int64_t ldy2; int split;
 };
@@ -249,7 +249,7 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
                 float part = dpart[hh];
                 part += __shfl_xor(part, 16);
                 part += __shfl_xor(part, 32);
-                if (valid && q == 0) a.dot_out[y * DH + hh] = part;
+                if (valid && q == 0) a.dot_out[y * a.dot_ld + hh] = part;
             }
         }
     }
@@ -324,6 +324,7 @@ rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s)
     k.tiles = a.tiles; k.Y = a.Y; k.ldy = a.ldy; k.scatter = a.scatter;
     k.row_scale = a.ep.row_scale;
     k.dot_vec = a.ep.dot_vec; k.dot_out = a.ep.dot_out;
+    k.dot_ld = a.ep.dot_ld ? a.ep.dot_ld : a.ep.dot_heads;
     k.residual = a.ep.residual; k.ld_res = a.ep.ld_res;
     k.Y2 = a.ep.Y2; k.ldy2 = a.ep.ldy2; k.split = a.ep.split;
     if (a.trans_b && a.nparts != 1) return fail(RGNN_EINVAL, "transposed B takes one part");

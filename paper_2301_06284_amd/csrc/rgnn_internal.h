@@ -178,10 +178,12 @@ struct GemmEpilogue {
     // a per-row scalar applied to the tiles of matrix A), indexed by scatter id.
     const float *row_scale = nullptr;
     // Optional row dot products of the output with a per-type vector, written to
-    // dot_out[scatter_row * heads + head] (heads split the output columns).
+    // dot_out[scatter_row * dot_ld + head] (heads split the output columns;
+    // dot_ld 0 means heads).
     const float *dot_vec = nullptr;    // [types, Nc]
     float *dot_out = nullptr;
     int dot_heads = 1;
+    int64_t dot_ld = 0;
     // Optional residual: Y[row] += res[row] (same row index as the output).
     const float *residual = nullptr;
     int64_t ld_res = 0;
@@ -234,7 +236,14 @@ struct TravArgs {
     float *vatt = nullptr;               // [V, heads] destination attention term per vseg
     float *vscale = nullptr;             // aggregate-first: [V] softmax scale per vseg
     int relu = 0;
+    // transform-first with the attention+message rows: each row of M holds the
+    // d_out message features, then the per-head source terms (row stride
+    // att_row_ld()); the traversal reads the terms instead of forming them
+    int att_in_row = 0;
 };
+// Row stride (floats) of the attention+message rows: d_out message features,
+// then the heads' source terms padded to whole 16-byte groups.
+inline int att_row_ld(int d_out, int heads) { return d_out + 4 * ((heads + 3) / 4); }
 // vatt[vs, k] = h_v . wtp[r, k] for every virtual segment (v, r).
 rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s);
 rgnn_status launch_rgcn_traverse_tf(const TravArgs &a, hipStream_t s);

@@ -264,10 +264,17 @@ __global__ __launch_bounds__(256) void seg_attn_kernel(TK k, int64_t V, const in
 // belong to one head; the running maximum, denominator and weighted row sum of
 // that head are rescaled as the maximum grows, and a destination's result is
 // written when its last edge is consumed.  k.wsp holds w_src [R, D].
-template <int D, int H>
+//
+// ATT: the rows are attention+message rows (the proposal of Section
+// "Discussion and Future Work": the attention term and the message in one
+// tensor of width hidden + 1, here hidden + the heads, padded to a 16-byte
+// multiple), written by the GEMM epilogue; each lane reads its head's source
+// term from the row (same line as the row's tail) instead of forming the dot.
+template <int D, int H, bool ATT>
 __global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
 {
     constexpr int G = D / 4, GPB = 256 / G, LH = G / H;
+    constexpr int LDM = ATT ? D + 4 * ((H + 3) / 4) : D;   // row stride of M
     constexpr int kU = 4;   // each entry carries two rows: half the batch of the other traversals
     __shared__ Stage<H> stage[GPB];
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
@@ -302,15 +309,16 @@ __global__ __launch_bounds__(256) void rgat_tf1_kernel(TK k)
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u < it.ne ? base + u : it.ne - 1;
-                X[u] = ld4(k.M + (size_t)st.eidx[e] * D + gl * 4);
-                Xw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
+                X[u] = ld4(k.M + (size_t)st.eidx[e] * LDM + gl * 4);
+                if (ATT) Xw[u].x = k.M[(size_t)st.eidx[e] * LDM + D + head];
+                else Xw[u] = ld4(k.wsp + (size_t)st.vrel[st.evs[e]] * D + gl * 4);
             }
         };
         auto consume = [&](const float4 (&X)[kU], const float4 (&Xw)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
-                const float src_term = gsum<LH>(dot4(X[u], Xw[u]));
+                const float src_term = ATT ? Xw[u].x : gsum<LH>(dot4(X[u], Xw[u]));
                 if (e < it.ne) {
                     while (e >= st.dptr[j + 1]) { flush(j); ++j; }
                     const float z = leaky(src_term + st.vw[st.evs[e] * H + head], k.slope);
@@ -386,8 +394,12 @@ rgnn_status launch_rgat_traverse_tf(const TravArgs &a, hipStream_t s)
     TK k = make_tk(a);
     LaunchScope ls("rgat_traverse_tf", s);
     const unsigned nb = blocks_for(a.g->n_items, 256 / (a.d / 4));
-    if (!a.wsp) return fail(RGNN_EINVAL, "RGAT traversal needs w_src");
-#define RGAT_TF(D, H) hipLaunchKernelGGL((rgat_tf1_kernel<D, H>), dim3(nb), dim3(256), 0, s, k)
+    if (!a.wsp && !a.att_in_row) return fail(RGNN_EINVAL, "RGAT traversal needs w_src");
+#define RGAT_TF(D, H)                                                                        \
+    do {                                                                                     \
+        if (a.att_in_row) hipLaunchKernelGGL((rgat_tf1_kernel<D, H, true>), dim3(nb), dim3(256), 0, s, k); \
+        else hipLaunchKernelGGL((rgat_tf1_kernel<D, H, false>), dim3(nb), dim3(256), 0, s, k);            \
+    } while (0)
     if (a.d == 32 && a.heads == 1) RGAT_TF(32, 1);
     else if (a.d == 32 && a.heads == 2) RGAT_TF(32, 2);
     else if (a.d == 64 && a.heads == 1) RGAT_TF(64, 1);

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "librgnn.so")
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PLAN_AUTO, PLAN_TRANSFORM_FIRST, PLAN_AGGREGATE_FIRST = 0, 1, 2
 PLAN_TRANSFORM_FIRST_UNREORDERED = 3
+PLAN_TRANSFORM_FIRST_ATTMSG = 4
 LAYER_RGCN, LAYER_RGAT, LAYER_HGT, LAYER_RGAT_BACKWARD, LAYER_SEGMENT_GEMM = 0, 1, 2, 3, 4
 LAYER_RGCN_BACKWARD, LAYER_HGT_BACKWARD = 5, 6
 SOFTMAX_PER_DST, SOFTMAX_PER_DST_REL = 0, 1

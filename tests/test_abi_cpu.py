@@ -106,9 +106,16 @@ def test_workspace_and_plan_model():
     g = workloads.make_graph(1)
     G = rgnn.Graph.from_dict(g, host_only=True)
     for layer, heads in [(rgnn.LAYER_RGCN, 1), (rgnn.LAYER_RGAT, 1), (rgnn.LAYER_RGAT, 4),
-                         (rgnn.LAYER_HGT, 4), (rgnn.LAYER_RGAT_BACKWARD, 1)]:
+                         (rgnn.LAYER_HGT, 4), (rgnn.LAYER_RGAT_BACKWARD, 1), (rgnn.LAYER_RGAT_BACKWARD, 4)]:
         for plan in (1, 2):
             assert rgnn.workspace_size(G, layer, 64, 64, heads, plan) > 0
+    # the attention+message rows are wider than the message rows
+    assert (rgnn.workspace_size(G, rgnn.LAYER_RGAT, 64, 64, 1, rgnn.PLAN_TRANSFORM_FIRST_ATTMSG) >
+            rgnn.workspace_size(G, rgnn.LAYER_RGAT, 64, 64, 1, rgnn.PLAN_TRANSFORM_FIRST))
+    with pytest.raises(rgnn.RgnnError):
+        rgnn.workspace_size(G, rgnn.LAYER_RGCN, 64, 64, 1, rgnn.PLAN_TRANSFORM_FIRST_ATTMSG)
+    with pytest.raises(rgnn.RgnnError):
+        rgnn.workspace_size(G, rgnn.LAYER_RGAT, 64, 64, 1, 5)
     plan, tf, af = rgnn.select_plan(G, rgnn.LAYER_RGAT, 64, 64, 1)
     assert plan == (2 if af < tf else 1) and tf > 0 and af > 0
     # multi-head RGAT always resolves to transform-first

@@ -131,10 +131,10 @@ def test_workload1_graph_index_bit_exact():
 
 
 # ------------------------------------------------------------------ workload 2
-@pytest.mark.parametrize("plan", [1, 2])
+@pytest.mark.parametrize("plan", [1, 2, 4])
 def test_workload2_rgat(plan):
-    """Both plans, every output row and every destination's softmax
-    statistics."""
+    """Every plan (4: attention+message rows), every output row and every
+    destination's softmax statistics."""
     g, t, run = load(2)
     print(f"workload 2 rgat plan={plan}", flush=True)
     got, saved = run.rgat(plan=plan, want_saved=True)
@@ -146,6 +146,18 @@ def test_workload2_rgat(plan):
     has = np.bincount(g["dst"], minlength=g["N"]) > 0
     np.testing.assert_allclose(s[has, 0], mx[has, 0], rtol=1e-4, atol=1e-4)
     np.testing.assert_allclose(s[has, 1], sm[has, 0], rtol=1e-4)
+
+
+@pytest.mark.parametrize("plan", [1, 2])
+def test_workload2_rgat_four_heads(plan):
+    """Four heads of 16 columns on the 880k-node graph, transform-first and
+    aggregate-first, every output row."""
+    g, t, run = load(2)
+    print(f"workload 2 rgat 4 heads plan={plan}", flush=True)
+    got, saved = run.rgat(heads=4, plan=plan, want_saved=True)
+    check_properties(g, got, saved)
+    r = ref("rgat4", lambda: oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=4))
+    assert row_err(got, r) <= TOL
 
 
 def test_workload2_rgat_per_relation_softmax():

@@ -92,8 +92,11 @@ def test_rgcn_dims(d_in, d_out, plan):
 
 
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 2), (1, 4)])
+@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 2), (1, 4), (2, 2), (2, 4), (4, 1), (4, 2), (4, 4)])
 def test_rgat_small(kind, plan, heads):
+    """Plans 1 (transform-first), 2 (aggregate-first; several heads as one
+    masked pass per head) and 4 (transform-first with attention+message
+    rows), 1 to 4 heads: output and saved statistics against the oracle."""
     g = graph(kind)
     t = workloads.tiny_tensors(2, g, 64, 64, heads=heads, att_var=1.0)
     print(f"rgat {kind} plan={plan} heads={heads}", flush=True)
@@ -108,7 +111,7 @@ def test_rgat_small(kind, plan, heads):
     np.testing.assert_allclose(sv[..., 1], sm, rtol=1e-4, atol=1e-5)
 
 
-@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 8)])
+@pytest.mark.parametrize("plan,heads", [(1, 1), (2, 1), (1, 8), (2, 8), (4, 8), (4, 1)])
 def test_rgat_d128(plan, heads):
     g = graph("hub", seed=4)
     t = workloads.tiny_tensors(4, g, 128, 128, heads=heads, att_var=1.0)
@@ -665,7 +668,8 @@ def test_hgt_forward_saved_statistics(kind, d, heads):
 def test_rgat_ablation_plans(kind, heads):
     """Transform-first with and without compact materialization (graph flag)
     and with and without linear operator reordering of the destination term
-    all give the layer's output."""
+    and with the attention term carried in the message rows all give the
+    layer's output."""
     g = graph(kind, seed=37)
     t = workloads.tiny_tensors(37, g, 64, 64, heads=heads, att_var=1.0)
     ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads)
@@ -674,7 +678,7 @@ def test_rgat_ablation_plans(kind, heads):
         run = Runner(g, t, compact=compact)
         if not compact:
             assert run.G.info()["num_src_pairs"] == g["E"]
-        for plan in (1, 3):
+        for plan in (1, 3, 4):
             assert row_err(run.rgat(heads=heads, plan=plan), ref) <= TOL, (compact, plan)
         run.close()
 
