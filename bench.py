@@ -214,7 +214,8 @@ def sweep(args):
     transform-first without and
     with compact materialization (graph flag) and without and with linear
     operator reordering of the attention's destination term (RGAT plan 3 vs 1),
-    and of the fused aggregate-first plan, with the plan the model selects."""
+    with the attention term carried in the message rows (plan 4), and of the
+    fused aggregate-first plan, with the plan the model selects."""
     import torch
     from paper_2301_06284_amd import rgnn
     torch.cuda.set_device(0)
@@ -238,7 +239,8 @@ def sweep(args):
         for lname, layer in (("rgat", rgnn.LAYER_RGAT), ("rgcn", rgnn.LAYER_RGCN)):
             auto = rgnn.select_plan(c.G, layer, d, d, 1)[0]
             cases = [("vanilla", False, 3), ("compact", True, 3), ("reorder", False, 1),
-                     ("compact+reorder", True, 1), ("aggregate-first fused", True, 2)]
+                     ("compact+reorder", True, 1), ("compact+reorder, attention+message rows", True, 4),
+                     ("aggregate-first fused", True, 2)]
             if layer == rgnn.LAYER_RGCN:
                 cases = [("vanilla", False, 1), ("compact", True, 1), ("aggregate-first fused", True, 2)]
             for label, compact, plan in cases:
@@ -378,6 +380,14 @@ def main():
         k4h = kernel_profile(rgnn, torch, fn4, max(3, K // 2))
         layers["rgat_fwd_am_like_880k_4heads"] = {"edges_per_s": inf["num_edges"] / (m4h * 1e-3), "ms": m4h,
                                                   "kernels_ms": {k: round(v[1], 4) for k, v in k4h.items()}}
+        del ws4
+        # the same with aggregate-first (one masked pass per head)
+        ws4 = c.ws(rgnn.LAYER_RGAT, d, d, 4, rgnn.PLAN_AGGREGATE_FIRST)
+        fn4a = lambda: rgnn.rgat_forward(c.G, c.T["h"], c.T["W"], c.T["w_src"], c.T["w_dst"], out, sv4, ws4,
+                                         d, d, 4, 0.2, 0, rgnn.PLAN_AGGREGATE_FIRST)
+        m4a = time_steps(torch, fn4a, K, W)
+        layers["rgat_fwd_am_like_880k_4heads_aggregate_first"] = {"edges_per_s": inf["num_edges"] / (m4a * 1e-3),
+                                                                  "ms": m4a}
         del ws4, sv4
     if other in plans:
         layers["rgat_fwd_am_like_880k_" + names[other]] = {

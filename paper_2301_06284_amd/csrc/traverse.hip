@@ -361,6 +361,72 @@ __global__ __launch_bounds__(256) void rgcn_tf_kernel(TK k)
     aggregate_item<D, 1, false>(k, it, st, k.M, gl, 0, 0.f, 0.f);
 }
 
+// The same with the reordered vectors of every relation staged in LDS (when
+// they fit) and each group taking SB batches of S consecutive segments: the
+// next batch's destination rows are in flight while the current batch's dot
+// products are formed, and its indices two batches ahead.
+constexpr int kSegBatches = 4;
+
+template <int D, int H>
+__global__ __launch_bounds__(256) void seg_attn_lds_kernel(TK k, int64_t V, const int32_t *vseg_dst, int R)
+{
+    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int S = kSegPerGroup, SB = kSegBatches;
+    extern __shared__ float4 wts[];   // [R, H, D / 4]
+    const int gl = threadIdx.x % G;
+    for (int i = threadIdx.x; i < R * H * G; i += 256) wts[i] = ld4(k.wtp + (size_t)i * 4);
+    __syncthreads();
+    const int64_t base = ((int64_t)blockIdx.x * GPB + threadIdx.x / G) * (S * SB);
+    if (base >= V) return;
+    int v[2][S], r[2][S];
+    float4 hv[2][S];
+    auto idx = [&](int slot, int b) {
+#pragma unroll
+        for (int i = 0; i < S; ++i) {
+            const int64_t vs0 = base + b * S + i, vs = vs0 < V ? vs0 : V - 1;
+            v[slot][i] = vseg_dst[vs];
+            r[slot][i] = k.vseg_rel[vs];
+        }
+    };
+    auto rows = [&](int slot) {
+#pragma unroll
+        for (int i = 0; i < S; ++i) hv[slot][i] = ld4(k.h + (size_t)v[slot][i] * D + gl * 4);
+    };
+    constexpr int NM = (S * H + G - 1) / G;
+    auto compute = [&](int slot, int b) {
+        const int64_t vs0 = base + b * S;
+        float mine[NM];
+#pragma unroll
+        for (int m = 0; m < NM; ++m) mine[m] = 0.f;
+#pragma unroll
+        for (int i = 0; i < S; ++i)
+#pragma unroll
+            for (int hh = 0; hh < H; ++hh) {
+                const float p = gsum<G>(dot4(hv[slot][i], wts[(r[slot][i] * H + hh) * G + gl]));
+                const int t = i * H + hh;
+                if (gl == t % G) mine[t / G] = p;
+            }
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const int t = m * G + gl;
+            if (t < S * H && vs0 * H + t < V * H) k.vatt[(size_t)vs0 * H + t] = mine[m];
+        }
+    };
+    idx(0, 0);
+    rows(0);
+    idx(1, 1);
+#pragma unroll
+    for (int b = 0; b < SB; ++b) {
+        const int cur = b & 1, nxt = cur ^ 1;
+        if (b + 1 < SB) {
+            if (base + (b + 1) * S < V) rows(nxt);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (base + b * S < V) compute(cur, b);
+        if (b + 2 < SB) idx(cur, b + 2);
+    }
+}
+
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 
 }  // namespace
@@ -370,6 +436,26 @@ rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s)
     if (a.g->V == 0) return RGNN_OK;
     TK k = make_tk(a);
     LaunchScope ls("seg_attn", s);
+    const size_t wbytes = (size_t)a.g->R * a.heads * a.d * sizeof(float);
+    if (wbytes <= 32768 && a.heads <= 2) {
+        const unsigned nbl = blocks_for((a.g->V + kSegPerGroup * kSegBatches - 1) / (kSegPerGroup * kSegBatches),
+                                        256 / (a.d / 4));
+#define SAL(D, H) hipLaunchKernelGGL((seg_attn_lds_kernel<D, H>), dim3(nbl), dim3(256), wbytes, s, k, a.g->V, \
+                                     a.g->dev.vseg_dst, a.g->R)
+        bool done = true;
+        if (a.d == 32 && a.heads == 1) SAL(32, 1);
+        else if (a.d == 32 && a.heads == 2) SAL(32, 2);
+        else if (a.d == 64 && a.heads == 1) SAL(64, 1);
+        else if (a.d == 64 && a.heads == 2) SAL(64, 2);
+        else if (a.d == 128 && a.heads == 1) SAL(128, 1);
+        else if (a.d == 128 && a.heads == 2) SAL(128, 2);
+        else done = false;
+#undef SAL
+        if (done) {
+            hipError_t e = hipGetLastError();
+            return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_attn launch");
+        }
+    }
     const unsigned nb = blocks_for((a.g->V + kSegPerGroup - 1) / kSegPerGroup, 256 / (a.d / 4));
 #define SA(D, H) hipLaunchKernelGGL((seg_attn_kernel<D, H>), dim3(nb), dim3(256), 0, s, k, a.g->V, \
                                     a.g->dev.vseg_dst)
