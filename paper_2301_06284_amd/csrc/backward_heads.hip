@@ -44,6 +44,7 @@ constexpr int kE = kChunkEdges, kDst = kMaxDstPerItem;
 // of every head)
 constexpr int mh_threads(int D) { return D == 32 ? 64 : 128; }
 constexpr int kU = 4;      // edges per prefetch batch
+constexpr int kDstKU = 2;  // edges per prefetch batch of the destination pass
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
@@ -80,17 +81,22 @@ struct HK {
     const Item *items;
     const int32_t *item_slot, *dst_vsegptr, *vseg_ptr, *vseg_rel, *vseg_pos, *e2u, *vseg_seg;
     const float *M, *w_src, *wtp, *saved, *vatt, *G;
-    const float2 *sv_in;     // [N, H] merged (S', Z') of split destinations
+    float2 *sv;              // [N, H] (S', Z') per destination and head: written by pass 1 for
+                             // whole destinations, by the merge for split ones
     float2 *ssum;            // [slots, H] (S', Z') of each piece of a split destination
     float2 *svs;             // per-segment softmax: [V, H] (S', Z') per vseg, then per segment
     float slope;
-    float *ay;               // [E, H, 2] per sorted in-edge and head: (alpha, Y); pieces park (q, dalpha)
+    float *ay;               // [E, H, 2] per sorted in-edge and head: (q, dalpha) from pass 1
+                             // (q with the sign bit set where the logit is <= 0), then (alpha, Y)
     float *ysum;             // [V, H] per vseg (by-relation position) and head: sum of Y
     float *dh;               // [N, D] destination terms written here
     const int32_t *split_items;
     int64_t n_split_items;
 };
 
+// Only indices and the forward's maxima live in LDS (about 2 KB per item):
+// the per-edge (q, dalpha) and per-destination (S', Z') go to global memory
+// (their own outputs' buffers), which keeps occupancy at the register limit.
 template <int H, bool SEG>
 struct MStage {
     int eidx[kE];            // compact pair of each edge (row of M)
@@ -100,20 +106,18 @@ struct MStage {
     int vpos[kE];            // by-relation position of each segment
     int vdj[kE];             // item-local destination of each segment
     int dptr[kDst + 1];
-    float vw[kE * H];        // destination term of each segment and head, then its sum of Y
-    float ea[kE * H];        // q of each edge and head, sign bit set where the logit is <= 0
-    float eda[kE * H];       // dalpha of each edge and head
-    float dM[kDst * H];      // reference maximum of each destination and head
-    float dsv[kDst * H], dzs[kDst * H];   // S' and Z' of each destination and head
-    float vM[SEG ? kE * H : 1];           // per-segment softmax: reference maximum per segment
+    float dM[SEG ? 1 : kDst * H];   // reference maximum of each destination and head
+    float vM[SEG ? kE * H : 1];     // per-segment softmax: reference maximum per segment
 };
 
 // PHASE 0: every item; whole destinations run all passes, pieces of split
-//          destinations run pass 1, leave (S', Z') in ssum and park (q, dalpha).
-// PHASE 1: pieces of split destinations: pass 2 with the merged (S', Z').
-// SEG: PHASE 0 runs pass 1 for every item (per-vseg (S', Z') to svs, parked
-//      (q, dalpha)); PHASE 1 runs passes 2 and 3 for every item.
-template <int D, int H, int PHASE, bool SEG>
+//          destinations run pass 1 and leave (S', Z') in ssum.
+// PHASE 1: pieces of split destinations: the segment sums and pass 2 with the
+//          merged (S', Z').
+// SEG: PHASE 0 runs pass 1 for every item (per-vseg (S', Z') to svs); PHASE 1
+//      runs the rest for every item.
+// KU: edges per prefetch batch of pass 1 (two batches in flight).
+template <int D, int H, int PHASE, bool SEG, int KU>
 __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
 {
     constexpr int G = D / 4, GPB = mh_threads(D) / G, LH = G / H;
@@ -122,6 +126,7 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
     const int head = gl / LH;
     const bool hl = gl % LH == 0;   // the lane that records its head's scalars
     MStage<H, SEG> &st = stage[gi];
+    float2 *ay2 = reinterpret_cast<float2 *>(k.ay);
     const int64_t gidx = (int64_t)blockIdx.x * GPB + gi;
     const int64_t item = PHASE == 1 && !SEG ? (gidx < k.n_split_items ? k.split_items[gidx] : k.n_items) : gidx;
     bool valid = item < k.n_items;
@@ -141,11 +146,9 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
             st.vpos[j] = k.vseg_pos[vs0 + j];
             for (int e = a; e < b; ++e) st.evs[e] = j;
         }
-        for (int i = gl; i < nv * H; i += G) {
-            st.vw[i] = k.vatt[(size_t)vs0 * H + i];
-            if (SEG && PHASE == 0)
+        if (SEG && PHASE == 0)
+            for (int i = gl; i < nv * H; i += G)
                 st.vM[i] = k.saved[((size_t)k.vseg_seg[vs0 + i / H] * H + i % H) * 2];
-        }
         if (gl == 0) st.vptr[nv] = ne;
         auto dvs = [&](int jj) {
             const int vs = k.dst_vsegptr[dst0 + jj];
@@ -156,63 +159,49 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
             st.dptr[j] = k.vseg_ptr[vs0 + a] - e0;
             for (int jv = a; jv < b; ++jv) st.vdj[jv] = j;
         }
-        if (!SEG)
-            for (int i = gl; i < nd * H; i += G) {
-                const int64_t vh = (int64_t)dst0 * H + i;
-                st.dM[i] = k.saved[vh * 2];
-                if (PHASE == 1) {
-                    const float2 sz = k.sv_in[vh];
-                    st.dsv[i] = sz.x;
-                    st.dzs[i] = sz.y;
-                }
-            }
+        if (!SEG && PHASE == 0)
+            for (int i = gl; i < nd * H; i += G) st.dM[i] = k.saved[((int64_t)dst0 * H + i) * 2];
         if (gl == 0) st.dptr[nd] = ne;
-        for (int e = gl; e < ne; e += G) {
-            if (PHASE == 0) st.eidx[e] = k.e2u[e0 + e];
-        }
-        if (PHASE == 1)
-            for (int i = gl; i < ne * H; i += G) {
-                const float2 p = reinterpret_cast<const float2 *>(k.ay)[(size_t)e0 * H + i];
-                st.ea[i] = p.x;
-                st.eda[i] = p.y;
-            }
+        if (PHASE == 0)
+            for (int e = gl; e < ne; e += G) st.eidx[e] = k.e2u[e0 + e];
     }
     __syncthreads();
 
-    // pass 1: per edge and head the logit, q and dalpha; (S', Z') per
+    // pass 1: per edge and head the logit, q and dalpha (to ay); (S', Z') per
     // destination (or per vseg)
     if (PHASE == 0 && valid && ne > 0) {
         int j = 0, jv = 0;
         while (st.dptr[j + 1] == st.dptr[j]) ++j;
         float s = 0.f, zs = 0.f;
-        // ping-pong batches of (message row, w_src row, G row of the destination)
-        float4 Am[kU], Aw[kU], Ag[kU], Bm[kU], Bw[kU], Bg[kU];
-        auto load = [&](float4 (&Xm)[kU], float4 (&Xw)[kU], float4 (&Xg)[kU], int base) {
+        // ping-pong batches of (message row, w_src row, G row of the destination,
+        // the segment's destination term)
+        float4 Am[KU], Aw[KU], Ag[KU], Bm[KU], Bw[KU], Bg[KU];
+        float Av[KU], Bv[KU];
+        auto load = [&](float4 (&Xm)[KU], float4 (&Xw)[KU], float4 (&Xg)[KU], float (&Xv)[KU], int base) {
 #pragma unroll
-            for (int u = 0; u < kU; ++u) {
+            for (int u = 0; u < KU; ++u) {
                 const int e = base + u < ne ? base + u : ne - 1;
                 const int jj = st.evs[e];
                 Xm[u] = ld4(k.M + (size_t)st.eidx[e] * D + gl * 4);
                 Xw[u] = ld4(k.w_src + (size_t)st.vrel[jj] * D + gl * 4);
                 Xg[u] = ld4(k.G + (size_t)(dst0 + st.vdj[jj]) * D + gl * 4);
+                Xv[u] = k.vatt[(size_t)(vs0 + jj) * H + head];
             }
         };
-        auto consume = [&](const float4 (&Xm)[kU], const float4 (&Xw)[kU], const float4 (&Xg)[kU], int base) {
+        auto consume = [&](const float4 (&Xm)[KU], const float4 (&Xw)[KU], const float4 (&Xg)[KU],
+                           const float (&Xv)[KU], int base) {
 #pragma unroll
-            for (int u = 0; u < kU; ++u) {
+            for (int u = 0; u < KU; ++u) {
                 const int e = base + u;
                 const float ys = gsum<LH>(dot4(Xm[u], Xw[u]));
                 const float da = gsum<LH>(dot4(Xm[u], Xg[u]));
                 if (e < ne) {
-                    const float y = ys + st.vw[jv * H + head];
+                    const float y = ys + Xv[u];
                     const float z = leaky(y, k.slope);
                     const float q = __expf(z - (SEG ? st.vM[jv * H + head] : st.dM[j * H + head]));
-                    s = __builtin_fmaf(q, da, s);   // the same operation as the segment sums of pass 2
+                    s = __builtin_fmaf(q, da, s);   // the same operation as the segment sums
                     zs += q;
-                    if (hl) {
-                        st.ea[e * H + head] = y > 0.f ? q : -q;
-                        st.eda[e * H + head] = da;
-                    }
+                    if (hl) ay2[(size_t)(e0 + e) * H + head] = make_float2(y > 0.f ? q : -q, da);
                     if (e + 1 == st.vptr[jv + 1]) {
                         if (SEG) {
                             if (hl) k.svs[(size_t)(vs0 + jv) * H + head] = make_float2(s, zs);
@@ -223,12 +212,8 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
                         if (e + 1 == st.dptr[j + 1]) {
                             if (!SEG) {
                                 if (hl) {
-                                    if (slot < 0) {
-                                        st.dsv[j * H + head] = s;
-                                        st.dzs[j * H + head] = zs;
-                                    } else {
-                                        k.ssum[(size_t)slot * H + head] = make_float2(s, zs);
-                                    }
+                                    if (slot < 0) k.sv[(size_t)(dst0 + j) * H + head] = make_float2(s, zs);
+                                    else k.ssum[(size_t)slot * H + head] = make_float2(s, zs);
                                 }
                                 s = 0.f;
                                 zs = 0.f;
@@ -240,62 +225,70 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
                 }
             }
         };
-        load(Am, Aw, Ag, 0);
+        load(Am, Aw, Ag, Av, 0);
         __builtin_amdgcn_sched_barrier(0);
-        for (int eb = 0; eb < ne; eb += 2 * kU) {
-            load(Bm, Bw, Bg, eb + kU);
+        for (int eb = 0; eb < ne; eb += 2 * KU) {
+            load(Bm, Bw, Bg, Bv, eb + KU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Am, Aw, Ag, eb);
-            load(Am, Aw, Ag, eb + 2 * kU);
+            consume(Am, Aw, Ag, Av, eb);
+            load(Am, Aw, Ag, Av, eb + 2 * KU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Bm, Bw, Bg, eb + kU);
+            consume(Bm, Bw, Bg, Bv, eb + KU);
         }
     }
+    // the workgroup's global writes of pass 1 are visible to it after the barrier
     __syncthreads();
 
     const bool fin = valid && (PHASE == 1 || (!SEG && slot < 0));
-    if (PHASE == 0 && valid && (SEG || slot >= 0)) {   // park (q, dalpha)
-        for (int i = gl; i < ne * H; i += G)
-            reinterpret_cast<float2 *>(k.ay)[(size_t)e0 * H + i] = make_float2(st.ea[i], st.eda[i]);
-    }
-    // pass 2: (alpha, Y) per edge and head; the sum of Y per segment and head
-    if (fin) {
-        for (int i = gl; i < ne * H; i += G) {
-            const int e = i / H, hh = i % H, jv = st.evs[e];
-            const float2 sz = SEG ? k.svs[(size_t)(vs0 + jv) * H + hh]
-                                  : make_float2(st.dsv[st.vdj[jv] * H + hh], st.dzs[st.vdj[jv] * H + hh]);
-            const float a = st.ea[i];
-            const float al = sz.y > 0.f ? fabsf(a) / sz.y : 0.f;
-            const float dz = sz.y > 0.f ? mul_sub_exact(st.eda[i], sz.y, sz.x) / sz.y : 0.f;
-            const float Y = al * dz * (signbit(a) ? k.slope : 1.f);
-            reinterpret_cast<float2 *>(k.ay)[(size_t)e0 * H + i] = make_float2(al, Y);
-        }
-    }
-    __syncthreads();
+    auto sz_of = [&](int jv, int hh) {
+        return SEG ? k.svs[(size_t)(vs0 + jv) * H + hh] : k.sv[(size_t)(dst0 + st.vdj[jv]) * H + hh];
+    };
+    // the sum of Y per segment and head, from (q, dalpha) before pass 2
+    // replaces them; four edges' pairs in flight per lane
     if (fin) {
         for (int i = gl; i < nv * H; i += G) {
             const int jv = i / H, hh = i % H;
-            const float2 sz = SEG ? k.svs[(size_t)(vs0 + jv) * H + hh]
-                                  : make_float2(st.dsv[st.vdj[jv] * H + hh], st.dzs[st.vdj[jv] * H + hh]);
+            const float2 sz = sz_of(jv, hh);
             float ap = 0.f, bp = 0.f, an = 0.f, bn = 0.f;
-            for (int e = st.vptr[jv]; e < st.vptr[jv + 1]; ++e) {
-                const float a = st.ea[e * H + hh], q = fabsf(a);
-                if (signbit(a)) {
-                    an = __builtin_fmaf(q, st.eda[e * H + hh], an);
-                    bn += q;
-                } else {
-                    ap = __builtin_fmaf(q, st.eda[e * H + hh], ap);
-                    bp += q;
+            const int eb = st.vptr[jv], ee = st.vptr[jv + 1];
+            for (int e = eb; e < ee; e += 4) {
+                float2 p[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    p[u] = ay2[(size_t)(e0 + (e + u < ee ? e + u : ee - 1)) * H + hh];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (e + u >= ee) break;
+                    const float a = p[u].x, q = fabsf(a);
+                    if (signbit(a)) {
+                        an = __builtin_fmaf(q, p[u].y, an);
+                        bn += q;
+                    } else {
+                        ap = __builtin_fmaf(q, p[u].y, ap);
+                        bp += q;
+                    }
                 }
             }
             const float ys = sz.y > 0.f ? (cross_diff(ap, sz.y, sz.x, bp) + k.slope * cross_diff(an, sz.y, sz.x, bn)) /
                                               (sz.y * sz.y)
                                         : 0.f;
             k.ysum[(size_t)st.vpos[jv] * H + hh] = ys;
-            st.vw[i] = ys;
         }
     }
-    __syncthreads();
+    __syncthreads();   // every (q, dalpha) of the item has been read; ysum is visible
+    // pass 2: (alpha, Y) per edge and head, over the pairs written by pass 1
+    if (fin) {
+        for (int i = gl; i < ne * H; i += G) {
+            const int e = i / H, hh = i % H, jv = st.evs[e];
+            const float2 sz = sz_of(jv, hh);
+            const float2 p = ay2[(size_t)e0 * H + i];
+            const float a = p.x;
+            const float al = sz.y > 0.f ? fabsf(a) / sz.y : 0.f;
+            const float dz = sz.y > 0.f ? mul_sub_exact(p.y, sz.y, sz.x) / sz.y : 0.f;
+            const float Y = al * dz * (signbit(a) ? k.slope : 1.f);
+            ay2[(size_t)e0 * H + i] = make_float2(al, Y);
+        }
+    }
     // pass 3: destination term dh_v = sum over v's segments and heads of ysum * wt'
     if (fin && slot < 0 && (PHASE == 0 || SEG)) {
         float4 acc = zero4();
@@ -309,36 +302,39 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
         };
         constexpr int SB = 2;   // segments per batch
         float4 Aw[SB][H], Bw[SB][H];
-        auto load = [&](float4 (&Xw)[SB][H], int base) {
+        float Ay[SB][H], By[SB][H];
+        auto load = [&](float4 (&Xw)[SB][H], float (&Xy)[SB][H], int base) {
 #pragma unroll
             for (int u = 0; u < SB; ++u) {
                 const int jv = base + u < nv ? base + u : (nv > 0 ? nv - 1 : 0);
 #pragma unroll
-                for (int hh = 0; hh < H; ++hh)
+                for (int hh = 0; hh < H; ++hh) {
                     Xw[u][hh] = ld4(k.wtp + ((size_t)st.vrel[jv] * H + hh) * D + gl * 4);
+                    Xy[u][hh] = k.ysum[(size_t)st.vpos[jv] * H + hh];
+                }
             }
         };
-        auto consume = [&](const float4 (&Xw)[SB][H], int base) {
+        auto consume = [&](const float4 (&Xw)[SB][H], const float (&Xy)[SB][H], int base) {
 #pragma unroll
             for (int u = 0; u < SB; ++u) {
                 const int jv = base + u;
                 if (jv < nv) {
                     flush_to(st.vdj[jv]);
 #pragma unroll
-                    for (int hh = 0; hh < H; ++hh) acc = lin4(acc, 1.f, Xw[u][hh], st.vw[jv * H + hh]);
+                    for (int hh = 0; hh < H; ++hh) acc = lin4(acc, 1.f, Xw[u][hh], Xy[u][hh]);
                 }
             }
         };
         if (nv > 0) {
-            load(Aw, 0);
+            load(Aw, Ay, 0);
             __builtin_amdgcn_sched_barrier(0);
             for (int b = 0; b < nv; b += 2 * SB) {
-                load(Bw, b + SB);
+                load(Bw, By, b + SB);
                 __builtin_amdgcn_sched_barrier(0);
-                consume(Aw, b);
-                load(Aw, b + 2 * SB);
+                consume(Aw, Ay, b);
+                load(Aw, Ay, b + 2 * SB);
                 __builtin_amdgcn_sched_barrier(0);
-                consume(Bw, b + SB);
+                consume(Bw, By, b + SB);
             }
         }
         flush_to(nd);
@@ -715,7 +711,7 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
     k.n_items = g->n_items; k.items = x.items; k.item_slot = x.item_slot; k.dst_vsegptr = x.dst_vsegptr;
     k.vseg_ptr = x.vseg_ptr; k.vseg_rel = x.vseg_rel; k.vseg_pos = x.vseg_pos; k.e2u = x.e2u;
     k.vseg_seg = x.vseg_seg; k.M = w.M; k.w_src = w_src; k.wtp = w.wtp; k.saved = saved; k.vatt = w.vatt;
-    k.G = Gm; k.sv_in = w.sv; k.ssum = w.ssum; k.svs = w.svs; k.slope = slope; k.ay = w.ay; k.ysum = w.ysum;
+    k.G = Gm; k.sv = w.sv; k.ssum = w.ssum; k.svs = w.svs; k.slope = slope; k.ay = w.ay; k.ysum = w.ysum;
     k.dh = dh; k.split_items = x.split_items; k.n_split_items = g->n_split_items;
     constexpr int NTH = mh_threads(D), GPB = NTH / (D / 4);
     if (g->n_items) {
@@ -723,7 +719,7 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
         if (per_seg) {
             {
                 LaunchScope ls("rgat_bwd_heads_dst", s);
-                hipLaunchKernelGGL((mh_dst_kernel<D, H, 0, true>), grid, dim3(NTH), 0, s, k);
+                hipLaunchKernelGGL((mh_dst_kernel<D, H, 0, true, kDstKU>), grid, dim3(NTH), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_dst launch");
             if (g->U_dst) {
@@ -734,12 +730,12 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_merge_seg launch");
             {
                 LaunchScope ls("rgat_bwd_heads_dst_seg", s);
-                hipLaunchKernelGGL((mh_dst_kernel<D, H, 1, true>), grid, dim3(NTH), 0, s, k);
+                hipLaunchKernelGGL((mh_dst_kernel<D, H, 1, true, kDstKU>), grid, dim3(NTH), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_dst launch");
         } else {
             LaunchScope ls("rgat_bwd_heads_dst", s);
-            hipLaunchKernelGGL((mh_dst_kernel<D, H, 0, false>), grid, dim3(NTH), 0, s, k);
+            hipLaunchKernelGGL((mh_dst_kernel<D, H, 0, false, kDstKU>), grid, dim3(NTH), 0, s, k);
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_dst launch");
         }
         if (g->n_split) {
@@ -753,7 +749,7 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
                 if (g->n_split_items) {
                     LaunchScope ls("rgat_bwd_heads_dst_split", s);
                     const dim3 sgrid((unsigned)((g->n_split_items + GPB - 1) / GPB));
-                    hipLaunchKernelGGL((mh_dst_kernel<D, H, 1, false>), sgrid, dim3(NTH), 0, s, k);
+                    hipLaunchKernelGGL((mh_dst_kernel<D, H, 1, false, kDstKU>), sgrid, dim3(NTH), 0, s, k);
                 }
                 if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_dst launch");
             }
