@@ -538,6 +538,172 @@ __global__ __launch_bounds__(256) void mh_zero_split_pairs_kernel(const int32_t 
 }
 
 // dh_u += sum of the rows of u's pairs in source-major order (dHp = dM W_r^T).
+// ---------------------------------------------------------------- pair-major pass (d <= 64)
+// One workgroup per chunk of virtual pairs of one relation r (a compact pair,
+// or a piece of at most kPairPiece of its out-edges).  In steps of KB virtual
+// pairs, every group of D/4 lanes forms the dM rows of its pairs from their
+// out-edges (the alpha-weighted G rows summed in out-edge order, plus the sum
+// of Y times w_src[r], per head) and fetches their h_u rows, both into LDS; then
+// on the matrix cores
+//   dHp rows  = dM W_r^T    (stored at the virtual pair's source-major row)
+//   partial  += h^T dM       (the chunk's share of dW_r, 16 rows per wave)
+// and per head the chunk's sum of ypair h_u (its share of dws').  The
+// per-pair gradient dM and the per-pair Y sums never go to memory.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+struct PF {
+    const Tile *tiles;
+    const int32_t *vpair_oe0, *vpair_ne, *vpair_src, *vpair_smpos;
+    const int32_t *out_pos, *out_dst;   // sorted in-edge position and destination of each out-edge
+    const float *G, *ay, *w_src, *W, *h;
+    float *dHp;              // [NVP, D] rows in source-major order
+    float *partial;          // [chunks, D, D]
+    float *pvec;             // [chunks, H, D]
+};
+
+template <int D, int H>
+__global__ __launch_bounds__(256) void mh_pair_fused_kernel(PF k)
+{
+    static_assert(H <= 4, "the per-head Y sums ride in the four padding floats of an LDS row");
+    constexpr int G = D / 4, NG = 256 / G, LH = G / H;
+    constexpr int KB = 64, P = D + 4;
+    constexpr int RPG = KB / NG;        // pair rows per group and step
+    constexpr int NCB = D / 16, KC = D / 16;
+    static_assert(RPG * NG == KB, "a step must split evenly over the groups");
+    __shared__ float Ws[D * P];         // W_r, row-major: Ws[i * P + j] = W_r[i][j]
+    __shared__ float As[KB * P];        // h_u rows of the step's virtual pairs, their sums of Y
+                                        // per head in the row padding (H <= 4)
+    __shared__ float Bs[KB * P];        // their dM rows
+    const Tile t = k.tiles[blockIdx.x];
+    const int r = t.type;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, q = lane >> 4;
+    const int gl = tid % G, gi = tid / G, head = gl / LH;
+    const bool hl = gl % LH == 0;
+    for (int i = tid; i < D * D / 4; i += 256) {
+        const int row = i / (D / 4), c4 = (i % (D / 4)) * 4;
+        *reinterpret_cast<float4 *>(&Ws[row * P + c4]) = ld4(k.W + ((size_t)r * D + row) * D + c4);
+    }
+    const float4 ws = ld4(k.w_src + (size_t)r * D + gl * 4);
+    const float2 *ay2 = reinterpret_cast<const float2 *>(k.ay);
+    // outer-product accumulators: NCB blocks of h^T dM, and one block of h^T Y
+    // (its first H columns: the chunk's dws' share per head)
+    floatx4 acc[NCB + 1];
+#pragma unroll
+    for (int cb = 0; cb <= NCB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < t.rows; k0 += KB) {
+        // gather: the group's RPG rows together, two out-edges of each per batch
+        int oe[RPG], ne[RPG], us[RPG];
+#pragma unroll
+        for (int s = 0; s < RPG; ++s) {
+            const int rr = gi + NG * s;
+            const bool ok = k0 + rr < t.rows;
+            const int vp = t.row0 + (ok ? k0 + rr : 0);
+            oe[s] = k.vpair_oe0[vp];
+            ne[s] = ok ? k.vpair_ne[vp] : 0;
+            us[s] = k.vpair_src[vp];
+        }
+        float4 hr[RPG], am[RPG];
+        float ys[RPG];
+        int nmax = 0;
+#pragma unroll
+        for (int s = 0; s < RPG; ++s) {
+            hr[s] = ld4(k.h + (size_t)us[s] * D + gl * 4);
+            am[s] = zero4();
+            ys[s] = 0.f;
+            nmax = ne[s] > nmax ? ne[s] : nmax;
+        }
+        for (int o = 0; o < nmax; o += 2) {
+            int pos[RPG][2], dv[RPG][2];
+#pragma unroll
+            for (int s = 0; s < RPG; ++s)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int e = oe[s] + (o + u < ne[s] ? o + u : 0);
+                    pos[s][u] = k.out_pos[e];
+                    dv[s][u] = k.out_dst[e];
+                }
+            float4 gr[RPG][2];
+            float2 a[RPG][2];
+#pragma unroll
+            for (int s = 0; s < RPG; ++s)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    gr[s][u] = ld4(k.G + (size_t)dv[s][u] * D + gl * 4);
+                    a[s][u] = ay2[(size_t)pos[s][u] * H + head];
+                }
+#pragma unroll
+            for (int s = 0; s < RPG; ++s)
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    if (o + u < ne[s]) {
+                        am[s] = lin4(am[s], 1.f, gr[s][u], a[s][u].x);
+                        ys[s] += a[s][u].y;
+                    }
+        }
+#pragma unroll
+        for (int s = 0; s < RPG; ++s) {
+            const int rr = gi + NG * s;
+            const bool ok = ne[s] > 0;
+            *reinterpret_cast<float4 *>(&As[rr * P + gl * 4]) = ok ? hr[s] : zero4();
+            *reinterpret_cast<float4 *>(&Bs[rr * P + gl * 4]) = ok ? lin4(am[s], 1.f, ws, ys[s]) : zero4();
+            if (hl) As[rr * P + D + head] = ok ? ys[s] : 0.f;
+        }
+        __syncthreads();
+        // dHp rows of this wave's 16 virtual pairs (transposed block: lane
+        // (li, q) ends with row li, columns 4q .. 4q + 3 of each column block)
+        {
+            const int p0 = wave * 16;
+            floatx4 o4[NCB];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) o4[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                const float4 b4 = *reinterpret_cast<const float4 *>(&Bs[(p0 + li) * P + c * 16 + q * 4]);
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const float4 a4 = *reinterpret_cast<const float4 *>(&Ws[(cb * 16 + li) * P + c * 16 + q * 4]);
+                    o4[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, b4.x, o4[cb], 0, 0, 0);
+                    o4[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, b4.y, o4[cb], 0, 0, 0);
+                    o4[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, b4.z, o4[cb], 0, 0, 0);
+                    o4[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, b4.w, o4[cb], 0, 0, 0);
+                }
+            }
+            const int row = k0 + p0 + li;
+            if (p0 < KB && row < t.rows) {
+                float *dst = k.dHp + (size_t)k.vpair_smpos[t.row0 + row] * D + q * 4;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    st4(dst + cb * 16, make_float4(o4[cb][0], o4[cb][1], o4[cb][2], o4[cb][3]));
+            }
+        }
+        // the chunk's dW_r share: rows 16 wave .. of h^T dM, k over the step's pairs
+        if (wave * 16 < D) {
+#pragma unroll 4
+            for (int kk = 0; kk < KB; kk += 4) {
+                const float av = As[(kk + q) * P + wave * 16 + li];
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[(kk + q) * P + cb * 16 + li], acc[cb], 0, 0, 0);
+                const float yv = li < H ? As[(kk + q) * P + D + li] : 0.f;
+                acc[NCB] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, yv, acc[NCB], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    if (wave * 16 < D) {
+        float *out = k.partial + (size_t)blockIdx.x * D * D;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) out[(size_t)(wave * 16 + q * 4 + v) * D + cb * 16 + li] = acc[cb][v];
+        if (li < H)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                k.pvec[((size_t)blockIdx.x * H + li) * D + wave * 16 + q * 4 + v] = acc[NCB][v];
+    }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void mh_src_sum_kernel(int64_t N, const int32_t *src_pairptr, const float *dHp,
                                                          float *dh)
@@ -665,13 +831,15 @@ size_t mh_layout(const rgnn_graph *g, int D, int H, void *base, MhWs *w)
     MhWs x;
     x.wtp = take(R * H * D);
     x.vatt = take(V * H);
-    x.M = take(U * D);              // messages, then their gradients dM
-    x.dHp = take(U * D);
+    const size_t NVP = std::max<size_t>((size_t)g->n_vpairs, U);
+    const size_t NCH = std::max<size_t>((size_t)g->n_tiles_vpairs, (size_t)g->n_tiles_outer_pairs);
+    x.M = take(U * D);              // messages (then, at d = 128, their gradients dM)
+    x.dHp = take(NVP * D);          // dM W_r^T per (virtual) pair, source-major
     x.ay = take((size_t)g->E * H * 2);
     x.ysum = take(V * H);
     x.ypair = take(U * H);
-    x.partial = take((size_t)g->n_tiles_outer_pairs * D * D);
-    x.pvec = take((size_t)g->n_tiles_outer_pairs * H * D);
+    x.partial = take(NCH * D * D);
+    x.pvec = take(NCH * H * D);
     x.yvec = take((size_t)g->n_tiles_outer * H * D);
     x.dws = take(R * H * D);
     x.dwt = take(R * H * D);
@@ -761,58 +929,90 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_split_dst_term launch");
         }
     }
-    // dM per pair (the messages' buffer is reused: M is not read after this)
-    float *dM = w.M;
-    if (g->n_osplit) {
-        LaunchScope ls("zero", s);
-        hipLaunchKernelGGL((mh_zero_split_pairs_kernel<D, H>), dim3((unsigned)g->n_osplit), dim3(256), 0, s,
-                           x.osplit, x.out_ptr, x.out_pair, dM, w.ypair);
+    const int32_t *pairchunkptr = x.rel_pairchunkptr;
+    if constexpr (D <= 64) {
+        // one pair-major pass: dM per virtual pair, dHp = dM W_r^T and the
+        // chunk shares of dW_r and dws' (dM stays on chip)
+        if (g->n_tiles_vpairs) {
+            PF p{};
+            p.tiles = x.tiles_vpairs; p.vpair_oe0 = x.vpair_oe0; p.vpair_ne = x.vpair_ne;
+            p.vpair_src = x.vpair_src; p.vpair_smpos = x.vpair_smpos; p.out_pos = x.out_pos; p.out_dst = x.out_dst;
+            p.G = Gm; p.ay = w.ay; p.w_src = w_src; p.W = W; p.h = h;
+            p.dHp = w.dHp; p.partial = w.partial; p.pvec = w.pvec;
+            LaunchScope ls("rgat_bwd_heads_pair", s);
+            hipLaunchKernelGGL((mh_pair_fused_kernel<D, H>), dim3((unsigned)g->n_tiles_vpairs), dim3(256), 0, s, p);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_pair_fused launch");
+        if (g->N) {
+            LaunchScope ls("rgat_bwd_heads_src_sum", s);
+            constexpr int SPB = 256 / (D / 4);
+            hipLaunchKernelGGL(mh_src_sum_kernel<D>, dim3((unsigned)((g->N + SPB - 1) / SPB)), dim3(256), 0, s, g->N,
+                               x.src_vpairptr, w.dHp, dh);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_src_sum launch");
+        if ((st = launch_chunk_sum(w.partial, x.rel_vpairchunkptr, g->R, dW, D, s)) != RGNN_OK) return st;
+        pairchunkptr = x.rel_vpairchunkptr;
+        {   // dwt' per relation and head
+            LaunchScope ls("rgat_bwd_heads_gemv", s);
+            if (g->n_tiles_outer)
+                hipLaunchKernelGGL((mh_gemv_kernel<D, H>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
+                                   x.tiles_outer, x.vsegdst_byrel, w.ysum, h, w.yvec);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_gemv launch");
+    } else {
+        // dM per pair (the messages' buffer is reused: M is not read after this)
+        float *dM = w.M;
+        if (g->n_osplit) {
+            LaunchScope ls("zero", s);
+            hipLaunchKernelGGL((mh_zero_split_pairs_kernel<D, H>), dim3((unsigned)g->n_osplit), dim3(256), 0, s,
+                               x.osplit, x.out_ptr, x.out_pair, dM, w.ypair);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "zero launch");
+        if (g->n_oitems) {
+            PK p{};
+            p.n_items = g->n_oitems; p.items = x.oitems; p.out_ptr = x.out_ptr; p.out_pos = x.out_pos;
+            p.out_rel = x.out_rel; p.out_pair = x.out_pair; p.out_dst = x.out_dst; p.G = Gm; p.ay = w.ay;
+            p.w_src = w_src; p.dM = dM; p.ypair = w.ypair;
+            LaunchScope ls("rgat_bwd_heads_pair", s);
+            hipLaunchKernelGGL((mh_pair_kernel<D, H>), dim3((unsigned)((g->n_oitems + GPB - 1) / GPB)), dim3(NTH), 0, s,
+                               p);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_pair launch");
+        {   // dHp = dM W_r^T, rows in source-major pair order
+            GemmArgs ga;
+            ga.X = dM; ga.ldx = D; ga.gather = nullptr;
+            ga.W[0] = W; ga.trans_b = 1; ga.K = D; ga.Nc = D;
+            ga.tiles = x.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
+            ga.Y = w.dHp; ga.ldy = D; ga.scatter = x.pair_smpos;
+            if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+        }
+        if (g->N) {
+            LaunchScope ls("rgat_bwd_heads_src_sum", s);
+            constexpr int SPB = 256 / (D / 4);
+            hipLaunchKernelGGL(mh_src_sum_kernel<D>, dim3((unsigned)((g->N + SPB - 1) / SPB)), dim3(256), 0, s, g->N,
+                               x.src_pairptr, w.dHp, dh);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_src_sum launch");
+        // dW: outer products h_u^T dM over the pairs of each relation, summed in order
+        if ((st = launch_outer_chunks(x.tiles_outer_pairs, g->n_tiles_outer_pairs, x.uniq_src, 2, h, D, dM, D,
+                                      w.partial, D, s)) != RGNN_OK)
+            return st;
+        if ((st = launch_chunk_sum(w.partial, x.rel_pairchunkptr, g->R, dW, D, s)) != RGNN_OK) return st;
+        {   // dws' and dwt' per relation and head
+            LaunchScope ls("rgat_bwd_heads_gemv", s);
+            if (g->n_tiles_outer_pairs)
+                hipLaunchKernelGGL((mh_gemv_kernel<D, H>), dim3((unsigned)g->n_tiles_outer_pairs), dim3(256), 0, s,
+                                   x.tiles_outer_pairs, x.uniq_src, w.ypair, h, w.pvec);
+            if (g->n_tiles_outer)
+                hipLaunchKernelGGL((mh_gemv_kernel<D, H>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
+                                   x.tiles_outer, x.vsegdst_byrel, w.ysum, h, w.yvec);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_gemv launch");
     }
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "zero launch");
-    if (g->n_oitems) {
-        PK p{};
-        p.n_items = g->n_oitems; p.items = x.oitems; p.out_ptr = x.out_ptr; p.out_pos = x.out_pos;
-        p.out_rel = x.out_rel; p.out_pair = x.out_pair; p.out_dst = x.out_dst; p.G = Gm; p.ay = w.ay;
-        p.w_src = w_src; p.dM = dM; p.ypair = w.ypair;
-        LaunchScope ls("rgat_bwd_heads_pair", s);
-        hipLaunchKernelGGL((mh_pair_kernel<D, H>), dim3((unsigned)((g->n_oitems + GPB - 1) / GPB)), dim3(NTH), 0, s,
-                           p);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_pair launch");
-    {   // dHp = dM W_r^T, rows in source-major pair order
-        GemmArgs ga;
-        ga.X = dM; ga.ldx = D; ga.gather = nullptr;
-        ga.W[0] = W; ga.trans_b = 1; ga.K = D; ga.Nc = D;
-        ga.tiles = x.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
-        ga.Y = w.dHp; ga.ldy = D; ga.scatter = x.pair_smpos;
-        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
-    }
-    if (g->N) {
-        LaunchScope ls("rgat_bwd_heads_src_sum", s);
-        constexpr int SPB = 256 / (D / 4);
-        hipLaunchKernelGGL(mh_src_sum_kernel<D>, dim3((unsigned)((g->N + SPB - 1) / SPB)), dim3(256), 0, s, g->N,
-                           x.src_pairptr, w.dHp, dh);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_src_sum launch");
-    // dW: outer products h_u^T dM over the pairs of each relation, summed in order
-    if ((st = launch_outer_chunks(x.tiles_outer_pairs, g->n_tiles_outer_pairs, x.uniq_src, 2, h, D, dM, D,
-                                  w.partial, D, s)) != RGNN_OK)
-        return st;
-    if ((st = launch_chunk_sum(w.partial, x.rel_pairchunkptr, g->R, dW, D, s)) != RGNN_OK) return st;
-    {   // dws' and dwt' per relation and head
-        LaunchScope ls("rgat_bwd_heads_gemv", s);
-        if (g->n_tiles_outer_pairs)
-            hipLaunchKernelGGL((mh_gemv_kernel<D, H>), dim3((unsigned)g->n_tiles_outer_pairs), dim3(256), 0, s,
-                               x.tiles_outer_pairs, x.uniq_src, w.ypair, h, w.pvec);
-        if (g->n_tiles_outer)
-            hipLaunchKernelGGL((mh_gemv_kernel<D, H>), dim3((unsigned)g->n_tiles_outer), dim3(256), 0, s,
-                               x.tiles_outer, x.vsegdst_byrel, w.ysum, h, w.yvec);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_gemv launch");
     {
         LaunchScope ls("rgat_bwd_heads_finalize", s);
         hipLaunchKernelGGL((mh_reduce_kernel<D, H>), dim3((unsigned)g->R, H * D / 64), dim3(1024), 0, s, w.pvec,
-                           x.rel_pairchunkptr, w.yvec, x.rel_chunkptr, w.dws, w.dwt);
+                           pairchunkptr, w.yvec, x.rel_chunkptr, w.dws, w.dwt);
         hipLaunchKernelGGL((mh_finalize_kernel<D, H>), dim3((unsigned)g->R, D * D / 256), dim3(256), 0, s, W, w_dst,
                            w.dws, w.dwt, dW, dws, dwt);
     }

@@ -365,6 +365,43 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             for (int64_t i = 0; i < g->U_src; ++i) x.src_pairptr[(size_t)x.uniq_src[i] + 1]++;
             for (int64_t u = 0; u < N; ++u) x.src_pairptr[u + 1] += x.src_pairptr[u];
         }
+        // virtual pairs: a pair's out-edges are consecutive in the out-edge
+        // order (src, rel, position); pieces of at most kPairPiece of them, in
+        // (rel, src) order, then their rows in source-major order and chunks
+        // per relation
+        {
+            std::vector<int32_t> oe0((size_t)g->U_src, -1), oen((size_t)g->U_src, 0);
+            for (int64_t q = 0; q < E; ++q) {
+                const int32_t p = x.out_pair[q];
+                if (oe0[p] < 0) oe0[p] = (int32_t)q;
+                oen[p]++;
+            }
+            x.vpair_oe0.clear(); x.vpair_ne.clear(); x.vpair_src.clear();
+            std::vector<int32_t> rel_vpairptr((size_t)R + 1, 0);
+            for (int32_t r = 0; r < R; ++r) {
+                for (int32_t p = x.uniq_rel_ptr[r]; p < x.uniq_rel_ptr[r + 1]; ++p)
+                    for (int32_t o = 0; o < oen[p]; o += kPairPiece) {
+                        x.vpair_oe0.push_back(oe0[p] + o);
+                        x.vpair_ne.push_back(std::min<int32_t>(kPairPiece, oen[p] - o));
+                        x.vpair_src.push_back(x.uniq_src[p]);
+                    }
+                rel_vpairptr[(size_t)r + 1] = (int32_t)x.vpair_src.size();
+            }
+            g->n_vpairs = (int64_t)x.vpair_src.size();
+            std::vector<int32_t> vp((size_t)g->n_vpairs);
+            for (int64_t i = 0; i < g->n_vpairs; ++i) vp[i] = (int32_t)i;
+            counting_sort(vp, x.vpair_src.data(), N, tmp, cnt);
+            x.vpair_smpos.resize((size_t)g->n_vpairs);
+            for (int64_t i = 0; i < g->n_vpairs; ++i) x.vpair_smpos[vp[i]] = (int32_t)i;
+            x.src_vpairptr.assign((size_t)N + 1, 0);
+            for (int64_t i = 0; i < g->n_vpairs; ++i) x.src_vpairptr[(size_t)x.vpair_src[i] + 1]++;
+            for (int64_t u = 0; u < N; ++u) x.src_vpairptr[u + 1] += x.src_vpairptr[u];
+            build_tiles(rel_vpairptr, kPairChunkRows, x.tiles_vpairs);
+            g->n_tiles_vpairs = (int64_t)x.tiles_vpairs.size();
+            x.rel_vpairchunkptr.assign((size_t)R + 1, 0);
+            for (const Tile &t : x.tiles_vpairs) x.rel_vpairchunkptr[(size_t)t.type + 1]++;
+            for (int32_t r = 0; r < R; ++r) x.rel_vpairchunkptr[r + 1] += x.rel_vpairchunkptr[r];
+        }
     } catch (const std::bad_alloc &) {
         return fail(RGNN_ENOMEM, "host allocation failed while building the graph index");
     }
@@ -426,6 +463,10 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.rel_pairchunkptr, x.rel_pairchunkptr);
     parts.push_back(Part{(void **)&d.tiles_outer_pairs, x.tiles_outer_pairs.data(),
                          x.tiles_outer_pairs.size() * sizeof(Tile)});
+    add32(&d.vpair_oe0, x.vpair_oe0); add32(&d.vpair_ne, x.vpair_ne); add32(&d.vpair_src, x.vpair_src);
+    add32(&d.vpair_smpos, x.vpair_smpos); add32(&d.src_vpairptr, x.src_vpairptr);
+    add32(&d.rel_vpairchunkptr, x.rel_vpairchunkptr);
+    parts.push_back(Part{(void **)&d.tiles_vpairs, x.tiles_vpairs.data(), x.tiles_vpairs.size() * sizeof(Tile)});
     size_t total = 0;
     for (auto &p : parts) total += (p.bytes + 255) & ~size_t(255);
     total = std::max<size_t>(total, 256);
@@ -494,6 +535,8 @@ rgnn_status create_common(int64_t N, int32_t T, int32_t R, int64_t E, const int3
         g->host.out_pos.swap(empty.out_pos); g->host.out_vseg.swap(empty.out_vseg);
         g->host.out_rel.swap(empty.out_rel); g->host.out_pair.swap(empty.out_pair);
         g->host.out_vs.swap(empty.out_vs); g->host.out_dst.swap(empty.out_dst);
+        g->host.vpair_oe0.swap(empty.vpair_oe0); g->host.vpair_ne.swap(empty.vpair_ne);
+        g->host.vpair_src.swap(empty.vpair_src); g->host.vpair_smpos.swap(empty.vpair_smpos);
     }
     *out = g;
     return RGNN_OK;

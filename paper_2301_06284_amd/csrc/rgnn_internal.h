@@ -30,6 +30,10 @@ constexpr int kBigRange = 32;
 constexpr int kMergeChunk = 128;
 // rows (segments or nodes) per K-chunk of the backward outer-product GEMMs
 constexpr int kOuterRows = 2048;
+// several-head backward, pair pass: out-edges per virtual pair (longer pairs
+// are cut into pieces) and virtual pairs per workgroup chunk
+constexpr int kPairPiece = 64;
+constexpr int kPairChunkRows = 1024;
 
 struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type `type`
     int32_t type, row0, rows, pad;
@@ -89,6 +93,14 @@ struct HostIndex {
     std::vector<int32_t> pair_smpos;     // [U_src] position of each pair in that order
     std::vector<Tile> tiles_outer_pairs;  // outer-product chunks over the pairs of each relation
     std::vector<int32_t> rel_pairchunkptr;   // those chunks per relation [R+1]
+    // virtual pairs: the compact pairs of each relation in (rel, src) order, cut
+    // into pieces of at most kPairPiece out-edges
+    std::vector<int32_t> vpair_oe0, vpair_ne;   // out-edge range of each virtual pair [NVP]
+    std::vector<int32_t> vpair_src;             // its source [NVP]
+    std::vector<int32_t> vpair_smpos;           // its row in source-major order [NVP]
+    std::vector<int32_t> src_vpairptr;          // virtual pairs of each source in that order [N+1]
+    std::vector<Tile> tiles_vpairs;             // chunks of kPairChunkRows virtual pairs of one relation
+    std::vector<int32_t> rel_vpairchunkptr;     // those chunks per relation [R+1]
 };
 
 // Device copies (one allocation, carved).
@@ -125,6 +137,9 @@ struct DeviceIndex {
     Item *oitems = nullptr;
     int32_t *src_pairptr = nullptr, *pair_smpos = nullptr, *rel_pairchunkptr = nullptr;
     Tile *tiles_outer_pairs = nullptr;
+    int32_t *vpair_oe0 = nullptr, *vpair_ne = nullptr, *vpair_src = nullptr, *vpair_smpos = nullptr;
+    int32_t *src_vpairptr = nullptr, *rel_vpairchunkptr = nullptr;
+    Tile *tiles_vpairs = nullptr;
 };
 
 }  // namespace rgnn
@@ -141,6 +156,7 @@ struct rgnn_graph {
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
     int64_t n_oitems = 0, n_osplit = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
+    int64_t n_vpairs = 0, n_tiles_vpairs = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
