@@ -934,15 +934,46 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "outer_gemm launch");
 }
 
+namespace {
+
+// dW[t] = sum of the partials of t's chunks [chunkptr[t], chunkptr[t + 1]),
+// per 64 entries (blockIdx.y): 16 slices of threads take every 16th chunk
+// (four loads in flight), the slice sums are added in slice order.
+template <int D>
+__global__ __launch_bounds__(1024) void chunk_sum_kernel(const float *partial, const int32_t *chunkptr, float *dW)
+{
+    constexpr int NS = 16, U = 4;
+    __shared__ float red[NS][64];
+    const int t = blockIdx.x, li = threadIdx.x % 64, c = threadIdx.x / 64;
+    const int i = blockIdx.y * 64 + li;
+    const int c0 = chunkptr[t], c1 = chunkptr[t + 1];
+    float s = 0.f;
+    for (int ch = c0 + c; ch < c1; ch += NS * U) {
+        float p[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) p[u] = ch + u * NS < c1 ? partial[(size_t)(ch + u * NS) * D * D + i] : 0.f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) s += p[u];
+    }
+    red[c][li] = s;
+    __syncthreads();
+    if (c == 0) {
+        float tot = 0.f;
+        for (int cc = 0; cc < NS; ++cc) tot += red[cc][li];
+        dW[(size_t)t * D * D + i] = tot;
+    }
+}
+
+}  // namespace
+
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s)
 {
     if (R == 0) return RGNN_OK;
     {
         LaunchScope ls("chunk_sum", s);
-#define CS(D) hipLaunchKernelGGL((bwd_finalize_kernel<D, false>), dim3((unsigned)R, D * D / 256), dim3(256), 0, s, \
-                                 partial, chunkptr, nullptr, nullptr, nullptr, nullptr, nullptr, dW, nullptr, nullptr, \
-                                 0, D, 0)
+#define CS(D) hipLaunchKernelGGL((chunk_sum_kernel<D>), dim3((unsigned)R, D * D / 64), dim3(1024), 0, s, \
+                                 partial, chunkptr, dW)
         if (d == 32) CS(32);
         else if (d == 64) CS(64);
         else if (d == 128) CS(128);

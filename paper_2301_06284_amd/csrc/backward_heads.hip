@@ -715,12 +715,15 @@ __global__ __launch_bounds__(256) void mh_src_sum_kernel(int64_t N, const int32_
     const int b = src_pairptr[u], e = src_pairptr[u + 1];
     if (b == e) return;
     float4 acc = ld4(dh + (size_t)u * D + gl * 4);
-    int i = b;
-    for (; i + 1 < e; i += 2) {
-        const float4 x0 = ld4(dHp + (size_t)i * D + gl * 4), x1 = ld4(dHp + (size_t)(i + 1) * D + gl * 4);
-        acc = add4(acc, add4(x0, x1));
+    // rows in batches of four (clamped loads, all in flight together)
+    for (int i = b; i < e; i += 4) {
+        float4 x[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = ld4(dHp + (size_t)(i + j < e ? i + j : e - 1) * D + gl * 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (i + j < e) acc = add4(acc, x[j]);
     }
-    if (i < e) acc = add4(acc, ld4(dHp + (size_t)i * D + gl * 4));
     st4(dh + (size_t)u * D + gl * 4, acc);
 }
 
