@@ -51,8 +51,10 @@
 //   3. A source-major traversal over the out-edges (sorted by source, then
 //      relation) that gathers dS rows and forms dh_u = (destination term) +
 //      sum alpha dS + Y ws'_r with one store per source row: the scatter of
-//      the paper's backward becomes a gather, with no per-edge atomics.  It
-//      also sums Y per (source, relation) pair, the compact rows of the
+//      the paper's backward becomes a gather, with no per-edge atomics.
+//      Pieces of sources with more than kChunkEdges out-edges leave their sums
+//      in slots, added to dh in slot order by one workgroup per such source.
+//      It also sums Y per (source, relation) pair, the compact rows of the
 //      forward.
 //   4. dws'_r = sum over r's compact pairs of ysum_pair * h_src, by chunks of
 //      pairs; an outer-product MFMA GEMM for dW over K-chunks of segments of
@@ -94,10 +96,6 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(
 __device__ __forceinline__ float4 lin4(float4 a, float s, float4 b, float t)
 {
     return make_float4(a.x * s + b.x * t, a.y * s + b.y * t, a.z * s + b.z * t, a.w * s + b.w * t);
-}
-__device__ __forceinline__ void atomic_add4(float *p, float4 v)
-{
-    atomicAdd(p + 0, v.x); atomicAdd(p + 1, v.y); atomicAdd(p + 2, v.z); atomicAdd(p + 3, v.w);
 }
 
 // ---------------------------------------------------------------- destination-major traversal
@@ -503,6 +501,8 @@ struct SK {
     float *dh;                   // holds the destination terms on entry
     float *ypair;                // [U_src] sum of Y per compact (src, rel) pair, zeroed before
                                  // (written by a store, or by atomics for split sources)
+    const int32_t *item_slot;    // slot of each piece of a split source, else -1
+    float *part;                 // [slots, D] such pieces' sums, added to dh in slot order later
 };
 
 struct SStage {
@@ -525,10 +525,12 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_src_kernel(SK k)
     const bool valid = item < k.n_items;
     int n0 = 0, nn = 0, q0 = 0, nq = 0;
     bool split = false;   // a piece of a source whose out-edges span several items
+    int slot = -1;
     if (valid) {
         const Item x = k.items[item];
         n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
-        split = nn == 1 && k.out_ptr[n0 + 1] - k.out_ptr[n0] > nq;
+        slot = k.item_slot[item];
+        split = slot >= 0;
         for (int e = gl; e < nq; e += G) {
             const int p = k.out_pos[q0 + e];
             st.evs[e] = k.out_vseg[q0 + e];
@@ -587,9 +589,8 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_src_kernel(SK k)
                     ysrc = 0.f;
                 }
                 if (node_end) {
-                    float *p = k.dh + (size_t)(n0 + j) * D + gl * 4;
-                    if (split) atomic_add4(p, acc);
-                    else st4(p, add4(acc, Xh[u]));
+                    if (split) st4(k.part + (size_t)slot * D + gl * 4, acc);
+                    else st4(k.dh + (size_t)(n0 + j) * D + gl * 4, add4(acc, Xh[u]));
                     acc = zero4();
                     ++j;
                     while (j < nn && st.optr[j + 1] == st.optr[j]) ++j;
@@ -836,7 +837,7 @@ __global__ void zero_kernel(float *p, int64_t n)
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct BwdWs {
-    float *wsp, *wtp, *vatt, *dS, *Sa, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec;
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec, *part;
     float2 *ssum, *sv, *svs;
 };
 
@@ -867,6 +868,7 @@ size_t bwd_layout(const rgnn_graph *g, int D, void *base, BwdWs *w)
     x.pwt = take((size_t)g->R * D);
     x.partial = take(nchunks * D * D);
     x.yvec = take(nchunks * D);
+    x.part = take((size_t)std::max<int64_t>(g->n_oslots, 1) * D);
     if (w) *w = x;
     return off;
 }
@@ -936,6 +938,34 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
 
 namespace {
 
+// One 1024-thread workgroup per split source: groups of D/4 lanes take every NG-th slot
+// (four rows in flight), the group sums are added in group order, then to dh.
+template <int D>
+__global__ __launch_bounds__(1024) void src_merge_kernel(const int32_t *osplit, const int32_t *slotptr,
+                                                         const float *part, float *dh)
+{
+    constexpr int G = D / 4, NG = 1024 / G, U = 4;
+    __shared__ float4 red[NG][G];
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    const int b = slotptr[blockIdx.x], e = slotptr[blockIdx.x + 1];
+    float4 acc = zero4();
+    for (int sl = b + gi; sl < e; sl += NG * U) {
+        float4 x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = sl + u * NG < e ? ld4(part + (size_t)(sl + u * NG) * D + gl * 4) : zero4();
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
+    }
+    red[gi][gl] = acc;
+    __syncthreads();
+    if (gi == 0) {
+        float4 t = zero4();
+        for (int j = 0; j < NG; ++j) t = add4(t, red[j][gl]);
+        float *p = dh + (size_t)osplit[blockIdx.x] * D + gl * 4;
+        st4(p, add4(ld4(p), t));
+    }
+}
+
 // dW[t] = sum of the partials of t's chunks [chunkptr[t], chunkptr[t + 1]),
 // per 64 entries (blockIdx.y): 16 slices of threads take every 16th chunk
 // (four loads in flight), the slice sums are added in slice order.
@@ -965,6 +995,23 @@ __global__ __launch_bounds__(1024) void chunk_sum_kernel(const float *partial, c
 }
 
 }  // namespace
+
+rgnn_status launch_src_merge(const rgnn_graph *g, const float *part, float *dh, int d, hipStream_t s)
+{
+    if (g->n_osplit == 0) return RGNN_OK;
+    {
+        LaunchScope ls("src_merge", s);
+#define SM(D) hipLaunchKernelGGL((src_merge_kernel<D>), dim3((unsigned)g->n_osplit), dim3(1024), 0, s, g->dev.osplit, \
+                                 g->dev.osplit_slotptr, part, dh)
+        if (d == 32) SM(32);
+        else if (d == 64) SM(64);
+        else if (d == 128) SM(128);
+        else return fail(RGNN_EUNSUPPORTED, "source merge: d must be 32, 64 or 128");
+#undef SM
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "src_merge launch");
+}
 
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s)
@@ -1086,12 +1133,14 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
         sk.n_items = g->n_oitems; sk.items = g->dev.oitems; sk.out_ptr = g->dev.out_ptr;
         sk.out_pos = g->dev.out_pos; sk.out_vseg = g->dev.out_vseg; sk.out_rel = g->dev.out_rel;
         sk.out_pair = g->dev.out_pair; sk.wsp = w.wsp; sk.dS = w.dS; sk.ay = w.ay; sk.dh = dh; sk.ypair = w.ypair;
+        sk.item_slot = g->dev.oitem_slot; sk.part = w.part;
         LaunchScope ls("rgat_bwd_src", s);
         constexpr int GPB = item_threads(D) / (D / 4);
         hipLaunchKernelGGL(bwd_src_kernel<D>, dim3((unsigned)((g->n_oitems + GPB - 1) / GPB)), dim3(item_threads(D)),
                            0, s, sk);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "bwd_src launch");
+    if ((st = launch_src_merge(g, w.part, dh, D, s)) != RGNN_OK) return st;
     if (g->n_tiles_pairs) {   // dws' per pair tile
         LaunchScope ls("rgat_bwd_pair_gemv", s);
         hipLaunchKernelGGL(pair_gemv_kernel<D>, dim3((unsigned)g->n_tiles_pairs), dim3(256), 0, s,

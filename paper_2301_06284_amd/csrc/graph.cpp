@@ -297,14 +297,19 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             // work items over out-edges: bundles of small sources, pieces of large ones
             x.oitems.clear();
             x.osplit.clear();
+            x.oitem_slot.clear();
+            x.osplit_slotptr.assign(1, 0);
             auto odeg = [&](int64_t u) { return x.out_ptr[u + 1] - x.out_ptr[u]; };
             int64_t u = 0;
             while (u < N) {
                 if (odeg(u) > C) {
                     x.osplit.push_back((int32_t)u);
-                    for (int32_t q = x.out_ptr[u]; q < x.out_ptr[u + 1]; q += C)
+                    for (int32_t q = x.out_ptr[u]; q < x.out_ptr[u + 1]; q += C) {
                         x.oitems.push_back(Item{(int32_t)u, (int32_t)u + 1, q,
                                                 std::min<int32_t>(q + C, x.out_ptr[u + 1])});
+                        x.oitem_slot.push_back(x.osplit_slotptr.back() + (q - x.out_ptr[u]) / C);
+                    }
+                    x.osplit_slotptr.push_back(x.osplit_slotptr.back() + (odeg(u) + C - 1) / C);
                     ++u;
                 } else {
                     const int64_t u0 = u;
@@ -314,10 +319,12 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
                         ++u;
                     }
                     x.oitems.push_back(Item{(int32_t)u0, (int32_t)u, x.out_ptr[u0], x.out_ptr[u]});
+                    x.oitem_slot.push_back(-1);
                 }
             }
             g->n_oitems = (int64_t)x.oitems.size();
             g->n_osplit = (int64_t)x.osplit.size();
+            g->n_oslots = x.osplit_slotptr.back();
         }
 
         // ---- GEMM tile tables ----
@@ -437,6 +444,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
     add32(&d.big_chunkptr, x.big_chunkptr); add32(&d.chunk_lo, x.chunk_lo); add32(&d.chunk_hi, x.chunk_hi);
     add32(&d.seg_vsegptr, x.seg_vsegptr); add32(&d.big_seg, x.big_seg); add32(&d.osplit, x.osplit);
+    add32(&d.oitem_slot, x.oitem_slot); add32(&d.osplit_slotptr, x.osplit_slotptr);
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});

@@ -13,8 +13,9 @@
 //      the by-relation order; dh = Gp W0^T by the typed GEMM (or zeros).
 //   3. A source-major traversal over the out-edges (sorted by source, then
 //      relation) gathers the dS rows and adds their sum to dh with one store
-//      per source: the per-edge scatter becomes a gather (float atomics only
-//      for pieces of sources with more than kChunkEdges out-edges).
+//      per source: the per-edge scatter becomes a gather.  Pieces of sources
+//      with more than kChunkEdges out-edges leave their sums in slots that one
+//      workgroup per such source adds in slot order (no atomics anywhere).
 //   4. Sbar by the fused aggregate-first kernel's sums-only mode; dW_r and dW0
 //      by outer-product MFMA chunks (K = segments or nodes) and ordered sums.
 #include "rgnn_internal.h"
@@ -30,10 +31,6 @@ __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
-__device__ __forceinline__ void atomic_add4(float *p, float4 v)
-{
-    atomicAdd(p + 0, v.x); atomicAdd(p + 1, v.y); atomicAdd(p + 2, v.z); atomicAdd(p + 3, v.w);
-}
 
 // Gp = G where out > 0, else 0 (ReLU derivative from the forward output).
 __global__ __launch_bounds__(256) void relu_mask_kernel(const float *G, const float *out, float *Gp, int64_t n4)
@@ -55,8 +52,9 @@ struct RStage {
 // out-edge work item (bundles of small sources or pieces of large ones).
 template <int D>
 __global__ __launch_bounds__(256) void rgcn_bwd_src_kernel(int64_t n_items, const Item *items,
+                                                           const int32_t *item_slot,
                                                            const int32_t *out_ptr, const int32_t *out_vseg,
-                                                           const float *dS, float *dh)
+                                                           const float *dS, float *dh, float *part)
 {
     constexpr int G = D / 4, GPB = 256 / G;
     __shared__ RStage stage[GPB];
@@ -66,10 +64,12 @@ __global__ __launch_bounds__(256) void rgcn_bwd_src_kernel(int64_t n_items, cons
     const bool valid = item < n_items;
     int n0 = 0, nn = 0, q0 = 0, nq = 0;
     bool split = false;   // a piece of a source whose out-edges span several items
+    int slot = -1;
     if (valid) {
         const Item x = items[item];
         n0 = x.dst0; nn = x.dst1 - x.dst0; q0 = x.vs0; nq = x.vs1 - x.vs0;
-        split = nn == 1 && out_ptr[n0 + 1] - out_ptr[n0] > nq;
+        slot = item_slot[item];
+        split = slot >= 0;
         for (int e = gl; e < nq; e += G) st.evs[e] = out_vseg[q0 + e];
         auto opos = [&](int jj) {
             const int q = out_ptr[n0 + jj];
@@ -104,9 +104,9 @@ __global__ __launch_bounds__(256) void rgcn_bwd_src_kernel(int64_t n_items, cons
             if (e < nq) {
                 acc = add4(acc, Xd[u]);
                 if (e + 1 == st.optr[j + 1]) {   // the source's last out-edge in this item
-                    float *p = dh + (size_t)(n0 + j) * D + gl * 4;
-                    if (split) atomic_add4(p, acc);
-                    else st4(p, add4(Xh[u], acc));
+                    // a piece of a split source leaves its sum in its slot
+                    if (split) st4(part + (size_t)slot * D + gl * 4, acc);
+                    else st4(dh + (size_t)(n0 + j) * D + gl * 4, add4(Xh[u], acc));
                     acc = zero4();
                     ++j;
                     while (j < nn && st.optr[j + 1] == st.optr[j]) ++j;
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(256) void zero4_kernel(float *p, int64_t n4)
 inline unsigned blocks_for(int64_t n, int per_block) { return (unsigned)((n + per_block - 1) / per_block); }
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
-struct RgcnBwdWs { float *Gp, *dS, *Sb, *partial; };
+struct RgcnBwdWs { float *Gp, *dS, *Sb, *partial, *part; };
 
 size_t rgcn_bwd_layout(const rgnn_graph *g, int D, void *base, RgcnBwdWs *w)
 {
@@ -152,6 +152,7 @@ size_t rgcn_bwd_layout(const rgnn_graph *g, int D, void *base, RgcnBwdWs *w)
     x.dS = take((size_t)std::max<int64_t>(g->V, 1) * D);
     x.Sb = take((size_t)std::max<int64_t>(g->V, 1) * D);
     x.partial = take(nchunks * D * D);
+    x.part = take((size_t)std::max<int64_t>(g->n_oslots, 1) * D);
     if (w) *w = x;
     return off;
 }
@@ -205,9 +206,11 @@ rgnn_status rgcn_backward_d(const rgnn_graph *g, const float *h, const float *W,
         {
             LaunchScope ls("rgcn_bwd_src", s);
             hipLaunchKernelGGL(rgcn_bwd_src_kernel<D>, dim3(blocks_for(g->n_oitems, 256 / G)), dim3(256), 0, s,
-                               g->n_oitems, g->dev.oitems, g->dev.out_ptr, g->dev.out_vseg, w.dS, dh);
+                               g->n_oitems, g->dev.oitems, g->dev.oitem_slot, g->dev.out_ptr, g->dev.out_vseg, w.dS,
+                               dh, w.part);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgcn_bwd_src launch");
+        if ((st = launch_src_merge(g, w.part, dh, D, s)) != RGNN_OK) return st;
     }
     // dW_r = sum over r's segments of Sbar^T Gp_v
     if (g->V > 0) {

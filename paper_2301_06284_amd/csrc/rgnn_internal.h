@@ -70,6 +70,9 @@ struct HostIndex {
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
     std::vector<int32_t> big_seg;      // (dst, rel) segments with > kBigRange virtual segments
     std::vector<int32_t> osplit;       // sources whose out-edges span several out-edge items
+    std::vector<int32_t> oitem_slot;   // per out-edge item: its slot if it is a piece of such a
+                                       // source, else -1 [n_oitems]
+    std::vector<int32_t> osplit_slotptr;   // slots of each of those sources [n_osplit+1]
     std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
     std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
@@ -119,6 +122,7 @@ struct DeviceIndex {
     int32_t *big_split = nullptr, *big_vdst = nullptr;
     int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr, *osplit = nullptr;
+    int32_t *oitem_slot = nullptr, *osplit_slotptr = nullptr;
     float *invcnt_byrel = nullptr;
     Tile *tiles_nodes_outer = nullptr;
     int32_t *nodes_chunkptr = nullptr;
@@ -155,7 +159,7 @@ struct rgnn_graph {
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
-    int64_t n_oitems = 0, n_osplit = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
+    int64_t n_oitems = 0, n_osplit = 0, n_oslots = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
     int64_t n_vpairs = 0, n_tiles_vpairs = 0;
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
@@ -315,6 +319,9 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
                                 const float *X, int ldx, const float *Gm, int ldg, float *partial, int d,
                                 hipStream_t s);
 // dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (d x d each).
+// Pieces of split sources: dh[osplit[i]] += the partial rows of its slots
+// [osplit_slotptr[i], osplit_slotptr[i + 1]) in slot order (d in {32, 64, 128}).
+rgnn_status launch_src_merge(const rgnn_graph *g, const float *part, float *dh, int d, hipStream_t s);
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s);
 // RGAT backward with several heads (2 to 8, d / heads >= 16) in one pass over
