@@ -466,8 +466,9 @@ def test_rgat_backward_multihead(kind, heads):
     assert row_err(gt, dwt) <= TOL
 
 
-@pytest.mark.parametrize("d,heads", [(64, 2), (64, 4), (128, 8)])
-def test_rgat_backward_multihead_mid_size(d, heads):
+@pytest.mark.parametrize("d,heads,kind", [(64, 2, "hub"), (64, 4, "hub"), (128, 8, "hub"), (64, 4, "srchub"),
+                                         (32, 2, "srchub"), (128, 4, "srchub")])
+def test_rgat_backward_multihead_mid_size(d, heads, kind):
     """Several heads on a 200k-edge graph with hubs (split destinations and
     sources with many out-edges), every gradient in full, at the standard
     cancellation floor.
@@ -479,10 +480,13 @@ def test_rgat_backward_multihead_mid_size(d, heads):
     10^5-edge hub (dh norm ~1e-5 of the median) and whose one in-edge forms a
     one-edge softmax, whose Jacobian is exactly zero: with alpha normalised by
     the forward's denominator instead, that zero came out as ~1e-7 |dalpha|,
-    a 3e-4 row error."""
-    g = workloads.tiny_graph(46, N=20000, E=200000, R=12, T=2, kind="hub")
+    a 3e-4 row error.
+    With a source hub (half the edges leave node 0: pairs of ~8 000 out-edges,
+    cut into 64-edge pieces over several workgroup chunks at d <= 64, and a
+    source split over ~1 500 out-edge items) the same checks hold."""
+    g = workloads.tiny_graph(46, N=20000, E=200000, R=12, T=2, kind=kind)
     t = workloads.tiny_tensors(46, g, d, d, heads=heads, att_var=1.0)
-    print(f"rgat backward d={d} heads={heads} mid size", flush=True)
+    print(f"rgat backward d={d} heads={heads} {kind} mid size", flush=True)
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(heads=heads)
     run.close()
@@ -511,6 +515,30 @@ def test_rgat_backward_mid_size_one_head(plan):
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
     assert row_err(gs, dws) <= TOL
     assert row_err(gt, dwt) <= TOL
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_backward_mid_size_source_hub(d):
+    """One-head RGAT and RGCN backward on a 200k-edge graph whose node 0 sends
+    half the edges: its out-edges span ~1 500 work items, whose sums are added
+    to its row in slot order."""
+    g = workloads.tiny_graph(47, N=20000, E=200000, R=12, T=2, kind="srchub")
+    t = workloads.tiny_tensors(47, g, d, d, heads=1, att_var=1.0)
+    print(f"rgat/rgcn backward d={d} source hub mid size", flush=True)
+    run = Runner(g, t)
+    gh, gW, gs, gt = run.rgat_backward(heads=1)
+    rh, rW, rW0 = run.rgcn_backward(W0=True, relu=False)
+    run.close()
+    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, d), dW.reshape(-1, d)) <= TOL
+    assert row_err(gs, dws) <= TOL
+    assert row_err(gt, dwt) <= TOL
+    eh, eW, eW0 = oracle.rgcn_backward(g, t["h"], t["W"], t["W0"], t["grad_out"], relu=False)
+    assert row_err(rh, eh) <= TOL
+    assert row_err(rW.reshape(-1, d), eW.reshape(-1, d)) <= TOL
+    assert row_err(rW0, eW0) <= TOL
 
 
 @pytest.mark.parametrize("kind", KINDS)
