@@ -753,6 +753,101 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
     }
 }
 
+// The same product at D = 128 with one workgroup per chunk computing all of
+// the 128 x 128 partial (the 64 x 64 tiling above reads every row twice):
+// 32-row steps staged in LDS, each wave 32 rows of the product (two row
+// blocks against all eight column blocks: ten LDS reads per sixteen MFMAs).
+template <bool YS, bool GATHER, bool GA>
+__global__ __launch_bounds__(256) void outer_gemm128_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
+                                                            const float *Sa, int lda,
+                                                            const float *Gm, int ldb, const float *h,
+                                                            const float *ysum, float *partial,
+                                                            float *yvec)
+{
+    constexpr int D = 128, KB = 32, P = D + 4;
+    constexpr int SL = KB * (D / 4) / 256;   // float4 slots of each operand per thread and step
+    __shared__ float As[KB * P];
+    __shared__ float Bs[KB * P];
+    __shared__ float4 yred[YS ? 256 : 1];
+    const Tile t = chunks[blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int li = lane & 15, q = lane >> 4;
+    const int c4 = (tid % (D / 4)) * 4;     // this thread's columns in every slot
+    const int rbase = tid / (D / 4);         // its first row of a step (rows rbase + 8 sl)
+    floatx4 acc[2][8];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float4 yacc = zero4();
+    auto row_of = [&](int k0, int sl) { return t.row0 + min(k0 + rbase + 8 * sl, t.rows - 1); };
+    int vi[SL], vn[SL];
+    float4 ra[SL], rb4[SL], rh[SL];
+    float ry[SL];
+    auto load_idx = [&](int k0, int (&v)[SL]) {
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) v[sl] = (GATHER || GA) ? vsegdst_byrel[row_of(k0, sl)] : row_of(k0, sl);
+    };
+    auto load_rows = [&](int k0, const int (&v)[SL]) {
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+            const int row = row_of(k0, sl);
+            ra[sl] = ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + c4);
+            rb4[sl] = ld4(Gm + (size_t)(GATHER ? v[sl] : row) * ldb + c4);
+            if (YS) {
+                rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
+                ry[sl] = ysum[row];
+            }
+        }
+    };
+    load_idx(0, vi);
+    load_rows(0, vi);
+    load_idx(KB, vn);
+    for (int k0 = 0; k0 < t.rows; k0 += KB) {
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+            const int rr = rbase + 8 * sl;
+            const bool ok = k0 + rr < t.rows;
+            *reinterpret_cast<float4 *>(&As[rr * P + c4]) = ok ? ra[sl] : zero4();
+            *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = ok ? rb4[sl] : zero4();
+            if (YS && ok) yacc = lin4(yacc, 1.f, rh[sl], ry[sl]);
+        }
+        __syncthreads();
+        load_rows(k0 + KB, vn);
+        load_idx(k0 + 2 * KB, vn);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll 2
+        for (int kk = 0; kk < KB; kk += 4) {
+            const float a0 = As[(kk + q) * P + w * 32 + li];
+            const float a1 = As[(kk + q) * P + w * 32 + 16 + li];
+#pragma unroll
+            for (int cb = 0; cb < 8; ++cb) {
+                const float b = Bs[(kk + q) * P + cb * 16 + li];
+                acc[0][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b, acc[0][cb], 0, 0, 0);
+                acc[1][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b, acc[1][cb], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    float *out = partial + (size_t)blockIdx.x * D * D;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                out[(size_t)(w * 32 + rb * 16 + q * 4 + v) * D + cb * 16 + li] = acc[rb][cb][v];
+    if (YS) {
+        yred[tid] = yacc;
+        __syncthreads();
+        if (tid < D / 4) {
+            float4 s = zero4();
+            for (int i = tid; i < 256; i += D / 4) s = add4(s, yred[i]);
+            st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
+        }
+    }
+}
+
 // Per relation r: pws = sum of r's pair-tile vectors, pwt = sum of r's
 // segment-chunk vectors, both in a fixed order.
 template <int D>
@@ -905,19 +1000,35 @@ template <int D>
 void outer_chunks_d(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x, const float *X,
                     int ldx, const float *Gm, int ldg, float *partial, hipStream_t s)
 {
-    const dim3 grid((unsigned)nchunks, outer_tiles(D));
-    if (gather && gather_x == 2)   // only the first operand gathered
-        hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, true>), grid, dim3(256), 0, s,
-                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
-    else if (gather && gather_x)
-        hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, true>), grid, dim3(256), 0, s,
-                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
-    else if (gather)
-        hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, false>), grid, dim3(256), 0, s,
-                           chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
-    else
-        hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, false>), grid, dim3(256), 0, s,
-                           chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    if constexpr (D == 128) {
+        const dim3 grid((unsigned)nchunks);
+        if (gather && gather_x == 2)
+            hipLaunchKernelGGL((outer_gemm128_kernel<false, false, true>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else if (gather && gather_x)
+            hipLaunchKernelGGL((outer_gemm128_kernel<false, true, true>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else if (gather)
+            hipLaunchKernelGGL((outer_gemm128_kernel<false, true, false>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else
+            hipLaunchKernelGGL((outer_gemm128_kernel<false, false, false>), grid, dim3(256), 0, s,
+                               chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    } else {
+        const dim3 grid((unsigned)nchunks, outer_tiles(D));
+        if (gather && gather_x == 2)   // only the first operand gathered
+            hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, true>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else if (gather && gather_x)
+            hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, true>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else if (gather)
+            hipLaunchKernelGGL((outer_gemm_kernel<D, false, true, false>), grid, dim3(256), 0, s,
+                               chunks, gather, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+        else
+            hipLaunchKernelGGL((outer_gemm_kernel<D, false, false, false>), grid, dim3(256), 0, s,
+                               chunks, nullptr, X, ldx, Gm, ldg, nullptr, nullptr, partial, nullptr);
+    }
 }
 
 rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32_t *gather, int gather_x,
@@ -1149,10 +1260,16 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "pair_gemv launch");
     if (g->n_tiles_outer) {
         LaunchScope ls("outer_gemm", s);
-        hipLaunchKernelGGL((outer_gemm_kernel<D, true, true, false>), dim3((unsigned)g->n_tiles_outer, outer_tiles(D)),
-                           dim3(256), 0, s,
-                           g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, D, Gm, D, h, w.ysum,
-                           w.partial, w.yvec);
+        if constexpr (D == 128)
+            hipLaunchKernelGGL((outer_gemm128_kernel<true, true, false>), dim3((unsigned)g->n_tiles_outer),
+                               dim3(256), 0, s,
+                               g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, D, Gm, D, h, w.ysum,
+                               w.partial, w.yvec);
+        else
+            hipLaunchKernelGGL((outer_gemm_kernel<D, true, true, false>), dim3((unsigned)g->n_tiles_outer, outer_tiles(D)),
+                               dim3(256), 0, s,
+                               g->dev.tiles_outer, g->dev.vsegdst_byrel, w.Sa, D, Gm, D, h, w.ysum,
+                               w.partial, w.yvec);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "outer_gemm launch");
     {
