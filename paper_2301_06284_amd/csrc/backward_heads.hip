@@ -652,7 +652,7 @@ __global__ __launch_bounds__(256) void mh_pair_fused_kernel(PF k)
         __syncthreads();
         // dHp rows of this wave's 16 virtual pairs (transposed block: lane
         // (li, q) ends with row li, columns 4q .. 4q + 3 of each column block)
-        {
+        if (wave * 16 < KB) {
             const int p0 = wave * 16;
             floatx4 o4[NCB];
 #pragma unroll
@@ -670,7 +670,7 @@ __global__ __launch_bounds__(256) void mh_pair_fused_kernel(PF k)
                 }
             }
             const int row = k0 + p0 + li;
-            if (p0 < KB && row < t.rows) {
+            if (row < t.rows) {
                 float *dst = k.dHp + (size_t)k.vpair_smpos[t.row0 + row] * D + q * 4;
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
