@@ -127,6 +127,15 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
     // only from its load to its MFMAs.
     constexpr int PF = K * NC <= 64 * 64 ? 2 : 1;
     float4 ab[MB][KC];
+    // SR: the results leave through a wave-private LDS tile, 32 columns at a
+    // time, so that each store instruction writes whole 128-byte lines (eight
+    // rows of 32 columns) instead of sixteen half lines; residual and
+    // accumulated operands are read in that row layout too.  Not for the
+    // 128-deep shapes, whose MFMAs are the limit (the tile made them 1-2 %
+    // slower; the 64-deep ones 8-16 % faster).
+    constexpr bool SR = NCB % 2 == 0 && K != 128;
+    constexpr int TP = 36;   // padded tile row (conflict-free b128 writes and reads)
+    __shared__ float Ysm[SR ? 4 * 16 * TP : 1];
     auto load_block = [&](int i) {
         const float *p = a.X + (int64_t)xr[i] * a.ldx + q * 4;
 #pragma unroll
@@ -163,8 +172,33 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
         // (a) epilogue operands of this block
         float sc = 1.f;
         float4 ex[NCB];
+        int64_t y2[2];      // SR: the block rows 8j + lane / 8 this lane stores
+        bool ok2[2];
         if (EP & EP_SCALE) sc = a.row_scale[y];
-        if (EP & (EP_RESID | EP_ACC)) {
+        if constexpr (SR) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int r2 = 8 * j + (lane >> 3);
+                y2[j] = __shfl(yr[i], r2);
+                ok2[j] = rb * 16 + r2 < tile.rows;
+            }
+            if (EP & (EP_RESID | EP_ACC)) {   // ex[2h + j]: columns 32h + 4 (lane % 8) of row y2[j]
+#pragma unroll
+                for (int hj = 0; hj < NCB; ++hj) {
+                    const int j = hj % 2, col = (hj / 2) * 32 + (lane & 7) * 4;
+                    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+                    if (EP & EP_RESID) {
+                        const float4 t = *reinterpret_cast<const float4 *>(a.residual + y2[j] * a.ld_res + col);
+                        x = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
+                    }
+                    if (EP & EP_ACC) {
+                        const float4 t = *reinterpret_cast<const float4 *>(a.Y + y2[j] * a.ldy + col);
+                        x = make_float4(x.x + t.x, x.y + t.y, x.z + t.z, x.w + t.w);
+                    }
+                    ex[hj] = x;
+                }
+            }
+        } else if (EP & (EP_RESID | EP_ACC)) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -232,6 +266,30 @@ __global__ __launch_bounds__(256) void typed_gemm_kernel(GemmK a)
                 if (EP & EP_DOT) {
                     const float4 d = *reinterpret_cast<const float4 *>(&dvs[cb * 16 + q * 4]);
                     dpart[cb / CBH] += v.x * d.x + v.y * d.y + v.z * d.z + v.w * d.w;
+                }
+                if constexpr (SR) {
+                    float *ts = Ysm + wave * 16 * TP;
+                    *reinterpret_cast<float4 *>(&ts[li * TP + (cb & 1) * 16 + q * 4]) = v;
+                    if (cb & 1) {   // a 32-column half is complete: out in the row layout
+                        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                        for (int jr = 0; jr < 2; ++jr) {
+                            float4 w = *reinterpret_cast<const float4 *>(&ts[(8 * jr + (lane >> 3)) * TP + (lane & 7) * 4]);
+                            if (!ok2[jr]) continue;
+                            const int col = (cb - 1) * 16 + (lane & 7) * 4;
+                            if (EP & (EP_RESID | EP_ACC)) {
+                                const float4 x = ex[(cb / 2) * 2 + jr];
+                                w = make_float4(w.x + x.x, w.y + x.y, w.z + x.z, w.w + x.w);
+                            }
+                            if (EP & EP_RELU) w = make_float4(fmaxf(w.x, 0.f), fmaxf(w.y, 0.f), fmaxf(w.z, 0.f), fmaxf(w.w, 0.f));
+                            if ((EP & EP_SPLIT) && col >= a.split)
+                                *reinterpret_cast<float4 *>(a.Y2 + y2[jr] * a.ldy2 + (col - a.split)) = w;
+                            else
+                                *reinterpret_cast<float4 *>(a.Y + y2[jr] * a.ldy + col) = w;
+                        }
+                        __builtin_amdgcn_wave_barrier();
+                    }
+                    continue;
                 }
                 if (!valid) continue;
                 if (EP & (EP_RESID | EP_ACC)) v = make_float4(v.x + ex[cb].x, v.y + ex[cb].y, v.z + ex[cb].z, v.w + ex[cb].w);
