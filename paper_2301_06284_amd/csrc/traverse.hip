@@ -363,29 +363,36 @@ __global__ __launch_bounds__(256) void rgcn_tf_kernel(TK k)
 
 // The same with the reordered vectors of every relation staged in LDS (when
 // they fit) and each group taking SB batches of S consecutive segments: the
-// next batch's destination rows are in flight while the current batch's dot
-// products are formed, and its indices two batches ahead.
+// workgroup's (destination, relation) pairs are staged in LDS with coalesced
+// loads next to the vectors, and the next batch's destination rows are in
+// flight while the current batch's dot products are formed.
 constexpr int kSegBatches = 4;
 
 template <int D, int H>
 __global__ __launch_bounds__(256) void seg_attn_lds_kernel(TK k, int64_t V, const int32_t *vseg_dst, int R)
 {
     constexpr int G = D / 4, GPB = 256 / G;
-    constexpr int S = kSegPerGroup, SB = kSegBatches;
+    constexpr int S = kSegPerGroup, SB = kSegBatches, SW = GPB * S * SB;
     extern __shared__ float4 wts[];   // [R, H, D / 4]
-    const int gl = threadIdx.x % G;
+    __shared__ int2 sidx[SW];         // (destination, relation) of the workgroup's segments
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    const int64_t wbase = (int64_t)blockIdx.x * SW;
     for (int i = threadIdx.x; i < R * H * G; i += 256) wts[i] = ld4(k.wtp + (size_t)i * 4);
+    for (int i = threadIdx.x; i < SW; i += 256) {
+        const int64_t vs = wbase + i < V ? wbase + i : V - 1;
+        sidx[i] = make_int2(vseg_dst[vs], k.vseg_rel[vs]);
+    }
     __syncthreads();
-    const int64_t base = ((int64_t)blockIdx.x * GPB + threadIdx.x / G) * (S * SB);
+    const int64_t base = wbase + (int64_t)gi * (S * SB);
     if (base >= V) return;
     int v[2][S], r[2][S];
     float4 hv[2][S];
     auto idx = [&](int slot, int b) {
 #pragma unroll
         for (int i = 0; i < S; ++i) {
-            const int64_t vs0 = base + b * S + i, vs = vs0 < V ? vs0 : V - 1;
-            v[slot][i] = vseg_dst[vs];
-            r[slot][i] = k.vseg_rel[vs];
+            const int2 x = sidx[gi * S * SB + b * S + i];
+            v[slot][i] = x.x;
+            r[slot][i] = x.y;
         }
     };
     auto rows = [&](int slot) {
