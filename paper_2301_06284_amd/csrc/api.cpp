@@ -524,13 +524,16 @@ rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *
         FusedArgs fa;
         fa.g = g; fa.h = h; fa.W = W; fa.wsp = w.wsp; fa.vatt = w.vatt; fa.slope = neg_slope;
         fa.d_in = d_in; fa.d_out = d_out; fa.softmax = 1; fa.T = w.T; fa.vstat = w.vstat;
+        if (!per_seg) {   // destinations with one segment are finished in the fused kernel
+            fa.out = out; fa.saved = saved;
+        }
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
         if (per_seg) {
             TravArgs ta;
             ta.g = g; ta.vstat = w.vstat; ta.vscale = w.vscale; ta.saved = saved;   // [U_dst, 2]
             if ((st = launch_seg_softmax_scale(ta, s)) != RGNN_OK) return st;
             if ((st = launch_vseg_reduce(g, w.T, w.vscale, d_out, out, 0, 0, s)) != RGNN_OK) return st;
-        } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, w.vscale, s)) != RGNN_OK) {
+        } else if ((st = launch_softmax_reduce(g, w.vstat, w.T, d_out, out, saved, w.vscale, 1, s)) != RGNN_OK) {
             return st;
         }
     }

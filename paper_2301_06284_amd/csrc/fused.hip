@@ -53,6 +53,7 @@ struct FK {
     const float *h, *W, *wsp, *vatt;
     float slope;
     float *T, *vstat;
+    float *out, *saved;          // softmax: rows of destinations with one virtual segment
     const int32_t *pos;          // sums only: output row of each virtual segment
     float *S;
 };
@@ -150,6 +151,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
         int lso[2];      // first source index of the row in ssrc
         int fp[2];       // position of the row in the fused order
         float va[2];     // destination attention term
+        int sid[2];      // output row: vs (a T row), or ~v when the row finishes destination v
         int nmax;        // edge count of the block's longest segment
     };
     auto setup = [&](int rb, Blk &b) {
@@ -161,10 +163,11 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
             b.fr[h2] = srow[b.valid[h2] ? row : rb * 16];
             b.lso[h2] = (int)(b.fr[h2].e0 - te0);
             b.va[h2] = MODE == kModeSoftmax ? k.vatt[b.fr[h2].vs] : 0.f;
+            b.sid[h2] = MODE == kModeSoftmax && k.out && b.fr[h2].cnt < 0 ? b.fr[h2].cnt : b.fr[h2].vs;
         }
-        float nm = gmax<32>(fmaxf((float)b.fr[0].ne, (float)b.fr[1].ne));
-        nm = fmaxf(nm, __shfl_xor(nm, 32));
-        b.nmax = __builtin_amdgcn_readfirstlane((int)nm);
+        // rows are sorted by edge count inside a relation (largest first), so
+        // the block's first row is its longest
+        b.nmax = __builtin_amdgcn_readfirstlane(srow[rb * 16].ne);
     };
     // batches of KU edges of both rows (indices from LDS); a row already
     // finished issues no gathers (most segments are one or two edges long)
@@ -268,7 +271,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 if (!valid[h2]) continue;
-                const float sc = 1.f / (float)fr[h2].cnt;
+                const float sc = 1.f / (float)(fr[h2].cnt < 0 ? fr[h2].ne : fr[h2].cnt);
                 float *o = k.S + (size_t)k.pos[fr[h2].vs] * DI + gp * 4;
 #pragma unroll
                 for (int c = 0; c < CH; ++c) {
@@ -279,22 +282,35 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
             cur = nxt;
             continue;
         }
-        // row sums -> MFMA operand layout by lane permutes: lane (li, q) takes
-        // features 16c + 4q .. +3 of row li, held by lane 8 (li % 8) + 4 (c % 2) + q
-        // in its chunk c / 2 of row set li / 8
+        // A destination with one virtual segment is finished here: its softmax
+        // denominator is the segment's own sum, so the row sum is divided by it
+        // before the transform and the product is the output row (saved gets
+        // (m, s)); every other segment leaves T and (m, s) for the reduction.
+        bool fin[2];
+        float *rowp[2];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
-            if (MODE == kModeMean) {
-                const float sc = 1.f / (float)fr[h2].cnt;
+            fin[h2] = MODE == kModeSoftmax && cur.sid[h2] < 0;
+            rowp[h2] = (fin[h2] ? k.out + (size_t)~cur.sid[h2] * DO : k.T + (size_t)cur.sid[h2] * DO) + gp * 4;
+            if (MODE != kModeSum) {
+                const float sc = MODE == kModeMean ? 1.f / (float)(fr[h2].cnt < 0 ? fr[h2].ne : fr[h2].cnt)
+                                                   : (fin[h2] ? 1.f / s[h2] : 1.f);
 #pragma unroll
                 for (int c = 0; c < CH; ++c) {
                     float4 &a = acc[h2][c];
                     a = make_float4(a.x * sc, a.y * sc, a.z * sc, a.w * sc);
                 }
             }
-            if (MODE == kModeSoftmax && valid[h2] && gp == 0)
-                *reinterpret_cast<float2 *>(k.vstat + (size_t)cur.fp[h2] * 2) = make_float2(m[h2], s[h2]);
+            if (MODE == kModeSoftmax && valid[h2] && gp == 0) {
+                if (!fin[h2])
+                    *reinterpret_cast<float2 *>(k.vstat + (size_t)cur.fp[h2] * 2) = make_float2(m[h2], s[h2]);
+                else if (k.saved)
+                    *reinterpret_cast<float2 *>(k.saved + (size_t)~cur.sid[h2] * 2) = make_float2(m[h2], s[h2]);
+            }
         }
+        // row sums -> MFMA operand layout by lane permutes: lane (li, q) takes
+        // features 16c + 4q .. +3 of row li, held by lane 8 (li % 8) + 4 (c % 2) + q
+        // in its chunk c / 2 of row set li / 8
         const bool hi = li >= 8;
         float4 sb[KC];
 #pragma unroll
@@ -347,7 +363,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
                         v[t] = gp >= 4 ? b : a;
                     }
                     if (valid[h2])
-                        st4(k.T + (size_t)fr[h2].vs * DO + (c0 / 2 + cc) * 32 + gp * 4,
+                        st4(rowp[h2] + (c0 / 2 + cc) * 32,
                             make_float4(v[0], v[1], v[2], v[3]));
                 }
             }
@@ -404,6 +420,7 @@ rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s)
     k.ntiles = g->n_tiles_fused; k.nedges = g->E; k.src = g->dev.fused_src;
     k.h = a.h; k.W = a.W; k.wsp = a.wsp; k.vatt = a.vatt; k.slope = a.slope;
     k.T = a.T; k.vstat = a.vstat; k.S = a.S; k.pos = g->dev.vseg_pos;
+    k.out = a.out; k.saved = a.saved;
     if (a.softmax && (!a.wsp || !a.vatt || !a.vstat))
         return fail(RGNN_EINVAL, "fused softmax aggregation needs wsp, vatt and vstat");
     if (a.S && a.softmax) return fail(RGNN_EINVAL, "segment means are for the mean aggregation");

@@ -175,7 +175,9 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             for (int64_t i = 0; i < g->V; ++i) {
                 const int32_t vs = fperm[i];
                 const int32_t b = x.vseg_ptr[vs], n = x.vseg_ptr[vs + 1] - b;
-                x.fused_rows[i] = FusedRow{vs, fpos, n, x.vseg_cnt[vs]};
+                const int32_t v = x.vseg_dst[vs];
+                const bool only = x.dst_vsegptr[(size_t)v + 1] - x.dst_vsegptr[v] == 1;
+                x.fused_rows[i] = FusedRow{vs, fpos, n, only ? ~v : x.vseg_cnt[vs]};
                 x.vseg_fpos[vs] = (int32_t)i;
                 for (int32_t j = 0; j < n; ++j) x.fused_src[(size_t)fpos + j] = x.in_src[(size_t)b + j];
                 fpos += n;

@@ -264,7 +264,8 @@ __device__ __forceinline__ void softmax_reduce_big(int v, const int32_t *dst_vse
 // exp-weighted transformed row T_i relative to m_i; (m_i, s_i) stored at the
 // segment's fused position fpos[i]):
 //   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
-// and saved[v] = (M, Z) ((0, 0) without in-edges).  Blocks [0, nbig) take the
+// and saved[v] = (M, Z) ((0, 0) without in-edges); with skip1, destinations
+// with a single segment are skipped (finished by the fused kernel).  Blocks [0, nbig) take the
 // destinations of big_vdst; the others a group of D/4 lanes per destination,
 // the statistics taken over the group's lanes (fixed butterfly), the rows
 // summed in segment order.
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t 
                                                              const int32_t *dst_vsegptr,
                                                              const int32_t *fpos, const float *vstat,
                                                              const float *T, float *out, float *saved,
-                                                             float *scale)
+                                                             float *scale, int skip1)
 {
     if ((int64_t)blockIdx.x < nbig) {
         softmax_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, fpos, vstat, T, out, saved, scale);
@@ -285,7 +286,7 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t 
     const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
     if (v >= N) return;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    if (e - b > kBigRange) return;
+    if (e - b > kBigRange || (skip1 && e - b == 1)) return;
     // rows in batches of four, two batches in flight; the first goes out before
     // the statistics are gathered (the rows do not depend on them)
     float4 ta[4], tb[4];
@@ -688,7 +689,7 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
 }
 
 rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
-                                  float *out, float *saved, float *scale, hipStream_t s)
+                                  float *out, float *saved, float *scale, int skip1, hipStream_t s)
 {
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 32, 64 or 128");
@@ -699,7 +700,7 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
         LaunchScope ls("softmax_reduce", s);
 #define SR(D) hipLaunchKernelGGL((softmax_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
                                  g->dev.big_vdst, g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, \
-                                 saved, scale)
+                                 saved, scale, skip1)
         if (d == 32) SR(32);
         else if (d == 64) SR(64);
         else SR(128);

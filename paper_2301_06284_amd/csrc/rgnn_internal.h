@@ -42,7 +42,9 @@ struct Tile {          // one typed-GEMM tile: rows [row0, row0 + rows) of type 
 struct FusedRow {      // one virtual segment in the fused aggregate-first order
     int32_t vs;           // virtual segment id
     int32_t e0, ne;       // its in-edges' sources at [e0, e0 + ne) of the fused source list
-    int32_t cnt;          // edge count of its whole (dst, rel) segment
+    int32_t cnt;          // edge count of its whole (dst, rel) segment; ~v (negative) when the
+                          // segment is the only virtual segment of its destination v (then
+                          // the whole segment is this one: its count is ne)
 };
 
 struct Item {          // one traversal work item
@@ -287,8 +289,10 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
 // (fused order) and the segments' transformed rows summed: out_v = sum_i
 // exp(m_i - M_v) / Z_v * T_i; saved[v] = (M_v, Z_v) when saved is not NULL.
 // scale [V]: scratch (the weights of destinations with many segments).
+// skip1: destinations with a single virtual segment are left alone (the fused
+// kernel wrote their rows and statistics).
 rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const float *T, int d,
-                                  float *out, float *saved, float *scale, hipStream_t s);
+                                  float *out, float *saved, float *scale, int skip1, hipStream_t s);
 
 // Fused aggregate-first gather + segment sum + transform: per virtual segment
 // T[vs] = S_vs W_r with S_vs the segment's mean of h_u (softmax == 0) or its
@@ -305,6 +309,9 @@ struct FusedArgs {
     int softmax = 0;
     float *T = nullptr;           // [V, d_out]
     float *vstat = nullptr;       // [V, 2] (softmax), indexed by fused position
+    // softmax, optional: a destination with a single virtual segment gets its
+    // output row [N, d_out] and (max, sum) [N, 2] here, not in T and vstat
+    float *out = nullptr, *saved = nullptr;
     // S given (softmax == 0): write the segment means S_vs = (1/c) sum h_u
     // themselves, at the segment's by-relation position [V, d_in], no transform
     float *S = nullptr;
