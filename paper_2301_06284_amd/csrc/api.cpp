@@ -563,14 +563,27 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     HgtWs w;
     hgt_layout(g, d, heads, ws, &w);
     hipStream_t s = (hipStream_t)stream;
-    // K | V | Q of every node by node-typed GEMMs (segment MM over node types):
-    // one GEMM with the three weights side by side at d = 64, one per
+    // The segment queries QP = Q_t Wqp[r] need Q only through that product.
+    // When every relation's destinations share one node type t(r) (typed
+    // relations), Wq[t(r)] folds into the per-relation weight, QP = h_t
+    // (Wq[t(r)] Wqp[r]), and Q is never formed; otherwise (and when the
+    // traversal forms the queries itself from Q at d = 128) Q is projected
+    // with K and V.
+    const bool fused_query = d == 128 && hgt_fused_query_fits(g->R, d, heads);
+    const bool fold_q = !fused_query && g->rel_dst_typed;
+    // K | V (| Q) of every node by node-typed GEMMs (segment MM over node
+    // types): one GEMM with the weights side by side at d = 64, one per
     // projection otherwise (a 3d-wide weight tile would not fit LDS at 128)
     GemmArgs ga;
     ga.X = h; ga.ldx = d; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
     ga.K = d;
     ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
-    if (d == 64) {
+    if (d == 64 && fold_q) {
+        ga.W[0] = Wk; ga.W[1] = Wv; ga.nparts = 2;
+        ga.Nc = 2 * d;
+        ga.Y = w.KV; ga.ldy = 2 * d;
+        if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
+    } else if (d == 64) {
         ga.W[0] = Wk; ga.W[1] = Wv; ga.W[2] = Wq; ga.nparts = 3;
         ga.Nc = 3 * d;
         ga.Y = w.KV; ga.ldy = 2 * d;
@@ -581,14 +594,14 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         const float *Wp[3] = {Wk, Wv, Wq};
         float *Yp[3] = {w.KV, w.KV + d, w.Q};
         const int64_t ld[3] = {2 * d, 2 * d, d};
-        for (int p = 0; p < 3; ++p) {
+        for (int p = 0; p < (fold_q ? 2 : 3); ++p) {
             ga.W[0] = Wp[p]; ga.Y = Yp[p]; ga.ldy = ld[p];
             if ((st = launch_typed_gemm(ga, s)) != RGNN_OK) return st;
         }
     }
     HgtArgs ha;
     ha.g = g; ha.KV = w.KV; ha.Wmsg = Wmsg;
-    if (d == 128 && hgt_fused_query_fits(g->R, d, heads)) {
+    if (fused_query) {
         // the traversal forms each segment's reordered query Q_t (mu scale Watt[r]^T)
         // from LDS-resident blocks at the segment's first edge.  Measured on the
         // 1.9M-node graph this wins only at d = 128 (the 128-wide segment-query
@@ -596,13 +609,21 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         // vector-matrix product in the traversal costs more than the GEMM.
         ha.QP = nullptr; ha.Q = w.Q; ha.Watt = Watt; ha.mu = mu; ha.scale = att_scale;
     } else {
-        // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r] (segment MM over relations)
-        if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) return st;
+        // reordered query of every (dst, rel) segment: QP = Q_t Wqp[r], or
+        // h_t (Wq[t(r)] Wqp[r]) with the projection folded in (segment MM over
+        // relations; Wqp[r] alone is block-diagonal over the heads)
+        if (fold_q) {
+            if ((st = launch_hgt_qp_fold(Wq, Watt, mu, att_scale, g->dev.rel_dsttype, g->R, d, heads, w.Wqp, s)) !=
+                RGNN_OK)
+                return st;
+        } else if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, d, heads, w.Wqp, s)) != RGNN_OK) {
+            return st;
+        }
         GemmArgs gq;
-        gq.X = w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
+        gq.X = fold_q ? h : w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
         gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
         gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
-        gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = heads;
+        gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = fold_q ? 1 : heads;
         if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
         ha.QP = w.QP;
     }

@@ -118,6 +118,19 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         x.ntype_ptr.assign((size_t)T + 1, 0);
         for (int64_t n = 0; n < N; ++n) x.ntype_ptr[(size_t)ntype[n] + 1]++;
         for (int32_t t = 0; t < T; ++t) x.ntype_ptr[t + 1] += x.ntype_ptr[t];
+        // the destination node type of every relation (-1 when it has several;
+        // a relation without edges takes type 0)
+        x.rel_dsttype.assign((size_t)R, -2);
+        for (int64_t e = 0; e < E; ++e) {
+            int32_t &t = x.rel_dsttype[rel[e]];
+            const int32_t te = ntype[dst[e]];
+            t = t == -2 ? te : (t == te ? t : -1);
+        }
+        g->rel_dst_typed = true;
+        for (int32_t r = 0; r < R; ++r) {
+            if (x.rel_dsttype[r] == -2) x.rel_dsttype[r] = 0;
+            if (x.rel_dsttype[r] < 0) g->rel_dst_typed = false;
+        }
 
         // ---- virtual segments: segments cut into pieces of at most C edges ----
         x.vseg_ptr.clear(); x.vseg_rel.clear(); x.vseg_dst.clear(); x.vseg_cnt.clear(); x.vseg_seg.clear();
@@ -435,7 +448,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.in_eid, x.in_eid); add32(&d.seg_ptr, x.seg_ptr); add32(&d.seg_rel, x.seg_rel);
     add32(&d.dst_segptr, x.dst_segptr); add32(&d.uniq_src, x.uniq_src);
     add32(&d.uniq_rel_ptr, x.uniq_rel_ptr); add32(&d.e2u, x.e2u);
-    add32(&d.ntype_perm, x.ntype_perm); add32(&d.ntype_ptr, x.ntype_ptr);
+    add32(&d.ntype_perm, x.ntype_perm); add32(&d.ntype_ptr, x.ntype_ptr); add32(&d.rel_dsttype, x.rel_dsttype);
     add32(&d.vseg_ptr, x.vseg_ptr); add32(&d.vseg_rel, x.vseg_rel); add32(&d.vseg_dst, x.vseg_dst);
     add32(&d.vseg_cnt, x.vseg_cnt); add32(&d.dst_vsegptr, x.dst_vsegptr);
     add32(&d.vseg_byrel, x.vseg_byrel); add32(&d.rel_vsegptr, x.rel_vsegptr);

@@ -271,6 +271,23 @@ __global__ void hgt_qp_weights_kernel(const float *Watt, const float *mu, float 
     Wqp[idx] = v;
 }
 
+// Wc[r][j][n] = sum_k Wq[t][j][k] Wqp[r][k][n], t = rel_dsttype[r]: only the
+// k of n's head block contribute (Wqp[r] is block-diagonal), so each entry is
+// a dk-term product of a Wq row piece with a row of Watt[r, i].
+__global__ void hgt_qp_fold_kernel(const float *Wq, const float *Watt, const float *mu, float scale,
+                                   const int32_t *rel_dsttype, int R, int D, int heads, float *Wc)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)R * D * D) return;
+    const int r = (int)(idx / (D * D)), j = (int)(idx / D % D), n = (int)(idx % D);
+    const int dk = D / heads, i = n / dk;
+    const float *wq = Wq + ((size_t)rel_dsttype[r] * D + j) * D + i * dk;
+    const float *wa = Watt + (((size_t)r * heads + i) * dk + (n - i * dk)) * dk;
+    float acc = 0.f;
+    for (int k = 0; k < dk; ++k) acc = fmaf(wq[k], wa[k], acc);
+    Wc[idx] = mu[r] * scale * acc;
+}
+
 template <int D, int H>
 hipError_t launch_hgt_shape(const HK &k, int64_t n_items, int R, hipStream_t s)
 {
@@ -353,6 +370,19 @@ rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scal
                        R, d, heads, Wqp);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt_qp_weights launch");
+}
+
+rgnn_status launch_hgt_qp_fold(const float *Wq, const float *Watt, const float *mu, float scale,
+                               const int32_t *rel_dsttype, int R, int d, int heads, float *Wc, hipStream_t s)
+{
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "HGT supports d = 32, 64, 128");
+    const int64_t n = (int64_t)R * d * d;
+    if (n == 0) return RGNN_OK;
+    LaunchScope ls("hgt_qp_weights", s);
+    hipLaunchKernelGGL(hgt_qp_fold_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, Wq, Watt, mu, scale,
+                       rel_dsttype, R, d, heads, Wc);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "hgt_qp_fold launch");
 }
 
 }  // namespace rgnn

@@ -406,7 +406,7 @@ inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct HgtBwdWs {
     float *KV, *Q, *Wqp, *QP, *agg, *partial, *saved, *dagg, *Wmt, *dP, *Sal, *Aac, *Bac, *sfin,
-        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2, *rec, *Wc;
+        *spart, *dQP, *Tq, *dQ, *dKV, *chunks, *OT, *M2, *rec, *Wc, *Wf;
 };
 
 size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w)
@@ -432,6 +432,7 @@ size_t hgt_bwd_layout(const rgnn_graph *g, int D, int H, void *base, HgtBwdWs *w
     x.Wc = take((size_t)g->T * D * 3 * D);
     x.chunks = take(nchunks * D * D); x.OT = take(R * D * D); x.M2 = take(R * D * D);
     x.rec = take(N * H * 4);
+    x.Wf = take(R * D * D);
     if (w) *w = x;
     return off;
 }
@@ -500,11 +501,18 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     }
     if ((st = launch_hgt_qp_weights(Watt, mu, att_scale, g->R, D, H, w.Wqp, s)) != RGNN_OK) return st;
     {
+        // the segment queries exactly as the forward forms them (with the query
+        // projection folded into the per-relation weight when the relations
+        // are typed), so that the recomputed scores match its statistics
+        const bool fold_q = g->rel_dst_typed && !(D == 128 && hgt_fused_query_fits(g->R, D, H));
+        if (fold_q &&
+            (st = launch_hgt_qp_fold(Wq, Watt, mu, att_scale, g->dev.rel_dsttype, g->R, D, H, w.Wf, s)) != RGNN_OK)
+            return st;
         GemmArgs gq;
-        gq.X = w.Q; gq.ldx = D; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
-        gq.W[0] = w.Wqp; gq.K = D; gq.Nc = D;
+        gq.X = fold_q ? h : w.Q; gq.ldx = D; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
+        gq.W[0] = fold_q ? w.Wf : w.Wqp; gq.K = D; gq.Nc = D;
         gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
-        gq.Y = w.QP; gq.ldy = D; gq.ep.diag_blocks = H;
+        gq.Y = w.QP; gq.ldy = D; gq.ep.diag_blocks = fold_q ? 1 : H;
         if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
     }
     if (!saved) {

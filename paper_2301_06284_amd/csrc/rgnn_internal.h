@@ -58,6 +58,7 @@ struct HostIndex {
     std::vector<int32_t> seg_ptr, seg_rel, dst_segptr;
     std::vector<int32_t> uniq_src, uniq_rel_ptr, e2u;
     std::vector<int32_t> ntype_perm, ntype_ptr;
+    std::vector<int32_t> rel_dsttype;   // node type of every relation's destinations (-1: mixed)
     // scheduling
     std::vector<int32_t> vseg_ptr, vseg_rel, vseg_dst, vseg_cnt, dst_vsegptr;
     std::vector<int32_t> vseg_byrel, rel_vsegptr, vsegdst_byrel;
@@ -115,7 +116,7 @@ struct DeviceIndex {
     int32_t *rowptr = nullptr, *in_src = nullptr, *in_rel = nullptr, *in_eid = nullptr;
     int32_t *seg_ptr = nullptr, *seg_rel = nullptr, *dst_segptr = nullptr;
     int32_t *uniq_src = nullptr, *uniq_rel_ptr = nullptr, *e2u = nullptr;
-    int32_t *ntype_perm = nullptr, *ntype_ptr = nullptr;
+    int32_t *ntype_perm = nullptr, *ntype_ptr = nullptr, *rel_dsttype = nullptr;
     int32_t *vseg_ptr = nullptr, *vseg_rel = nullptr, *vseg_dst = nullptr, *vseg_cnt = nullptr;
     int32_t *dst_vsegptr = nullptr, *vseg_byrel = nullptr, *rel_vsegptr = nullptr;
     int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr, *rel_pairtileptr = nullptr;
@@ -163,6 +164,7 @@ struct rgnn_graph {
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
     int64_t n_oitems = 0, n_osplit = 0, n_oslots = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
     int64_t n_vpairs = 0, n_tiles_vpairs = 0;
+    bool rel_dst_typed = false;   // every relation's destinations share one node type
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
 };
@@ -364,6 +366,11 @@ bool hgt_fused_query_fits(int R, int d, int heads);
 // that Q_t Wqp[r] is the reordered query of segment (t, r).
 rgnn_status launch_hgt_qp_weights(const float *Watt, const float *mu, float scale, int R, int d,
                                   int heads, float *Wqp, hipStream_t s);
+// Wc[r] (d x d) = Wq[rel_dsttype[r]] Wqp[r]: the query projection folded into
+// the reordered query weights, so that h_t Wc[r] is the query of segment (t, r)
+// when every destination of r has node type rel_dsttype[r].
+rgnn_status launch_hgt_qp_fold(const float *Wq, const float *Watt, const float *mu, float scale,
+                               const int32_t *rel_dsttype, int R, int d, int heads, float *Wc, hipStream_t s);
 
 // One head's share of a several-head RGAT backward run as one-head passes:
 // only the output columns [col0, col1) of dW take the outer products (the

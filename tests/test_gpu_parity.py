@@ -286,6 +286,25 @@ def test_hgt_hidden_sizes(kind, d, heads):
     assert row_err(got, ref) <= TOL
 
 
+@pytest.mark.parametrize("kind", ["typed", "typedhub"])
+@pytest.mark.parametrize("d,heads", [(32, 1), (32, 2), (64, 1), (64, 2), (64, 4), (128, 2), (128, 8)])
+def test_hgt_typed_relations(kind, d, heads):
+    """Relations that each join one source type to one destination type: the
+    forward folds the query projection into the segment-query weights (all
+    widths where the traversal does not form the queries itself)."""
+    g = graph(kind, T=4, R=7)
+    t = workloads.tiny_tensors(51, g, d, d, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)
+    scale = 1.0 / np.sqrt(d // heads)
+    print(f"hgt typed d={d} {kind} heads={heads}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt(heads, scale)
+    ref = oracle.hgt_forward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                             t["mu"], heads=heads, att_scale=scale)
+    run.close()
+    assert row_err(got, ref) <= TOL
+
+
 @pytest.mark.parametrize("heads,R", [(2, 12), (4, 24)])
 def test_hgt_many_relations(heads, R):
     """Enough relations that the per-relation message matrices no longer fit
@@ -618,6 +637,25 @@ def test_hgt_backward_hidden_sizes(kind, d, heads, use_saved):
     t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)   # distinct priors
     scale = 1.0 / np.sqrt(d // heads)
     print(f"hgt backward d={d} heads={heads} {kind} saved={use_saved}", flush=True)
+    run = Runner(g, t)
+    got = run.hgt_backward(heads, scale, use_saved=use_saved)
+    run.close()
+    ref = oracle.hgt_backward(g, t["h"], t["Wk"], t["Wq"], t["Wv"], t["Wa"], t["Watt"], t["Wmsg"],
+                              t["mu"], t["grad_out"], heads=heads, att_scale=scale)
+    check_hgt_grads(got, ref, heads, d)
+
+
+@pytest.mark.parametrize("use_saved", [False, True])
+@pytest.mark.parametrize("kind", ["typed", "typedhub"])
+@pytest.mark.parametrize("d,heads", [(32, 2), (64, 4), (128, 8)])
+def test_hgt_backward_typed_relations(kind, d, heads, use_saved):
+    """Typed relations: the backward recomputes the folded segment queries the
+    forward used, so the saved statistics match its scores."""
+    g = graph(kind, T=4, R=7, E=3000)
+    t = workloads.tiny_tensors(57, g, d, d, heads=heads)
+    t["mu"] = (1.0 + 0.25 * np.arange(7)).astype(np.float32)
+    scale = 1.0 / np.sqrt(d // heads)
+    print(f"hgt backward typed d={d} heads={heads} {kind} saved={use_saved}", flush=True)
     run = Runner(g, t)
     got = run.hgt_backward(heads, scale, use_saved=use_saved)
     run.close()

@@ -175,6 +175,10 @@ def tiny_graph(seed: int, N: int, E: int, R: int, T: int = 1, kind: str = "rando
           "complete" every ordered pair (s, t) once, including s == t, relation 0;
           "isolated" destinations drawn from the first half of the nodes only;
           "dups"     a few (u, v, r) triples repeated many times;
+          "typed"    every relation joins one source node type to one
+                     destination node type (as in heterogeneous graphs);
+          "typedhub" the same with half the edges at the first node of
+                     their relation's destination type;
           "empty"    no edges at all.
     """
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
@@ -201,6 +205,19 @@ def tiny_graph(seed: int, N: int, E: int, R: int, T: int = 1, kind: str = "rando
             k = max(1, E // 8)
             pick = rng.integers(0, k, E)
             src, dst, rel = src[pick], dst[pick], rel[pick]
+        elif kind in ("typed", "typedhub"):
+            ntype[: min(T, N)] = np.arange(min(T, N), dtype=np.int32)   # no empty type
+            members = [np.flatnonzero(ntype == t).astype(np.int32) for t in range(T)]
+            dtype_r = np.arange(R) % T
+            stype_r = (np.arange(R) * 3 + 1) % T
+            for r in range(R):
+                m = rel == r
+                ds, ss = members[dtype_r[r]], members[stype_r[r]]
+                dst[m] = ds[rng.integers(0, len(ds), int(m.sum()))]
+                src[m] = ss[rng.integers(0, len(ss), int(m.sum()))]
+                if kind == "typedhub":
+                    hub = m & (np.arange(E) % 2 == 0)
+                    dst[hub] = ds[0]
     return dict(N=int(N), E=int(len(src)), R=int(R), T=int(T),
                 src=np.ascontiguousarray(src, np.int32),
                 dst=np.ascontiguousarray(dst, np.int32),
