@@ -1049,31 +1049,81 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
 
 namespace {
 
-// One 1024-thread workgroup per split source: groups of D/4 lanes take every NG-th slot
-// (four rows in flight), the group sums are added in group order, then to dh.
-template <int D>
-__global__ __launch_bounds__(1024) void src_merge_kernel(const int32_t *osplit, const int32_t *slotptr,
-                                                         const float *part, float *dh)
-{
-    constexpr int G = D / 4, NG = 1024 / G, U = 4;
-    __shared__ float4 red[NG][G];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int b = slotptr[blockIdx.x], e = slotptr[blockIdx.x + 1];
-    float4 acc = zero4();
-    for (int sl = b + gi; sl < e; sl += NG * U) {
-        float4 x[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) x[u] = sl + u * NG < e ? ld4(part + (size_t)(sl + u * NG) * D + gl * 4) : zero4();
-#pragma unroll
-        for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
+// Sums of slot rows (rows of W floats, V floats per lane, G = W / V lanes per
+// row).  A wave per entry: its 64 / G groups take every (64 / G)-th slot (U
+// rows in flight), then the groups' sums are combined by a butterfly over
+// the group bits (every lane ends with the same bits).  An entry with more
+// than kWaveSlots slots takes a whole 1024-thread workgroup: sixteen waves do
+// the same, and their sums are added in wave order.
+template <int V>
+struct SlotVec;
+template <>
+struct SlotVec<4> {
+    float4 v;
+    __device__ void zero() { v = zero4(); }
+    __device__ void load(const float *p) { v = ld4(p); }
+    __device__ void add(const SlotVec &o) { v = add4(v, o.v); }
+    __device__ void xor_add(int m)
+    {
+        v = add4(v, make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m), __shfl_xor(v.w, m)));
     }
-    red[gi][gl] = acc;
+    __device__ void store(float *p, bool acc) const { st4(p, acc ? add4(ld4(p), v) : v); }
+};
+template <>
+struct SlotVec<2> {
+    float2 v;
+    __device__ void zero() { v = make_float2(0.f, 0.f); }
+    __device__ void load(const float *p) { v = *reinterpret_cast<const float2 *>(p); }
+    __device__ void add(const SlotVec &o) { v = make_float2(v.x + o.v.x, v.y + o.v.y); }
+    __device__ void xor_add(int m) { v = make_float2(v.x + __shfl_xor(v.x, m), v.y + __shfl_xor(v.y, m)); }
+    __device__ void store(float *p, bool acc) const
+    {
+        float2 *q = reinterpret_cast<float2 *>(p);
+        *q = acc ? make_float2(q->x + v.x, q->y + v.y) : v;
+    }
+};
+
+template <int W, bool ACC>
+__global__ __launch_bounds__(1024) void slot_sum_kernel(int64_t n, int64_t nwide, const int32_t *order,
+                                                        const int32_t *ids, const int32_t *slotptr,
+                                                        const float *part, float *out)
+{
+    constexpr int V = W % 4 == 0 ? 4 : 2, G = W / V, GW = 64 / G, U = 4;
+    static_assert(G >= 1 && G <= 64 && G * V == W, "row width");
+    __shared__ SlotVec<V> red[16][G];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bool wide = (int64_t)blockIdx.x < nwide;
+    const int64_t k = wide ? (int64_t)blockIdx.x : nwide + ((int64_t)blockIdx.x - nwide) * 16 + wave;
+    if (!wide && k >= n) return;   // whole waves; the narrow path has no barrier
+    const int i = order[k];
+    const int b = slotptr[i], e = slotptr[i + 1];
+    const int gl = lane % G, gw = lane / G;
+    const int gi = wide ? wave * GW + gw : gw, ng = wide ? 16 * GW : GW;
+    SlotVec<V> acc;
+    acc.zero();
+    for (int sl = b + gi; sl < e; sl += ng * U) {
+        SlotVec<V> x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (sl + u * ng < e) x[u].load(part + (size_t)(sl + u * ng) * W + gl * V);
+            else x[u].zero();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc.add(x[u]);
+    }
+#pragma unroll
+    for (int m = G; m < 64; m <<= 1) acc.xor_add(m);
+    float *o = out + (size_t)ids[i] * W + gl * V;
+    if (!wide) {
+        if (gw == 0) acc.store(o, ACC);
+        return;
+    }
+    if (gw == 0) red[wave][gl] = acc;
     __syncthreads();
-    if (gi == 0) {
-        float4 t = zero4();
-        for (int j = 0; j < NG; ++j) t = add4(t, red[j][gl]);
-        float *p = dh + (size_t)osplit[blockIdx.x] * D + gl * 4;
-        st4(p, add4(ld4(p), t));
+    if (wave == 0 && gw == 0) {
+        SlotVec<V> t = red[0][gl];
+        for (int w = 1; w < 16; ++w) t.add(red[w][gl]);
+        t.store(o, ACC);
     }
 }
 
@@ -1107,21 +1157,44 @@ __global__ __launch_bounds__(1024) void chunk_sum_kernel(const float *partial, c
 
 }  // namespace
 
-rgnn_status launch_src_merge(const rgnn_graph *g, const float *part, float *dh, int d, hipStream_t s)
+rgnn_status launch_slot_sum(int64_t n, int64_t nwide, const int32_t *order, const int32_t *ids,
+                            const int32_t *slotptr, const float *part, float *out, int w, bool accumulate,
+                            const char *name, hipStream_t s)
 {
-    if (g->n_osplit == 0) return RGNN_OK;
+    if (n == 0) return RGNN_OK;
+    const unsigned nb = (unsigned)(nwide + (n - nwide + 15) / 16);
     {
-        LaunchScope ls("src_merge", s);
-#define SM(D) hipLaunchKernelGGL((src_merge_kernel<D>), dim3((unsigned)g->n_osplit), dim3(1024), 0, s, g->dev.osplit, \
-                                 g->dev.osplit_slotptr, part, dh)
-        if (d == 32) SM(32);
-        else if (d == 64) SM(64);
-        else if (d == 128) SM(128);
-        else return fail(RGNN_EUNSUPPORTED, "source merge: d must be 32, 64 or 128");
-#undef SM
+        LaunchScope ls(name, s);
+#define SS(W)                                                                                              \
+    do {                                                                                                   \
+        if (accumulate)                                                                                    \
+            hipLaunchKernelGGL((slot_sum_kernel<W, true>), dim3(nb), dim3(1024), 0, s, n, nwide, order, ids, \
+                               slotptr, part, out);                                                        \
+        else                                                                                               \
+            hipLaunchKernelGGL((slot_sum_kernel<W, false>), dim3(nb), dim3(1024), 0, s, n, nwide, order,    \
+                               ids, slotptr, part, out);                                                   \
+    } while (0)
+        switch (w) {
+        case 2: SS(2); break;
+        case 4: SS(4); break;
+        case 8: SS(8); break;
+        case 16: SS(16); break;
+        case 32: SS(32); break;
+        case 64: SS(64); break;
+        case 128: SS(128); break;
+        default: return fail(RGNN_EUNSUPPORTED, "slot sums: unsupported row width");
+        }
+#undef SS
     }
     hipError_t e = hipGetLastError();
-    return e == hipSuccess ? RGNN_OK : hip_fail(e, "src_merge launch");
+    return e == hipSuccess ? RGNN_OK : hip_fail(e, "slot_sum launch");
+}
+
+rgnn_status launch_src_merge(const rgnn_graph *g, const float *part, float *dh, int d, hipStream_t s)
+{
+    if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "source merge: d must be 32, 64 or 128");
+    return launch_slot_sum(g->n_osplit, g->n_osplit_wide, g->dev.osplit_order, g->dev.osplit,
+                           g->dev.osplit_slotptr, part, dh, d, true, "src_merge", s);
 }
 
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,

@@ -90,6 +90,7 @@ struct HK {
                              // (q with the sign bit set where the logit is <= 0), then (alpha, Y)
     float *ysum;             // [V, H] per vseg (by-relation position) and head: sum of Y
     float *dh;               // [N, D] destination terms written here
+    float *dpart;            // [slots, D] a split destination's term, per piece (summed after)
     const int32_t *split_items;
     int64_t n_split_items;
 };
@@ -244,8 +245,54 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
         return SEG ? k.svs[(size_t)(vs0 + jv) * H + hh] : k.sv[(size_t)(dst0 + st.vdj[jv]) * H + hh];
     };
     // the sum of Y per segment and head, from (q, dalpha) before pass 2
-    // replaces them; four edges' pairs in flight per lane
-    if (fin) {
+    // replaces them.  A piece of a split destination with few segments (of
+    // many edges): the group's lanes take its edges (all in flight) and the
+    // four sums per head are reduced over the group; otherwise a lane takes a
+    // (segment, head) pair with four edges' pairs in flight.
+    if (fin && PHASE == 1 && !SEG && nv * H <= G / 2) {
+        constexpr int NPL = (kE + G - 1) / G;   // edges per lane
+        for (int jv = 0; jv < nv; ++jv) {
+            const int eb = st.vptr[jv], ee = st.vptr[jv + 1];
+            float2 p[NPL][H];
+#pragma unroll
+            for (int u = 0; u < NPL; ++u) {
+                const int e = eb + gl + u * G;
+#pragma unroll
+                for (int hh = 0; hh < H; ++hh)
+                    p[u][hh] = e < ee ? ay2[(size_t)(e0 + e) * H + hh] : make_float2(0.f, 0.f);
+            }
+            float ap[H], bp[H], an[H], bn[H];
+#pragma unroll
+            for (int hh = 0; hh < H; ++hh) {
+                ap[hh] = bp[hh] = an[hh] = bn[hh] = 0.f;
+#pragma unroll
+                for (int u = 0; u < NPL; ++u) {
+                    const float a = p[u][hh].x, q = fabsf(a);
+                    if (signbit(a)) {
+                        an[hh] = __builtin_fmaf(q, p[u][hh].y, an[hh]);
+                        bn[hh] += q;
+                    } else {
+                        ap[hh] = __builtin_fmaf(q, p[u][hh].y, ap[hh]);
+                        bp[hh] += q;
+                    }
+                }
+                ap[hh] = gsum<G>(ap[hh]);
+                bp[hh] = gsum<G>(bp[hh]);
+                an[hh] = gsum<G>(an[hh]);
+                bn[hh] = gsum<G>(bn[hh]);
+            }
+#pragma unroll
+            for (int hh = 0; hh < H; ++hh) {
+                if (gl != hh) continue;
+                const float2 sz = sz_of(jv, hh);
+                const float ys = sz.y > 0.f ? (cross_diff(ap[hh], sz.y, sz.x, bp[hh]) +
+                                               k.slope * cross_diff(an[hh], sz.y, sz.x, bn[hh])) /
+                                                  (sz.y * sz.y)
+                                            : 0.f;
+                k.ysum[(size_t)st.vpos[jv] * H + hh] = ys;
+            }
+        }
+    } else if (fin) {
         for (int i = gl; i < nv * H; i += G) {
             const int jv = i / H, hh = i % H;
             const float2 sz = sz_of(jv, hh);
@@ -290,12 +337,13 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
         }
     }
     // pass 3: destination term dh_v = sum over v's segments and heads of ysum * wt'
-    if (fin && slot < 0 && (PHASE == 0 || SEG)) {
+    // (a piece of a split destination writes its segments' share to its slot)
+    if (fin && (slot < 0 ? PHASE == 0 || SEG : PHASE == 1)) {
         float4 acc = zero4();
         int j = 0;
         auto flush_to = [&](int jn) {
             while (j < jn) {
-                st4(k.dh + (size_t)(dst0 + j) * D + gl * 4, acc);
+                st4((slot < 0 ? k.dh + (size_t)(dst0 + j) * D : k.dpart + (size_t)slot * D) + gl * 4, acc);
                 acc = zero4();
                 ++j;
             }
@@ -341,29 +389,6 @@ __global__ __launch_bounds__(mh_threads(D)) void mh_dst_kernel(HK k)
     }
 }
 
-// (S', Z') of split destinations: one workgroup per split destination, the
-// pieces' parts summed per head in a fixed order (thread parts, then threads).
-template <int H>
-__global__ __launch_bounds__(256) void mh_merge_s_kernel(const int32_t *split_dst, const int32_t *split_slotptr,
-                                                         const float2 *ssum, float2 *sv)
-{
-    __shared__ float2 part[256];
-    const int i = blockIdx.x;
-    const int b = split_slotptr[i], e = split_slotptr[i + 1];
-    for (int hh = 0; hh < H; ++hh) {
-        float2 s = make_float2(0.f, 0.f);
-        for (int sl = b + (int)threadIdx.x; sl < e; sl += 256) s = add2(s, ssum[(size_t)sl * H + hh]);
-        part[threadIdx.x] = s;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            float2 t = make_float2(0.f, 0.f);
-            for (int j = 0; j < 256; ++j) t = add2(t, part[j]);
-            sv[(size_t)split_dst[i] * H + hh] = t;
-        }
-        __syncthreads();
-    }
-}
-
 // Per-segment softmax: (S', Z') of a (dst, rel) segment cut into several
 // vsegs, summed in vseg order and written back to each of them.
 template <int H>
@@ -378,45 +403,6 @@ __global__ __launch_bounds__(256) void mh_merge_seg_s_kernel(int64_t U, const in
     float2 s = make_float2(0.f, 0.f);
     for (int vs = b; vs < e; ++vs) s = add2(s, svs[(size_t)vs * H + hh]);
     for (int vs = b; vs < e; ++vs) svs[(size_t)vs * H + hh] = s;
-}
-
-// Destination term of a split destination: its segments (spread over
-// several items) summed by one workgroup, segments strided over groups and
-// combined in group order.
-template <int D, int H>
-__global__ __launch_bounds__(1024) void mh_split_dst_term_kernel(const int32_t *split_dst, const int32_t *dst_vsegptr,
-                                                                 const int32_t *vseg_rel, const int32_t *vseg_pos,
-                                                                 const float *ysum, const float *wtp, float *dh)
-{
-    constexpr int G = D / 4, NG = 1024 / G, U = 4;
-    __shared__ float4 part[NG][G];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int v = split_dst[blockIdx.x];
-    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    float4 acc = zero4();
-    for (int vs0 = b + gi; vs0 < e; vs0 += U * NG) {
-        int r[U];
-        size_t pos[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int vs = vs0 + u * NG < e ? vs0 + u * NG : vs0;
-            r[u] = vseg_rel[vs];
-            pos[u] = (size_t)vseg_pos[vs] * H;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (vs0 + u * NG < e)
-#pragma unroll
-                for (int hh = 0; hh < H; ++hh)
-                    acc = lin4(acc, 1.f, ld4(wtp + ((size_t)r[u] * H + hh) * D + gl * 4), ysum[pos[u] + hh]);
-    }
-    part[gi][gl] = acc;
-    __syncthreads();
-    if (gi == 0) {
-        float4 t = zero4();
-        for (int j = 0; j < NG; ++j) t = add4(t, part[j][gl]);
-        st4(dh + (size_t)v * D + gl * 4, t);
-    }
 }
 
 // ---------------------------------------------------------------- source-major pass
@@ -817,7 +803,7 @@ __global__ __launch_bounds__(256) void mh_finalize_kernel(const float *W, const 
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct MhWs {
-    float *wtp, *vatt, *M, *dHp, *ay, *ysum, *ypair, *partial, *pvec, *yvec, *dws, *dwt;
+    float *wtp, *vatt, *M, *dHp, *ay, *ysum, *ypair, *partial, *pvec, *yvec, *dws, *dwt, *dpart;
     float2 *ssum, *sv, *svs;
 };
 
@@ -849,6 +835,7 @@ size_t mh_layout(const rgnn_graph *g, int D, int H, void *base, MhWs *w)
     x.ssum = (float2 *)take((size_t)g->n_slots * H * 2);
     x.sv = (float2 *)take((size_t)g->N * H * 2);
     x.svs = (float2 *)take(V * H * 2);
+    x.dpart = take((size_t)g->n_slots * D);
     if (w) *w = x;
     return off;
 }
@@ -883,7 +870,7 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
     k.vseg_ptr = x.vseg_ptr; k.vseg_rel = x.vseg_rel; k.vseg_pos = x.vseg_pos; k.e2u = x.e2u;
     k.vseg_seg = x.vseg_seg; k.M = w.M; k.w_src = w_src; k.wtp = w.wtp; k.saved = saved; k.vatt = w.vatt;
     k.G = Gm; k.sv = w.sv; k.ssum = w.ssum; k.svs = w.svs; k.slope = slope; k.ay = w.ay; k.ysum = w.ysum;
-    k.dh = dh; k.split_items = x.split_items; k.n_split_items = g->n_split_items;
+    k.dh = dh; k.dpart = w.dpart; k.split_items = x.split_items; k.n_split_items = g->n_split_items;
     constexpr int NTH = mh_threads(D), GPB = NTH / (D / 4);
     if (g->n_items) {
         const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
@@ -911,12 +898,11 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
         }
         if (g->n_split) {
             if (!per_seg) {
-                {
-                    LaunchScope ls("rgat_bwd_heads_merge", s);
-                    hipLaunchKernelGGL(mh_merge_s_kernel<H>, dim3((unsigned)g->n_split), dim3(256), 0, s,
-                                       x.split_dst, x.split_slotptr, w.ssum, w.sv);
-                }
-                if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_merge launch");
+                // (S', Z') of split destinations: their pieces' parts summed per head
+                if ((st = launch_slot_sum(g->n_split, g->n_split_wide, x.split_order, x.split_dst, x.split_slotptr,
+                                          reinterpret_cast<const float *>(w.ssum), reinterpret_cast<float *>(w.sv),
+                                          2 * H, false, "rgat_bwd_heads_merge", s)) != RGNN_OK)
+                    return st;
                 if (g->n_split_items) {
                     LaunchScope ls("rgat_bwd_heads_dst_split", s);
                     const dim3 sgrid((unsigned)((g->n_split_items + GPB - 1) / GPB));
@@ -924,12 +910,10 @@ rgnn_status mh_backward_dh(const rgnn_graph *g, const float *h, const float *W, 
                 }
                 if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_dst launch");
             }
-            {
-                LaunchScope ls("rgat_bwd_heads_split_dst_term", s);
-                hipLaunchKernelGGL((mh_split_dst_term_kernel<D, H>), dim3((unsigned)g->n_split), dim3(1024), 0, s,
-                                   x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, w.ysum, w.wtp, dh);
-            }
-            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "mh_split_dst_term launch");
+            // destination terms of split destinations: the pieces' shares summed
+            if ((st = launch_slot_sum(g->n_split, g->n_split_wide, x.split_order, x.split_dst, x.split_slotptr,
+                                      w.dpart, dh, D, false, "rgat_bwd_heads_split_dst_term", s)) != RGNN_OK)
+                return st;
         }
     }
     const int32_t *pairchunkptr = x.rel_pairchunkptr;

@@ -270,6 +270,18 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             x.big_chunkptr.push_back((int32_t)x.chunk_lo.size());
         }
         g->n_big_chunks = (int64_t)x.chunk_lo.size();
+        auto order_by_slots = [](const std::vector<int32_t> &ptr, std::vector<int32_t> &order, int64_t &nwide) {
+            const int64_t n = (int64_t)ptr.size() - 1;
+            order.resize((size_t)n);
+            for (int64_t i = 0; i < n; ++i) order[i] = (int32_t)i;
+            std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {   // ties in index order
+                const int32_t na = ptr[a + 1] - ptr[a], nb = ptr[b + 1] - ptr[b];
+                return na != nb ? na > nb : a < b;
+            });
+            nwide = 0;
+            while (nwide < n && ptr[order[nwide] + 1] - ptr[order[nwide]] > kWaveSlots) ++nwide;
+        };
+        order_by_slots(x.split_slotptr, x.split_order, g->n_split_wide);
         // destinations with many segments, largest first (ties in id order):
         // their reductions take whole workgroups at the front of the grid
         x.big_vdst.clear();
@@ -340,6 +352,7 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             g->n_oitems = (int64_t)x.oitems.size();
             g->n_osplit = (int64_t)x.osplit.size();
             g->n_oslots = x.osplit_slotptr.back();
+            order_by_slots(x.osplit_slotptr, x.osplit_order, g->n_osplit_wide);
         }
 
         // ---- GEMM tile tables ----
@@ -460,6 +473,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.big_chunkptr, x.big_chunkptr); add32(&d.chunk_lo, x.chunk_lo); add32(&d.chunk_hi, x.chunk_hi);
     add32(&d.seg_vsegptr, x.seg_vsegptr); add32(&d.big_seg, x.big_seg); add32(&d.osplit, x.osplit);
     add32(&d.oitem_slot, x.oitem_slot); add32(&d.osplit_slotptr, x.osplit_slotptr);
+    add32(&d.split_order, x.split_order); add32(&d.osplit_order, x.osplit_order);
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});

@@ -25,6 +25,9 @@ constexpr int kFusedTileEdges = 4096;
 // Reductions over more records than this (partials of a split destination,
 // segments of one destination) get a whole workgroup instead of one group.
 constexpr int kBigRange = 32;
+// Split destinations / sources with more slots than this have their slot sums
+// taken by a whole workgroup, the others by a single wave.
+constexpr int kWaveSlots = 64;
 // the partials of a destination split over more than kBigRange items are
 // merged in two levels: chunks of kMergeChunk partials, then the chunks
 constexpr int kMergeChunk = 128;
@@ -66,6 +69,7 @@ struct HostIndex {
     std::vector<int32_t> item_slot, split_dst, split_slotptr;
     std::vector<int32_t> split_items;   // items that are pieces of split destinations (slot >= 0)
     std::vector<int32_t> big_split;   // indices into split_dst with > kBigRange slots
+    std::vector<int32_t> split_order;   // indices into split_dst, most slots first [n_split]
     std::vector<int32_t> big_chunkptr;  // chunks of each big split [n_big_split + 1]
     std::vector<int32_t> chunk_lo, chunk_hi;   // slot range of each chunk [n_big_chunks]
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments,
@@ -76,6 +80,7 @@ struct HostIndex {
     std::vector<int32_t> oitem_slot;   // per out-edge item: its slot if it is a piece of such a
                                        // source, else -1 [n_oitems]
     std::vector<int32_t> osplit_slotptr;   // slots of each of those sources [n_osplit+1]
+    std::vector<int32_t> osplit_order;     // indices into osplit, most slots first [n_osplit]
     std::vector<FusedRow> fused_rows;  // vsegs by (rel, edge count desc, id) [V]
     std::vector<Tile> tiles_fused;     // tiles over fused_rows (pad: first fused_src position)
     std::vector<int32_t> fused_src;    // in-edge sources, segment by segment in fused order [E]
@@ -126,6 +131,7 @@ struct DeviceIndex {
     int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr, *osplit = nullptr;
     int32_t *oitem_slot = nullptr, *osplit_slotptr = nullptr;
+    int32_t *split_order = nullptr, *osplit_order = nullptr;
     float *invcnt_byrel = nullptr;
     Tile *tiles_nodes_outer = nullptr;
     int32_t *nodes_chunkptr = nullptr;
@@ -164,6 +170,7 @@ struct rgnn_graph {
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
     int64_t n_oitems = 0, n_osplit = 0, n_oslots = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
     int64_t n_vpairs = 0, n_tiles_vpairs = 0;
+    int64_t n_split_wide = 0, n_osplit_wide = 0;   // split lists' entries with > kWaveSlots slots
     bool rel_dst_typed = false;   // every relation's destinations share one node type
     rgnn::HostIndex host;
     rgnn::DeviceIndex dev;
@@ -329,8 +336,16 @@ rgnn_status launch_outer_chunks(const Tile *chunks, int64_t nchunks, const int32
                                 hipStream_t s);
 // dW[r] = sum of partial[c] for c in [chunkptr[r], chunkptr[r+1]) in order (d x d each).
 // Pieces of split sources: dh[osplit[i]] += the partial rows of its slots
-// [osplit_slotptr[i], osplit_slotptr[i + 1]) in slot order (d in {32, 64, 128}).
+// [osplit_slotptr[i], osplit_slotptr[i + 1]) in a fixed order (d in {32, 64, 128}).
 rgnn_status launch_src_merge(const rgnn_graph *g, const float *part, float *dh, int d, hipStream_t s);
+// out[ids[i] * w ...] = (accumulate: +=) the sum of the w-float rows part[sl], sl in
+// [slotptr[i], slotptr[i + 1]), for all n entries, in a fixed order (w in {2, 4, 8,
+// 16, 32, 64, 128}).  order lists the entries with the nwide ones holding more than
+// kWaveSlots slots first: each of those takes a 1024-thread workgroup, the others a
+// wave each (sixteen per workgroup).
+rgnn_status launch_slot_sum(int64_t n, int64_t nwide, const int32_t *order, const int32_t *ids,
+                            const int32_t *slotptr, const float *part, float *out, int w, bool accumulate,
+                            const char *name, hipStream_t s);
 rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int R, float *dW, int d,
                              hipStream_t s);
 // RGAT backward with several heads (2 to 8, d / heads >= 16) in one pass over
