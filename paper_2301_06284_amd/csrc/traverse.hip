@@ -368,17 +368,20 @@ __global__ __launch_bounds__(256) void rgcn_tf_kernel(TK k)
 // flight while the current batch's dot products are formed.
 constexpr int kSegBatches = 4;
 
-template <int D, int H>
-__global__ __launch_bounds__(256) void seg_attn_lds_kernel(TK k, int64_t V, const int32_t *vseg_dst, int R)
+// NT threads per workgroup: 256, or 1024 when the vectors of several heads
+// take most of the LDS (one workgroup per CU then stages them once for four
+// times the segments).
+template <int D, int H, int NT>
+__global__ __launch_bounds__(NT) void seg_attn_lds_kernel(TK k, int64_t V, const int32_t *vseg_dst, int R)
 {
-    constexpr int G = D / 4, GPB = 256 / G;
+    constexpr int G = D / 4, GPB = NT / G;
     constexpr int S = kSegPerGroup, SB = kSegBatches, SW = GPB * S * SB;
     extern __shared__ float4 wts[];   // [R, H, D / 4]
     __shared__ int2 sidx[SW];         // (destination, relation) of the workgroup's segments
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     const int64_t wbase = (int64_t)blockIdx.x * SW;
-    for (int i = threadIdx.x; i < R * H * G; i += 256) wts[i] = ld4(k.wtp + (size_t)i * 4);
-    for (int i = threadIdx.x; i < SW; i += 256) {
+    for (int i = threadIdx.x; i < R * H * G; i += NT) wts[i] = ld4(k.wtp + (size_t)i * 4);
+    for (int i = threadIdx.x; i < SW; i += NT) {
         const int64_t vs = wbase + i < V ? wbase + i : V - 1;
         sidx[i] = make_int2(vseg_dst[vs], k.vseg_rel[vs]);
     }
@@ -447,8 +450,8 @@ rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s)
     if (wbytes <= 32768 && a.heads <= 2) {
         const unsigned nbl = blocks_for((a.g->V + kSegPerGroup * kSegBatches - 1) / (kSegPerGroup * kSegBatches),
                                         256 / (a.d / 4));
-#define SAL(D, H) hipLaunchKernelGGL((seg_attn_lds_kernel<D, H>), dim3(nbl), dim3(256), wbytes, s, k, a.g->V, \
-                                     a.g->dev.vseg_dst, a.g->R)
+#define SAL(D, H) hipLaunchKernelGGL((seg_attn_lds_kernel<D, H, 256>), dim3(nbl), dim3(256), wbytes, s, k, \
+                                     a.g->V, a.g->dev.vseg_dst, a.g->R)
         bool done = true;
         if (a.d == 32 && a.heads == 1) SAL(32, 1);
         else if (a.d == 32 && a.heads == 2) SAL(32, 2);
@@ -459,6 +462,37 @@ rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s)
         else done = false;
 #undef SAL
         if (done) {
+            hipError_t e = hipGetLastError();
+            return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_attn launch");
+        }
+    }
+    // larger vector sets (several heads, d = 128): 1024-thread workgroups, one per CU
+    const size_t sidx_bytes = (size_t)(1024 / (a.d / 4)) * kSegPerGroup * kSegBatches * sizeof(int2);
+    if (wbytes + sidx_bytes <= 160 * 1024) {
+        const unsigned nbl = blocks_for((a.g->V + kSegPerGroup * kSegBatches - 1) / (kSegPerGroup * kSegBatches),
+                                        1024 / (a.d / 4));
+        hipError_t ea = hipSuccess;
+#define SAW(D, H)                                                                                          \
+    do {                                                                                                   \
+        ea = hipFuncSetAttribute((const void *)seg_attn_lds_kernel<D, H, 1024>,                            \
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)wbytes);                 \
+        if (ea == hipSuccess)                                                                              \
+            hipLaunchKernelGGL((seg_attn_lds_kernel<D, H, 1024>), dim3(nbl), dim3(1024), wbytes, s, k, a.g->V, \
+                               a.g->dev.vseg_dst, a.g->R);                                                 \
+    } while (0)
+        bool done = true;
+        if (a.d == 32 && a.heads == 1) SAW(32, 1);
+        else if (a.d == 32 && a.heads == 2) SAW(32, 2);
+        else if (a.d == 64 && a.heads == 1) SAW(64, 1);
+        else if (a.d == 64 && a.heads == 2) SAW(64, 2);
+        else if (a.d == 64 && a.heads == 4) SAW(64, 4);
+        else if (a.d == 128 && a.heads == 1) SAW(128, 1);
+        else if (a.d == 128 && a.heads == 2) SAW(128, 2);
+        else if (a.d == 128 && a.heads == 8) SAW(128, 8);   // (128, 4) would spill
+        else done = false;
+#undef SAW
+        if (done) {
+            if (ea != hipSuccess) return hip_fail(ea, "hipFuncSetAttribute (seg_attn LDS)");
             hipError_t e = hipGetLastError();
             return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_attn launch");
         }
