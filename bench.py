@@ -132,8 +132,23 @@ def rgat_tf_model(info, d, H):
     }
 
 
-def rgat_af_model(info, d):
-    """Algorithmic bytes / flops per launch of the aggregate-first RGAT kernels."""
+def single_segment_dsts(G):
+    """Destinations whose in-edges form one virtual segment (one relation, at
+    most chunk_edges edges): the fused kernel finishes them itself."""
+    import numpy as np
+    inf = G.info()
+    dseg = np.diff(G.export("dst_segptr").astype(np.int64))
+    sptr = G.export("seg_ptr").astype(np.int64)
+    first = G.export("dst_segptr")[:-1].astype(np.int64)
+    one = dseg == 1
+    cnt = sptr[np.minimum(first + 1, len(sptr) - 1)] - sptr[np.minimum(first, len(sptr) - 1)]
+    return int(np.count_nonzero(one & (cnt <= inf["chunk_edges"])))
+
+
+def rgat_af_model(info, d, n_single=0):
+    """Algorithmic bytes / flops per launch of the aggregate-first RGAT kernels.
+    n_single: destinations with a single virtual segment, finished by the fused
+    kernel (their output row and statistics replace the T row and (max, sum))."""
     E, N, V, R = info["num_edges"], info["num_nodes"], info["num_vsegs"], info["num_rels"]
     return {
         # per edge: source index and gathered h row; per segment: its table
@@ -146,8 +161,10 @@ def rgat_af_model(info, d):
         # per segment T row and scale read, per destination offsets and output row
         "vseg_reduce": dict(bytes=V * (4 * d + 4) + N * (4 + 4 * d), flops=2.0 * V * d),
         # per segment T row, fused position and (max, sum); per destination
-        # offsets, output row and saved (max, sum)
-        "softmax_reduce": dict(bytes=V * (4 * d + 4 + 8) + N * (4 + 4 * d + 8), flops=2.0 * V * d),
+        # offsets, output row and saved (max, sum) -- except the segments and
+        # rows of the destinations the fused kernel finished (offsets only)
+        "softmax_reduce": dict(bytes=(V - n_single) * (4 * d + 4 + 8) + N * 4 + (N - n_single) * (4 * d + 8),
+                               flops=2.0 * (V - n_single) * d),
         # per destination its h row (consecutive segments share it); per
         # segment its destination, relation and term written; W_r w_dst per relation
         "seg_attn": dict(bytes=N * 4 * d + V * 12 + R * 4 * d, flops=2.0 * V * d),
@@ -368,7 +385,8 @@ def main():
         plans[p] = (ms, kern, fn, each)
         del ws
     ms, kern, fn, each = plans[plan]
-    model = rgat_tf_model(inf, d, H) if plan == rgnn.PLAN_TRANSFORM_FIRST else rgat_af_model(inf, d)
+    model = (rgat_tf_model(inf, d, H) if plan == rgnn.PLAN_TRANSFORM_FIRST
+             else rgat_af_model(inf, d, single_segment_dsts(c.G)))
     kname, kms, kgbs, ktfl, km = roofline_of(kern, model)
     E = inf["num_edges"]
     value = E / (ms * 1e-3)
