@@ -401,9 +401,10 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             for (int64_t u = 0; u < N; ++u) x.src_pairptr[u + 1] += x.src_pairptr[u];
         }
         // virtual pairs: a pair's out-edges are consecutive in the out-edge
-        // order (src, rel, position); pieces of at most kPairPiece of them, in
-        // (rel, src) order, then their rows in source-major order and chunks
-        // per relation
+        // order (src, rel, position); pieces of at most kPairPiece of them, per
+        // relation ordered by out-edge count (most first, then by source), so
+        // that the pairs a workgroup gathers together have similar counts;
+        // then their rows in source-major order and chunks per relation
         {
             std::vector<int32_t> oe0((size_t)g->U_src, -1), oen((size_t)g->U_src, 0);
             for (int64_t q = 0; q < E; ++q) {
@@ -413,12 +414,24 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
             }
             x.vpair_oe0.clear(); x.vpair_ne.clear(); x.vpair_src.clear();
             std::vector<int32_t> rel_vpairptr((size_t)R + 1, 0);
+            std::vector<int32_t> bucket_cnt((size_t)kPairPiece + 2, 0);
             for (int32_t r = 0; r < R; ++r) {
+                // counting sort of the relation's pieces by descending count
+                std::fill(bucket_cnt.begin(), bucket_cnt.end(), 0);
+                for (int32_t p = x.uniq_rel_ptr[r]; p < x.uniq_rel_ptr[r + 1]; ++p)
+                    for (int32_t o = 0; o < oen[p]; o += kPairPiece)
+                        bucket_cnt[(size_t)(kPairPiece - std::min<int32_t>(kPairPiece, oen[p] - o)) + 1]++;
+                for (int32_t b = 0; b <= kPairPiece; ++b) bucket_cnt[(size_t)b + 1] += bucket_cnt[b];
+                const size_t base = x.vpair_src.size();
+                const size_t n = base + (size_t)bucket_cnt[(size_t)kPairPiece + 1];
+                x.vpair_oe0.resize(n); x.vpair_ne.resize(n); x.vpair_src.resize(n);
                 for (int32_t p = x.uniq_rel_ptr[r]; p < x.uniq_rel_ptr[r + 1]; ++p)
                     for (int32_t o = 0; o < oen[p]; o += kPairPiece) {
-                        x.vpair_oe0.push_back(oe0[p] + o);
-                        x.vpair_ne.push_back(std::min<int32_t>(kPairPiece, oen[p] - o));
-                        x.vpair_src.push_back(x.uniq_src[p]);
+                        const int32_t ne = std::min<int32_t>(kPairPiece, oen[p] - o);
+                        const size_t at = base + (size_t)bucket_cnt[(size_t)(kPairPiece - ne)]++;
+                        x.vpair_oe0[at] = oe0[p] + o;
+                        x.vpair_ne[at] = ne;
+                        x.vpair_src[at] = x.uniq_src[p];
                     }
                 rel_vpairptr[(size_t)r + 1] = (int32_t)x.vpair_src.size();
             }
