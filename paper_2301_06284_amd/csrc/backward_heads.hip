@@ -31,6 +31,8 @@
 // source-major pair order, summed per source into dh; outer-product MFMA
 // chunks of h_u^T dM per relation; per-head GEMVs for dws' and dwt'; a
 // per-relation finalize.
+#include <type_traits>
+
 #include "rgnn_internal.h"
 #include "wave_ops.h"
 
@@ -599,34 +601,43 @@ __global__ __launch_bounds__(256) void mh_pair_fused_kernel(PF k)
             ys[s] = 0.f;
             nmax = ne[s] > nmax ? ne[s] : nmax;
         }
-        for (int o = 0; o < nmax; o += 2) {
-            int pos[RPG][2], dv[RPG][2];
+        // the wave's largest count (pairs are ordered by count, so a step's
+        // pairs mostly share it): batches of two out-edges, one for an odd tail
+#pragma unroll
+        for (int m = 1; m < 64; m <<= 1) nmax = max(nmax, __shfl_xor(nmax, m));
+        nmax = __builtin_amdgcn_readfirstlane(nmax);
+        auto batch = [&](auto nu_c, int o) {
+            constexpr int NU = decltype(nu_c)::value;
+            int pos[RPG][NU], dv[RPG][NU];
 #pragma unroll
             for (int s = 0; s < RPG; ++s)
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
+                for (int u = 0; u < NU; ++u) {
                     const int e = oe[s] + (o + u < ne[s] ? o + u : 0);
                     pos[s][u] = k.out_pos[e];
                     dv[s][u] = k.out_dst[e];
                 }
-            float4 gr[RPG][2];
-            float2 a[RPG][2];
+            float4 gr[RPG][NU];
+            float2 a[RPG][NU];
 #pragma unroll
             for (int s = 0; s < RPG; ++s)
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
+                for (int u = 0; u < NU; ++u) {
                     gr[s][u] = ld4(k.G + (size_t)dv[s][u] * D + gl * 4);
                     a[s][u] = ay2[(size_t)pos[s][u] * H + head];
                 }
 #pragma unroll
             for (int s = 0; s < RPG; ++s)
 #pragma unroll
-                for (int u = 0; u < 2; ++u)
+                for (int u = 0; u < NU; ++u)
                     if (o + u < ne[s]) {
                         am[s] = lin4(am[s], 1.f, gr[s][u], a[s][u].x);
                         ys[s] += a[s][u].y;
                     }
-        }
+        };
+        int o = 0;
+        for (; o + 1 < nmax; o += 2) batch(std::integral_constant<int, 2>{}, o);
+        if (o < nmax) batch(std::integral_constant<int, 1>{}, o);
 #pragma unroll
         for (int s = 0; s < RPG; ++s) {
             const int rr = gi + NG * s;
