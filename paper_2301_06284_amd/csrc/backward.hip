@@ -858,9 +858,20 @@ __global__ __launch_bounds__(1024) void bwd_reduce_kernel(const float *pvec, con
     constexpr int NC = 1024 / D;
     __shared__ float red[2][NC][D];
     const int r = blockIdx.x, i = threadIdx.x % D, c = threadIdx.x / D;
-    float a = 0.f, b = 0.f;
-    for (int t = rel_pairtileptr[r] + c; t < rel_pairtileptr[r + 1]; t += NC) a += pvec[(size_t)t * D + i];
-    for (int ch = rel_chunkptr[r] + c; ch < rel_chunkptr[r + 1]; ch += NC) b += yvec[(size_t)ch * D + i];
+    constexpr int U = 4;   // loads in flight per thread
+    auto strided_sum = [&](const float *vec, int t0, int t1) {
+        float acc = 0.f;
+        for (int t = t0 + c; t < t1; t += NC * U) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = t + u * NC < t1 ? vec[(size_t)(t + u * NC) * D + i] : 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc += x[u];
+        }
+        return acc;
+    };
+    const float a = strided_sum(pvec, rel_pairtileptr[r], rel_pairtileptr[r + 1]);
+    const float b = strided_sum(yvec, rel_chunkptr[r], rel_chunkptr[r + 1]);
     red[0][c][i] = a;
     red[1][c][i] = b;
     __syncthreads();

@@ -758,8 +758,8 @@ __global__ __launch_bounds__(256) void mh_gemv_kernel(const Tile *tiles, const i
 
 // Per relation r (blockIdx.x) and 64 entries of its [H, D] vectors
 // (blockIdx.y): dws'[r] = sum of its pair chunks' vectors, dwt'[r] = sum of
-// its segment chunks' vectors.  16 threads per entry take every 16th chunk;
-// their sums are added in thread order.
+// its segment chunks' vectors.  16 threads per entry take every 16th chunk
+// (four loads in flight); their sums are added in thread order.
 template <int D, int H>
 __global__ __launch_bounds__(1024) void mh_reduce_kernel(const float *pvec, const int32_t *rel_pairchunkptr,
                                                          const float *yvec, const int32_t *rel_chunkptr, float *dws,
@@ -769,9 +769,20 @@ __global__ __launch_bounds__(1024) void mh_reduce_kernel(const float *pvec, cons
     __shared__ float2 red[NS][64];
     const int r = blockIdx.x, li = threadIdx.x % 64, c = threadIdx.x / 64;
     const int i = blockIdx.y * 64 + li;   // entry of [H, D]
-    float a = 0.f, b = 0.f;
-    for (int t = rel_pairchunkptr[r] + c; t < rel_pairchunkptr[r + 1]; t += NS) a += pvec[(size_t)t * H * D + i];
-    for (int t = rel_chunkptr[r] + c; t < rel_chunkptr[r + 1]; t += NS) b += yvec[(size_t)t * H * D + i];
+    constexpr int U = 4;
+    auto strided_sum = [&](const float *vec, int t0, int t1) {
+        float acc = 0.f;
+        for (int t = t0 + c; t < t1; t += NS * U) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = t + u * NS < t1 ? vec[(size_t)(t + u * NS) * H * D + i] : 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc += x[u];
+        }
+        return acc;
+    };
+    const float a = strided_sum(pvec, rel_pairchunkptr[r], rel_pairchunkptr[r + 1]);
+    const float b = strided_sum(yvec, rel_chunkptr[r], rel_chunkptr[r + 1]);
     red[c][li] = make_float2(a, b);
     __syncthreads();
     if (c == 0) {
@@ -797,17 +808,33 @@ __global__ __launch_bounds__(256) void mh_finalize_kernel(const float *W, const 
         dW[(size_t)r * D * D + idx] += dwt[((size_t)r * H + hh) * D + i] * w_dst[(size_t)r * D + j];
     }
     if (blockIdx.y) return;
-    for (int j = threadIdx.x; j < D; j += 256) {
-        const int hh = j / DK;
-        const float *a = dws + ((size_t)r * H + hh) * D, *b = dwt + ((size_t)r * H + hh) * D;
-        float sa = 0.f, sb = 0.f;
-        for (int i = 0; i < D; ++i) {
-            const float w = Wr[(size_t)i * D + j];
-            sa += a[i] * w;
-            sb += b[i] * w;
-        }
-        dw_src[(size_t)r * D + j] = sa;
-        dw_dst[(size_t)r * D + j] = sb;
+    // column j: threads (part q, j) take the rows i = q, q + NQ, ... (all loads
+    // of a part issued together), the parts are added in order
+    constexpr int NQ = 256 / D, RI = D / NQ;
+    __shared__ float2 red[NQ][D];
+    const int j = threadIdx.x % D, q = threadIdx.x / D, hh = j / DK;
+    const float *a = dws + ((size_t)r * H + hh) * D, *b = dwt + ((size_t)r * H + hh) * D;
+    float w[RI], av[RI], bv[RI];
+#pragma unroll
+    for (int t = 0; t < RI; ++t) {
+        const int i = q + NQ * t;
+        w[t] = Wr[(size_t)i * D + j];
+        av[t] = a[i];
+        bv[t] = b[i];
+    }
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int t = 0; t < RI; ++t) {
+        sa += av[t] * w[t];
+        sb += bv[t] * w[t];
+    }
+    red[q][j] = make_float2(sa, sb);
+    __syncthreads();
+    if (q == 0) {
+        float2 s = red[0][j];
+        for (int qq = 1; qq < NQ; ++qq) s = add2(s, red[qq][j]);
+        dw_src[(size_t)r * D + j] = s.x;
+        dw_dst[(size_t)r * D + j] = s.y;
     }
 }
 
