@@ -1139,30 +1139,31 @@ __global__ __launch_bounds__(1024) void slot_sum_kernel(int64_t n, int64_t nwide
 }
 
 // dW[t] = sum of the partials of t's chunks [chunkptr[t], chunkptr[t + 1]),
-// per 64 entries (blockIdx.y): 16 slices of threads take every 16th chunk
-// (four loads in flight), the slice sums are added in slice order.
+// per 256 entries (blockIdx.y; four per lane): 16 slices of threads take
+// every 16th chunk (eight loads in flight), the slice sums are added in slice
+// order.
 template <int D>
 __global__ __launch_bounds__(1024) void chunk_sum_kernel(const float *partial, const int32_t *chunkptr, float *dW)
 {
-    constexpr int NS = 16, U = 4;
-    __shared__ float red[NS][64];
+    constexpr int NS = 16, U = 8;
+    __shared__ float4 red[NS][64];
     const int t = blockIdx.x, li = threadIdx.x % 64, c = threadIdx.x / 64;
-    const int i = blockIdx.y * 64 + li;
+    const int i = blockIdx.y * 256 + li * 4;
     const int c0 = chunkptr[t], c1 = chunkptr[t + 1];
-    float s = 0.f;
+    float4 s = zero4();
     for (int ch = c0 + c; ch < c1; ch += NS * U) {
-        float p[U];
+        float4 p[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) p[u] = ch + u * NS < c1 ? partial[(size_t)(ch + u * NS) * D * D + i] : 0.f;
+        for (int u = 0; u < U; ++u) p[u] = ch + u * NS < c1 ? ld4(partial + (size_t)(ch + u * NS) * D * D + i) : zero4();
 #pragma unroll
-        for (int u = 0; u < U; ++u) s += p[u];
+        for (int u = 0; u < U; ++u) s = add4(s, p[u]);
     }
     red[c][li] = s;
     __syncthreads();
     if (c == 0) {
-        float tot = 0.f;
-        for (int cc = 0; cc < NS; ++cc) tot += red[cc][li];
-        dW[(size_t)t * D * D + i] = tot;
+        float4 tot = zero4();
+        for (int cc = 0; cc < NS; ++cc) tot = add4(tot, red[cc][li]);
+        st4(dW + (size_t)t * D * D + i, tot);
     }
 }
 
@@ -1214,7 +1215,7 @@ rgnn_status launch_chunk_sum(const float *partial, const int32_t *chunkptr, int 
     if (R == 0) return RGNN_OK;
     {
         LaunchScope ls("chunk_sum", s);
-#define CS(D) hipLaunchKernelGGL((chunk_sum_kernel<D>), dim3((unsigned)R, D * D / 64), dim3(1024), 0, s, \
+#define CS(D) hipLaunchKernelGGL((chunk_sum_kernel<D>), dim3((unsigned)R, D * D / 256), dim3(1024), 0, s, \
                                  partial, chunkptr, dW)
         if (d == 32) CS(32);
         else if (d == 64) CS(64);
