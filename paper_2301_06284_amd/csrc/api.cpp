@@ -380,10 +380,12 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
     } else {
         // fused gather + per-(dst, rel) mean + W_r per virtual segment, then
         // the segments of each destination summed
+        // (a destination with a single virtual segment gets its row from the fused kernel)
         FusedArgs fa;
         fa.g = g; fa.h = h; fa.W = W; fa.d_in = d_in; fa.d_out = d_out; fa.T = w.T;
+        fa.out = out; fa.relu = relu_in_traversal;
         if ((st = launch_af_fused(fa, s)) != RGNN_OK) return st;
-        if ((st = launch_vseg_reduce(g, w.T, nullptr, d_out, out, 0, relu_in_traversal, s)) != RGNN_OK)
+        if ((st = launch_vseg_reduce(g, w.T, nullptr, d_out, out, 0, relu_in_traversal, s, 0, 1)) != RGNN_OK)
             return st;
     }
     if (W0) {   // virtual self-loop h_v W0, accumulated into out (then the activation)

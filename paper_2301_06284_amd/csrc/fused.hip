@@ -53,7 +53,9 @@ struct FK {
     const float *h, *W, *wsp, *vatt;
     float slope;
     float *T, *vstat;
-    float *out, *saved;          // softmax: rows of destinations with one virtual segment
+    float *out, *saved;          // rows of destinations with one virtual segment (softmax: and
+                                 // their statistics)
+    int relu;                    // mean: ReLU on those rows
     const int32_t *pos;          // sums only: output row of each virtual segment
     float *S;
 };
@@ -163,7 +165,7 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
             b.fr[h2] = srow[b.valid[h2] ? row : rb * 16];
             b.lso[h2] = (int)(b.fr[h2].e0 - te0);
             b.va[h2] = MODE == kModeSoftmax ? k.vatt[b.fr[h2].vs] : 0.f;
-            b.sid[h2] = MODE == kModeSoftmax && k.out && b.fr[h2].cnt < 0 ? b.fr[h2].cnt : b.fr[h2].vs;
+            b.sid[h2] = MODE != kModeSum && k.out && b.fr[h2].cnt < 0 ? b.fr[h2].cnt : b.fr[h2].vs;
         }
         // rows are sorted by edge count inside a relation (largest first), so
         // the block's first row is its longest
@@ -282,15 +284,16 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
             cur = nxt;
             continue;
         }
-        // A destination with one virtual segment is finished here: its softmax
-        // denominator is the segment's own sum, so the row sum is divided by it
-        // before the transform and the product is the output row (saved gets
-        // (m, s)); every other segment leaves T and (m, s) for the reduction.
+        // A destination with one virtual segment is finished here: its output
+        // row is the segment's own transformed row (softmax: its denominator is
+        // the segment's own sum, so the row sum is divided by it before the
+        // transform, and saved gets (m, s)); every other segment leaves T (and
+        // (m, s)) for the reduction.
         bool fin[2];
         float *rowp[2];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
-            fin[h2] = MODE == kModeSoftmax && cur.sid[h2] < 0;
+            fin[h2] = MODE != kModeSum && cur.sid[h2] < 0;
             rowp[h2] = (fin[h2] ? k.out + (size_t)~cur.sid[h2] * DO : k.T + (size_t)cur.sid[h2] * DO) + gp * 4;
             if (MODE != kModeSum) {
                 const float sc = MODE == kModeMean ? 1.f / (float)(fr[h2].cnt < 0 ? fr[h2].ne : fr[h2].cnt)
@@ -362,6 +365,9 @@ __global__ __launch_bounds__(64 * NWAVE) __attribute__((amdgpu_waves_per_eu(WPE)
                         const float a = __shfl(lo[t], sl), b = __shfl(hi4[t], sl);
                         v[t] = gp >= 4 ? b : a;
                     }
+                    if (MODE == kModeMean && fin[h2] && k.relu)
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) v[t] = fmaxf(v[t], 0.f);
                     if (valid[h2])
                         st4(rowp[h2] + (c0 / 2 + cc) * 32,
                             make_float4(v[0], v[1], v[2], v[3]));
@@ -420,7 +426,7 @@ rgnn_status launch_af_fused(const FusedArgs &a, hipStream_t s)
     k.ntiles = g->n_tiles_fused; k.nedges = g->E; k.src = g->dev.fused_src;
     k.h = a.h; k.W = a.W; k.wsp = a.wsp; k.vatt = a.vatt; k.slope = a.slope;
     k.T = a.T; k.vstat = a.vstat; k.S = a.S; k.pos = g->dev.vseg_pos;
-    k.out = a.out; k.saved = a.saved;
+    k.out = a.out; k.saved = a.saved; k.relu = a.relu;
     if (a.softmax && (!a.wsp || !a.vatt || !a.vstat))
         return fail(RGNN_EINVAL, "fused softmax aggregation needs wsp, vatt and vstat");
     if (a.S && a.softmax) return fail(RGNN_EINVAL, "segment means are for the mean aggregation");

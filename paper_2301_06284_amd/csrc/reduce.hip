@@ -131,12 +131,14 @@ __device__ __forceinline__ void vseg_reduce_big(int v, const int32_t *dst_vsegpt
 
 // out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
 // ReLU), out rows ldo floats apart.  Blocks [0, nbig) take the destinations of
-// big_vdst; the others a group of D/4 lanes per destination.
+// big_vdst; the others a group of D/4 lanes per destination (with skip1, none
+// for a destination with a single segment).
 template <int D>
 __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbig, const int32_t *big_vdst,
                                                           const int32_t *dst_vsegptr,
                                                           const float *T, const float *scale,
-                                                          float *out, int64_t ldo, int accumulate, int relu)
+                                                          float *out, int64_t ldo, int accumulate, int relu,
+                                                          int skip1)
 {
     if ((int64_t)blockIdx.x < nbig) {
         vseg_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, T, scale, out, ldo, accumulate, relu);
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbi
     const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
     if (v >= N) return;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    if (e - b > kBigRange) return;
+    if (e - b > kBigRange || (skip1 && e - b == 1)) return;
     float4 acc = accumulate ? ld4(out + (size_t)v * ldo + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     // rows in batches of four (all in flight together), summed in segment order
     for (int i0 = b; i0 < e; i0 += 4) {
@@ -668,7 +670,7 @@ rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s)
 }
 
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
-                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo)
+                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo, int skip1)
 {
     if (ldo == 0) ldo = d;
     if (g->N == 0) return RGNN_OK;
@@ -678,7 +680,8 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
     {
         LaunchScope ls("vseg_reduce", s);
 #define VR(D) hipLaunchKernelGGL((vseg_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
-                                 g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, ldo, accumulate, relu)
+                                 g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, ldo, accumulate, relu, \
+                                 skip1)
         if (d == 32) VR(32);
         else if (d == 64) VR(64);
         else VR(128);

@@ -290,9 +290,11 @@ rgnn_status launch_merge_partials(const rgnn_graph *g, int d, int heads, int sof
 // exp(m_i - M_seg) / Z_seg from the pieces' (max, sum) in a.vstat, to a.vscale.
 rgnn_status launch_seg_softmax_scale(const TravArgs &a, hipStream_t s);
 // out_v (+)= sum over v's virtual segments of scale[vs] * T[vs] (scale NULL: 1);
-// out rows ldo floats apart (0: d).
+// out rows ldo floats apart (0: d).  skip1: destinations with a single virtual
+// segment are left alone (the fused kernel wrote their rows).
 rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float *scale, int d,
-                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo = 0);
+                               float *out, int accumulate, int relu, hipStream_t s, int64_t ldo = 0,
+                               int skip1 = 0);
 
 // Softmax per destination finished from the per-segment (max, sum) in vstat
 // (fused order) and the segments' transformed rows summed: out_v = sum_i
@@ -318,9 +320,11 @@ struct FusedArgs {
     int softmax = 0;
     float *T = nullptr;           // [V, d_out]
     float *vstat = nullptr;       // [V, 2] (softmax), indexed by fused position
-    // softmax, optional: a destination with a single virtual segment gets its
-    // output row [N, d_out] and (max, sum) [N, 2] here, not in T and vstat
+    // optional: a destination with a single virtual segment gets its output
+    // row [N, d_out] here, not in T (softmax: and its (max, sum) [N, 2] in
+    // saved, not in vstat; mean: with ReLU when relu is set)
     float *out = nullptr, *saved = nullptr;
+    int relu = 0;
     // S given (softmax == 0): write the segment means S_vs = (1/c) sum h_u
     // themselves, at the segment's by-relation position [V, d_in], no transform
     float *S = nullptr;
