@@ -292,6 +292,15 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         });
         g->n_big_split = (int64_t)x.big_split.size();
         g->n_big_vdst = (int64_t)x.big_vdst.size();
+        // destinations a segment reduction still visits when the fused kernel
+        // finishes those with a single virtual segment (the rest up to
+        // kBigRange segments, empty ones included), in id order
+        x.reduce_dst.clear();
+        for (int64_t u = 0; u < N; ++u) {
+            const int32_t n = x.dst_vsegptr[u + 1] - x.dst_vsegptr[u];
+            if (n != 1 && n <= kBigRange) x.reduce_dst.push_back((int32_t)u);
+        }
+        g->n_reduce_dst = (int64_t)x.reduce_dst.size();
 
         // ---- out-edges: in-edge positions by (src, rel, position) ----
         {
@@ -482,7 +491,7 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     add32(&d.rel_pairtileptr, x.rel_pairtileptr);
     add32(&d.item_slot, x.item_slot); add32(&d.split_dst, x.split_dst); add32(&d.split_items, x.split_items);
     add32(&d.split_slotptr, x.split_slotptr);
-    add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst);
+    add32(&d.big_split, x.big_split); add32(&d.big_vdst, x.big_vdst); add32(&d.reduce_dst, x.reduce_dst);
     add32(&d.big_chunkptr, x.big_chunkptr); add32(&d.chunk_lo, x.chunk_lo); add32(&d.chunk_hi, x.chunk_hi);
     add32(&d.seg_vsegptr, x.seg_vsegptr); add32(&d.big_seg, x.big_seg); add32(&d.osplit, x.osplit);
     add32(&d.oitem_slot, x.oitem_slot); add32(&d.osplit_slotptr, x.osplit_slotptr);

@@ -131,14 +131,14 @@ __device__ __forceinline__ void vseg_reduce_big(int v, const int32_t *dst_vsegpt
 
 // out_v (+)= sum of the (scaled) transformed segment rows of v (then optional
 // ReLU), out rows ldo floats apart.  Blocks [0, nbig) take the destinations of
-// big_vdst; the others a group of D/4 lanes per destination (with skip1, none
-// for a destination with a single segment).
+// big_vdst; the others a group of D/4 lanes per destination: every one of the
+// N nodes, or the N listed in vlist (those the fused kernel did not finish).
 template <int D>
 __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbig, const int32_t *big_vdst,
                                                           const int32_t *dst_vsegptr,
                                                           const float *T, const float *scale,
                                                           float *out, int64_t ldo, int accumulate, int relu,
-                                                          int skip1)
+                                                          const int32_t *vlist)
 {
     if ((int64_t)blockIdx.x < nbig) {
         vseg_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, T, scale, out, ldo, accumulate, relu);
@@ -146,10 +146,11 @@ __global__ __launch_bounds__(256) void vseg_reduce_kernel(int64_t N, int64_t nbi
     }
     constexpr int G = D / 4, GPB = 256 / G;
     const int gl = threadIdx.x % G;
-    const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
-    if (v >= N) return;
+    const int64_t t = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
+    if (t >= N) return;
+    const int64_t v = vlist ? (int64_t)vlist[t] : t;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    if (e - b > kBigRange || (skip1 && e - b == 1)) return;
+    if (e - b > kBigRange) return;
     float4 acc = accumulate ? ld4(out + (size_t)v * ldo + gl * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     // rows in batches of four (all in flight together), summed in segment order
     for (int i0 = b; i0 < e; i0 += 4) {
@@ -266,8 +267,8 @@ __device__ __forceinline__ void softmax_reduce_big(int v, const int32_t *dst_vse
 // exp-weighted transformed row T_i relative to m_i; (m_i, s_i) stored at the
 // segment's fused position fpos[i]):
 //   M = max_i m_i,  Z = sum_i s_i exp(m_i - M),  out_v = sum_i exp(m_i - M) / Z * T_i
-// and saved[v] = (M, Z) ((0, 0) without in-edges); with skip1, destinations
-// with a single segment are skipped (finished by the fused kernel).  Blocks [0, nbig) take the
+// and saved[v] = (M, Z) ((0, 0) without in-edges); with vlist, only the N
+// listed destinations (those the fused kernel did not finish).  Blocks [0, nbig) take the
 // destinations of big_vdst; the others a group of D/4 lanes per destination,
 // the statistics taken over the group's lanes (fixed butterfly), the rows
 // summed in segment order.
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t 
                                                              const int32_t *dst_vsegptr,
                                                              const int32_t *fpos, const float *vstat,
                                                              const float *T, float *out, float *saved,
-                                                             float *scale, int skip1)
+                                                             float *scale, const int32_t *vlist)
 {
     if ((int64_t)blockIdx.x < nbig) {
         softmax_reduce_big<D, 256, 8>(big_vdst[blockIdx.x], dst_vsegptr, fpos, vstat, T, out, saved, scale);
@@ -285,10 +286,11 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t 
     constexpr int G = D / 4, GPB = 256 / G;
     constexpr int NE = (kBigRange + G - 1) / G;   // statistics entries per lane
     const int gl = threadIdx.x % G;
-    const int64_t v = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
-    if (v >= N) return;
+    const int64_t t = ((int64_t)blockIdx.x - nbig) * GPB + threadIdx.x / G;
+    if (t >= N) return;
+    const int64_t v = vlist ? (int64_t)vlist[t] : t;
     const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    if (e - b > kBigRange || (skip1 && e - b == 1)) return;
+    if (e - b > kBigRange) return;
     // rows in batches of four, two batches in flight; the first goes out before
     // the statistics are gathered (the rows do not depend on them)
     float4 ta[4], tb[4];
@@ -676,12 +678,15 @@ rgnn_status launch_vseg_reduce(const rgnn_graph *g, const float *T, const float 
     if (g->N == 0) return RGNN_OK;
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "reduce: d must be 32, 64 or 128");
     const int64_t nbig = g->n_big_vdst;
-    const unsigned nb = (unsigned)nbig + blocks_for(g->N, 256 / (d / 4));
+    const int32_t *vlist = skip1 ? g->dev.reduce_dst : nullptr;
+    const int64_t n = skip1 ? g->n_reduce_dst : g->N;
+    const unsigned nb = (unsigned)nbig + blocks_for(n, 256 / (d / 4));
+    if (nb == 0) return RGNN_OK;
     {
         LaunchScope ls("vseg_reduce", s);
-#define VR(D) hipLaunchKernelGGL((vseg_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
+#define VR(D) hipLaunchKernelGGL((vseg_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, n, nbig, \
                                  g->dev.big_vdst, g->dev.dst_vsegptr, T, scale, out, ldo, accumulate, relu, \
-                                 skip1)
+                                 vlist)
         if (d == 32) VR(32);
         else if (d == 64) VR(64);
         else VR(128);
@@ -698,12 +703,15 @@ rgnn_status launch_softmax_reduce(const rgnn_graph *g, const float *vstat, const
     if (d != 32 && d != 64 && d != 128) return fail(RGNN_EUNSUPPORTED, "softmax reduce: d must be 32, 64 or 128");
     if (g->n_big_vdst && !scale) return fail(RGNN_EINVAL, "softmax reduce needs its scale scratch");
     const int64_t nbig = g->n_big_vdst;
-    const unsigned nb = (unsigned)nbig + blocks_for(g->N, 256 / (d / 4));
+    const int32_t *vlist = skip1 ? g->dev.reduce_dst : nullptr;
+    const int64_t n = skip1 ? g->n_reduce_dst : g->N;
+    const unsigned nb = (unsigned)nbig + blocks_for(n, 256 / (d / 4));
+    if (nb == 0) return RGNN_OK;
     {
         LaunchScope ls("softmax_reduce", s);
-#define SR(D) hipLaunchKernelGGL((softmax_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, g->N, nbig, \
+#define SR(D) hipLaunchKernelGGL((softmax_reduce_kernel<D>), dim3(nb), dim3(256), 0, s, n, nbig, \
                                  g->dev.big_vdst, g->dev.dst_vsegptr, g->dev.vseg_fpos, vstat, T, out, \
-                                 saved, scale, skip1)
+                                 saved, scale, vlist)
         if (d == 32) SR(32);
         else if (d == 64) SR(64);
         else SR(128);

@@ -72,6 +72,7 @@ struct HostIndex {
     std::vector<int32_t> split_order;   // indices into split_dst, most slots first [n_split]
     std::vector<int32_t> big_chunkptr;  // chunks of each big split [n_big_split + 1]
     std::vector<int32_t> chunk_lo, chunk_hi;   // slot range of each chunk [n_big_chunks]
+    std::vector<int32_t> reduce_dst;  // destinations with 0 or 2..kBigRange virtual segments
     std::vector<int32_t> big_vdst;    // destinations with > kBigRange virtual segments,
                                       // largest first
     std::vector<int32_t> seg_vsegptr;  // first virtual segment of each (dst, rel) segment [U_dst+1]
@@ -127,7 +128,7 @@ struct DeviceIndex {
     int32_t *vsegdst_byrel = nullptr, *rel_chunkptr = nullptr, *rel_pairtileptr = nullptr;
     Item *items = nullptr;
     int32_t *item_slot = nullptr, *split_dst = nullptr, *split_slotptr = nullptr, *split_items = nullptr;
-    int32_t *big_split = nullptr, *big_vdst = nullptr;
+    int32_t *big_split = nullptr, *big_vdst = nullptr, *reduce_dst = nullptr;
     int32_t *big_chunkptr = nullptr, *chunk_lo = nullptr, *chunk_hi = nullptr;
     int32_t *seg_vsegptr = nullptr, *big_seg = nullptr, *osplit = nullptr;
     int32_t *oitem_slot = nullptr, *osplit_slotptr = nullptr;
@@ -167,7 +168,7 @@ struct rgnn_graph {
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
-    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0;
+    int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0, n_reduce_dst = 0;
     int64_t n_oitems = 0, n_osplit = 0, n_oslots = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
     int64_t n_vpairs = 0, n_tiles_vpairs = 0;
     int64_t n_split_wide = 0, n_osplit_wide = 0;   // split lists' entries with > kWaveSlots slots
