@@ -113,6 +113,7 @@ struct BK {
     float *ay;       // [E, 2]  per sorted in-edge: (alpha, Y); pieces hold (signed alpha, dalpha) in between
     float *ysum;     // [V]     sum of Y per segment (by-relation order)
     float *dh;       // [N, D]  destination terms written (acc_dh: added) here
+    float *dpart;    // [slots, D] a split destination's term, per piece (summed after)
     int acc_dh;
     const int32_t *split_items;   // PHASE 1 without SEG runs over these items only
     int64_t n_split_items;
@@ -138,12 +139,13 @@ struct BStage {
 // PHASE 0: every item.  Whole destinations run all passes; pieces of split
 //          destinations run pass 1, leave their part of (S', Z') in ssum and park
 //          (signed q, dalpha) in ay.
-// PHASE 1: pieces of split destinations only: pass 2 with the merged s_v (their
-//          destination term is summed by split_dst_term_kernel).
+// PHASE 1: pieces of split destinations only: pass 2 with the merged s_v and
+//          pass 3 for their own segments, written to the piece's slot (the slots
+//          of a destination are summed afterwards).
 // SEG (softmax per (dst, rel) segment): PHASE 0 runs pass 1 for every item,
 //          writing each vseg's part of (S', Z') to svs and parking (q, dalpha);
 //          once the parts are summed per segment, PHASE 1 runs passes 2 and 3
-//          for every item (pass 3 for whole destinations only).
+//          for every item (pass 3 of a piece to its slot).
 template <int D, int PHASE, bool SEG>
 __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
 {
@@ -334,12 +336,19 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
     }
     __syncthreads();
     // pass 3: destination term dh_v = sum over v's segments of ysum * wt'_r,
-    // streaming the wt' rows of the item's segments in ping-pong batches
-    if (fin && slot < 0 && (PHASE == 0 || SEG)) {
+    // streaming the wt' rows of the item's segments in ping-pong batches (a
+    // piece of a split destination writes its segments' share to its slot)
+    if (fin && (slot < 0 ? PHASE == 0 || SEG : PHASE == 1)) {
         float4 acc = zero4();
         int j = 0;
         auto flush_to = [&](int jn) {   // finish destinations [j, jn)
             while (j < jn) {
+                if (slot >= 0) {
+                    st4(k.dpart + (size_t)slot * D + gl * 4, acc);
+                    acc = zero4();
+                    ++j;
+                    continue;
+                }
                 float *p = k.dh + (size_t)(dst0 + j) * D + gl * 4;
                 st4(p, k.acc_dh ? add4(acc, ld4(p)) : acc);
                 acc = zero4();
@@ -380,38 +389,6 @@ __global__ __launch_bounds__(item_threads(D)) void bwd_traverse_kernel(BK k)
     }
 }
 
-__global__ __launch_bounds__(256) void merge_s_kernel(int64_t n_split, const int32_t *split_dst,
-                                                      const int32_t *split_slotptr,
-                                                      const float2 *ssum, float2 *sv)
-{
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= n_split) return;
-    if (split_slotptr[i + 1] - split_slotptr[i] > kBigRange) return;
-    float2 s = make_float2(0.f, 0.f);
-    for (int sl = split_slotptr[i]; sl < split_slotptr[i + 1]; ++sl) s = add2(s, ssum[sl]);
-    sv[split_dst[i]] = s;
-}
-
-// One workgroup per split destination with many partials; thread sums are
-// added in thread order.
-__global__ __launch_bounds__(256) void merge_s_big_kernel(const int32_t *big_split,
-                                                          const int32_t *split_dst,
-                                                          const int32_t *split_slotptr,
-                                                          const float2 *ssum, float2 *sv)
-{
-    __shared__ float2 part[256];
-    const int i = big_split[blockIdx.x];
-    float2 s = make_float2(0.f, 0.f);
-    for (int sl = split_slotptr[i] + (int)threadIdx.x; sl < split_slotptr[i + 1]; sl += 256) s = add2(s, ssum[sl]);
-    part[threadIdx.x] = s;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float2 t = make_float2(0.f, 0.f);
-        for (int j = 0; j < 256; ++j) t = add2(t, part[j]);
-        sv[split_dst[i]] = t;
-    }
-}
-
 // Per-segment softmax: (S', Z') of a (dst, rel) segment cut into several
 // vsegs is the sum of its vsegs' parts (in vseg order), written back to each.
 __global__ __launch_bounds__(256) void merge_seg_s_kernel(int64_t U, const int32_t *seg_vsegptr, float2 *svs)
@@ -447,50 +424,6 @@ __global__ __launch_bounds__(256) void merge_seg_s_big_kernel(const int32_t *big
     for (int vs = b + (int)threadIdx.x; vs < e; vs += 256) svs[vs] = tot;
 }
 
-// Destination term of a split destination (its segments span several work
-// items): one workgroup of NTH threads per destination, segments strided over
-// 16-lane groups (U in flight) and combined in group order.  Destinations
-// split over more than kBigRange items (the hubs) take 1024-thread
-// workgroups in a launch of their own (BIG).
-template <int D, int NTH, int U, bool BIG>
-__global__ __launch_bounds__(NTH) void split_dst_term_kernel(const int32_t *big_split, const int32_t *split_slotptr,
-                                                             const int32_t *split_dst, const int32_t *dst_vsegptr,
-                                                             const int32_t *vseg_rel, const int32_t *vseg_pos,
-                                                             const float *ysum, const float *wtp, float *dh,
-                                                             int acc_dh)
-{
-    constexpr int G = D / 4, NG = NTH / G;
-    __shared__ float4 part[NG][G];
-    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
-    const int i = BIG ? big_split[blockIdx.x] : (int)blockIdx.x;
-    if (!BIG && split_slotptr[i + 1] - split_slotptr[i] > kBigRange) return;
-    const int v = split_dst[i];
-    const int b = dst_vsegptr[v], e = dst_vsegptr[v + 1];
-    float4 acc = zero4();
-    for (int vs0 = b + gi; vs0 < e; vs0 += U * NG) {
-        float4 w[U];
-        float y[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int vs = vs0 + u * NG;
-            if (vs < e) {
-                w[u] = ld4(wtp + (size_t)vseg_rel[vs] * D + gl * 4);
-                y[u] = ysum[vseg_pos[vs]];
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (vs0 + u * NG < e) acc = lin4(acc, 1.f, w[u], y[u]);
-    }
-    part[gi][gl] = acc;
-    __syncthreads();
-    if (gi == 0) {
-        float4 t = zero4();
-        for (int j = 0; j < NG; ++j) t = add4(t, part[j][gl]);
-        float *p = dh + (size_t)v * D + gl * 4;
-        st4(p, acc_dh ? add4(t, ld4(p)) : t);
-    }
-}
 
 // ---------------------------------------------------------------- source-major traversal
 struct SK {
@@ -943,7 +876,7 @@ __global__ void zero_kernel(float *p, int64_t n)
 inline size_t pad256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct BwdWs {
-    float *wsp, *wtp, *vatt, *dS, *Sa, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec, *part;
+    float *wsp, *wtp, *vatt, *dS, *Sa, *ay, *ysum, *ypair, *pvec, *pws, *pwt, *partial, *yvec, *part, *dpart;
     float2 *ssum, *sv, *svs;
 };
 
@@ -975,6 +908,7 @@ size_t bwd_layout(const rgnn_graph *g, int D, void *base, BwdWs *w)
     x.partial = take(nchunks * D * D);
     x.yvec = take(nchunks * D);
     x.part = take((size_t)std::max<int64_t>(g->n_oslots, 1) * D);
+    x.dpart = take((size_t)std::max<int64_t>(g->n_slots, 1) * D);
     if (w) *w = x;
     return off;
 }
@@ -987,19 +921,6 @@ hipError_t zero(float *p, int64_t n, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int D>
-void launch_split_dst_term(const rgnn_graph *g, const float *ysum, const float *wtp, float *dh, int acc_dh,
-                           hipStream_t s)
-{
-    const DeviceIndex &x = g->dev;
-    hipLaunchKernelGGL((split_dst_term_kernel<D, 256, 4, false>), dim3((unsigned)g->n_split), dim3(256), 0, s,
-                       nullptr, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos, ysum, wtp, dh,
-                       acc_dh);
-    if (g->n_big_split)
-        hipLaunchKernelGGL((split_dst_term_kernel<D, 1024, 8, true>), dim3((unsigned)g->n_big_split), dim3(1024),
-                           0, s, x.big_split, x.split_slotptr, x.split_dst, x.dst_vsegptr, x.vseg_rel, x.vseg_pos,
-                           ysum, wtp, dh, acc_dh);
-}
 
 // 64 x 64 tiles of the D x D outer products
 constexpr unsigned outer_tiles(int D) { return D > 64 ? (unsigned)(D / 64) * (D / 64) : 1u; }
@@ -1259,7 +1180,7 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
     k.in_src = g->dev.in_src; k.h = h; k.wsp = w.wsp; k.saved = saved; k.dS = w.dS;
     k.vatt = w.vatt; k.sv_in = w.sv; k.slope = slope; k.Sa = w.Sa; k.ssum = w.ssum; k.ay = w.ay;
     k.ysum = w.ysum; k.vseg_seg = g->dev.vseg_seg; k.svs = w.svs; k.acc_dh = hd.acc;
-    k.split_items = g->dev.split_items; k.n_split_items = g->n_split_items;
+    k.split_items = g->dev.split_items; k.n_split_items = g->n_split_items; k.dpart = w.dpart;
     if (g->n_items && per_seg) {
         constexpr int GPB = item_threads(D) / (D / 4);
         const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
@@ -1283,11 +1204,11 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
             hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, true>), grid, dim3(item_threads(D)), 0, s, k);
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
-        if (g->n_split) {
-            LaunchScope ls("rgat_bwd_split_dst_term", s);
-            launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, hd.acc, s);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
+        // split destinations: their pieces' shares of the destination term summed
+        if ((st = launch_slot_sum(g->n_split, g->n_split_wide, g->dev.split_order, g->dev.split_dst,
+                                  g->dev.split_slotptr, w.dpart, dh, D, hd.acc != 0, "rgat_bwd_split_dst_term",
+                                  s)) != RGNN_OK)
+            return st;
     } else if (g->n_items) {
         constexpr int GPB = item_threads(D) / (D / 4);
         const dim3 grid((unsigned)((g->n_items + GPB - 1) / GPB));
@@ -1297,29 +1218,21 @@ rgnn_status rgat_backward_d(const rgnn_graph *g, const float *h, const float *W,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
         if (g->n_split) {
-            {
-                LaunchScope ls("rgat_bwd_merge_s", s);
-                hipLaunchKernelGGL(merge_s_kernel, dim3((unsigned)((g->n_split + 255) / 256)), dim3(256), 0,
-                                   s, g->n_split, g->dev.split_dst, g->dev.split_slotptr, w.ssum, w.sv);
-            }
-            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s launch");
-            if (g->n_big_split) {
-                LaunchScope ls("rgat_bwd_merge_s_big", s);
-                hipLaunchKernelGGL(merge_s_big_kernel, dim3((unsigned)g->n_big_split), dim3(256), 0, s,
-                                   g->dev.big_split, g->dev.split_dst, g->dev.split_slotptr, w.ssum, w.sv);
-            }
-            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "merge_s_big launch");
+            // (S', Z') of split destinations: their pieces' parts summed
+            if ((st = launch_slot_sum(g->n_split, g->n_split_wide, g->dev.split_order, g->dev.split_dst,
+                                      g->dev.split_slotptr, reinterpret_cast<const float *>(w.ssum),
+                                      reinterpret_cast<float *>(w.sv), 2, false, "rgat_bwd_merge_s", s)) != RGNN_OK)
+                return st;
             {
                 LaunchScope ls("rgat_bwd_traverse_split", s);
                 const dim3 sgrid((unsigned)((g->n_split_items + GPB - 1) / GPB));
                 hipLaunchKernelGGL((bwd_traverse_kernel<D, 1, false>), sgrid, dim3(item_threads(D)), 0, s, k);
             }
             if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "rgat_bwd launch");
-            {
-                LaunchScope ls("rgat_bwd_split_dst_term", s);
-                launch_split_dst_term<D>(g, w.ysum, w.wtp, dh, hd.acc, s);
-            }
-            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "split_dst_term launch");
+            if ((st = launch_slot_sum(g->n_split, g->n_split_wide, g->dev.split_order, g->dev.split_dst,
+                                      g->dev.split_slotptr, w.dpart, dh, D, hd.acc != 0, "rgat_bwd_split_dst_term",
+                                      s)) != RGNN_OK)
+                return st;
         }
     }
     // dh += source terms (dh holds the destination terms); Y sums per compact pair
