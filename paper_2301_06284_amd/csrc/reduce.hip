@@ -349,7 +349,8 @@ __global__ __launch_bounds__(256) void softmax_reduce_kernel(int64_t N, int64_t 
 
 // ---------------------------------------------------------------- merges
 // Combine the partials of destinations split over several items, in slot
-// order.  softmax: partial = (m, s) per head then acc[D]; else acc only.
+// order (all maxima, then the records eight at a time in flight).  softmax:
+// partial = (m, s) per head then acc[D]; else acc only.
 template <int D, int H, bool SOFTMAX>
 __global__ __launch_bounds__(256) void merge_kernel(int64_t n_split, const int32_t *split_dst,
                                                     const int32_t *split_slotptr,
@@ -366,16 +367,31 @@ __global__ __launch_bounds__(256) void merge_kernel(int64_t n_split, const int32
     const int b = split_slotptr[i], e = split_slotptr[i + 1];
     if (e - b > kBigRange) return;
     const int head = gl / LH;
+    constexpr int U = 8;   // records in flight
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (SOFTMAX) {
+        // every slot's maximum at once, then the records in batches of U
         float M = -INFINITY;
-        for (int sl = b; sl < e; ++sl) M = fmaxf(M, partial[(size_t)sl * REC + head * 2]);
+#pragma unroll
+        for (int j = 0; j < kBigRange; ++j)
+            M = fmaxf(M, b + j < e ? partial[(size_t)(b + j) * REC + head * 2] : -INFINITY);
         float Z = 0.f;
-        for (int sl = b; sl < e; ++sl) {
-            const float *pr = partial + (size_t)sl * REC;
-            const float c = __expf(pr[head * 2] - M);
-            Z += pr[head * 2 + 1] * c;
-            acc = lin4(acc, 1.f, ld4(pr + OFF + gl * 4), c);
+        for (int sl0 = b; sl0 < e; sl0 += U) {
+            float4 a[U];
+            float2 ms[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const float *pr = partial + (size_t)(sl0 + u < e ? sl0 + u : sl0) * REC;
+                a[u] = ld4(pr + OFF + gl * 4);
+                ms[u] = make_float2(pr[head * 2], pr[head * 2 + 1]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (sl0 + u >= e) break;
+                const float c = __expf(ms[u].x - M);
+                Z += ms[u].y * c;
+                acc = lin4(acc, 1.f, a[u], c);
+            }
         }
         acc = scale4(acc, Z > 0.f ? 1.f / Z : 0.f);
         if (saved && gl % LH == 0) {
@@ -383,7 +399,16 @@ __global__ __launch_bounds__(256) void merge_kernel(int64_t n_split, const int32
             saved[((size_t)v * H + head) * 2 + 1] = Z;
         }
     } else {
-        for (int sl = b; sl < e; ++sl) acc = add4(acc, ld4(partial + (size_t)sl * REC + OFF + gl * 4));
+        for (int sl0 = b; sl0 < e; sl0 += U) {
+            float4 a[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) a[u] = ld4(partial + (size_t)(sl0 + u < e ? sl0 + u : sl0) * REC + OFF + gl * 4);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (sl0 + u >= e) break;
+                acc = add4(acc, a[u]);
+            }
+        }
     }
     st4(out + (size_t)v * D + gl * 4, relu ? relu4(acc) : acc);
 }
