@@ -37,10 +37,12 @@ METRIC = "edges/sec per RGNN layer fwd (RGAT, HGT) on 1 MI355X; achieved HBM GB/
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
+    # 100 timed steps of the headline layer (~60 ms): a mean that a few slow
+    # steps do not move
+    p.add_argument("--steps", type=int, default=100)
     # the first ~30 ms of continuous work run slower (the device's clocks
-    # ramp up): 40 warm-up steps of the headline layer cover that
-    p.add_argument("--warmup", type=int, default=40)
+    # ramp up): 50 warm-up steps of the headline layer cover that
+    p.add_argument("--warmup", type=int, default=50)
     p.add_argument("--only", choices=["headline", "all"], default="all",
                    help="headline: time only the RGAT workload of the headline")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline leg")
