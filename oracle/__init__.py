@@ -53,7 +53,7 @@ def _load():
                                             vp, vp, vp, vp, vp, vp, vp, f64, i32, i32, i64, vp,
                                             vp]
         _lib.oracle_rgat_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
-                                              vp, vp, f64, i32, vp, vp, vp, vp, vp, vp, vp]
+                                              vp, vp, f64, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         _lib.oracle_rgcn_backward.argtypes = [i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp,
                                               i32, vp, vp, vp, vp, vp, vp]
         _lib.oracle_hgt_backward.argtypes = [i64, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp,
@@ -158,25 +158,61 @@ def hgt_forward(g, h, Wk, Wq, Wv, Wa, Watt, Wmsg, mu, heads, att_scale=None,
 
 
 def rgat_backward(g, h, W, w_src, w_dst, grad_out, heads=1, neg_slope=0.2, scope=0,
-                  node_mask=None, rel_mask=None):
+                  node_mask=None, rel_mask=None, kink_flip=None, want_Y=False):
     """Gradients of L = sum(out * grad_out) of the RGAT layer with the softmax
     over each destination's in-edges (scope 0) or over its in-edges of one
     relation (scope 1).  Returns (dh, dW, dw_src, dw_dst); entries outside the
-    masks are zero."""
+    masks are zero.  kink_flip: None or a boolean [E, heads] array; where set,
+    the leaky ReLU's derivative is taken from the other side of its kink (the
+    derivative at y = 0 is one-sided: either side is a correct result where y
+    lies within rounding of zero, see rgat_preactivations).  want_Y: also
+    return Y = dL/dy [E, heads] (NaN for edges whose destination the masks
+    left unvisited)."""
     h, W, w_src, w_dst, G = map(_f32, (h, W, w_src, w_dst, grad_out))
     src, dst, rel = _i32(g["src"]), _i32(g["dst"]), _i32(g["rel"])
     N, R = g["N"], g["R"]
     d_in, d_out = W.shape[1], W.shape[2]
     nm = None if node_mask is None else np.ascontiguousarray(node_mask, np.uint8)
     rm = None if rel_mask is None else np.ascontiguousarray(rel_mask, np.uint8)
+    kf = None
+    if kink_flip is not None:
+        kf = np.ascontiguousarray(np.asarray(kink_flip, bool).reshape(g["E"], heads), np.uint8)
     dh = np.zeros((N, d_in)); dW = np.zeros((R, d_in, d_out))
     dws = np.zeros((R, d_out)); dwd = np.zeros((R, d_out))
+    Y = np.empty((g["E"], heads)) if want_Y else None
     rc = _load().oracle_rgat_backward(N, g["E"], R, d_in, d_out, heads, _p(src), _p(dst),
                                       _p(rel), _p(h), _p(W), _p(w_src), _p(w_dst),
-                                      float(neg_slope), int(scope), _p(G), _p(nm), _p(rm), _p(dh), _p(dW),
-                                      _p(dws), _p(dwd))
+                                      float(neg_slope), int(scope), _p(G), _p(nm), _p(rm), _p(kf), _p(dh),
+                                      _p(dW), _p(dws), _p(dwd), _p(Y))
     _check(rc, "rgat_backward")
-    return dh, dW, dws, dwd
+    return (dh, dW, dws, dwd, Y) if want_Y else (dh, dW, dws, dwd)
+
+
+def rgat_preactivations(g, h, W, w_src, w_dst, heads=1, chunk=1 << 20):
+    """The RGAT attention logits before the leaky ReLU, edge by edge (Listing 1,
+    Section 3.2.1): y_e,k = (h_u W_r)[k] . w_src[r][k] + (h_v W_r)[k] . w_dst[r][k]
+    over head k's columns, in fp64.  Also returns each logit's rounding scale,
+    sum_j |(h_u W_r)_j w_src_j| + |(h_v W_r)_j w_dst_j| over the same columns:
+    an fp32 evaluation can put y on either side of zero where |y| is within a
+    small multiple of 2^-24 of that scale.  Returns (y, scale), both [E, heads]."""
+    src, dst, rel = (np.asarray(g[k]) for k in ("src", "dst", "rel"))
+    E = len(src)
+    h = np.asarray(h, np.float64)
+    d_out = W.shape[2]
+    dk = d_out // heads
+    y = np.zeros((E, heads)); scale = np.zeros((E, heads))
+    for r in range(W.shape[0]):
+        Wr = np.asarray(W[r], np.float64)
+        ws, wd = np.asarray(w_src[r], np.float64), np.asarray(w_dst[r], np.float64)
+        er = np.nonzero(rel == r)[0]
+        for c0 in range(0, len(er), chunk):
+            e = er[c0:c0 + chunk]
+            ps, pd = (h[src[e]] @ Wr) * ws, (h[dst[e]] @ Wr) * wd
+            for k in range(heads):
+                cols = slice(k * dk, (k + 1) * dk)
+                y[e, k] = ps[:, cols].sum(axis=1) + pd[:, cols].sum(axis=1)
+                scale[e, k] = np.abs(ps[:, cols]).sum(axis=1) + np.abs(pd[:, cols]).sum(axis=1)
+    return y, scale
 
 
 def rgcn_backward(g, h, W, W0, grad_out, relu=False, node_mask=None, rel_mask=None,

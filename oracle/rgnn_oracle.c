@@ -450,6 +450,14 @@ int oracle_hgt_forward(int64_t N, int64_t E, int32_t R, int32_t T, int32_t d,
  * rel_mask  (nullable): compute dW, dw_src, dw_dst only for those relations.
  * Entries outside the masks are left at zero.  Only destinations that feed a
  * requested entry are visited.
+ * kink_flip (nullable, [E, H] by edge id): the leaky ReLU has no derivative at
+ * y = 0; where kink_flip[e * H + k] != 0 the derivative is taken from the
+ * other side of the kink (1 for y <= 0, slope for y > 0).  A caller flags the
+ * edges whose pre-activation lies within rounding of zero, where an fp32
+ * evaluation may land on either side and both one-sided derivatives are
+ * correct results.
+ * Y_out (nullable, [E, H] by edge id): receives Y_e,k = dL/dy_e,k of every edge
+ * whose destination was visited (NaN for the others).
  *
  * Every sum over edges runs in one fixed order, the "global edge order":
  * destinations in increasing id, each destination's in-edges in increasing
@@ -472,6 +480,7 @@ typedef struct {
     double slope;
     const in_lists *a;
     double *AL, *YY;   /* [E, H] alpha and Y by edge id */
+    const uint8_t *flip;   /* [E, H] or NULL: derivative from the other side of the kink */
 } rgat_bwd_ctx;
 
 typedef struct {
@@ -560,7 +569,8 @@ static int rgat_bwd_dst(const rgat_bwd_ctx *c, int64_t v, int inner, rgat_bwd_sc
             const double y = Y[q * H + k];
             const double dz = al[q * H + k] * (dal[q * H + k] - sv[GRP(q) + k]);
             c->AL[e * H + k] = al[q * H + k];
-            c->YY[e * H + k] = dz * (y > 0.0 ? 1.0 : c->slope);
+            const int pos = (y > 0.0) != (c->flip && c->flip[e * H + k]);
+            c->YY[e * H + k] = dz * (pos ? 1.0 : c->slope);
         }
     }
 #undef GRP
@@ -598,8 +608,8 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
                          const int32_t *rel, const float *h, const float *W,
                          const float *w_src, const float *w_dst, double neg_slope,
                          int32_t scope, const float *G, const uint8_t *node_mask,
-                         const uint8_t *rel_mask, double *dh, double *dW, double *dw_src,
-                         double *dw_dst)
+                         const uint8_t *rel_mask, const uint8_t *kink_flip, double *dh, double *dW,
+                         double *dw_src, double *dw_dst, double *Y_out)
 {
     if (check_coo(N, E, R, src, dst, rel) || d_in <= 0 || d_in > 512 || d_out <= 0 ||
         d_out > 512 || heads <= 0 || d_out % heads)
@@ -649,7 +659,7 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
         free(rf); free(of);
     }
     rgat_bwd_ctx c = {N, E, R, d_in, d_out, H, scope, src, dst, rel, h, W, w_src, w_dst, G,
-                      neg_slope, &a, AL, YY};
+                      neg_slope, &a, AL, YY, kink_flip};
     /* stage A */
     if (!err) {
 #pragma omp parallel reduction(| : err)
@@ -667,6 +677,10 @@ int oracle_rgat_backward(int64_t N, int64_t E, int32_t R, int32_t d_in, int32_t 
             if (need[v] && a.ptr[v + 1] - a.ptr[v] > BIG_ROW && rgat_bwd_dst(&c, v, 1, &sc)) err = 1;
         rgat_bwd_scratch_free(&sc);
     }
+    if (!err && Y_out)
+        for (int64_t e = 0; e < E; ++e)
+            for (int k = 0; k < H; ++k)
+                Y_out[e * H + k] = need[dst[e]] ? YY[e * H + k] : NAN;
     /* stage B: jobs (relation, block of dW rows) then (relation, block of dw columns) */
     if (!err) {
         const int nbi = (d_in + RGAT_BWD_ROWS - 1) / RGAT_BWD_ROWS;

@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 import workloads
-from helpers import TOL, Runner, row_err
+from helpers import TOL, Runner, rgat_backward_ref, row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +62,42 @@ def test_segment_gemm(K, Nc):
         rows = np.arange(type_ptr[t], type_ptr[t + 1])
         ref[scatter[rows]] = X[gather[rows]].astype(np.float64) @ W[t].astype(np.float64)
     assert row_err(Y.cpu().numpy(), ref) <= TOL
+
+
+@pytest.mark.parametrize("K,Nc", [(32, 32), (64, 64), (128, 128), (64, 128), (128, 64)])
+def test_segment_gemm_fp32_grade(K, Nc):
+    """Every output entry within a few fp32 unit roundoffs of the exact product,
+    relative to sum_k |x_k w_k| (a sequential fp32 dot product is bounded by K of
+    them): the 64-deep shapes, whose products run on split bf16 pieces, must be
+    as accurate as the fp32 MFMA ones.  Rows span twelve decades of scale, and
+    a plain bf16 (or two-piece bf16) product would miss the bound by far."""
+    import torch
+    from paper_2301_06284_amd import rgnn
+    rng = np.random.default_rng(1000 + K + Nc)
+    type_ptr = np.array([0, 700, 701, 1500, 2048], np.int64)
+    M, T = int(type_ptr[-1]), len(type_ptr) - 1
+    X = (rng.standard_normal((M, K)) * 10.0 ** rng.uniform(-6, 6, (M, 1))).astype(np.float32)
+    W = (rng.standard_normal((T, K, Nc)) * 10.0 ** rng.uniform(-3, 3, (T, 1, Nc))).astype(np.float32)
+    gather = np.arange(M, dtype=np.int32)
+    scatter = rng.permutation(M).astype(np.int32)
+    print(f"segment_gemm fp32 grade {K}x{Nc}", flush=True)
+    dev = torch.device("cuda:0")
+    Y = torch.zeros(M, Nc, device=dev)
+    ws = torch.empty(rgnn.segment_gemm_workspace_size(M, T), dtype=torch.uint8, device=dev)
+    rgnn.segment_gemm(torch.from_numpy(X).to(dev), torch.from_numpy(gather).to(dev), type_ptr,
+                      torch.from_numpy(W).to(dev), Y, torch.from_numpy(scatter).to(dev), ws, K, Nc)
+    torch.cuda.synchronize()
+    got = Y.cpu().numpy().astype(np.float64)
+    u = 2.0 ** -24
+    worst = 0.0
+    for t in range(T):
+        rows = np.arange(type_ptr[t], type_ptr[t + 1])
+        x, w = X[rows].astype(np.float64), W[t].astype(np.float64)
+        exact = x @ w
+        scale = np.abs(x) @ np.abs(w)
+        worst = max(worst, float((np.abs(got[scatter[rows]] - exact) / (u * scale)).max()))
+    print(f"  max error / (u sum |x w|) = {worst:.2f}", flush=True)
+    assert worst <= 8.0
 
 
 @pytest.mark.parametrize("kind", KINDS)
@@ -343,7 +379,7 @@ def test_rgat_backward_small(kind):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward()
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    dh, dW, dws, dwt = rgat_backward_ref(g, t)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
@@ -361,8 +397,7 @@ def test_rgat_backward_per_relation_softmax(kind):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(scope=1)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
-                                            scope=1)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, scope=1)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     # a relation whose segments each repeat one (src, rel) pair has uniform
@@ -391,8 +426,7 @@ def test_rgat_per_relation_softmax_multihead(kind, heads):
         assert np.isfinite(sv).all() and (sv[..., 1] >= 1 - 1e-5).all()
     gh, gW, gs, gt = run.rgat_backward(heads=heads, scope=1)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
-                                            heads=heads, scope=1)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, heads=heads, scope=1)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64), cancel_floor=1e-6) <= TOL
@@ -412,8 +446,7 @@ def test_rgat_backward_per_relation_softmax_hub_segments():
     assert np.isfinite(sv).all() and (sv[..., 1] >= 1 - 1e-5).all()
     gh, gW, gs, gt = run.rgat_backward(scope=1)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
-                                            scope=1)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, scope=1)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     # a relation whose segments each repeat one (src, rel) pair has uniform
@@ -438,8 +471,7 @@ def test_rgat_backward_hidden_sizes(kind, d, heads, scope):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(heads=heads, scope=scope)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
-                                            heads=heads, scope=scope)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, heads=heads, scope=scope)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, d), dW.reshape(-1, d), cancel_floor=1e-6) <= TOL
@@ -476,8 +508,7 @@ def test_rgat_backward_multihead(kind, heads):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(heads=heads)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"],
-                                            heads=heads)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, heads=heads)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
@@ -509,7 +540,7 @@ def test_rgat_backward_multihead_mid_size(d, heads, kind):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(heads=heads)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=heads)
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, heads=heads)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, d), dW.reshape(-1, d)) <= TOL
@@ -528,7 +559,7 @@ def test_rgat_backward_mid_size_one_head(plan):
     run = Runner(g, t)
     gh, gW, gs, gt = run.rgat_backward(heads=1, plan=plan)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    dh, dW, dws, dwt = rgat_backward_ref(g, t)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, 64), dW.reshape(-1, 64)) <= TOL
@@ -548,7 +579,7 @@ def test_backward_mid_size_source_hub(d):
     gh, gW, gs, gt = run.rgat_backward(heads=1)
     rh, rW, rW0 = run.rgcn_backward(W0=True, relu=False)
     run.close()
-    dh, dW, dws, dwt = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"])
+    dh, dW, dws, dwt = rgat_backward_ref(g, t)
     isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
     assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
     assert row_err(gW.reshape(-1, d), dW.reshape(-1, d)) <= TOL

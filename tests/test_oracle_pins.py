@@ -361,7 +361,10 @@ def test_hgt_zero_attention_weight_is_mean():
 
 
 # ---------------------------------------------------------------- RGAT backward
-def rgat_torch_dense(g, h, W, ws, wt, H, slope, scope=0):
+def rgat_torch_dense(g, h, W, ws, wt, H, slope, scope=0, flip=None):
+    """flip: None or a boolean [R, N (destination), N (source), H] tensor: where
+    set, the leaky ReLU keeps its value but differentiates with the slope of
+    the other side of its kink."""
     R, N = g["R"], g["N"]
     d_out = W.shape[2]
     dh = d_out // H
@@ -369,7 +372,12 @@ def rgat_torch_dense(g, h, W, ws, wt, H, slope, scope=0):
     M = torch.einsum("ui,rij->ruj", h, W).reshape(R, N, H, dh)
     S = torch.einsum("ruhc,rhc->ruh", M, ws.reshape(R, H, dh))
     Tt = torch.einsum("rvhc,rhc->rvh", M, wt.reshape(R, H, dh))
-    Z = torch.nn.functional.leaky_relu(S[:, None] + Tt[:, :, None], slope)
+    Y = S[:, None] + Tt[:, :, None]
+    Z = torch.nn.functional.leaky_relu(Y, slope)
+    if flip is not None:
+        one = torch.ones_like(Y)
+        d = torch.where((Y > 0) != flip, one, slope * one).detach()
+        Z = Z.detach() + Y * d - (Y * d).detach()
     mask = (A > 0)[..., None].expand_as(Z)
     dims = (0, 2) if scope == 0 else (2,)   # per destination, or per (relation, destination)
     mx = torch.where(mask, Z, torch.tensor(-torch.inf, dtype=Z.dtype)).amax(dim=dims, keepdim=True)
@@ -412,6 +420,44 @@ def test_rgat_backward_per_relation_softmax_vs_autograd(kind, H):
                                             t["grad_out"], heads=H, scope=1)
     for got, k in [(dh, "h"), (dW, "W"), (dws, "w_src"), (dwd, "w_dst")]:
         np.testing.assert_allclose(got, ts[k].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+
+
+@pytest.mark.parametrize("kind,H", [("random", 1), ("dups", 2)])
+def test_rgat_backward_kink_flip_vs_autograd(kind, H):
+    """kink_flip: on the flagged (edge, head) entries the leaky ReLU's
+    derivative comes from the other side of its kink while every value stays
+    the same -- autograd of the dense layer with that one-sided derivative on
+    the same entries.  (Duplicate edges share their logit, so their flags come
+    from the dense (relation, destination, source) entry.)"""
+    g = tiny_graph(56, N=14, E=70, R=3, kind=kind)
+    t = tiny_tensors(56, g, 6, 8, heads=H, att_var=1.0)
+    dense_flag = np.random.default_rng(56).random((g["R"], g["N"], g["N"], H)) < 0.5
+    kf = dense_flag[g["rel"], g["dst"], g["src"]]
+    assert kf.any() and not kf.all()
+    ts = {k: torch.tensor(t[k], dtype=torch.float64, requires_grad=True)
+          for k in ("h", "W", "w_src", "w_dst")}
+    out = rgat_torch_dense(g, ts["h"], ts["W"], ts["w_src"], ts["w_dst"], H, 0.2, flip=torch.tensor(dense_flag))
+    (out * torch.tensor(t["grad_out"], dtype=torch.float64)).sum().backward()
+    got = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=H, kink_flip=kf)
+    plain = oracle.rgat_backward(g, t["h"], t["W"], t["w_src"], t["w_dst"], t["grad_out"], heads=H)
+    for a, b, k in zip(got, plain, ("h", "W", "w_src", "w_dst")):
+        np.testing.assert_allclose(a, ts[k].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=k)
+        assert np.abs(a - b).max() > 1e-6, k     # the flags do change the gradients
+
+
+def test_rgat_preactivations_match_dense():
+    """The pre-activation helper against the dense per-relation logits."""
+    g = tiny_graph(57, N=14, E=70, R=3, kind="dups")
+    t = tiny_tensors(57, g, 6, 8, heads=2, att_var=1.0)
+    y, scale = oracle.rgat_preactivations(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=2)
+    h, W = t["h"].astype(np.float64), t["W"].astype(np.float64)
+    for e in range(g["E"]):
+        u, v, r = g["src"][e], g["dst"][e], g["rel"][e]
+        ps, pd = (h[u] @ W[r]) * t["w_src"][r], (h[v] @ W[r]) * t["w_dst"][r]
+        for k in range(2):
+            c = slice(4 * k, 4 * k + 4)
+            assert abs(y[e, k] - (ps[c].sum() + pd[c].sum())) <= 1e-12 * (1 + scale[e, k])
+            assert abs(scale[e, k] - (np.abs(ps[c]).sum() + np.abs(pd[c]).sum())) <= 1e-12 * (1 + scale[e, k])
 
 
 def test_rgat_backward_per_relation_one_relation_is_per_destination():
