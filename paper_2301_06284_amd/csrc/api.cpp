@@ -366,6 +366,7 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
     if (plan == RGNN_PLAN_TRANSFORM_FIRST) {
         // compact materialization: one message row per unique (src, rel) pair
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
@@ -390,6 +391,7 @@ extern "C" rgnn_status rgcn_forward(const rgnn_graph_t *g, const float *h, const
     }
     if (W0) {   // virtual self-loop h_v W0, accumulated into out (then the activation)
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = h; ga.ldx = d_in; ga.W[0] = W0; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_all; ga.ntiles = g->n_tiles_all;
         ga.Y = out; ga.ldy = d_out;
@@ -483,6 +485,7 @@ rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *
         // without reordering: the segment's h_v W_r row is materialized and its
         // dot products with w_dst[r] taken in the GEMM epilogue
         GemmArgs gd;
+        gd.split_bf16 = 1;
         gd.X = h; gd.ldx = d_in; gd.gather = g->dev.vsegdst_byrel;
         gd.W[0] = W; gd.K = d_in; gd.Nc = d_out;
         gd.tiles = g->dev.tiles_vsegs; gd.ntiles = g->n_tiles_vsegs;
@@ -500,6 +503,7 @@ rgnn_status rgat_forward_impl(const rgnn_graph *g, const float *h, const float *
     if (plan != RGNN_PLAN_AGGREGATE_FIRST) {
         const bool attmsg = plan == RGNN_PLAN_TRANSFORM_FIRST_ATTMSG;
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = h; ga.ldx = d_in; ga.gather = g->dev.uniq_src;
         ga.W[0] = W; ga.K = d_in; ga.Nc = d_out;
         ga.tiles = g->dev.tiles_pairs; ga.ntiles = g->n_tiles_pairs;
@@ -577,6 +581,7 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
     // types): one GEMM with the weights side by side at d = 64, one per
     // projection otherwise (a 3d-wide weight tile would not fit LDS at 128)
     GemmArgs ga;
+    ga.split_bf16 = 1;
     ga.X = h; ga.ldx = d; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
     ga.K = d;
     ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
@@ -622,6 +627,7 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
             return st;
         }
         GemmArgs gq;
+        gq.split_bf16 = 1;
         gq.X = fold_q ? h : w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
         gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
         gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
@@ -635,6 +641,7 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         return st;
     if (flags & RGNN_FLAG_A_LINEAR) {
         GemmArgs gb;
+        gb.split_bf16 = 1;
         gb.X = w.agg; gb.ldx = d; gb.gather = g->dev.ntype_perm; gb.scatter = g->dev.ntype_perm;
         gb.W[0] = Wa; gb.K = d; gb.Nc = d;
         gb.tiles = g->dev.tiles_nodes; gb.ntiles = g->n_tiles_nodes;
@@ -766,6 +773,7 @@ extern "C" rgnn_status rgnn_segment_gemm(const float *X, int64_t ldx, const int3
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "tile table upload");
     GemmArgs ga;
+    ga.split_bf16 = 1;
     ga.X = X; ga.ldx = ldx; ga.gather = gather; ga.W[0] = W; ga.K = K; ga.Nc = Nc;
     ga.tiles = dt; ga.ntiles = (int64_t)tiles.size();
     ga.Y = Y; ga.ldy = ldy; ga.scatter = scatter;

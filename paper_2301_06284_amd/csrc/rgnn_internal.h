@@ -241,6 +241,11 @@ struct GemmArgs {
     float *Y = nullptr;   int64_t ldy = 0;
     const int32_t *scatter = nullptr;    // row -> Y row (NULL: identity)
     GemmEpilogue ep;
+    // Products from exact three-piece bf16 splits on the bf16 matrix cores
+    // (fp32-accurate, see gemm.hip) for the 64- and 128-deep shapes.  The
+    // forward layers take it; the backward passes keep the fp32 matrix
+    // cores, whose rounding their gradient tests are pinned at.
+    int split_bf16 = 0;
 };
 rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s);
 

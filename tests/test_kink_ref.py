@@ -36,3 +36,19 @@ def test_kink_ref_accepts_flagged_flips_only(monkeypatch):
     got = oracle.rgat_backward(*args, heads=2, kink_flip=flip)
     assert max(row_err(a.reshape(len(a), -1), b.reshape(len(b), -1)) for a, b in zip(got, ref)) > TOL
 
+
+
+def test_kink_ref_many_deltas_on_one_row():
+    """More than twelve kink choices on one row: the row may lie anywhere
+    within base +- the sum of the deltas' magnitudes, and not beyond."""
+    from helpers import KinkRef
+    rng = np.random.default_rng(3)
+    base = rng.standard_normal((3, 8))
+    deltas = [(np.array([1]), 1e-3 * rng.standard_normal((1, 8))) for _ in range(20)]
+    ref = KinkRef(base, deltas)
+    pick = base.copy()
+    pick[1] += sum(d[1][0] for d in deltas[::3])
+    assert row_err(pick, ref) <= 1e-12
+    off = pick.copy()
+    off[1, 0] += 25e-3 * 20
+    assert row_err(off, ref) > TOL
