@@ -630,7 +630,9 @@ extern "C" rgnn_status hgt_forward(const rgnn_graph_t *g, const float *h, const 
         gq.split_bf16 = 1;
         gq.X = fold_q ? h : w.Q; gq.ldx = d; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
         gq.W[0] = w.Wqp; gq.K = d; gq.Nc = d;
-        gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
+        // tiles by destination range: each destination row is gathered by its
+        // relations' tiles on one XCD, from L2 after the first
+        gq.tiles = g->dev.tiles_vsegs_dst; gq.ntiles = g->n_tiles_vsegs_dst;
         gq.Y = w.QP; gq.ldy = d; gq.ep.diag_blocks = fold_q ? 1 : heads;
         if ((st = launch_typed_gemm(gq, s)) != RGNN_OK) return st;
         ha.QP = w.QP;

@@ -200,7 +200,7 @@ __global__ __launch_bounds__((64 * wg_waves<K, NC, S3>())) void typed_gemm_kerne
     // for wider ones whose accumulators and B fragments already fill the VGPR
     // budget); the loop is fully unrolled, so each block's registers are live
     // only from its load to its MFMAs.
-    constexpr int PF = K * NC <= 64 * 64 ? 2 : 1;
+    constexpr int PF = K * NC <= 64 * 64 || (S3 && K == 64) ? 2 : 1;
     float4 ab[MB][KC];
     // SR: the results leave through a wave-private LDS tile, 32 columns at a
     // time, so that each store instruction writes whole 128-byte lines (eight

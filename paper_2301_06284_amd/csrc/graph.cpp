@@ -43,6 +43,58 @@ void build_tiles(const std::vector<int32_t> &type_ptr, int tile_rows, std::vecto
             out.push_back(Tile{t, r0, std::min<int32_t>(tile_rows, type_ptr[t + 1] - r0), 0});
 }
 
+// The rows of each relation (sorted by destination) cut where the destination
+// crosses a multiple of `span` node ids, at most tile_rows rows per tile; the
+// tiles of eight consecutive destination ranges are interleaved (range i of a
+// group at tile positions i, i + 8, ...; empty tiles fill the gaps), so that
+// the tiles of one range -- one per relation that enters it -- land on the same
+// XCD (workgroups are dealt to the eight XCDs in turn) at about the same time:
+// a destination row gathered by several relations' tiles is read from HBM once
+// and from that XCD's L2 after that.
+void build_tiles_dst_ranges(const std::vector<int32_t> &rel_ptr, const std::vector<int32_t> &row_dst, int32_t span,
+                            int tile_rows, std::vector<Tile> &out)
+{
+    out.clear();
+    const int R = (int)rel_ptr.size() - 1;
+    if (R <= 0 || rel_ptr[R] == 0) return;
+    struct Chunk { int32_t range, rel, row0, rows; };
+    std::vector<Chunk> ch;
+    for (int r = 0; r < R; ++r)
+        for (int32_t i = rel_ptr[r]; i < rel_ptr[r + 1];) {
+            const int32_t rg = row_dst[i] / span;
+            int32_t j = i;
+            while (j < rel_ptr[r + 1] && row_dst[j] / span == rg && j - i < tile_rows) ++j;
+            ch.push_back(Chunk{rg, r, i, j - i});
+            i = j;
+        }
+    // (range, relation, first row): a total order, so an in-place sort suffices
+    std::sort(ch.begin(), ch.end(), [](const Chunk &a, const Chunk &b) {
+        return a.range != b.range ? a.range < b.range : (a.rel != b.rel ? a.rel < b.rel : a.row0 < b.row0);
+    });
+    for (size_t a = 0; a < ch.size();) {
+        size_t beg[8], end[8], m = 0;
+        int ng = 0;
+        size_t b = a;
+        while (b < ch.size() && ng < 8) {
+            size_t e = b;
+            while (e < ch.size() && ch[e].range == ch[b].range) ++e;
+            beg[ng] = b; end[ng] = e; ++ng;
+            m = std::max(m, e - b);
+            b = e;
+        }
+        for (size_t j = 0; j < m; ++j)
+            for (int i = 0; i < 8; ++i) {
+                if (i < ng && beg[i] + j < end[i]) {
+                    const Chunk &c = ch[beg[i] + j];
+                    out.push_back(Tile{c.rel, c.row0, c.rows, 0});
+                } else {
+                    out.push_back(Tile{0, 0, 0, 0});
+                }
+            }
+        a = b;
+    }
+}
+
 rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const int32_t *src,
                              const int32_t *dst, const int32_t *rel, const int32_t *ntype,
                              int32_t flags, rgnn_graph *g)
@@ -367,6 +419,8 @@ rgnn_status build_host_index(int64_t N, int32_t T, int32_t R, int64_t E, const i
         // ---- GEMM tile tables ----
         build_tiles(x.uniq_rel_ptr, kGemmTileRows, x.tiles_pairs);
         build_tiles(x.rel_vsegptr, kGemmTileRows, x.tiles_vsegs);
+        build_tiles_dst_ranges(x.rel_vsegptr, x.vsegdst_byrel, kGemmTileRows, kGemmTileRows, x.tiles_vsegs_dst);
+        g->n_tiles_vsegs_dst = (int64_t)x.tiles_vsegs_dst.size();
         build_tiles(x.ntype_ptr, kGemmTileRows, x.tiles_nodes);
         std::vector<int32_t> all{0, (int32_t)N};
         build_tiles(all, kGemmTileRows, x.tiles_all);
@@ -499,6 +553,8 @@ rgnn_status upload(rgnn_graph *g, hipStream_t s)
     parts.push_back(Part{(void **)&d.items, x.items.data(), x.items.size() * sizeof(Item)});
     parts.push_back(Part{(void **)&d.tiles_pairs, x.tiles_pairs.data(), x.tiles_pairs.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_vsegs, x.tiles_vsegs.data(), x.tiles_vsegs.size() * sizeof(Tile)});
+    parts.push_back(Part{(void **)&d.tiles_vsegs_dst, x.tiles_vsegs_dst.data(),
+                         x.tiles_vsegs_dst.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_nodes, x.tiles_nodes.data(), x.tiles_nodes.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_all, x.tiles_all.data(), x.tiles_all.size() * sizeof(Tile)});
     parts.push_back(Part{(void **)&d.tiles_outer, x.tiles_outer.data(), x.tiles_outer.size() * sizeof(Tile)});

@@ -88,6 +88,7 @@ struct HostIndex {
     std::vector<int32_t> vseg_fpos;    // position of each vseg in fused_rows [V]
     std::vector<int32_t> vseg_seg;     // (dst, rel) segment of each vseg [V]
     std::vector<Tile> tiles_pairs, tiles_vsegs, tiles_nodes, tiles_all, tiles_outer;
+    std::vector<Tile> tiles_vsegs_dst;   // tiles_vsegs' rows by destination range, XCD-interleaved
     std::vector<int32_t> rel_chunkptr;   // outer-product chunks per relation [R+1]
     std::vector<float> invcnt_byrel;      // 1 / c_{v,r} of each virtual segment, by-relation order
     std::vector<Tile> tiles_nodes_outer;  // outer-product chunks over all nodes
@@ -143,6 +144,7 @@ struct DeviceIndex {
     int32_t *vseg_fpos = nullptr;
     int32_t *vseg_seg = nullptr;
     Tile *tiles_fused = nullptr;
+    Tile *tiles_vsegs_dst = nullptr;
     Tile *tiles_pairs = nullptr, *tiles_vsegs = nullptr, *tiles_nodes = nullptr,
          *tiles_all = nullptr, *tiles_outer = nullptr;
     int32_t *out_ptr = nullptr, *out_pos = nullptr, *out_vseg = nullptr, *out_rel = nullptr;
@@ -167,6 +169,7 @@ struct rgnn_graph {
     int32_t chunk = rgnn::kChunkEdges;
     int32_t device = -1;
     int64_t n_tiles_pairs = 0, n_tiles_vsegs = 0, n_tiles_nodes = 0, n_tiles_all = 0;
+    int64_t n_tiles_vsegs_dst = 0;
     int64_t n_tiles_outer = 0, n_tiles_fused = 0, n_tiles_nodes_outer = 0, n_tiles_types_outer = 0;
     int64_t n_big_split = 0, n_big_vdst = 0, n_big_seg = 0, n_big_chunks = 0, n_reduce_dst = 0;
     int64_t n_oitems = 0, n_osplit = 0, n_oslots = 0, n_split_items = 0, n_tiles_outer_pairs = 0;
