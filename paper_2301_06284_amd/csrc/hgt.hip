@@ -18,8 +18,8 @@
 // d / 4 lanes; lane l holds features 4l..4l+3, so head i is lanes
 // [i*LH, (i+1)*LH) with LH = d_k / 4.  Each item first stages its edge
 // sources and segment / destination boundaries in LDS, then streams the
-// K|V rows of its edges, with their segments' query rows (L1 hits after a
-// segment's first edge), kU at a time with the next kU in flight.
+// K|V rows of its edges, kU at a time with the next kU in flight; each
+// segment's query row is loaded once, while the segment before it runs.
 #include "rgnn_internal.h"
 #include "wave_ops.h"
 
@@ -53,7 +53,6 @@ struct HS {
 template <bool FQ>
 struct HStage {
     int eidx[kE];          // source node of each edge
-    int evs[kE];           // item-local virtual segment of each edge
     int vptr[kE + 1];      // item-local edge offset of each virtual segment
     int vrel[kE];
     int dptr[kDst + 1];    // item-local edge offset of each destination
@@ -147,11 +146,10 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
         e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
         slot = k.item_slot[item];
         for (int j = gl; j < nv; j += G) {
-            const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
+            const int a = k.vseg_ptr[vs0 + j] - e0;
             st.vptr[j] = a;
             st.vrel[j] = k.vseg_rel[vs0 + j];
             if (FQ) st.vdst[j] = k.vseg_dst[vs0 + j];
-            for (int e = a; e < b; ++e) st.evs[e] = j;
         }
         if (gl == 0) st.vptr[nv] = ne;
         auto dst_edge = [&](int jj) {
@@ -184,35 +182,40 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
     };
     int j = 0, jv = 0;
     while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush(j); ++j; }
-    float4 qcur = zero4(), qp = zero4();   // FQ: Q row of segment jv's destination; its query
-    if (FQ && ne > 0) qcur = ld4(k.Q + (size_t)st.vdst[0] * D + gl * 4);
+    // qcur: FQ, the Q row of segment jv's destination; otherwise segment jv's
+    // reordered query row, loaded one segment ahead.  qp: segment jv's query.
+    float4 qcur = zero4(), qp = zero4();
+    if (ne > 0) qcur = FQ ? ld4(k.Q + (size_t)st.vdst[0] * D + gl * 4) : ld4(k.QP + (size_t)vs0 * D + gl * 4);
     if (ne > 0) {
         // Ping-pong batches: batch A is consumed while batch B is in flight.
-        // Each edge brings its K|V row and its segment's reordered query row
-        // (a cache hit after the segment's first edge).
-        float4 Ak[kU], Av[kU], Aq[kU], Bk[kU], Bv[kU], Bq[kU];
-        auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], float4 (&Xq)[kU], int base) {
+        // Each edge brings its K|V row; each segment's query row is read once,
+        // at the segment before it.
+        float4 Ak[kU], Av[kU], Bk[kU], Bv[kU];
+        auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u < ne ? base + u : ne - 1;
                 const size_t row = (size_t)st.eidx[e] * (2 * D);
                 Xk[u] = ld4(k.KV + row + gl * 4);
                 Xv[u] = ld4(k.KV + row + D + gl * 4);
-                if (!FQ) Xq[u] = ld4(k.QP + (size_t)(vs0 + st.evs[e]) * D + gl * 4);
             }
         };
-        auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
-                           int base) {
+        auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
                 if (e < ne) {
-                    if (FQ && e == st.vptr[jv]) {   // first edge of segment jv: form its query
-                        qp = head_vecmat<LH, G, true>(qcur, Wq + (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK, gl);
-                        if (jv + 1 < nv && st.vdst[jv + 1] != st.vdst[jv])
-                            qcur = ld4(k.Q + (size_t)st.vdst[jv + 1] * D + gl * 4);
+                    if (e == st.vptr[jv]) {   // first edge of segment jv: its query
+                        if (FQ) {
+                            qp = head_vecmat<LH, G, true>(qcur, Wq + (size_t)st.vrel[jv] * MAT + (size_t)head * DK * DK, gl);
+                            if (jv + 1 < nv && st.vdst[jv + 1] != st.vdst[jv])
+                                qcur = ld4(k.Q + (size_t)st.vdst[jv + 1] * D + gl * 4);
+                        } else {
+                            qp = qcur;
+                            if (jv + 1 < nv) qcur = ld4(k.QP + (size_t)(vs0 + jv + 1) * D + gl * 4);
+                        }
                     }
-                    const float a = gsum<LH>(dot4(Xk[u], FQ ? qp : Xq[u]));
+                    const float a = gsum<LH>(dot4(Xk[u], qp));
                     const float mn = fmaxf(m, a);
                     const float c1 = __expf(m - mn), c2 = __expf(a - mn);
                     s = s * c1 + c2;
@@ -233,15 +236,15 @@ __global__ __launch_bounds__(HS<D>::NTH) void hgt_kernel(HK k)
                 }
             }
         };
-        load(Ak, Av, Aq, 0);
+        load(Ak, Av, 0);
         __builtin_amdgcn_sched_barrier(0);
         for (int eb = 0; eb < ne; eb += 2 * kU) {
-            load(Bk, Bv, Bq, eb + kU);
+            load(Bk, Bv, eb + kU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Ak, Av, Aq, eb);
-            load(Ak, Av, Aq, eb + 2 * kU);
+            consume(Ak, Av, eb);
+            load(Ak, Av, eb + 2 * kU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Bk, Bv, Bq, eb + kU);
+            consume(Bk, Bv, eb + kU);
         }
     }
     while (j < nd) { flush(j); ++j; }
