@@ -67,7 +67,6 @@ __global__ void hgt_msgT_weights_kernel(const float *Wmsg, int R, int D, int hea
 template <int H>
 struct DStage {
     int eidx[kE];                  // source node of each edge
-    int evs[kE];                   // item-local virtual segment of each edge
     int vptr[kE + 1];              // item-local first edge of each virtual segment
     int vpos[kE];                  // by-relation position of each virtual segment
     int dptr[kDst + 1];            // item-local first edge of each destination
@@ -100,10 +99,8 @@ __global__ __launch_bounds__(256) void hgt_bwd_dst_kernel(DKArgs k)
         e0 = k.vseg_ptr[x.vs0]; ne = k.vseg_ptr[x.vs1] - e0;
         slot = k.item_slot[item];
         for (int j = gl; j < nv; j += G) {
-            const int a = k.vseg_ptr[vs0 + j] - e0, b = k.vseg_ptr[vs0 + j + 1] - e0;
-            st.vptr[j] = a;
+            st.vptr[j] = k.vseg_ptr[vs0 + j] - e0;
             st.vpos[j] = k.vseg_pos[vs0 + j];
-            for (int e = a; e < b; ++e) st.evs[e] = j;
         }
         if (gl == 0) st.vptr[nv] = ne;
         auto dst_edge = [&](int jj) {
@@ -136,28 +133,35 @@ __global__ __launch_bounds__(256) void hgt_bwd_dst_kernel(DKArgs k)
     int j = 0, jv = 0;
     while (j < nd && st.dptr[j + 1] == st.dptr[j]) { flush_dst(j); ++j; }
     if (ne > 0) {
-        // ping-pong batches of (K row, V row, segment QP row, segment dP row)
-        float4 Ak[kU], Av[kU], Aq[kU], Ap[kU], Bk[kU], Bv[kU], Bq[kU], Bp[kU];
-        auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], float4 (&Xq)[kU], float4 (&Xp)[kU], int base) {
+        // ping-pong batches of (K row, V row); each segment's QP and dP rows
+        // are read once, while the segment before it runs
+        float4 qn = ld4(k.QP + (size_t)vs0 * D + gl * 4), pn = ld4(k.dP + (size_t)vs0 * D + gl * 4);
+        float4 qs = zero4(), ps = zero4();
+        float4 Ak[kU], Av[kU], Bk[kU], Bv[kU];
+        auto load = [&](float4 (&Xk)[kU], float4 (&Xv)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u < ne ? base + u : ne - 1;
                 const size_t row = (size_t)st.eidx[e] * (2 * D);
-                const size_t vrow = (size_t)(vs0 + st.evs[e]) * D;
                 Xk[u] = ld4(k.KV + row + gl * 4);
                 Xv[u] = ld4(k.KV + row + D + gl * 4);
-                Xq[u] = ld4(k.QP + vrow + gl * 4);
-                Xp[u] = ld4(k.dP + vrow + gl * 4);
             }
         };
-        auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], const float4 (&Xq)[kU],
-                           const float4 (&Xp)[kU], int base) {
+        auto consume = [&](const float4 (&Xk)[kU], const float4 (&Xv)[kU], int base) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int e = base + u;
                 if (e < ne) {
-                    const float a = gsum<LH>(dot4(Xk[u], Xq[u]));
-                    const float da = gsum<LH>(dot4(Xv[u], Xp[u]));
+                    if (e == st.vptr[jv]) {   // first edge of segment jv
+                        qs = qn; ps = pn;
+                        if (jv + 1 < nv) {
+                            const size_t vrow = (size_t)(vs0 + jv + 1) * D + gl * 4;
+                            qn = ld4(k.QP + vrow);
+                            pn = ld4(k.dP + vrow);
+                        }
+                    }
+                    const float a = gsum<LH>(dot4(Xk[u], qs));
+                    const float da = gsum<LH>(dot4(Xv[u], ps));
                     const float al = __expf(a - st.dm[j * H + head]) * st.dzi[j * H + head];
                     sal = axpy4(sal, al, Xv[u]);
                     bac = axpy4(bac, al, Xk[u]);
@@ -179,15 +183,15 @@ __global__ __launch_bounds__(256) void hgt_bwd_dst_kernel(DKArgs k)
                 }
             }
         };
-        load(Ak, Av, Aq, Ap, 0);
+        load(Ak, Av, 0);
         __builtin_amdgcn_sched_barrier(0);
         for (int eb = 0; eb < ne; eb += 2 * kU) {
-            load(Bk, Bv, Bq, Bp, eb + kU);
+            load(Bk, Bv, eb + kU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Ak, Av, Aq, Ap, eb);
-            load(Ak, Av, Aq, Ap, eb + 2 * kU);
+            consume(Ak, Av, eb);
+            load(Ak, Av, eb + 2 * kU);
             __builtin_amdgcn_sched_barrier(0);
-            consume(Bk, Bv, Bq, Bp, eb + kU);
+            consume(Bk, Bv, eb + kU);
         }
     }
     while (j < nd) { flush_dst(j); ++j; }
