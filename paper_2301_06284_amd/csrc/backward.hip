@@ -687,9 +687,31 @@ __global__ __launch_bounds__(256) void outer_gemm_kernel(const Tile *chunks, con
 }
 
 // The same product at D = 128 with one workgroup per chunk computing all of
-// the 128 x 128 partial (the 64 x 64 tiling above reads every row twice):
-// 32-row steps staged in LDS, each wave 32 rows of the product (two row
-// blocks against all eight column blocks: ten LDS reads per sixteen MFMAs).
+// the 128 x 128 partial (the 64 x 64 tiling above reads every row twice).
+// The products run on the bf16 matrix cores from exact three-piece splits of
+// both operands (x = x1 + x2 + x3, the six piece products of order >= 2^-16
+// accumulated in fp32, smallest first; the typed GEMM's split path, which has
+// the derivation): 32-row steps, each thread loading one column of 16 rows
+// of both operands (every load instruction covers 256 contiguous bytes) and
+// writing its column's pieces k-contiguous into three transposed bf16 planes
+// per operand, so each MFMA operand fragment is one ds_read_b128; each wave
+// computes 32 rows of the product (two row blocks against all eight column
+// blocks).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ void split3_8(const float *x, bf16x8 &hi, bf16x8 &mid, bf16x8 &lo)
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const __bf16 a = (__bf16)x[j];
+        const float r = x[j] - (float)a;
+        const __bf16 b = (__bf16)r;
+        hi[j] = a;
+        mid[j] = b;
+        lo[j] = (__bf16)(r - (float)b);
+    }
+}
+
 template <bool YS, bool GATHER, bool GA>
 __global__ __launch_bounds__(256) void outer_gemm128_kernel(const Tile *chunks, const int32_t *vsegdst_byrel,
                                                             const float *Sa, int lda,
@@ -697,68 +719,88 @@ __global__ __launch_bounds__(256) void outer_gemm128_kernel(const Tile *chunks, 
                                                             const float *ysum, float *partial,
                                                             float *yvec)
 {
-    constexpr int D = 128, KB = 32, P = D + 4;
-    constexpr int SL = KB * (D / 4) / 256;   // float4 slots of each operand per thread and step
-    __shared__ float As[KB * P];
-    __shared__ float Bs[KB * P];
-    __shared__ float4 yred[YS ? 256 : 1];
+    constexpr int D = 128, KB = 32, RG = 16;    // rows per step; rows per thread and step
+    constexpr int KP = KB + 8;                  // padded bf16 row of a transposed plane
+    constexpr int PL = D * KP;                  // bf16 per plane
+    __shared__ __attribute__((aligned(16))) __bf16 At[3 * PL];   // At[p][a][k]: pieces of Sa
+    __shared__ __attribute__((aligned(16))) __bf16 Bt[3 * PL];   // Bt[p][b][k]: pieces of Gm
+    __shared__ float yred[YS ? 256 : 1];
     const Tile t = chunks[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int li = lane & 15, q = lane >> 4;
-    const int c4 = (tid % (D / 4)) * 4;     // this thread's columns in every slot
-    const int rbase = tid / (D / 4);         // its first row of a step (rows rbase + 8 sl)
+    const int col = tid % D, rg = tid / D;      // this thread's column and row group (16 rows)
     floatx4 acc[2][8];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float4 yacc = zero4();
-    auto row_of = [&](int k0, int sl) { return t.row0 + min(k0 + rbase + 8 * sl, t.rows - 1); };
-    int vi[SL], vn[SL];
-    float4 ra[SL], rb4[SL], rh[SL];
-    float ry[SL];
-    auto load_idx = [&](int k0, int (&v)[SL]) {
+    float yacc = 0.f;
+    auto row_of = [&](int k0, int i) { return t.row0 + min(k0 + rg * RG + i, t.rows - 1); };
+    int vi[RG];
+    float xa[RG], xb[RG], xh[YS ? RG : 1], xy[YS ? RG : 1];
+    auto load_rows = [&](int k0) {
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) v[sl] = (GATHER || GA) ? vsegdst_byrel[row_of(k0, sl)] : row_of(k0, sl);
-    };
-    auto load_rows = [&](int k0, const int (&v)[SL]) {
+        for (int i = 0; i < RG; ++i) vi[i] = (GATHER || GA) ? vsegdst_byrel[row_of(k0, i)] : row_of(k0, i);
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) {
-            const int row = row_of(k0, sl);
-            ra[sl] = ld4(Sa + (size_t)(GA ? v[sl] : row) * lda + c4);
-            rb4[sl] = ld4(Gm + (size_t)(GATHER ? v[sl] : row) * ldb + c4);
+        for (int i = 0; i < RG; ++i) {
+            const int row = row_of(k0, i);
+            xa[i] = Sa[(size_t)(GA ? vi[i] : row) * lda + col];
+            xb[i] = Gm[(size_t)(GATHER ? vi[i] : row) * ldb + col];
             if (YS) {
-                rh[sl] = ld4(h + (size_t)v[sl] * D + c4);
-                ry[sl] = ysum[row];
+                xh[i] = h[(size_t)vi[i] * D + col];
+                xy[i] = ysum[row];
             }
         }
     };
-    load_idx(0, vi);
-    load_rows(0, vi);
-    load_idx(KB, vn);
+    load_rows(0);
     for (int k0 = 0; k0 < t.rows; k0 += KB) {
+        // stage this step's pieces (rows past the chunk as zeros)
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) {
-            const int rr = rbase + 8 * sl;
-            const bool ok = k0 + rr < t.rows;
-            *reinterpret_cast<float4 *>(&As[rr * P + c4]) = ok ? ra[sl] : zero4();
-            *reinterpret_cast<float4 *>(&Bs[rr * P + c4]) = ok ? rb4[sl] : zero4();
-            if (YS && ok) yacc = lin4(yacc, 1.f, rh[sl], ry[sl]);
+        for (int hh = 0; hh < 2; ++hh) {
+            float va[8], vb[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int i = 8 * hh + j;
+                const bool ok = k0 + rg * RG + i < t.rows;
+                va[j] = ok ? xa[i] : 0.f;
+                vb[j] = ok ? xb[i] : 0.f;
+                if (YS && ok) yacc = fmaf(xy[i], xh[i], yacc);
+            }
+            bf16x8 p0, p1, p2;
+            const int o = col * KP + rg * RG + 8 * hh;
+            split3_8(va, p0, p1, p2);
+            *reinterpret_cast<bf16x8 *>(&At[o]) = p0;
+            *reinterpret_cast<bf16x8 *>(&At[PL + o]) = p1;
+            *reinterpret_cast<bf16x8 *>(&At[2 * PL + o]) = p2;
+            split3_8(vb, p0, p1, p2);
+            *reinterpret_cast<bf16x8 *>(&Bt[o]) = p0;
+            *reinterpret_cast<bf16x8 *>(&Bt[PL + o]) = p1;
+            *reinterpret_cast<bf16x8 *>(&Bt[2 * PL + o]) = p2;
         }
         __syncthreads();
-        load_rows(k0 + KB, vn);
-        load_idx(k0 + 2 * KB, vn);
+        if (k0 + KB < t.rows) load_rows(k0 + KB);   // the next step's rows in flight
         __builtin_amdgcn_sched_barrier(0);
-#pragma unroll 2
-        for (int kk = 0; kk < KB; kk += 4) {
-            const float a0 = As[(kk + q) * P + w * 32 + li];
-            const float a1 = As[(kk + q) * P + w * 32 + 16 + li];
+        // A = Sa^T (rows a of the product), B = Gm (columns b); lane (li, q)
+        // supplies k = 8q .. 8q + 7 of its row / column
+        bf16x8 af[2][3];
 #pragma unroll
-            for (int cb = 0; cb < 8; ++cb) {
-                const float b = Bs[(kk + q) * P + cb * 16 + li];
-                acc[0][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b, acc[0][cb], 0, 0, 0);
-                acc[1][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b, acc[1][cb], 0, 0, 0);
-            }
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+                af[rb][pl] = *reinterpret_cast<const bf16x8 *>(&At[pl * PL + (w * 32 + rb * 16 + li) * KP + 8 * q]);
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) {
+            bf16x8 bfr[3];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+                bfr[pl] = *reinterpret_cast<const bf16x8 *>(&Bt[pl * PL + (cb * 16 + li) * KP + 8 * q]);
+            // the six piece products, smallest first (planes of A, B)
+            constexpr int PA[6] = {0, 2, 1, 1, 0, 0}, PB[6] = {2, 0, 1, 0, 1, 0};
+#pragma unroll
+            for (int u = 0; u < 6; ++u)
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb)
+                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb][PA[u]], bfr[PB[u]], acc[rb][cb], 0, 0, 0);
         }
         __syncthreads();
     }
@@ -773,11 +815,7 @@ __global__ __launch_bounds__(256) void outer_gemm128_kernel(const Tile *chunks, 
     if (YS) {
         yred[tid] = yacc;
         __syncthreads();
-        if (tid < D / 4) {
-            float4 s = zero4();
-            for (int i = tid; i < 256; i += D / 4) s = add4(s, yred[i]);
-            st4(yvec + (size_t)blockIdx.x * D + tid * 4, s);
-        }
+        if (tid < D) yvec[(size_t)blockIdx.x * D + tid] = yred[tid] + yred[tid + D];
     }
 }
 
