@@ -320,7 +320,13 @@ rgnn_status hgt_backward(const rgnn_graph_t *g, const float *h, const float *Wk,
  *   X [*, ldx >= K], W [T, K, Nc], Y [*, ldy >= Nc]; gather, scatter: DEVICE
  *   int32 [M] or NULL for the identity.  K in {64, 128}, Nc in {64, 128}, or
  *   K = Nc = 32.
- *   Rows written twice through `scatter` race; the caller avoids that. */
+ *   Rows written twice through `scatter` race; the caller avoids that.
+ *   Arithmetic: fp32 inputs and outputs with fp32 accuracy.  For K, Nc in
+ *   {64, 128} each product is formed from an exact split of both operands into
+ *   three bf16 pieces on the bf16 matrix cores (six piece products accumulated
+ *   in fp32; the dropped ones are below 2^-23 |x||w|); X and W must then be
+ *   finite with magnitude below 3.38e38.  The forward layers use the same
+ *   products. */
 rgnn_status rgnn_segment_gemm(const float *X, int64_t ldx, const int32_t *gather,
                               const int64_t *type_ptr, int32_t num_types, const float *W,
                               int32_t K, int32_t Nc, float *Y, int64_t ldy,
