@@ -29,6 +29,10 @@
  *     allocates no device memory inside the layer calls.  Two calls may run
  *     concurrently on different streams only with distinct workspaces.
  *   - On error nothing is enqueued and rgnn_last_error() describes the cause.
+ *   - Arithmetic is fp32-accurate.  The forward layers' dense transforms form
+ *     each fp32 product from exact three-piece bf16 splits on the bf16 matrix
+ *     cores (see rgnn_segment_gemm), so their inputs (features, weights) must be
+ *     finite with magnitude below 3.38e38.
  */
 #ifndef RGNN_H
 #define RGNN_H
