@@ -446,6 +446,7 @@ rgnn_status node_gemm_t(const rgnn_graph *g, int D, const float *X, int64_t ldx,
                         const float *residual, int accumulate, hipStream_t s)
 {
     GemmArgs ga;
+    ga.split_bf16 = 1;
     ga.X = X; ga.ldx = ldx; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
     ga.W[0] = W; ga.trans_b = 1; ga.K = D; ga.Nc = D;
     ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
@@ -483,6 +484,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     const float *stats = saved ? saved : w.saved;
     {
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = h; ga.ldx = D; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
         ga.K = D;
         ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;
@@ -513,6 +515,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
             (st = launch_hgt_qp_fold(Wq, Watt, mu, att_scale, g->dev.rel_dsttype, g->R, D, H, w.Wf, s)) != RGNN_OK)
             return st;
         GemmArgs gq;
+        gq.split_bf16 = 1;
         gq.X = fold_q ? h : w.Q; gq.ldx = D; gq.gather = g->dev.vsegdst_byrel; gq.scatter = g->dev.vseg_byrel;
         gq.W[0] = fold_q ? w.Wf : w.Wqp; gq.K = D; gq.Nc = D;
         gq.tiles = g->dev.tiles_vsegs; gq.ntiles = g->n_tiles_vsegs;
@@ -544,6 +547,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "msgT weights launch");
         GemmArgs gp;
+        gp.split_bf16 = 1;
         gp.X = dagg; gp.ldx = D; gp.gather = g->dev.vsegdst_byrel; gp.scatter = g->dev.vseg_byrel;
         gp.W[0] = w.Wmt; gp.K = D; gp.Nc = D;
         gp.tiles = g->dev.tiles_vsegs; gp.ntiles = g->n_tiles_vsegs;
@@ -584,6 +588,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
     if (a_linear && dWa && saved) {
         if (g->V > 0) {
             GemmArgs gm;
+            gm.split_bf16 = 1;
             gm.X = w.Sal; gm.ldx = D; gm.W[0] = w.Wmt; gm.trans_b = 1; gm.K = D; gm.Nc = D;
             gm.tiles = g->dev.tiles_vsegs; gm.ntiles = g->n_tiles_vsegs;
             gm.Y = w.Tq; gm.ldy = D; gm.scatter = g->dev.vseg_byrel; gm.ep.diag_blocks = H;
@@ -601,6 +606,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "hgt_bwd_dqp launch");
         GemmArgs gt;
+        gt.split_bf16 = 1;
         gt.X = w.dQP; gt.ldx = D; gt.W[0] = w.Wqp; gt.trans_b = 1; gt.K = D; gt.Nc = D;
         gt.tiles = g->dev.tiles_vsegs; gt.ntiles = g->n_tiles_vsegs;
         gt.Y = w.Tq; gt.ldy = D; gt.scatter = g->dev.vseg_byrel; gt.ep.diag_blocks = H;
@@ -673,6 +679,7 @@ rgnn_status hgt_backward_d(const rgnn_graph *g, const float *h, const float *Wk,
         }
         if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "cat weights launch");
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = w.dKV; ga.ldx = 3 * D; ga.gather = g->dev.ntype_perm; ga.scatter = g->dev.ntype_perm;
         ga.W[0] = w.Wc; ga.trans_b = 1; ga.K = 3 * D; ga.Nc = D;
         ga.tiles = g->dev.tiles_nodes; ga.ntiles = g->n_tiles_nodes;

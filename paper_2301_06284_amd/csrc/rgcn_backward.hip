@@ -180,6 +180,7 @@ rgnn_status rgcn_backward_d(const rgnn_graph *g, const float *h, const float *W,
     if (g->V > 0) {
         // dS = (Gp_v W_r^T) / c per segment, by-relation order
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = Gp; ga.ldx = D; ga.gather = g->dev.vsegdst_byrel;
         ga.W[0] = W; ga.trans_b = 1; ga.K = D; ga.Nc = D;
         ga.tiles = g->dev.tiles_vsegs; ga.ntiles = g->n_tiles_vsegs;
@@ -190,6 +191,7 @@ rgnn_status rgcn_backward_d(const rgnn_graph *g, const float *h, const float *W,
     // dh = Gp W0^T (or zeros), then the relation terms gathered over out-edges
     if (W0) {
         GemmArgs ga;
+        ga.split_bf16 = 1;
         ga.X = Gp; ga.ldx = D; ga.W[0] = W0; ga.trans_b = 1; ga.K = D; ga.Nc = D;
         ga.tiles = g->dev.tiles_all; ga.ntiles = g->n_tiles_all;
         ga.Y = dh; ga.ldy = D;

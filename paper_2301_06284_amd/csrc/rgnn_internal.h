@@ -246,8 +246,9 @@ struct GemmArgs {
     GemmEpilogue ep;
     // Products from exact three-piece bf16 splits on the bf16 matrix cores
     // (fp32-accurate, see gemm.hip) for the 64- and 128-deep shapes.  The
-    // forward layers take it; the backward passes keep the fp32 matrix
-    // cores, whose rounding their gradient tests are pinned at.
+    // forward layers and the RGCN and HGT backward passes take it; the RGAT
+    // backward keeps the fp32 matrix cores (its gradients' near-cancelling
+    // rows -- softmax Jacobian sums -- are pinned at that rounding).
     int split_bf16 = 0;
 };
 rgnn_status launch_typed_gemm(const GemmArgs &a, hipStream_t s);
