@@ -371,16 +371,21 @@ constexpr int kSegBatches = 4;
 // NT threads per workgroup: 256, or 1024 when the vectors of several heads
 // take most of the LDS (one workgroup per CU then stages them once for four
 // times the segments).
-template <int D, int H, int NT>
+// GW: the vectors too many for LDS (hundreds of relations at d = 128) are read
+// from global memory (L2-resident) with each batch's rows, four segments per
+// batch.
+constexpr int kSegPerGroupGW = 4;
+template <int D, int H, int NT, bool GW = false>
 __global__ __launch_bounds__(NT) void seg_attn_lds_kernel(TK k, int64_t V, const int32_t *vseg_dst, int R)
 {
     constexpr int G = D / 4, GPB = NT / G;
-    constexpr int S = kSegPerGroup, SB = kSegBatches, SW = GPB * S * SB;
-    extern __shared__ float4 wts[];   // [R, H, D / 4]
+    constexpr int S = GW ? kSegPerGroupGW : kSegPerGroup, SB = kSegBatches, SW = GPB * S * SB;
+    extern __shared__ float4 wts[];   // [R, H, D / 4] (not GW)
     __shared__ int2 sidx[SW];         // (destination, relation) of the workgroup's segments
     const int gl = threadIdx.x % G, gi = threadIdx.x / G;
     const int64_t wbase = (int64_t)blockIdx.x * SW;
-    for (int i = threadIdx.x; i < R * H * G; i += NT) wts[i] = ld4(k.wtp + (size_t)i * 4);
+    if (!GW)
+        for (int i = threadIdx.x; i < R * H * G; i += NT) wts[i] = ld4(k.wtp + (size_t)i * 4);
     for (int i = threadIdx.x; i < SW; i += NT) {
         const int64_t vs = wbase + i < V ? wbase + i : V - 1;
         sidx[i] = make_int2(vseg_dst[vs], k.vseg_rel[vs]);
@@ -390,6 +395,7 @@ __global__ __launch_bounds__(NT) void seg_attn_lds_kernel(TK k, int64_t V, const
     if (base >= V) return;
     int v[2][S], r[2][S];
     float4 hv[2][S];
+    float4 wr[GW ? 2 : 1][GW ? S : 1][GW ? H : 1];
     auto idx = [&](int slot, int b) {
 #pragma unroll
         for (int i = 0; i < S; ++i) {
@@ -401,6 +407,13 @@ __global__ __launch_bounds__(NT) void seg_attn_lds_kernel(TK k, int64_t V, const
     auto rows = [&](int slot) {
 #pragma unroll
         for (int i = 0; i < S; ++i) hv[slot][i] = ld4(k.h + (size_t)v[slot][i] * D + gl * 4);
+        if constexpr (GW) {
+#pragma unroll
+            for (int i = 0; i < S; ++i)
+#pragma unroll
+                for (int hh = 0; hh < H; ++hh)
+                    wr[slot][i][hh] = ld4(k.wtp + ((size_t)r[slot][i] * H + hh) * D + gl * 4);
+        }
     };
     constexpr int NM = (S * H + G - 1) / G;
     auto compute = [&](int slot, int b) {
@@ -412,7 +425,10 @@ __global__ __launch_bounds__(NT) void seg_attn_lds_kernel(TK k, int64_t V, const
         for (int i = 0; i < S; ++i)
 #pragma unroll
             for (int hh = 0; hh < H; ++hh) {
-                const float p = gsum<G>(dot4(hv[slot][i], wts[(r[slot][i] * H + hh) * G + gl]));
+                float4 w;
+                if constexpr (GW) w = wr[slot][i][hh];
+                else w = wts[(r[slot][i] * H + hh) * G + gl];
+                const float p = gsum<G>(dot4(hv[slot][i], w));
                 const int t = i * H + hh;
                 if (gl == t % G) mine[t / G] = p;
             }
@@ -493,6 +509,25 @@ rgnn_status launch_seg_attn(const TravArgs &a, hipStream_t s)
 #undef SAW
         if (done) {
             if (ea != hipSuccess) return hip_fail(ea, "hipFuncSetAttribute (seg_attn LDS)");
+            hipError_t e = hipGetLastError();
+            return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_attn launch");
+        }
+    }
+    if (a.heads <= 2) {   // batches pipelined per group, the vectors read with the rows
+        constexpr int SPG = kSegPerGroupGW * kSegBatches;
+        const unsigned nbg = blocks_for((a.g->V + SPG - 1) / SPG, 256 / (a.d / 4));
+#define SAG(D, H) hipLaunchKernelGGL((seg_attn_lds_kernel<D, H, 256, true>), dim3(nbg), dim3(256), 0, s, k, \
+                                     a.g->V, a.g->dev.vseg_dst, a.g->R)
+        bool done = true;
+        if (a.d == 32 && a.heads == 1) SAG(32, 1);
+        else if (a.d == 32 && a.heads == 2) SAG(32, 2);
+        else if (a.d == 64 && a.heads == 1) SAG(64, 1);
+        else if (a.d == 64 && a.heads == 2) SAG(64, 2);
+        else if (a.d == 128 && a.heads == 1) SAG(128, 1);
+        else if (a.d == 128 && a.heads == 2) SAG(128, 2);
+        else done = false;
+#undef SAG
+        if (done) {
             hipError_t e = hipGetLastError();
             return e == hipSuccess ? RGNN_OK : hip_fail(e, "seg_attn launch");
         }

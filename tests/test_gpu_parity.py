@@ -100,6 +100,28 @@ def test_segment_gemm_fp32_grade(K, Nc):
     assert worst <= 8.0
 
 
+@pytest.mark.parametrize("d,heads", [(128, 1), (128, 2), (64, 1)])
+def test_rgat_many_relations(d, heads):
+    """More relations than the segment-term kernel can stage in LDS (their
+    reordered w_dst vectors: 700 x d floats per head): the vectors are read
+    with the rows instead.  Forward (both plans) and backward."""
+    g = graph("random", seed=9, N=600, E=6000, R=700, T=2)
+    t = workloads.tiny_tensors(9, g, d, d, heads=heads, att_var=1.0)
+    print(f"rgat many relations d={d} heads={heads}", flush=True)
+    run = Runner(g, t)
+    ref = oracle.rgat_forward(g, t["h"], t["W"], t["w_src"], t["w_dst"], heads=heads)
+    for plan in (1, 2) if heads == 1 else (1,):
+        assert row_err(run.rgat(heads=heads, plan=plan), ref) <= TOL
+    gh, gW, gs, gt = run.rgat_backward(heads=heads)
+    run.close()
+    dh, dW, dws, dwt = rgat_backward_ref(g, t, heads=heads)
+    isolated = (np.bincount(g["src"], minlength=g["N"]) + np.bincount(g["dst"], minlength=g["N"])) == 0
+    assert row_err(gh, dh, structural_zero=isolated, cancel_floor=1e-6) <= TOL
+    assert row_err(gW.reshape(-1, d), dW.reshape(-1, d), cancel_floor=1e-6) <= TOL
+    assert row_err(gs, dws, cancel_floor=1e-6) <= TOL
+    assert row_err(gt, dwt, cancel_floor=1e-6) <= TOL
+
+
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("plan", [1, 2])
 @pytest.mark.parametrize("W0,relu", [(True, False), (False, False), (True, True), (False, True)])
